@@ -1,0 +1,311 @@
+"""ctypes front end of the CPU oracle (test infrastructure only).
+
+Only tests/, the smoke check and the benchmark's CPU-baseline leg import
+this package.  It wraps the plain C oracle in bytecomp_oracle.c one tensor
+at a time and, for tensor lists, loops over tensors in Python and lays the
+payloads out back to back: sparse payloads at offsets that are prefix sums
+of the per-tensor k, sign payloads at prefix sums of the per-tensor word
+counts, one scale per tensor.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+from . import build as _build
+
+_lib = None
+
+F32, F16 = 0, 1
+_DT = {np.dtype(np.float32): F32, np.dtype(np.float16): F16}
+
+_u64 = ctypes.c_uint64
+_u32 = ctypes.c_uint32
+_vp = ctypes.c_void_p
+_dbl = ctypes.c_double
+_int = ctypes.c_int
+_flt = ctypes.c_float
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_build.LIB):
+            _build.build()
+        L = ctypes.CDLL(_build.LIB)
+        L.bco_k.restype = _u64
+        L.bco_k.argtypes = [_u64, _dbl]
+        L.bco_words.restype = _u64
+        L.bco_words.argtypes = [_u64]
+        L.bco_f16_to_f32.restype = _flt
+        L.bco_f16_to_f32.argtypes = [ctypes.c_uint16]
+        L.bco_compress_topk.restype = _int
+        L.bco_compress_topk.argtypes = [_vp, _int, _vp, _u64, _u64, _vp, _vp, _vp]
+        L.bco_compress_topk_sampled.restype = _int
+        L.bco_compress_topk_sampled.argtypes = [_vp, _int, _vp, _u64, _u64, _dbl, _u64, _u32,
+                                                _vp, _vp, _vp, _vp]
+        L.bco_compress_randk.restype = _int
+        L.bco_compress_randk.argtypes = [_vp, _int, _vp, _u64, _u64, _u64, _u32, _vp, _vp, _vp]
+        L.bco_compress_sign.restype = _int
+        L.bco_compress_sign.argtypes = [_vp, _int, _vp, _u64, _vp, _vp, _vp]
+        L.bco_residual_update_sparse.restype = _int
+        L.bco_residual_update_sparse.argtypes = [_vp, _int, _vp, _u64, _u64, _vp, _vp]
+        L.bco_residual_update_sign.restype = _int
+        L.bco_residual_update_sign.argtypes = [_vp, _int, _vp, _u64, _vp, _flt]
+        L.bco_aggregate_sparse.restype = _int
+        L.bco_aggregate_sparse.argtypes = [_int, _u64, _vp, _vp, _vp, _flt, _vp]
+        L.bco_aggregate_sign.restype = _int
+        L.bco_aggregate_sign.argtypes = [_int, _u64, _vp, _vp, _flt, _vp]
+        L.bco_philox4x64_10.restype = None
+        L.bco_philox4x64_10.argtypes = [_vp, _vp, _vp]
+        L.bco_feistel_half_bits.restype = _u32
+        L.bco_feistel_half_bits.argtypes = [_u64]
+        L.bco_randk_round_keys.restype = None
+        L.bco_randk_round_keys.argtypes = [_u64, _u32, _vp]
+        L.bco_feistel_encrypt.restype = _u64
+        L.bco_feistel_encrypt.argtypes = [_u64, _u32, _vp]
+        L.bco_randk_index.restype = _u64
+        L.bco_randk_index.argtypes = [_u64, _u64, _u32, _u64]
+        L.bco_sample_size.restype = _u64
+        L.bco_sample_size.argtypes = [_u64]
+        _lib = L
+    return _lib
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data
+
+
+# ---------------------------------------------------------------- sizes
+
+def k_for(n, ratio):
+    return int(lib().bco_k(int(n), float(ratio)))
+
+
+def words_for(n):
+    return int(lib().bco_words(int(n)))
+
+
+def sparse_offsets(ns, ratio):
+    off = np.zeros(len(ns) + 1, dtype=np.int64)
+    for t, n in enumerate(ns):
+        off[t + 1] = off[t] + k_for(n, ratio)
+    return off
+
+
+def word_offsets(ns):
+    off = np.zeros(len(ns) + 1, dtype=np.int64)
+    for t, n in enumerate(ns):
+        off[t + 1] = off[t] + words_for(n)
+    return off
+
+
+# ------------------------------------------------------- per-tensor calls
+
+def f16_to_f32(h):
+    return lib().bco_f16_to_f32(int(h))
+
+
+def _grad(g):
+    g = np.ascontiguousarray(g)
+    if g.dtype not in _DT:
+        raise TypeError("gradient dtype must be float32 or float16")
+    return g, _DT[g.dtype]
+
+
+def _resid(e, n):
+    if e is None:
+        return None
+    e = np.ascontiguousarray(e, dtype=np.float32)
+    assert e.size == n
+    return e
+
+
+def compress_topk(g, e, ratio):
+    g, dt = _grad(g)
+    n = g.size
+    e = _resid(e, n)
+    k = k_for(n, ratio)
+    idx = np.empty(k, np.uint32)
+    val = np.empty(k, np.float32)
+    e_out = np.empty(n, np.float32) if e is not None else None
+    rc = lib().bco_compress_topk(_p(g), dt, _p(e), n, k, _p(idx), _p(val), _p(e_out))
+    assert rc == 0, rc
+    return idx, val, e_out
+
+
+def compress_topk_sampled(g, e, ratio, seed, tensor_id, want_candidates=False):
+    g, dt = _grad(g)
+    n = g.size
+    e = _resid(e, n)
+    k = k_for(n, ratio)
+    idx = np.empty(k, np.uint32)
+    val = np.empty(k, np.float32)
+    e_out = np.empty(n, np.float32) if e is not None else None
+    nc = np.zeros(1, np.uint64)
+    rc = lib().bco_compress_topk_sampled(_p(g), dt, _p(e), n, k, float(ratio), int(seed),
+                                         int(tensor_id), _p(idx), _p(val), _p(e_out), _p(nc))
+    assert rc == 0, rc
+    if want_candidates:
+        return idx, val, e_out, int(nc[0])
+    return idx, val, e_out
+
+
+def compress_randk(g, e, ratio, seed, tensor_id):
+    g, dt = _grad(g)
+    n = g.size
+    e = _resid(e, n)
+    k = k_for(n, ratio)
+    idx = np.empty(k, np.uint32)
+    val = np.empty(k, np.float32)
+    e_out = np.empty(n, np.float32) if e is not None else None
+    rc = lib().bco_compress_randk(_p(g), dt, _p(e), n, k, int(seed), int(tensor_id),
+                                  _p(idx), _p(val), _p(e_out))
+    assert rc == 0, rc
+    return idx, val, e_out
+
+
+def compress_sign(g, e):
+    g, dt = _grad(g)
+    n = g.size
+    e = _resid(e, n)
+    words = np.empty(words_for(n), np.uint32)
+    scale = np.zeros(1, np.float32)
+    e_out = np.empty(n, np.float32) if e is not None else None
+    rc = lib().bco_compress_sign(_p(g), dt, _p(e), n, _p(words), _p(scale), _p(e_out))
+    assert rc == 0, rc
+    return words, scale[0], e_out
+
+
+def residual_update_sparse(g, e, idx, val):
+    g, dt = _grad(g)
+    n = g.size
+    e = np.array(e, dtype=np.float32, copy=True)
+    idx = np.ascontiguousarray(idx, np.uint32)
+    val = np.ascontiguousarray(val, np.float32)
+    rc = lib().bco_residual_update_sparse(_p(g), dt, _p(e), n, idx.size, _p(idx), _p(val))
+    assert rc == 0, rc
+    return e
+
+
+def residual_update_sign(g, e, words, scale):
+    g, dt = _grad(g)
+    n = g.size
+    e = np.array(e, dtype=np.float32, copy=True)
+    words = np.ascontiguousarray(words, np.uint32)
+    rc = lib().bco_residual_update_sign(_p(g), dt, _p(e), n, _p(words), float(scale))
+    assert rc == 0, rc
+    return e
+
+
+def aggregate_sparse(n, idx_list, val_list, alpha=1.0):
+    W = len(idx_list)
+    idx_list = [np.ascontiguousarray(a, np.uint32) for a in idx_list]
+    val_list = [np.ascontiguousarray(a, np.float32) for a in val_list]
+    ip = (ctypes.c_void_p * max(W, 1))(*[a.ctypes.data for a in idx_list])
+    vp = (ctypes.c_void_p * max(W, 1))(*[a.ctypes.data for a in val_list])
+    kw = np.array([a.size for a in idx_list] or [0], dtype=np.uint64)
+    out = np.empty(n, np.float32)
+    rc = lib().bco_aggregate_sparse(W, n, ctypes.cast(ip, _vp), ctypes.cast(vp, _vp),
+                                    _p(kw), float(alpha), _p(out))
+    assert rc == 0, rc
+    return out
+
+
+def aggregate_sign(n, words_list, scales, alpha=1.0):
+    W = len(words_list)
+    words_list = [np.ascontiguousarray(a, np.uint32) for a in words_list]
+    wp = (ctypes.c_void_p * max(W, 1))(*[a.ctypes.data for a in words_list])
+    sc = np.ascontiguousarray(np.asarray(scales, dtype=np.float32).reshape(-1))
+    out = np.empty(n, np.float32)
+    rc = lib().bco_aggregate_sign(W, n, ctypes.cast(wp, _vp), _p(sc), float(alpha), _p(out))
+    assert rc == 0, rc
+    return out
+
+
+def philox4x64_10(ctr, key):
+    c = np.ascontiguousarray(ctr, np.uint64)
+    k = np.ascontiguousarray(key, np.uint64)
+    out = np.empty(4, np.uint64)
+    lib().bco_philox4x64_10(_p(c), _p(k), _p(out))
+    return out
+
+
+def feistel_half_bits(n):
+    return int(lib().bco_feistel_half_bits(int(n)))
+
+
+def randk_round_keys(seed, tensor_id):
+    rk = np.empty(4, np.uint32)
+    lib().bco_randk_round_keys(int(seed), int(tensor_id), _p(rk))
+    return rk
+
+
+def feistel_encrypt(x, h, rk):
+    rk = np.ascontiguousarray(rk, np.uint32)
+    return int(lib().bco_feistel_encrypt(int(x), int(h), _p(rk)))
+
+
+def randk_index(n, seed, tensor_id, j):
+    return int(lib().bco_randk_index(int(n), int(seed), int(tensor_id), int(j)))
+
+
+def sample_size(n):
+    return int(lib().bco_sample_size(int(n)))
+
+
+# ------------------------------------------------------ tensor-list calls
+
+KINDS = ("topk", "topk_sampled", "randk", "sign")
+
+
+def compress_set(kind, ratio, seed, grads, resids):
+    """Compress a list of tensors; returns (payload dict, list of new residuals).
+
+    Sparse kinds: payload {"idx", "val", "off"}; sign: {"bits", "scale", "off"}.
+    """
+    T = len(grads)
+    ns = [g.size for g in grads]
+    new_e = []
+    if kind == "sign":
+        off = word_offsets(ns)
+        bits = np.empty(int(off[-1]), np.uint32)
+        scale = np.empty(T, np.float32)
+        for t in range(T):
+            w, s, e_out = compress_sign(grads[t], None if resids is None else resids[t])
+            bits[off[t]:off[t + 1]] = w
+            scale[t] = s
+            new_e.append(e_out)
+        return {"bits": bits, "scale": scale, "off": off}, new_e
+    off = sparse_offsets(ns, ratio)
+    idx = np.empty(int(off[-1]), np.uint32)
+    val = np.empty(int(off[-1]), np.float32)
+    for t in range(T):
+        e = None if resids is None else resids[t]
+        if kind == "topk":
+            i, v, e_out = compress_topk(grads[t], e, ratio)
+        elif kind == "topk_sampled":
+            i, v, e_out = compress_topk_sampled(grads[t], e, ratio, seed, t)
+        elif kind == "randk":
+            i, v, e_out = compress_randk(grads[t], e, ratio, seed, t)
+        else:
+            raise ValueError(kind)
+        idx[off[t]:off[t + 1]] = i
+        val[off[t]:off[t + 1]] = v
+        new_e.append(e_out)
+    return {"idx": idx, "val": val, "off": off}, new_e
+
+
+def aggregate_set(kind, ns, payloads, alpha=1.0):
+    """Aggregate W payload dicts (laid out as compress_set returns) per tensor."""
+    outs = []
+    for t, n in enumerate(ns):
+        if kind == "sign":
+            ws = [p["bits"][p["off"][t]:p["off"][t + 1]] for p in payloads]
+            ss = [p["scale"][t] for p in payloads]
+            outs.append(aggregate_sign(n, ws, ss, alpha))
+        else:
+            ii = [p["idx"][p["off"][t]:p["off"][t + 1]] for p in payloads]
+            vv = [p["val"][p["off"][t]:p["off"][t + 1]] for p in payloads]
+            outs.append(aggregate_sparse(n, ii, vv, alpha))
+    return outs

@@ -1,0 +1,204 @@
+"""Seeded synthetic workloads for the compression hot path.
+
+This module holds tensor-shape recipes and seeded input generators only: no
+part of the compression method's arithmetic lives here.  Sizes that depend
+on the method (the number of sparse entries per tensor, the number of sign
+words per tensor) are passed in by the caller.
+
+The paper trains VGG16, ResNet101, UGATIT, BERT-base, GPT2 and LSTM on real
+datasets (paper Sec. 5.1, benchmark-model table); no dataset or trained
+weight is used here.  Instead every gradient tensor is drawn from a normal
+distribution whose scale is itself random per tensor, with the tensor shapes
+of the model families named by each workload.  Randomness comes from numpy's
+PCG64 seeded by SeedSequence([2205, workload, tensor_id, role]) with
+role 0 = gradient, 1 = residual, 2 = per-tensor scale, 3 + w = worker w.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+ROLE_G, ROLE_E, ROLE_SIGMA, ROLE_WORKER = 0, 1, 2, 3
+SEED = 14465  # API seed used for random-k and the threshold sample
+
+
+def rng_for(workload: int, tid: int, role: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([2205, workload, tid, role])))
+
+
+# ------------------------------------------------------------------ shapes
+
+def resnet50_shapes():
+    """ResNet-50: 7x7 stem conv + BN, bottleneck stages [3, 4, 6, 3] of
+    widths 64/128/256/512 (expansion 4, 1x1 downsample + BN on each stage's
+    first block), then the 1000-way classifier.  161 tensors."""
+    shapes = [(64, 3, 7, 7), (64,), (64,)]
+    cin = 64
+    for width, blocks in zip((64, 128, 256, 512), (3, 4, 6, 3)):
+        for b in range(blocks):
+            shapes += [(width, cin, 1, 1), (width,), (width,),
+                       (width, width, 3, 3), (width,), (width,),
+                       (4 * width, width, 1, 1), (4 * width,), (4 * width,)]
+            if b == 0:
+                shapes += [(4 * width, cin, 1, 1), (4 * width,), (4 * width,)]
+            cin = 4 * width
+    shapes += [(1000, 2048), (1000,)]
+    return shapes
+
+
+def bert_base_shapes():
+    """BERT-base: word/position/token-type embeddings + LayerNorm, 12 layers
+    of Q/K/V/O projections with biases, attention-output LayerNorm, FFN
+    768->3072->768 with biases and output LayerNorm, then the pooler.
+    199 tensors."""
+    d, f = 768, 3072
+    shapes = [(30522, d), (512, d), (2, d), (d,), (d,)]
+    for _ in range(12):
+        for _q in range(4):
+            shapes += [(d, d), (d,)]
+        shapes += [(d,), (d,)]
+        shapes += [(f, d), (f,), (d, f), (d,)]
+        shapes += [(d,), (d,)]
+    shapes += [(d, d), (d,)]
+    return shapes
+
+
+def gpt2_xl_shapes():
+    """GPT-2-XL: 50257x1600 token embedding, 1024x1600 position table,
+    48 blocks of (LN, fused QKV 1600x4800, projection, LN, MLP 1600->6400
+    ->1600 with biases), final LN.  580 tensors."""
+    d, f = 1600, 6400
+    shapes = [(50257, d), (1024, d)]
+    for _ in range(48):
+        shapes += [(d,), (d,), (d, 3 * d), (3 * d,), (d, d), (d,),
+                   (d,), (d,), (d, f), (f,), (f, d), (d,)]
+    shapes += [(d,), (d,)]
+    return shapes
+
+
+def many_small_sizes(count=4096, lo=768, hi=65536, workload=5):
+    """Sizes floor(exp(U(ln lo, ln hi))), one draw per tensor."""
+    out = []
+    for t in range(count):
+        u = rng_for(workload, t, ROLE_SIGMA).uniform(math.log(lo), math.log(hi))
+        out.append(int(math.floor(math.exp(u))))
+    return out
+
+
+def numel(shape):
+    n = 1
+    for s in shape:
+        n *= int(s)
+    return n
+
+
+# --------------------------------------------------------------- workloads
+
+@dataclass
+class Workload:
+    """One tensor set plus the aggregation fan-in it is measured with."""
+    wid: int
+    name: str
+    kind: str              # "topk" | "topk_sampled" | "randk" | "sign"
+    ratio: float
+    W: int
+    sizes: list = field(default_factory=list)
+    grad_dtype: str = "float32"
+    sigma_mode: str = "loguniform"   # or "fixed:<sigma>"
+    resid_mode: str = "tenth"        # "zero" | "tenth" | "fixed:<sigma>"
+
+    @property
+    def T(self):
+        return len(self.sizes)
+
+    @property
+    def n_total(self):
+        return int(sum(self.sizes))
+
+
+def workload(wid: int, shrink: int = 1) -> Workload:
+    """The five measured workloads; `shrink` > 1 divides every tensor size
+    (at least 1 element) for fast parity runs of the same structure."""
+    def s(ns):
+        return [max(1, n // shrink) for n in ns]
+    if wid == 1:
+        return Workload(1, "single 2^20 fp32 tensor, exact top-k 1%, W=8", "topk", 0.01, 8,
+                        s([1 << 20]), "float32", "fixed:0.01", "zero")
+    if wid == 2:
+        return Workload(2, "ResNet-50 gradients (161 fp32 tensors, 25.6M), sign+EF, W=64", "sign",
+                        0.01, 64, s([numel(x) for x in resnet50_shapes()]))
+    if wid == 3:
+        return Workload(3, "BERT-base gradients (199 fp32 tensors, 109.5M), sampled top-k 1%, W=64",
+                        "topk_sampled", 0.01, 64, s([numel(x) for x in bert_base_shapes()]))
+    if wid == 4:
+        return Workload(4, "GPT-2-XL gradients (580 fp32 tensors, 1.56B), random-k 1%, W=16",
+                        "randk", 0.01, 16, s([numel(x) for x in gpt2_xl_shapes()]))
+    if wid == 5:
+        return Workload(5, "4096 small fp16 tensors (768..65536, ~60M), sign+fp32 EF, W=32", "sign",
+                        0.01, 32, s(many_small_sizes()), "float16", "fixed:1e-3", "fixed:1e-4")
+    raise ValueError(wid)
+
+
+def sigma_of(wl: Workload, tid: int) -> float:
+    if wl.sigma_mode.startswith("fixed:"):
+        return float(wl.sigma_mode.split(":")[1])
+    return float(10.0 ** rng_for(wl.wid, tid, ROLE_SIGMA).uniform(-4.0, -1.0))
+
+
+def gradient(wl: Workload, tid: int, tie_heavy: bool = False) -> np.ndarray:
+    n = wl.sizes[tid]
+    sig = sigma_of(wl, tid)
+    rng = rng_for(wl.wid, tid, ROLE_G)
+    if tie_heavy:
+        levels = (np.arange(-8, 8, dtype=np.float64) + 0.5) * (sig / 4.0)
+        x = levels[rng.integers(0, 16, size=n)]
+    else:
+        x = rng.standard_normal(n) * sig
+    return x.astype(np.float16 if wl.grad_dtype == "float16" else np.float32)
+
+
+def residual(wl: Workload, tid: int) -> np.ndarray:
+    n = wl.sizes[tid]
+    if wl.resid_mode == "zero":
+        return np.zeros(n, np.float32)
+    if wl.resid_mode.startswith("fixed:"):
+        sig = float(wl.resid_mode.split(":")[1])
+    else:
+        sig = sigma_of(wl, tid) / 10.0
+    return (rng_for(wl.wid, tid, ROLE_E).standard_normal(n) * sig).astype(np.float32)
+
+
+def sparse_payload(wl: Workload, w: int, counts, offs):
+    """Worker w's sparse payload: for tensor t, counts[t] distinct indices in
+    [0, n_t), ascending, at offs[t], and values ~ N(0, sigma_t^2)."""
+    total = int(offs[-1])
+    idx = np.empty(total, np.uint32)
+    val = np.empty(total, np.float32)
+    for t, n in enumerate(wl.sizes):
+        k = int(counts[t])
+        rng = rng_for(wl.wid, t, ROLE_WORKER + w)
+        sel = np.sort(rng.choice(n, size=k, replace=False)).astype(np.uint32)
+        idx[offs[t]:offs[t] + k] = sel
+        val[offs[t]:offs[t] + k] = (rng.standard_normal(k) * sigma_of(wl, t)).astype(np.float32)
+    return idx, val
+
+
+def sign_payload(wl: Workload, w: int, word_counts, offs):
+    """Worker w's sign payload: uniformly random words (bits past the end of
+    each tensor cleared) and scales sigma_t*sqrt(2/pi)*(1 + 0.05 N(0,1))."""
+    total = int(offs[-1])
+    bits = np.empty(total, np.uint32)
+    scale = np.empty(wl.T, np.float32)
+    for t, n in enumerate(wl.sizes):
+        nw = int(word_counts[t])
+        rng = rng_for(wl.wid, t, ROLE_WORKER + w)
+        words = rng.integers(0, 1 << 32, size=nw, dtype=np.uint64).astype(np.uint32)
+        tail = n - 32 * (nw - 1) if nw else 0
+        if nw and tail < 32:
+            words[-1] &= np.uint32((1 << tail) - 1)
+        bits[offs[t]:offs[t] + nw] = words
+        scale[t] = np.float32(sigma_of(wl, t) * math.sqrt(2.0 / math.pi)
+                              * (1.0 + 0.05 * rng.standard_normal()))
+    return bits, scale

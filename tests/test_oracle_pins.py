@@ -1,0 +1,457 @@
+"""Pins of the CPU oracle against things other than itself.
+
+Each test checks an oracle function against brute force, a closed form, a
+hand-worked example (tests/golden/hand_examples.json), an invariant that the
+definition implies, or an independent library routine (numpy.lexsort,
+numpy.packbits, numpy float16 conversion, numpy.random.Philox).
+"""
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_examples.json")
+f32 = np.float32
+
+
+def F(xs):
+    return np.array([float(x) for x in xs], dtype=np.float64).astype(f32) if xs is not None else None
+
+
+def bits(x):
+    return np.asarray(x, f32).view(np.uint32)
+
+
+def hexbits(xs):
+    return np.array([int(h, 16) for h in xs], dtype=np.uint32)
+
+
+@pytest.fixture(scope="module")
+def golden():
+    with open(GOLDEN) as fh:
+        return json.load(fh)
+
+
+# ------------------------------------------------------------------ sizes
+
+def test_k_rule_stated_value():
+    # the single-tensor workload states k = 1% of 2^20 = 10486
+    assert O.k_for(1 << 20, 0.01) == 10486
+
+
+@pytest.mark.parametrize("ratio", [0.01, 0.001, 0.25, 0.5, 0.999, 1.0, 0.123457])
+def test_k_rule_is_exact_ceiling(ratio):
+    ppm = round(ratio * 1e6)
+    for n in list(range(0, 300)) + [767, 768, 1000, 4095, 4096, 65536, 1048577, 80411200, (1 << 32) - 1]:
+        want = 0 if n == 0 else min(n, max(1, math.ceil(Fraction(n * ppm, 10**6))))
+        assert O.k_for(n, ratio) == want, (n, ratio)
+
+
+def test_word_count():
+    for n in range(0, 200):
+        assert O.words_for(n) == -(-n // 32)
+
+
+# ------------------------------------------------------------- fp16 input
+
+def test_f16_widening_matches_numpy_for_every_pattern():
+    h = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    want = h.view(np.float16).astype(np.float32)
+    got = np.array([O.f16_to_f32(int(x)) for x in h], dtype=np.float32)
+    finite = np.isfinite(want)
+    assert np.array_equal(bits(got[finite]), bits(want[finite]))
+    assert np.array_equal(np.isnan(got), np.isnan(want))
+    assert np.array_equal(got[np.isinf(want)], want[np.isinf(want)])
+
+
+# ------------------------------------------------------------------ top-k
+
+def brute_topk(v, k):
+    key = bits(v) & np.uint32(0x7FFFFFFF)
+    order = np.lexsort((np.arange(v.size), -key.astype(np.int64)))
+    return np.sort(order[:k]).astype(np.uint32)
+
+
+def _inputs(rng, n, mode):
+    if mode == "normal":
+        g = (rng.standard_normal(n) * 0.01).astype(f32)
+        e = (rng.standard_normal(n) * 0.001).astype(f32)
+    elif mode == "ties":
+        levels = np.array([-4, -3, -2, -1, -0.5, -0.25, 0, -0.0, 0.25, 0.5, 1, 2, 3, 4, 5, -5], f32)
+        g = levels[rng.integers(0, 16, n)]
+        e = np.zeros(n, f32)
+    elif mode == "equal":
+        g = np.full(n, 0.75, f32)
+        e = np.zeros(n, f32)
+    elif mode == "zeros":
+        g = np.where(rng.random(n) < 0.5, f32(0.0), f32(-0.0)).astype(f32)
+        e = np.where(rng.random(n) < 0.5, f32(0.0), f32(-0.0)).astype(f32)
+    elif mode == "huge":
+        g = (rng.standard_normal(n) * 1e-3).astype(f32)
+        g[rng.integers(0, n)] = f32(3e38)
+        e = np.zeros(n, f32)
+    else:
+        raise ValueError(mode)
+    return g, e
+
+
+@pytest.mark.parametrize("mode", ["normal", "ties", "equal", "zeros", "huge"])
+@pytest.mark.parametrize("n", [1, 2, 7, 31, 32, 33, 64, 65, 257, 1000, 4096])
+def test_topk_matches_lexsort_brute_force(mode, n):
+    rng = np.random.default_rng(n * 7 + len(mode))
+    g, e = _inputs(rng, n, mode)
+    v = g + e
+    for ratio in (0.01, 0.1, 0.37, 1.0):
+        idx, val, e_out = O.compress_topk(g, e, ratio)
+        k = O.k_for(n, ratio)
+        want = brute_topk(v, k)
+        assert np.array_equal(idx, want)
+        assert np.array_equal(bits(val), bits(v[idx]))
+        # reconstruction: decompress + residual == v, bit for bit
+        rec = e_out.copy()
+        rec[idx] = val
+        assert np.array_equal(bits(rec), bits(v))
+        assert np.all(bits(e_out[idx]) == 0)
+
+
+def test_topk_tie_invariant_on_tie_heavy_input():
+    rng = np.random.default_rng(5)
+    g, e = _inputs(rng, 3000, "ties")
+    v = g + e
+    key = bits(v) & np.uint32(0x7FFFFFFF)
+    for ratio in (0.05, 0.2, 0.5):
+        idx, _, _ = O.compress_topk(g, e, ratio)
+        sel = np.zeros(v.size, bool)
+        sel[idx] = True
+        tau = key[sel].min()
+        assert key[~sel].max(initial=0) <= tau
+        # among entries equal to the k-th key, the selected ones have the lowest indices
+        eq = np.nonzero(key == tau)[0]
+        chosen = eq[sel[eq]]
+        rest = eq[~sel[eq]]
+        if rest.size and chosen.size:
+            assert chosen.max() < rest.min()
+        assert np.all(np.diff(idx.astype(np.int64)) > 0)
+
+
+def test_topk_hand_examples(golden):
+    a, b, z = golden["topk"]
+    idx, val, e_out = O.compress_topk(F(a["g"]), F(a["e"]), a["ratio"])
+    assert idx.tolist() == a["idx"]
+    assert np.array_equal(val, F(a["val"]))
+    assert np.array_equal(e_out, F(a["e_new"]))
+    g, e = F(b["g"]), F(b["e"])
+    assert np.array_equal(bits(g + e), hexbits(b["v_bits"]))
+    for case in b["cases"]:
+        idx, val, _ = O.compress_topk(g, e, case["ratio"])
+        assert idx.tolist() == case["idx"]
+        if "val_bits" in case:
+            assert np.array_equal(bits(val), hexbits(case["val_bits"]))
+    idx, val, e_out = O.compress_topk(F(z["g"]), F(z["e"]), z["ratio"])
+    assert idx.tolist() == z["idx"]
+    assert np.array_equal(val, F(z["val"]))
+    assert np.array_equal(bits(e_out), hexbits(z["e_new_bits"]))
+
+
+def test_topk_without_residual_uses_gradient():
+    rng = np.random.default_rng(3)
+    g = (rng.standard_normal(500)).astype(f32)
+    idx, val, e_out = O.compress_topk(g, None, 0.1)
+    assert e_out is None
+    assert np.array_equal(idx, brute_topk(g, 50))
+
+
+def test_topk_fp16_gradient():
+    rng = np.random.default_rng(4)
+    g = (rng.standard_normal(999) * 1e-3).astype(np.float16)
+    e = (rng.standard_normal(999) * 1e-4).astype(f32)
+    v = g.astype(f32) + e
+    idx, val, _ = O.compress_topk(g, e, 0.05)
+    assert np.array_equal(idx, brute_topk(v, O.k_for(999, 0.05)))
+
+
+# -------------------------------------------------------- sampled top-k
+
+def test_sampled_topk_equals_exact_topk_and_exercises_both_paths():
+    rng = np.random.default_rng(11)
+    saw_trim = saw_topup = False
+    for trial in range(60):
+        n = int(rng.integers(1, 3000))
+        mode = ["normal", "ties", "equal", "zeros"][trial % 4]
+        g, e = _inputs(rng, n, mode)
+        for ratio in (0.01, 0.3, 0.6):
+            k = O.k_for(n, ratio)
+            idx, val, e_out, nc = O.compress_topk_sampled(g, e, ratio, 14465 + trial, trial,
+                                                          want_candidates=True)
+            i2, v2, e2 = O.compress_topk(g, e, ratio)
+            assert np.array_equal(idx, i2)
+            assert np.array_equal(bits(val), bits(v2))
+            assert np.array_equal(bits(e_out), bits(e2))
+            saw_trim |= nc >= k
+            saw_topup |= nc < k
+    assert saw_trim and saw_topup
+
+
+# ------------------------------------------------------------- Philox
+
+def test_philox_matches_numpy_philox4x64():
+    rng = np.random.default_rng(21)
+    m = np.uint64(2**64 - 1)
+    for _ in range(40):
+        ctr = rng.integers(0, 2**63, size=4, dtype=np.uint64) * np.uint64(2) + rng.integers(0, 2, size=4, dtype=np.uint64)
+        key = rng.integers(0, 2**63, size=2, dtype=np.uint64)
+        # numpy increments the 256-bit counter before producing a block
+        prev = ctr.copy()
+        i = 0
+        while True:
+            if prev[i] == 0:
+                prev[i] = m
+                i += 1
+                if i == 4:
+                    break
+            else:
+                prev[i] -= np.uint64(1)
+                break
+        # pass uint64 arrays: numpy converts Python-int lists through float
+        bg = np.random.Philox(counter=prev.astype(np.uint64), key=key.astype(np.uint64))
+        want = bg.random_raw(4).astype(np.uint64)
+        got = O.philox4x64_10(ctr, key)
+        assert np.array_equal(got, want)
+
+
+def test_philox_published_zero_vector_via_numpy():
+    m = 2**64 - 1
+    bg = np.random.Philox(counter=[m, m, m, m], key=[0, 0])
+    assert np.array_equal(O.philox4x64_10([0, 0, 0, 0], [0, 0]), bg.random_raw(4).astype(np.uint64))
+
+
+# ------------------------------------------------------------- random-k
+
+@pytest.mark.parametrize("h", [1, 2, 3, 5, 8])
+def test_feistel_is_a_bijection(h):
+    rk = O.randk_round_keys(987654321, 17)
+    dom = 1 << (2 * h)
+    img = [O.feistel_encrypt(x, h, rk) for x in range(dom)]
+    assert sorted(img) == list(range(dom))
+
+
+def test_feistel_domain_bits():
+    for n, h in [(1, 1), (2, 1), (4, 1), (5, 2), (16, 2), (17, 3), (64, 3), (65, 4),
+                 (1 << 20, 10), ((1 << 20) + 1, 11), (80411200, 14)]:
+        assert O.feistel_half_bits(n) == h, n
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 5, 17, 100, 777, 1024])
+def test_cycle_walk_is_a_permutation_of_the_tensor(n):
+    img = [O.randk_index(n, 42, 3, j) for j in range(n)]
+    assert sorted(img) == list(range(n))
+
+
+def test_randk_payload_properties():
+    rng = np.random.default_rng(8)
+    for n in (1, 10, 99, 1000, 12345):
+        g = rng.standard_normal(n).astype(f32)
+        e = rng.standard_normal(n).astype(f32) * f32(0.1)
+        v = g + e
+        for ratio in (0.01, 0.2, 1.0):
+            k = O.k_for(n, ratio)
+            idx, val, e_out = O.compress_randk(g, e, ratio, 14465, 7)
+            assert idx.size == k and np.all(np.diff(idx.astype(np.int64)) > 0)
+            assert idx.max(initial=0) < n
+            assert np.array_equal(bits(val), bits(v[idx]))
+            rec = e_out.copy()
+            rec[idx] = val
+            assert np.array_equal(bits(rec), bits(v))
+            want = np.sort([O.randk_index(n, 14465, 7, j) for j in range(k)]).astype(np.uint32)
+            assert np.array_equal(idx, want)
+            if ratio == 1.0:
+                assert np.array_equal(idx, np.arange(n, dtype=np.uint32))
+
+
+def test_randk_depends_on_seed_and_tensor_id():
+    g = np.ones(5000, f32)
+    a, _, _ = O.compress_randk(g, None, 0.01, 1, 0)
+    b, _, _ = O.compress_randk(g, None, 0.01, 2, 0)
+    c, _, _ = O.compress_randk(g, None, 0.01, 1, 1)
+    d, _, _ = O.compress_randk(g, None, 0.01, 1, 0)
+    assert not np.array_equal(a, b) and not np.array_equal(a, c)
+    assert np.array_equal(a, d)
+
+
+def test_randk_inclusion_frequency_is_uniform():
+    # chi-square over 2000 seeds: every coordinate of a 1000-element tensor is
+    # included with probability k/n = 1/100
+    n, k, seeds = 1000, 10, 2000
+    counts = np.zeros(n)
+    g = np.ones(n, f32)
+    for s in range(seeds):
+        idx, _, _ = O.compress_randk(g, None, 0.01, 1_000_003 * s + 17, 5)
+        counts[idx] += 1
+    expected = seeds * k / n
+    chi2 = float(((counts - expected) ** 2 / expected).sum())
+    # 999 degrees of freedom: mean 999, sd ~ 44.7; 5-sigma band
+    assert 999 - 5 * 44.7 < chi2 < 999 + 5 * 44.7, chi2
+    # pairs: the permutation is not a fixed stride (consecutive picks differ)
+    idx, _, _ = O.compress_randk(np.ones(10**6, f32), None, 0.01, 99, 0)
+    gaps = np.diff(idx.astype(np.int64))
+    assert gaps.std() > 0.5 * gaps.mean()
+
+
+# ------------------------------------------------------------------- sign
+
+def test_sign_hand_examples(golden):
+    c, c1, c2, c3 = golden["sign"]
+    w, s, e_out = O.compress_sign(F(c["g"]), F(c["e"]))
+    assert np.array_equal(w, hexbits(c["words"]))
+    assert s == f32(c["scale"])
+    assert np.array_equal(e_out, F(c["e_new"]))
+    w, s, e_out = O.compress_sign(F(c1["g"]), F(c1["e"]))
+    assert np.array_equal(w, hexbits(c1["words"]))
+    assert bits(s) == int(c1["scale_bits"], 16)
+    assert bits(e_out[0]) == int(c1["e_new0_bits"], 16)
+    w, s, e_out = O.compress_sign(F(c2["g"]), F(c2["e"]))
+    assert np.array_equal(w, hexbits(c2["words"]))
+    assert s == f32(c2["scale"])
+    assert bits(e_out[0]) == int(c2["e_new0_bits"], 16)
+    x = np.array([(-1) ** i * (i + 1) / 64 for i in range(40)], f32)
+    w, s, _ = O.compress_sign(x, None)
+    assert np.array_equal(w, hexbits(c3["words"]))
+    assert s == f32(c3["scale"])
+
+
+@pytest.mark.parametrize("n", [0, 1, 31, 32, 33, 63, 64, 65, 1000, 4097])
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_sign_against_packbits_and_closed_forms(n, dtype):
+    rng = np.random.default_rng(n + 3)
+    g = (rng.standard_normal(n) * 1e-3).astype(dtype)
+    if n > 4:
+        g[:4] = np.array([0.0, -0.0, 0.0, -0.0], dtype)
+    e = (rng.standard_normal(n) * 1e-4).astype(f32)
+    if n > 4:
+        e[:4] = np.array([0.0, -0.0, -0.0, 0.0], f32)
+    v = g.astype(f32) + e
+    w, s, e_out = O.compress_sign(g, e)
+    sb = (bits(v) >> 31).astype(np.uint8)
+    packed = np.packbits(np.concatenate([sb, np.zeros((-n) % 32, np.uint8)]), bitorder="little")
+    assert np.array_equal(w, packed.view("<u4"))
+    assert sum(bin(int(x)).count("1") for x in w) == int(sb.sum())
+    if n == 0:
+        assert bits(s) == 0
+        return
+    # the scale is the fp64 mean of |v|: compare with the exact mean
+    exact = Fraction(0)
+    for x in np.abs(v.astype(np.float64)):
+        exact += Fraction(float(x))
+    mean = exact / n
+    assert abs(Fraction(float(s)) - mean) <= Fraction(float(np.spacing(f32(s))))
+    # decoded magnitudes sum to n*s exactly
+    dec = np.where(sb == 1, -s, s).astype(f32)
+    assert math.fsum(np.abs(dec.astype(np.float64))) == n * float(s)
+    # residual is the correctly rounded difference v - decoded
+    for i in range(min(n, 300)):
+        exact_r = Fraction(float(v[i])) - Fraction(float(dec[i]))
+        r = Fraction(float(e_out[i]))
+        half_ulp = Fraction(float(np.spacing(np.abs(e_out[i])))) / 2
+        assert abs(r - exact_r) <= half_ulp
+
+
+# -------------------------------------------------------- residual update
+
+@pytest.mark.parametrize("kind", ["topk", "randk", "sign"])
+def test_fused_equals_split_residual_update(kind):
+    rng = np.random.default_rng(12)
+    n = 3001
+    g = (rng.standard_normal(n) * 0.02).astype(f32)
+    e = (rng.standard_normal(n) * 0.002).astype(f32)
+    v = g + e
+    if kind == "sign":
+        w, s, e_fused = O.compress_sign(g, e)
+        w2, s2, _ = O.compress_sign(v, None)
+        assert np.array_equal(w, w2) and s == s2
+        e_split = O.residual_update_sign(g, e, w2, s2)
+    else:
+        comp = O.compress_topk if kind == "topk" else (lambda a, b, r: O.compress_randk(a, b, r, 5, 1))
+        idx, val, e_fused = comp(g, e, 0.01)
+        idx2, val2, _ = comp(v, None, 0.01)
+        assert np.array_equal(idx, idx2) and np.array_equal(val, val2)
+        e_split = O.residual_update_sparse(g, e, idx2, val2)
+    assert np.array_equal(bits(e_fused), bits(e_split))
+
+
+# -------------------------------------------------------------- aggregates
+
+def test_sparse_aggregate_hand_example(golden):
+    d = golden["aggregate_sparse"][0]
+    out = O.aggregate_sparse(d["n"], [np.array(w["idx"]) for w in d["workers"]],
+                             [F(w["val"]) for w in d["workers"]], float(d["alpha"]))
+    assert np.array_equal(out, F(d["out"]))
+
+
+def test_sign_aggregate_hand_example(golden):
+    d = golden["aggregate_sign"][0]
+    out = O.aggregate_sign(d["n"], [hexbits(w["words"]) for w in d["workers"]],
+                           [f32(w["scale"]) for w in d["workers"]], float(d["alpha"]))
+    assert np.array_equal(out, F(d["out"]))
+
+
+def test_sparse_aggregate_single_worker_is_decompress():
+    rng = np.random.default_rng(2)
+    n = 1000
+    idx = np.sort(rng.choice(n, 77, replace=False)).astype(np.uint32)
+    val = rng.standard_normal(77).astype(f32)
+    out = O.aggregate_sparse(n, [idx], [val], 1.0)
+    dense = np.zeros(n, f32)
+    dense[idx] = val
+    assert np.array_equal(bits(out), bits(dense))
+
+
+def test_sparse_aggregate_disjoint_supports_is_exact_sum():
+    rng = np.random.default_rng(3)
+    n, W = 4096, 8
+    perm = rng.permutation(n)
+    parts = np.array_split(perm[:W * 100], W)
+    idx = [np.sort(p).astype(np.uint32) for p in parts]
+    val = [rng.standard_normal(p.size).astype(f32) for p in parts]
+    out = O.aggregate_sparse(n, idx, val, 0.125)
+    dense = np.zeros(n, np.float64)
+    for i, v in zip(idx, val):
+        dense[i] += v
+    assert np.array_equal(out, (dense * 0.125).astype(f32))
+
+
+def test_sparse_aggregate_brute_force_order():
+    # worker-ascending fp32 accumulation, checked element by element with
+    # Python floats rounded through numpy float32 at every step
+    rng = np.random.default_rng(4)
+    n, W = 64, 6
+    idx = [np.sort(rng.choice(n, 20, replace=False)).astype(np.uint32) for _ in range(W)]
+    val = [(rng.standard_normal(20) * 10.0 ** rng.integers(-3, 3)).astype(f32) for _ in range(W)]
+    out = O.aggregate_sparse(n, idx, val, 0.5)
+    for i in range(n):
+        acc = f32(0.0)
+        for w in range(W):
+            hit = np.nonzero(idx[w] == i)[0]
+            if hit.size:
+                acc = f32(acc + val[w][hit[0]])
+        assert bits(out[i]) == bits(f32(f32(0.5) * acc))
+
+
+def test_sign_aggregate_zero_bits_and_single_worker():
+    n, W = 100, 5
+    words = [np.zeros(4, np.uint32) for _ in range(W)]
+    scales = [f32(0.1 * (w + 1)) for w in range(W)]
+    out = O.aggregate_sign(n, words, scales, 1.0)
+    acc = f32(0)
+    for s in scales:
+        acc = f32(acc + s)
+    assert np.all(out == acc)
+    rng = np.random.default_rng(6)
+    g = rng.standard_normal(n).astype(f32)
+    w, s, _ = O.compress_sign(g, None)
+    out = O.aggregate_sign(n, [w], [s], 1.0)
+    assert np.array_equal(out, np.where(g < 0, -s, s).astype(f32))

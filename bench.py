@@ -1,0 +1,260 @@
+"""Benchmark of the compression hot path on one MI355X.
+
+One step = compress (with error feedback) every tensor of the workload, then
+decompress-and-aggregate W workers' payloads of the same tensor list: the
+whole hot path for that workload's operator.  Inputs (gradients, residuals,
+the W generated worker payloads) are resident in HBM before timing starts.
+
+value = algorithmic bytes per step / time per step, in GB/s, where the
+algorithmic bytes are what the method must move:
+  compress:  read g (4 B/elem fp32, 2 B fp16) + read e (4 B) + write e (4 B)
+             + write the payload (8 B per sparse entry; 4 B per sign word
+             + 4 B per tensor scale)
+  aggregate: read W payloads + write the dense fp32 output (4 B/elem).
+The roofline entry reports the dominant kernel's algorithmic bytes per
+launch over its average launch time (HIP events on the launch stream)
+against the 8 TB/s HBM peak.  The CPU baseline times the oracle (single
+thread) on a bounded sample of the same workload.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "gradient GB/s through compress+EF and decompress-aggregate; % of HBM peak"
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(wl, off, kind):
+    n = wl.n_total
+    gbytes = 2 if wl.grad_dtype == "float16" else 4
+    if kind == "sign":
+        payload = 4 * int(off[-1]) + 4 * wl.T
+    else:
+        payload = 8 * int(off[-1])
+    comp = (gbytes + 8) * n + payload
+    agg = wl.W * payload + 4 * n
+    return comp, agg, payload
+
+
+def make_inputs(wl, off, device):
+    import torch
+    from paper_2205_14465_amd import workloads as WL
+    kind = wl.kind
+    tdt = torch.float16 if wl.grad_dtype == "float16" else torch.float32
+    # gradients and residuals live in one flat buffer each, tensors as views
+    # at 256-byte aligned offsets (as a framework's gradient buckets would)
+    starts, pos = [], 0
+    for n in wl.sizes:
+        starts.append(pos)
+        pos += (n + 63) // 64 * 64
+    g_flat = torch.empty(pos, dtype=tdt, device=device)
+    e_flat = torch.empty(pos, dtype=torch.float32, device=device)
+    for t, n in enumerate(wl.sizes):
+        g_flat[starts[t]:starts[t] + n].copy_(torch.from_numpy(WL.gradient(wl, t)))
+        e_flat[starts[t]:starts[t] + n].copy_(torch.from_numpy(WL.residual(wl, t)))
+    grads = [g_flat[s:s + n] for s, n in zip(starts, wl.sizes)]
+    resids = [e_flat[s:s + n] for s, n in zip(starts, wl.sizes)]
+    counts = [int(off[t + 1] - off[t]) for t in range(wl.T)]
+    payloads = []
+    for w in range(wl.W):
+        if kind == "sign":
+            b, s = WL.sign_payload(wl, w, counts, off)
+            payloads.append({"bits": torch.from_numpy(b.view(np.int32)).to(device),
+                             "scale": torch.from_numpy(s).to(device)})
+        else:
+            i, v = WL.sparse_payload(wl, w, counts, off)
+            payloads.append({"idx": torch.from_numpy(i.view(np.int32)).to(device),
+                             "val": torch.from_numpy(v).to(device)})
+    out_flat = torch.empty(pos, dtype=torch.float32, device=device)
+    outs = [out_flat[s:s + n] for s, n in zip(starts, wl.sizes)]
+    return grads, resids, payloads, outs
+
+
+def cpu_baseline(wl, off, budget_s=15.0):
+    """Time the oracle (one thread) on a bounded sample of the workload:
+    whole tensors in workload order until ~budget_s of compress work, and
+    the aggregate of the same tensors over all W workers."""
+    import oracle as O
+    from paper_2205_14465_amd import workloads as WL
+    kind = wl.kind
+    counts = [int(off[t + 1] - off[t]) for t in range(wl.T)]
+    comp_bytes = agg_bytes = 0
+    comp_s = agg_s = 0.0
+    used = []
+    gbytes = 2 if wl.grad_dtype == "float16" else 4
+    order = list(range(wl.T))
+    for t in order:
+        if comp_s + agg_s > budget_s:
+            break
+        g = WL.gradient(wl, t)
+        e = WL.residual(wl, t)
+        t0 = time.perf_counter()
+        if kind == "sign":
+            w_, s_, _ = O.compress_sign(g, e)
+        elif kind == "topk":
+            O.compress_topk(g, e, wl.ratio)
+        elif kind == "topk_sampled":
+            O.compress_topk_sampled(g, e, wl.ratio, WL.SEED, t)
+        else:
+            O.compress_randk(g, e, wl.ratio, WL.SEED, t)
+        comp_s += time.perf_counter() - t0
+        n = wl.sizes[t]
+        pay = (4 * counts[t] + 4) if kind == "sign" else 8 * counts[t]
+        comp_bytes += (gbytes + 8) * n + pay
+        # aggregate this tensor over W generated payloads
+        lists = []
+        for w in range(wl.W):
+            rng = WL.rng_for(wl.wid, t, WL.ROLE_WORKER + w)
+            if kind == "sign":
+                lists.append(WL.random_sign_words(rng, [n], [counts[t]])[0])
+            else:
+                i, v = WL.random_sparse_lists(rng, [n], [counts[t]])
+                lists.append((i[0], v[0]))
+        t0 = time.perf_counter()
+        if kind == "sign":
+            O.aggregate_sign(n, lists, [np.float32(1e-3)] * wl.W, 1.0 / wl.W)
+        else:
+            O.aggregate_sparse(n, [a for a, _ in lists], [b for _, b in lists], 1.0 / wl.W)
+        agg_s += time.perf_counter() - t0
+        agg_bytes += wl.W * pay + 4 * n
+        used.append(t)
+    total = comp_bytes + agg_bytes
+    secs = comp_s + agg_s
+    return {"value": round(total / secs / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"{len(used)} of {wl.T} tensors ({sum(wl.sizes[t] for t in used)} elements), "
+                      f"compress + aggregate over W={wl.W}, single thread, {secs:.1f} s",
+            "compress_gbs": round(comp_bytes / comp_s / 1e9, 3) if comp_s else None,
+            "aggregate_gbs": round(agg_bytes / agg_s / 1e9, 3) if agg_s else None}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the compression hot path has no inter-GPU step "
+              "here (worker payloads are generated inputs); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2205_14465_amd import binding as B
+    from paper_2205_14465_amd import workloads as WL
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    B.lib()
+    wl = WL.workload(args.workload)
+    kind = wl.kind
+    off = B.bytecomp_layout(kind, wl.ratio, wl.sizes)
+    log(f"workload {wl.wid}: {wl.name}; generating inputs")
+    grads, resids, payloads, outs = make_inputs(wl, off, dev)
+    own = B.alloc_payload(kind, wl.ratio, wl.sizes, device=dev)
+    ws = B.alloc_workspace(kind, wl.ratio, wl.sizes, wl.W, device=dev)
+    comp_b, agg_b, pay_b = algorithmic_bytes(wl, off, kind)
+    alpha = 1.0 / wl.W
+    stream = torch.cuda.current_stream()
+
+    def compress():
+        B.bytecomp_compress(kind, wl.ratio, WL.SEED, grads, resids, own, ws, stream=stream)
+
+    def aggregate():
+        B.bytecomp_decompress_aggregate(kind, wl.ratio, payloads, wl.sizes, outs, alpha, ws,
+                                        stream=stream)
+
+    log("warmup")
+    for _ in range(args.warmup):
+        compress()
+        aggregate()
+    torch.cuda.synchronize()
+    assert B.bytecomp_device_status(ws) == 0
+
+    # whole-step timing (the contract): K steps between two synchronisations
+    log(f"timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        compress()
+        aggregate()
+    torch.cuda.synchronize()
+    step_s = (time.perf_counter() - t0) / args.steps
+
+    # per-operation device time with HIP events on the launch stream
+    reps = max(args.steps, 10)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(reps)]
+    for r in range(reps):
+        ev[r][0].record(stream)
+        compress()
+        ev[r][1].record(stream)
+        ev[r][2].record(stream)
+        aggregate()
+        ev[r][3].record(stream)
+    torch.cuda.synchronize()
+    comp_ms = sorted(ev[r][0].elapsed_time(ev[r][1]) for r in range(reps))
+    agg_ms = sorted(ev[r][2].elapsed_time(ev[r][3]) for r in range(reps))
+    comp_avg = sum(comp_ms) / reps
+    agg_avg = sum(agg_ms) / reps
+    assert B.bytecomp_device_status(ws) == 0
+
+    value = (comp_b + agg_b) / step_s / 1e9
+    comp_gbs = comp_b / (comp_avg * 1e-3) / 1e9
+    agg_gbs = agg_b / (agg_avg * 1e-3) / 1e9
+    if agg_avg >= comp_avg:
+        dom = {"kernel": "aggregate_sparse" if kind != "sign" else "aggregate_sign",
+               "bytes": agg_b, "ms": agg_avg}
+    else:
+        dom = {"kernel": {"sign": "sign_compress_coop", "randk": "randk_stream"}.get(kind, "topk_compact"),
+               "bytes": comp_b, "ms": comp_avg, "note": "compress call (all of its kernels)"}
+    achieved = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
+    line = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(step_s * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16+f32" if wl.grad_dtype == "float16" else "f32",
+        "data": "synthetic",
+        "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
+        "config": {"workload": wl.name, "kind": kind, "tensors": wl.T, "elements": wl.n_total,
+                   "ratio": wl.ratio if kind != "sign" else None, "W": wl.W,
+                   "payload_bytes_per_worker": pay_b},
+        "ops": {"compress_ms": round(comp_avg, 4), "compress_gbs": round(comp_gbs, 1),
+                "compress_pct_peak": round(100 * comp_gbs / HBM_PEAK_GBS, 2),
+                "aggregate_ms": round(agg_avg, 4), "aggregate_gbs": round(agg_gbs, 1),
+                "aggregate_pct_peak": round(100 * agg_gbs / HBM_PEAK_GBS, 2),
+                "compress_ms_p10_p90": [round(comp_ms[reps // 10], 4), round(comp_ms[(9 * reps) // 10], 4)],
+                "aggregate_ms_p10_p90": [round(agg_ms[reps // 10], 4), round(agg_ms[(9 * reps) // 10], 4)]},
+        "roofline": {"bound": "hbm", "kernel": dom["kernel"], "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle)")
+        line["cpu_baseline"] = cpu_baseline(wl, off, args.cpu_budget)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,172 @@
+/*
+ * bytecomp.h -- C ABI of the MI355X (gfx950) gradient-compression library.
+ *
+ * The library implements the per-tensor compression pipeline of ByteComp
+ * (arXiv 2205.14465): compress each gradient tensor with error feedback,
+ * exchange the payloads, then decompress and aggregate the N gathered
+ * payloads (paper Sec. 3.1, Reason #2, indivisible scheme; Table "eight
+ * action tasks": Comp, Comm_comp, Decomp).  The exchange itself is the
+ * caller's: this library compresses, aggregates, and updates residuals.
+ *
+ * Operators (paper Sec. 5.1, "Compression algorithms"; Sec. 2.3):
+ *   BC_TOPK          exact top-k sparsification
+ *   BC_TOPK_SAMPLED  DGC-style top-k: threshold from a seeded sample, then
+ *                    trimmed or topped up to exactly k (same result as
+ *                    BC_TOPK, different cost)
+ *   BC_RANDK         seeded random-k (Randomk)
+ *   BC_SIGN1         1-bit sign with one scale per tensor (EFSignSGD)
+ * Error feedback (paper Sec. 2.3 and Sec. 5.1): the compressed vector is
+ * v = g + e_old and the residual e_new = v - decompress(payload) is written
+ * back in place.
+ *
+ * Conventions for every entry point:
+ *   - Pointers named "device" must be device memory of the current HIP
+ *     device; pointers named "host" are read before the call returns.
+ *   - All work is enqueued on `stream` (a hipStream_t, NULL = the null
+ *     stream); calls return without synchronising.  Argument errors are
+ *     detected on the host before anything is enqueued: the call then
+ *     returns a negative status and has no side effect.  Faults inside
+ *     kernels surface at the caller's next synchronisation; with the
+ *     environment variable BYTECOMP_DEBUG=1 every call synchronises and
+ *     checks.
+ *   - The caller owns every buffer.  The library keeps a small cache of
+ *     per-device descriptor tables (allocated on first use of a tensor
+ *     list and reused while the list is unchanged) and nothing else.
+ *   - Sizes: 0 <= n < 2^32 elements per tensor (indices are uint32);
+ *     0 < ratio <= 1 with at least one part per million; T >= 0 (T = 0 is
+ *     a no-op); W >= 1.
+ *   - Alignment: fp32 gradients, residuals and aggregate outputs must be
+ *     16-byte aligned; fp16 gradients 8-byte aligned (BC_E_ALIGN otherwise).
+ *   - No C++ exception crosses this interface.
+ */
+#ifndef BYTECOMP_H
+#define BYTECOMP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum bc_kind { BC_TOPK = 0, BC_TOPK_SAMPLED = 1, BC_RANDK = 2, BC_SIGN1 = 3 };
+enum bc_dtype { BC_F32 = 0, BC_F16 = 1 };
+
+enum bc_status {
+    BC_OK = 0,
+    BC_E_NULL = -1,       /* a required pointer is NULL                       */
+    BC_E_KIND = -2,       /* unknown kind                                     */
+    BC_E_DTYPE = -3,      /* unknown gradient dtype                           */
+    BC_E_RATIO = -4,      /* ratio outside (0, 1] or below one part per million */
+    BC_E_SIZE = -5,       /* a tensor has 2^32 or more elements               */
+    BC_E_COUNT = -6,      /* T < 0, W < 1, or too many tensors/workers        */
+    BC_E_WORKSPACE = -7,  /* workspace NULL or smaller than required          */
+    BC_E_HIP = -8,        /* a HIP runtime call failed                        */
+    BC_E_ALIGN = -9,      /* a dense buffer violates the alignment rule       */
+    BC_E_DEVICE = -10     /* a kernel reported a failure (see bytecomp_device_status) */
+};
+
+/* One gradient tensor to compress.
+ *   grad      device, n elements of `dtype`, read only
+ *   residual  device, n fp32 error-feedback values, updated in place;
+ *             NULL turns error feedback off (v = g, nothing written back)
+ *   n         element count
+ *   dtype     BC_F32 or BC_F16
+ *   tensor_id key of the per-tensor random streams (BC_RANDK, the sample
+ *             of BC_TOPK_SAMPLED); by convention the tensor's position in
+ *             the model, kept stable when only a subset is compressed */
+typedef struct bc_tensor {
+    const void* grad;
+    float* residual;
+    uint64_t n;
+    uint32_t dtype;
+    uint32_t tensor_id;
+} bc_tensor;
+
+/* One worker's payload for a list of T tensors, all device pointers.
+ * Sparse kinds use idx/val: tensor t occupies entries [off[t], off[t+1])
+ * (off from bytecomp_layout), indices tensor-local, strictly ascending,
+ * values fp32.  BC_SIGN1 uses bits/scale: tensor t occupies words
+ * [off[t], off[t+1]), element i of the tensor at bit (i mod 32) of word
+ * off[t] + i/32 (1 = negative), bits past the tensor's end zero, and
+ * scale[t] is its fp32 scale.  Unused members may be NULL. */
+typedef struct bc_payload {
+    uint32_t* idx;
+    float* val;
+    uint32_t* bits;
+    float* scale;
+} bc_payload;
+
+/* Human-readable text for a status code (static storage). */
+const char* bytecomp_strerror(int status);
+
+/* Payload layout (host only, no device work).
+ * Sparse kinds: off[t+1] - off[t] = k_t = min(n_t, max(1, ceil(n_t *
+ * ratio))) (0 when n_t = 0), the ratio taken in whole parts per million;
+ * this reads the paper's "1% compression rate" (Sec. 5.1) as an exact k.
+ * BC_SIGN1: off[t+1] - off[t] = ceil(n_t / 32) words (ratio ignored).
+ *   n    host, T element counts
+ *   off  host, T+1 entries written, off[0] = 0 */
+int bytecomp_layout(int kind, double ratio, const uint64_t* n, int T, uint64_t* off);
+
+/* Bytes of device workspace that bytecomp_compress and
+ * bytecomp_decompress_aggregate need for this tensor list (host only).
+ * W is the aggregation fan-in (use 1 for compression only). */
+int bytecomp_workspace_size(int kind, double ratio, const uint64_t* n, int T, int W,
+                            size_t* bytes);
+
+/* Zero a workspace (enqueued on `stream`).  A workspace must be zero
+ * before its first use; every successful call leaves the counters it used
+ * at zero again, so one initialisation suffices.  Re-initialise after a
+ * call that failed inside a kernel. */
+int bytecomp_workspace_init(void* ws, size_t ws_bytes, void* stream);
+
+/* Compress T tensors with error feedback (paper Sec. 2.3, Sec. 5.1).
+ *   kind, ratio  operator and compression rate (ratio unused by BC_SIGN1)
+ *   seed         key of the random streams (BC_RANDK, BC_TOPK_SAMPLED);
+ *                vary it per iteration
+ *   t            host, T tensor descriptors
+ *   out          payload to write (device pointers), laid out as
+ *                bytecomp_layout describes
+ *   ws, ws_bytes device workspace of at least bytecomp_workspace_size
+ * Results: BC_TOPK and BC_TOPK_SAMPLED select the k_t entries of largest
+ * |v| (ties to the lower index); BC_RANDK selects k_t distinct indices
+ * from a keyed permutation of [0, n_t); both emit indices ascending with
+ * values v[idx]; the residual becomes v with the selected entries +0.0.
+ * BC_SIGN1 emits the sign bits of v and scale s_t = mean |v| (summed in
+ * fp64) rounded to fp32; the residual becomes v - (bit ? -s_t : +s_t). */
+int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t, int T,
+                      bc_payload out, void* ws, size_t ws_bytes, void* stream);
+
+/* Decompress W workers' payloads and aggregate them (paper Sec. 3.1,
+ * Reason #2: each node decompresses the gathered payloads and aggregates
+ * them; the aggregation is not an Allreduce because compressed
+ * aggregation is not associative, Sec. 4.2.1, Dimension 3).
+ *   in     host array of W payloads (device pointers), same layout for all
+ *   n      host, T element counts
+ *   out    host array of T device pointers to dense fp32 outputs
+ *   alpha  scale applied to each sum (1 = sum, 1/W = mean)
+ * out_t[i] = alpha * (sum over workers w = 0..W-1, in that order, of the
+ * decoded value of worker w at i), each addition in fp32, starting from
+ * +0.0; elements no worker sent are alpha * 0. */
+int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, int W,
+                                  const uint64_t* n, int T, float* const* out, float alpha,
+                                  void* ws, size_t ws_bytes, void* stream);
+
+/* Error-feedback update from a payload computed elsewhere (e.g. by a CPU
+ * compressor, the paper's CPU offloading, Sec. 4.4.3):
+ * residual <- (g + residual) - decompress(own), elementwise in fp32.
+ * Every tensor must have a non-NULL residual. */
+int bytecomp_residual_update(int kind, double ratio, const bc_tensor* t, int T,
+                             bc_payload own, void* stream);
+
+/* Read (synchronously, on `stream`) and clear the kernel failure flags a
+ * workspace holds; *flags receives them (0 = none).  Bit 0: a bounded
+ * wait for another workgroup's partial result ran out. */
+int bytecomp_device_status(void* ws, size_t ws_bytes, void* stream, uint32_t* flags);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BYTECOMP_H */

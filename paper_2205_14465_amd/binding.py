@@ -1,0 +1,217 @@
+"""Thin ctypes binding of libbytecomp.so (the C ABI in include/bytecomp.h).
+
+Argument marshalling only: every step of the compression path runs in the
+gfx950 kernels of the library.  PyTorch supplies device memory and streams.
+The library must have been built in-tree (paper_2205_14465_amd/build.py);
+importing this module without it raises, so a missing extension fails
+loudly instead of falling back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Sequence
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libbytecomp.so")
+
+BC_TOPK, BC_TOPK_SAMPLED, BC_RANDK, BC_SIGN1 = 0, 1, 2, 3
+BC_F32, BC_F16 = 0, 1
+KIND = {"topk": BC_TOPK, "topk_sampled": BC_TOPK_SAMPLED, "randk": BC_RANDK, "sign": BC_SIGN1}
+STATUS = {0: "BC_OK", -1: "BC_E_NULL", -2: "BC_E_KIND", -3: "BC_E_DTYPE", -4: "BC_E_RATIO",
+          -5: "BC_E_SIZE", -6: "BC_E_COUNT", -7: "BC_E_WORKSPACE", -8: "BC_E_HIP",
+          -9: "BC_E_ALIGN", -10: "BC_E_DEVICE"}
+
+
+class bc_tensor(ctypes.Structure):
+    _fields_ = [("grad", ctypes.c_void_p), ("residual", ctypes.c_void_p), ("n", ctypes.c_uint64),
+                ("dtype", ctypes.c_uint32), ("tensor_id", ctypes.c_uint32)]
+
+
+class bc_payload(ctypes.Structure):
+    _fields_ = [("idx", ctypes.c_void_p), ("val", ctypes.c_void_p), ("bits", ctypes.c_void_p),
+                ("scale", ctypes.c_void_p)]
+
+
+class BytecompError(RuntimeError):
+    def __init__(self, fn, code):
+        self.code = code
+        super().__init__(f"{fn} failed: {STATUS.get(code, code)} ({_strerror(code)})")
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        # PyTorch ships its own copy of the HIP runtime (same soname).  Load
+        # it first so that this library binds to the copy torch uses; loading
+        # ours first would put two HIP runtimes in the process.
+        import torch  # noqa: F401
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built; run paper_2205_14465_amd/build.py "
+                              "(or __graft_entry__.build())")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, u64, i32, dbl, flt, sz = (ctypes.c_void_p, ctypes.c_uint64, ctypes.c_int, ctypes.c_double,
+                                      ctypes.c_float, ctypes.c_size_t)
+        L.bytecomp_strerror.restype = ctypes.c_char_p
+        L.bytecomp_strerror.argtypes = [i32]
+        L.bytecomp_layout.restype = i32
+        L.bytecomp_layout.argtypes = [i32, dbl, vp, i32, vp]
+        L.bytecomp_workspace_size.restype = i32
+        L.bytecomp_workspace_size.argtypes = [i32, dbl, vp, i32, i32, ctypes.POINTER(sz)]
+        L.bytecomp_workspace_init.restype = i32
+        L.bytecomp_workspace_init.argtypes = [vp, sz, vp]
+        L.bytecomp_compress.restype = i32
+        L.bytecomp_compress.argtypes = [i32, dbl, u64, ctypes.POINTER(bc_tensor), i32, bc_payload, vp,
+                                        sz, vp]
+        L.bytecomp_decompress_aggregate.restype = i32
+        L.bytecomp_decompress_aggregate.argtypes = [i32, dbl, ctypes.POINTER(bc_payload), i32, vp, i32,
+                                                    vp, flt, vp, sz, vp]
+        L.bytecomp_residual_update.restype = i32
+        L.bytecomp_residual_update.argtypes = [i32, dbl, ctypes.POINTER(bc_tensor), i32, bc_payload, vp]
+        L.bytecomp_device_status.restype = i32
+        L.bytecomp_device_status.argtypes = [vp, sz, vp, ctypes.POINTER(ctypes.c_uint32)]
+        _lib = L
+    return _lib
+
+
+def _strerror(code):
+    try:
+        return lib().bytecomp_strerror(code).decode()
+    except Exception:
+        return "?"
+
+
+def _check(fn, code):
+    if code != 0:
+        raise BytecompError(fn, code)
+
+
+def _kind(kind):
+    return KIND[kind] if isinstance(kind, str) else int(kind)
+
+
+def _u64_array(values):
+    arr = (ctypes.c_uint64 * max(len(values), 1))(*[int(v) for v in values])
+    return arr
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream_handle(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+# ------------------------------------------------------------ host-only
+
+def bytecomp_layout(kind, ratio, ns: Sequence[int]):
+    off = (ctypes.c_uint64 * (len(ns) + 1))()
+    _check("bytecomp_layout", lib().bytecomp_layout(_kind(kind), float(ratio), _u64_array(ns), len(ns), off))
+    return [int(x) for x in off]
+
+
+def bytecomp_workspace_size(kind, ratio, ns: Sequence[int], W: int = 1):
+    out = ctypes.c_size_t(0)
+    _check("bytecomp_workspace_size",
+           lib().bytecomp_workspace_size(_kind(kind), float(ratio), _u64_array(ns), len(ns), int(W),
+                                         ctypes.byref(out)))
+    return int(out.value)
+
+
+# --------------------------------------------------------------- device
+
+def _tensor_list(grads, resids, tensor_ids):
+    import torch
+    T = len(grads)
+    arr = (bc_tensor * max(T, 1))()
+    for t, g in enumerate(grads):
+        e = None if resids is None else resids[t]
+        if g.dtype == torch.float32:
+            dt = BC_F32
+        elif g.dtype == torch.float16:
+            dt = BC_F16
+        else:
+            dt = 99  # rejected by the library with BC_E_DTYPE
+        arr[t].grad = g.data_ptr() if g.numel() else None
+        arr[t].residual = None if e is None else e.data_ptr()
+        arr[t].n = g.numel()
+        arr[t].dtype = dt
+        arr[t].tensor_id = t if tensor_ids is None else int(tensor_ids[t])
+    return arr
+
+
+def _payload(p):
+    if p is None:
+        return bc_payload()
+    return bc_payload(idx=p.get("idx") is not None and p["idx"].data_ptr() or None,
+                      val=p.get("val") is not None and p["val"].data_ptr() or None,
+                      bits=p.get("bits") is not None and p["bits"].data_ptr() or None,
+                      scale=p.get("scale") is not None and p["scale"].data_ptr() or None)
+
+
+def bytecomp_workspace_init(ws, stream=None):
+    _check("bytecomp_workspace_init",
+           lib().bytecomp_workspace_init(_ptr(ws), ws.numel() * ws.element_size(), _stream_handle(stream)))
+
+
+def bytecomp_compress(kind, ratio, seed, grads, resids, out, ws, stream=None, tensor_ids=None):
+    """grads/resids: lists of device tensors (resids None = error feedback off);
+    out: payload dict of device tensors ('idx','val' or 'bits','scale');
+    ws: device uint8 tensor of at least bytecomp_workspace_size bytes."""
+    arr = _tensor_list(grads, resids, tensor_ids)
+    _check("bytecomp_compress",
+           lib().bytecomp_compress(_kind(kind), float(ratio), int(seed) & (2**64 - 1), arr, len(grads),
+                                   _payload(out), _ptr(ws), ws.numel() * ws.element_size(),
+                                   _stream_handle(stream)))
+
+
+def bytecomp_decompress_aggregate(kind, ratio, payloads, ns, outs, alpha, ws, stream=None):
+    W = len(payloads)
+    pa = (bc_payload * max(W, 1))(*[_payload(p) for p in payloads])
+    T = len(ns)
+    op = (ctypes.c_void_p * max(T, 1))(*[o.data_ptr() if o.numel() else None for o in outs])
+    _check("bytecomp_decompress_aggregate",
+           lib().bytecomp_decompress_aggregate(_kind(kind), float(ratio), pa, W, _u64_array(ns), T, op,
+                                               float(alpha), _ptr(ws), ws.numel() * ws.element_size(),
+                                               _stream_handle(stream)))
+
+
+def bytecomp_residual_update(kind, ratio, grads, resids, own, stream=None, tensor_ids=None):
+    arr = _tensor_list(grads, resids, tensor_ids)
+    _check("bytecomp_residual_update",
+           lib().bytecomp_residual_update(_kind(kind), float(ratio), arr, len(grads), _payload(own),
+                                          _stream_handle(stream)))
+
+
+def bytecomp_device_status(ws, stream=None):
+    f = ctypes.c_uint32(0)
+    _check("bytecomp_device_status",
+           lib().bytecomp_device_status(_ptr(ws), ws.numel() * ws.element_size(), _stream_handle(stream),
+                                        ctypes.byref(f)))
+    return int(f.value)
+
+
+# ------------------------------------------------------------ allocation
+
+def alloc_payload(kind, ratio, ns, device="cuda"):
+    """Device buffers for one worker's payload of the given tensor list."""
+    import torch
+    off = bytecomp_layout(kind, ratio, ns)
+    total = off[-1]
+    if _kind(kind) == BC_SIGN1:
+        return {"bits": torch.zeros(max(total, 1), dtype=torch.int32, device=device),
+                "scale": torch.zeros(max(len(ns), 1), dtype=torch.float32, device=device), "off": off}
+    return {"idx": torch.zeros(max(total, 1), dtype=torch.int32, device=device),
+            "val": torch.zeros(max(total, 1), dtype=torch.float32, device=device), "off": off}
+
+
+def alloc_workspace(kind, ratio, ns, W=1, device="cuda"):
+    import torch
+    return torch.zeros(bytecomp_workspace_size(kind, ratio, ns, W), dtype=torch.uint8, device=device)

@@ -1,0 +1,522 @@
+// api.hip -- the C ABI (include/bytecomp.h): argument validation, payload
+// layout, workspace planning, the per-device descriptor cache, and the
+// launch sequences of the gfx950 kernels.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <vector>
+
+#include "../../include/bytecomp.h"
+#include "launch.hpp"
+
+namespace bc {
+
+namespace {
+
+constexpr int kMaxT = 1 << 20;
+constexpr int kMaxW = 1024;
+constexpr uint64_t kMaxN = (1ull << 32) - 65536;  // uint32 indices, chunk arithmetic headroom
+
+bool debug_mode() {
+    static int mode = -1;
+    if (mode < 0) {
+        const char* e = std::getenv("BYTECOMP_DEBUG");
+        mode = (e && e[0] == '1') ? 1 : 0;
+    }
+    return mode == 1;
+}
+
+uint64_t ratio_ppm(double ratio) {
+    if (!(ratio > 0.0) || ratio > 1.0) return 0;
+    return (uint64_t)std::llround(ratio * 1e6);
+}
+
+uint64_t k_of(uint64_t n, uint64_t ppm) {
+    if (n == 0) return 0;
+    uint64_t k = (n * ppm + 999999u) / 1000000u;
+    if (k < 1) k = 1;
+    if (k > n) k = n;
+    return k;
+}
+
+uint64_t words_of(uint64_t n) { return (n + 31u) / 32u; }
+
+bool is_sparse(int kind) { return kind == BC_TOPK || kind == BC_TOPK_SAMPLED || kind == BC_RANDK; }
+
+size_t align256(size_t x) { return (x + 255u) & ~(size_t)255u; }
+
+// ----------------------------------------------------- descriptor cache
+// Device copies of descriptor tables, keyed by their exact bytes and the
+// device; a hit costs no copy.  Entries are uploaded from pinned host
+// memory on the calling stream; other streams wait on the upload event.
+struct Entry {
+    int device = -1;
+    std::vector<unsigned char> key;
+    void* dev = nullptr;
+    void* pinned = nullptr;
+    size_t cap = 0;
+    hipStream_t upload_stream = nullptr;
+    hipEvent_t ready = nullptr;
+    hipEvent_t used = nullptr;
+    hipStream_t last_stream = nullptr;
+    bool multi_stream = false;
+    uint64_t tick = 0;
+};
+
+std::mutex g_mu;
+Entry g_cache[32];
+uint64_t g_tick = 0;
+
+hipError_t cache_get(const void* bytes, size_t len, hipStream_t s, Entry** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    Entry* victim = nullptr;
+    for (Entry& en : g_cache) {
+        if (en.device == dev && en.key.size() == len && std::memcmp(en.key.data(), bytes, len) == 0) {
+            if (en.upload_stream != s) {
+                e = hipStreamWaitEvent(s, en.ready, 0);
+                if (e != hipSuccess) return e;
+            }
+            en.tick = ++g_tick;
+            *out = &en;
+            return hipSuccess;
+        }
+        if (!victim || en.tick < victim->tick) victim = &en;
+    }
+    Entry& en = *victim;
+    if (en.device >= 0) {
+        // make sure no queued kernel still reads the old table
+        if (en.multi_stream) {
+            e = hipDeviceSynchronize();
+        } else if (en.used) {
+            e = hipEventSynchronize(en.used);
+        }
+        if (e != hipSuccess) return e;
+    }
+    if (en.device != dev || en.cap < len) {
+        if (en.dev) (void)hipFree(en.dev);
+        if (en.pinned) (void)hipHostFree(en.pinned);
+        if (en.ready) (void)hipEventDestroy(en.ready);
+        if (en.used) (void)hipEventDestroy(en.used);
+        en = Entry();
+        size_t cap = len < 4096 ? 4096 : len;
+        if ((e = hipMalloc(&en.dev, cap)) != hipSuccess) { en = Entry(); return e; }
+        if ((e = hipHostMalloc(&en.pinned, cap, hipHostMallocDefault)) != hipSuccess) {
+            (void)hipFree(en.dev);
+            en = Entry();
+            return e;
+        }
+        (void)hipEventCreateWithFlags(&en.ready, hipEventDisableTiming);
+        (void)hipEventCreateWithFlags(&en.used, hipEventDisableTiming);
+        en.cap = cap;
+        en.device = dev;
+    }
+    std::memcpy(en.pinned, bytes, len);
+    en.key.assign((const unsigned char*)bytes, (const unsigned char*)bytes + len);
+    e = hipMemcpyAsync(en.dev, en.pinned, len, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipEventRecord(en.ready, s);
+    if (e != hipSuccess) { en.key.clear(); return e; }
+    en.upload_stream = s;
+    en.last_stream = s;
+    en.multi_stream = false;
+    en.tick = ++g_tick;
+    *out = &en;
+    return hipSuccess;
+}
+
+void cache_mark_used(Entry* en, hipStream_t s) {
+    if (en->last_stream != s) en->multi_stream = true;
+    en->last_stream = s;
+    (void)hipEventRecord(en->used, s);
+}
+
+// ------------------------------------------------------------ device info
+std::mutex g_dev_mu;
+DevInfo g_dev[64];
+bool g_dev_ok[64];
+
+}  // namespace
+
+hipError_t sign_coop_occupancy(int* blocks_per_cu);
+
+hipError_t device_info(int dev, DevInfo* out) {
+    std::lock_guard<std::mutex> lk(g_dev_mu);
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    if (!g_dev_ok[dev]) {
+        hipDeviceProp_t p;
+        hipError_t e = hipGetDeviceProperties(&p, dev);
+        if (e != hipSuccess) return e;
+        DevInfo di;
+        di.cus = p.multiProcessorCount;
+        di.coop_ok = p.cooperativeLaunch != 0;
+        int b = 0;
+        e = sign_coop_occupancy(&b);
+        if (e != hipSuccess) return e;
+        di.sign_coop_blocks_per_cu = b > 0 ? b : 1;
+        g_dev[dev] = di;
+        g_dev_ok[dev] = true;
+    }
+    *out = g_dev[dev];
+    return hipSuccess;
+}
+
+// -------------------------------------------------------------- workspace
+WsPlan plan_workspace(int kind, int T, uint64_t C, uint64_t sum_k) {
+    WsPlan p;
+    std::memset(&p, 0, sizeof(p));
+    size_t at = 256;  // header
+    auto take = [&](size_t& field, size_t bytes) {
+        field = bytes ? at : 0;
+        at = align256(at + bytes);
+    };
+    const size_t t = (size_t)T;
+    if (kind == BC_SIGN1) {
+        take(p.s_cnt, t * 4);
+        take(p.s_ready, t * 4);
+        take(p.s_val, t * 4);
+        take(p.s_partial, (size_t)C * 8);
+    } else if (kind == BC_TOPK || kind == BC_TOPK_SAMPLED) {
+        take(p.t_hist, t * kBins0 * 4);
+        take(p.t_thr, t * 4);
+        take(p.t_prefix, t * 4);
+        take(p.t_krem, t * 4);
+        take(p.t_fb, t * 4);
+        take(p.t_cand, (size_t)C * kChunk * 8);
+        take(p.t_ccount, (size_t)C * 4);
+        take(p.t_gt, (size_t)C * 4);
+        take(p.t_eq, (size_t)C * 4);
+        take(p.t_off, (size_t)C * 8);
+        take(p.t_eqb, (size_t)C * 4);
+    } else if (kind == BC_RANDK) {
+        const size_t nb = ((size_t)C + kBlock * 16 - 1) / (kBlock * 16);
+        take(p.r_keys, t * 16);
+        take(p.r_tmp, (size_t)sum_k * 4);
+        take(p.r_ccount, (size_t)C * 4);
+        take(p.r_coff, ((size_t)C + 1 + nb) * 8);
+        take(p.r_cursor, (size_t)C * 8);
+    }
+    p.total = at;
+    return p;
+}
+
+Ws carve_workspace(void* base, const WsPlan& p) {
+    char* b = (char*)base;
+    auto at = [&](size_t off) -> void* { return off ? (void*)(b + off) : nullptr; };
+    Ws w;
+    std::memset(&w, 0, sizeof(w));
+    w.flags = (uint32_t*)b;
+    w.s_cnt = (uint32_t*)at(p.s_cnt);
+    w.s_ready = (uint32_t*)at(p.s_ready);
+    w.s_val = (float*)at(p.s_val);
+    w.s_partial = (double*)at(p.s_partial);
+    w.t_hist = (uint32_t*)at(p.t_hist);
+    w.t_thr = (uint32_t*)at(p.t_thr);
+    w.t_prefix = (uint32_t*)at(p.t_prefix);
+    w.t_krem = (uint32_t*)at(p.t_krem);
+    w.t_fb = (uint32_t*)at(p.t_fb);
+    w.t_cand = (uint2*)at(p.t_cand);
+    w.t_ccount = (uint32_t*)at(p.t_ccount);
+    w.t_gt = (uint32_t*)at(p.t_gt);
+    w.t_eq = (uint32_t*)at(p.t_eq);
+    w.t_off = (uint64_t*)at(p.t_off);
+    w.t_eqb = (uint32_t*)at(p.t_eqb);
+    w.r_keys = (uint32_t*)at(p.r_keys);
+    w.r_tmp = (uint32_t*)at(p.r_tmp);
+    w.r_ccount = (uint32_t*)at(p.r_ccount);
+    w.r_coff = (uint64_t*)at(p.r_coff);
+    w.r_cursor = (unsigned long long*)at(p.r_cursor);
+    return w;
+}
+
+hipError_t launch_zero_header(uint32_t* flags, hipStream_t s);
+
+}  // namespace bc
+
+using namespace bc;
+
+namespace {
+
+int hip_status(hipError_t e) { return e == hipSuccess ? BC_OK : BC_E_HIP; }
+
+int finish(int rc, hipStream_t s, void* ws) {
+    if (rc != BC_OK || !debug_mode()) return rc;
+    if (hipStreamSynchronize(s) != hipSuccess) return BC_E_HIP;
+    if (ws) {
+        uint32_t f = 0;
+        if (hipMemcpy(&f, ws, 4, hipMemcpyDeviceToHost) != hipSuccess) return BC_E_HIP;
+        if (f) return BC_E_DEVICE;
+    }
+    return BC_OK;
+}
+
+// Validate a tensor list and build its descriptor table.
+int build_tdesc(int kind, uint64_t ppm, const bc_tensor* t, int T, bool need_resid,
+                std::vector<TDesc>& d, uint32_t& C, uint32_t& max_chunks, uint64_t& sum_k,
+                bool& any16, bool& any32) {
+    d.resize((size_t)T);
+    uint64_t chunks = 0, off = 0;
+    max_chunks = 0;
+    any16 = any32 = false;
+    for (int i = 0; i < T; ++i) {
+        const bc_tensor& x = t[i];
+        if (x.dtype != BC_F32 && x.dtype != BC_F16) return BC_E_DTYPE;
+        if (x.n >= kMaxN) return BC_E_SIZE;
+        if (x.n > 0 && !x.grad) return BC_E_NULL;
+        if (need_resid && x.n > 0 && !x.residual) return BC_E_NULL;
+        const uintptr_t ga = (uintptr_t)x.grad, ra = (uintptr_t)x.residual;
+        if ((x.dtype == BC_F32 && (ga & 15u)) || (x.dtype == BC_F16 && (ga & 7u)) || (ra & 15u))
+            return BC_E_ALIGN;
+        const uint64_t nc = (x.n + kChunk - 1) / kChunk;
+        TDesc& o = d[(size_t)i];
+        o.grad = x.grad;
+        o.resid = x.n ? x.residual : nullptr;
+        o.n = (uint32_t)x.n;
+        o.dtype = x.dtype;
+        o.tid = x.tensor_id;
+        const uint64_t cnt = is_sparse(kind) ? k_of(x.n, ppm) : words_of(x.n);
+        o.k = (uint32_t)cnt;
+        o.off = off;
+        o.chunk0 = (uint32_t)chunks;
+        o.nchunks = (uint32_t)nc;
+        off += cnt;
+        chunks += nc;
+        if (nc > max_chunks) max_chunks = (uint32_t)nc;
+        if (x.n) (x.dtype == BC_F16 ? any16 : any32) = true;
+    }
+    if (chunks >= (1ull << 31)) return BC_E_SIZE;
+    C = (uint32_t)chunks;
+    sum_k = off;
+    return BC_OK;
+}
+
+int check_kind_ratio(int kind, double ratio, uint64_t& ppm) {
+    if (kind < BC_TOPK || kind > BC_SIGN1) return BC_E_KIND;
+    ppm = 1;
+    if (is_sparse(kind)) {
+        ppm = ratio_ppm(ratio);
+        if (ppm == 0) return BC_E_RATIO;
+    }
+    return BC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* bytecomp_strerror(int status) {
+    switch (status) {
+        case BC_OK: return "ok";
+        case BC_E_NULL: return "a required pointer is NULL";
+        case BC_E_KIND: return "unknown compression kind";
+        case BC_E_DTYPE: return "unknown gradient dtype";
+        case BC_E_RATIO: return "ratio outside (0, 1] or below one part per million";
+        case BC_E_SIZE: return "tensor or call too large";
+        case BC_E_COUNT: return "invalid tensor or worker count";
+        case BC_E_WORKSPACE: return "workspace missing or too small";
+        case BC_E_HIP: return "HIP runtime error";
+        case BC_E_ALIGN: return "dense buffer not aligned (fp32 and outputs 16 B, fp16 8 B)";
+        case BC_E_DEVICE: return "a kernel reported a failure";
+        default: return "unknown status";
+    }
+}
+
+int bytecomp_layout(int kind, double ratio, const uint64_t* n, int T, uint64_t* off) {
+    uint64_t ppm;
+    int rc = check_kind_ratio(kind, ratio, ppm);
+    if (rc) return rc;
+    if (T < 0 || T > kMaxT) return BC_E_COUNT;
+    if (!off || (T > 0 && !n)) return BC_E_NULL;
+    off[0] = 0;
+    for (int t = 0; t < T; ++t) {
+        if (n[t] >= kMaxN) return BC_E_SIZE;
+        off[t + 1] = off[t] + (is_sparse(kind) ? k_of(n[t], ppm) : words_of(n[t]));
+    }
+    return BC_OK;
+}
+
+int bytecomp_workspace_size(int kind, double ratio, const uint64_t* n, int T, int W, size_t* bytes) {
+    uint64_t ppm;
+    int rc = check_kind_ratio(kind, ratio, ppm);
+    if (rc) return rc;
+    if (T < 0 || T > kMaxT || W < 1 || W > kMaxW) return BC_E_COUNT;
+    if (!bytes || (T > 0 && !n)) return BC_E_NULL;
+    uint64_t C = 0, sk = 0;
+    for (int t = 0; t < T; ++t) {
+        if (n[t] >= kMaxN) return BC_E_SIZE;
+        C += (n[t] + kChunk - 1) / kChunk;
+        sk += is_sparse(kind) ? k_of(n[t], ppm) : 0;
+    }
+    *bytes = plan_workspace(kind, T, C, sk).total;
+    return BC_OK;
+}
+
+int bytecomp_workspace_init(void* ws, size_t ws_bytes, void* stream) {
+    if (!ws) return BC_E_NULL;
+    if (ws_bytes < 256) return BC_E_WORKSPACE;
+    return hip_status(launch_zero_header((uint32_t*)ws, (hipStream_t)stream));
+}
+
+int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t, int T,
+                      bc_payload out, void* ws, size_t ws_bytes, void* stream) {
+    uint64_t ppm;
+    int rc = check_kind_ratio(kind, ratio, ppm);
+    if (rc) return rc;
+    if (T < 0 || T > kMaxT) return BC_E_COUNT;
+    if (T == 0) return BC_OK;
+    if (!t) return BC_E_NULL;
+    if (is_sparse(kind) ? (!out.idx || !out.val) : (!out.bits || !out.scale)) return BC_E_NULL;
+    if (!ws) return BC_E_WORKSPACE;
+    std::vector<TDesc> d;
+    uint32_t C, maxc;
+    uint64_t sum_k;
+    bool a16, a32;
+    try {
+        rc = build_tdesc(kind, ppm, t, T, false, d, C, maxc, sum_k, a16, a32);
+    } catch (const std::bad_alloc&) {
+        return BC_E_SIZE;
+    }
+    if (rc) return rc;
+    const WsPlan plan = plan_workspace(kind, T, C, sum_k);
+    if (ws_bytes < plan.total) return BC_E_WORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return BC_E_HIP;
+    DevInfo di;
+    if (device_info(dev, &di) != hipSuccess) return BC_E_HIP;
+    const Ws w = carve_workspace(ws, plan);
+    std::lock_guard<std::mutex> lk(g_mu);
+    Entry* en = nullptr;
+    hipError_t e = cache_get(d.data(), d.size() * sizeof(TDesc), s, &en);
+    if (e != hipSuccess) return BC_E_HIP;
+    const TDesc* dd = (const TDesc*)en->dev;
+    switch (kind) {
+        case BC_SIGN1:
+            e = launch_sign_compress(dd, T, C, maxc, a16, a32, out.bits, out.scale, w, di, s);
+            break;
+        case BC_TOPK:
+        case BC_TOPK_SAMPLED:
+            e = launch_topk(kind == BC_TOPK ? 0 : 1, ratio, seed, dd, T, C, a16, a32, out.idx, out.val,
+                            w, s);
+            break;
+        default:
+            e = launch_randk(seed, dd, T, C, sum_k, a16, a32, out.idx, out.val, w, s);
+            break;
+    }
+    cache_mark_used(en, s);
+    return finish(hip_status(e), s, ws);
+}
+
+int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, int W,
+                                  const uint64_t* n, int T, float* const* out, float alpha,
+                                  void* ws, size_t ws_bytes, void* stream) {
+    uint64_t ppm;
+    int rc = check_kind_ratio(kind, ratio, ppm);
+    if (rc) return rc;
+    if (T < 0 || T > kMaxT || W < 1 || W > kMaxW) return BC_E_COUNT;
+    if (T == 0) return BC_OK;
+    if (!in || !n || !out) return BC_E_NULL;
+    if (!ws) return BC_E_WORKSPACE;
+    if (ws_bytes < 256) return BC_E_WORKSPACE;
+    const bool sparse = is_sparse(kind);
+    const uint32_t unit = sparse ? kSparseTile : kSignAggUnit;
+    std::vector<unsigned char> table;
+    try {
+        table.resize((size_t)T * sizeof(ADesc) + (size_t)W * sizeof(WDesc));
+    } catch (const std::bad_alloc&) {
+        return BC_E_SIZE;
+    }
+    ADesc* a = (ADesc*)table.data();
+    WDesc* wd = (WDesc*)(table.data() + (size_t)T * sizeof(ADesc));
+    uint64_t units = 0, off = 0;
+    for (int i = 0; i < T; ++i) {
+        if (n[i] >= kMaxN) return BC_E_SIZE;
+        if (n[i] > 0 && !out[i]) return BC_E_NULL;
+        if ((uintptr_t)out[i] & 15u) return BC_E_ALIGN;
+        const uint64_t cnt = sparse ? k_of(n[i], ppm) : words_of(n[i]);
+        const uint64_t nu = (n[i] + unit - 1) / unit;
+        a[i].out = out[i];
+        a[i].n = (uint32_t)n[i];
+        a[i].k = (uint32_t)cnt;
+        a[i].off = off;
+        a[i].unit0 = (uint32_t)units;
+        a[i].nunits = (uint32_t)nu;
+        off += cnt;
+        units += nu;
+    }
+    if (units >= (1ull << 31)) return BC_E_SIZE;
+    for (int q = 0; q < W; ++q) {
+        if (sparse) {
+            if (off && (!in[q].idx || !in[q].val)) return BC_E_NULL;
+            wd[q].a = in[q].idx;
+            wd[q].b = in[q].val;
+        } else {
+            if (!in[q].bits || !in[q].scale) return BC_E_NULL;
+            wd[q].a = in[q].bits;
+            wd[q].b = in[q].scale;
+        }
+    }
+    hipStream_t s = (hipStream_t)stream;
+    std::lock_guard<std::mutex> lk(g_mu);
+    Entry* en = nullptr;
+    hipError_t e = cache_get(table.data(), table.size(), s, &en);
+    if (e != hipSuccess) return BC_E_HIP;
+    const ADesc* ad = (const ADesc*)en->dev;
+    const WDesc* wdd = (const WDesc*)((const char*)en->dev + (size_t)T * sizeof(ADesc));
+    if (sparse)
+        e = launch_aggregate_sparse(ad, T, (uint32_t)units, wdd, W, alpha, s);
+    else
+        e = launch_aggregate_sign(ad, T, (uint32_t)units, wdd, W, alpha, s);
+    cache_mark_used(en, s);
+    return finish(hip_status(e), s, ws);
+}
+
+int bytecomp_residual_update(int kind, double ratio, const bc_tensor* t, int T, bc_payload own,
+                             void* stream) {
+    uint64_t ppm;
+    int rc = check_kind_ratio(kind, ratio, ppm);
+    if (rc) return rc;
+    if (T < 0 || T > kMaxT) return BC_E_COUNT;
+    if (T == 0) return BC_OK;
+    if (!t) return BC_E_NULL;
+    if (is_sparse(kind) ? (!own.idx || !own.val) : (!own.bits || !own.scale)) return BC_E_NULL;
+    std::vector<TDesc> d;
+    uint32_t C, maxc;
+    uint64_t sum_k;
+    bool a16, a32;
+    try {
+        rc = build_tdesc(kind, ppm, t, T, true, d, C, maxc, sum_k, a16, a32);
+    } catch (const std::bad_alloc&) {
+        return BC_E_SIZE;
+    }
+    if (rc) return rc;
+    hipStream_t s = (hipStream_t)stream;
+    std::lock_guard<std::mutex> lk(g_mu);
+    Entry* en = nullptr;
+    hipError_t e = cache_get(d.data(), d.size() * sizeof(TDesc), s, &en);
+    if (e != hipSuccess) return BC_E_HIP;
+    e = launch_residual_update(kind, (const TDesc*)en->dev, T, C, a16, a32, own.idx, own.val,
+                               own.bits, own.scale, s);
+    cache_mark_used(en, s);
+    return finish(hip_status(e), s, nullptr);
+}
+
+int bytecomp_device_status(void* ws, size_t ws_bytes, void* stream, uint32_t* flags) {
+    if (!ws || !flags) return BC_E_NULL;
+    if (ws_bytes < 256) return BC_E_WORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
+    uint32_t f = 0;
+    hipError_t e = hipMemcpyAsync(&f, ws, 4, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e == hipSuccess) e = launch_zero_header((uint32_t*)ws, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return BC_E_HIP;
+    *flags = f;
+    return BC_OK;
+}
+
+}  // extern "C"

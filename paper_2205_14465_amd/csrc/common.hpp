@@ -1,0 +1,282 @@
+// common.hpp -- device-side descriptors and helpers shared by the gfx950
+// kernels of the compression library.  Everything here is product code;
+// nothing is shared with the CPU oracle.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace bc {
+
+// ---------------------------------------------------------------- geometry
+// Streaming passes: one 256-thread workgroup (four wave64s) owns a chunk of
+// 4096 consecutive elements of one tensor; thread j holds elements
+// 1024*r + 4*j + q (r, q = 0..3) so every load instruction of a wave reads
+// 1 KiB of fp32 contiguously.
+constexpr int kBlock = 256;
+constexpr int kChunk = 4096;
+constexpr int kEpt = kChunk / kBlock;     // 16 elements per thread
+constexpr int kRounds = 4;                // 4 rounds of 1024 elements
+constexpr int kChunkWords = kChunk / 32;  // 128 sign words per chunk
+constexpr int kBins0 = 2048;              // radix digit 0: key bits 30..20
+constexpr int kBins12 = 1024;             // radix digits 1, 2: bits 19..10, 9..0
+
+// ------------------------------------------------------------ descriptors
+// One tensor of a compress or residual-update call (48 bytes).
+struct TDesc {
+    const void* grad;
+    float* resid;       // nullptr: error feedback off
+    uint32_t n;
+    uint32_t dtype;     // 0 fp32, 1 fp16
+    uint32_t tid;
+    uint32_t k;         // sparse: k_t; sign: word count
+    uint64_t off;       // payload offset of this tensor (entries or words)
+    uint32_t chunk0;    // first global chunk index
+    uint32_t nchunks;
+};
+static_assert(sizeof(TDesc) == 48, "TDesc layout");
+
+// One tensor of an aggregate call (32 bytes).
+struct ADesc {
+    float* out;
+    uint32_t n;
+    uint32_t k;         // sparse: k_t; sign: word count
+    uint64_t off;       // payload offset (same for every worker)
+    uint32_t unit0;     // first global work unit (tile / wave chunk)
+    uint32_t nunits;
+};
+static_assert(sizeof(ADesc) == 32, "ADesc layout");
+
+// One worker's payload in an aggregate call.
+struct WDesc {
+    const uint32_t* a;  // sparse: idx; sign: bits
+    const float* b;     // sparse: val; sign: scale
+};
+
+// Largest t with d[t].chunk0 <= c (tensors without chunks share chunk0 with
+// their successor, so the search lands on the tensor that owns chunk c).
+template <typename D, uint32_t D::*Field>
+__device__ __forceinline__ int find_owner(const D* __restrict__ d, int T, uint32_t c) {
+    int lo = 0, hi = T - 1;
+    while (lo < hi) {
+        int mid = (lo + hi + 1) >> 1;
+        if (d[mid].*Field <= c) lo = mid; else hi = mid - 1;
+    }
+    return lo;
+}
+
+__device__ __forceinline__ int tensor_of_chunk(const TDesc* __restrict__ d, int T, uint32_t c) {
+    return find_owner<TDesc, &TDesc::chunk0>(d, T, c);
+}
+
+// ------------------------------------------------------------- bit helpers
+__device__ __forceinline__ uint32_t f2u(float x) { return __float_as_uint(x); }
+__device__ __forceinline__ float u2f(uint32_t u) { return __uint_as_float(u); }
+__device__ __forceinline__ uint32_t key_of(float x) { return f2u(x) & 0x7FFFFFFFu; }
+
+// IEEE binary16 bits -> fp32 (exact, subnormals included: v_cvt_f32_f16
+// with fp16 denormals enabled, the HIP default).
+__device__ __forceinline__ float h2f(uint32_t bits16) {
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)bits16);
+}
+
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+__device__ __forceinline__ int wave_id() {
+    return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+}
+
+// ----------------------------------------------------------- chunk loading
+// Load the 16 elements a thread owns of chunk `j` of tensor `td`, forming
+// v = widen(g) + e (e = 0 when there is no residual or `use_resid` is
+// false).  Elements past the tensor's end read as +0.0 and are reported
+// invalid through `valid` (bit 4*r + q).
+template <int DT>
+__device__ __forceinline__ void load_chunk(const TDesc& td, uint32_t j, bool use_resid,
+                                           float v[kEpt], uint32_t& valid) {
+    const uint32_t base = j * (uint32_t)kChunk;
+    const uint32_t n = td.n;
+    valid = 0;
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r) {
+        const uint32_t e0 = base + 1024u * r + 4u * threadIdx.x;
+        float g4[4] = {0.f, 0.f, 0.f, 0.f};
+        float e4[4] = {0.f, 0.f, 0.f, 0.f};
+        if (e0 + 3 < n) {
+            if (DT == 0) {
+                float4 x = *reinterpret_cast<const float4*>((const float*)td.grad + e0);
+                g4[0] = x.x; g4[1] = x.y; g4[2] = x.z; g4[3] = x.w;
+            } else {
+                uint2 h = *reinterpret_cast<const uint2*>((const uint16_t*)td.grad + e0);
+                g4[0] = h2f(h.x & 0xFFFFu);
+                g4[1] = h2f(h.x >> 16);
+                g4[2] = h2f(h.y & 0xFFFFu);
+                g4[3] = h2f(h.y >> 16);
+            }
+            if (use_resid) {
+                float4 y = *reinterpret_cast<const float4*>(td.resid + e0);
+                e4[0] = y.x; e4[1] = y.y; e4[2] = y.z; e4[3] = y.w;
+            }
+            valid |= 0xFu << (4 * r);
+        } else {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                if (e0 + q < n) {
+                    if (DT == 0) g4[q] = ((const float*)td.grad)[e0 + q];
+                    else g4[q] = h2f(((const uint16_t*)td.grad)[e0 + q]);
+                    if (use_resid) e4[q] = td.resid[e0 + q];
+                    valid |= 1u << (4 * r + q);
+                }
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[4 * r + q] = use_resid ? g4[q] + e4[q] : g4[q];
+    }
+}
+
+// Runtime dtype dispatch (uniform per workgroup: a chunk has one tensor).
+__device__ __forceinline__ void load_v(const TDesc& td, uint32_t j, bool use_resid, float v[kEpt],
+                                       uint32_t& valid) {
+    if (td.dtype == 0) load_chunk<0>(td, j, use_resid, v, valid);
+    else load_chunk<1>(td, j, use_resid, v, valid);
+}
+
+// Load v that an earlier pass already stored (the residual buffer holds v),
+// or recompute it from the gradient when error feedback is off.
+__device__ __forceinline__ void load_stored_v(const TDesc& td, uint32_t j, float v[kEpt],
+                                              uint32_t& valid) {
+    if (td.resid) {
+        const uint32_t base = j * (uint32_t)kChunk;
+        valid = 0;
+#pragma unroll
+        for (int r = 0; r < kRounds; ++r) {
+            const uint32_t e0 = base + 1024u * r + 4u * threadIdx.x;
+            if (e0 + 3 < td.n) {
+                float4 y = *reinterpret_cast<const float4*>(td.resid + e0);
+                v[4 * r] = y.x; v[4 * r + 1] = y.y; v[4 * r + 2] = y.z; v[4 * r + 3] = y.w;
+                valid |= 0xFu << (4 * r);
+            } else {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    bool ok = e0 + q < td.n;
+                    v[4 * r + q] = ok ? td.resid[e0 + q] : 0.f;
+                    valid |= (ok ? 1u : 0u) << (4 * r + q);
+                }
+            }
+        }
+    } else if (td.dtype == 0) {
+        load_chunk<0>(td, j, false, v, valid);
+    } else {
+        load_chunk<1>(td, j, false, v, valid);
+    }
+}
+
+// Store 16 per-thread values back to a dense fp32 tensor (same pattern).
+__device__ __forceinline__ void store_chunk(float* dst, uint32_t n, uint32_t j, const float v[kEpt]) {
+    const uint32_t base = j * (uint32_t)kChunk;
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r) {
+        const uint32_t e0 = base + 1024u * r + 4u * threadIdx.x;
+        if (e0 + 3 < n) {
+            *reinterpret_cast<float4*>(dst + e0) =
+                make_float4(v[4 * r], v[4 * r + 1], v[4 * r + 2], v[4 * r + 3]);
+        } else {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                if (e0 + q < n) dst[e0 + q] = v[4 * r + q];
+        }
+    }
+}
+
+// --------------------------------------------------------- block reductions
+// Sum of a double over the 256 threads in a fixed tree (deterministic for a
+// given block shape); every thread receives the total.
+__device__ __forceinline__ double block_sum_f64(double x, double* sh /* >= 4 */) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
+    if (lane_id() == 0) sh[threadIdx.x >> 6] = x;
+    __syncthreads();
+    double t = (sh[0] + sh[1]) + (sh[2] + sh[3]);
+    __syncthreads();
+    return t;
+}
+
+// Exclusive prefix of a 64-bit value over the block (thread order), plus
+// the block total.  `sh` needs 4 entries.
+__device__ __forceinline__ uint64_t block_excl_scan_u64(uint64_t x, uint64_t* sh, uint64_t& total) {
+    const int lane = lane_id();
+    uint64_t inc = x;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        uint64_t y = __shfl_up(inc, o, 64);
+        if (lane >= o) inc += y;
+    }
+    if (lane == 63) sh[threadIdx.x >> 6] = inc;
+    __syncthreads();
+    const int w = threadIdx.x >> 6;
+    uint64_t before = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) before += (q < w) ? sh[q] : 0;
+    total = sh[0] + sh[1] + sh[2] + sh[3];
+    __syncthreads();
+    return before + inc - x;
+}
+
+// ------------------------------------------------------- device atomics
+__device__ __forceinline__ uint32_t atomic_add_agent(uint32_t* p, uint32_t v) {
+    return __hip_atomic_fetch_add(p, v, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t atomic_load_acquire(uint32_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void atomic_store_release(uint32_t* p, uint32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void atomic_store_relaxed(uint32_t* p, uint32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ------------------------------------------------------------- Philox
+// Philox4x64-10 counter-based generator (Salmon et al., SC'11): ten rounds
+// of two 64x64->128-bit multiplies on counter words 0 and 2, a fixed word
+// permutation and xor with the remaining words and the key; the key is
+// advanced by the two Weyl constants before every round but the first.
+struct U64x4 { uint64_t v[4]; };
+
+__host__ __device__ inline void mul_hilo64(uint64_t a, uint64_t b, uint64_t& hi, uint64_t& lo) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    hi = __umul64hi(a, b);
+    lo = a * b;
+#else
+    unsigned __int128 p = (unsigned __int128)a * b;
+    hi = (uint64_t)(p >> 64);
+    lo = (uint64_t)p;
+#endif
+}
+
+__host__ __device__ inline U64x4 philox4x64_10(U64x4 c, uint64_t k0, uint64_t k1) {
+    const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+    const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        if (r) { k0 += W0; k1 += W1; }
+        uint64_t h0, l0, h1, l1;
+        mul_hilo64(M0, c.v[0], h0, l0);
+        mul_hilo64(M1, c.v[2], h1, l1);
+        U64x4 o;
+        o.v[0] = h1 ^ c.v[1] ^ k0;
+        o.v[1] = l1;
+        o.v[2] = h0 ^ c.v[3] ^ k1;
+        o.v[3] = l0;
+        c = o;
+    }
+    return c;
+}
+
+// Random-stream ids (second key word).
+constexpr uint64_t kStreamRandk = 0;
+constexpr uint64_t kStreamSample = 1;
+
+// Workspace header: failure flags (bit 0: a bounded wait ran out).
+constexpr uint32_t kFlagWaitTimeout = 1u;
+
+}  // namespace bc

@@ -1,0 +1,409 @@
+// kernels_topk.hip -- top-k sparsification with error feedback on gfx950:
+// exact top-k and the DGC-style sampled-threshold variant (paper Sec. 2.3,
+// sparsification; Sec. 5.1, DGC at a 1% rate with error feedback).
+//
+// Result (both kinds): the k_t entries of v = g + e_old with the largest
+// |v| (keys = magnitude bits), ties to the lower index, emitted with
+// ascending indices and values v[idx]; residual e_new = v with the chosen
+// entries set to +0.0.
+//
+// Pipeline (all tensors of a call advance together, one launch per step):
+//   exact:    stream pass 1 writes e_new = v and a 2048-bin histogram of
+//             key bits 30..20 per tensor -> exact bin of the k-th key ->
+//             stream pass 2 re-reads v and compacts the candidates (keys at
+//             or above that bin) per 4096-element chunk, in index order.
+//   sampled:  a seeded 1% sample (runs of 64 elements) histogrammed per
+//             tensor -> threshold bin with a margin -> ONE stream pass
+//             writes e_new = v and compacts candidates.  If a tensor ends
+//             with fewer than k candidates, the exact histogram path runs
+//             for that tensor only (reading v back from e_new).
+//   both:     radix select over the candidates only (digits of 11, 10 and
+//             10 bits, histograms in LDS, merged with integer atomics)
+//             finds the k-th key tau and how many tau-ties to keep; a scan
+//             over chunks places each chunk's winners; the emit pass writes
+//             the payload and zeroes e_new at the winners.
+// Trimming or topping up to exactly k in the selection order makes the
+// sampled kind return the same entries as the exact kind.
+#include "launch.hpp"
+
+namespace bc {
+
+namespace {
+
+enum FindMode : int {
+    kFindThrExact = 0,    // histogram of all keys -> bin of the k-th key
+    kFindThrSample = 1,   // histogram of sample keys -> threshold with margin
+    kFindDigit0 = 2,      // candidates' bits 30..20 (sets t_fb if too few)
+    kFindDigit1 = 3,      // bits 19..10
+    kFindDigit2 = 4,      // bits 9..0
+};
+
+constexpr uint32_t kAllCandidatesBelow = 16u * kChunk;  // small tensors skip the sample
+
+__device__ __forceinline__ bool active(const uint32_t* fb, int t, bool fb_only) {
+    return !fb_only || fb[t] != 0u;
+}
+
+// Flush a block's LDS histogram into the tensor's global histogram.
+__device__ __forceinline__ void flush_hist(const uint32_t* lh, uint32_t* gh, int bins) {
+    for (int b = threadIdx.x; b < bins; b += kBlock) {
+        const uint32_t x = lh[b];
+        if (x) atomicAdd(gh + b, x);
+    }
+}
+
+}  // namespace
+
+// Stream pass of the exact path: e_new = v (when `write_resid`) and the
+// histogram of key bits 30..20.  With `fb_only` it re-reads the stored v of
+// tensors flagged for the fallback.
+__global__ __launch_bounds__(kBlock) void topk_hist_pass(const TDesc* __restrict__ d, int T,
+                                                         int write_resid, int fb_only, Ws ws) {
+    __shared__ uint32_t lh[kBins0];
+    const uint32_t c = blockIdx.x;
+    const int t = tensor_of_chunk(d, T, c);
+    if (!active(ws.t_fb, t, fb_only)) return;
+    const TDesc td = d[t];
+    const uint32_t j = c - td.chunk0;
+    for (int b = threadIdx.x; b < kBins0; b += kBlock) lh[b] = 0;
+    float v[kEpt];
+    uint32_t valid;
+    if (write_resid) {
+        load_v(td, j, td.resid != nullptr, v, valid);
+        if (td.resid) store_chunk(td.resid, td.n, j, v);
+    } else {
+        load_stored_v(td, j, v, valid);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kEpt; ++i)
+        if ((valid >> i) & 1u) atomicAdd(&lh[key_of(v[i]) >> 20], 1u);
+    __syncthreads();
+    flush_hist(lh, ws.t_hist + (size_t)t * kBins0, kBins0);
+}
+
+// Seeded sample: each 4096-element chunk of a tensor larger than
+// kAllCandidatesBelow contributes one run of 64 consecutive elements with
+// probability 0.64 (an expected 1% of the tensor); one wave per chunk.
+__global__ __launch_bounds__(kBlock) void topk_sample_hist(const TDesc* __restrict__ d, int T,
+                                                           uint32_t C, uint64_t seed, Ws ws) {
+    const uint32_t c = blockIdx.x * 4u + (threadIdx.x >> 6);
+    if (c >= C) return;
+    const int t = tensor_of_chunk(d, T, c);
+    const TDesc td = d[t];
+    if (td.n < kAllCandidatesBelow) return;
+    const uint32_t j = c - td.chunk0;
+    U64x4 ctr = {{(uint64_t)td.tid, (uint64_t)j, 0, 0}};
+    const U64x4 r = philox4x64_10(ctr, seed, kStreamSample);
+    const uint32_t u = (uint32_t)(r.v[0] >> 32);
+    if (u >= 2748779069u) return;  // 0.64 * 2^32
+    const uint32_t len = (j + 1 == td.nchunks) ? td.n - j * (uint32_t)kChunk : (uint32_t)kChunk;
+    if (len < 64) return;
+    const uint32_t start = j * (uint32_t)kChunk + (uint32_t)(r.v[1] % (uint64_t)(len - 63));
+    const uint32_t i = start + lane_id();
+    float g;
+    if (td.dtype == 0) g = ((const float*)td.grad)[i];
+    else g = h2f(((const uint16_t*)td.grad)[i]);
+    const float v = td.resid ? g + td.resid[i] : g;
+    atomicAdd(ws.t_hist + (size_t)t * kBins0 + (key_of(v) >> 20), 1u);
+}
+
+// One workgroup per tensor: read (and clear) the tensor's histogram and
+// pick the bin / digit the mode asks for.
+__global__ __launch_bounds__(kBlock) void topk_find(const TDesc* __restrict__ d, double ratio,
+                                                    int mode, int fb_only, Ws ws) {
+    __shared__ uint64_t sh[4];
+    __shared__ uint32_t found_bin, found_above, found_total;
+    const int t = blockIdx.x;
+    const TDesc td = d[t];
+    if (td.k == 0 || !active(ws.t_fb, t, fb_only)) return;
+    const int bins = (mode == kFindDigit1 || mode == kFindDigit2) ? kBins12 : kBins0;
+    const int per = bins / kBlock;
+    uint32_t* gh = ws.t_hist + (size_t)t * kBins0;
+    // thread i owns bins [bins - (i+1)*per, bins - i*per): thread 0 the top
+    const int hi = bins - threadIdx.x * per;
+    uint32_t h[8];
+    uint32_t mine = 0;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        if (q < per) {
+            h[q] = gh[hi - 1 - q];
+            gh[hi - 1 - q] = 0;
+            mine += h[q];
+        }
+    }
+    uint64_t total64;
+    const uint64_t above0 = block_excl_scan_u64(mine, sh, total64);
+    const uint32_t total = (uint32_t)total64;
+    uint32_t target;
+    if (mode == kFindThrExact) {
+        target = td.k;
+    } else if (mode == kFindThrSample) {
+        if (td.n < kAllCandidatesBelow || total == 0) {
+            if (threadIdx.x == 0) ws.t_thr[t] = 0;
+            return;
+        }
+        // k rule on the sample size, plus a margin so that the candidates
+        // usually cover the k-th key of the tensor
+        const uint64_t ppm = (uint64_t)llround(ratio * 1e6);
+        uint64_t ks = ((uint64_t)total * ppm + 999999u) / 1000000u;
+        if (ks < 1) ks = 1;
+        uint64_t tg = ks + ks / 4 + 16;
+        target = (uint32_t)(tg < total ? tg : total);
+    } else if (mode == kFindDigit0) {
+        target = td.k;
+        if (total < td.k) {  // too few candidates: exact fallback for this tensor
+            if (threadIdx.x == 0) ws.t_fb[t] = 1u;
+            return;
+        }
+        if (threadIdx.x == 0) ws.t_fb[t] = 0u;
+    } else {
+        target = ws.t_krem[t];
+    }
+    if (threadIdx.x == 0) found_total = total;
+    uint32_t above = (uint32_t)above0;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        if (q < per) {
+            if (above < target && target <= above + h[q]) {
+                found_bin = (uint32_t)(hi - 1 - q);
+                found_above = above;
+            }
+            above += h[q];
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x != 0) return;
+    const uint32_t b = found_bin;
+    switch (mode) {
+        case kFindThrExact:
+        case kFindThrSample:
+            ws.t_thr[t] = b << 20;
+            break;
+        case kFindDigit0:
+            ws.t_prefix[t] = b << 20;
+            ws.t_krem[t] = target - found_above;
+            break;
+        case kFindDigit1:
+            ws.t_prefix[t] |= b << 10;
+            ws.t_krem[t] = target - found_above;
+            break;
+        default:
+            ws.t_prefix[t] |= b;
+            ws.t_krem[t] = target - found_above;
+            break;
+    }
+    (void)found_total;
+}
+
+// Candidate compaction.  Stream mode (sampled main pass): v = g + e,
+// e_new = v written back.  Re-read mode: v from the residual (or g).
+// Candidates = valid entries with key >= t_thr[t], compacted in index
+// order into the chunk's slot of t_cand; also the LDS histogram of their
+// key bits 30..20.
+__global__ __launch_bounds__(kBlock) void topk_compact(const TDesc* __restrict__ d, int T,
+                                                       int stream_mode, int fb_only, Ws ws) {
+    __shared__ uint32_t lh[kBins0];
+    __shared__ uint64_t sh[4];
+    const uint32_t c = blockIdx.x;
+    const int t = tensor_of_chunk(d, T, c);
+    if (!active(ws.t_fb, t, fb_only)) return;
+    const TDesc td = d[t];
+    const uint32_t j = c - td.chunk0;
+    for (int b = threadIdx.x; b < kBins0; b += kBlock) lh[b] = 0;
+    float v[kEpt];
+    uint32_t valid;
+    if (stream_mode) {
+        load_v(td, j, td.resid != nullptr, v, valid);
+        if (td.resid) store_chunk(td.resid, td.n, j, v);
+    } else {
+        load_stored_v(td, j, v, valid);
+    }
+    const uint32_t thr = ws.t_thr[t];
+    uint32_t pm = 0;
+#pragma unroll
+    for (int i = 0; i < kEpt; ++i)
+        if (((valid >> i) & 1u) && key_of(v[i]) >= thr) pm |= 1u << i;
+    uint64_t packed = 0;
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r) packed |= (uint64_t)__popc((pm >> (4 * r)) & 0xFu) << (16 * r);
+    uint64_t tot;
+    const uint64_t pre = block_excl_scan_u64(packed, sh, tot);
+    uint2* out = ws.t_cand + (size_t)c * kChunk;
+    uint32_t base = 0;
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r) {
+        uint32_t rank = base + (uint32_t)((pre >> (16 * r)) & 0xFFFFu);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int i = 4 * r + q;
+            if ((pm >> i) & 1u) {
+                const uint32_t e = j * (uint32_t)kChunk + 1024u * r + 4u * threadIdx.x + q;
+                out[rank++] = make_uint2(e, f2u(v[i]));
+                atomicAdd(&lh[key_of(v[i]) >> 20], 1u);
+            }
+        }
+        base += (uint32_t)((tot >> (16 * r)) & 0xFFFFu);
+    }
+    if (threadIdx.x == 0) ws.t_ccount[c] = base;
+    __syncthreads();
+    flush_hist(lh, ws.t_hist + (size_t)t * kBins0, kBins0);
+}
+
+// Radix pass over a chunk's candidates: histogram of the next digit among
+// candidates whose higher bits match the prefix chosen so far.
+__global__ __launch_bounds__(kBlock) void topk_cand_hist(const TDesc* __restrict__ d, int T,
+                                                         int pass, Ws ws) {
+    __shared__ uint32_t lh[kBins12];
+    const uint32_t c = blockIdx.x;
+    const uint32_t m = ws.t_ccount[c];
+    if (m == 0) return;
+    const int t = tensor_of_chunk(d, T, c);
+    const uint32_t prefix = ws.t_prefix[t];
+    const int shift = pass == 1 ? 10 : 0;
+    const int match_shift = pass == 1 ? 20 : 10;
+    for (int b = threadIdx.x; b < kBins12; b += kBlock) lh[b] = 0;
+    __syncthreads();
+    const uint2* cand = ws.t_cand + (size_t)c * kChunk;
+    for (uint32_t i = threadIdx.x; i < m; i += kBlock) {
+        const uint32_t key = cand[i].y & 0x7FFFFFFFu;
+        if ((key >> match_shift) == (prefix >> match_shift))
+            atomicAdd(&lh[(key >> shift) & (kBins12 - 1)], 1u);
+    }
+    __syncthreads();
+    flush_hist(lh, ws.t_hist + (size_t)t * kBins0, kBins12);
+}
+
+// Per chunk: candidates above tau and equal to tau.
+__global__ __launch_bounds__(kBlock) void topk_cand_count(const TDesc* __restrict__ d, int T, Ws ws) {
+    __shared__ uint64_t sh[4];
+    const uint32_t c = blockIdx.x;
+    const uint32_t m = ws.t_ccount[c];
+    const int t = tensor_of_chunk(d, T, c);
+    const uint32_t tau = ws.t_prefix[t];
+    const uint2* cand = ws.t_cand + (size_t)c * kChunk;
+    uint64_t x = 0;
+    for (uint32_t i = threadIdx.x; i < m; i += kBlock) {
+        const uint32_t key = cand[i].y & 0x7FFFFFFFu;
+        x += (key > tau) ? 1ull : 0ull;
+        x += (key == tau) ? (1ull << 32) : 0ull;
+    }
+    uint64_t tot;
+    block_excl_scan_u64(x, sh, tot);
+    if (threadIdx.x == 0) {
+        ws.t_gt[c] = (uint32_t)tot;
+        ws.t_eq[c] = (uint32_t)(tot >> 32);
+    }
+}
+
+// One workgroup per tensor: place every chunk's winners.  eqb[c] = number
+// of tau-equal candidates in earlier chunks; a chunk keeps its tau-equal
+// candidates while the running count stays below the number needed.
+__global__ __launch_bounds__(kBlock) void topk_cand_scan(const TDesc* __restrict__ d, Ws ws) {
+    __shared__ uint64_t sh[4];
+    const int t = blockIdx.x;
+    const TDesc td = d[t];
+    if (td.k == 0) return;
+    const uint32_t need = ws.t_krem[t];
+    uint64_t carry_eq = 0, carry_pos = td.off;
+    for (uint32_t c0 = 0; c0 < td.nchunks; c0 += kBlock) {
+        const uint32_t cl = c0 + threadIdx.x;
+        const bool in = cl < td.nchunks;
+        const uint32_t c = td.chunk0 + cl;
+        const uint32_t gt = in ? ws.t_gt[c] : 0u;
+        const uint32_t eq = in ? ws.t_eq[c] : 0u;
+        uint64_t tot_eq;
+        const uint64_t eqb = carry_eq + block_excl_scan_u64(eq, sh, tot_eq);
+        const uint64_t left = eqb < need ? need - eqb : 0;
+        const uint32_t taken = (uint32_t)(left < eq ? left : eq);
+        uint64_t tot_sel;
+        const uint64_t pos = carry_pos + block_excl_scan_u64((uint64_t)gt + taken, sh, tot_sel);
+        if (in) {
+            ws.t_off[c] = pos;
+            ws.t_eqb[c] = (uint32_t)(eqb < 0xFFFFFFFFull ? eqb : 0xFFFFFFFFull);
+        }
+        carry_eq += tot_eq;
+        carry_pos += tot_sel;
+    }
+}
+
+// Emit the winners of a chunk in index order and clear them in e_new.
+__global__ __launch_bounds__(kBlock) void topk_emit(const TDesc* __restrict__ d, int T,
+                                                    uint32_t* __restrict__ idx,
+                                                    float* __restrict__ val, Ws ws) {
+    __shared__ uint64_t sh[4];
+    const uint32_t c = blockIdx.x;
+    const uint32_t m = ws.t_ccount[c];
+    if (m == 0) return;
+    const int t = tensor_of_chunk(d, T, c);
+    float* resid = d[t].resid;
+    const uint64_t end = d[t].off + d[t].k;
+    const uint32_t tau = ws.t_prefix[t];
+    const uint32_t need = ws.t_krem[t];
+    const uint2* cand = ws.t_cand + (size_t)c * kChunk;
+    uint64_t eq_seen = ws.t_eqb[c];
+    uint64_t pos = ws.t_off[c];
+    for (uint32_t i0 = 0; i0 < m; i0 += kBlock) {
+        const uint32_t i = i0 + threadIdx.x;
+        uint2 e = make_uint2(0, 0);
+        uint32_t key = 0;
+        if (i < m) {
+            e = cand[i];
+            key = e.y & 0x7FFFFFFFu;
+        }
+        const bool is_eq = i < m && key == tau;
+        uint64_t n_eq;
+        const uint64_t eq_rank = eq_seen + block_excl_scan_u64(is_eq ? 1u : 0u, sh, n_eq);
+        const bool sel = i < m && (key > tau || (is_eq && eq_rank < need));
+        uint64_t n_sel;
+        const uint64_t at = pos + block_excl_scan_u64(sel ? 1u : 0u, sh, n_sel);
+        if (sel && at < end) {
+            idx[at] = e.x;
+            val[at] = u2f(e.y);
+            if (resid) resid[e.x] = 0.f;
+        }
+        eq_seen += n_eq;
+        pos += n_sel;
+    }
+}
+
+__global__ void topk_zero_hist(uint32_t* h, uint64_t n) {
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (uint64_t)gridDim.x * blockDim.x)
+        h[i] = 0u;
+}
+
+hipError_t launch_topk(int kind, double ratio, uint64_t seed, const TDesc* d, int T, uint32_t C,
+                       bool, bool, uint32_t* idx, float* val, const Ws& ws, hipStream_t s) {
+    if (C == 0) return hipSuccess;
+    const dim3 blk(kBlock);
+    const uint64_t hn = (uint64_t)T * kBins0;
+    uint32_t zb = (uint32_t)((hn + 255) / 256);
+    if (zb > 4096) zb = 4096;
+    hipLaunchKernelGGL(topk_zero_hist, dim3(zb), dim3(256), 0, s, ws.t_hist, hn);
+    if (kind == 0) {  // exact
+        hipLaunchKernelGGL(topk_hist_pass, dim3(C), blk, 0, s, d, T, 1, 0, ws);
+        hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindThrExact, 0, ws);
+        hipLaunchKernelGGL(topk_compact, dim3(C), blk, 0, s, d, T, 0, 0, ws);
+        hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit0, 0, ws);
+    } else {  // sampled threshold, exact fallback per tensor
+        hipLaunchKernelGGL(topk_sample_hist, dim3((C + 3) / 4), blk, 0, s, d, T, C, seed, ws);
+        hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindThrSample, 0, ws);
+        hipLaunchKernelGGL(topk_compact, dim3(C), blk, 0, s, d, T, 1, 0, ws);
+        hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit0, 0, ws);
+        hipLaunchKernelGGL(topk_hist_pass, dim3(C), blk, 0, s, d, T, 0, 1, ws);
+        hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindThrExact, 1, ws);
+        hipLaunchKernelGGL(topk_compact, dim3(C), blk, 0, s, d, T, 0, 1, ws);
+        hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit0, 1, ws);
+    }
+    hipLaunchKernelGGL(topk_cand_hist, dim3(C), blk, 0, s, d, T, 1, ws);
+    hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit1, 0, ws);
+    hipLaunchKernelGGL(topk_cand_hist, dim3(C), blk, 0, s, d, T, 2, ws);
+    hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit2, 0, ws);
+    hipLaunchKernelGGL(topk_cand_count, dim3(C), blk, 0, s, d, T, ws);
+    hipLaunchKernelGGL(topk_cand_scan, dim3(T), blk, 0, s, d, ws);
+    hipLaunchKernelGGL(topk_emit, dim3(C), blk, 0, s, d, T, idx, val, ws);
+    return hipGetLastError();
+}
+
+}  // namespace bc

@@ -1,0 +1,86 @@
+// launch.hpp -- host-side launchers of the gfx950 kernels and the
+// workspace carve-up they share.  Included by the C-ABI layer only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "common.hpp"
+
+namespace bc {
+
+// Pointers into the caller's workspace.  Every call clears the counters it
+// uses in its first kernel, so the workspace needs no initialisation and may
+// be shared by calls of different kinds and shapes (not concurrently).
+struct Ws {
+    uint32_t* flags;        // header: failure flags
+    // BC_SIGN1
+    uint32_t* s_cnt;        // [T] arrival counters          
+    uint32_t* s_ready;      // [T] scale-published flags     
+    float* s_val;           // [T] published scales
+    double* s_partial;      // [C] per-chunk sums of |v|
+    // BC_TOPK, BC_TOPK_SAMPLED
+    uint32_t* t_hist;       // [T * 2048] histograms         
+    uint32_t* t_thr;        // [T] candidate threshold (key)
+    uint32_t* t_prefix;     // [T] radix-select prefix (key)
+    uint32_t* t_krem;       // [T] entries still to select
+    uint32_t* t_fb;         // [T] 1 = tensor needs the exact-histogram fallback
+    uint2* t_cand;          // [C * 4096] candidates (local index, value bits)
+    uint32_t* t_ccount;     // [C] candidates per chunk
+    uint32_t* t_gt;         // [C] candidates above the threshold key
+    uint32_t* t_eq;         // [C] candidates equal to the threshold key
+    uint64_t* t_off;        // [C] payload position of a chunk's first winner
+    uint32_t* t_eqb;        // [C] equal-key candidates in earlier chunks
+    // BC_RANDK
+    uint32_t* r_keys;       // [T * 4] Feistel round keys
+    uint32_t* r_tmp;        // [sum k] generated indices
+    uint32_t* r_ccount;     // [C] indices per chunk          
+    uint64_t* r_coff;       // [C + 1] payload position of each chunk, then
+                            // [ceil(C / 4096)] scan block sums
+    unsigned long long* r_cursor;  // [C] scatter cursors
+};
+
+// Byte offsets of every region for a call shape; `total` is the workspace
+// size.  Regions a kind does not use have size 0.
+struct WsPlan {
+    size_t flags, s_cnt, s_ready, s_val, s_partial;
+    size_t t_hist, t_thr, t_prefix, t_krem, t_fb, t_cand, t_ccount, t_gt, t_eq, t_off, t_eqb;
+    size_t r_keys, r_tmp, r_ccount, r_coff, r_cursor;
+    size_t total;
+};
+
+WsPlan plan_workspace(int kind, int T, uint64_t chunks, uint64_t sum_k);
+Ws carve_workspace(void* base, const WsPlan& p);
+
+struct DevInfo {
+    int cus;
+    int sign_coop_blocks_per_cu;
+    bool coop_ok;
+};
+hipError_t device_info(int dev, DevInfo* out);
+
+// ------------------------------------------------------------- launchers
+// d: device TDesc[T]; C: total chunks.  Return the first HIP error.
+hipError_t launch_sign_compress(const TDesc* d, int T, uint32_t C, uint32_t max_chunks,
+                                bool any_f16, bool any_f32, uint32_t* bits, float* scale,
+                                const Ws& ws, const DevInfo& di, hipStream_t s);
+hipError_t launch_topk(int kind, double ratio, uint64_t seed, const TDesc* d, int T, uint32_t C,
+                       bool any_f16, bool any_f32, uint32_t* idx, float* val, const Ws& ws,
+                       hipStream_t s);
+hipError_t launch_randk(uint64_t seed, const TDesc* d, int T, uint32_t C, uint64_t sum_k,
+                        bool any_f16, bool any_f32, uint32_t* idx, float* val, const Ws& ws,
+                        hipStream_t s);
+hipError_t launch_residual_update(int kind, const TDesc* d, int T, uint32_t C, bool any_f16,
+                                  bool any_f32, const uint32_t* idx, const float* val,
+                                  const uint32_t* bits, const float* scale, hipStream_t s);
+hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t units, const WDesc* w, int W,
+                                   float alpha, hipStream_t s);
+hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t units, const WDesc* w, int W,
+                                 float alpha, hipStream_t s);
+
+// Work-unit sizes of the aggregate kernels (elements per unit).
+constexpr uint32_t kSparseTile = 2048;   // one wave's LDS tile
+constexpr uint32_t kSignAggUnit = 512;   // one wave: 8 elements per lane
+
+}  // namespace bc

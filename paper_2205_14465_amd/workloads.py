@@ -202,3 +202,27 @@ def sign_payload(wl: Workload, w: int, word_counts, offs):
         scale[t] = np.float32(sigma_of(wl, t) * math.sqrt(2.0 / math.pi)
                               * (1.0 + 0.05 * rng.standard_normal()))
     return bits, scale
+
+
+# ------------------------------------------------- generic test inputs
+
+def random_sparse_lists(rng: np.random.Generator, ns, counts, sigma=1.0):
+    """One worker's payload for arbitrary tensor sizes: counts[t] distinct
+    ascending indices in [0, ns[t]) and N(0, sigma^2) values, concatenated."""
+    idx = [np.sort(rng.choice(int(n), size=int(k), replace=False)).astype(np.uint32) if k else
+           np.zeros(0, np.uint32) for n, k in zip(ns, counts)]
+    val = [(rng.standard_normal(int(k)) * sigma).astype(np.float32) for k in counts]
+    return idx, val
+
+
+def random_sign_words(rng: np.random.Generator, ns, word_counts):
+    """One worker's sign words for arbitrary tensor sizes (bits past each
+    tensor's end cleared), one list entry per tensor."""
+    out = []
+    for n, nw in zip(ns, word_counts):
+        w = rng.integers(0, 1 << 32, size=int(nw), dtype=np.uint64).astype(np.uint32)
+        tail = int(n) - 32 * (int(nw) - 1) if nw else 0
+        if nw and tail < 32:
+            w[-1] &= np.uint32((1 << tail) - 1)
+        out.append(w)
+    return out

@@ -1,0 +1,120 @@
+"""CPU-only checks of the C ABI: the library loads, exports every function
+include/bytecomp.h declares, and rejects bad arguments with the documented
+status before touching the device."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2205_14465_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bytecomp.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(bytecomp_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_api():
+    names = declared_functions()
+    for must in ("bytecomp_compress", "bytecomp_decompress_aggregate", "bytecomp_residual_update",
+                 "bytecomp_layout", "bytecomp_workspace_size"):
+        assert must in names
+
+
+def test_every_declared_symbol_is_exported():
+    L = B.lib()
+    for name in declared_functions():
+        assert hasattr(L, name), name
+
+
+def test_status_strings():
+    L = B.lib()
+    for code in range(0, -11, -1):
+        assert L.bytecomp_strerror(code)
+    assert L.bytecomp_strerror(-999) == b"unknown status"
+
+
+def test_layout_matches_k_rule_and_word_count():
+    import oracle as O
+    ns = [0, 1, 31, 32, 33, 1 << 20, 80411200, 768]
+    for kind in ("topk", "topk_sampled", "randk"):
+        for ratio in (0.01, 0.5, 1.0, 0.000001):
+            off = B.bytecomp_layout(kind, ratio, ns)
+            assert np.array_equal(np.array(off), O.sparse_offsets(ns, ratio))
+    assert np.array_equal(np.array(B.bytecomp_layout("sign", 0.0, ns)), O.word_offsets(ns))
+
+
+def _status(fn):
+    with pytest.raises(B.BytecompError) as ei:
+        fn()
+    return ei.value.code
+
+
+def test_argument_errors():
+    L = B.lib()
+    assert _status(lambda: B.bytecomp_layout(7, 0.01, [4])) == -2
+    assert _status(lambda: B.bytecomp_layout("topk", 0.0, [4])) == -4
+    assert _status(lambda: B.bytecomp_layout("topk", 1.5, [4])) == -4
+    assert _status(lambda: B.bytecomp_layout("topk", 1e-8, [4])) == -4
+    assert _status(lambda: B.bytecomp_layout("topk", float("nan"), [4])) == -4
+    assert B.bytecomp_layout("sign", 0.0, [4]) == [0, 1]  # ratio unused by sign
+    assert _status(lambda: B.bytecomp_layout("topk", 0.01, [1 << 32])) == -5
+    assert _status(lambda: B.bytecomp_workspace_size("topk", 0.01, [4], 0)) == -6
+    assert _status(lambda: B.bytecomp_workspace_size("topk", 0.01, [4], 5000)) == -6
+    sz = ctypes.c_size_t(0)
+    assert L.bytecomp_workspace_size(0, 0.01, None, 1, 1, ctypes.byref(sz)) == -1
+    # compress: argument errors come back before any device work
+    t = (B.bc_tensor * 1)()
+    t[0].grad = 0x1000
+    t[0].residual = 0x2000
+    t[0].n = 100
+    t[0].dtype = 0
+    pay = B.bc_payload(idx=0x3000, val=0x4000)
+    ws = ctypes.c_void_p(0x5000)
+    assert L.bytecomp_compress(9, 0.01, 0, t, 1, pay, ws, 1 << 20, None) == -2
+    assert L.bytecomp_compress(0, 2.0, 0, t, 1, pay, ws, 1 << 20, None) == -4
+    assert L.bytecomp_compress(0, 0.01, 0, t, -1, pay, ws, 1 << 20, None) == -6
+    assert L.bytecomp_compress(0, 0.01, 0, t, 0, pay, ws, 1 << 20, None) == 0  # T = 0: no-op
+    assert L.bytecomp_compress(0, 0.01, 0, None, 1, pay, ws, 1 << 20, None) == -1
+    assert L.bytecomp_compress(0, 0.01, 0, t, 1, B.bc_payload(), ws, 1 << 20, None) == -1
+    assert L.bytecomp_compress(3, 0.01, 0, t, 1, pay, ws, 1 << 20, None) == -1  # sign needs bits
+    assert L.bytecomp_compress(0, 0.01, 0, t, 1, pay, None, 1 << 20, None) == -7
+    assert L.bytecomp_compress(0, 0.01, 0, t, 1, pay, ws, 16, None) == -7
+    t[0].dtype = 5
+    assert L.bytecomp_compress(0, 0.01, 0, t, 1, pay, ws, 1 << 30, None) == -3
+    t[0].dtype = 0
+    t[0].grad = 0x1004
+    assert L.bytecomp_compress(0, 0.01, 0, t, 1, pay, ws, 1 << 30, None) == -9
+    t[0].grad = 0x1000
+    t[0].n = 1 << 32
+    assert L.bytecomp_compress(0, 0.01, 0, t, 1, pay, ws, 1 << 30, None) == -5
+    t[0].n = 100
+    t[0].grad = None
+    assert L.bytecomp_compress(0, 0.01, 0, t, 1, pay, ws, 1 << 30, None) == -1
+    # aggregate
+    n = (ctypes.c_uint64 * 1)(100)
+    outs = (ctypes.c_void_p * 1)(0x6000)
+    ins = (B.bc_payload * 1)(pay)
+    assert L.bytecomp_decompress_aggregate(0, 0.01, ins, 0, n, 1, outs, 1.0, ws, 1 << 20, None) == -6
+    assert L.bytecomp_decompress_aggregate(0, 0.01, None, 1, n, 1, outs, 1.0, ws, 1 << 20, None) == -1
+    assert L.bytecomp_decompress_aggregate(3, 0.01, ins, 1, n, 1, outs, 1.0, ws, 1 << 20, None) == -1
+    bad = (ctypes.c_void_p * 1)(0x6004)
+    assert L.bytecomp_decompress_aggregate(0, 0.01, ins, 1, n, 1, bad, 1.0, ws, 1 << 20, None) == -9
+    assert L.bytecomp_decompress_aggregate(0, 0.01, ins, 1, n, 1, outs, 1.0, ws, 8, None) == -7
+    # residual update requires a residual
+    t[0].grad = 0x1000
+    t[0].residual = None
+    assert L.bytecomp_residual_update(0, 0.01, t, 1, pay, None) == -1
+
+
+def test_workspace_size_grows_with_inputs():
+    a = B.bytecomp_workspace_size("topk_sampled", 0.01, [1 << 20], 1)
+    b = B.bytecomp_workspace_size("topk_sampled", 0.01, [1 << 21], 1)
+    assert b > a >= 8 * (1 << 20)
+    assert B.bytecomp_workspace_size("sign", 0.01, [], 64) == 256

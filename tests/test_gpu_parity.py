@@ -1,0 +1,238 @@
+"""GPU parity: the HIP library (through its C ABI) against the CPU oracle,
+element by element, on seeded inputs that span several chunks and ragged
+tails, plus the edge cases (single elements, empty tensors, ties, signed
+zeros, fp16 subnormals, error feedback off, the sampled path's fallback).
+
+Bars: indices, packed sign bits, selected values, sparse residuals and both
+aggregates bit-exact; sign scales within 1e-6 relative (fp32 gradients) or
+1e-3 (fp16 gradients); sign residuals bit-exact where the scales agree,
+else within the same relative bound of |v| + s.
+"""
+import numpy as np
+import pytest
+
+import oracle as O
+from tests.helpers import (assert_resid_equal, assert_sign_close, assert_sparse_equal, bits,
+                           gpu_aggregate, gpu_compress)
+from paper_2205_14465_amd import workloads as WL
+
+pytestmark = pytest.mark.gpu
+
+RAGGED = [1, 2, 31, 32, 33, 63, 64, 65, 1000, 4095, 4096, 4097, 8191, 3 * 4096 + 17, 65536, 65537,
+          100003, 300001]
+SEED = 14465
+
+
+def make_set(ns, rng, dtype=np.float32, sigma=0.01, mode="normal"):
+    grads, resids = [], []
+    for n in ns:
+        if mode == "ties":
+            levels = np.array([-4, -3, -2, -1, -0.5, -0.25, 0, -0.0, 0.25, 0.5, 1, 2, 3, 4, 5, -5])
+            g = (levels[rng.integers(0, 16, n)] * sigma).astype(dtype)
+            e = np.zeros(n, np.float32)
+        else:
+            g = (rng.standard_normal(n) * sigma).astype(dtype)
+            e = (rng.standard_normal(n) * sigma * 0.1).astype(np.float32)
+        if n >= 4:
+            g[:2] = np.array([0.0, -0.0], dtype)
+            e[:2] = np.array([-0.0, -0.0], np.float32)
+        grads.append(g)
+        resids.append(e)
+    return grads, resids
+
+
+# ------------------------------------------------------------- compression
+
+@pytest.mark.parametrize("kind", ["topk", "topk_sampled", "randk"])
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_sparse_compress_ragged(kind, dtype):
+    rng = np.random.default_rng(100 + len(kind))
+    grads, resids = make_set(RAGGED, rng, dtype)
+    got, got_e = gpu_compress(kind, 0.01, SEED, grads, resids)
+    want, want_e = O.compress_set(kind, 0.01, SEED, grads, resids)
+    assert_sparse_equal(got, want, RAGGED)
+    assert_resid_equal(got_e, want_e)
+
+
+@pytest.mark.parametrize("kind", ["topk", "topk_sampled", "randk"])
+@pytest.mark.parametrize("ratio", [0.001, 0.05, 0.3, 1.0])
+def test_sparse_compress_ratios(kind, ratio):
+    rng = np.random.default_rng(7)
+    ns = [5, 4097, 70001, 131072]
+    grads, resids = make_set(ns, rng)
+    got, got_e = gpu_compress(kind, ratio, SEED + 1, grads, resids)
+    want, want_e = O.compress_set(kind, ratio, SEED + 1, grads, resids)
+    assert_sparse_equal(got, want, ns)
+    assert_resid_equal(got_e, want_e)
+
+
+@pytest.mark.parametrize("kind", ["topk", "topk_sampled"])
+def test_topk_tie_heavy(kind):
+    rng = np.random.default_rng(9)
+    ns = [100, 4096 * 5 + 3, 200000]
+    grads, resids = make_set(ns, rng, mode="ties")
+    for ratio in (0.01, 0.2, 0.5):
+        got, got_e = gpu_compress(kind, ratio, SEED, grads, resids)
+        want, want_e = O.compress_set(kind, ratio, SEED, grads, resids)
+        assert_sparse_equal(got, want, ns)
+        assert_resid_equal(got_e, want_e)
+
+
+@pytest.mark.parametrize("kind", ["topk", "topk_sampled", "randk", "sign"])
+def test_error_feedback_off(kind):
+    rng = np.random.default_rng(11)
+    ns = [3, 4096, 70000]
+    grads, _ = make_set(ns, rng)
+    got, got_e = gpu_compress(kind, 0.01, SEED, grads, None)
+    want, want_e = O.compress_set(kind, 0.01, SEED, grads, None)
+    assert got_e is None
+    if kind == "sign":
+        assert_sign_close(got, want, grads, None, None, None)
+    else:
+        assert_sparse_equal(got, want, ns)
+
+
+def test_sampled_fallback_path_matches_exact():
+    # ratio 1 (and 0.95) on tensors above the all-candidates size forces the
+    # candidate set from the sample to fall short of k: exact fallback
+    rng = np.random.default_rng(13)
+    ns = [70000, 140001]
+    grads, resids = make_set(ns, rng)
+    for ratio in (1.0, 0.95):
+        got, got_e = gpu_compress("topk_sampled", ratio, SEED, grads, resids)
+        want, want_e = O.compress_set("topk", ratio, SEED, grads, resids)
+        assert_sparse_equal(got, want, ns)
+        assert_resid_equal(got_e, want_e)
+
+
+def test_randk_tensor_id_keys_the_stream():
+    rng = np.random.default_rng(15)
+    ns = [50000, 50000]
+    grads, resids = make_set(ns, rng)
+    ids = [7, 123456]
+    got, _ = gpu_compress("randk", 0.01, 99, grads, resids, tensor_ids=ids)
+    for t in range(2):
+        i, v, _ = O.compress_randk(grads[t], resids[t], 0.01, 99, ids[t])
+        assert np.array_equal(got["idx"][got["off"][t]:got["off"][t + 1]], i)
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_sign_compress_ragged(dtype):
+    rng = np.random.default_rng(17)
+    grads, resids = make_set(RAGGED + [0, 5], rng, dtype, sigma=1e-3)
+    got, got_e = gpu_compress("sign", 0.01, 0, grads, resids)
+    want, want_e = O.compress_set("sign", 0.01, 0, grads, resids)
+    assert_sign_close(got, want, grads, resids, got_e, want_e)
+
+
+def test_sign_fp16_subnormals_exact():
+    # every fp16 subnormal and a spread of normals: widening must be exact
+    h = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    g = h.view(np.float16)
+    g = g[np.isfinite(g)].copy()
+    e = np.zeros(g.size, np.float32)
+    got, got_e = gpu_compress("sign", 0.01, 0, [g], [e])
+    want, want_e = O.compress_set("sign", 0.01, 0, [g], [e])
+    assert_sign_close(got, want, [g], [e], got_e, want_e)
+    got, got_e = gpu_compress("topk", 0.3, 0, [g], [e])
+    want, want_e = O.compress_set("topk", 0.3, 0, [g], [e])
+    assert_sparse_equal(got, want, [g.size])
+    assert_resid_equal(got_e, want_e)
+
+
+def test_compress_is_deterministic():
+    rng = np.random.default_rng(19)
+    ns = [4096 * 300 + 5, 77]
+    grads, resids = make_set(ns, rng)
+    for kind in ("sign", "topk_sampled", "randk"):
+        a, ae = gpu_compress(kind, 0.01, SEED, grads, resids)
+        b, be = gpu_compress(kind, 0.01, SEED, grads, resids)
+        for key in a:
+            assert np.array_equal(np.asarray(a[key]).view(np.uint8), np.asarray(b[key]).view(np.uint8)), (kind, key)
+        assert_resid_equal(ae, be)
+
+
+# ------------------------------------------------------------- aggregation
+
+@pytest.mark.parametrize("W", [1, 2, 8, 64])
+def test_sparse_aggregate_ragged(W):
+    rng = np.random.default_rng(21 + W)
+    ns = [1, 31, 2048, 2049, 4096 * 3 + 5, 100000, 0, 7]
+    counts = [O.k_for(n, 0.05) for n in ns]
+    payloads = []
+    for w in range(W):
+        idx, val = WL.random_sparse_lists(rng, ns, counts)
+        payloads.append({"idx": np.concatenate(idx), "val": np.concatenate(val),
+                         "off": O.sparse_offsets(ns, 0.05)})
+    alpha = 1.0 / W
+    got = gpu_aggregate("topk", 0.05, ns, payloads, alpha)
+    want = O.aggregate_set("topk", ns, payloads, alpha)
+    for t in range(len(ns)):
+        assert np.array_equal(bits(got[t]), bits(want[t])), t
+
+
+def test_sparse_aggregate_dense_overlap():
+    # every worker sends every index (ratio 1): maximal overlap, long runs
+    rng = np.random.default_rng(23)
+    ns = [5000, 70001]
+    W = 5
+    payloads = []
+    for w in range(W):
+        idx = [np.arange(n, dtype=np.uint32) for n in ns]
+        val = [(rng.standard_normal(n) * 10.0 ** rng.integers(-3, 3)).astype(np.float32) for n in ns]
+        payloads.append({"idx": np.concatenate(idx), "val": np.concatenate(val),
+                         "off": O.sparse_offsets(ns, 1.0)})
+    got = gpu_aggregate("randk", 1.0, ns, payloads, 1.0)
+    want = O.aggregate_set("randk", ns, payloads, 1.0)
+    for t in range(len(ns)):
+        assert np.array_equal(bits(got[t]), bits(want[t])), t
+
+
+@pytest.mark.parametrize("W", [1, 3, 32, 64])
+def test_sign_aggregate_ragged(W):
+    rng = np.random.default_rng(31 + W)
+    ns = [1, 31, 32, 33, 511, 512, 513, 4096 * 2 + 7, 100001, 0]
+    wc = [O.words_for(n) for n in ns]
+    payloads = []
+    for w in range(W):
+        words = WL.random_sign_words(rng, ns, wc)
+        payloads.append({"bits": np.concatenate(words),
+                         "scale": (np.abs(rng.standard_normal(len(ns))) * 1e-3).astype(np.float32),
+                         "off": O.word_offsets(ns)})
+    got = gpu_aggregate("sign", 0.01, ns, payloads, 1.0 / W)
+    want = O.aggregate_set("sign", ns, payloads, 1.0 / W)
+    for t in range(len(ns)):
+        assert np.array_equal(bits(got[t]), bits(want[t])), t
+
+
+# ---------------------------------------------------- residual update (API)
+
+@pytest.mark.parametrize("kind", ["topk", "randk", "sign"])
+def test_residual_update_matches_fused(kind):
+    import torch
+    from paper_2205_14465_amd import binding as B
+    from tests.helpers import torch_dev
+    rng = np.random.default_rng(41)
+    ns = [33, 4096 * 2 + 9, 70000]
+    grads, resids = make_set(ns, rng)
+    fused, fused_e = gpu_compress(kind, 0.01, SEED, grads, resids)
+    v = [g + e for g, e in zip(grads, resids)]
+    own, _ = gpu_compress(kind, 0.01, SEED, v, None)
+    dg = [torch_dev(g) for g in grads]
+    de = [torch_dev(e) for e in resids]
+    if kind == "sign":
+        dp = {"bits": torch_dev(own["bits"].view(np.int32)), "scale": torch_dev(own["scale"])}
+    else:
+        dp = {"idx": torch_dev(own["idx"].view(np.int32)), "val": torch_dev(own["val"])}
+    B.bytecomp_residual_update(kind, 0.01, dg, de, dp)
+    torch.cuda.synchronize()
+    split_e = [e.cpu().numpy() for e in de]
+    assert_resid_equal(split_e, fused_e)
+    # and against the oracle's residual update
+    for t in range(len(ns)):
+        sl = slice(own["off"][t], own["off"][t + 1])
+        if kind == "sign":
+            want = O.residual_update_sign(grads[t], resids[t], own["bits"][sl], own["scale"][t])
+        else:
+            want = O.residual_update_sparse(grads[t], resids[t], own["idx"][sl], own["val"][sl])
+        assert np.array_equal(bits(split_e[t]), bits(want)), t

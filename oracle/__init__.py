@@ -56,6 +56,14 @@ def lib():
         L.bco_aggregate_sparse.argtypes = [_int, _u64, _vp, _vp, _vp, _flt, _vp]
         L.bco_aggregate_sign.restype = _int
         L.bco_aggregate_sign.argtypes = [_int, _u64, _vp, _vp, _flt, _vp]
+        L.bco_aggregate_sign_ordered.restype = _int
+        L.bco_aggregate_sign_ordered.argtypes = [_int, _u64, _vp, _vp, _flt, _vp]
+        L.bco_sign_span_limit.restype = _int
+        L.bco_sign_span_limit.argtypes = [_int]
+        L.bco_sign_exact_applies.restype = _int
+        L.bco_sign_exact_applies.argtypes = [_int, _vp]
+        L.bco_exact_sum_f32.restype = _flt
+        L.bco_exact_sum_f32.argtypes = [_vp, _u64]
         L.bco_philox4x64_10.restype = None
         L.bco_philox4x64_10.argtypes = [_vp, _vp, _vp]
         L.bco_feistel_half_bits.restype = _u32
@@ -212,15 +220,30 @@ def aggregate_sparse(n, idx_list, val_list, alpha=1.0):
     return out
 
 
-def aggregate_sign(n, words_list, scales, alpha=1.0):
+def aggregate_sign(n, words_list, scales, alpha=1.0, ordered=False):
     W = len(words_list)
     words_list = [np.ascontiguousarray(a, np.uint32) for a in words_list]
     wp = (ctypes.c_void_p * max(W, 1))(*[a.ctypes.data for a in words_list])
     sc = np.ascontiguousarray(np.asarray(scales, dtype=np.float32).reshape(-1))
     out = np.empty(n, np.float32)
-    rc = lib().bco_aggregate_sign(W, n, ctypes.cast(wp, _vp), _p(sc), float(alpha), _p(out))
+    fn = lib().bco_aggregate_sign_ordered if ordered else lib().bco_aggregate_sign
+    rc = fn(W, n, ctypes.cast(wp, _vp), _p(sc), float(alpha), _p(out))
     assert rc == 0, rc
     return out
+
+
+def sign_span_limit(W):
+    return int(lib().bco_sign_span_limit(int(W)))
+
+
+def sign_exact_applies(scales):
+    sc = np.ascontiguousarray(np.asarray(scales, dtype=np.float32).reshape(-1))
+    return bool(lib().bco_sign_exact_applies(sc.size, _p(sc)))
+
+
+def exact_sum_f32(x):
+    x = np.ascontiguousarray(x, np.float32)
+    return np.float32(lib().bco_exact_sum_f32(_p(x), x.size))
 
 
 def philox4x64_10(ctr, key):

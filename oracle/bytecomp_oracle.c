@@ -25,7 +25,10 @@
  *
  * Arithmetic: fp32 where the gradients are fp32, IEEE round-to-nearest-even,
  * compiled with -O2 -ffp-contract=off (no FMA contraction, no fast-math).
- * The mean-|v| scale is accumulated in fp64 in index order.
+ * The mean-|v| scale is accumulated in fp64 in index order.  The sparse
+ * aggregate adds the workers' values in worker order in fp32; the sign
+ * aggregate is the exact sum rounded once (a 320-bit fixed-point sum),
+ * with the worker-ordered fp32 sum for scale sets outside fp64 exactness.
  *
  * Parity status of each function is pinned by tests under tests/ against
  * brute force, closed forms, hand-worked examples and library routines
@@ -456,9 +459,9 @@ int bco_residual_update_sign(const void* g, int dtype, float* e_inout, uint64_t 
 /* tensors and aggregates them).                                        */
 /*                                                                      */
 /* Reading: aggregation is a sum scaled by alpha (alpha = 1 for a sum,  */
-/* 1/W for a mean); each output element starts at +0.0 and receives the */
-/* workers' decoded contributions in ascending worker order, one fp32   */
-/* addition each; the result is alpha times that sum, rounded to fp32.  */
+/* 1/W for a mean).  Sparse: each output element starts at +0.0 and     */
+/* receives the workers' values in ascending worker order, one fp32     */
+/* addition each, then alpha times that sum.  Sign: see below.          */
 /* ------------------------------------------------------------------ */
 
 int bco_aggregate_sparse(int W, uint64_t n, const uint32_t* const* idx_w,
@@ -480,8 +483,10 @@ int bco_aggregate_sparse(int W, uint64_t n, const uint32_t* const* idx_w,
     return 0;
 }
 
-int bco_aggregate_sign(int W, uint64_t n, const uint32_t* const* words_w,
-                       const float* scale_w, float alpha, float* out)
+/* Sign aggregate, worker-ordered form: each output starts at +0.0 and adds
+ * the W decoded values in ascending worker order, one fp32 addition each. */
+int bco_aggregate_sign_ordered(int W, uint64_t n, const uint32_t* const* words_w,
+                               const float* scale_w, float alpha, float* out)
 {
     for (uint64_t i = 0; i < n; ++i) {
         float acc = 0.0f;
@@ -493,6 +498,135 @@ int bco_aggregate_sign(int W, uint64_t n, const uint32_t* const* words_w,
         out[i] = alpha * acc;
     }
     return 0;
+}
+
+/* Exact sum of fp32 terms in a 320-bit two's-complement fixed-point integer
+ * whose unit is 2^-149 (the smallest fp32 subnormal), then one
+ * round-to-nearest-even to fp32.  Finite terms only. */
+typedef struct { uint64_t l[5]; } acc320_t;
+
+static void acc_add_shifted(acc320_t* a, uint64_t m, int pos, int negative)
+{
+    /* t = m << pos as a 320-bit value */
+    uint64_t t[5] = { 0, 0, 0, 0, 0 };
+    int limb = pos / 64, sh = pos % 64;
+    t[limb] = m << sh;
+    if (sh && limb + 1 < 5) t[limb + 1] = m >> (64 - sh);
+    if (negative) { /* two's complement of t */
+        unsigned __int128 c = 1;
+        for (int q = 0; q < 5; ++q) {
+            c += (unsigned __int128)(~t[q]);
+            t[q] = (uint64_t)c;
+            c >>= 64;
+        }
+    }
+    unsigned __int128 c = 0;
+    for (int q = 0; q < 5; ++q) {
+        c += (unsigned __int128)a->l[q] + t[q];
+        a->l[q] = (uint64_t)c;
+        c >>= 64;
+    }
+}
+
+static void acc_add_f32(acc320_t* a, float x)
+{
+    uint32_t u = f2u(x);
+    uint32_t e = (u >> 23) & 255u, f = u & 0x7FFFFFu;
+    if (e == 0 && f == 0) return;
+    uint64_t m = e ? (uint64_t)(f | 0x800000u) : (uint64_t)f;
+    int pos = e ? (int)e - 1 : 0; /* value = m * 2^(pos - 149) */
+    acc_add_shifted(a, m, pos, (int)(u >> 31));
+}
+
+static float acc_round_f32(const acc320_t* a)
+{
+    uint64_t v[5];
+    int neg = (int)(a->l[4] >> 63);
+    memcpy(v, a->l, sizeof v);
+    if (neg) {
+        unsigned __int128 c = 1;
+        for (int q = 0; q < 5; ++q) {
+            c += (unsigned __int128)(~v[q]);
+            v[q] = (uint64_t)c;
+            c >>= 64;
+        }
+    }
+    int h = -1;
+    for (int q = 4; q >= 0 && h < 0; --q)
+        if (v[q]) h = q * 64 + 63 - __builtin_clzll(v[q]);
+    if (h < 0) return 0.0f; /* exact zero rounds to +0.0 */
+    float mag;
+    if (h < 24) {
+        mag = ldexpf((float)v[0], -149); /* fewer than 25 bits: exact */
+    } else {
+        /* 24 leading bits, the round bit below them, and a sticky bit */
+        uint64_t mant = 0;
+        for (int b = h; b > h - 24; --b) mant = (mant << 1) | ((v[b / 64] >> (b % 64)) & 1u);
+        int rb = (int)((v[(h - 24) / 64] >> ((h - 24) % 64)) & 1u);
+        int sticky = 0;
+        for (int b = h - 25; b >= 0 && !sticky; --b) sticky = (int)((v[b / 64] >> (b % 64)) & 1u);
+        if (rb && (sticky || (mant & 1u))) ++mant;
+        mag = ldexpf((float)mant, h - 23 - 149);
+    }
+    return neg ? -mag : mag;
+}
+
+/* Largest binade distance between the scales for which an fp64 sum of the
+ * W decoded values is exact: 24 + span + ceil(log2 W) <= 53. */
+int bco_sign_span_limit(int W)
+{
+    int lg = 0;
+    while ((1 << lg) < W) ++lg;
+    return 29 - lg;
+}
+
+/* 1 when the exact-sum form applies: every scale finite and zero or normal,
+ * and the nonzero scales' binary exponents within bco_sign_span_limit(W). */
+int bco_sign_exact_applies(int W, const float* scale_w)
+{
+    int emin = 1000, emax = -1000;
+    for (int w = 0; w < W; ++w) {
+        uint32_t u = f2u(scale_w[w]);
+        uint32_t e = (u >> 23) & 255u;
+        if (e == 255u) return 0;
+        if (e == 0u) {
+            if (u & 0x7FFFFFu) return 0; /* subnormal */
+            continue;
+        }
+        if ((int)e < emin) emin = (int)e;
+        if ((int)e > emax) emax = (int)e;
+    }
+    return emax < emin || emax - emin <= bco_sign_span_limit(W);
+}
+
+/* Sign aggregate (reading): the exact sum of the W decoded values, rounded
+ * once to fp32, times alpha in fp32.  For scale sets outside the exact-sum
+ * form's range (non-finite or subnormal scales, or exponents spread wider
+ * than bco_sign_span_limit) the worker-ordered fp32 sum is used instead. */
+int bco_aggregate_sign(int W, uint64_t n, const uint32_t* const* words_w,
+                       const float* scale_w, float alpha, float* out)
+{
+    if (!bco_sign_exact_applies(W, scale_w))
+        return bco_aggregate_sign_ordered(W, n, words_w, scale_w, alpha, out);
+    for (uint64_t i = 0; i < n; ++i) {
+        acc320_t a;
+        memset(&a, 0, sizeof a);
+        for (int w = 0; w < W; ++w) {
+            uint32_t bit = (words_w[w][i / 32] >> (i % 32)) & 1u;
+            acc_add_f32(&a, bit ? -scale_w[w] : scale_w[w]);
+        }
+        out[i] = alpha * acc_round_f32(&a);
+    }
+    return 0;
+}
+
+/* Exact sum of m fp32 values rounded once to fp32 (exported for pins). */
+float bco_exact_sum_f32(const float* x, uint64_t m)
+{
+    acc320_t a;
+    memset(&a, 0, sizeof a);
+    for (uint64_t i = 0; i < m; ++i) acc_add_f32(&a, x[i]);
+    return acc_round_f32(&a);
 }
 
 /* Bit pattern helpers exported for tests. */

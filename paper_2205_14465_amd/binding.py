@@ -198,6 +198,50 @@ def bytecomp_device_status(ws, stream=None):
     return int(f.value)
 
 
+# ---------------------------------------------------------- prepared calls
+# For tensor lists that stay the same across iterations (a model's
+# gradients), the ctypes argument arrays are built once; a call then costs
+# one foreign-function call.
+
+class CompressCall:
+    def __init__(self, kind, ratio, grads, resids, out, ws, stream=None, tensor_ids=None):
+        self.kind = _kind(kind)
+        self.ratio = float(ratio)
+        self.T = len(grads)
+        self.arr = _tensor_list(grads, resids, tensor_ids)
+        self.out = _payload(out)
+        self.ws = _ptr(ws)
+        self.ws_bytes = ws.numel() * ws.element_size()
+        self.stream = _stream_handle(stream)
+        self._keep = (grads, resids, out, ws)
+
+    def __call__(self, seed):
+        _check("bytecomp_compress",
+               lib().bytecomp_compress(self.kind, self.ratio, int(seed) & (2**64 - 1), self.arr, self.T,
+                                       self.out, self.ws, self.ws_bytes, self.stream))
+
+
+class AggregateCall:
+    def __init__(self, kind, ratio, payloads, ns, outs, alpha, ws, stream=None):
+        self.kind = _kind(kind)
+        self.ratio = float(ratio)
+        self.W = len(payloads)
+        self.pa = (bc_payload * max(self.W, 1))(*[_payload(p) for p in payloads])
+        self.T = len(ns)
+        self.ns = _u64_array(ns)
+        self.op = (ctypes.c_void_p * max(self.T, 1))(*[o.data_ptr() if o.numel() else None for o in outs])
+        self.alpha = float(alpha)
+        self.ws = _ptr(ws)
+        self.ws_bytes = ws.numel() * ws.element_size()
+        self.stream = _stream_handle(stream)
+        self._keep = (payloads, outs, ws)
+
+    def __call__(self):
+        _check("bytecomp_decompress_aggregate",
+               lib().bytecomp_decompress_aggregate(self.kind, self.ratio, self.pa, self.W, self.ns, self.T,
+                                                   self.op, self.alpha, self.ws, self.ws_bytes, self.stream))
+
+
 # ------------------------------------------------------------ allocation
 
 def alloc_payload(kind, ratio, ns, device="cuda"):

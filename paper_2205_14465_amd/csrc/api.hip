@@ -71,7 +71,10 @@ std::mutex g_mu;
 Entry g_cache[32];
 uint64_t g_tick = 0;
 
-hipError_t cache_get(const void* bytes, size_t len, hipStream_t s, Entry** out) {
+// The device copy holds the key bytes followed by `extra` bytes derived
+// from them (the chunk- or unit-to-tensor maps), built only on a miss.
+template <typename Fill>
+hipError_t cache_get(const void* bytes, size_t len, size_t extra, Fill fill, hipStream_t s, Entry** out) {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
@@ -98,13 +101,14 @@ hipError_t cache_get(const void* bytes, size_t len, hipStream_t s, Entry** out) 
         }
         if (e != hipSuccess) return e;
     }
-    if (en.device != dev || en.cap < len) {
+    const size_t total = len + extra;
+    if (en.device != dev || en.cap < total) {
         if (en.dev) (void)hipFree(en.dev);
         if (en.pinned) (void)hipHostFree(en.pinned);
         if (en.ready) (void)hipEventDestroy(en.ready);
         if (en.used) (void)hipEventDestroy(en.used);
         en = Entry();
-        size_t cap = len < 4096 ? 4096 : len;
+        size_t cap = total < 4096 ? 4096 : total;
         if ((e = hipMalloc(&en.dev, cap)) != hipSuccess) { en = Entry(); return e; }
         if ((e = hipHostMalloc(&en.pinned, cap, hipHostMallocDefault)) != hipSuccess) {
             (void)hipFree(en.dev);
@@ -117,8 +121,9 @@ hipError_t cache_get(const void* bytes, size_t len, hipStream_t s, Entry** out) 
         en.device = dev;
     }
     std::memcpy(en.pinned, bytes, len);
+    fill((unsigned char*)en.pinned + len);
     en.key.assign((const unsigned char*)bytes, (const unsigned char*)bytes + len);
-    e = hipMemcpyAsync(en.dev, en.pinned, len, hipMemcpyHostToDevice, s);
+    e = hipMemcpyAsync(en.dev, en.pinned, total, hipMemcpyHostToDevice, s);
     if (e == hipSuccess) e = hipEventRecord(en.ready, s);
     if (e != hipSuccess) { en.key.clear(); return e; }
     en.upload_stream = s;
@@ -158,6 +163,8 @@ hipError_t device_info(int dev, DevInfo* out) {
         e = sign_coop_occupancy(&b);
         if (e != hipSuccess) return e;
         di.sign_coop_blocks_per_cu = b > 0 ? b : 1;
+        const char* sp = std::getenv("BYTECOMP_SIGN_PATH");
+        di.sign_two_pass = sp && std::strcmp(sp, "twopass") == 0;
         g_dev[dev] = di;
         g_dev_ok[dev] = true;
     }
@@ -177,7 +184,7 @@ WsPlan plan_workspace(int kind, int T, uint64_t C, uint64_t sum_k) {
     const size_t t = (size_t)T;
     if (kind == BC_SIGN1) {
         take(p.s_cnt, t * 4);
-        take(p.s_ready, t * 4);
+        take(p.s_ready, t * 8);
         take(p.s_val, t * 4);
         take(p.s_partial, (size_t)C * 8);
     } else if (kind == BC_TOPK || kind == BC_TOPK_SAMPLED) {
@@ -294,6 +301,12 @@ int build_tdesc(int kind, uint64_t ppm, const bc_tensor* t, int T, bool need_res
     return BC_OK;
 }
 
+// chunk -> tensor map stored after the descriptor table
+void fill_chunk_map(const std::vector<TDesc>& d, uint32_t* m) {
+    for (size_t i = 0; i < d.size(); ++i)
+        for (uint32_t q = 0; q < d[i].nchunks; ++q) m[d[i].chunk0 + q] = (uint32_t)i;
+}
+
 int check_kind_ratio(int kind, double ratio, uint64_t& ppm) {
     if (kind < BC_TOPK || kind > BC_SIGN1) return BC_E_KIND;
     ppm = 1;
@@ -391,7 +404,8 @@ int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t,
     const Ws w = carve_workspace(ws, plan);
     std::lock_guard<std::mutex> lk(g_mu);
     Entry* en = nullptr;
-    hipError_t e = cache_get(d.data(), d.size() * sizeof(TDesc), s, &en);
+    hipError_t e = cache_get(d.data(), d.size() * sizeof(TDesc), (size_t)C * 4,
+                             [&](void* dst) { fill_chunk_map(d, (uint32_t*)dst); }, s, &en);
     if (e != hipSuccess) return BC_E_HIP;
     const TDesc* dd = (const TDesc*)en->dev;
     switch (kind) {
@@ -463,7 +477,13 @@ int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, 
     hipStream_t s = (hipStream_t)stream;
     std::lock_guard<std::mutex> lk(g_mu);
     Entry* en = nullptr;
-    hipError_t e = cache_get(table.data(), table.size(), s, &en);
+    hipError_t e = cache_get(table.data(), table.size(), (size_t)units * 4,
+                             [&](void* dst) {
+                                 uint32_t* m = (uint32_t*)dst;
+                                 for (int i = 0; i < T; ++i)
+                                     for (uint32_t q = 0; q < a[i].nunits; ++q) m[a[i].unit0 + q] = (uint32_t)i;
+                             },
+                             s, &en);
     if (e != hipSuccess) return BC_E_HIP;
     const ADesc* ad = (const ADesc*)en->dev;
     const WDesc* wdd = (const WDesc*)((const char*)en->dev + (size_t)T * sizeof(ADesc));
@@ -497,7 +517,8 @@ int bytecomp_residual_update(int kind, double ratio, const bc_tensor* t, int T, 
     hipStream_t s = (hipStream_t)stream;
     std::lock_guard<std::mutex> lk(g_mu);
     Entry* en = nullptr;
-    hipError_t e = cache_get(d.data(), d.size() * sizeof(TDesc), s, &en);
+    hipError_t e = cache_get(d.data(), d.size() * sizeof(TDesc), (size_t)C * 4,
+                             [&](void* dst) { fill_chunk_map(d, (uint32_t*)dst); }, s, &en);
     if (e != hipSuccess) return BC_E_HIP;
     e = launch_residual_update(kind, (const TDesc*)en->dev, T, C, a16, a32, own.idx, own.val,
                                own.bits, own.scale, s);

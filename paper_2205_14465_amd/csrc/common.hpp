@@ -65,8 +65,10 @@ __device__ __forceinline__ int find_owner(const D* __restrict__ d, int T, uint32
     return lo;
 }
 
+// The device descriptor table of a call is followed by a chunk -> tensor
+// map (one uint32 per chunk), built on the host when the table is cached.
 __device__ __forceinline__ int tensor_of_chunk(const TDesc* __restrict__ d, int T, uint32_t c) {
-    return find_owner<TDesc, &TDesc::chunk0>(d, T, c);
+    return (int)reinterpret_cast<const uint32_t*>(d + T)[c];
 }
 
 // ------------------------------------------------------------- bit helpers

@@ -16,21 +16,21 @@
 // worker's adds never collide and need no atomics).  Cursors are found by a
 // binary search only where a wave's run starts inside a tensor.
 //
-// Sign: each wave owns 512 output elements, 8 per lane.  For worker w the 16
-// words covering them are fetched with scalar loads; each 64-bit word pair
-// is a lane mask that selects -s_w or +s_w with one v_cndmask, then one
-// v_add per element and worker.
+// Sign: the exact sum of the workers' decoded values, rounded once to fp32,
+// computed with fp64 lookup tables of eight-worker partial sums (exact while
+// the scales' exponents stay within a span fp64 can hold); outside that
+// range the worker-ordered fp32 sum.
 #include "launch.hpp"
 
 namespace bc {
 
 namespace {
 
-typedef const uint32_t __attribute__((address_space(4)))* cu32p;
 typedef const float __attribute__((address_space(4)))* cf32p;
 
-__device__ __forceinline__ int unit_owner(const ADesc* __restrict__ a, int T, uint32_t u) {
-    return find_owner<ADesc, &ADesc::unit0>(a, T, u);
+// The aggregate table is [ADesc x T][WDesc x W][unit -> tensor map].
+__device__ __forceinline__ int unit_owner(const WDesc* __restrict__ wd, int W, uint32_t u) {
+    return (int)reinterpret_cast<const uint32_t*>(wd + W)[u];
 }
 
 // First position p in [0, k) with idx[p] >= x (k if none).
@@ -65,7 +65,7 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
     ADesc ad{};
     for (uint32_t u = u_beg; u < u_end; ++u) {
         if (t < 0 || u >= ad.unit0 + ad.nunits) {
-            t = unit_owner(a, T, u);
+            t = unit_owner(wd, W, u);
             ad = a[t];
             const uint32_t lo0 = (u - ad.unit0) * kSparseTile;
             for (int w = lane; w < W; w += 64)
@@ -142,46 +142,147 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
 }
 
 // ------------------------------------------------------------------- sign
+namespace {
+
+constexpr int kSignGroup = 4;  // workers whose words are in flight together (ordered form)
+
+// Ordered form: acc[q] += (bit q of word) ? -s : +s for the lane's 32
+// elements, one fp32 addition per element and worker in worker order: the
+// bit is moved to the sign position (v_lshlrev) and spliced into s (v_bfi).
+__device__ __forceinline__ void sign_word_accumulate(float (&acc)[32], uint32_t word, float s) {
+    const uint32_t su = f2u(s);
+    const uint32_t sign = 0x80000000u;
+#pragma unroll
+    for (int q = 0; q < 32; ++q) {
+        const uint32_t t = word << (31 - q);
+        uint32_t d;
+        asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(d) : "v"(sign), "v"(t), "v"(su));
+        acc[q] += u2f(d);
+    }
+}
+
+}  // namespace
+
+// Each workgroup owns 8192 output elements of one tensor: lane l the 32
+// elements of word l of the workgroup's 256-word block (one coalesced
+// 1 KiB load per worker).
+//
+// Exact form (scale exponents within span_limit binades, all finite and
+// normal or zero): every partial sum of the decoded values is exact in
+// fp64.  Workers are taken eight at a time; the 256 possible sums of a
+// group's eight +-s_w are tabulated in LDS (fp64), the eight sign bits of an
+// element form the table index, and the fp64 sum of the group entries is
+// the exact sum, rounded once to fp32 at the end.  The eight words of a
+// group are transposed into per-element bytes with shift/and-or steps that
+// each serve four elements.
+//
+// Ordered form (otherwise): worker-ordered fp32 additions.
 __global__ __launch_bounds__(kBlock) void aggregate_sign(const ADesc* __restrict__ a, int T,
                                                          uint32_t U, const WDesc* __restrict__ wd,
-                                                         int W, float alpha) {
-    const uint32_t u = blockIdx.x * 4u + (uint32_t)wave_id();
-    if (u >= U) return;
-    const int lane = lane_id();
-    const int t = unit_owner(a, T, u);
+                                                         int W, float alpha, int span_limit) {
+    __shared__ double tab[8 * 256];
+    __shared__ float sc[1024];
+    __shared__ int emin_sh, emax_sh, bad_sh;
+    const uint32_t u = blockIdx.x;
+    const int t = unit_owner(wd, W, u);
     const ADesc ad = a[t];
     const uint32_t j = u - ad.unit0;
-    const uint32_t lo = j * kSignAggUnit;
-    const uint64_t woff = ad.off + (uint64_t)j * 16u;
-    const uint32_t nwords = (ad.k - j * 16u) < 16u ? (ad.k - j * 16u) : 16u;
-    float acc[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] = 0.f;
-    for (int w = 0; w < W; ++w) {
-        const WDesc p = wd[w];
-        const float s = ((cf32p)p.b)[t];
-        uint32_t word[16];
-        const cu32p bp = (cu32p)(p.a + woff);
-        if (nwords == 16u) {
-#pragma unroll
-            for (int i = 0; i < 16; ++i) word[i] = bp[i];
-        } else {
-#pragma unroll
-            for (int i = 0; i < 16; ++i) word[i] = (uint32_t)i < nwords ? bp[i] : 0u;
-        }
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const uint64_t m = (uint64_t)word[2 * e] | ((uint64_t)word[2 * e + 1] << 32);
-            float dv;
-            asm("v_cndmask_b32_e64 %0, %1, -%1, %2" : "=v"(dv) : "v"(s), "s"(m));
-            acc[e] += dv;
+    const uint32_t wi = j * 256u + threadIdx.x;  // word of the tensor this lane owns
+    const bool has = wi < ad.k;
+    const uint64_t woff = ad.off + wi;
+    if (threadIdx.x == 0) {
+        emin_sh = 1000;
+        emax_sh = -1000;
+        bad_sh = 0;
+    }
+    __syncthreads();
+    for (int w = threadIdx.x; w < W; w += kBlock) {
+        const float sv = ((cf32p)wd[w].b)[t];
+        sc[w] = sv;
+        const uint32_t e = (f2u(sv) >> 23) & 255u;
+        if (e == 255u || (e == 0u && (f2u(sv) & 0x7FFFFFu))) atomicOr(&bad_sh, 1);
+        else if (e) {
+            atomicMin(&emin_sh, (int)e);
+            atomicMax(&emax_sh, (int)e);
         }
     }
-    float* out = ad.out + lo;
+    __syncthreads();
+    const bool exact = !bad_sh && (emax_sh < emin_sh || emax_sh - emin_sh <= span_limit);
+    const uint32_t e0 = wi * 32u;
+    float* out = ad.out + e0;
+    float res[32];
+    if (exact) {
+        double S[32];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        const uint32_t i = 64u * e + lane;
-        if (lo + i < ad.n) out[i] = alpha * acc[e];
+        for (int q = 0; q < 32; ++q) S[q] = 0.0;
+        const int G = (W + 7) / 8;
+        for (int g0 = 0; g0 < G; g0 += 8) {
+            __syncthreads();
+            for (int x = threadIdx.x; x < 8 * 256; x += kBlock) {
+                const int gi = g0 + (x >> 8), pat = x & 255;
+                double acc = 0.0;
+                if (gi < G) {
+#pragma unroll
+                    for (int jj = 0; jj < 8; ++jj) {
+                        const int w = 8 * gi + jj;
+                        const double sv = w < W ? (double)sc[w] : 0.0;
+                        acc += ((pat >> jj) & 1) ? -sv : sv;
+                    }
+                }
+                tab[x] = acc;
+            }
+            __syncthreads();
+            const int gend = (G - g0) < 8 ? (G - g0) : 8;
+            for (int gg = 0; gg < gend; ++gg) {
+                const int wbase = 8 * (g0 + gg);
+                uint32_t idx4[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) idx4[q] = 0u;
+#pragma unroll
+                for (int jj = 0; jj < 8; ++jj) {
+                    const int w = wbase + jj;
+                    const uint32_t word = (has && w < W) ? wd[w].a[woff] : 0u;
+                    const uint32_t x = word << jj;
+                    const uint32_t m = 0x01010101u << jj;
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) idx4[q] |= (x >> q) & m;
+                }
+                const double* tb = tab + gg * 256;
+#pragma unroll
+                for (int q = 0; q < 32; ++q) S[q] += tb[(idx4[q & 7] >> (8 * (q >> 3))) & 255u];
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < 32; ++q) res[q] = alpha * (float)S[q];
+    } else {
+        float acc[32];
+#pragma unroll
+        for (int q = 0; q < 32; ++q) acc[q] = 0.f;
+        for (int w0 = 0; w0 < W; w0 += kSignGroup) {
+            uint32_t word[kSignGroup];
+            float sv[kSignGroup];
+#pragma unroll
+            for (int g = 0; g < kSignGroup; ++g) {
+                const int w = w0 + g < W ? w0 + g : W - 1;
+                sv[g] = sc[w];
+                word[g] = has ? wd[w].a[woff] : 0u;
+            }
+#pragma unroll
+            for (int g = 0; g < kSignGroup; ++g)
+                if (w0 + g < W) sign_word_accumulate(acc, word[g], sv[g]);
+        }
+#pragma unroll
+        for (int q = 0; q < 32; ++q) res[q] = alpha * acc[q];
+    }
+    if (!has) return;
+    if (e0 + 32u <= ad.n) {
+#pragma unroll
+        for (int q = 0; q < 32; q += 4)
+            *reinterpret_cast<float4*>(out + q) = make_float4(res[q], res[q + 1], res[q + 2], res[q + 3]);
+    } else {
+#pragma unroll
+        for (int q = 0; q < 32; ++q)
+            if (e0 + q < ad.n) out[q] = res[q];
     }
 }
 
@@ -237,7 +338,10 @@ hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t U, const WDes
 hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t U, const WDesc* w, int W,
                                  float alpha, hipStream_t s) {
     if (U == 0) return hipSuccess;
-    hipLaunchKernelGGL(aggregate_sign, dim3((U + 3) / 4), dim3(kBlock), 0, s, a, T, U, w, W, alpha);
+    int lg = 0;
+    while ((1 << lg) < W) ++lg;
+    const int span_limit = 29 - lg;  // 24 + span + ceil(log2 W) <= 53
+    hipLaunchKernelGGL(aggregate_sign, dim3(U), dim3(kBlock), 0, s, a, T, U, w, W, alpha, span_limit);
     return hipGetLastError();
 }
 

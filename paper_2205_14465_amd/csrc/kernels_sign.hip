@@ -18,7 +18,9 @@
 // ends first, so every wait ends.  The wait is bounded anyway: after
 // ~2^22 polls it records kFlagWaitTimeout in the workspace and goes on.
 // When a tensor is larger than the grid (or cooperative launch is not
-// available) a two-pass variant reads g and e twice.
+// available, or BYTECOMP_SIGN_PATH=twopass) a two-pass variant runs
+// instead: pass 1 writes the bits, the chunk partial sums and v (into e);
+// pass 2 re-reads v and writes the residual.
 #include "launch.hpp"
 
 namespace bc {
@@ -61,6 +63,16 @@ __device__ __forceinline__ double reduce_partials(const double* p, uint32_t m, d
     return block_sum_f64(acc, sh);
 }
 
+// Same sum, reading partials that other workgroups published with
+// agent-scope atomic stores.
+__device__ __forceinline__ double reduce_partials_atomic(double* p, uint32_t m, double* sh) {
+    double acc = 0.0;
+    for (uint32_t q = threadIdx.x; q < m; q += kBlock)
+        acc += __longlong_as_double((long long)__hip_atomic_load((unsigned long long*)p + q, __ATOMIC_RELAXED,
+                                                                 __HIP_MEMORY_SCOPE_AGENT));
+    return block_sum_f64(acc, sh);
+}
+
 __device__ __forceinline__ void store_sign_residual(const TDesc& td, uint32_t j, float s,
                                                     float v[kEpt]) {
 #pragma unroll
@@ -97,25 +109,37 @@ __global__ __launch_bounds__(kBlock) void sign_compress_coop(const TDesc* __rest
             s = (float)(p / (double)td.n);
             if (threadIdx.x == 0) scale_out[t] = s;
         } else {
+            // Cross-workgroup exchange uses agent-scope atomics only (coherent
+            // across the chip's L2 caches) and no acquire/release fences, which
+            // on this GPU would write back or invalidate a whole L2.
             if (threadIdx.x == 0) {
-                ws.s_partial[c] = p;
-                const uint32_t old = atomic_add_agent(ws.s_cnt + t, 1u);
+                __hip_atomic_store((unsigned long long*)ws.s_partial + c, (unsigned long long)__double_as_longlong(p),
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                // the partial store completes before the arrival is counted
+                __builtin_amdgcn_s_waitcnt(0);
+                const uint32_t old = __hip_atomic_fetch_add(ws.s_cnt + t, 1u, __ATOMIC_RELAXED,
+                                                            __HIP_MEMORY_SCOPE_AGENT);
                 last_sh = (old == td.nchunks - 1);
             }
             __syncthreads();
             if (last_sh) {
-                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-                const double tot = reduce_partials(ws.s_partial + td.chunk0, td.nchunks, sh);
+                const double tot = reduce_partials_atomic(ws.s_partial + td.chunk0, td.nchunks, sh);
                 s = (float)(tot / (double)td.n);
                 if (threadIdx.x == 0) {
                     scale_out[t] = s;
-                    ws.s_val[t] = s;
-                    atomic_store_release(ws.s_ready + t, 1u);
+                    // scale and "published" flag travel in one 64-bit word
+                    __hip_atomic_store((unsigned long long*)ws.s_ready + t,
+                                       (1ull << 32) | (unsigned long long)f2u(s), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
                 }
             } else {
                 if (threadIdx.x == 0) {
                     uint32_t spins = 0;
-                    while (atomic_load_acquire(ws.s_ready + t) == 0u) {
+                    unsigned long long x;
+                    for (;;) {
+                        x = __hip_atomic_load((unsigned long long*)ws.s_ready + t, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT);
+                        if (x >> 32) break;
                         __builtin_amdgcn_s_sleep(2);
                         if (++spins > kSpinLimit) {
                             __hip_atomic_fetch_or(ws.flags, kFlagWaitTimeout, __ATOMIC_RELAXED,
@@ -123,7 +147,7 @@ __global__ __launch_bounds__(kBlock) void sign_compress_coop(const TDesc* __rest
                             break;
                         }
                     }
-                    s_sh = ws.s_val[t];
+                    s_sh = u2f((uint32_t)x);
                 }
                 __syncthreads();
                 s = s_sh;
@@ -146,6 +170,7 @@ __global__ __launch_bounds__(kBlock) void sign_pass1(const TDesc* __restrict__ d
     uint32_t valid;
     load_v(td, j, td.resid != nullptr, v, valid);
     store_sign_words(v, bits + td.off + (uint64_t)j * kChunkWords, chunk_words(td, j));
+    if (td.resid) store_chunk(td.resid, td.n, j, v);  // v parked in e for the second pass
     const double p = block_sum_f64(thread_abs_sum(v), sh);
     if (threadIdx.x == 0) ws.s_partial[c] = p;
 }
@@ -174,7 +199,7 @@ __global__ __launch_bounds__(kBlock) void sign_pass2(const TDesc* __restrict__ d
     const uint32_t j = c - td.chunk0;
     float v[kEpt];
     uint32_t valid;
-    load_v(td, j, true, v, valid);
+    load_stored_v(td, j, v, valid);  // e holds v after the first pass
     store_sign_residual(td, j, ws.s_val[t], v);
 }
 
@@ -184,7 +209,7 @@ __global__ void sign_prep(const TDesc* __restrict__ d, int T, float* __restrict_
     const int t = blockIdx.x * blockDim.x + threadIdx.x;
     if (t >= T) return;
     ws.s_cnt[t] = 0u;
-    ws.s_ready[t] = 0u;
+    ((unsigned long long*)ws.s_ready)[t] = 0ull;
     if (d[t].nchunks == 0) scale_out[t] = 0.f;
 }
 
@@ -226,7 +251,7 @@ hipError_t launch_sign_compress(const TDesc* d, int T, uint32_t C, uint32_t max_
     if (e != hipSuccess || C == 0) return e;
     const uint32_t cap = (uint32_t)di.cus * (uint32_t)di.sign_coop_blocks_per_cu;
     const uint32_t G = C < cap ? C : cap;
-    if (di.coop_ok && max_chunks <= G) {
+    if (di.coop_ok && max_chunks <= G && !di.sign_two_pass) {
         void* args[] = {(void*)&d, (void*)&T, (void*)&C, (void*)&bits, (void*)&scale, (void*)&ws};
         return hipLaunchCooperativeKernel((const void*)sign_compress_coop, dim3(G), dim3(kBlock), args,
                                           0, s);

@@ -84,28 +84,47 @@ __global__ __launch_bounds__(kBlock) void topk_hist_pass(const TDesc* __restrict
 
 // Seeded sample: each 4096-element chunk of a tensor larger than
 // kAllCandidatesBelow contributes one run of 64 consecutive elements with
-// probability 0.64 (an expected 1% of the tensor); one wave per chunk.
+// probability 0.64 (an expected 1% of the tensor).  A workgroup covers 16
+// consecutive chunks, one wave per chunk in turn; when they all belong to
+// one tensor (the usual case) the keys are binned in LDS first so the
+// global histogram sees one atomic per non-empty bin.
+constexpr uint32_t kSampleChunksPerBlock = 16;
+
 __global__ __launch_bounds__(kBlock) void topk_sample_hist(const TDesc* __restrict__ d, int T,
                                                            uint32_t C, uint64_t seed, Ws ws) {
-    const uint32_t c = blockIdx.x * 4u + (threadIdx.x >> 6);
-    if (c >= C) return;
-    const int t = tensor_of_chunk(d, T, c);
-    const TDesc td = d[t];
-    if (td.n < kAllCandidatesBelow) return;
-    const uint32_t j = c - td.chunk0;
-    U64x4 ctr = {{(uint64_t)td.tid, (uint64_t)j, 0, 0}};
-    const U64x4 r = philox4x64_10(ctr, seed, kStreamSample);
-    const uint32_t u = (uint32_t)(r.v[0] >> 32);
-    if (u >= 2748779069u) return;  // 0.64 * 2^32
-    const uint32_t len = (j + 1 == td.nchunks) ? td.n - j * (uint32_t)kChunk : (uint32_t)kChunk;
-    if (len < 64) return;
-    const uint32_t start = j * (uint32_t)kChunk + (uint32_t)(r.v[1] % (uint64_t)(len - 63));
-    const uint32_t i = start + lane_id();
-    float g;
-    if (td.dtype == 0) g = ((const float*)td.grad)[i];
-    else g = h2f(((const uint16_t*)td.grad)[i]);
-    const float v = td.resid ? g + td.resid[i] : g;
-    atomicAdd(ws.t_hist + (size_t)t * kBins0 + (key_of(v) >> 20), 1u);
+    __shared__ uint32_t lh[kBins0];
+    const uint32_t c0 = blockIdx.x * kSampleChunksPerBlock;
+    const uint32_t c1 = (c0 + kSampleChunksPerBlock < C) ? c0 + kSampleChunksPerBlock : C;
+    const int t0 = tensor_of_chunk(d, T, c0);
+    const bool same = tensor_of_chunk(d, T, c1 - 1) == t0;
+    if (same && d[t0].n < kAllCandidatesBelow) return;
+    if (same)
+        for (int b = threadIdx.x; b < kBins0; b += kBlock) lh[b] = 0;
+    __syncthreads();
+    for (uint32_t c = c0 + (threadIdx.x >> 6); c < c1; c += 4) {
+        const int t = tensor_of_chunk(d, T, c);
+        const TDesc td = d[t];
+        if (td.n < kAllCandidatesBelow) continue;
+        const uint32_t j = c - td.chunk0;
+        U64x4 ctr = {{(uint64_t)td.tid, (uint64_t)j, 0, 0}};
+        const U64x4 r = philox4x64_10(ctr, seed, kStreamSample);
+        const uint32_t u = (uint32_t)(r.v[0] >> 32);
+        if (u >= 2748779069u) continue;  // 0.64 * 2^32
+        const uint32_t len = (j + 1 == td.nchunks) ? td.n - j * (uint32_t)kChunk : (uint32_t)kChunk;
+        if (len < 64) continue;
+        const uint32_t start = j * (uint32_t)kChunk + (uint32_t)(r.v[1] % (uint64_t)(len - 63));
+        const uint32_t i = start + lane_id();
+        float g;
+        if (td.dtype == 0) g = ((const float*)td.grad)[i];
+        else g = h2f(((const uint16_t*)td.grad)[i]);
+        const float v = td.resid ? g + td.resid[i] : g;
+        const uint32_t bin = key_of(v) >> 20;
+        if (same) atomicAdd(&lh[bin], 1u);
+        else atomicAdd(ws.t_hist + (size_t)t * kBins0 + bin, 1u);
+    }
+    if (!same) return;
+    __syncthreads();
+    flush_hist(lh, ws.t_hist + (size_t)t0 * kBins0, kBins0);
 }
 
 // One workgroup per tensor: read (and clear) the tensor's histogram and
@@ -387,7 +406,8 @@ hipError_t launch_topk(int kind, double ratio, uint64_t seed, const TDesc* d, in
         hipLaunchKernelGGL(topk_compact, dim3(C), blk, 0, s, d, T, 0, 0, ws);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit0, 0, ws);
     } else {  // sampled threshold, exact fallback per tensor
-        hipLaunchKernelGGL(topk_sample_hist, dim3((C + 3) / 4), blk, 0, s, d, T, C, seed, ws);
+        hipLaunchKernelGGL(topk_sample_hist, dim3((C + kSampleChunksPerBlock - 1) / kSampleChunksPerBlock), blk,
+                           0, s, d, T, C, seed, ws);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindThrSample, 0, ws);
         hipLaunchKernelGGL(topk_compact, dim3(C), blk, 0, s, d, T, 1, 0, ws);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit0, 0, ws);

@@ -17,7 +17,7 @@ struct Ws {
     uint32_t* flags;        // header: failure flags
     // BC_SIGN1
     uint32_t* s_cnt;        // [T] arrival counters          
-    uint32_t* s_ready;      // [T] scale-published flags     
+    uint32_t* s_ready;      // [T] 64-bit words: bit 32 = published, low 32 = scale     
     float* s_val;           // [T] published scales
     double* s_partial;      // [C] per-chunk sums of |v|
     // BC_TOPK, BC_TOPK_SAMPLED
@@ -57,6 +57,7 @@ struct DevInfo {
     int cus;
     int sign_coop_blocks_per_cu;
     bool coop_ok;
+    bool sign_two_pass;  // BYTECOMP_SIGN_PATH=twopass
 };
 hipError_t device_info(int dev, DevInfo* out);
 
@@ -81,6 +82,6 @@ hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t units, const WD
 
 // Work-unit sizes of the aggregate kernels (elements per unit).
 constexpr uint32_t kSparseTile = 2048;   // one wave's LDS tile
-constexpr uint32_t kSignAggUnit = 512;   // one wave: 8 elements per lane
+constexpr uint32_t kSignAggUnit = 8192;  // one workgroup: 32 elements per lane
 
 }  // namespace bc

@@ -226,3 +226,53 @@ def random_sign_words(rng: np.random.Generator, ns, word_counts):
             w[-1] &= np.uint32((1 << tail) - 1)
         out.append(w)
     return out
+
+
+# --------------------------------------------- on-device generation (large)
+# For the 1.56B-element workload, drawing every input with numpy on the host
+# takes minutes; these generators draw the same distributions on the device
+# with torch's seeded generator.  Sparse worker payloads use one index per
+# stratum (stratum j of tensor t covers [floor(j n/k), floor((j+1) n/k))),
+# which keeps indices distinct and ascending with the same density.
+
+def _torch_gen(device, *key):
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(int(np.random.SeedSequence([2205, *key]).generate_state(1, np.uint64)[0] >> 1))
+    return g
+
+
+def device_gradient(wl: Workload, tid: int, out, gen):
+    import torch
+    n = wl.sizes[tid]
+    x = torch.randn(n, generator=gen, device=out.device, dtype=torch.float32) * sigma_of(wl, tid)
+    out.copy_(x.to(out.dtype))
+
+
+def device_residual(wl: Workload, tid: int, out, gen):
+    import torch
+    n = wl.sizes[tid]
+    if wl.resid_mode == "zero":
+        out.zero_()
+        return
+    sig = float(wl.resid_mode.split(":")[1]) if wl.resid_mode.startswith("fixed:") else sigma_of(wl, tid) / 10.0
+    out.copy_(torch.randn(n, generator=gen, device=out.device, dtype=torch.float32) * sig)
+
+
+def device_sparse_payload(wl: Workload, w: int, counts, offs, device):
+    import torch
+    gen = _torch_gen(device, wl.wid, w, ROLE_WORKER)
+    total = int(offs[-1])
+    idx = torch.empty(total, dtype=torch.int64, device=device)
+    val = torch.empty(total, dtype=torch.float32, device=device)
+    for t, n in enumerate(wl.sizes):
+        k = int(counts[t])
+        if k == 0:
+            continue
+        j = torch.arange(k, device=device, dtype=torch.int64)
+        lo = (j * n) // k
+        hi = ((j + 1) * n) // k
+        u = torch.rand(k, generator=gen, device=device, dtype=torch.float64)
+        idx[offs[t]:offs[t] + k] = lo + torch.floor(u * (hi - lo).to(torch.float64)).to(torch.int64)
+        val[offs[t]:offs[t] + k] = torch.randn(k, generator=gen, device=device) * sigma_of(wl, t)
+    return idx.to(torch.int32), val

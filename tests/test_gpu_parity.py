@@ -188,10 +188,10 @@ def test_sparse_aggregate_dense_overlap():
         assert np.array_equal(bits(got[t]), bits(want[t])), t
 
 
-@pytest.mark.parametrize("W", [1, 3, 32, 64])
+@pytest.mark.parametrize("W", [1, 3, 8, 32, 64, 71, 130])
 def test_sign_aggregate_ragged(W):
     rng = np.random.default_rng(31 + W)
-    ns = [1, 31, 32, 33, 511, 512, 513, 4096 * 2 + 7, 100001, 0]
+    ns = [1, 31, 32, 33, 511, 512, 513, 2047, 2048, 2049, 8191, 8192, 8193, 8192 * 2 + 7, 100001, 0]
     wc = [O.words_for(n) for n in ns]
     payloads = []
     for w in range(W):
@@ -201,6 +201,29 @@ def test_sign_aggregate_ragged(W):
                          "off": O.word_offsets(ns)})
     got = gpu_aggregate("sign", 0.01, ns, payloads, 1.0 / W)
     want = O.aggregate_set("sign", ns, payloads, 1.0 / W)
+    for t in range(len(ns)):
+        assert np.array_equal(bits(got[t]), bits(want[t])), t
+
+
+@pytest.mark.parametrize("W", [4, 64])
+def test_sign_aggregate_wide_scale_span_takes_ordered_form(W):
+    # a tensor whose worker scales span more binades than fp64 can sum exactly
+    # is aggregated in worker order; its neighbour keeps the exact form
+    rng = np.random.default_rng(33 + W)
+    ns = [8192 + 100, 5000]
+    wc = [O.words_for(n) for n in ns]
+    limit = O.sign_span_limit(W)
+    payloads = []
+    for w in range(W):
+        words = WL.random_sign_words(rng, ns, wc)
+        wide = np.float32(2.0 ** -(limit + 3) if w == 1 else 1e-3 * (1 + 0.05 * rng.standard_normal()))
+        narrow = np.float32(1e-3 * (1 + 0.05 * rng.standard_normal()))
+        payloads.append({"bits": np.concatenate(words), "scale": np.array([wide, narrow], np.float32),
+                         "off": O.word_offsets(ns)})
+    assert not O.sign_exact_applies([p["scale"][0] for p in payloads])
+    assert O.sign_exact_applies([p["scale"][1] for p in payloads])
+    got = gpu_aggregate("sign", 0.01, ns, payloads, 1.0)
+    want = O.aggregate_set("sign", ns, payloads, 1.0)
     for t in range(len(ns)):
         assert np.array_equal(bits(got[t]), bits(want[t])), t
 

@@ -393,10 +393,12 @@ def test_sparse_aggregate_hand_example(golden):
 
 
 def test_sign_aggregate_hand_example(golden):
+    # the two workers' values are exact binary fractions: both forms agree
     d = golden["aggregate_sign"][0]
-    out = O.aggregate_sign(d["n"], [hexbits(w["words"]) for w in d["workers"]],
-                           [f32(w["scale"]) for w in d["workers"]], float(d["alpha"]))
-    assert np.array_equal(out, F(d["out"]))
+    for ordered in (False, True):
+        out = O.aggregate_sign(d["n"], [hexbits(w["words"]) for w in d["workers"]],
+                               [f32(w["scale"]) for w in d["workers"]], float(d["alpha"]), ordered=ordered)
+        assert np.array_equal(out, F(d["out"]))
 
 
 def test_sparse_aggregate_single_worker_is_decompress():
@@ -441,15 +443,104 @@ def test_sparse_aggregate_brute_force_order():
         assert bits(out[i]) == bits(f32(f32(0.5) * acc))
 
 
+def exact_round(values):
+    """Exact rational sum of float32 values, rounded once to float32
+    (Fraction -> nearest float64 is exact-enough only as a first step, so
+    the rounding to float32 is done on the rational directly)."""
+    tot = sum((Fraction(float(v)) for v in values), Fraction(0))
+    return fraction_to_f32(tot)
+
+
+def fraction_to_f32(q):
+    if q == 0:
+        return f32(0.0)
+    sign = -1 if q < 0 else 1
+    q = abs(q)
+    # find e with 2^e <= q < 2^(e+1)
+    e = q.numerator.bit_length() - q.denominator.bit_length()
+    if Fraction(2) ** e > q:
+        e -= 1
+    exp = max(e, -126) - 23           # unit in the last place (subnormals below -126)
+    scaled = q / Fraction(2) ** exp   # mantissa as a rational, < 2^24
+    m = scaled.numerator // scaled.denominator
+    rem = scaled - m
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and m % 2 == 1):
+        m += 1
+    return f32(sign * float(m) * 2.0 ** exp)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_exact_sum_matches_rational_arithmetic(seed):
+    rng = np.random.default_rng(seed)
+    for trial in range(300):
+        m = int(rng.integers(1, 70))
+        kind = trial % 5
+        if kind == 0:      # wide exponent range, subnormals included
+            x = (rng.standard_normal(m) * 10.0 ** rng.integers(-44, 38, m)).astype(f32)
+        elif kind == 1:    # cancellation: pairs x, -x plus a tiny remainder
+            h = (rng.standard_normal(m) * 1e3).astype(f32)
+            x = np.concatenate([h, -h, (rng.standard_normal(2) * 1e-30).astype(f32)])
+        elif kind == 2:    # ties at the rounding point: 1 + 2^-24 patterns
+            x = np.array([1.0, 2.0 ** -24] + [2.0 ** -60] * int(rng.integers(0, 3)), f32)
+        elif kind == 3:    # similar magnitudes (the sign aggregate's case)
+            x = (np.where(rng.random(m) < 0.5, -1, 1) * 1e-3 * (1 + 0.05 * rng.standard_normal(m))).astype(f32)
+        else:              # subnormal-only
+            x = (rng.integers(-(1 << 23), 1 << 23, m) * 2.0 ** -149).astype(f32)
+        got = O.exact_sum_f32(x)
+        want = exact_round(x)
+        assert bits(got) == bits(want), (trial, x.tolist())
+
+
+def test_sign_aggregate_exact_form_per_element():
+    rng = np.random.default_rng(77)
+    n, W = 90, 7
+    words = [rng.integers(0, 1 << 32, 3, dtype=np.uint64).astype(np.uint32) for _ in range(W)]
+    scales = (np.abs(rng.standard_normal(W)) * 1e-3).astype(f32)
+    assert O.sign_exact_applies(scales)
+    out = O.aggregate_sign(n, words, scales, 0.25)
+    for i in range(n):
+        d = [(-scales[w] if (words[w][i // 32] >> (i % 32)) & 1 else scales[w]) for w in range(W)]
+        assert bits(out[i]) == bits(f32(f32(0.25) * exact_round(d))), i
+
+
+def test_sign_aggregate_exact_is_within_recursive_sum_bound_of_ordered():
+    # |exact_rounded - ordered| <= (W-1) u sum|d| + u |sum|  (Higham, recursive summation)
+    rng = np.random.default_rng(78)
+    n, W = 4000, 64
+    words = [rng.integers(0, 1 << 32, 125, dtype=np.uint64).astype(np.uint32) for _ in range(W)]
+    scales = (1e-3 * (1 + 0.05 * rng.standard_normal(W))).astype(f32)
+    a = O.aggregate_sign(n, words, scales, 1.0)
+    b = O.aggregate_sign(n, words, scales, 1.0, ordered=True)
+    u = 2.0 ** -24
+    bound = (W - 1) * u * float(np.sum(scales, dtype=np.float64)) + u * np.abs(a.astype(np.float64))
+    assert np.all(np.abs(a.astype(np.float64) - b.astype(np.float64)) <= bound + 1e-45)
+    assert np.any(a != b)  # the two forms are genuinely different readings
+
+
+def test_sign_aggregate_wide_scale_span_uses_ordered_form():
+    W = 4
+    limit = O.sign_span_limit(W)
+    assert limit == 27
+    words = [np.array([0x5], np.uint32), np.array([0x3], np.uint32), np.array([0x0], np.uint32),
+             np.array([0x7], np.uint32)]
+    wide = np.array([1.0, 2.0 ** -(limit + 1), 0.5, 0.25], f32)
+    assert not O.sign_exact_applies(wide)
+    assert np.array_equal(O.aggregate_sign(3, words, wide, 1.0),
+                          O.aggregate_sign(3, words, wide, 1.0, ordered=True))
+    narrow = np.array([1.0, 2.0 ** -limit, 0.5, 0.25], f32)
+    assert O.sign_exact_applies(narrow)
+    for bad in (np.array([1.0, np.inf, 1, 1], f32), np.array([1.0, 1e-40, 1, 1], f32)):
+        assert not O.sign_exact_applies(bad)
+    assert O.sign_exact_applies(np.array([0.0, 0.0, 1.0, 1.0], f32))
+    assert O.sign_span_limit(64) == 23 and O.sign_span_limit(65) == 22 and O.sign_span_limit(1) == 29
+
+
 def test_sign_aggregate_zero_bits_and_single_worker():
     n, W = 100, 5
     words = [np.zeros(4, np.uint32) for _ in range(W)]
     scales = [f32(0.1 * (w + 1)) for w in range(W)]
     out = O.aggregate_sign(n, words, scales, 1.0)
-    acc = f32(0)
-    for s in scales:
-        acc = f32(acc + s)
-    assert np.all(out == acc)
+    assert np.all(out == exact_round(scales))
     rng = np.random.default_rng(6)
     g = rng.standard_normal(n).astype(f32)
     w, s, _ = O.compress_sign(g, None)

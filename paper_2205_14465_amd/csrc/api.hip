@@ -164,7 +164,8 @@ hipError_t device_info(int dev, DevInfo* out) {
         if (e != hipSuccess) return e;
         di.sign_coop_blocks_per_cu = b > 0 ? b : 1;
         const char* sp = std::getenv("BYTECOMP_SIGN_PATH");
-        di.sign_two_pass = sp && std::strcmp(sp, "twopass") == 0;
+        di.sign_one_pass = sp && std::strcmp(sp, "onepass") == 0;
+        di.any_empty = false;
         g_dev[dev] = di;
         g_dev_ok[dev] = true;
     }
@@ -402,6 +403,7 @@ int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t,
     DevInfo di;
     if (device_info(dev, &di) != hipSuccess) return BC_E_HIP;
     const Ws w = carve_workspace(ws, plan);
+    for (int i = 0; i < T && !di.any_empty; ++i) di.any_empty = t[i].n == 0;
     std::lock_guard<std::mutex> lk(g_mu);
     Entry* en = nullptr;
     hipError_t e = cache_get(d.data(), d.size() * sizeof(TDesc), (size_t)C * 4,

@@ -71,6 +71,24 @@ __device__ __forceinline__ int tensor_of_chunk(const TDesc* __restrict__ d, int 
     return (int)reinterpret_cast<const uint32_t*>(d + T)[c];
 }
 
+// Pointers read from descriptor tables are generic; viewing them in the
+// global address space lets the compiler use global (not flat) memory
+// instructions with scalar base addresses.
+#define BC_GLOBAL __attribute__((address_space(1)))
+template <typename T>
+__device__ __forceinline__ BC_GLOBAL T* gp(T* p) { return (BC_GLOBAL T*)p; }
+template <typename T>
+__device__ __forceinline__ const BC_GLOBAL T* gp(const T* p) { return (const BC_GLOBAL T*)p; }
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+// 16- and 8-byte global loads/stores (addresses aligned accordingly)
+__device__ __forceinline__ f32x4 ldg4f(const float* p) { return *(const BC_GLOBAL f32x4*)p; }
+__device__ __forceinline__ u32x4 ldg4u(const void* p) { return *(const BC_GLOBAL u32x4*)p; }
+__device__ __forceinline__ u32x2 ldg2u(const void* p) { return *(const BC_GLOBAL u32x2*)p; }
+__device__ __forceinline__ void stg4f(float* p, f32x4 v) { *(BC_GLOBAL f32x4*)p = v; }
+
 // ------------------------------------------------------------- bit helpers
 __device__ __forceinline__ uint32_t f2u(float x) { return __float_as_uint(x); }
 __device__ __forceinline__ float u2f(uint32_t u) { return __uint_as_float(u); }
@@ -105,17 +123,17 @@ __device__ __forceinline__ void load_chunk(const TDesc& td, uint32_t j, bool use
         float e4[4] = {0.f, 0.f, 0.f, 0.f};
         if (e0 + 3 < n) {
             if (DT == 0) {
-                float4 x = *reinterpret_cast<const float4*>((const float*)td.grad + e0);
+                const f32x4 x = ldg4f((const float*)td.grad + e0);
                 g4[0] = x.x; g4[1] = x.y; g4[2] = x.z; g4[3] = x.w;
             } else {
-                uint2 h = *reinterpret_cast<const uint2*>((const uint16_t*)td.grad + e0);
+                const u32x2 h = ldg2u((const uint16_t*)td.grad + e0);
                 g4[0] = h2f(h.x & 0xFFFFu);
                 g4[1] = h2f(h.x >> 16);
                 g4[2] = h2f(h.y & 0xFFFFu);
                 g4[3] = h2f(h.y >> 16);
             }
             if (use_resid) {
-                float4 y = *reinterpret_cast<const float4*>(td.resid + e0);
+                const f32x4 y = ldg4f(td.resid + e0);
                 e4[0] = y.x; e4[1] = y.y; e4[2] = y.z; e4[3] = y.w;
             }
             valid |= 0xFu << (4 * r);
@@ -123,15 +141,75 @@ __device__ __forceinline__ void load_chunk(const TDesc& td, uint32_t j, bool use
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 if (e0 + q < n) {
-                    if (DT == 0) g4[q] = ((const float*)td.grad)[e0 + q];
-                    else g4[q] = h2f(((const uint16_t*)td.grad)[e0 + q]);
-                    if (use_resid) e4[q] = td.resid[e0 + q];
+                    if (DT == 0) g4[q] = gp((const float*)td.grad)[e0 + q];
+                    else g4[q] = h2f(gp((const uint16_t*)td.grad)[e0 + q]);
+                    if (use_resid) e4[q] = gp(td.resid)[e0 + q];
                     valid |= 1u << (4 * r + q);
                 }
             }
         }
 #pragma unroll
         for (int q = 0; q < 4; ++q) v[4 * r + q] = use_resid ? g4[q] + e4[q] : g4[q];
+    }
+}
+
+// Raw chunk data held in registers between issuing the loads and using
+// them (lets a kernel prefetch its next chunk before a wait).  g[i] holds
+// element i's fp32 bits or, for fp16 gradients, its 16 bits.
+struct RawChunk {
+    uint32_t g[kEpt];
+    float e[kEpt];
+    uint32_t valid;
+};
+
+__device__ __forceinline__ void load_raw(const TDesc& td, uint32_t j, bool use_resid, RawChunk& r) {
+    const uint32_t base = j * (uint32_t)kChunk;
+    const uint32_t n = td.n;
+    r.valid = 0;
+#pragma unroll
+    for (int rr = 0; rr < kRounds; ++rr) {
+        const uint32_t e0 = base + 1024u * rr + 4u * threadIdx.x;
+        if (e0 + 3 < n) {
+            if (td.dtype == 0) {
+                const u32x4 x = ldg4u((const float*)td.grad + e0);
+                r.g[4 * rr] = x.x; r.g[4 * rr + 1] = x.y; r.g[4 * rr + 2] = x.z; r.g[4 * rr + 3] = x.w;
+            } else {
+                const u32x2 h = ldg2u((const uint16_t*)td.grad + e0);
+                r.g[4 * rr] = h.x & 0xFFFFu; r.g[4 * rr + 1] = h.x >> 16;
+                r.g[4 * rr + 2] = h.y & 0xFFFFu; r.g[4 * rr + 3] = h.y >> 16;
+            }
+            if (use_resid) {
+                const f32x4 y = ldg4f(td.resid + e0);
+                r.e[4 * rr] = y.x; r.e[4 * rr + 1] = y.y; r.e[4 * rr + 2] = y.z; r.e[4 * rr + 3] = y.w;
+            }
+            r.valid |= 0xFu << (4 * rr);
+        } else {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const bool ok = e0 + q < n;
+                if (td.dtype == 0) r.g[4 * rr + q] = ok ? gp((const uint32_t*)td.grad)[e0 + q] : 0u;
+                else r.g[4 * rr + q] = ok ? (uint32_t)gp((const uint16_t*)td.grad)[e0 + q] : 0u;
+                if (use_resid) r.e[4 * rr + q] = ok ? gp(td.resid)[e0 + q] : 0.f;
+                r.valid |= (ok ? 1u : 0u) << (4 * rr + q);
+            }
+        }
+        if (!use_resid) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) r.e[4 * rr + q] = 0.f;
+        }
+    }
+}
+
+// v = widen(g) + e from a RawChunk (e = 0 without residual); invalid
+// elements read as +0.0.
+__device__ __forceinline__ void raw_to_v(const TDesc& td, bool use_resid, const RawChunk& r,
+                                         float v[kEpt]) {
+#pragma unroll
+    for (int i = 0; i < kEpt; ++i) {
+        const float g0 = td.dtype == 0 ? u2f(r.g[i]) : h2f(r.g[i]);
+        float g = g0;
+        g = ((r.valid >> i) & 1u) ? g : 0.f;
+        v[i] = use_resid ? g + r.e[i] : g;
     }
 }
 
@@ -153,14 +231,14 @@ __device__ __forceinline__ void load_stored_v(const TDesc& td, uint32_t j, float
         for (int r = 0; r < kRounds; ++r) {
             const uint32_t e0 = base + 1024u * r + 4u * threadIdx.x;
             if (e0 + 3 < td.n) {
-                float4 y = *reinterpret_cast<const float4*>(td.resid + e0);
+                const f32x4 y = ldg4f(td.resid + e0);
                 v[4 * r] = y.x; v[4 * r + 1] = y.y; v[4 * r + 2] = y.z; v[4 * r + 3] = y.w;
                 valid |= 0xFu << (4 * r);
             } else {
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     bool ok = e0 + q < td.n;
-                    v[4 * r + q] = ok ? td.resid[e0 + q] : 0.f;
+                    v[4 * r + q] = ok ? gp(td.resid)[e0 + q] : 0.f;
                     valid |= (ok ? 1u : 0u) << (4 * r + q);
                 }
             }
@@ -179,12 +257,11 @@ __device__ __forceinline__ void store_chunk(float* dst, uint32_t n, uint32_t j, 
     for (int r = 0; r < kRounds; ++r) {
         const uint32_t e0 = base + 1024u * r + 4u * threadIdx.x;
         if (e0 + 3 < n) {
-            *reinterpret_cast<float4*>(dst + e0) =
-                make_float4(v[4 * r], v[4 * r + 1], v[4 * r + 2], v[4 * r + 3]);
+            stg4f(dst + e0, f32x4{v[4 * r], v[4 * r + 1], v[4 * r + 2], v[4 * r + 3]});
         } else {
 #pragma unroll
             for (int q = 0; q < 4; ++q)
-                if (e0 + q < n) dst[e0 + q] = v[4 * r + q];
+                if (e0 + q < n) gp(dst)[e0 + q] = v[4 * r + q];
         }
     }
 }

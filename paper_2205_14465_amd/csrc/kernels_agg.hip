@@ -38,17 +38,25 @@ __device__ __forceinline__ uint32_t lower_bound_u32(const uint32_t* idx, uint32_
     uint32_t lo = 0, hi = k;
     while (lo < hi) {
         const uint32_t mid = (lo + hi) >> 1;
-        if (idx[mid] < x) lo = mid + 1; else hi = mid;
+        if (gp(idx)[mid] < x) lo = mid + 1; else hi = mid;
     }
     return lo;
 }
 
-constexpr int kPrefetch = 8;  // workers whose first 64 entries are loaded together
 
 }  // namespace
 
 // ----------------------------------------------------------------- sparse
 // Dynamic LDS: 4 waves x (2048 floats tile + W cursors).
+//
+// The next entries of kSparseSlots workers are kept in flight in registers
+// (slot w % kSparseSlots holds worker w): as soon as a worker's entries for
+// the tile have been added, its slot is refilled with the worker that comes
+// kSparseSlots later, or, when W is a multiple of kSparseSlots and the
+// next tile continues the tensor, with the same worker's entries for the
+// next tile (its cursor is then final).
+constexpr int kSparseSlots = 16;
+
 __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restrict__ a, int T,
                                                            uint32_t U, const WDesc* __restrict__ wd,
                                                            int W, float alpha) {
@@ -61,8 +69,16 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
     const uint64_t gw = (uint64_t)blockIdx.x * 4 + wave;
     const uint32_t u_beg = (uint32_t)((gw * U) / nw);
     const uint32_t u_end = (uint32_t)(((gw + 1) * U) / nw);
+    const bool cross = (W % kSparseSlots) == 0;
+    // Every slot load is issued unconditionally (index clamped into the
+    // tensor's entries, validity kept apart) so that the compiler can count
+    // the loads in flight exactly and wait only for the one it needs.
+    uint32_t x[kSparseSlots];
+    float y[kSparseSlots];
+    bool ok[kSparseSlots];
     int t = -1;
     ADesc ad{};
+    bool primed = false;  // slots already hold this tile's first entries
     for (uint32_t u = u_beg; u < u_end; ++u) {
         if (t < 0 || u >= ad.unit0 + ad.nunits) {
             t = unit_owner(wd, W, u);
@@ -71,70 +87,79 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
             for (int w = lane; w < W; w += 64)
                 cur[w] = lo0 == 0 ? 0u : lower_bound_u32(wd[w].a + ad.off, ad.k, lo0);
             __builtin_amdgcn_wave_barrier();
+            primed = false;
+        }
+        const uint32_t klast = ad.k - 1;  // a tile exists, so k >= 1
+        if (!primed) {
+#pragma unroll
+            for (int q = 0; q < kSparseSlots; ++q) {
+                const int w = q < W ? q : W - 1;
+                const uint32_t i = cur[w] + lane;
+                const uint32_t ic = i < ad.k ? i : klast;
+                x[q] = gp(wd[w].a)[ad.off + ic];
+                y[q] = gp(wd[w].b)[ad.off + ic];
+                ok[q] = q < W && i < ad.k;
+            }
         }
         const uint32_t lo = (u - ad.unit0) * kSparseTile;
         const uint32_t hi = (lo + kSparseTile < ad.n) ? lo + kSparseTile : ad.n;
+        const bool next_same = cross && u + 1 < u_end && u + 1 < ad.unit0 + ad.nunits;
         for (int i = lane; i < (int)kSparseTile; i += 64) tile[i] = 0.f;
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
-        for (int w0 = 0; w0 < W; w0 += kPrefetch) {
-            uint32_t x[kPrefetch];
-            float y[kPrefetch];
-            uint32_t c[kPrefetch];
+        for (int w0 = 0; w0 < W; w0 += kSparseSlots) {
 #pragma unroll
-            for (int q = 0; q < kPrefetch; ++q) {
-                x[q] = 0xFFFFFFFFu;
-                y[q] = 0.f;
-                c[q] = 0;
-                if (w0 + q < W) {
-                    c[q] = cur[w0 + q];
-                    const uint32_t i = c[q] + lane;
-                    if (i < ad.k) {
-                        x[q] = wd[w0 + q].a[ad.off + i];
-                        y[q] = wd[w0 + q].b[ad.off + i];
-                    }
-                }
-            }
-#pragma unroll
-            for (int q = 0; q < kPrefetch; ++q) {
+            for (int q = 0; q < kSparseSlots; ++q) {
                 const int w = w0 + q;
                 if (w >= W) break;
-                uint32_t cc = c[q];
-                uint32_t xi = x[q];
-                float yi = y[q];
-                for (;;) {
-                    const bool in = xi < hi;
+                uint32_t cc = cur[w];
+                uint32_t cnt;
+                {
+                    const bool in = ok[q] && x[q] < hi;
                     const uint64_t m = __ballot(in);
                     // entries below the tile can only come from an unsorted
                     // payload; they are skipped rather than written out of range
-                    if (in && xi >= lo) tile[xi - lo] += yi;
-                    const uint32_t cnt = (uint32_t)__popcll(m);
+                    if (in && x[q] >= lo) tile[x[q] - lo] += y[q];
+                    cnt = (uint32_t)__popcll(m);
                     cc += cnt;
-                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
                     __builtin_amdgcn_wave_barrier();
-                    if (cnt < 64) break;
+                }
+                // more than 64 entries of this worker in the tile (dense
+                // payloads): keep reading in a loop of its own
+                while (cnt == 64) {
                     const uint32_t i = cc + lane;
-                    xi = 0xFFFFFFFFu;
-                    yi = 0.f;
-                    if (i < ad.k) {
-                        xi = wd[w].a[ad.off + i];
-                        yi = wd[w].b[ad.off + i];
-                    }
+                    const bool oki = i < ad.k;
+                    const uint32_t ic = oki ? i : klast;
+                    const uint32_t xi = gp(wd[w].a)[ad.off + ic];
+                    const float yi = gp(wd[w].b)[ad.off + ic];
+                    const bool in = oki && xi < hi;
+                    const uint64_t m = __ballot(in);
+                    if (in && xi >= lo) tile[xi - lo] += yi;
+                    cnt = (uint32_t)__popcll(m);
+                    cc += cnt;
+                    __builtin_amdgcn_wave_barrier();
                 }
                 if (lane == 0) cur[w] = cc;
+                // refill the slot: the worker kSparseSlots later in this
+                // tile, or this worker's entries for the next tile
+                const int wn = w + kSparseSlots;
+                const bool later = wn < W;
+                const int wr = later ? wn : w;
+                const uint32_t i = (later ? cur[wn] : cc) + lane;
+                const uint32_t ic = i < ad.k ? i : klast;
+                x[q] = gp(wd[wr].a)[ad.off + ic];
+                y[q] = gp(wd[wr].b)[ad.off + ic];
+                ok[q] = (later || next_same) && i < ad.k;
             }
-            __builtin_amdgcn_wave_barrier();
         }
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        primed = next_same;
         float* out = ad.out + lo;
         const uint32_t len = hi - lo;
         for (uint32_t i = 4u * lane; i < len; i += 256u) {
             if (i + 3 < len) {
-                float4 r = make_float4(alpha * tile[i], alpha * tile[i + 1], alpha * tile[i + 2],
-                                       alpha * tile[i + 3]);
-                *reinterpret_cast<float4*>(out + i) = r;
+                stg4f(out + i, f32x4{alpha * tile[i], alpha * tile[i + 1], alpha * tile[i + 2],
+                                     alpha * tile[i + 3]});
             } else {
-                for (uint32_t q = i; q < len; ++q) out[q] = alpha * tile[q];
+                for (uint32_t q = i; q < len; ++q) gp(out)[q] = alpha * tile[q];
             }
         }
         __builtin_amdgcn_wave_barrier();
@@ -173,7 +198,7 @@ __device__ __forceinline__ void sign_word_accumulate(float (&acc)[32], uint32_t 
 // group's eight +-s_w are tabulated in LDS (fp64), the eight sign bits of an
 // element form the table index, and the fp64 sum of the group entries is
 // the exact sum, rounded once to fp32 at the end.  The eight words of a
-// group are transposed into per-element bytes with shift/and-or steps that
+// group are transposed into per-element bytes with rotate/and-or steps that
 // each serve four elements.
 //
 // Ordered form (otherwise): worker-ordered fp32 additions.
@@ -241,11 +266,13 @@ __global__ __launch_bounds__(kBlock) void aggregate_sign(const ADesc* __restrict
 #pragma unroll
                 for (int jj = 0; jj < 8; ++jj) {
                     const int w = wbase + jj;
-                    const uint32_t word = (has && w < W) ? wd[w].a[woff] : 0u;
-                    const uint32_t x = word << jj;
+                    const uint32_t word = (has && w < W) ? gp(wd[w].a)[woff] : 0u;
                     const uint32_t m = 0x01010101u << jj;
+                    // rotate bits q, q+8, q+16, q+24 of the word to jj, jj+8,
+                    // jj+16, jj+24 (v_alignbit), then mask them in (v_and_or)
 #pragma unroll
-                    for (int q = 0; q < 8; ++q) idx4[q] |= (x >> q) & m;
+                    for (int q = 0; q < 8; ++q)
+                        idx4[q] |= __builtin_amdgcn_alignbit(word, word, (uint32_t)((q - jj) & 31)) & m;
                 }
                 const double* tb = tab + gg * 256;
 #pragma unroll
@@ -265,7 +292,7 @@ __global__ __launch_bounds__(kBlock) void aggregate_sign(const ADesc* __restrict
             for (int g = 0; g < kSignGroup; ++g) {
                 const int w = w0 + g < W ? w0 + g : W - 1;
                 sv[g] = sc[w];
-                word[g] = has ? wd[w].a[woff] : 0u;
+                word[g] = has ? gp(wd[w].a)[woff] : 0u;
             }
 #pragma unroll
             for (int g = 0; g < kSignGroup; ++g)
@@ -278,11 +305,11 @@ __global__ __launch_bounds__(kBlock) void aggregate_sign(const ADesc* __restrict
     if (e0 + 32u <= ad.n) {
 #pragma unroll
         for (int q = 0; q < 32; q += 4)
-            *reinterpret_cast<float4*>(out + q) = make_float4(res[q], res[q + 1], res[q + 2], res[q + 3]);
+            stg4f(out + q, f32x4{res[q], res[q + 1], res[q + 2], res[q + 3]});
     } else {
 #pragma unroll
         for (int q = 0; q < 32; ++q)
-            if (e0 + q < ad.n) out[q] = res[q];
+            if (e0 + q < ad.n) gp(out)[q] = res[q];
     }
 }
 
@@ -307,9 +334,9 @@ __global__ __launch_bounds__(kBlock) void sparse_residual_update(const TDesc* __
     __syncthreads();
     for (uint32_t base = start_sh;; base += kBlock) {
         const uint32_t i = base + threadIdx.x;
-        const uint32_t x = i < td.k ? ix[i] : 0xFFFFFFFFu;
+        const uint32_t x = i < td.k ? gp(ix)[i] : 0xFFFFFFFFu;
         const bool in = x < hi;
-        if (in && x >= lo) dec[x - lo] = vx[i];
+        if (in && x >= lo) dec[x - lo] = gp(vx)[i];
         if (__syncthreads_count(in) < kBlock) break;
     }
     __syncthreads();

@@ -17,10 +17,12 @@
 // running workgroup or is the next chunk of a workgroup whose own wait
 // ends first, so every wait ends.  The wait is bounded anyway: after
 // ~2^22 polls it records kFlagWaitTimeout in the workspace and goes on.
-// When a tensor is larger than the grid (or cooperative launch is not
-// available, or BYTECOMP_SIGN_PATH=twopass) a two-pass variant runs
-// instead: pass 1 writes the bits, the chunk partial sums and v (into e);
-// pass 2 re-reads v and writes the residual.
+// By default a two-pass variant runs instead (BYTECOMP_SIGN_PATH=onepass
+// selects the one-pass kernel where every tensor fits the grid): pass 1
+// writes the bits, the chunk partial sums and v (into e); pass 2 sums the
+// partials of its tensor, re-reads v and writes the residual.  The re-read
+// of v mostly hits the 256 MB last-level cache for tensor sets of
+// ResNet-50 size, so its HBM traffic stays close to the one-pass kernel's.
 #include "launch.hpp"
 
 namespace bc {
@@ -95,13 +97,25 @@ __global__ __launch_bounds__(kBlock) void sign_compress_coop(const TDesc* __rest
     __shared__ double sh[4];
     __shared__ float s_sh;
     __shared__ int last_sh;
-    for (uint32_t c = blockIdx.x; c < C; c += gridDim.x) {
+    // The next chunk's g and e are loaded into registers before this chunk's
+    // wait for its tensor's scale, so the wait overlaps the next loads.
+    RawChunk raw;
+    uint32_t c = blockIdx.x;
+    if (c < C) {
+        const TDesc td0 = d[tensor_of_chunk(d, T, c)];
+        load_raw(td0, c - td0.chunk0, td0.resid != nullptr, raw);
+    }
+    for (; c < C; c += gridDim.x) {
         const int t = tensor_of_chunk(d, T, c);
         const TDesc td = d[t];
         const uint32_t j = c - td.chunk0;
         float v[kEpt];
-        uint32_t valid;
-        load_v(td, j, td.resid != nullptr, v, valid);
+        raw_to_v(td, td.resid != nullptr, raw, v);
+        const uint32_t cn = c + gridDim.x;
+        if (cn < C) {
+            const TDesc tdn = d[tensor_of_chunk(d, T, cn)];
+            load_raw(tdn, cn - tdn.chunk0, tdn.resid != nullptr, raw);
+        }
         store_sign_words(v, bits + td.off + (uint64_t)j * kChunkWords, chunk_words(td, j));
         const double p = block_sum_f64(thread_abs_sum(v), sh);
         float s;
@@ -159,6 +173,8 @@ __global__ __launch_bounds__(kBlock) void sign_compress_coop(const TDesc* __rest
 }
 
 // --------------------------------------------------------------- two pass
+constexpr uint32_t kInlineScaleChunks = 1024;
+
 __global__ __launch_bounds__(kBlock) void sign_pass1(const TDesc* __restrict__ d, int T,
                                                      uint32_t* __restrict__ bits, Ws ws) {
     __shared__ double sh[4];
@@ -180,6 +196,7 @@ __global__ __launch_bounds__(kBlock) void sign_finalize(const TDesc* __restrict_
     __shared__ double sh[4];
     const int t = blockIdx.x;
     const TDesc td = d[t];
+    if (td.nchunks > 0 && td.nchunks <= kInlineScaleChunks) return;  // pass 2 does it
     float s = 0.f;
     if (td.nchunks > 0) {
         const double tot = reduce_partials(ws.s_partial + td.chunk0, td.nchunks, sh);
@@ -191,16 +208,31 @@ __global__ __launch_bounds__(kBlock) void sign_finalize(const TDesc* __restrict_
     }
 }
 
-__global__ __launch_bounds__(kBlock) void sign_pass2(const TDesc* __restrict__ d, int T, Ws ws) {
+// Pass 2.  A tensor with at most kInlineScaleChunks chunks has its scale
+// summed from the chunk partials by every workgroup of the tensor (the same
+// fixed-order sum as sign_finalize; the first workgroup also stores it);
+// larger tensors read the scale sign_finalize stored.
+
+__global__ __launch_bounds__(kBlock) void sign_pass2(const TDesc* __restrict__ d, int T,
+                                                     float* __restrict__ scale_out, Ws ws) {
+    __shared__ double sh[4];
     const uint32_t c = blockIdx.x;
     const int t = tensor_of_chunk(d, T, c);
     const TDesc td = d[t];
-    if (!td.resid) return;
     const uint32_t j = c - td.chunk0;
+    float s;
+    if (td.nchunks <= kInlineScaleChunks) {
+        const double tot = reduce_partials(ws.s_partial + td.chunk0, td.nchunks, sh);
+        s = (float)(tot / (double)td.n);
+        if (j == 0 && threadIdx.x == 0) scale_out[t] = s;
+    } else {
+        s = ws.s_val[t];
+    }
+    if (!td.resid) return;
     float v[kEpt];
     uint32_t valid;
     load_stored_v(td, j, v, valid);  // e holds v after the first pass
-    store_sign_residual(td, j, ws.s_val[t], v);
+    store_sign_residual(td, j, s, v);
 }
 
 // Per-call preparation: clear the arrival counters and flags of the
@@ -246,19 +278,21 @@ hipError_t launch_sign_compress(const TDesc* d, int T, uint32_t C, uint32_t max_
                                 bool, uint32_t* bits, float* scale, const Ws& ws,
                                 const DevInfo& di, hipStream_t s) {
     if (T <= 0) return hipSuccess;
-    hipLaunchKernelGGL(sign_prep, dim3((T + 255) / 256), dim3(256), 0, s, d, T, scale, ws);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess || C == 0) return e;
     const uint32_t cap = (uint32_t)di.cus * (uint32_t)di.sign_coop_blocks_per_cu;
     const uint32_t G = C < cap ? C : cap;
-    if (di.coop_ok && max_chunks <= G && !di.sign_two_pass) {
+    if (di.sign_one_pass && di.coop_ok && C > 0 && max_chunks <= G) {
+        hipLaunchKernelGGL(sign_prep, dim3((T + 255) / 256), dim3(256), 0, s, d, T, scale, ws);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
         void* args[] = {(void*)&d, (void*)&T, (void*)&C, (void*)&bits, (void*)&scale, (void*)&ws};
         return hipLaunchCooperativeKernel((const void*)sign_compress_coop, dim3(G), dim3(kBlock), args,
                                           0, s);
     }
-    hipLaunchKernelGGL(sign_pass1, dim3(C), dim3(kBlock), 0, s, d, T, bits, ws);
-    hipLaunchKernelGGL(sign_finalize, dim3(T), dim3(kBlock), 0, s, d, scale, ws);
-    hipLaunchKernelGGL(sign_pass2, dim3(C), dim3(kBlock), 0, s, d, T, ws);
+    if (C > 0) hipLaunchKernelGGL(sign_pass1, dim3(C), dim3(kBlock), 0, s, d, T, bits, ws);
+    // tensors without elements, or with more chunks than pass 2 sums inline
+    if (max_chunks > kInlineScaleChunks || C == 0 || di.any_empty)
+        hipLaunchKernelGGL(sign_finalize, dim3(T), dim3(kBlock), 0, s, d, scale, ws);
+    if (C > 0) hipLaunchKernelGGL(sign_pass2, dim3(C), dim3(kBlock), 0, s, d, T, scale, ws);
     return hipGetLastError();
 }
 

@@ -115,9 +115,9 @@ __global__ __launch_bounds__(kBlock) void topk_sample_hist(const TDesc* __restri
         const uint32_t start = j * (uint32_t)kChunk + (uint32_t)(r.v[1] % (uint64_t)(len - 63));
         const uint32_t i = start + lane_id();
         float g;
-        if (td.dtype == 0) g = ((const float*)td.grad)[i];
-        else g = h2f(((const uint16_t*)td.grad)[i]);
-        const float v = td.resid ? g + td.resid[i] : g;
+        if (td.dtype == 0) g = gp((const float*)td.grad)[i];
+        else g = h2f(gp((const uint16_t*)td.grad)[i]);
+        const float v = td.resid ? g + gp(td.resid)[i] : g;
         const uint32_t bin = key_of(v) >> 20;
         if (same) atomicAdd(&lh[bin], 1u);
         else atomicAdd(ws.t_hist + (size_t)t * kBins0 + bin, 1u);
@@ -379,7 +379,7 @@ __global__ __launch_bounds__(kBlock) void topk_emit(const TDesc* __restrict__ d,
         if (sel && at < end) {
             idx[at] = e.x;
             val[at] = u2f(e.y);
-            if (resid) resid[e.x] = 0.f;
+            if (resid) gp(resid)[e.x] = 0.f;
         }
         eq_seen += n_eq;
         pos += n_sel;

@@ -57,7 +57,8 @@ struct DevInfo {
     int cus;
     int sign_coop_blocks_per_cu;
     bool coop_ok;
-    bool sign_two_pass;  // BYTECOMP_SIGN_PATH=twopass
+    bool sign_one_pass;  // BYTECOMP_SIGN_PATH=onepass
+    bool any_empty;      // per call: some tensor has no elements
 };
 hipError_t device_info(int dev, DevInfo* out);
 

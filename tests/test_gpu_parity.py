@@ -216,7 +216,7 @@ def test_sign_aggregate_wide_scale_span_takes_ordered_form(W):
     payloads = []
     for w in range(W):
         words = WL.random_sign_words(rng, ns, wc)
-        wide = np.float32(2.0 ** -(limit + 3) if w == 1 else 1e-3 * (1 + 0.05 * rng.standard_normal()))
+        wide = np.float32(1e-3 * 2.0 ** -(limit + 2) if w == 1 else 1e-3 * (1 + 0.05 * rng.standard_normal()))
         narrow = np.float32(1e-3 * (1 + 0.05 * rng.standard_normal()))
         payloads.append({"bits": np.concatenate(words), "scale": np.array([wide, narrow], np.float32),
                          "off": O.word_offsets(ns)})

@@ -163,6 +163,10 @@ hipError_t device_info(int dev, DevInfo* out) {
         e = sign_coop_occupancy(&b);
         if (e != hipSuccess) return e;
         di.sign_coop_blocks_per_cu = b > 0 ? b : 1;
+        b = 0;
+        e = aggregate_sign_occupancy(&b);
+        if (e != hipSuccess) return e;
+        di.agg_sign_blocks_per_cu = b > 0 ? b : 1;
         const char* sp = std::getenv("BYTECOMP_SIGN_PATH");
         di.sign_one_pass = sp && std::strcmp(sp, "onepass") == 0;
         di.any_empty = false;
@@ -188,6 +192,7 @@ WsPlan plan_workspace(int kind, int T, uint64_t C, uint64_t sum_k) {
         take(p.s_ready, t * 8);
         take(p.s_val, t * 4);
         take(p.s_partial, (size_t)C * 8);
+        take(p.s_wide, t * 4);
     } else if (kind == BC_TOPK || kind == BC_TOPK_SAMPLED) {
         take(p.t_hist, t * kBins0 * 4);
         take(p.t_thr, t * 4);
@@ -222,6 +227,7 @@ Ws carve_workspace(void* base, const WsPlan& p) {
     w.s_ready = (uint32_t*)at(p.s_ready);
     w.s_val = (float*)at(p.s_val);
     w.s_partial = (double*)at(p.s_partial);
+    w.s_wide = (uint32_t*)at(p.s_wide);
     w.t_hist = (uint32_t*)at(p.t_hist);
     w.t_thr = (uint32_t*)at(p.t_thr);
     w.t_prefix = (uint32_t*)at(p.t_prefix);
@@ -442,12 +448,13 @@ int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, 
     const uint32_t unit = sparse ? kSparseTile : kSignAggUnit;
     std::vector<unsigned char> table;
     try {
-        table.resize((size_t)T * sizeof(ADesc) + (size_t)W * sizeof(WDesc));
+        table.resize((size_t)T * sizeof(ADesc) + (size_t)2 * padded_workers(W) * sizeof(uint64_t));
     } catch (const std::bad_alloc&) {
         return BC_E_SIZE;
     }
     ADesc* a = (ADesc*)table.data();
-    WDesc* wd = (WDesc*)(table.data() + (size_t)T * sizeof(ADesc));
+    uint64_t* wa = (uint64_t*)(table.data() + (size_t)T * sizeof(ADesc));
+    uint64_t* wb = wa + padded_workers(W);
     uint64_t units = 0, off = 0;
     for (int i = 0; i < T; ++i) {
         if (n[i] >= kMaxN) return BC_E_SIZE;
@@ -465,18 +472,38 @@ int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, 
         units += nu;
     }
     if (units >= (1ull << 31)) return BC_E_SIZE;
+    uint32_t* wide = nullptr;  // sign: per-tensor fp64-form flags in the workspace
+    if (!sparse) {
+        uint64_t C = 0;
+        for (int i = 0; i < T; ++i) C += (n[i] + kChunk - 1) / kChunk;
+        const WsPlan plan = plan_workspace(kind, T, C, 0);
+        if (ws_bytes < plan.total) return BC_E_WORKSPACE;
+        wide = carve_workspace(ws, plan).s_wide;
+    }
+    // the sign kernel addresses a worker's words with a 32-bit byte offset
+    if (!sparse && off >= (1ull << 30)) return BC_E_SIZE;
     for (int q = 0; q < W; ++q) {
         if (sparse) {
             if (off && (!in[q].idx || !in[q].val)) return BC_E_NULL;
-            wd[q].a = in[q].idx;
-            wd[q].b = in[q].val;
+            wa[q] = (uint64_t)(uintptr_t)in[q].idx;
+            wb[q] = (uint64_t)(uintptr_t)in[q].val;
         } else {
             if (!in[q].bits || !in[q].scale) return BC_E_NULL;
-            wd[q].a = in[q].bits;
-            wd[q].b = in[q].scale;
+            wa[q] = (uint64_t)(uintptr_t)in[q].bits;
+            wb[q] = (uint64_t)(uintptr_t)in[q].scale;
         }
     }
+    // descriptors W .. padded_workers(W)-1 repeat the last worker, so that
+    // kernels may read worker descriptors sixteen at a time
+    for (int q = W; q < padded_workers(W); ++q) {
+        wa[q] = wa[W - 1];
+        wb[q] = wb[W - 1];
+    }
     hipStream_t s = (hipStream_t)stream;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return BC_E_HIP;
+    DevInfo di;
+    if (device_info(dev, &di) != hipSuccess) return BC_E_HIP;
     std::lock_guard<std::mutex> lk(g_mu);
     Entry* en = nullptr;
     hipError_t e = cache_get(table.data(), table.size(), (size_t)units * 4,
@@ -488,11 +515,12 @@ int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, 
                              s, &en);
     if (e != hipSuccess) return BC_E_HIP;
     const ADesc* ad = (const ADesc*)en->dev;
-    const WDesc* wdd = (const WDesc*)((const char*)en->dev + (size_t)T * sizeof(ADesc));
+    const uint64_t* wdd = (const uint64_t*)((const char*)en->dev + (size_t)T * sizeof(ADesc));
     if (sparse)
         e = launch_aggregate_sparse(ad, T, (uint32_t)units, wdd, W, alpha, s);
     else
-        e = launch_aggregate_sign(ad, T, (uint32_t)units, wdd, W, alpha, s);
+        e = launch_aggregate_sign(ad, T, (uint32_t)units, wdd, W, alpha, wide,
+                                  (uint32_t)(di.cus * di.agg_sign_blocks_per_cu), s);
     cache_mark_used(en, s);
     return finish(hip_status(e), s, ws);
 }

@@ -48,10 +48,10 @@ struct ADesc {
 static_assert(sizeof(ADesc) == 32, "ADesc layout");
 
 // One worker's payload in an aggregate call.
-struct WDesc {
-    const uint32_t* a;  // sparse: idx; sign: bits
-    const float* b;     // sparse: val; sign: scale
-};
+// Worker table of the aggregate descriptor (pointers stored as uint64):
+// a[Wp] (sparse: idx, sign: bits), then b[Wp] (sparse: val, sign: scale),
+// then the unit -> tensor map; Wp = padded_workers(W) (launch.hpp) and the
+// slots past W repeat worker W-1.
 
 // Largest t with d[t].chunk0 <= c (tensors without chunks share chunk0 with
 // their successor, so the search lands on the tensor that owns chunk c).

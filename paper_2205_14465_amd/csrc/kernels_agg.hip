@@ -28,9 +28,16 @@ namespace {
 
 typedef const float __attribute__((address_space(4)))* cf32p;
 
-// The aggregate table is [ADesc x T][WDesc x W][unit -> tensor map].
-__device__ __forceinline__ int unit_owner(const WDesc* __restrict__ wd, int W, uint32_t u) {
-    return (int)reinterpret_cast<const uint32_t*>(wd + W)[u];
+// The aggregate table is [ADesc x T][a x Wp][b x Wp][unit -> tensor map]
+// with Wp = padded_workers(W); slots past W repeat worker W-1.
+__device__ __forceinline__ const uint32_t* w_a(const uint64_t* __restrict__ wp, int w) {
+    return (const uint32_t*)wp[w];
+}
+__device__ __forceinline__ const float* w_b(const uint64_t* __restrict__ wp, int W, int w) {
+    return (const float*)wp[padded_workers(W) + w];
+}
+__device__ __forceinline__ int unit_owner(const uint64_t* __restrict__ wp, int W, uint32_t u) {
+    return (int)reinterpret_cast<const uint32_t*>(wp + 2 * padded_workers(W))[u];
 }
 
 // First position p in [0, k) with idx[p] >= x (k if none).
@@ -58,7 +65,7 @@ __device__ __forceinline__ uint32_t lower_bound_u32(const uint32_t* idx, uint32_
 constexpr int kSparseSlots = 16;
 
 __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restrict__ a, int T,
-                                                           uint32_t U, const WDesc* __restrict__ wd,
+                                                           uint32_t U, const uint64_t* __restrict__ wp,
                                                            int W, float alpha) {
     extern __shared__ uint32_t lds[];
     const int wave = wave_id();
@@ -81,11 +88,11 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
     bool primed = false;  // slots already hold this tile's first entries
     for (uint32_t u = u_beg; u < u_end; ++u) {
         if (t < 0 || u >= ad.unit0 + ad.nunits) {
-            t = unit_owner(wd, W, u);
+            t = unit_owner(wp, W, u);
             ad = a[t];
             const uint32_t lo0 = (u - ad.unit0) * kSparseTile;
             for (int w = lane; w < W; w += 64)
-                cur[w] = lo0 == 0 ? 0u : lower_bound_u32(wd[w].a + ad.off, ad.k, lo0);
+                cur[w] = lo0 == 0 ? 0u : lower_bound_u32(w_a(wp, w) + ad.off, ad.k, lo0);
             __builtin_amdgcn_wave_barrier();
             primed = false;
         }
@@ -96,8 +103,8 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
                 const int w = q < W ? q : W - 1;
                 const uint32_t i = cur[w] + lane;
                 const uint32_t ic = i < ad.k ? i : klast;
-                x[q] = gp(wd[w].a)[ad.off + ic];
-                y[q] = gp(wd[w].b)[ad.off + ic];
+                x[q] = gp(w_a(wp, w))[ad.off + ic];
+                y[q] = gp(w_b(wp, W, w))[ad.off + ic];
                 ok[q] = q < W && i < ad.k;
             }
         }
@@ -129,8 +136,8 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
                     const uint32_t i = cc + lane;
                     const bool oki = i < ad.k;
                     const uint32_t ic = oki ? i : klast;
-                    const uint32_t xi = gp(wd[w].a)[ad.off + ic];
-                    const float yi = gp(wd[w].b)[ad.off + ic];
+                    const uint32_t xi = gp(w_a(wp, w))[ad.off + ic];
+                    const float yi = gp(w_b(wp, W, w))[ad.off + ic];
                     const bool in = oki && xi < hi;
                     const uint64_t m = __ballot(in);
                     if (in && xi >= lo) tile[xi - lo] += yi;
@@ -146,8 +153,8 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
                 const int wr = later ? wn : w;
                 const uint32_t i = (later ? cur[wn] : cc) + lane;
                 const uint32_t ic = i < ad.k ? i : klast;
-                x[q] = gp(wd[wr].a)[ad.off + ic];
-                y[q] = gp(wd[wr].b)[ad.off + ic];
+                x[q] = gp(w_a(wp, wr))[ad.off + ic];
+                y[q] = gp(w_b(wp, W, wr))[ad.off + ic];
                 ok[q] = (later || next_same) && i < ad.k;
             }
         }
@@ -171,145 +178,326 @@ namespace {
 
 constexpr int kSignGroup = 4;  // workers whose words are in flight together (ordered form)
 
-// Ordered form: acc[q] += (bit q of word) ? -s : +s for the lane's 32
+// Word at a 32-bit byte offset from a wave-uniform base: the form the
+// backend emits as a global load with an SGPR base and a VGPR offset.
+__device__ __forceinline__ uint32_t ld_word(const uint32_t* base, uint32_t byte_off) {
+    return *(const BC_GLOBAL uint32_t*)((const BC_GLOBAL char*)gp(base) + byte_off);
+}
+
+// Transposes the four 8x8 bit matrices held byte-wise in x[0..7]: on
+// return bit c of byte r of x[i] is what bit i of byte r of x[c] was.
+// Three rounds of block swaps (4x4, 2x2, 1x1 blocks), each exchanging bits
+// between two words with a shift, an xor-and and two xors.
+__host__ __device__ __forceinline__ void transpose_bytes8(uint32_t (&x)[8]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const uint32_t t = ((x[i] >> 4) ^ x[i + 4]) & 0x0F0F0F0Fu;
+        x[i + 4] ^= t;
+        x[i] ^= t << 4;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; i += 4) {
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const uint32_t t = ((x[i + k] >> 2) ^ x[i + k + 2]) & 0x33333333u;
+            x[i + k + 2] ^= t;
+            x[i + k] ^= t << 2;
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 8; i += 2) {
+        const uint32_t t = ((x[i] >> 1) ^ x[i + 1]) & 0x55555555u;
+        x[i + 1] ^= t;
+        x[i] ^= t << 1;
+    }
+}
+
+// Ordered form: acc[q] += (bit q of half) ? -s : +s for the lane's 16
 // elements, one fp32 addition per element and worker in worker order: the
 // bit is moved to the sign position (v_lshlrev) and spliced into s (v_bfi).
-__device__ __forceinline__ void sign_word_accumulate(float (&acc)[32], uint32_t word, float s) {
+__device__ __forceinline__ void sign_half_accumulate(float (&acc)[16], uint32_t half, float s) {
     const uint32_t su = f2u(s);
     const uint32_t sign = 0x80000000u;
 #pragma unroll
-    for (int q = 0; q < 32; ++q) {
-        const uint32_t t = word << (31 - q);
+    for (int q = 0; q < 16; ++q) {
+        const uint32_t t = half << (31 - q);
         uint32_t d;
         asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(d) : "v"(sign), "v"(t), "v"(su));
         acc[q] += u2f(d);
     }
 }
 
-}  // namespace
+// Integer image of a scale for the 32-bit exact form: the scale as a
+// multiple of 2^(emin - 150), the unit in the last place of the smallest
+// normal scale of the tensor (zero stays zero).
+__device__ __forceinline__ int32_t scale_units(float s, int emin) {
+    const uint32_t b = f2u(s);
+    const int e = (int)((b >> 23) & 255u);
+    if (e == 0) return 0;
+    const int32_t m = (int32_t)(((b & 0x7FFFFFu) | 0x800000u) << (e - emin));
+    return (b >> 31) ? -m : m;
+}
 
-// Each workgroup owns 8192 output elements of one tensor: lane l the 32
-// elements of word l of the workgroup's 256-word block (one coalesced
-// 1 KiB load per worker).
-//
-// Exact form (scale exponents within span_limit binades, all finite and
-// normal or zero): every partial sum of the decoded values is exact in
-// fp64.  Workers are taken eight at a time; the 256 possible sums of a
-// group's eight +-s_w are tabulated in LDS (fp64), the eight sign bits of an
-// element form the table index, and the fp64 sum of the group entries is
-// the exact sum, rounded once to fp32 at the end.  The eight words of a
-// group are transposed into per-element bytes with rotate/and-or steps that
-// each serve four elements.
-//
-// Ordered form (otherwise): worker-ordered fp32 additions.
-__global__ __launch_bounds__(kBlock) void aggregate_sign(const ADesc* __restrict__ a, int T,
-                                                         uint32_t U, const WDesc* __restrict__ wd,
-                                                         int W, float alpha, int span_limit) {
-    __shared__ double tab[8 * 256];
-    __shared__ float sc[1024];
-    __shared__ int emin_sh, emax_sh, bad_sh;
-    const uint32_t u = blockIdx.x;
-    const int t = unit_owner(wd, W, u);
-    const ADesc ad = a[t];
-    const uint32_t j = u - ad.unit0;
-    const uint32_t wi = j * 256u + threadIdx.x;  // word of the tensor this lane owns
-    const bool has = wi < ad.k;
-    const uint64_t woff = ad.off + wi;
+// Tables of groups g .. g+7 (g a multiple of 8): tab[256 gi + p] = sum over
+// the eight workers 8(g+gi)+c of (bit c of p ? -s : +s), each entry the sum
+// of two four-worker entries sub[32 gi + 16 hh + p'].  Workers past W count
+// as zero.  Called by the whole workgroup.
+template <typename Acc>
+__device__ __forceinline__ void build_tables(int g, int W, const float* sc, int emin, Acc* tab, Acc* sub) {
+    __syncthreads();  // earlier lookups are done with the tables
+    {
+        const int x = threadIdx.x;  // kBlock == 8 * 32 entries
+        const int w0 = 8 * (g + (x >> 5)) + 4 * ((x >> 4) & 1), pat = x & 15;
+        Acc acc = (Acc)0;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            Acc sv = (Acc)0;
+            if (w0 + c < W) {
+                if constexpr (sizeof(Acc) == 4) sv = scale_units(sc[w0 + c], emin);
+                else sv = (double)sc[w0 + c];
+            }
+            acc += ((pat >> c) & 1) ? -sv : sv;
+        }
+        sub[x] = acc;
+    }
+    __syncthreads();
+    for (int x = threadIdx.x; x < 8 * 256; x += kBlock) {
+        const int gi = x >> 8, pat = x & 255;
+        tab[x] = sub[32 * gi + (pat & 15)] + sub[32 * gi + 16 + (pat >> 4)];
+    }
+    __syncthreads();
+}
+
+// One step: add the table entries of groups g and g+1 for the lane's 16
+// elements.  w[jj] is worker 8g+jj's word, w[8+jj] worker 8(g+1)+jj's.
+// v_perm packs the lane's half-word of each pair (selectors 0-3 pick bytes
+// of the second operand, 4-7 of the first): low half <- group g, high half
+// <- group g+1; after the bit-matrix transpose byte r of idx4[q] holds, at
+// bit jj, worker 8(g + (r>>1)) + jj's bit for element q + 8 (r & 1) of the
+// half.
+template <typename Acc>
+__device__ __forceinline__ void lookup_step(Acc (&S)[16], const uint32_t* w, uint32_t sel,
+                                            const Acc* tab, int g) {
+    uint32_t idx4[8];
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) idx4[jj] = __builtin_amdgcn_perm(w[8 + jj], w[jj], sel);
+    transpose_bytes8(idx4);
+    const Acc* ta = tab + (g & 7) * 256;
+    const Acc* tb = ta + 256;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        S[q] += ta[idx4[q] & 255u];
+        S[q + 8] += ta[(idx4[q] >> 8) & 255u];
+        S[q] += tb[(idx4[q] >> 16) & 255u];
+        S[q + 8] += tb[idx4[q] >> 24];
+    }
+}
+
+// Scales of tensor t into sc[] and its form: 0 ordered, 1 int32 exact,
+// 2 fp64 exact; emin = smallest biased exponent of its normal scales.
+__device__ __forceinline__ void tensor_form(const uint64_t* __restrict__ wp, int W, int t, float* sc,
+                                            int* emin_sh, int* emax_sh, int* bad_sh, int span_limit,
+                                            int int_span_limit, int& form, int& emin) {
+    __syncthreads();  // the previous tensor's scales and tables are done with
     if (threadIdx.x == 0) {
-        emin_sh = 1000;
-        emax_sh = -1000;
-        bad_sh = 0;
+        *emin_sh = 1000;
+        *emax_sh = -1000;
+        *bad_sh = 0;
     }
     __syncthreads();
     for (int w = threadIdx.x; w < W; w += kBlock) {
-        const float sv = ((cf32p)wd[w].b)[t];
+        const float sv = ((cf32p)w_b(wp, W, w))[t];
         sc[w] = sv;
         const uint32_t e = (f2u(sv) >> 23) & 255u;
-        if (e == 255u || (e == 0u && (f2u(sv) & 0x7FFFFFu))) atomicOr(&bad_sh, 1);
+        if (e == 255u || (e == 0u && (f2u(sv) & 0x7FFFFFu))) atomicOr(bad_sh, 1);
         else if (e) {
-            atomicMin(&emin_sh, (int)e);
-            atomicMax(&emax_sh, (int)e);
+            atomicMin(emin_sh, (int)e);
+            atomicMax(emax_sh, (int)e);
         }
     }
     __syncthreads();
-    const bool exact = !bad_sh && (emax_sh < emin_sh || emax_sh - emin_sh <= span_limit);
-    const uint32_t e0 = wi * 32u;
+    const int span = *emax_sh < *emin_sh ? 0 : *emax_sh - *emin_sh;
+    form = *bad_sh ? 0 : span <= int_span_limit ? 1 : span <= span_limit ? 2 : 0;
+    emin = *emax_sh < *emin_sh ? 1 : *emin_sh;
+}
+
+__device__ __forceinline__ void store16(const ADesc& ad, uint32_t e0, const float (&res)[16]) {
     float* out = ad.out + e0;
-    float res[32];
-    if (exact) {
-        double S[32];
+    if (e0 + 16u <= ad.n) {
 #pragma unroll
-        for (int q = 0; q < 32; ++q) S[q] = 0.0;
-        const int G = (W + 7) / 8;
-        for (int g0 = 0; g0 < G; g0 += 8) {
-            __syncthreads();
-            for (int x = threadIdx.x; x < 8 * 256; x += kBlock) {
-                const int gi = g0 + (x >> 8), pat = x & 255;
-                double acc = 0.0;
-                if (gi < G) {
-#pragma unroll
-                    for (int jj = 0; jj < 8; ++jj) {
-                        const int w = 8 * gi + jj;
-                        const double sv = w < W ? (double)sc[w] : 0.0;
-                        acc += ((pat >> jj) & 1) ? -sv : sv;
-                    }
-                }
-                tab[x] = acc;
-            }
-            __syncthreads();
-            const int gend = (G - g0) < 8 ? (G - g0) : 8;
-            for (int gg = 0; gg < gend; ++gg) {
-                const int wbase = 8 * (g0 + gg);
-                uint32_t idx4[8];
-#pragma unroll
-                for (int q = 0; q < 8; ++q) idx4[q] = 0u;
-#pragma unroll
-                for (int jj = 0; jj < 8; ++jj) {
-                    const int w = wbase + jj;
-                    const uint32_t word = (has && w < W) ? gp(wd[w].a)[woff] : 0u;
-                    const uint32_t m = 0x01010101u << jj;
-                    // rotate bits q, q+8, q+16, q+24 of the word to jj, jj+8,
-                    // jj+16, jj+24 (v_alignbit), then mask them in (v_and_or)
-#pragma unroll
-                    for (int q = 0; q < 8; ++q)
-                        idx4[q] |= __builtin_amdgcn_alignbit(word, word, (uint32_t)((q - jj) & 31)) & m;
-                }
-                const double* tb = tab + gg * 256;
-#pragma unroll
-                for (int q = 0; q < 32; ++q) S[q] += tb[(idx4[q & 7] >> (8 * (q >> 3))) & 255u];
-            }
-        }
-#pragma unroll
-        for (int q = 0; q < 32; ++q) res[q] = alpha * (float)S[q];
-    } else {
-        float acc[32];
-#pragma unroll
-        for (int q = 0; q < 32; ++q) acc[q] = 0.f;
-        for (int w0 = 0; w0 < W; w0 += kSignGroup) {
-            uint32_t word[kSignGroup];
-            float sv[kSignGroup];
-#pragma unroll
-            for (int g = 0; g < kSignGroup; ++g) {
-                const int w = w0 + g < W ? w0 + g : W - 1;
-                sv[g] = sc[w];
-                word[g] = has ? gp(wd[w].a)[woff] : 0u;
-            }
-#pragma unroll
-            for (int g = 0; g < kSignGroup; ++g)
-                if (w0 + g < W) sign_word_accumulate(acc, word[g], sv[g]);
-        }
-#pragma unroll
-        for (int q = 0; q < 32; ++q) res[q] = alpha * acc[q];
-    }
-    if (!has) return;
-    if (e0 + 32u <= ad.n) {
-#pragma unroll
-        for (int q = 0; q < 32; q += 4)
-            stg4f(out + q, f32x4{res[q], res[q + 1], res[q + 2], res[q + 3]});
+        for (int q = 0; q < 16; q += 4) stg4f(out + q, f32x4{res[q], res[q + 1], res[q + 2], res[q + 3]});
     } else {
 #pragma unroll
-        for (int q = 0; q < 32; ++q)
+        for (int q = 0; q < 16; ++q)
             if (e0 + q < ad.n) gp(out)[q] = res[q];
+    }
+}
+
+}  // namespace
+
+// Units of 4096 output elements (128 words of one tensor) are split into
+// gridDim.x contiguous ranges, one per workgroup; a workgroup walks its
+// range in order and reloads the scales (and rebuilds its tables) only when
+// the tensor changes.  Within a unit, lanes 2i and 2i+1 share word i, each
+// taking 16 of its elements (half h = lane parity covers elements
+// 16h .. 16h+15 of the word).
+//
+// Exact forms: workers are taken in groups of eight; the 256 possible sums
+// of a group's eight +-s_w are tabulated in LDS, the eight sign bits of an
+// element form the table index, and the sum of the group entries is the
+// exact sum, rounded once to fp32 at the end.  When the scales' exponents
+// span at most int_span_limit binades every scale is an integer multiple of
+// 2^(emin-150) below 2^(24+span), and the whole sum stays below 2^31 in
+// those units: tables and sums are int32.  Up to span_limit binades they
+// are fp64 (every partial sum exact).  Worker slots past W (up to the
+// padded descriptor count) read worker W-1's words; their table terms are
+// zero, so those bits select nothing.
+//
+// Ordered form (non-finite or subnormal scales, or a span beyond
+// span_limit): worker-ordered fp32 additions.
+//
+// aggregate_sign computes the int32 and ordered forms and marks tensors of
+// the fp64 form in wide[t]; the words of its first kS steps (16 kS workers)
+// are requested together at the start of a unit, so each wave keeps up to
+// 64 loads in flight.  aggregate_sign_wide, launched next on the same
+// stream over the same ranges, computes the marked tensors; the fp64 form
+// needs many more registers, and keeping it in its own kernel leaves the
+// common forms their occupancy.
+template <int kS>
+__global__ __launch_bounds__(kBlock) void aggregate_sign(const ADesc* __restrict__ a, int T, uint32_t U,
+                                                         const uint64_t* __restrict__ wp, int W,
+                                                         float alpha, int span_limit, int int_span_limit,
+                                                         uint32_t* __restrict__ wide) {
+    __shared__ int32_t tab[8 * 256];
+    __shared__ int32_t sub[8 * 32];
+    __shared__ float sc[1024];
+    __shared__ int emin_sh, emax_sh, bad_sh;
+    const uint32_t h = threadIdx.x & 1u;
+    const uint32_t lw = threadIdx.x >> 1;
+    const uint32_t sel = h ? 0x07060302u : 0x05040100u;
+    const int G = (W + 7) / 8;
+    const uint32_t ub = (uint32_t)((uint64_t)blockIdx.x * U / gridDim.x);
+    const uint32_t ue = (uint32_t)((uint64_t)(blockIdx.x + 1) * U / gridDim.x);
+    int t_cur = -1, form = 0, emin = 0;
+    bool tab_ok = false;
+    for (uint32_t u = ub; u < ue; ++u) {
+        const int t = unit_owner(wp, W, u);
+        const ADesc ad = a[t];
+        const uint32_t wi = (u - ad.unit0) * (kSignAggUnit / 32u) + lw;  // word of the tensor
+        const bool has = wi < ad.k;
+        // lanes past the tensor read its first word (their sums are dropped)
+        const uint32_t wload = (uint32_t)(ad.off + (has ? wi : 0u)) * 4u;
+        if (t != t_cur) {
+            tensor_form(wp, W, t, sc, &emin_sh, &emax_sh, &bad_sh, span_limit, int_span_limit, form, emin);
+            t_cur = t;
+            tab_ok = false;
+            if (threadIdx.x == 0) wide[t] = form == 2 ? 1u : 0u;
+        }
+        if (form == 2) continue;  // aggregate_sign_wide writes this unit
+        float res[16];
+        if (form == 1) {
+            // 16 kS <= 16 ceil(G / 2) = Wp: every slot read here exists
+            uint32_t wv[16 * kS];
+#pragma unroll
+            for (int jj = 0; jj < 16 * kS; ++jj) wv[jj] = ld_word(w_a(wp, jj), wload);
+            int32_t S[16];
+#pragma unroll
+            for (int q = 0; q < 16; ++q) S[q] = 0;
+            if (!tab_ok) build_tables<int32_t>(0, W, sc, emin, tab, sub);
+            tab_ok = G <= 8;  // one batch holds every group: keep it
+#pragma unroll
+            for (int st = 0; st < kS; ++st)
+                if (2 * st < G) lookup_step<int32_t>(S, wv + 16 * st, sel, tab, 2 * st);
+            for (int g = 2 * kS; g < G; g += 2) {  // more than 16 kS workers
+                if ((g & 7) == 0) build_tables<int32_t>(g, W, sc, emin, tab, sub);
+                uint32_t w16[16];
+#pragma unroll
+                for (int jj = 0; jj < 16; ++jj) w16[jj] = ld_word(w_a(wp, 8 * g + jj), wload);
+                lookup_step<int32_t>(S, w16, sel, tab, g);
+            }
+            // exact: |S| < 2^31 and the unit is a power of two
+            const double unit = __builtin_ldexp(1.0, emin - 150);
+#pragma unroll
+            for (int q = 0; q < 16; ++q) res[q] = alpha * (float)((double)S[q] * unit);
+        } else {
+            float acc[16];
+#pragma unroll
+            for (int q = 0; q < 16; ++q) acc[q] = 0.f;
+            for (int w0 = 0; w0 < W; w0 += kSignGroup) {
+                uint32_t word[kSignGroup];
+                float sv[kSignGroup];
+#pragma unroll
+                for (int g = 0; g < kSignGroup; ++g) {
+                    const int w = w0 + g < W ? w0 + g : W - 1;
+                    sv[g] = sc[w];
+                    word[g] = ld_word(w_a(wp, w), wload);
+                }
+#pragma unroll
+                for (int g = 0; g < kSignGroup; ++g)
+                    if (w0 + g < W) sign_half_accumulate(acc, word[g] >> (16u * h), sv[g]);
+            }
+#pragma unroll
+            for (int q = 0; q < 16; ++q) res[q] = alpha * acc[q];
+        }
+        if (has) store16(ad, wi * 32u + 16u * h, res);
+    }
+}
+
+// fp64 exact form for the tensors aggregate_sign marked; one step's words
+// load while the previous step's lookups run.
+__global__ __launch_bounds__(kBlock) void aggregate_sign_wide(const ADesc* __restrict__ a, int T, uint32_t U,
+                                                              const uint64_t* __restrict__ wp, int W,
+                                                              float alpha, int span_limit,
+                                                              int int_span_limit,
+                                                              const uint32_t* __restrict__ wide) {
+    __shared__ double tab[8 * 256];
+    __shared__ double sub[8 * 32];
+    __shared__ float sc[1024];
+    __shared__ int emin_sh, emax_sh, bad_sh;
+    const uint32_t h = threadIdx.x & 1u;
+    const uint32_t lw = threadIdx.x >> 1;
+    const uint32_t sel = h ? 0x07060302u : 0x05040100u;
+    const int G = (W + 7) / 8;
+    const uint32_t ub = (uint32_t)((uint64_t)blockIdx.x * U / gridDim.x);
+    const uint32_t ue = (uint32_t)((uint64_t)(blockIdx.x + 1) * U / gridDim.x);
+    int t_cur = -1, form = 0, emin = 0;
+    bool tab_ok = false;
+    for (uint32_t u = ub; u < ue; ++u) {
+        const int t = unit_owner(wp, W, u);
+        if (((const uint32_t __attribute__((address_space(4)))*)wide)[t] == 0u) continue;
+        const ADesc ad = a[t];
+        const uint32_t wi = (u - ad.unit0) * (kSignAggUnit / 32u) + lw;
+        const bool has = wi < ad.k;
+        const uint32_t wload = (uint32_t)(ad.off + (has ? wi : 0u)) * 4u;
+        if (t != t_cur) {
+            tensor_form(wp, W, t, sc, &emin_sh, &emax_sh, &bad_sh, span_limit, int_span_limit, form, emin);
+            t_cur = t;
+            tab_ok = false;
+        }
+        double S[16];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) S[q] = 0.0;
+        uint32_t w16[16];
+#pragma unroll
+        for (int jj = 0; jj < 16; ++jj) w16[jj] = ld_word(w_a(wp, jj), wload);
+        for (int g = 0; g < G; g += 2) {
+            if ((g & 7) == 0 && !tab_ok) {
+                build_tables<double>(g, W, sc, emin, tab, sub);
+                tab_ok = G <= 8;
+            }
+            uint32_t cur[16];
+#pragma unroll
+            for (int jj = 0; jj < 16; ++jj) cur[jj] = w16[jj];
+            if (g + 2 < G) {
+#pragma unroll
+                for (int jj = 0; jj < 16; ++jj) w16[jj] = ld_word(w_a(wp, 8 * (g + 2) + jj), wload);
+            }
+            lookup_step<double>(S, cur, sel, tab, g);
+        }
+        float res[16];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) res[q] = alpha * (float)S[q];
+        if (has) store16(ad, wi * 32u + 16u * h, res);
     }
 }
 
@@ -351,7 +539,7 @@ __global__ __launch_bounds__(kBlock) void sparse_residual_update(const TDesc* __
 }
 
 // -------------------------------------------------------------- launchers
-hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t U, const WDesc* w, int W,
+hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W,
                                    float alpha, hipStream_t s) {
     if (U == 0) return hipSuccess;
     // enough waves to fill the chip several times over; each owns ~U/waves tiles
@@ -362,14 +550,34 @@ hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t U, const WDes
     return hipGetLastError();
 }
 
-hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t U, const WDesc* w, int W,
-                                 float alpha, hipStream_t s) {
+hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W,
+                                 float alpha, uint32_t* wide, uint32_t max_blocks, hipStream_t s) {
     if (U == 0) return hipSuccess;
     int lg = 0;
     while ((1 << lg) < W) ++lg;
     const int span_limit = 29 - lg;  // 24 + span + ceil(log2 W) <= 53
-    hipLaunchKernelGGL(aggregate_sign, dim3(U), dim3(kBlock), 0, s, a, T, U, w, W, alpha, span_limit);
+    const int G = (W + 7) / 8;
+    int lg8 = 0;
+    while ((1 << lg8) < 8 * G) ++lg8;
+    const int int_span_limit = 7 - lg8;  // 24 + span + ceil(log2 8G) <= 31
+    const uint32_t blocks = U < max_blocks ? U : max_blocks;
+    const int steps = (G + 1) / 2;
+    const dim3 grid(blocks), block(kBlock);
+    if (steps <= 1)
+        hipLaunchKernelGGL(aggregate_sign<1>, grid, block, 0, s, a, T, U, w, W, alpha, span_limit, int_span_limit, wide);
+    else if (steps == 2)
+        hipLaunchKernelGGL(aggregate_sign<2>, grid, block, 0, s, a, T, U, w, W, alpha, span_limit, int_span_limit, wide);
+    else if (steps == 3)
+        hipLaunchKernelGGL(aggregate_sign<3>, grid, block, 0, s, a, T, U, w, W, alpha, span_limit, int_span_limit, wide);
+    else
+        hipLaunchKernelGGL(aggregate_sign<4>, grid, block, 0, s, a, T, U, w, W, alpha, span_limit, int_span_limit, wide);
+    hipLaunchKernelGGL(aggregate_sign_wide, grid, block, 0, s, a, T, U, w, W, alpha, span_limit, int_span_limit,
+                       (const uint32_t*)wide);
     return hipGetLastError();
+}
+
+hipError_t aggregate_sign_occupancy(int* blocks_per_cu) {
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, aggregate_sign<4>, kBlock, 0);
 }
 
 hipError_t launch_sign_residual_update(const TDesc* d, int T, uint32_t C, const uint32_t* bits,

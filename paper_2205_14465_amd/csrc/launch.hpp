@@ -20,6 +20,7 @@ struct Ws {
     uint32_t* s_ready;      // [T] 64-bit words: bit 32 = published, low 32 = scale     
     float* s_val;           // [T] published scales
     double* s_partial;      // [C] per-chunk sums of |v|
+    uint32_t* s_wide;       // [T] aggregate: 1 = tensor takes the fp64 exact form
     // BC_TOPK, BC_TOPK_SAMPLED
     uint32_t* t_hist;       // [T * 2048] histograms         
     uint32_t* t_thr;        // [T] candidate threshold (key)
@@ -44,7 +45,7 @@ struct Ws {
 // Byte offsets of every region for a call shape; `total` is the workspace
 // size.  Regions a kind does not use have size 0.
 struct WsPlan {
-    size_t flags, s_cnt, s_ready, s_val, s_partial;
+    size_t flags, s_cnt, s_ready, s_val, s_partial, s_wide;
     size_t t_hist, t_thr, t_prefix, t_krem, t_fb, t_cand, t_ccount, t_gt, t_eq, t_off, t_eqb;
     size_t r_keys, r_tmp, r_ccount, r_coff, r_cursor;
     size_t total;
@@ -56,6 +57,7 @@ Ws carve_workspace(void* base, const WsPlan& p);
 struct DevInfo {
     int cus;
     int sign_coop_blocks_per_cu;
+    int agg_sign_blocks_per_cu;
     bool coop_ok;
     bool sign_one_pass;  // BYTECOMP_SIGN_PATH=onepass
     bool any_empty;      // per call: some tensor has no elements
@@ -76,13 +78,17 @@ hipError_t launch_randk(uint64_t seed, const TDesc* d, int T, uint32_t C, uint64
 hipError_t launch_residual_update(int kind, const TDesc* d, int T, uint32_t C, bool any_f16,
                                   bool any_f32, const uint32_t* idx, const float* val,
                                   const uint32_t* bits, const float* scale, hipStream_t s);
-hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t units, const WDesc* w, int W,
+hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t units, const uint64_t* wp, int W,
                                    float alpha, hipStream_t s);
-hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t units, const WDesc* w, int W,
-                                 float alpha, hipStream_t s);
+hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t units, const uint64_t* wp, int W,
+                                 float alpha, uint32_t* wide, uint32_t max_blocks, hipStream_t s);
+hipError_t aggregate_sign_occupancy(int* blocks_per_cu);
 
 // Work-unit sizes of the aggregate kernels (elements per unit).
+// Worker descriptors in the aggregate table are padded to a multiple of 16.
+__host__ __device__ constexpr int padded_workers(int W) { return (W + 15) & ~15; }
+
 constexpr uint32_t kSparseTile = 2048;   // one wave's LDS tile
-constexpr uint32_t kSignAggUnit = 8192;  // one workgroup: 32 elements per lane
+constexpr uint32_t kSignAggUnit = 4096;  // one workgroup: 16 elements per lane
 
 }  // namespace bc

@@ -188,7 +188,7 @@ def test_sparse_aggregate_dense_overlap():
         assert np.array_equal(bits(got[t]), bits(want[t])), t
 
 
-@pytest.mark.parametrize("W", [1, 3, 8, 32, 64, 71, 130])
+@pytest.mark.parametrize("W", [1, 3, 8, 17, 24, 32, 64, 71, 130])
 def test_sign_aggregate_ragged(W):
     rng = np.random.default_rng(31 + W)
     ns = [1, 31, 32, 33, 511, 512, 513, 2047, 2048, 2049, 8191, 8192, 8193, 8192 * 2 + 7, 100001, 0]
@@ -226,6 +226,68 @@ def test_sign_aggregate_wide_scale_span_takes_ordered_form(W):
     want = O.aggregate_set("sign", ns, payloads, 1.0)
     for t in range(len(ns)):
         assert np.array_equal(bits(got[t]), bits(want[t])), t
+
+
+def _scales_with_span(rng, W, span):
+    """W fp32 scales near 1e-3 whose binary exponents span exactly `span`
+    binades (worker 0 at the low end, worker 1 at the high end)."""
+    base = np.float32(2.0 ** -10)
+    s = (base * (1 + rng.random(W))).astype(np.float32)  # exponent -10
+    if W >= 2:
+        s[0] = base * np.float32(1.25)
+        s[1] = np.float32(base * np.float32(2.0 ** span) * np.float32(1.5))
+    return s
+
+
+@pytest.mark.parametrize("W", [8, 32, 64, 71, 128, 130])
+def test_sign_aggregate_exact_forms_by_scale_span(W):
+    # one call whose tensors fall in every form: int32 tables (spans up to
+    # 7 - ceil(log2(8 ceil(W/8)))), fp64 tables (up to 29 - ceil(log2 W)),
+    # and the worker-ordered sum beyond; results match the oracle bit for bit
+    rng = np.random.default_rng(51 + W)
+    limit = O.sign_span_limit(W)
+    int_limit = 7 - int(np.ceil(np.log2(8 * ((W + 7) // 8))))
+    spans = sorted({0, 1, max(int_limit, 0), int_limit + 1, limit - 1, limit, limit + 1, limit + 5})
+    spans = [sp for sp in spans if sp >= 0]
+    ns = [4096 * 3 + 77 if i % 2 == 0 else 5000 + 31 * i for i in range(len(spans))]
+    wc = [O.words_for(n) for n in ns]
+    per_t = [_scales_with_span(rng, W, sp) for sp in spans]
+    payloads = []
+    for w in range(W):
+        words = WL.random_sign_words(rng, ns, wc)
+        payloads.append({"bits": np.concatenate(words),
+                         "scale": np.array([per_t[t][w] for t in range(len(ns))], np.float32),
+                         "off": O.word_offsets(ns)})
+    for t, sp in enumerate(spans):
+        assert O.sign_exact_applies(per_t[t]) == (sp <= limit), (t, sp)
+    got = gpu_aggregate("sign", 0.01, ns, payloads, 1.0 / W)
+    want = O.aggregate_set("sign", ns, payloads, 1.0 / W)
+    for t in range(len(ns)):
+        assert np.array_equal(bits(got[t]), bits(want[t])), (t, spans[t])
+
+
+@pytest.mark.parametrize("W", [32, 64, 128])
+def test_sign_aggregate_integer_form_extremes(W):
+    # largest sums the int32 form admits: every scale at the top of the
+    # widest span it takes, all signs equal (both polarities) and mixed
+    int_limit = 7 - int(np.ceil(np.log2(8 * ((W + 7) // 8))))
+    top = np.float32(np.nextafter(np.float32(2.0 ** (-9 + int_limit)), np.float32(0)))
+    scales = np.full(W, top, np.float32)
+    scales[0] = np.float32(2.0 ** -10)  # sets emin, so the span is int_limit
+    ns = [4096 + 64, 4096 + 64, 777]
+    wc = [O.words_for(n) for n in ns]
+    rng = np.random.default_rng(61)
+    payloads = []
+    for w in range(W):
+        words = [np.zeros(wc[0], np.uint32), np.full(wc[1], 0xFFFFFFFF, np.uint32),
+                 WL.random_sign_words(rng, [ns[2]], [wc[2]])[0]]
+        words[1][-1] &= np.uint32((1 << (ns[1] % 32)) - 1) if ns[1] % 32 else np.uint32(0xFFFFFFFF)
+        payloads.append({"bits": np.concatenate(words), "scale": scales.copy(), "off": O.word_offsets(ns)})
+    got = gpu_aggregate("sign", 0.01, ns, payloads, 1.0)
+    want = O.aggregate_set("sign", ns, payloads, 1.0)
+    for t in range(len(ns)):
+        assert np.array_equal(bits(got[t]), bits(want[t])), t
+    assert np.all(got[0] > 0) and np.all(got[1] < 0)
 
 
 # ---------------------------------------------------- residual update (API)

@@ -161,14 +161,14 @@ def source_digest(files):
     return h.hexdigest()
 
 
-def counted_traffic(kernel, workload_name):
+def counted_traffic(kernel, slug):
     """HBM bytes per launch of `kernel` counted by rocprofv3 (FETCH_SIZE and
     WRITE_SIZE, each in its own run), scaled by what the same counters read
     for the 1 GiB read + 1 GiB write calibration pass.  The figures live in
-    profiles/traffic_<kernel>_<workload>.txt on a line starting 'TRAFFIC ';
+    profiles/traffic_<kernel>_<workload slug>.txt on a line starting 'TRAFFIC ';
     they are dropped (None) once the kernel's sources differ from the ones
     the counters were taken on."""
-    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload_name}.txt")
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{slug}.txt")
     if not os.path.exists(path):
         return None
     rec = None
@@ -285,10 +285,13 @@ def main():
     agg_kernel = "aggregate_sparse" if kind != "sign" else "aggregate_sign"
     if agg_avg >= comp_avg:
         dom = {"kernel": agg_kernel, "bytes": agg_b, "ms": agg_avg}
+        if kind == "sign":
+            dom["note"] = ("event span of the aggregate call: aggregate_sign, then "
+                           "aggregate_sign_wide (tensors of the fp64 form only)")
     else:
         dom = {"kernel": f"compress call ({kind})", "bytes": comp_b, "ms": comp_avg}
     achieved = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
-    traffic = counted_traffic(dom["kernel"], wl.name)
+    traffic = counted_traffic(dom["kernel"], wl.slug)
     line = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -315,7 +318,7 @@ def main():
         "copy_gbs_reference": round(copy_gbs, 1),
         "roofline": {"bound": "hbm", "kernel": dom["kernel"], "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": traffic},
+                     "traffic": traffic, **({"note": dom["note"]} if "note" in dom else {})},
     }
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")

@@ -118,7 +118,8 @@ int bytecomp_workspace_size(int kind, double ratio, const uint64_t* n, int T, in
 /* Zero a workspace (enqueued on `stream`).  A workspace must be zero
  * before its first use; every successful call leaves the counters it used
  * at zero again, so one initialisation suffices.  Re-initialise after a
- * call that failed inside a kernel. */
+ * call that failed inside a kernel.  Calls that share a workspace must be
+ * ordered (one stream, or synchronised streams): they race otherwise. */
 int bytecomp_workspace_init(void* ws, size_t ws_bytes, void* stream);
 
 /* Compress T tensors with error feedback (paper Sec. 2.3, Sec. 5.1).
@@ -145,10 +146,19 @@ int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t,
  *   in     host array of W payloads (device pointers), same layout for all
  *   n      host, T element counts
  *   out    host array of T device pointers to dense fp32 outputs
+ *          (16-byte aligned)
  *   alpha  scale applied to each sum (1 = sum, 1/W = mean)
- * out_t[i] = alpha * (sum over workers w = 0..W-1, in that order, of the
- * decoded value of worker w at i), each addition in fp32, starting from
- * +0.0; elements no worker sent are alpha * 0. */
+ *   ws     workspace: BC_SIGN1 needs bytecomp_workspace_size bytes (it keeps
+ *          one flag per tensor there); sparse kinds need its 256-byte header
+ * Sparse kinds: out_t[i] = alpha * (sum over workers w = 0..W-1, in that
+ * order, of worker w's value at i), each addition in fp32 starting from
+ * +0.0; elements no worker sent are alpha * 0.
+ * BC_SIGN1: out_t[i] = alpha * fl32(exact sum over w of d_w,i), d_w,i =
+ * -s_w,t if worker w's bit i is set, else +s_w,t: the exact real sum
+ * rounded once to fp32.  This form applies when tensor t's W scales are
+ * finite and normal or zero and their binary exponents span at most
+ * 29 - ceil(log2 W) binades; otherwise the worker-ordered fp32 sum, as for
+ * the sparse kinds.  Results are deterministic. */
 int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, int W,
                                   const uint64_t* n, int T, float* const* out, float alpha,
                                   void* ws, size_t ws_bytes, void* stream);

@@ -117,6 +117,12 @@ class Workload:
     def n_total(self):
         return int(sum(self.sizes))
 
+    @property
+    def slug(self):
+        """Short file-name form of the workload."""
+        return {1: "single2p20_topk_w8", 2: "resnet50_sign_w64", 3: "bertbase_topksampled_w64",
+                4: "gpt2xl_randk_w16", 5: "small4096_fp16sign_w32"}[self.wid]
+
 
 def workload(wid: int, shrink: int = 1) -> Workload:
     """The five measured workloads; `shrink` > 1 divides every tensor size

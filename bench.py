@@ -49,52 +49,6 @@ def algorithmic_bytes(wl, off, kind):
     return comp, agg, payload
 
 
-HOST_GEN_LIMIT = 200_000_000  # elements; larger workloads draw their inputs on the device
-
-
-def make_inputs(wl, off, device):
-    import torch
-    from paper_2205_14465_amd import workloads as WL
-    kind = wl.kind
-    on_device = wl.n_total > HOST_GEN_LIMIT
-    tdt = torch.float16 if wl.grad_dtype == "float16" else torch.float32
-    # gradients and residuals live in one flat buffer each, tensors as views
-    # at 256-byte aligned offsets (as a framework's gradient buckets would)
-    starts, pos = [], 0
-    for n in wl.sizes:
-        starts.append(pos)
-        pos += (n + 63) // 64 * 64
-    g_flat = torch.empty(pos, dtype=tdt, device=device)
-    e_flat = torch.empty(pos, dtype=torch.float32, device=device)
-    gen = WL._torch_gen(device, wl.wid, 0, WL.ROLE_G) if on_device else None
-    for t, n in enumerate(wl.sizes):
-        if on_device:
-            WL.device_gradient(wl, t, g_flat[starts[t]:starts[t] + n], gen)
-            WL.device_residual(wl, t, e_flat[starts[t]:starts[t] + n], gen)
-        else:
-            g_flat[starts[t]:starts[t] + n].copy_(torch.from_numpy(WL.gradient(wl, t)))
-            e_flat[starts[t]:starts[t] + n].copy_(torch.from_numpy(WL.residual(wl, t)))
-    grads = [g_flat[s:s + n] for s, n in zip(starts, wl.sizes)]
-    resids = [e_flat[s:s + n] for s, n in zip(starts, wl.sizes)]
-    counts = [int(off[t + 1] - off[t]) for t in range(wl.T)]
-    payloads = []
-    for w in range(wl.W):
-        if kind == "sign":
-            b, s = WL.sign_payload(wl, w, counts, off)
-            payloads.append({"bits": torch.from_numpy(b.view(np.int32)).to(device),
-                             "scale": torch.from_numpy(s).to(device)})
-        elif on_device:
-            i, v = WL.device_sparse_payload(wl, w, counts, off, device)
-            payloads.append({"idx": i, "val": v})
-        else:
-            i, v = WL.sparse_payload(wl, w, counts, off)
-            payloads.append({"idx": torch.from_numpy(i.view(np.int32)).to(device),
-                             "val": torch.from_numpy(v).to(device)})
-    out_flat = torch.empty(pos, dtype=torch.float32, device=device)
-    outs = [out_flat[s:s + n] for s, n in zip(starts, wl.sizes)]
-    return grads, resids, payloads, outs
-
-
 def cpu_baseline(wl, off, budget_s=15.0):
     """Time the oracle (one thread) on a bounded sample of the workload:
     whole tensors in workload order until ~budget_s of compress work, and
@@ -215,7 +169,7 @@ def main():
     kind = wl.kind
     off = B.bytecomp_layout(kind, wl.ratio, wl.sizes)
     log(f"workload {wl.wid}: {wl.name}; generating inputs")
-    grads, resids, payloads, outs = make_inputs(wl, off, dev)
+    grads, resids, payloads, outs = WL.device_inputs(wl, off, dev)
     own = B.alloc_payload(kind, wl.ratio, wl.sizes, device=dev)
     ws = B.alloc_workspace(kind, wl.ratio, wl.sizes, wl.W, device=dev)
     comp_b, agg_b, pay_b = algorithmic_bytes(wl, off, kind)

@@ -60,8 +60,8 @@ __device__ __forceinline__ uint32_t lower_bound_u32(const uint32_t* idx, uint32_
 // (slot w % kSparseSlots holds worker w): as soon as a worker's entries for
 // the tile have been added, its slot is refilled with the worker that comes
 // kSparseSlots later, or, when W is a multiple of kSparseSlots and the
-// next tile continues the tensor, with the same worker's entries for the
-// next tile (its cursor is then final).
+// next tile continues the tensor, with the entries of the slot's first
+// worker (w % kSparseSlots) for the next tile (its cursor is final by then).
 constexpr int kSparseSlots = 16;
 
 __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restrict__ a, int T,
@@ -147,11 +147,12 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
                 }
                 if (lane == 0) cur[w] = cc;
                 // refill the slot: the worker kSparseSlots later in this
-                // tile, or this worker's entries for the next tile
+                // tile, or else (W a multiple of kSparseSlots) worker q's
+                // entries for the next tile, its cursor being final here
                 const int wn = w + kSparseSlots;
                 const bool later = wn < W;
-                const int wr = later ? wn : w;
-                const uint32_t i = (later ? cur[wn] : cc) + lane;
+                const int wr = later ? wn : wn - W;
+                const uint32_t i = (later ? cur[wn] : (wr == w ? cc : cur[wr])) + lane;
                 const uint32_t ic = i < ad.k ? i : klast;
                 x[q] = gp(w_a(wp, wr))[ad.off + ic];
                 y[q] = gp(w_b(wp, W, wr))[ad.off + ic];

@@ -282,3 +282,52 @@ def device_sparse_payload(wl: Workload, w: int, counts, offs, device):
         idx[offs[t]:offs[t] + k] = lo + torch.floor(u * (hi - lo).to(torch.float64)).to(torch.int64)
         val[offs[t]:offs[t] + k] = torch.randn(k, generator=gen, device=device) * sigma_of(wl, t)
     return idx.to(torch.int32), val
+
+
+HOST_GEN_LIMIT = 200_000_000  # elements; larger workloads draw their inputs on the device
+
+
+def device_inputs(wl, off, device):
+    """Device-resident inputs of a workload: gradients and residuals as views
+    of one flat buffer each (256-byte aligned tensors, as a framework's
+    gradient buckets would be), the W worker payloads and the aggregate
+    outputs.  Workloads above HOST_GEN_LIMIT elements draw on the device."""
+    import torch
+    kind = wl.kind
+    on_device = wl.n_total > HOST_GEN_LIMIT
+    tdt = torch.float16 if wl.grad_dtype == "float16" else torch.float32
+    # gradients and residuals live in one flat buffer each, tensors as views
+    # at 256-byte aligned offsets (as a framework's gradient buckets would)
+    starts, pos = [], 0
+    for n in wl.sizes:
+        starts.append(pos)
+        pos += (n + 63) // 64 * 64
+    g_flat = torch.empty(pos, dtype=tdt, device=device)
+    e_flat = torch.empty(pos, dtype=torch.float32, device=device)
+    gen = _torch_gen(device, wl.wid, 0, ROLE_G) if on_device else None
+    for t, n in enumerate(wl.sizes):
+        if on_device:
+            device_gradient(wl, t, g_flat[starts[t]:starts[t] + n], gen)
+            device_residual(wl, t, e_flat[starts[t]:starts[t] + n], gen)
+        else:
+            g_flat[starts[t]:starts[t] + n].copy_(torch.from_numpy(gradient(wl, t)))
+            e_flat[starts[t]:starts[t] + n].copy_(torch.from_numpy(residual(wl, t)))
+    grads = [g_flat[s:s + n] for s, n in zip(starts, wl.sizes)]
+    resids = [e_flat[s:s + n] for s, n in zip(starts, wl.sizes)]
+    counts = [int(off[t + 1] - off[t]) for t in range(wl.T)]
+    payloads = []
+    for w in range(wl.W):
+        if kind == "sign":
+            b, s = sign_payload(wl, w, counts, off)
+            payloads.append({"bits": torch.from_numpy(b.view(np.int32)).to(device),
+                             "scale": torch.from_numpy(s).to(device)})
+        elif on_device:
+            i, v = device_sparse_payload(wl, w, counts, off, device)
+            payloads.append({"idx": i, "val": v})
+        else:
+            i, v = sparse_payload(wl, w, counts, off)
+            payloads.append({"idx": torch.from_numpy(i.view(np.int32)).to(device),
+                             "val": torch.from_numpy(v).to(device)})
+    out_flat = torch.empty(pos, dtype=torch.float32, device=device)
+    outs = [out_flat[s:s + n] for s, n in zip(starts, wl.sizes)]
+    return grads, resids, payloads, outs

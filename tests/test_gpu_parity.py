@@ -171,6 +171,26 @@ def test_sparse_aggregate_ragged(W):
         assert np.array_equal(bits(got[t]), bits(want[t])), t
 
 
+@pytest.mark.parametrize("W", [16, 32, 48])
+def test_sparse_aggregate_several_tiles_per_wave(W):
+    # a tensor of more than 8192 x 2 tiles, so that waves walk several
+    # consecutive tiles of it and carry their next-tile loads across tiles
+    # (W a multiple of 16)
+    rng = np.random.default_rng(23 + W)
+    ns = [2048 * 16384 * 2 + 777, 5000]
+    ratio = 0.002
+    counts = [O.k_for(n, ratio) for n in ns]
+    payloads = []
+    for w in range(W):
+        idx, val = WL.random_sparse_lists(rng, ns, counts)
+        payloads.append({"idx": np.concatenate(idx), "val": np.concatenate(val),
+                         "off": O.sparse_offsets(ns, ratio)})
+    got = gpu_aggregate("topk", ratio, ns, payloads, 1.0)
+    want = O.aggregate_set("topk", ns, payloads, 1.0)
+    for t in range(len(ns)):
+        assert np.array_equal(bits(got[t]), bits(want[t])), t
+
+
 def test_sparse_aggregate_dense_overlap():
     # every worker sends every index (ratio 1): maximal overlap, long runs
     rng = np.random.default_rng(23)

@@ -241,7 +241,7 @@ def main():
         dom = {"kernel": agg_kernel, "bytes": agg_b, "ms": agg_avg}
         if kind == "sign":
             dom["note"] = ("event span of the aggregate call: aggregate_sign, then "
-                           "aggregate_sign_wide (tensors of the fp64 form only)")
+                           "aggregate_sign_rest (tensors outside the int32 form only)")
     else:
         dom = {"kernel": f"compress call ({kind})", "bytes": comp_b, "ms": comp_avg}
     achieved = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9

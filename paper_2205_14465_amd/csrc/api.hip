@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <atomic>
 #include <mutex>
 #include <new>
 #include <vector>
@@ -163,10 +164,7 @@ hipError_t device_info(int dev, DevInfo* out) {
         e = sign_coop_occupancy(&b);
         if (e != hipSuccess) return e;
         di.sign_coop_blocks_per_cu = b > 0 ? b : 1;
-        b = 0;
-        e = aggregate_sign_occupancy(&b);
-        if (e != hipSuccess) return e;
-        di.agg_sign_blocks_per_cu = b > 0 ? b : 1;
+
         const char* sp = std::getenv("BYTECOMP_SIGN_PATH");
         di.sign_one_pass = sp && std::strcmp(sp, "onepass") == 0;
         di.any_empty = false;
@@ -192,7 +190,8 @@ WsPlan plan_workspace(int kind, int T, uint64_t C, uint64_t sum_k) {
         take(p.s_ready, t * 8);
         take(p.s_val, t * 4);
         take(p.s_partial, (size_t)C * 8);
-        take(p.s_wide, t * 4);
+        take(p.s_info, t ? (t + 1) * 4 : 0);
+        take(p.s_tab, t * 2048 * 4);
     } else if (kind == BC_TOPK || kind == BC_TOPK_SAMPLED) {
         take(p.t_hist, t * kBins0 * 4);
         take(p.t_thr, t * 4);
@@ -227,7 +226,8 @@ Ws carve_workspace(void* base, const WsPlan& p) {
     w.s_ready = (uint32_t*)at(p.s_ready);
     w.s_val = (float*)at(p.s_val);
     w.s_partial = (double*)at(p.s_partial);
-    w.s_wide = (uint32_t*)at(p.s_wide);
+    w.s_info = (uint32_t*)at(p.s_info);
+    w.s_tab = (int32_t*)at(p.s_tab);
     w.t_hist = (uint32_t*)at(p.t_hist);
     w.t_thr = (uint32_t*)at(p.t_thr);
     w.t_prefix = (uint32_t*)at(p.t_prefix);
@@ -433,6 +433,10 @@ int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t,
     return finish(hip_status(e), s, ws);
 }
 
+// Call number stamped by the sign aggregate into its workspace (so a flag
+// from an earlier call never reads as set); 0 is skipped.
+static std::atomic<uint32_t> g_agg_epoch{0};
+
 int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, int W,
                                   const uint64_t* n, int T, float* const* out, float alpha,
                                   void* ws, size_t ws_bytes, void* stream) {
@@ -472,13 +476,13 @@ int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, 
         units += nu;
     }
     if (units >= (1ull << 31)) return BC_E_SIZE;
-    uint32_t* wide = nullptr;  // sign: per-tensor fp64-form flags in the workspace
+    Ws w{};  // sign: per-tensor forms and lookup tables live in the workspace
     if (!sparse) {
         uint64_t C = 0;
         for (int i = 0; i < T; ++i) C += (n[i] + kChunk - 1) / kChunk;
         const WsPlan plan = plan_workspace(kind, T, C, 0);
         if (ws_bytes < plan.total) return BC_E_WORKSPACE;
-        wide = carve_workspace(ws, plan).s_wide;
+        w = carve_workspace(ws, plan);
     }
     // the sign kernel addresses a worker's words with a 32-bit byte offset
     if (!sparse && off >= (1ull << 30)) return BC_E_SIZE;
@@ -516,11 +520,13 @@ int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, 
     if (e != hipSuccess) return BC_E_HIP;
     const ADesc* ad = (const ADesc*)en->dev;
     const uint64_t* wdd = (const uint64_t*)((const char*)en->dev + (size_t)T * sizeof(ADesc));
-    if (sparse)
+    if (sparse) {
         e = launch_aggregate_sparse(ad, T, (uint32_t)units, wdd, W, alpha, s);
-    else
-        e = launch_aggregate_sign(ad, T, (uint32_t)units, wdd, W, alpha, wide,
-                                  (uint32_t)(di.cus * di.agg_sign_blocks_per_cu), s);
+    } else {
+        uint32_t epoch = ++g_agg_epoch;
+        if (epoch == 0) epoch = ++g_agg_epoch;
+        e = launch_aggregate_sign(ad, T, (uint32_t)units, wdd, W, alpha, w.s_info, w.s_tab, epoch, di.cus, s);
+    }
     cache_mark_used(en, s);
     return finish(hip_status(e), s, ws);
 }

@@ -282,6 +282,10 @@ __device__ __forceinline__ void lookup_step(Acc (&S)[16], const uint32_t* w, uin
     uint32_t idx4[8];
 #pragma unroll
     for (int jj = 0; jj < 8; ++jj) idx4[jj] = __builtin_amdgcn_perm(w[8 + jj], w[jj], sel);
+    // pin the packing here (empty asm on its results): the caller reloads
+    // w[] right after this step, and the words must be dead by then
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) asm volatile("" : "+v"(idx4[jj]));
     transpose_bytes8(idx4);
     const Acc* ta = tab + (g & 7) * 256;
     const Acc* tb = ta + 256;
@@ -336,41 +340,186 @@ __device__ __forceinline__ void store16(const ADesc& ad, uint32_t e0, const floa
 
 }  // namespace
 
-// Units of 4096 output elements (128 words of one tensor) are split into
-// gridDim.x contiguous ranges, one per workgroup; a workgroup walks its
-// range in order and reloads the scales (and rebuilds its tables) only when
-// the tensor changes.  Within a unit, lanes 2i and 2i+1 share word i, each
-// taking 16 of its elements (half h = lane parity covers elements
-// 16h .. 16h+15 of the word).
+// Sign aggregate.  A unit is 4096 output elements (128 words) of one
+// tensor; lanes 2i and 2i+1 share word i of the unit, each taking 16 of its
+// elements (half h = lane parity covers elements 16h .. 16h+15 of the word).
 //
 // Exact forms: workers are taken in groups of eight; the 256 possible sums
-// of a group's eight +-s_w are tabulated in LDS, the eight sign bits of an
-// element form the table index, and the sum of the group entries is the
-// exact sum, rounded once to fp32 at the end.  When the scales' exponents
-// span at most int_span_limit binades every scale is an integer multiple of
-// 2^(emin-150) below 2^(24+span), and the whole sum stays below 2^31 in
-// those units: tables and sums are int32.  Up to span_limit binades they
-// are fp64 (every partial sum exact).  Worker slots past W (up to the
-// padded descriptor count) read worker W-1's words; their table terms are
-// zero, so those bits select nothing.
+// of a group's eight +-s_w are tabulated, the eight sign bits of an element
+// form the table index, and the sum of the group entries is the exact sum,
+// rounded once to fp32 at the end.  When a tensor's scales span at most
+// int_span_limit binades every scale is an integer multiple of 2^(emin-150)
+// below 2^(24+span), and the whole sum stays below 2^31 in those units:
+// tables and sums are int32.  Up to span_limit binades they are fp64 (every
+// partial sum exact).  Ordered form (non-finite or subnormal scales, or a
+// wider span): worker-ordered fp32 additions.
 //
-// Ordered form (non-finite or subnormal scales, or a span beyond
-// span_limit): worker-ordered fp32 additions.
-//
-// aggregate_sign computes the int32 and ordered forms and marks tensors of
-// the fp64 form in wide[t]; the words of its first kS steps (16 kS workers)
-// are requested together at the start of a unit, so each wave keeps up to
-// 64 loads in flight.  aggregate_sign_wide, launched next on the same
-// stream over the same ranges, computes the marked tensors; the fp64 form
-// needs many more registers, and keeping it in its own kernel leaves the
-// common forms their occupancy.
+// Three launches: sign_agg_prep (one workgroup per tensor) classifies each
+// tensor and, for up to 64 workers, writes its int32 tables to the
+// workspace; aggregate_sign (one workgroup per unit, in unit order, so that
+// the workgroups resident at a time read neighbouring words of every
+// payload) copies its tensor's tables into LDS and sums the int32-form
+// units; aggregate_sign_rest sums the other units (every unit when W > 64)
+// with fp64 tables or in worker order.  The fp64 form needs many more
+// registers; keeping it apart leaves the common form its occupancy.
+__global__ __launch_bounds__(64) void sign_agg_prep(const ADesc* __restrict__ a, int T,
+                                                    const uint64_t* __restrict__ wp, int W,
+                                                    int span_limit, int int_span_limit,
+                                                    uint32_t* __restrict__ info,
+                                                    int32_t* __restrict__ tabs, int build,
+                                                    uint32_t epoch) {
+    // one wave per tensor
+    __shared__ float sc[1024];
+    __shared__ int32_t sub[8 * 32];
+    const int t = blockIdx.x;
+    if (a[t].nunits == 0) return;
+    const int lane = (int)threadIdx.x;
+    int lo = 1000, hi = -1000, bad = 0;
+    for (int w = lane; w < W; w += 64) {
+        const float sv = ((cf32p)w_b(wp, W, w))[t];
+        sc[w] = sv;
+        const int e = (int)((f2u(sv) >> 23) & 255u);
+        if (e == 255 || (e == 0 && (f2u(sv) & 0x7FFFFFu))) bad = 1;
+        else if (e) {
+            lo = e < lo ? e : lo;
+            hi = e > hi ? e : hi;
+        }
+    }
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) {
+        const int lo2 = __shfl_xor(lo, m, 64), hi2 = __shfl_xor(hi, m, 64);
+        lo = lo2 < lo ? lo2 : lo;
+        hi = hi2 > hi ? hi2 : hi;
+        bad |= __shfl_xor(bad, m, 64);
+    }
+    const int span = hi < lo ? 0 : hi - lo;
+    const int form = bad ? 0 : span <= int_span_limit ? 1 : span <= span_limit ? 2 : 0;
+    const int emin = hi < lo ? 1 : lo;
+    if (lane == 0) {
+        info[t] = (uint32_t)form | ((uint32_t)emin << 8);
+        if (form != 1) info[T] = epoch;  // aggregate_sign_rest has work this call
+    }
+    if (!build || form != 1) return;
+    __builtin_amdgcn_wave_barrier();
+    // sub[32 gi + 16 hh + p]: sum over workers 8 gi + 4 hh + c, c < 4, of
+    // (bit c of p ? -s : +s) in units of 2^(emin-150); zero past W
+    for (int x = lane; x < 8 * 32; x += 64) {
+        const int w0 = 8 * (x >> 5) + 4 * ((x >> 4) & 1), pat = x & 15;
+        int32_t acc = 0;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int32_t sv = w0 + c < W ? scale_units(sc[w0 + c], emin) : 0;
+            acc += ((pat >> c) & 1) ? -sv : sv;
+        }
+        sub[x] = acc;
+    }
+    __builtin_amdgcn_wave_barrier();
+    // tab[256 gi + p] = sub[32 gi + (p & 15)] + sub[32 gi + 16 + (p >> 4)],
+    // four entries per lane and store
+    int32_t* tt = tabs + (size_t)t * 2048;
+    for (int x = 4 * lane; x < 8 * 256; x += 256) {
+        const int gi = x >> 8, p0 = x & 255;
+        const int32_t hi16 = sub[32 * gi + 16 + (p0 >> 4)];
+        u32x4 v;
+        v.x = (uint32_t)(sub[32 * gi + ((p0 + 0) & 15)] + hi16);
+        v.y = (uint32_t)(sub[32 * gi + ((p0 + 1) & 15)] + hi16);
+        v.z = (uint32_t)(sub[32 * gi + ((p0 + 2) & 15)] + hi16);
+        v.w = (uint32_t)(sub[32 * gi + ((p0 + 3) & 15)] + hi16);
+        *(BC_GLOBAL u32x4*)(gp(tt) + x) = v;
+    }
+}
+
 template <int kS>
 __global__ __launch_bounds__(kBlock) void aggregate_sign(const ADesc* __restrict__ a, int T, uint32_t U,
                                                          const uint64_t* __restrict__ wp, int W,
-                                                         float alpha, int span_limit, int int_span_limit,
-                                                         uint32_t* __restrict__ wide) {
-    __shared__ int32_t tab[8 * 256];
-    __shared__ int32_t sub[8 * 32];
+                                                         float alpha, const uint32_t* __restrict__ info,
+                                                         const int32_t* __restrict__ tabs) {
+    // the tables (8 KiB), then, after the last lookup, the unit's 4096
+    // results (16 KiB) on their way to coalesced stores
+    __shared__ __attribute__((aligned(16))) float lds[4096];
+    int32_t* tab = reinterpret_cast<int32_t*>(lds);
+    const uint32_t u = blockIdx.x;
+    const int t = unit_owner(wp, W, u);
+    const uint32_t inf = ((const uint32_t __attribute__((address_space(4)))*)info)[t];
+    if ((inf & 255u) != 1u) return;  // aggregate_sign_rest writes this unit
+    const int emin = (int)((inf >> 8) & 255u);
+    const ADesc ad = a[t];
+    const uint32_t h = threadIdx.x & 1u;
+    const uint32_t sel = h ? 0x07060302u : 0x05040100u;
+    const int G = (W + 7) / 8;
+    const uint32_t wi = (u - ad.unit0) * (kSignAggUnit / 32u) + (threadIdx.x >> 1);  // word of the tensor
+    const bool has = wi < ad.k;
+    // lanes past the tensor read its first word (their sums are dropped)
+    const uint32_t wload = (uint32_t)(ad.off + (has ? wi : 0u)) * 4u;
+    // the tables of the 2 kS groups the steps read (groups past G are zero
+    // in the workspace), 16 bytes per lane and load, are requested first,
+    // then the words of its 16 kS workers (16 kS = 16 ceil(G/2) = Wp, so
+    // every slot exists)
+    const int32_t* tt = tabs + (size_t)t * 2048;
+    u32x4 tv[2];
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+        const int x = 4 * threadIdx.x + 1024 * r;
+        tv[r] = x < 512 * kS ? ldg4u(reinterpret_cast<const uint32_t*>(tt) + x) : u32x4{0u, 0u, 0u, 0u};
+    }
+    uint32_t wv[16 * kS];
+#pragma unroll
+    for (int jj = 0; jj < 16 * kS; ++jj) wv[jj] = ld_word(w_a(wp, jj), wload);
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+        const int x = 4 * threadIdx.x + 1024 * r;
+        if (x < 512 * kS) *reinterpret_cast<u32x4*>(tab + x) = tv[r];
+    }
+    __syncthreads();
+    int32_t S[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) S[q] = 0;
+#pragma unroll
+    for (int st = 0; st < kS; ++st)
+        if (2 * st < G) lookup_step<int32_t>(S, wv + 16 * st, sel, tab, 2 * st);
+    // exact: |S| < 2^31 and the unit is a power of two
+    const double unit = __builtin_ldexp(1.0, emin - 150);
+    float res[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) res[q] = alpha * (float)((double)S[q] * unit);
+    // Lane l holds unit elements 16 l .. 16 l + 15.  Through LDS (element e
+    // of the unit at lds[e]), store k of the workgroup writes elements
+    // 1024 k + 4 l' .. +3 for lane l': every store instruction covers 1 KiB
+    // of the output.
+    __syncthreads();  // every wave is past its lookups
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+        *reinterpret_cast<f32x4*>(lds + 16 * threadIdx.x + 4 * c) =
+            f32x4{res[4 * c], res[4 * c + 1], res[4 * c + 2], res[4 * c + 3]};
+    __syncthreads();
+    const uint32_t ebase = (u - ad.unit0) * kSignAggUnit;  // first element of the unit
+    const uint32_t nleft = ad.n - ebase;                     // > 0
+    float* out = ad.out + ebase;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const uint32_t e = 1024u * k + 4u * threadIdx.x;  // element of the unit
+        const f32x4 v = *reinterpret_cast<const f32x4*>(lds + e);
+        if (e + 4u <= nleft) {
+            stg4f(out + e, v);
+        } else {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                if (e + q < nleft) gp(out)[e + q] = v[q];
+        }
+    }
+}
+
+// The other forms: fp64 tables (one step's words load while the previous
+// step's lookups run) or the worker-ordered fp32 sum.  Workgroups walk
+// contiguous unit ranges and skip int32-form units unless `all`.
+__global__ __launch_bounds__(kBlock) void aggregate_sign_rest(const ADesc* __restrict__ a, int T, uint32_t U,
+                                                              const uint64_t* __restrict__ wp, int W,
+                                                              float alpha, int span_limit,
+                                                              int int_span_limit,
+                                                              const uint32_t* __restrict__ info,
+                                                              int all, uint32_t epoch) {
+    __shared__ double tab[8 * 256];
+    __shared__ double sub[8 * 32];
     __shared__ float sc[1024];
     __shared__ int emin_sh, emax_sh, bad_sh;
     const uint32_t h = threadIdx.x & 1u;
@@ -379,47 +528,45 @@ __global__ __launch_bounds__(kBlock) void aggregate_sign(const ADesc* __restrict
     const int G = (W + 7) / 8;
     const uint32_t ub = (uint32_t)((uint64_t)blockIdx.x * U / gridDim.x);
     const uint32_t ue = (uint32_t)((uint64_t)(blockIdx.x + 1) * U / gridDim.x);
+    if (!all && ((const uint32_t __attribute__((address_space(4)))*)info)[T] != epoch) return;
     int t_cur = -1, form = 0, emin = 0;
     bool tab_ok = false;
     for (uint32_t u = ub; u < ue; ++u) {
         const int t = unit_owner(wp, W, u);
+        if (!all && (((const uint32_t __attribute__((address_space(4)))*)info)[t] & 255u) == 1u) continue;
         const ADesc ad = a[t];
-        const uint32_t wi = (u - ad.unit0) * (kSignAggUnit / 32u) + lw;  // word of the tensor
+        const uint32_t wi = (u - ad.unit0) * (kSignAggUnit / 32u) + lw;
         const bool has = wi < ad.k;
-        // lanes past the tensor read its first word (their sums are dropped)
         const uint32_t wload = (uint32_t)(ad.off + (has ? wi : 0u)) * 4u;
         if (t != t_cur) {
             tensor_form(wp, W, t, sc, &emin_sh, &emax_sh, &bad_sh, span_limit, int_span_limit, form, emin);
             t_cur = t;
             tab_ok = false;
-            if (threadIdx.x == 0) wide[t] = form == 2 ? 1u : 0u;
         }
-        if (form == 2) continue;  // aggregate_sign_wide writes this unit
         float res[16];
-        if (form == 1) {
-            // 16 kS <= 16 ceil(G / 2) = Wp: every slot read here exists
-            uint32_t wv[16 * kS];
+        if (form != 0) {  // fp64 tables (also exact for int32-form tensors)
+            double S[16];
 #pragma unroll
-            for (int jj = 0; jj < 16 * kS; ++jj) wv[jj] = ld_word(w_a(wp, jj), wload);
-            int32_t S[16];
+            for (int q = 0; q < 16; ++q) S[q] = 0.0;
+            uint32_t w16[16];
 #pragma unroll
-            for (int q = 0; q < 16; ++q) S[q] = 0;
-            if (!tab_ok) build_tables<int32_t>(0, W, sc, emin, tab, sub);
-            tab_ok = G <= 8;  // one batch holds every group: keep it
+            for (int jj = 0; jj < 16; ++jj) w16[jj] = ld_word(w_a(wp, jj), wload);
+            for (int g = 0; g < G; g += 2) {
+                if ((g & 7) == 0 && !tab_ok) {
+                    build_tables<double>(g, W, sc, emin, tab, sub);
+                    tab_ok = G <= 8;
+                }
+                uint32_t cur[16];
 #pragma unroll
-            for (int st = 0; st < kS; ++st)
-                if (2 * st < G) lookup_step<int32_t>(S, wv + 16 * st, sel, tab, 2 * st);
-            for (int g = 2 * kS; g < G; g += 2) {  // more than 16 kS workers
-                if ((g & 7) == 0) build_tables<int32_t>(g, W, sc, emin, tab, sub);
-                uint32_t w16[16];
+                for (int jj = 0; jj < 16; ++jj) cur[jj] = w16[jj];
+                if (g + 2 < G) {
 #pragma unroll
-                for (int jj = 0; jj < 16; ++jj) w16[jj] = ld_word(w_a(wp, 8 * g + jj), wload);
-                lookup_step<int32_t>(S, w16, sel, tab, g);
+                    for (int jj = 0; jj < 16; ++jj) w16[jj] = ld_word(w_a(wp, 8 * (g + 2) + jj), wload);
+                }
+                lookup_step<double>(S, cur, sel, tab, g);
             }
-            // exact: |S| < 2^31 and the unit is a power of two
-            const double unit = __builtin_ldexp(1.0, emin - 150);
 #pragma unroll
-            for (int q = 0; q < 16; ++q) res[q] = alpha * (float)((double)S[q] * unit);
+            for (int q = 0; q < 16; ++q) res[q] = alpha * (float)S[q];
         } else {
             float acc[16];
 #pragma unroll
@@ -440,64 +587,6 @@ __global__ __launch_bounds__(kBlock) void aggregate_sign(const ADesc* __restrict
 #pragma unroll
             for (int q = 0; q < 16; ++q) res[q] = alpha * acc[q];
         }
-        if (has) store16(ad, wi * 32u + 16u * h, res);
-    }
-}
-
-// fp64 exact form for the tensors aggregate_sign marked; one step's words
-// load while the previous step's lookups run.
-__global__ __launch_bounds__(kBlock) void aggregate_sign_wide(const ADesc* __restrict__ a, int T, uint32_t U,
-                                                              const uint64_t* __restrict__ wp, int W,
-                                                              float alpha, int span_limit,
-                                                              int int_span_limit,
-                                                              const uint32_t* __restrict__ wide) {
-    __shared__ double tab[8 * 256];
-    __shared__ double sub[8 * 32];
-    __shared__ float sc[1024];
-    __shared__ int emin_sh, emax_sh, bad_sh;
-    const uint32_t h = threadIdx.x & 1u;
-    const uint32_t lw = threadIdx.x >> 1;
-    const uint32_t sel = h ? 0x07060302u : 0x05040100u;
-    const int G = (W + 7) / 8;
-    const uint32_t ub = (uint32_t)((uint64_t)blockIdx.x * U / gridDim.x);
-    const uint32_t ue = (uint32_t)((uint64_t)(blockIdx.x + 1) * U / gridDim.x);
-    int t_cur = -1, form = 0, emin = 0;
-    bool tab_ok = false;
-    for (uint32_t u = ub; u < ue; ++u) {
-        const int t = unit_owner(wp, W, u);
-        if (((const uint32_t __attribute__((address_space(4)))*)wide)[t] == 0u) continue;
-        const ADesc ad = a[t];
-        const uint32_t wi = (u - ad.unit0) * (kSignAggUnit / 32u) + lw;
-        const bool has = wi < ad.k;
-        const uint32_t wload = (uint32_t)(ad.off + (has ? wi : 0u)) * 4u;
-        if (t != t_cur) {
-            tensor_form(wp, W, t, sc, &emin_sh, &emax_sh, &bad_sh, span_limit, int_span_limit, form, emin);
-            t_cur = t;
-            tab_ok = false;
-        }
-        double S[16];
-#pragma unroll
-        for (int q = 0; q < 16; ++q) S[q] = 0.0;
-        uint32_t w16[16];
-#pragma unroll
-        for (int jj = 0; jj < 16; ++jj) w16[jj] = ld_word(w_a(wp, jj), wload);
-        for (int g = 0; g < G; g += 2) {
-            if ((g & 7) == 0 && !tab_ok) {
-                build_tables<double>(g, W, sc, emin, tab, sub);
-                tab_ok = G <= 8;
-            }
-            uint32_t cur[16];
-#pragma unroll
-            for (int jj = 0; jj < 16; ++jj) cur[jj] = w16[jj];
-            if (g + 2 < G) {
-#pragma unroll
-                for (int jj = 0; jj < 16; ++jj) w16[jj] = ld_word(w_a(wp, 8 * (g + 2) + jj), wload);
-            }
-            lookup_step<double>(S, cur, sel, tab, g);
-        }
-        float res[16];
-#pragma unroll
-        for (int q = 0; q < 16; ++q) res[q] = alpha * (float)S[q];
         if (has) store16(ad, wi * 32u + 16u * h, res);
     }
 }
@@ -551,8 +640,15 @@ hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t U, const uint
     return hipGetLastError();
 }
 
+namespace {
+// Resident workgroups per CU of aggregate_sign_rest, measured once per
+// process (launches run under the library's call lock).
+int g_rest_occ = 0;
+}  // namespace
+
 hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W,
-                                 float alpha, uint32_t* wide, uint32_t max_blocks, hipStream_t s) {
+                                 float alpha, uint32_t* info, int32_t* tabs, uint32_t epoch, int cus,
+                                 hipStream_t s) {
     if (U == 0) return hipSuccess;
     int lg = 0;
     while ((1 << lg) < W) ++lg;
@@ -561,24 +657,38 @@ hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t U, const uint64
     int lg8 = 0;
     while ((1 << lg8) < 8 * G) ++lg8;
     const int int_span_limit = 7 - lg8;  // 24 + span + ceil(log2 8G) <= 31
+    // up to 64 workers: int32-form units in aggregate_sign, the rest after
+    // it; more workers: every unit in aggregate_sign_rest
+    const int small = G <= 8;
+    hipLaunchKernelGGL(sign_agg_prep, dim3(T), dim3(64), 0, s, a, T, w, W, span_limit, int_span_limit, info,
+                       tabs, small, epoch);
+    if (small) {
+        const int steps = (G + 1) / 2;
+        const dim3 grid(U), block(kBlock);
+        const uint32_t* ci = info;
+        const int32_t* ct = tabs;
+        if (steps <= 1)
+            hipLaunchKernelGGL(aggregate_sign<1>, grid, block, 0, s, a, T, U, w, W, alpha, ci, ct);
+        else if (steps == 2)
+            hipLaunchKernelGGL(aggregate_sign<2>, grid, block, 0, s, a, T, U, w, W, alpha, ci, ct);
+        else if (steps == 3)
+            hipLaunchKernelGGL(aggregate_sign<3>, grid, block, 0, s, a, T, U, w, W, alpha, ci, ct);
+        else
+            hipLaunchKernelGGL(aggregate_sign<4>, grid, block, 0, s, a, T, U, w, W, alpha, ci, ct);
+    }
+    if (g_rest_occ == 0) {
+        int b = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, aggregate_sign_rest, kBlock, 0) != hipSuccess || b < 1)
+            b = 1;
+        g_rest_occ = b;
+    }
+    // with up to 64 workers the rest kernel usually has nothing to do and
+    // exits at once: one workgroup per CU keeps that launch short
+    const uint32_t max_blocks = (uint32_t)cus * (uint32_t)(small ? 1 : g_rest_occ);
     const uint32_t blocks = U < max_blocks ? U : max_blocks;
-    const int steps = (G + 1) / 2;
-    const dim3 grid(blocks), block(kBlock);
-    if (steps <= 1)
-        hipLaunchKernelGGL(aggregate_sign<1>, grid, block, 0, s, a, T, U, w, W, alpha, span_limit, int_span_limit, wide);
-    else if (steps == 2)
-        hipLaunchKernelGGL(aggregate_sign<2>, grid, block, 0, s, a, T, U, w, W, alpha, span_limit, int_span_limit, wide);
-    else if (steps == 3)
-        hipLaunchKernelGGL(aggregate_sign<3>, grid, block, 0, s, a, T, U, w, W, alpha, span_limit, int_span_limit, wide);
-    else
-        hipLaunchKernelGGL(aggregate_sign<4>, grid, block, 0, s, a, T, U, w, W, alpha, span_limit, int_span_limit, wide);
-    hipLaunchKernelGGL(aggregate_sign_wide, grid, block, 0, s, a, T, U, w, W, alpha, span_limit, int_span_limit,
-                       (const uint32_t*)wide);
+    hipLaunchKernelGGL(aggregate_sign_rest, dim3(blocks), dim3(kBlock), 0, s, a, T, U, w, W, alpha, span_limit,
+                       int_span_limit, (const uint32_t*)info, small ? 0 : 1, epoch);
     return hipGetLastError();
-}
-
-hipError_t aggregate_sign_occupancy(int* blocks_per_cu) {
-    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, aggregate_sign<4>, kBlock, 0);
 }
 
 hipError_t launch_sign_residual_update(const TDesc* d, int T, uint32_t C, const uint32_t* bits,

@@ -20,7 +20,9 @@ struct Ws {
     uint32_t* s_ready;      // [T] 64-bit words: bit 32 = published, low 32 = scale     
     float* s_val;           // [T] published scales
     double* s_partial;      // [C] per-chunk sums of |v|
-    uint32_t* s_wide;       // [T] aggregate: 1 = tensor takes the fp64 exact form
+    uint32_t* s_info;       // [T + 1] aggregate: form (bits 0-7) and smallest scale exponent
+                            // (8-15) per tensor; [T]: call number when some tensor is not int32
+    int32_t* s_tab;         // [T * 2048] aggregate: int32 lookup tables of each tensor
     // BC_TOPK, BC_TOPK_SAMPLED
     uint32_t* t_hist;       // [T * 2048] histograms         
     uint32_t* t_thr;        // [T] candidate threshold (key)
@@ -45,7 +47,7 @@ struct Ws {
 // Byte offsets of every region for a call shape; `total` is the workspace
 // size.  Regions a kind does not use have size 0.
 struct WsPlan {
-    size_t flags, s_cnt, s_ready, s_val, s_partial, s_wide;
+    size_t flags, s_cnt, s_ready, s_val, s_partial, s_info, s_tab;
     size_t t_hist, t_thr, t_prefix, t_krem, t_fb, t_cand, t_ccount, t_gt, t_eq, t_off, t_eqb;
     size_t r_keys, r_tmp, r_ccount, r_coff, r_cursor;
     size_t total;
@@ -57,7 +59,6 @@ Ws carve_workspace(void* base, const WsPlan& p);
 struct DevInfo {
     int cus;
     int sign_coop_blocks_per_cu;
-    int agg_sign_blocks_per_cu;
     bool coop_ok;
     bool sign_one_pass;  // BYTECOMP_SIGN_PATH=onepass
     bool any_empty;      // per call: some tensor has no elements
@@ -81,8 +82,8 @@ hipError_t launch_residual_update(int kind, const TDesc* d, int T, uint32_t C, b
 hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t units, const uint64_t* wp, int W,
                                    float alpha, hipStream_t s);
 hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t units, const uint64_t* wp, int W,
-                                 float alpha, uint32_t* wide, uint32_t max_blocks, hipStream_t s);
-hipError_t aggregate_sign_occupancy(int* blocks_per_cu);
+                                 float alpha, uint32_t* info, int32_t* tabs, uint32_t epoch, int cus,
+                                 hipStream_t s);
 
 // Work-unit sizes of the aggregate kernels (elements per unit).
 // Worker descriptors in the aggregate table are padded to a multiple of 16.

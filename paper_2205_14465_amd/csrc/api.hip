@@ -148,7 +148,6 @@ bool g_dev_ok[64];
 
 }  // namespace
 
-hipError_t sign_coop_occupancy(int* blocks_per_cu);
 
 hipError_t device_info(int dev, DevInfo* out) {
     std::lock_guard<std::mutex> lk(g_dev_mu);
@@ -159,14 +158,6 @@ hipError_t device_info(int dev, DevInfo* out) {
         if (e != hipSuccess) return e;
         DevInfo di;
         di.cus = p.multiProcessorCount;
-        di.coop_ok = p.cooperativeLaunch != 0;
-        int b = 0;
-        e = sign_coop_occupancy(&b);
-        if (e != hipSuccess) return e;
-        di.sign_coop_blocks_per_cu = b > 0 ? b : 1;
-
-        const char* sp = std::getenv("BYTECOMP_SIGN_PATH");
-        di.sign_one_pass = sp && std::strcmp(sp, "onepass") == 0;
         di.any_empty = false;
         g_dev[dev] = di;
         g_dev_ok[dev] = true;
@@ -186,8 +177,6 @@ WsPlan plan_workspace(int kind, int T, uint64_t C, uint64_t sum_k) {
     };
     const size_t t = (size_t)T;
     if (kind == BC_SIGN1) {
-        take(p.s_cnt, t * 4);
-        take(p.s_ready, t * 8);
         take(p.s_val, t * 4);
         take(p.s_partial, (size_t)C * 8);
         take(p.s_info, t ? (t + 1) * 4 : 0);
@@ -222,8 +211,6 @@ Ws carve_workspace(void* base, const WsPlan& p) {
     Ws w;
     std::memset(&w, 0, sizeof(w));
     w.flags = (uint32_t*)b;
-    w.s_cnt = (uint32_t*)at(p.s_cnt);
-    w.s_ready = (uint32_t*)at(p.s_ready);
     w.s_val = (float*)at(p.s_val);
     w.s_partial = (double*)at(p.s_partial);
     w.s_info = (uint32_t*)at(p.s_info);
@@ -418,7 +405,7 @@ int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t,
     const TDesc* dd = (const TDesc*)en->dev;
     switch (kind) {
         case BC_SIGN1:
-            e = launch_sign_compress(dd, T, C, maxc, a16, a32, out.bits, out.scale, w, di, s);
+            e = launch_sign_compress(dd, T, C, maxc, di.any_empty, out.bits, out.scale, w, s);
             break;
         case BC_TOPK:
         case BC_TOPK_SAMPLED:

@@ -16,8 +16,6 @@ namespace bc {
 struct Ws {
     uint32_t* flags;        // header: failure flags
     // BC_SIGN1
-    uint32_t* s_cnt;        // [T] arrival counters          
-    uint32_t* s_ready;      // [T] 64-bit words: bit 32 = published, low 32 = scale     
     float* s_val;           // [T] published scales
     double* s_partial;      // [C] per-chunk sums of |v|
     uint32_t* s_info;       // [T + 1] aggregate: form (bits 0-7) and smallest scale exponent
@@ -47,7 +45,7 @@ struct Ws {
 // Byte offsets of every region for a call shape; `total` is the workspace
 // size.  Regions a kind does not use have size 0.
 struct WsPlan {
-    size_t flags, s_cnt, s_ready, s_val, s_partial, s_info, s_tab;
+    size_t flags, s_val, s_partial, s_info, s_tab;
     size_t t_hist, t_thr, t_prefix, t_krem, t_fb, t_cand, t_ccount, t_gt, t_eq, t_off, t_eqb;
     size_t r_keys, r_tmp, r_ccount, r_coff, r_cursor;
     size_t total;
@@ -58,18 +56,14 @@ Ws carve_workspace(void* base, const WsPlan& p);
 
 struct DevInfo {
     int cus;
-    int sign_coop_blocks_per_cu;
-    bool coop_ok;
-    bool sign_one_pass;  // BYTECOMP_SIGN_PATH=onepass
     bool any_empty;      // per call: some tensor has no elements
 };
 hipError_t device_info(int dev, DevInfo* out);
 
 // ------------------------------------------------------------- launchers
 // d: device TDesc[T]; C: total chunks.  Return the first HIP error.
-hipError_t launch_sign_compress(const TDesc* d, int T, uint32_t C, uint32_t max_chunks,
-                                bool any_f16, bool any_f32, uint32_t* bits, float* scale,
-                                const Ws& ws, const DevInfo& di, hipStream_t s);
+hipError_t launch_sign_compress(const TDesc* d, int T, uint32_t C, uint32_t max_chunks, bool any_empty,
+                                uint32_t* bits, float* scale, const Ws& ws, hipStream_t s);
 hipError_t launch_topk(int kind, double ratio, uint64_t seed, const TDesc* d, int T, uint32_t C,
                        bool any_f16, bool any_f32, uint32_t* idx, float* val, const Ws& ws,
                        hipStream_t s);

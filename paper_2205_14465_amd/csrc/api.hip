@@ -6,7 +6,6 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
-#include <atomic>
 #include <mutex>
 #include <new>
 #include <vector>
@@ -179,7 +178,7 @@ WsPlan plan_workspace(int kind, int T, uint64_t C, uint64_t sum_k) {
     if (kind == BC_SIGN1) {
         take(p.s_val, t * 4);
         take(p.s_partial, (size_t)C * 8);
-        take(p.s_info, t ? (t + 1) * 4 : 0);
+        take(p.s_info, t * 4);
         take(p.s_tab, t * 2048 * 4);
     } else if (kind == BC_TOPK || kind == BC_TOPK_SAMPLED) {
         take(p.t_hist, t * kBins0 * 4);
@@ -420,10 +419,6 @@ int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t,
     return finish(hip_status(e), s, ws);
 }
 
-// Call number stamped by the sign aggregate into its workspace (so a flag
-// from an earlier call never reads as set); 0 is skipped.
-static std::atomic<uint32_t> g_agg_epoch{0};
-
 int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, int W,
                                   const uint64_t* n, int T, float* const* out, float alpha,
                                   void* ws, size_t ws_bytes, void* stream) {
@@ -510,9 +505,7 @@ int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, 
     if (sparse) {
         e = launch_aggregate_sparse(ad, T, (uint32_t)units, wdd, W, alpha, s);
     } else {
-        uint32_t epoch = ++g_agg_epoch;
-        if (epoch == 0) epoch = ++g_agg_epoch;
-        e = launch_aggregate_sign(ad, T, (uint32_t)units, wdd, W, alpha, w.s_info, w.s_tab, epoch, di.cus, s);
+        e = launch_aggregate_sign(ad, T, (uint32_t)units, wdd, W, alpha, w.s_info, w.s_tab, s);
     }
     cache_mark_used(en, s);
     return finish(hip_status(e), s, ws);

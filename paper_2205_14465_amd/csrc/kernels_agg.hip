@@ -298,6 +298,24 @@ __device__ __forceinline__ void lookup_step(Acc (&S)[16], const uint32_t* w, uin
     }
 }
 
+// Half of a step for the register-lean fp64 path: only elements
+// q + 8 half (q < 8) of the lane's sixteen.
+__device__ __forceinline__ void lookup_step_half(double (&S)[8], const uint32_t* w, uint32_t sel,
+                                                 const double* tab, int g, int half) {
+    uint32_t idx4[8];
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) idx4[jj] = __builtin_amdgcn_perm(w[8 + jj], w[jj], sel);
+    transpose_bytes8(idx4);
+    const double* ta = tab + (g & 7) * 256;
+    const double* tb = ta + 256;
+    const int sh = 8 * half;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        S[q] += ta[(idx4[q] >> sh) & 255u];
+        S[q] += tb[(idx4[q] >> (16 + sh)) & 255u];
+    }
+}
+
 // Scales of tensor t into sc[] and its form: 0 ordered, 1 int32 exact,
 // 2 fp64 exact; emin = smallest biased exponent of its normal scales.
 __device__ __forceinline__ void tensor_form(const uint64_t* __restrict__ wp, int W, int t, float* sc,
@@ -354,20 +372,18 @@ __device__ __forceinline__ void store16(const ADesc& ad, uint32_t e0, const floa
 // partial sum exact).  Ordered form (non-finite or subnormal scales, or a
 // wider span): worker-ordered fp32 additions.
 //
-// Three launches: sign_agg_prep (one workgroup per tensor) classifies each
-// tensor and, for up to 64 workers, writes its int32 tables to the
-// workspace; aggregate_sign (one workgroup per unit, in unit order, so that
-// the workgroups resident at a time read neighbouring words of every
-// payload) copies its tensor's tables into LDS and sums the int32-form
-// units; aggregate_sign_rest sums the other units (every unit when W > 64)
-// with fp64 tables or in worker order.  The fp64 form needs many more
-// registers; keeping it apart leaves the common form its occupancy.
+// Two launches: sign_agg_prep (one wave per tensor) classifies each tensor
+// and, for up to 64 workers, writes its int32 tables to the workspace;
+// aggregate_sign (one workgroup per unit, in unit order, so that the
+// workgroups resident at a time read neighbouring words of every payload)
+// copies its tensor's int32 tables into LDS and sums the unit.  Units of the
+// other forms (rare) take a slower path in the same kernel that is kept lean
+// in registers, so that the common form keeps its occupancy.
 __global__ __launch_bounds__(64) void sign_agg_prep(const ADesc* __restrict__ a, int T,
                                                     const uint64_t* __restrict__ wp, int W,
                                                     int span_limit, int int_span_limit,
                                                     uint32_t* __restrict__ info,
-                                                    int32_t* __restrict__ tabs, int build,
-                                                    uint32_t epoch) {
+                                                    int32_t* __restrict__ tabs, int build) {
     // one wave per tensor
     __shared__ float sc[1024];
     __shared__ int32_t sub[8 * 32];
@@ -395,10 +411,7 @@ __global__ __launch_bounds__(64) void sign_agg_prep(const ADesc* __restrict__ a,
     const int span = hi < lo ? 0 : hi - lo;
     const int form = bad ? 0 : span <= int_span_limit ? 1 : span <= span_limit ? 2 : 0;
     const int emin = hi < lo ? 1 : lo;
-    if (lane == 0) {
-        info[t] = (uint32_t)form | ((uint32_t)emin << 8);
-        if (form != 1) info[T] = epoch;  // aggregate_sign_rest has work this call
-    }
+    if (lane == 0) info[t] = (uint32_t)form | ((uint32_t)emin << 8);
     if (!build || form != 1) return;
     __builtin_amdgcn_wave_barrier();
     // sub[32 gi + 16 hh + p]: sum over workers 8 gi + 4 hh + c, c < 4, of
@@ -430,18 +443,19 @@ __global__ __launch_bounds__(64) void sign_agg_prep(const ADesc* __restrict__ a,
 }
 
 template <int kS>
-__global__ __launch_bounds__(kBlock) void aggregate_sign(const ADesc* __restrict__ a, int T, uint32_t U,
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) void aggregate_sign(const ADesc* __restrict__ a, int T, uint32_t U,
                                                          const uint64_t* __restrict__ wp, int W,
                                                          float alpha, const uint32_t* __restrict__ info,
-                                                         const int32_t* __restrict__ tabs) {
-    // the tables (8 KiB), then, after the last lookup, the unit's 4096
-    // results (16 KiB) on their way to coalesced stores
+                                                         const int32_t* __restrict__ tabs, int fast_ok) {
+    // the tables (int32: 8 KiB, fp64: 16 KiB), then, after the last lookup,
+    // the unit's 4096 results (16 KiB) on their way to coalesced stores
     __shared__ __attribute__((aligned(16))) float lds[4096];
-    int32_t* tab = reinterpret_cast<int32_t*>(lds);
+    __shared__ float sc[1024];
+    __shared__ double sub[8 * 32];
     const uint32_t u = blockIdx.x;
     const int t = unit_owner(wp, W, u);
     const uint32_t inf = ((const uint32_t __attribute__((address_space(4)))*)info)[t];
-    if ((inf & 255u) != 1u) return;  // aggregate_sign_rest writes this unit
+    const int form = (int)(inf & 255u);
     const int emin = (int)((inf >> 8) & 255u);
     const ADesc ad = a[t];
     const uint32_t h = threadIdx.x & 1u;
@@ -451,37 +465,85 @@ __global__ __launch_bounds__(kBlock) void aggregate_sign(const ADesc* __restrict
     const bool has = wi < ad.k;
     // lanes past the tensor read its first word (their sums are dropped)
     const uint32_t wload = (uint32_t)(ad.off + (has ? wi : 0u)) * 4u;
-    // the tables of the 2 kS groups the steps read (groups past G are zero
-    // in the workspace), 16 bytes per lane and load, are requested first,
-    // then the words of its 16 kS workers (16 kS = 16 ceil(G/2) = Wp, so
-    // every slot exists)
-    const int32_t* tt = tabs + (size_t)t * 2048;
-    u32x4 tv[2];
-#pragma unroll
-    for (int r = 0; r < 2; ++r) {
-        const int x = 4 * threadIdx.x + 1024 * r;
-        tv[r] = x < 512 * kS ? ldg4u(reinterpret_cast<const uint32_t*>(tt) + x) : u32x4{0u, 0u, 0u, 0u};
-    }
-    uint32_t wv[16 * kS];
-#pragma unroll
-    for (int jj = 0; jj < 16 * kS; ++jj) wv[jj] = ld_word(w_a(wp, jj), wload);
-#pragma unroll
-    for (int r = 0; r < 2; ++r) {
-        const int x = 4 * threadIdx.x + 1024 * r;
-        if (x < 512 * kS) *reinterpret_cast<u32x4*>(tab + x) = tv[r];
-    }
-    __syncthreads();
-    int32_t S[16];
-#pragma unroll
-    for (int q = 0; q < 16; ++q) S[q] = 0;
-#pragma unroll
-    for (int st = 0; st < kS; ++st)
-        if (2 * st < G) lookup_step<int32_t>(S, wv + 16 * st, sel, tab, 2 * st);
-    // exact: |S| < 2^31 and the unit is a power of two
-    const double unit = __builtin_ldexp(1.0, emin - 150);
     float res[16];
+    if (fast_ok && form == 1) {
+        // int32 form, up to 64 workers: the tables of the 2 kS groups the
+        // steps read (groups past G are zero in the workspace), 16 bytes per
+        // lane and load, are requested first, then the words of the 16 kS
+        // workers (16 kS = 16 ceil(G/2) = Wp, so every slot exists)
+        int32_t* tab = reinterpret_cast<int32_t*>(lds);
+        const int32_t* tt = tabs + (size_t)t * 2048;
+        u32x4 tv[2];
 #pragma unroll
-    for (int q = 0; q < 16; ++q) res[q] = alpha * (float)((double)S[q] * unit);
+        for (int r = 0; r < 2; ++r) {
+            const int x = 4 * threadIdx.x + 1024 * r;
+            tv[r] = x < 512 * kS ? ldg4u(reinterpret_cast<const uint32_t*>(tt) + x) : u32x4{0u, 0u, 0u, 0u};
+        }
+        uint32_t wv[16 * kS];
+#pragma unroll
+        for (int jj = 0; jj < 16 * kS; ++jj) wv[jj] = ld_word(w_a(wp, jj), wload);
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            const int x = 4 * threadIdx.x + 1024 * r;
+            if (x < 512 * kS) *reinterpret_cast<u32x4*>(tab + x) = tv[r];
+        }
+        __syncthreads();
+        int32_t S[16];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) S[q] = 0;
+#pragma unroll
+        for (int st = 0; st < kS; ++st)
+            if (2 * st < G) lookup_step<int32_t>(S, wv + 16 * st, sel, tab, 2 * st);
+        // exact: |S| < 2^31 and the unit is a power of two
+        const double unit = __builtin_ldexp(1.0, emin - 150);
+#pragma unroll
+        for (int q = 0; q < 16; ++q) res[q] = alpha * (float)((double)S[q] * unit);
+    } else {
+        // the other forms (rare: scales spread over many binades, or more
+        // than 64 workers), kept lean in registers so that they do not cost
+        // the int32 form its occupancy
+        for (int w = threadIdx.x; w < W; w += kBlock) sc[w] = ((cf32p)w_b(wp, W, w))[t];
+        __syncthreads();
+        if (form == 0) {
+            float acc[16];
+#pragma unroll
+            for (int q = 0; q < 16; ++q) acc[q] = 0.f;
+            for (int w0 = 0; w0 < W; w0 += kSignGroup) {
+                uint32_t word[kSignGroup];
+                float sv[kSignGroup];
+#pragma unroll
+                for (int g = 0; g < kSignGroup; ++g) {
+                    const int w = w0 + g < W ? w0 + g : W - 1;
+                    sv[g] = sc[w];
+                    word[g] = ld_word(w_a(wp, w), wload);
+                }
+#pragma unroll
+                for (int g = 0; g < kSignGroup; ++g)
+                    if (w0 + g < W) sign_half_accumulate(acc, word[g] >> (16u * h), sv[g]);
+            }
+#pragma unroll
+            for (int q = 0; q < 16; ++q) res[q] = alpha * acc[q];
+        } else {
+            // fp64 tables (exact for the int32 form's tensors too), the
+            // lane's sixteen elements in two halves of eight
+            double* tab = reinterpret_cast<double*>(lds);
+#pragma unroll
+            for (int half = 0; half < 2; ++half) {
+                double S[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) S[q] = 0.0;
+                for (int g = 0; g < G; g += 2) {
+                    if ((g & 7) == 0 && (half == 0 || G > 8)) build_tables<double>(g, W, sc, emin, tab, sub);
+                    uint32_t w16[16];
+#pragma unroll
+                    for (int jj = 0; jj < 16; ++jj) w16[jj] = ld_word(w_a(wp, 8 * g + jj), wload);
+                    lookup_step_half(S, w16, sel, tab, g, half);
+                }
+#pragma unroll
+                for (int q = 0; q < 8; ++q) res[8 * half + q] = alpha * (float)S[q];
+            }
+        }
+    }
     // Lane l holds unit elements 16 l .. 16 l + 15.  Through LDS (element e
     // of the unit at lds[e]), store k of the workgroup writes elements
     // 1024 k + 4 l' .. +3 for lane l': every store instruction covers 1 KiB
@@ -506,88 +568,6 @@ __global__ __launch_bounds__(kBlock) void aggregate_sign(const ADesc* __restrict
             for (int q = 0; q < 4; ++q)
                 if (e + q < nleft) gp(out)[e + q] = v[q];
         }
-    }
-}
-
-// The other forms: fp64 tables (one step's words load while the previous
-// step's lookups run) or the worker-ordered fp32 sum.  Workgroups walk
-// contiguous unit ranges and skip int32-form units unless `all`.
-__global__ __launch_bounds__(kBlock) void aggregate_sign_rest(const ADesc* __restrict__ a, int T, uint32_t U,
-                                                              const uint64_t* __restrict__ wp, int W,
-                                                              float alpha, int span_limit,
-                                                              int int_span_limit,
-                                                              const uint32_t* __restrict__ info,
-                                                              int all, uint32_t epoch) {
-    __shared__ double tab[8 * 256];
-    __shared__ double sub[8 * 32];
-    __shared__ float sc[1024];
-    __shared__ int emin_sh, emax_sh, bad_sh;
-    const uint32_t h = threadIdx.x & 1u;
-    const uint32_t lw = threadIdx.x >> 1;
-    const uint32_t sel = h ? 0x07060302u : 0x05040100u;
-    const int G = (W + 7) / 8;
-    const uint32_t ub = (uint32_t)((uint64_t)blockIdx.x * U / gridDim.x);
-    const uint32_t ue = (uint32_t)((uint64_t)(blockIdx.x + 1) * U / gridDim.x);
-    if (!all && ((const uint32_t __attribute__((address_space(4)))*)info)[T] != epoch) return;
-    int t_cur = -1, form = 0, emin = 0;
-    bool tab_ok = false;
-    for (uint32_t u = ub; u < ue; ++u) {
-        const int t = unit_owner(wp, W, u);
-        if (!all && (((const uint32_t __attribute__((address_space(4)))*)info)[t] & 255u) == 1u) continue;
-        const ADesc ad = a[t];
-        const uint32_t wi = (u - ad.unit0) * (kSignAggUnit / 32u) + lw;
-        const bool has = wi < ad.k;
-        const uint32_t wload = (uint32_t)(ad.off + (has ? wi : 0u)) * 4u;
-        if (t != t_cur) {
-            tensor_form(wp, W, t, sc, &emin_sh, &emax_sh, &bad_sh, span_limit, int_span_limit, form, emin);
-            t_cur = t;
-            tab_ok = false;
-        }
-        float res[16];
-        if (form != 0) {  // fp64 tables (also exact for int32-form tensors)
-            double S[16];
-#pragma unroll
-            for (int q = 0; q < 16; ++q) S[q] = 0.0;
-            uint32_t w16[16];
-#pragma unroll
-            for (int jj = 0; jj < 16; ++jj) w16[jj] = ld_word(w_a(wp, jj), wload);
-            for (int g = 0; g < G; g += 2) {
-                if ((g & 7) == 0 && !tab_ok) {
-                    build_tables<double>(g, W, sc, emin, tab, sub);
-                    tab_ok = G <= 8;
-                }
-                uint32_t cur[16];
-#pragma unroll
-                for (int jj = 0; jj < 16; ++jj) cur[jj] = w16[jj];
-                if (g + 2 < G) {
-#pragma unroll
-                    for (int jj = 0; jj < 16; ++jj) w16[jj] = ld_word(w_a(wp, 8 * (g + 2) + jj), wload);
-                }
-                lookup_step<double>(S, cur, sel, tab, g);
-            }
-#pragma unroll
-            for (int q = 0; q < 16; ++q) res[q] = alpha * (float)S[q];
-        } else {
-            float acc[16];
-#pragma unroll
-            for (int q = 0; q < 16; ++q) acc[q] = 0.f;
-            for (int w0 = 0; w0 < W; w0 += kSignGroup) {
-                uint32_t word[kSignGroup];
-                float sv[kSignGroup];
-#pragma unroll
-                for (int g = 0; g < kSignGroup; ++g) {
-                    const int w = w0 + g < W ? w0 + g : W - 1;
-                    sv[g] = sc[w];
-                    word[g] = ld_word(w_a(wp, w), wload);
-                }
-#pragma unroll
-                for (int g = 0; g < kSignGroup; ++g)
-                    if (w0 + g < W) sign_half_accumulate(acc, word[g] >> (16u * h), sv[g]);
-            }
-#pragma unroll
-            for (int q = 0; q < 16; ++q) res[q] = alpha * acc[q];
-        }
-        if (has) store16(ad, wi * 32u + 16u * h, res);
     }
 }
 
@@ -640,15 +620,8 @@ hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t U, const uint
     return hipGetLastError();
 }
 
-namespace {
-// Resident workgroups per CU of aggregate_sign_rest, measured once per
-// process (launches run under the library's call lock).
-int g_rest_occ = 0;
-}  // namespace
-
 hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W,
-                                 float alpha, uint32_t* info, int32_t* tabs, uint32_t epoch, int cus,
-                                 hipStream_t s) {
+                                 float alpha, uint32_t* info, int32_t* tabs, hipStream_t s) {
     if (U == 0) return hipSuccess;
     int lg = 0;
     while ((1 << lg) < W) ++lg;
@@ -657,37 +630,22 @@ hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t U, const uint64
     int lg8 = 0;
     while ((1 << lg8) < 8 * G) ++lg8;
     const int int_span_limit = 7 - lg8;  // 24 + span + ceil(log2 8G) <= 31
-    // up to 64 workers: int32-form units in aggregate_sign, the rest after
-    // it; more workers: every unit in aggregate_sign_rest
+    // the int32 tables (and the fast path) serve up to 64 workers
     const int small = G <= 8;
     hipLaunchKernelGGL(sign_agg_prep, dim3(T), dim3(64), 0, s, a, T, w, W, span_limit, int_span_limit, info,
-                       tabs, small, epoch);
-    if (small) {
-        const int steps = (G + 1) / 2;
-        const dim3 grid(U), block(kBlock);
-        const uint32_t* ci = info;
-        const int32_t* ct = tabs;
-        if (steps <= 1)
-            hipLaunchKernelGGL(aggregate_sign<1>, grid, block, 0, s, a, T, U, w, W, alpha, ci, ct);
-        else if (steps == 2)
-            hipLaunchKernelGGL(aggregate_sign<2>, grid, block, 0, s, a, T, U, w, W, alpha, ci, ct);
-        else if (steps == 3)
-            hipLaunchKernelGGL(aggregate_sign<3>, grid, block, 0, s, a, T, U, w, W, alpha, ci, ct);
-        else
-            hipLaunchKernelGGL(aggregate_sign<4>, grid, block, 0, s, a, T, U, w, W, alpha, ci, ct);
-    }
-    if (g_rest_occ == 0) {
-        int b = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, aggregate_sign_rest, kBlock, 0) != hipSuccess || b < 1)
-            b = 1;
-        g_rest_occ = b;
-    }
-    // with up to 64 workers the rest kernel usually has nothing to do and
-    // exits at once: one workgroup per CU keeps that launch short
-    const uint32_t max_blocks = (uint32_t)cus * (uint32_t)(small ? 1 : g_rest_occ);
-    const uint32_t blocks = U < max_blocks ? U : max_blocks;
-    hipLaunchKernelGGL(aggregate_sign_rest, dim3(blocks), dim3(kBlock), 0, s, a, T, U, w, W, alpha, span_limit,
-                       int_span_limit, (const uint32_t*)info, small ? 0 : 1, epoch);
+                       tabs, small);
+    const int steps = small ? (G + 1) / 2 : 1;
+    const dim3 grid(U), block(kBlock);
+    const uint32_t* ci = info;
+    const int32_t* ct = tabs;
+    if (steps <= 1)
+        hipLaunchKernelGGL(aggregate_sign<1>, grid, block, 0, s, a, T, U, w, W, alpha, ci, ct, small);
+    else if (steps == 2)
+        hipLaunchKernelGGL(aggregate_sign<2>, grid, block, 0, s, a, T, U, w, W, alpha, ci, ct, small);
+    else if (steps == 3)
+        hipLaunchKernelGGL(aggregate_sign<3>, grid, block, 0, s, a, T, U, w, W, alpha, ci, ct, small);
+    else
+        hipLaunchKernelGGL(aggregate_sign<4>, grid, block, 0, s, a, T, U, w, W, alpha, ci, ct, small);
     return hipGetLastError();
 }
 

@@ -18,8 +18,7 @@ struct Ws {
     // BC_SIGN1
     float* s_val;           // [T] published scales
     double* s_partial;      // [C] per-chunk sums of |v|
-    uint32_t* s_info;       // [T + 1] aggregate: form (bits 0-7) and smallest scale exponent
-                            // (8-15) per tensor; [T]: call number when some tensor is not int32
+    uint32_t* s_info;       // [T] aggregate: form (bits 0-7), smallest scale exponent (8-15)
     int32_t* s_tab;         // [T * 2048] aggregate: int32 lookup tables of each tensor
     // BC_TOPK, BC_TOPK_SAMPLED
     uint32_t* t_hist;       // [T * 2048] histograms         
@@ -76,8 +75,7 @@ hipError_t launch_residual_update(int kind, const TDesc* d, int T, uint32_t C, b
 hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t units, const uint64_t* wp, int W,
                                    float alpha, hipStream_t s);
 hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t units, const uint64_t* wp, int W,
-                                 float alpha, uint32_t* info, int32_t* tabs, uint32_t epoch, int cus,
-                                 hipStream_t s);
+                                 float alpha, uint32_t* info, int32_t* tabs, hipStream_t s);
 
 // Work-unit sizes of the aggregate kernels (elements per unit).
 // Worker descriptors in the aggregate table are padded to a multiple of 16.

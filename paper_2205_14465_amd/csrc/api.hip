@@ -186,6 +186,7 @@ WsPlan plan_workspace(int kind, int T, uint64_t C, uint64_t sum_k) {
         take(p.t_prefix, t * 4);
         take(p.t_krem, t * 4);
         take(p.t_fb, t * 4);
+        take(p.t_any, 4);
         take(p.t_cand, (size_t)C * kChunk * 8);
         take(p.t_ccount, (size_t)C * 4);
         take(p.t_gt, (size_t)C * 4);
@@ -219,6 +220,7 @@ Ws carve_workspace(void* base, const WsPlan& p) {
     w.t_prefix = (uint32_t*)at(p.t_prefix);
     w.t_krem = (uint32_t*)at(p.t_krem);
     w.t_fb = (uint32_t*)at(p.t_fb);
+    w.t_any = (uint32_t*)at(p.t_any);
     w.t_cand = (uint2*)at(p.t_cand);
     w.t_ccount = (uint32_t*)at(p.t_ccount);
     w.t_gt = (uint32_t*)at(p.t_gt);

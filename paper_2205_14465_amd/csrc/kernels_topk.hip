@@ -57,29 +57,32 @@ __device__ __forceinline__ void flush_hist(const uint32_t* lh, uint32_t* gh, int
 // Stream pass of the exact path: e_new = v (when `write_resid`) and the
 // histogram of key bits 30..20.  With `fb_only` it re-reads the stored v of
 // tensors flagged for the fallback.
-__global__ __launch_bounds__(kBlock) void topk_hist_pass(const TDesc* __restrict__ d, int T,
+__global__ __launch_bounds__(kBlock) void topk_hist_pass(const TDesc* __restrict__ d, int T, uint32_t C,
                                                          int write_resid, int fb_only, Ws ws) {
     __shared__ uint32_t lh[kBins0];
-    const uint32_t c = blockIdx.x;
-    const int t = tensor_of_chunk(d, T, c);
-    if (!active(ws.t_fb, t, fb_only)) return;
-    const TDesc td = d[t];
-    const uint32_t j = c - td.chunk0;
-    for (int b = threadIdx.x; b < kBins0; b += kBlock) lh[b] = 0;
-    float v[kEpt];
-    uint32_t valid;
-    if (write_resid) {
-        load_v(td, j, td.resid != nullptr, v, valid);
-        if (td.resid) store_chunk(td.resid, td.n, j, v);
-    } else {
-        load_stored_v(td, j, v, valid);
-    }
-    __syncthreads();
+    if (fb_only && ws.t_any[0] == 0u) return;  // no tensor fell back
+    for (uint32_t c = blockIdx.x; c < C; c += gridDim.x) {
+        const int t = tensor_of_chunk(d, T, c);
+        if (!active(ws.t_fb, t, fb_only)) continue;
+        const TDesc td = d[t];
+        const uint32_t j = c - td.chunk0;
+        for (int b = threadIdx.x; b < kBins0; b += kBlock) lh[b] = 0;
+        float v[kEpt];
+        uint32_t valid;
+        if (write_resid) {
+            load_v(td, j, td.resid != nullptr, v, valid);
+            if (td.resid) store_chunk(td.resid, td.n, j, v);
+        } else {
+            load_stored_v(td, j, v, valid);
+        }
+        __syncthreads();
 #pragma unroll
-    for (int i = 0; i < kEpt; ++i)
-        if ((valid >> i) & 1u) atomicAdd(&lh[key_of(v[i]) >> 20], 1u);
-    __syncthreads();
-    flush_hist(lh, ws.t_hist + (size_t)t * kBins0, kBins0);
+        for (int i = 0; i < kEpt; ++i)
+            if ((valid >> i) & 1u) atomicAdd(&lh[key_of(v[i]) >> 20], 1u);
+        __syncthreads();
+        flush_hist(lh, ws.t_hist + (size_t)t * kBins0, kBins0);
+        __syncthreads();
+    }
 }
 
 // Seeded sample: each 4096-element chunk of a tensor larger than
@@ -133,6 +136,7 @@ __global__ __launch_bounds__(kBlock) void topk_find(const TDesc* __restrict__ d,
                                                     int mode, int fb_only, Ws ws) {
     __shared__ uint64_t sh[4];
     __shared__ uint32_t found_bin, found_above, found_total;
+    if (fb_only && ws.t_any[0] == 0u) return;  // no tensor fell back
     const int t = blockIdx.x;
     const TDesc td = d[t];
     if (td.k == 0 || !active(ws.t_fb, t, fb_only)) return;
@@ -172,7 +176,10 @@ __global__ __launch_bounds__(kBlock) void topk_find(const TDesc* __restrict__ d,
     } else if (mode == kFindDigit0) {
         target = td.k;
         if (total < td.k) {  // too few candidates: exact fallback for this tensor
-            if (threadIdx.x == 0) ws.t_fb[t] = 1u;
+            if (threadIdx.x == 0) {
+                ws.t_fb[t] = 1u;
+                atomicOr(ws.t_any, 1u);
+            }
             return;
         }
         if (threadIdx.x == 0) ws.t_fb[t] = 0u;
@@ -220,176 +227,219 @@ __global__ __launch_bounds__(kBlock) void topk_find(const TDesc* __restrict__ d,
 // Candidates = valid entries with key >= t_thr[t], compacted in index
 // order into the chunk's slot of t_cand; also the LDS histogram of their
 // key bits 30..20.
-__global__ __launch_bounds__(kBlock) void topk_compact(const TDesc* __restrict__ d, int T,
+__global__ __launch_bounds__(kBlock) void topk_compact(const TDesc* __restrict__ d, int T, uint32_t C,
                                                        int stream_mode, int fb_only, Ws ws) {
     __shared__ uint32_t lh[kBins0];
     __shared__ uint64_t sh[4];
-    const uint32_t c = blockIdx.x;
-    const int t = tensor_of_chunk(d, T, c);
-    if (!active(ws.t_fb, t, fb_only)) return;
-    const TDesc td = d[t];
-    const uint32_t j = c - td.chunk0;
-    for (int b = threadIdx.x; b < kBins0; b += kBlock) lh[b] = 0;
-    float v[kEpt];
-    uint32_t valid;
-    if (stream_mode) {
-        load_v(td, j, td.resid != nullptr, v, valid);
-        if (td.resid) store_chunk(td.resid, td.n, j, v);
-    } else {
-        load_stored_v(td, j, v, valid);
-    }
-    const uint32_t thr = ws.t_thr[t];
-    uint32_t pm = 0;
-#pragma unroll
-    for (int i = 0; i < kEpt; ++i)
-        if (((valid >> i) & 1u) && key_of(v[i]) >= thr) pm |= 1u << i;
-    uint64_t packed = 0;
-#pragma unroll
-    for (int r = 0; r < kRounds; ++r) packed |= (uint64_t)__popc((pm >> (4 * r)) & 0xFu) << (16 * r);
-    uint64_t tot;
-    const uint64_t pre = block_excl_scan_u64(packed, sh, tot);
-    uint2* out = ws.t_cand + (size_t)c * kChunk;
-    uint32_t base = 0;
-#pragma unroll
-    for (int r = 0; r < kRounds; ++r) {
-        uint32_t rank = base + (uint32_t)((pre >> (16 * r)) & 0xFFFFu);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int i = 4 * r + q;
-            if ((pm >> i) & 1u) {
-                const uint32_t e = j * (uint32_t)kChunk + 1024u * r + 4u * threadIdx.x + q;
-                out[rank++] = make_uint2(e, f2u(v[i]));
-                atomicAdd(&lh[key_of(v[i]) >> 20], 1u);
-            }
+    if (fb_only && ws.t_any[0] == 0u) return;  // no tensor fell back
+    for (uint32_t c = blockIdx.x; c < C; c += gridDim.x) {
+        const int t = tensor_of_chunk(d, T, c);
+        if (!active(ws.t_fb, t, fb_only)) continue;
+        const TDesc td = d[t];
+        const uint32_t j = c - td.chunk0;
+        for (int b = threadIdx.x; b < kBins0; b += kBlock) lh[b] = 0;
+        float v[kEpt];
+        uint32_t valid;
+        if (stream_mode) {
+            load_v(td, j, td.resid != nullptr, v, valid);
+            if (td.resid) store_chunk(td.resid, td.n, j, v);
+        } else {
+            load_stored_v(td, j, v, valid);
         }
-        base += (uint32_t)((tot >> (16 * r)) & 0xFFFFu);
+        const uint32_t thr = ws.t_thr[t];
+        uint32_t pm = 0;
+#pragma unroll
+        for (int i = 0; i < kEpt; ++i)
+            if (((valid >> i) & 1u) && key_of(v[i]) >= thr) pm |= 1u << i;
+        uint64_t packed = 0;
+#pragma unroll
+        for (int r = 0; r < kRounds; ++r) packed |= (uint64_t)__popc((pm >> (4 * r)) & 0xFu) << (16 * r);
+        uint64_t tot;
+        const uint64_t pre = block_excl_scan_u64(packed, sh, tot);
+        uint2* out = ws.t_cand + (size_t)c * kChunk;
+        uint32_t base = 0;
+#pragma unroll
+        for (int r = 0; r < kRounds; ++r) {
+            uint32_t rank = base + (uint32_t)((pre >> (16 * r)) & 0xFFFFu);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int i = 4 * r + q;
+                if ((pm >> i) & 1u) {
+                    const uint32_t e = j * (uint32_t)kChunk + 1024u * r + 4u * threadIdx.x + q;
+                    out[rank++] = make_uint2(e, f2u(v[i]));
+                    atomicAdd(&lh[key_of(v[i]) >> 20], 1u);
+                }
+            }
+            base += (uint32_t)((tot >> (16 * r)) & 0xFFFFu);
+        }
+        if (threadIdx.x == 0) ws.t_ccount[c] = base;
+        __syncthreads();
+        flush_hist(lh, ws.t_hist + (size_t)t * kBins0, kBins0);
+        __syncthreads();
     }
-    if (threadIdx.x == 0) ws.t_ccount[c] = base;
-    __syncthreads();
-    flush_hist(lh, ws.t_hist + (size_t)t * kBins0, kBins0);
 }
 
-// Radix pass over a chunk's candidates: histogram of the next digit among
-// candidates whose higher bits match the prefix chosen so far.
-__global__ __launch_bounds__(kBlock) void topk_cand_hist(const TDesc* __restrict__ d, int T,
-                                                         int pass, Ws ws) {
+// Candidate passes.  A chunk holds about 50 candidates at a 1% rate.  The
+// histogram pass gives each workgroup a range of `span` chunks (sized so
+// that about a thousand workgroups remain), paying the clearing and flushing
+// of its LDS histogram once per range; the count and emit passes give each
+// wave one chunk.
+
+// Radix pass over the candidates of a chunk range: histogram of the next
+// digit among candidates whose higher bits match the prefix chosen so far.
+// The LDS histogram is flushed whenever the range moves to another tensor.
+__global__ __launch_bounds__(kBlock) void topk_cand_hist(const TDesc* __restrict__ d, int T, uint32_t C,
+                                                         uint32_t span, int pass, Ws ws) {
     __shared__ uint32_t lh[kBins12];
-    const uint32_t c = blockIdx.x;
-    const uint32_t m = ws.t_ccount[c];
-    if (m == 0) return;
-    const int t = tensor_of_chunk(d, T, c);
-    const uint32_t prefix = ws.t_prefix[t];
     const int shift = pass == 1 ? 10 : 0;
     const int match_shift = pass == 1 ? 20 : 10;
+    const uint32_t c0 = blockIdx.x * span;
+    const uint32_t c1 = c0 + span < C ? c0 + span : C;
     for (int b = threadIdx.x; b < kBins12; b += kBlock) lh[b] = 0;
     __syncthreads();
-    const uint2* cand = ws.t_cand + (size_t)c * kChunk;
-    for (uint32_t i = threadIdx.x; i < m; i += kBlock) {
-        const uint32_t key = cand[i].y & 0x7FFFFFFFu;
-        if ((key >> match_shift) == (prefix >> match_shift))
-            atomicAdd(&lh[(key >> shift) & (kBins12 - 1)], 1u);
+    int t = tensor_of_chunk(d, T, c0);
+    uint32_t prefix = ws.t_prefix[t];
+    uint32_t tend = d[t].chunk0 + d[t].nchunks;
+    for (uint32_t c = c0; c < c1; ++c) {
+        if (c >= tend) {  // next tensor: flush this one's counts
+            __syncthreads();
+            flush_hist(lh, ws.t_hist + (size_t)t * kBins0, kBins12);
+            __syncthreads();
+            for (int b = threadIdx.x; b < kBins12; b += kBlock) lh[b] = 0;
+            __syncthreads();
+            t = tensor_of_chunk(d, T, c);
+            prefix = ws.t_prefix[t];
+            tend = d[t].chunk0 + d[t].nchunks;
+        }
+        const uint32_t m = ws.t_ccount[c];
+        const uint2* cand = ws.t_cand + (size_t)c * kChunk;
+        for (uint32_t i = threadIdx.x; i < m; i += kBlock) {
+            const uint32_t key = cand[i].y & 0x7FFFFFFFu;
+            if ((key >> match_shift) == (prefix >> match_shift))
+                atomicAdd(&lh[(key >> shift) & (kBins12 - 1)], 1u);
+        }
     }
     __syncthreads();
     flush_hist(lh, ws.t_hist + (size_t)t * kBins0, kBins12);
 }
 
-// Per chunk: candidates above tau and equal to tau.
-__global__ __launch_bounds__(kBlock) void topk_cand_count(const TDesc* __restrict__ d, int T, Ws ws) {
-    __shared__ uint64_t sh[4];
-    const uint32_t c = blockIdx.x;
-    const uint32_t m = ws.t_ccount[c];
-    const int t = tensor_of_chunk(d, T, c);
-    const uint32_t tau = ws.t_prefix[t];
-    const uint2* cand = ws.t_cand + (size_t)c * kChunk;
-    uint64_t x = 0;
-    for (uint32_t i = threadIdx.x; i < m; i += kBlock) {
-        const uint32_t key = cand[i].y & 0x7FFFFFFFu;
-        x += (key > tau) ? 1ull : 0ull;
-        x += (key == tau) ? (1ull << 32) : 0ull;
-    }
-    uint64_t tot;
-    block_excl_scan_u64(x, sh, tot);
-    if (threadIdx.x == 0) {
-        ws.t_gt[c] = (uint32_t)tot;
-        ws.t_eq[c] = (uint32_t)(tot >> 32);
+// Per chunk: candidates above tau and equal to tau, one wave per chunk,
+// counted with ballots.
+__global__ __launch_bounds__(kBlock) void topk_cand_count(const TDesc* __restrict__ d, int T, uint32_t C,
+                                                          Ws ws) {
+    const int lane = lane_id();
+    const uint32_t c = blockIdx.x * (kBlock / 64) + wave_id();
+    if (c < C) {
+        const uint32_t m = ws.t_ccount[c];
+        const uint32_t tau = ws.t_prefix[tensor_of_chunk(d, T, c)];
+        const uint2* cand = ws.t_cand + (size_t)c * kChunk;
+        uint32_t gt = 0, eq = 0;
+        for (uint32_t i0 = 0; i0 < m; i0 += 64) {
+            const uint32_t i = i0 + lane;
+            const uint32_t key = i < m ? cand[i].y & 0x7FFFFFFFu : 0u;
+            gt += (uint32_t)__popcll(__ballot(i < m && key > tau));
+            eq += (uint32_t)__popcll(__ballot(i < m && key == tau));
+        }
+        if (lane == 0) {
+            ws.t_gt[c] = gt;
+            ws.t_eq[c] = eq;
+        }
     }
 }
 
 // One workgroup per tensor: place every chunk's winners.  eqb[c] = number
 // of tau-equal candidates in earlier chunks; a chunk keeps its tau-equal
-// candidates while the running count stays below the number needed.
+// candidates while the running count stays below the number needed.  Thread
+// i walks a contiguous run of the tensor's chunks; two block scans over the
+// runs' totals give every chunk its prefix.
 __global__ __launch_bounds__(kBlock) void topk_cand_scan(const TDesc* __restrict__ d, Ws ws) {
     __shared__ uint64_t sh[4];
     const int t = blockIdx.x;
     const TDesc td = d[t];
-    if (td.k == 0) return;
-    const uint32_t need = ws.t_krem[t];
-    uint64_t carry_eq = 0, carry_pos = td.off;
-    for (uint32_t c0 = 0; c0 < td.nchunks; c0 += kBlock) {
-        const uint32_t cl = c0 + threadIdx.x;
-        const bool in = cl < td.nchunks;
-        const uint32_t c = td.chunk0 + cl;
-        const uint32_t gt = in ? ws.t_gt[c] : 0u;
-        const uint32_t eq = in ? ws.t_eq[c] : 0u;
-        uint64_t tot_eq;
-        const uint64_t eqb = carry_eq + block_excl_scan_u64(eq, sh, tot_eq);
-        const uint64_t left = eqb < need ? need - eqb : 0;
-        const uint32_t taken = (uint32_t)(left < eq ? left : eq);
-        uint64_t tot_sel;
-        const uint64_t pos = carry_pos + block_excl_scan_u64((uint64_t)gt + taken, sh, tot_sel);
-        if (in) {
-            ws.t_off[c] = pos;
-            ws.t_eqb[c] = (uint32_t)(eqb < 0xFFFFFFFFull ? eqb : 0xFFFFFFFFull);
+    if (td.k == 0 || td.nchunks == 0) return;
+    const uint64_t need = ws.t_krem[t];
+    const uint32_t per = (td.nchunks + kBlock - 1) / kBlock;
+    const uint32_t lo = threadIdx.x * per;
+    const uint32_t hi = lo + per < td.nchunks ? lo + per : td.nchunks;
+    // tau-equal candidates before each run
+    uint64_t eq_run = 0;
+    for (uint32_t q = lo; q < hi; ++q) eq_run += ws.t_eq[td.chunk0 + q];
+    uint64_t tot;
+    uint64_t eqb = block_excl_scan_u64(eq_run, sh, tot);
+    // winners per chunk, and before each run
+    uint64_t sel_run = 0;
+    {
+        uint64_t e = eqb;
+        for (uint32_t q = lo; q < hi; ++q) {
+            const uint32_t c = td.chunk0 + q;
+            const uint32_t eq = ws.t_eq[c];
+            const uint64_t left = e < need ? need - e : 0;
+            sel_run += (uint64_t)ws.t_gt[c] + (left < eq ? left : eq);
+            e += eq;
         }
-        carry_eq += tot_eq;
-        carry_pos += tot_sel;
+    }
+    uint64_t pos = td.off + block_excl_scan_u64(sel_run, sh, tot);
+    for (uint32_t q = lo; q < hi; ++q) {
+        const uint32_t c = td.chunk0 + q;
+        const uint32_t eq = ws.t_eq[c];
+        const uint64_t left = eqb < need ? need - eqb : 0;
+        ws.t_off[c] = pos;
+        ws.t_eqb[c] = (uint32_t)(eqb < 0xFFFFFFFFull ? eqb : 0xFFFFFFFFull);
+        pos += (uint64_t)ws.t_gt[c] + (left < eq ? left : eq);
+        eqb += eq;
     }
 }
 
-// Emit the winners of a chunk in index order and clear them in e_new.
-__global__ __launch_bounds__(kBlock) void topk_emit(const TDesc* __restrict__ d, int T,
+// Emit the winners of a chunk in index order and clear them in e_new, one
+// wave per chunk; ranks come from ballots.
+__global__ __launch_bounds__(kBlock) void topk_emit(const TDesc* __restrict__ d, int T, uint32_t C,
                                                     uint32_t* __restrict__ idx,
                                                     float* __restrict__ val, Ws ws) {
-    __shared__ uint64_t sh[4];
-    const uint32_t c = blockIdx.x;
-    const uint32_t m = ws.t_ccount[c];
-    if (m == 0) return;
-    const int t = tensor_of_chunk(d, T, c);
-    float* resid = d[t].resid;
-    const uint64_t end = d[t].off + d[t].k;
-    const uint32_t tau = ws.t_prefix[t];
-    const uint32_t need = ws.t_krem[t];
-    const uint2* cand = ws.t_cand + (size_t)c * kChunk;
-    uint64_t eq_seen = ws.t_eqb[c];
-    uint64_t pos = ws.t_off[c];
-    for (uint32_t i0 = 0; i0 < m; i0 += kBlock) {
-        const uint32_t i = i0 + threadIdx.x;
-        uint2 e = make_uint2(0, 0);
-        uint32_t key = 0;
-        if (i < m) {
-            e = cand[i];
-            key = e.y & 0x7FFFFFFFu;
+    const int lane = lane_id();
+    const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;  // lanes under this one
+    const uint32_t c = blockIdx.x * (kBlock / 64) + wave_id();
+    const uint32_t m = c < C ? ws.t_ccount[c] : 0u;
+    if (m > 0) {
+        const int t = tensor_of_chunk(d, T, c);
+        float* resid = d[t].resid;
+        const uint64_t end = d[t].off + d[t].k;
+        const uint32_t tau = ws.t_prefix[t];
+        const uint64_t need = ws.t_krem[t];
+        const uint2* cand = ws.t_cand + (size_t)c * kChunk;
+        uint64_t eq_seen = ws.t_eqb[c];
+        uint64_t pos = ws.t_off[c];
+        for (uint32_t i0 = 0; i0 < m; i0 += 64) {
+            const uint32_t i = i0 + lane;
+            uint2 e = make_uint2(0, 0);
+            uint32_t key = 0;
+            if (i < m) {
+                e = cand[i];
+                key = e.y & 0x7FFFFFFFu;
+            }
+            const bool is_eq = i < m && key == tau;
+            const uint64_t meq = __ballot(is_eq);
+            const uint64_t eq_rank = eq_seen + (uint64_t)__popcll(meq & below);
+            const bool sel = i < m && (key > tau || (is_eq && eq_rank < need));
+            const uint64_t msel = __ballot(sel);
+            const uint64_t at = pos + (uint64_t)__popcll(msel & below);
+            if (sel && at < end) {
+                idx[at] = e.x;
+                val[at] = u2f(e.y);
+                if (resid) gp(resid)[e.x] = 0.f;
+            }
+            eq_seen += (uint64_t)__popcll(meq);
+            pos += (uint64_t)__popcll(msel);
         }
-        const bool is_eq = i < m && key == tau;
-        uint64_t n_eq;
-        const uint64_t eq_rank = eq_seen + block_excl_scan_u64(is_eq ? 1u : 0u, sh, n_eq);
-        const bool sel = i < m && (key > tau || (is_eq && eq_rank < need));
-        uint64_t n_sel;
-        const uint64_t at = pos + block_excl_scan_u64(sel ? 1u : 0u, sh, n_sel);
-        if (sel && at < end) {
-            idx[at] = e.x;
-            val[at] = u2f(e.y);
-            if (resid) gp(resid)[e.x] = 0.f;
-        }
-        eq_seen += n_eq;
-        pos += n_sel;
     }
 }
 
-__global__ void topk_zero_hist(uint32_t* h, uint64_t n) {
-    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-         i += (uint64_t)gridDim.x * blockDim.x)
-        h[i] = 0u;
+// Clear the tensors' histograms (T * 2048 words, a multiple of 4) and the
+// fallback flag at the start of a call.
+__global__ void topk_zero_hist(uint32_t* h, uint64_t n, uint32_t* any) {
+    const uint64_t n4 = n / 4;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (uint64_t)gridDim.x * blockDim.x)
+        reinterpret_cast<u32x4*>(h)[i] = u32x4{0u, 0u, 0u, 0u};
+    if (blockIdx.x == 0 && threadIdx.x == 0) any[0] = 0u;
 }
 
 hipError_t launch_topk(int kind, double ratio, uint64_t seed, const TDesc* d, int T, uint32_t C,
@@ -397,32 +447,39 @@ hipError_t launch_topk(int kind, double ratio, uint64_t seed, const TDesc* d, in
     if (C == 0) return hipSuccess;
     const dim3 blk(kBlock);
     const uint64_t hn = (uint64_t)T * kBins0;
-    uint32_t zb = (uint32_t)((hn + 255) / 256);
+    uint32_t zb = (uint32_t)((hn / 4 + 255) / 256);
     if (zb > 4096) zb = 4096;
-    hipLaunchKernelGGL(topk_zero_hist, dim3(zb), dim3(256), 0, s, ws.t_hist, hn);
+    hipLaunchKernelGGL(topk_zero_hist, dim3(zb), dim3(256), 0, s, ws.t_hist, hn, ws.t_any);
     if (kind == 0) {  // exact
-        hipLaunchKernelGGL(topk_hist_pass, dim3(C), blk, 0, s, d, T, 1, 0, ws);
+        hipLaunchKernelGGL(topk_hist_pass, dim3(C), blk, 0, s, d, T, C, 1, 0, ws);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindThrExact, 0, ws);
-        hipLaunchKernelGGL(topk_compact, dim3(C), blk, 0, s, d, T, 0, 0, ws);
+        hipLaunchKernelGGL(topk_compact, dim3(C), blk, 0, s, d, T, C, 0, 0, ws);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit0, 0, ws);
     } else {  // sampled threshold, exact fallback per tensor
         hipLaunchKernelGGL(topk_sample_hist, dim3((C + kSampleChunksPerBlock - 1) / kSampleChunksPerBlock), blk,
                            0, s, d, T, C, seed, ws);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindThrSample, 0, ws);
-        hipLaunchKernelGGL(topk_compact, dim3(C), blk, 0, s, d, T, 1, 0, ws);
+        hipLaunchKernelGGL(topk_compact, dim3(C), blk, 0, s, d, T, C, 1, 0, ws);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit0, 0, ws);
-        hipLaunchKernelGGL(topk_hist_pass, dim3(C), blk, 0, s, d, T, 0, 1, ws);
+        // fallback passes: small grids that walk the chunks, and return at
+        // once when no tensor fell back (the usual case)
+        const dim3 fb_grid(C < 1024u ? C : 1024u);
+        hipLaunchKernelGGL(topk_hist_pass, fb_grid, blk, 0, s, d, T, C, 0, 1, ws);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindThrExact, 1, ws);
-        hipLaunchKernelGGL(topk_compact, dim3(C), blk, 0, s, d, T, 0, 1, ws);
+        hipLaunchKernelGGL(topk_compact, fb_grid, blk, 0, s, d, T, C, 0, 1, ws);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit0, 1, ws);
     }
-    hipLaunchKernelGGL(topk_cand_hist, dim3(C), blk, 0, s, d, T, 1, ws);
+    uint32_t span = C / 1024u;
+    span = span < 1u ? 1u : (span > 16u ? 16u : span);
+    const dim3 hist_grid((C + span - 1) / span);
+    const dim3 wave_grid((C + kBlock / 64 - 1) / (kBlock / 64));
+    hipLaunchKernelGGL(topk_cand_hist, hist_grid, blk, 0, s, d, T, C, span, 1, ws);
     hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit1, 0, ws);
-    hipLaunchKernelGGL(topk_cand_hist, dim3(C), blk, 0, s, d, T, 2, ws);
+    hipLaunchKernelGGL(topk_cand_hist, hist_grid, blk, 0, s, d, T, C, span, 2, ws);
     hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit2, 0, ws);
-    hipLaunchKernelGGL(topk_cand_count, dim3(C), blk, 0, s, d, T, ws);
+    hipLaunchKernelGGL(topk_cand_count, wave_grid, blk, 0, s, d, T, C, ws);
     hipLaunchKernelGGL(topk_cand_scan, dim3(T), blk, 0, s, d, ws);
-    hipLaunchKernelGGL(topk_emit, dim3(C), blk, 0, s, d, T, idx, val, ws);
+    hipLaunchKernelGGL(topk_emit, wave_grid, blk, 0, s, d, T, C, idx, val, ws);
     return hipGetLastError();
 }
 

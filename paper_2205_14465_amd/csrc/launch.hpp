@@ -26,6 +26,7 @@ struct Ws {
     uint32_t* t_prefix;     // [T] radix-select prefix (key)
     uint32_t* t_krem;       // [T] entries still to select
     uint32_t* t_fb;         // [T] 1 = tensor needs the exact-histogram fallback
+    uint32_t* t_any;        // [1] nonzero when some tensor of the call needs it
     uint2* t_cand;          // [C * 4096] candidates (local index, value bits)
     uint32_t* t_ccount;     // [C] candidates per chunk
     uint32_t* t_gt;         // [C] candidates above the threshold key
@@ -45,7 +46,7 @@ struct Ws {
 // size.  Regions a kind does not use have size 0.
 struct WsPlan {
     size_t flags, s_val, s_partial, s_info, s_tab;
-    size_t t_hist, t_thr, t_prefix, t_krem, t_fb, t_cand, t_ccount, t_gt, t_eq, t_off, t_eqb;
+    size_t t_hist, t_thr, t_prefix, t_krem, t_fb, t_any, t_cand, t_ccount, t_gt, t_eq, t_off, t_eqb;
     size_t r_keys, r_tmp, r_ccount, r_coff, r_cursor;
     size_t total;
 };

@@ -433,7 +433,16 @@ int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, 
     if (!ws) return BC_E_WORKSPACE;
     if (ws_bytes < 256) return BC_E_WORKSPACE;
     const bool sparse = is_sparse(kind);
-    const uint32_t unit = sparse ? kSparseTile : kSignAggUnit;
+    uint32_t unit = kSignAggUnit;
+    if (sparse) {
+        uint64_t nt = 0, kt = 0;
+        for (int i = 0; i < T; ++i) {
+            if (n[i] >= kMaxN) return BC_E_SIZE;
+            nt += n[i];
+            kt += k_of(n[i], ppm);
+        }
+        unit = sparse_agg_tile(nt, kt);
+    }
     std::vector<unsigned char> table;
     try {
         table.resize((size_t)T * sizeof(ADesc) + (size_t)2 * padded_workers(W) * sizeof(uint64_t));
@@ -505,7 +514,7 @@ int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, 
     const ADesc* ad = (const ADesc*)en->dev;
     const uint64_t* wdd = (const uint64_t*)((const char*)en->dev + (size_t)T * sizeof(ADesc));
     if (sparse) {
-        e = launch_aggregate_sparse(ad, T, (uint32_t)units, wdd, W, alpha, s);
+        e = launch_aggregate_sparse(ad, T, (uint32_t)units, unit, wdd, W, alpha, di.cus, s);
     } else {
         e = launch_aggregate_sign(ad, T, (uint32_t)units, wdd, W, alpha, w.s_info, w.s_tab, s);
     }

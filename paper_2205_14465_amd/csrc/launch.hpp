@@ -73,8 +73,11 @@ hipError_t launch_randk(uint64_t seed, const TDesc* d, int T, uint32_t C, uint64
 hipError_t launch_residual_update(int kind, const TDesc* d, int T, uint32_t C, bool any_f16,
                                   bool any_f32, const uint32_t* idx, const float* val,
                                   const uint32_t* bits, const float* scale, hipStream_t s);
-hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t units, const uint64_t* wp, int W,
-                                   float alpha, hipStream_t s);
+// Sparse aggregate tile (elements per work unit) for a call whose tensors
+// hold n_total elements and k_total entries per worker.
+uint32_t sparse_agg_tile(uint64_t n_total, uint64_t k_total);
+hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t units, uint32_t tile, const uint64_t* wp,
+                                   int W, float alpha, int cus, hipStream_t s);
 hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t units, const uint64_t* wp, int W,
                                  float alpha, uint32_t* info, int32_t* tabs, hipStream_t s);
 
@@ -82,7 +85,6 @@ hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t units, const ui
 // Worker descriptors in the aggregate table are padded to a multiple of 16.
 __host__ __device__ constexpr int padded_workers(int W) { return (W + 15) & ~15; }
 
-constexpr uint32_t kSparseTile = 2048;   // one wave's LDS tile
 constexpr uint32_t kSignAggUnit = 4096;  // one workgroup: 16 elements per lane
 
 }  // namespace bc

@@ -58,7 +58,8 @@ enum bc_status {
     BC_E_KIND = -2,       /* unknown kind                                     */
     BC_E_DTYPE = -3,      /* unknown gradient dtype                           */
     BC_E_RATIO = -4,      /* ratio outside (0, 1] or below one part per million */
-    BC_E_SIZE = -5,       /* a tensor has 2^32 or more elements               */
+    BC_E_SIZE = -5,       /* a tensor has 2^32 or more elements, or a call is
+                             beyond a kind's limits (see bytecomp_compress)   */
     BC_E_COUNT = -6,      /* T < 0, W < 1, or too many tensors/workers        */
     BC_E_WORKSPACE = -7,  /* workspace NULL or smaller than required          */
     BC_E_HIP = -8,        /* a HIP runtime call failed                        */
@@ -135,7 +136,10 @@ int bytecomp_workspace_init(void* ws, size_t ws_bytes, void* stream);
  * from a keyed permutation of [0, n_t); both emit indices ascending with
  * values v[idx]; the residual becomes v with the selected entries +0.0.
  * BC_SIGN1 emits the sign bits of v and scale s_t = mean |v| (summed in
- * fp64) rounded to fp32; the residual becomes v - (bit ? -s_t : +s_t). */
+ * fp64) rounded to fp32; the residual becomes v - (bit ? -s_t : +s_t).
+ * Limits of BC_RANDK: fewer than 2^32 payload entries in the call and at
+ * most 2^22 chunks of 4096 elements (about 1.7e10 elements); BC_E_SIZE
+ * otherwise. */
 int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t, int T,
                       bc_payload out, void* ws, size_t ws_bytes, void* stream);
 

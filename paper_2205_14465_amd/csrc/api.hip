@@ -194,12 +194,15 @@ WsPlan plan_workspace(int kind, int T, uint64_t C, uint64_t sum_k) {
         take(p.t_off, (size_t)C * 8);
         take(p.t_eqb, (size_t)C * 4);
     } else if (kind == BC_RANDK) {
-        const size_t nb = ((size_t)C + kBlock * 16 - 1) / (kBlock * 16);
+        uint32_t S = 0, NB = 0;
+        randk_buckets((uint32_t)(C < 0xFFFFFFFFull ? C : 0xFFFFFFFFull), &S, &NB);
+        const size_t nscan = ((size_t)NB + kBlock * 16 - 1) / (kBlock * 16);
+        const size_t nblk = (size_t)((sum_k + kGenEntries - 1) / kGenEntries);
         take(p.r_keys, t * 16);
         take(p.r_tmp, (size_t)sum_k * 4);
-        take(p.r_ccount, (size_t)C * 4);
-        take(p.r_coff, ((size_t)C + 1 + nb) * 8);
-        take(p.r_cursor, (size_t)C * 8);
+        take(p.r_ccount, (size_t)NB * 4);
+        take(p.r_coff, ((size_t)NB + 1 + nscan) * 8);
+        take(p.r_hist, nblk * NB * 4);
     }
     p.total = at;
     return p;
@@ -231,7 +234,7 @@ Ws carve_workspace(void* base, const WsPlan& p) {
     w.r_tmp = (uint32_t*)at(p.r_tmp);
     w.r_ccount = (uint32_t*)at(p.r_ccount);
     w.r_coff = (uint64_t*)at(p.r_coff);
-    w.r_cursor = (unsigned long long*)at(p.r_cursor);
+    w.r_hist = (uint32_t*)at(p.r_hist);
     return w;
 }
 
@@ -389,6 +392,8 @@ int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t,
         return BC_E_SIZE;
     }
     if (rc) return rc;
+    // random-k: payload positions are 32-bit and the bucket count is bounded
+    if (kind == BC_RANDK && (sum_k >= (1ull << 32) || !randk_buckets(C, nullptr, nullptr))) return BC_E_SIZE;
     const WsPlan plan = plan_workspace(kind, T, C, sum_k);
     if (ws_bytes < plan.total) return BC_E_WORKSPACE;
     hipStream_t s = (hipStream_t)stream;

@@ -11,17 +11,25 @@
 // bits; round function: the "lowbias32" integer hash (C. Wellons,
 // hash-prospector) of the right half xor the round key.
 //
-// Instead of sorting the k indices, they are bucketed by the 4096-element
-// chunk they fall in (counts, scan, scatter); the streaming pass over each
-// chunk then marks its indices in an LDS bitmap, zeroes them in e_new and
-// emits (index, v) in index order, which is the sorted payload.
+// Instead of sorting the k indices, they are bucketed by runs of 2^S
+// consecutive 4096-element chunks (S from the call's chunk count): each
+// generating workgroup histograms its indices in LDS and writes one row of
+// per-bucket counts, a column pass and a scan give every workgroup its
+// position in every bucket, and a second pass places the indices there, so
+// no global atomics are used.  The streaming pass then takes one bucket per
+// workgroup: it marks the bucket's indices in an LDS bitmap, and for each
+// chunk zeroes them in e_new and emits (index, v) in index order, which is
+// the sorted payload.
 #include "launch.hpp"
+
+#include <mutex>
 
 namespace bc {
 
 namespace {
 
-constexpr int kScanBlock = kBlock * 16;  // chunk counters per scan block
+constexpr int kScanBlock = kBlock * 16;  // bucket sizes per scan block
+constexpr int kColBlock = 1024;          // threads of the column pass
 
 __device__ __forceinline__ uint32_t lowbias32(uint32_t x) {
     x ^= x >> 16;
@@ -62,11 +70,9 @@ __device__ __forceinline__ int tensor_of_entry(const TDesc* __restrict__ d, int 
 
 }  // namespace
 
-// Per-call preparation: clear the chunk counters, derive the round keys.
-__global__ void randk_prep(const TDesc* __restrict__ d, int T, uint32_t C, uint64_t seed, Ws ws) {
-    const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < C) ws.r_ccount[i] = 0u;
-    const int t = (int)i;
+// Per-call preparation: derive the round keys.
+__global__ void randk_prep(const TDesc* __restrict__ d, int T, uint64_t seed, Ws ws) {
+    const int t = (int)(blockIdx.x * blockDim.x + threadIdx.x);
     if (t >= T) return;
     U64x4 ctr = {{(uint64_t)d[t].tid, 0, 0, 0}};
     const U64x4 w = philox4x64_10(ctr, seed, kStreamRandk);
@@ -74,154 +80,373 @@ __global__ void randk_prep(const TDesc* __restrict__ d, int T, uint32_t C, uint6
     for (int r = 0; r < 4; ++r) ws.r_keys[4 * t + r] = (uint32_t)w.v[r] ^ (uint32_t)(w.v[r] >> 32);
 }
 
-// One thread per payload entry: generate the index, count it in its chunk.
-__global__ __launch_bounds__(kBlock) void randk_gen(const TDesc* __restrict__ d, int T,
-                                                    uint64_t sum_k, Ws ws) {
-    const uint64_t j = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (j >= sum_k) return;
-    const int t = tensor_of_entry(d, T, j);
+
+// A thread's view of the tensor that owns its current entry: what index
+// generation and bucketing need, refreshed only when an entry crosses into
+// a later tensor (entries are visited in increasing order).
+struct EntryTensor {
+    int t;
+    uint64_t off, next_off;  // first entry of this tensor and of the next
+    uint32_t n, chunk0, h, mask;
+    uint4 rk;
+};
+
+__device__ __forceinline__ void entry_tensor_load(const TDesc* __restrict__ d, int T, const uint32_t* keys,
+                                                  int t, EntryTensor& et) {
     const TDesc td = d[t];
-    const uint4 rk = *reinterpret_cast<const uint4*>(ws.r_keys + 4 * t);
-    const uint32_t h = half_bits(td.n);
-    const uint32_t mask = h >= 32 ? 0xFFFFFFFFu : ((1u << h) - 1u);
-    uint32_t x = feistel((uint32_t)(j - td.off), h, mask, rk);
-    while (x >= td.n) x = feistel(x, h, mask, rk);
-    ws.r_tmp[j] = x;
-    atomicAdd(ws.r_ccount + td.chunk0 + x / (uint32_t)kChunk, 1u);
+    et.t = t;
+    et.off = td.off;
+    et.next_off = t + 1 < T ? d[t + 1].off : ~0ull;
+    et.n = td.n;
+    et.chunk0 = td.chunk0;
+    et.h = half_bits(td.n);
+    et.mask = et.h >= 32 ? 0xFFFFFFFFu : ((1u << et.h) - 1u);
+    et.rk = *reinterpret_cast<const uint4*>(keys + 4 * t);
 }
 
-// Scan, step 1: sum of each block of 4096 chunk counters.
-__global__ __launch_bounds__(kBlock) void randk_scan_sums(uint32_t C, Ws ws, uint64_t* bsum) {
+__device__ __forceinline__ void entry_tensor_advance(const TDesc* __restrict__ d, int T, const uint32_t* keys,
+                                                     uint64_t j, EntryTensor& et) {
+    if (j < et.next_off) return;
+    int t = et.t;
+    while (t + 1 < T && d[t + 1].off <= j) ++t;
+    entry_tensor_load(d, T, keys, t, et);
+}
+
+// Generate the indices of kGenEntries consecutive payload entries, keep
+// them in r_tmp, and write this workgroup's row of bucket counts.
+__global__ __launch_bounds__(kGenBlock) void randk_count(const TDesc* __restrict__ d, int T, uint64_t sum_k,
+                                                         uint32_t S, uint32_t NB, Ws ws) {
+    extern __shared__ uint32_t hist[];  // [NB]
+    for (uint32_t b = threadIdx.x; b < NB; b += kGenBlock) hist[b] = 0;
+    __syncthreads();
+    const uint64_t j0 = (uint64_t)blockIdx.x * kGenEntries + threadIdx.x;
+    EntryTensor et;
+    if (j0 < sum_k) entry_tensor_load(d, T, ws.r_keys, tensor_of_entry(d, T, j0), et);
+    for (int q = 0; q < kGenPerThread; ++q) {
+        const uint64_t j = j0 + (uint64_t)q * kGenBlock;
+        if (j >= sum_k) break;
+        entry_tensor_advance(d, T, ws.r_keys, j, et);
+        uint32_t x = feistel((uint32_t)(j - et.off), et.h, et.mask, et.rk);
+        while (x >= et.n) x = feistel(x, et.h, et.mask, et.rk);
+        ws.r_tmp[j] = x;
+        atomicAdd(&hist[(et.chunk0 + x / (uint32_t)kChunk) >> S], 1u);
+    }
+    __syncthreads();
+    uint32_t* row = ws.r_hist + (size_t)blockIdx.x * NB;
+    for (uint32_t b = threadIdx.x; b < NB; b += kGenBlock) row[b] = hist[b];
+}
+
+// Per-workgroup counts to positions within each bucket: a workgroup of 16
+// waves takes 64 buckets (one per lane); wave w sums its share of the
+// generating workgroups' rows, the shares are combined in LDS, and each
+// wave then writes the exclusive prefix down its rows.  The bucket's size
+// goes to r_ccount.
+__global__ __launch_bounds__(kColBlock) void randk_columns(uint32_t NB, uint32_t nblk, Ws ws) {
+    __shared__ uint32_t part[kColBlock / 64][64];
+    const int lane = lane_id();
+    const int w = threadIdx.x >> 6;
+    const uint32_t bk = blockIdx.x * 64u + (uint32_t)lane;
+    const uint32_t per = (nblk + kColBlock / 64 - 1) / (kColBlock / 64);
+    const uint32_t g0 = (uint32_t)w * per;
+    const uint32_t g1 = g0 + per < nblk ? g0 + per : nblk;
+    const bool live = bk < NB;
+    uint32_t sum = 0;
+    for (uint32_t g = g0; g < g1; ++g) sum += live ? ws.r_hist[(size_t)g * NB + bk] : 0u;
+    part[w][lane] = sum;
+    __syncthreads();
+    uint32_t acc = 0, total = 0;
+    for (int q = 0; q < kColBlock / 64; ++q) {
+        acc += q < w ? part[q][lane] : 0u;
+        total += part[q][lane];
+    }
+    if (!live) return;
+    for (uint32_t g = g0; g < g1; ++g) {
+        uint32_t* p = ws.r_hist + (size_t)g * NB + bk;
+        const uint32_t c = *p;
+        *p = acc;
+        acc += c;
+    }
+    if (w == 0) ws.r_ccount[bk] = total;
+}
+
+// Scan, step 1: sum of each block of 4096 bucket sizes.
+__global__ __launch_bounds__(kBlock) void randk_scan_sums(uint32_t NB, Ws ws, uint64_t* bsum) {
     __shared__ uint64_t sh[4];
     const uint32_t b0 = blockIdx.x * (uint32_t)kScanBlock;
     uint64_t x = 0;
     for (int q = 0; q < 16; ++q) {
         const uint32_t c = b0 + q * kBlock + threadIdx.x;
-        if (c < C) x += ws.r_ccount[c];
+        if (c < NB) x += ws.r_ccount[c];
     }
     uint64_t tot;
     block_excl_scan_u64(x, sh, tot);
     if (threadIdx.x == 0) bsum[blockIdx.x] = tot;
 }
 
-// Scan, step 2: chunk payload offsets and scatter cursors.
-__global__ __launch_bounds__(kBlock) void randk_scan_apply(uint32_t C, Ws ws, const uint64_t* bsum) {
+// Scan, step 2: payload position of each bucket's first entry.
+__global__ __launch_bounds__(kBlock) void randk_scan_apply(uint32_t NB, Ws ws, const uint64_t* bsum) {
     __shared__ uint64_t sh[4];
     uint64_t pre = 0;
     for (uint32_t b = threadIdx.x; b < blockIdx.x; b += kBlock) pre += bsum[b];
     uint64_t base;
     block_excl_scan_u64(pre, sh, base);
-    // thread i owns 16 consecutive counters
+    // thread i owns 16 consecutive bucket sizes
     const uint32_t c0 = blockIdx.x * (uint32_t)kScanBlock + threadIdx.x * 16u;
     uint32_t cnt[16];
     uint64_t mine = 0;
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
-        cnt[q] = (c0 + q < C) ? ws.r_ccount[c0 + q] : 0u;
+        cnt[q] = (c0 + q < NB) ? ws.r_ccount[c0 + q] : 0u;
         mine += cnt[q];
     }
     uint64_t tot;
     uint64_t run = base + block_excl_scan_u64(mine, sh, tot);
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
-        if (c0 + q < C) {
-            ws.r_coff[c0 + q] = run;
-            ws.r_cursor[c0 + q] = run;
-        }
+        if (c0 + q < NB) ws.r_coff[c0 + q] = run;
         run += cnt[q];
     }
-    if (c0 < C && c0 + 16 >= C) ws.r_coff[C] = run;  // the thread holding the last counter
+    if (c0 < NB && c0 + 16 >= NB) ws.r_coff[NB] = run;  // the thread holding the last size
 }
 
-// Scatter each generated index into its chunk's bucket of the payload.
-__global__ __launch_bounds__(kBlock) void randk_scatter(const TDesc* __restrict__ d, int T,
-                                                        uint64_t sum_k, uint32_t* __restrict__ idx,
-                                                        Ws ws) {
-    const uint64_t j = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (j >= sum_k) return;
-    const int t = tensor_of_entry(d, T, j);
-    const uint32_t x = ws.r_tmp[j];
-    const uint32_t c = d[t].chunk0 + x / (uint32_t)kChunk;
-    const unsigned long long pos = atomicAdd(ws.r_cursor + c, 1ull);
-    if (pos < sum_k) idx[pos] = x;
+// Place each generated index in its bucket: the workgroup's position in the
+// bucket (payload start + column prefix) plus a rank taken in LDS.  The
+// value stored is the index's position within the bucket's 2^S chunks.
+__global__ __launch_bounds__(kGenBlock) void randk_place(const TDesc* __restrict__ d, int T, uint64_t sum_k,
+                                                         uint32_t S, uint32_t NB, uint32_t* __restrict__ idx,
+                                                         Ws ws) {
+    extern __shared__ uint32_t lds[];
+    uint32_t* base = lds;       // [NB] this workgroup's first position in each bucket
+    uint32_t* rank = lds + NB;  // [NB] entries placed so far
+    const uint32_t* row = ws.r_hist + (size_t)blockIdx.x * NB;
+    for (uint32_t b = threadIdx.x; b < NB; b += kGenBlock) {
+        base[b] = (uint32_t)ws.r_coff[b] + row[b];
+        rank[b] = 0;
+    }
+    __syncthreads();
+    const uint64_t j0 = (uint64_t)blockIdx.x * kGenEntries + threadIdx.x;
+    EntryTensor et;
+    if (j0 < sum_k) entry_tensor_load(d, T, ws.r_keys, tensor_of_entry(d, T, j0), et);
+    for (int q = 0; q < kGenPerThread; ++q) {
+        const uint64_t j = j0 + (uint64_t)q * kGenBlock;
+        if (j >= sum_k) break;
+        entry_tensor_advance(d, T, ws.r_keys, j, et);
+        const uint32_t x = ws.r_tmp[j];
+        const uint32_t gc = et.chunk0 + x / (uint32_t)kChunk;
+        const uint32_t b = gc >> S;
+        const uint32_t pos = base[b] + atomicAdd(&rank[b], 1u);
+        idx[pos] = ((gc - (b << S)) << 12) | (x & (uint32_t)(kChunk - 1));
+    }
 }
 
-// Stream pass: mark the chunk's indices, write e_new, emit sorted entries.
-__global__ __launch_bounds__(kBlock) void randk_stream(const TDesc* __restrict__ d, int T,
-                                                       uint32_t* __restrict__ idx,
+// One bucket per workgroup.  The bucket's indices are marked in an LDS
+// bitmap; per-chunk counts of the bitmap and their prefix give each chunk's
+// payload position.  Then every wave streams whole chunks on its own (no
+// workgroup barrier): lane l holds elements 256 r + 4 l + i (r < 16, i < 4)
+// of the chunk, writes e_new (selected entries zeroed) and emits its
+// selected (index, v) pairs at positions from a wave prefix over the
+// rounds, which is ascending index order.
+__global__ __launch_bounds__(kBlock) void randk_stream(const TDesc* __restrict__ d, int T, uint32_t C,
+                                                       uint32_t S, uint32_t* __restrict__ idx,
                                                        float* __restrict__ val, Ws ws) {
-    __shared__ uint32_t bm[kChunkWords];
-    __shared__ uint64_t sh[4];
-    const uint32_t c = blockIdx.x;
-    const int t = tensor_of_chunk(d, T, c);
-    const TDesc td = d[t];
-    const uint32_t j = c - td.chunk0;
-    const uint32_t lo = j * (uint32_t)kChunk;
-    const uint64_t beg = ws.r_coff[c], end = ws.r_coff[c + 1];
-    if (threadIdx.x < kChunkWords) bm[threadIdx.x] = 0u;
+    extern __shared__ uint32_t bm[];  // [2^S * 128] bits of the bucket's chunks
+    __shared__ uint32_t coff[(1u << kRandkMaxShift) + 1];
+    const int lane = lane_id();
+    const int wave = wave_id();
+    const uint32_t b = blockIdx.x;
+    const uint32_t c0 = b << S;
+    const uint32_t nc = (C - c0 < (1u << S)) ? C - c0 : (1u << S);
+    const uint64_t beg = ws.r_coff[b], end = ws.r_coff[b + 1];
+    for (uint32_t i = threadIdx.x; i < nc * (uint32_t)kChunkWords; i += kBlock) bm[i] = 0u;
     __syncthreads();
     for (uint64_t i = beg + threadIdx.x; i < end; i += kBlock) {
-        const uint32_t e = idx[i] - lo;
-        if (e < (uint32_t)kChunk) atomicOr(&bm[e >> 5], 1u << (e & 31));
+        const uint32_t y = idx[i];
+        if (y < (nc << 12)) atomicOr(&bm[y >> 5], 1u << (y & 31));
     }
-    float v[kEpt];
-    uint32_t valid;
-    load_v(td, j, td.resid != nullptr, v, valid);
     __syncthreads();
-    uint32_t pm = 0;
+    // selected entries per chunk (one wave per chunk), then their prefix
+    for (uint32_t q = (uint32_t)wave; q < nc; q += kBlock / 64) {
+        uint32_t c = __popc(bm[q * (uint32_t)kChunkWords + lane]) + __popc(bm[q * (uint32_t)kChunkWords + 64 + lane]);
 #pragma unroll
-    for (int r = 0; r < kRounds; ++r) {
-        const uint32_t word = bm[32 * r + (threadIdx.x >> 3)];
-        pm |= ((word >> (4 * (threadIdx.x & 7))) & 0xFu) << (4 * r);
+        for (int o = 32; o >= 1; o >>= 1) c += __shfl_xor(c, o, 64);
+        if (lane == 0) coff[q] = c;
     }
-    pm &= valid;
-    if (td.resid) {
-        float e_new[kEpt];
+    __syncthreads();
+    if (wave == 0) {
+        // exclusive prefix of nc <= 256 counts: four per lane
+        uint32_t x[4], run = 0;
 #pragma unroll
-        for (int i = 0; i < kEpt; ++i) e_new[i] = ((pm >> i) & 1u) ? 0.f : v[i];
-        store_chunk(td.resid, td.n, j, e_new);
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t q = 4u * lane + i;
+            x[i] = q < nc ? coff[q] : 0u;
+            run += x[i];
+        }
+        uint32_t inc = run;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const uint32_t y = __shfl_up(inc, o, 64);
+            if (lane >= o) inc += y;
+        }
+        uint32_t at = inc - run;
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t q = 4u * lane + i;
+            if (q <= nc) coff[q] = at;
+            at += x[i];
+        }
     }
-    uint64_t packed = 0;
+    __syncthreads();
+    for (uint32_t q = (uint32_t)wave; q < nc; q += kBlock / 64) {
+        const TDesc td = d[tensor_of_chunk(d, T, c0 + q)];
+        const uint32_t j = c0 + q - td.chunk0;
+        const bool use_e = td.resid != nullptr;
+        uint64_t base = beg + coff[q];
+        // the chunk in two halves of 2048 elements, emitted in order
+        for (uint32_t half = 0; half < 2; ++half) {
+            const uint32_t lo = j * (uint32_t)kChunk + 2048u * half;
+            float v[32];
+            uint32_t valid = 0;
 #pragma unroll
-    for (int r = 0; r < kRounds; ++r) packed |= (uint64_t)__popc((pm >> (4 * r)) & 0xFu) << (16 * r);
-    uint64_t tot;
-    const uint64_t pre = block_excl_scan_u64(packed, sh, tot);
-    uint64_t base = beg;
+            for (int r = 0; r < 8; ++r) {
+                const uint32_t e0 = lo + 256u * r + 4u * (uint32_t)lane;
+                float g4[4] = {0.f, 0.f, 0.f, 0.f}, e4[4] = {0.f, 0.f, 0.f, 0.f};
+                if (e0 + 3 < td.n) {
+                    if (td.dtype == 0) {
+                        const f32x4 x = ldg4f((const float*)td.grad + e0);
+                        g4[0] = x.x; g4[1] = x.y; g4[2] = x.z; g4[3] = x.w;
+                    } else {
+                        const u32x2 h = ldg2u((const uint16_t*)td.grad + e0);
+                        g4[0] = h2f(h.x & 0xFFFFu);
+                        g4[1] = h2f(h.x >> 16);
+                        g4[2] = h2f(h.y & 0xFFFFu);
+                        g4[3] = h2f(h.y >> 16);
+                    }
+                    if (use_e) {
+                        const f32x4 y = ldg4f(td.resid + e0);
+                        e4[0] = y.x; e4[1] = y.y; e4[2] = y.z; e4[3] = y.w;
+                    }
+                    valid |= 0xFu << (4 * r);
+                } else {
 #pragma unroll
-    for (int r = 0; r < kRounds; ++r) {
-        uint64_t at = base + ((pre >> (16 * r)) & 0xFFFFu);
+                    for (int i = 0; i < 4; ++i) {
+                        if (e0 + i < td.n) {
+                            g4[i] = td.dtype == 0 ? gp((const float*)td.grad)[e0 + i]
+                                                  : h2f(gp((const uint16_t*)td.grad)[e0 + i]);
+                            if (use_e) e4[i] = gp(td.resid)[e0 + i];
+                            valid |= 1u << (4 * r + i);
+                        }
+                    }
+                }
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int i = 4 * r + q;
-            if ((pm >> i) & 1u) {
-                idx[at] = lo + 1024u * r + 4u * threadIdx.x + q;
-                val[at] = v[i];
-                ++at;
+                for (int i = 0; i < 4; ++i) v[4 * r + i] = use_e ? g4[i] + e4[i] : g4[i];
+            }
+            uint32_t pm = 0;
+#pragma unroll
+            for (int r = 0; r < 8; ++r) {
+                const uint32_t word = bm[q * (uint32_t)kChunkWords + 64u * half + 8 * r + (lane >> 3)];
+                pm |= ((word >> (4 * (lane & 7))) & 0xFu) << (4 * r);
+            }
+            pm &= valid;
+            if (use_e) {
+#pragma unroll
+                for (int r = 0; r < 8; ++r) {
+                    const uint32_t e0 = lo + 256u * r + 4u * (uint32_t)lane;
+                    float o[4];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) o[i] = ((pm >> (4 * r + i)) & 1u) ? 0.f : v[4 * r + i];
+                    if (e0 + 3 < td.n) {
+                        stg4f(td.resid + e0, f32x4{o[0], o[1], o[2], o[3]});
+                    } else {
+#pragma unroll
+                        for (int i = 0; i < 4; ++i)
+                            if (e0 + i < td.n) gp(td.resid)[e0 + i] = o[i];
+                    }
+                }
+            }
+            // positions: 16-bit per-round counts, four rounds per 64-bit word,
+            // scanned over the lanes; a round's base is the sum of earlier rounds
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                uint64_t packed = 0;
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    packed |= (uint64_t)__popc((pm >> (16 * h + 4 * r)) & 0xFu) << (16 * r);
+                uint64_t inc = packed;
+#pragma unroll
+                for (int o = 1; o < 64; o <<= 1) {
+                    const uint64_t y = __shfl_up(inc, o, 64);
+                    if (lane >= o) inc += y;
+                }
+                const uint64_t tot = __shfl(inc, 63, 64);
+                const uint64_t pre = inc - packed;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int rr = 4 * h + r;
+                    uint64_t at = base + ((pre >> (16 * r)) & 0xFFFFu);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        if (((pm >> (4 * rr + i)) & 1u) && at < end) {  // the bucket's range bounds every write
+                            idx[at] = lo + 256u * rr + 4u * (uint32_t)lane + i;
+                            val[at] = v[4 * rr + i];
+                            ++at;
+                        }
+                    }
+                    base += (tot >> (16 * r)) & 0xFFFFu;
+                }
             }
         }
-        base += (tot >> (16 * r)) & 0xFFFFu;
     }
 }
+
+bool randk_buckets(uint32_t C, uint32_t* S, uint32_t* NB) {
+    uint32_t s = 0;
+    while (s < kRandkMaxShift && ((C + (1u << s) - 1) >> s) > kRandkBuckets) ++s;
+    const uint32_t nb = (C + (1u << s) - 1) >> s;
+    if (S) *S = s;
+    if (NB) *NB = nb;
+    return nb <= kRandkMaxBuckets;
+}
+
+namespace {
+// Dynamic LDS beyond 64 KiB must be allowed per kernel; raise a kernel's
+// limit to what a call needs (at most 2^8 chunks of bitmap, 128 KiB).
+hipError_t need_lds(const void* f, size_t bytes, size_t& allowed) {
+    if (bytes <= 64 * 1024 || bytes <= allowed) return hipSuccess;
+    const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    if (e == hipSuccess) allowed = bytes;
+    return e;
+}
+std::mutex g_lds_mu;
+size_t g_lds_place = 0, g_lds_stream = 0;
+}  // namespace
 
 hipError_t launch_randk(uint64_t seed, const TDesc* d, int T, uint32_t C, uint64_t sum_k, bool,
                         bool, uint32_t* idx, float* val, const Ws& ws, hipStream_t s) {
     if (C == 0 || T == 0) return hipSuccess;
+    uint32_t S, NB;
+    if (!randk_buckets(C, &S, &NB) || sum_k >= (1ull << 32)) return hipErrorInvalidValue;
+    const size_t lds_place = (size_t)NB * 8, lds_stream = ((size_t)kChunkWords * 4) << S;
+    {
+        std::lock_guard<std::mutex> lk(g_lds_mu);
+        hipError_t e = need_lds((const void*)randk_place, lds_place, g_lds_place);
+        if (e == hipSuccess) e = need_lds((const void*)randk_stream, lds_stream, g_lds_stream);
+        if (e != hipSuccess) return e;
+    }
     const dim3 blk(kBlock);
-    const uint32_t nb = (C + kScanBlock - 1) / kScanBlock;
-    uint64_t* bsum = ws.r_coff + (size_t)C + 1;  // scratch after the offsets
-    const uint32_t prep = ((uint32_t)T > C ? (uint32_t)T : C);
-    hipLaunchKernelGGL(randk_prep, dim3((prep + 255) / 256), dim3(256), 0, s, d, T, C, seed, ws);
-    if (sum_k) {
-        const uint64_t g = (sum_k + kBlock - 1) / kBlock;
-        hipLaunchKernelGGL(randk_gen, dim3((uint32_t)g), blk, 0, s, d, T, sum_k, ws);
+    const uint32_t nscan = (NB + kScanBlock - 1) / kScanBlock;
+    uint64_t* bsum = ws.r_coff + (size_t)NB + 1;  // scratch after the bucket offsets
+    hipLaunchKernelGGL(randk_prep, dim3((T + 255) / 256), dim3(256), 0, s, d, T, seed, ws);
+    const uint32_t nblk = (uint32_t)((sum_k + kGenEntries - 1) / kGenEntries);
+    if (nblk) {
+        hipLaunchKernelGGL(randk_count, dim3(nblk), dim3(kGenBlock), (size_t)NB * 4, s, d, T, sum_k, S, NB, ws);
     }
-    hipLaunchKernelGGL(randk_scan_sums, dim3(nb), blk, 0, s, C, ws, bsum);
-    hipLaunchKernelGGL(randk_scan_apply, dim3(nb), blk, 0, s, C, ws, bsum);
-    if (sum_k) {
-        const uint64_t g = (sum_k + kBlock - 1) / kBlock;
-        hipLaunchKernelGGL(randk_scatter, dim3((uint32_t)g), blk, 0, s, d, T, sum_k, idx, ws);
-    }
-    hipLaunchKernelGGL(randk_stream, dim3(C), blk, 0, s, d, T, idx, val, ws);
+    hipLaunchKernelGGL(randk_columns, dim3((NB + 63) / 64), dim3(kColBlock), 0, s, NB, nblk, ws);
+    hipLaunchKernelGGL(randk_scan_sums, dim3(nscan), blk, 0, s, NB, ws, bsum);
+    hipLaunchKernelGGL(randk_scan_apply, dim3(nscan), blk, 0, s, NB, ws, bsum);
+    if (nblk)
+        hipLaunchKernelGGL(randk_place, dim3(nblk), dim3(kGenBlock), lds_place, s, d, T, sum_k, S, NB, idx, ws);
+    hipLaunchKernelGGL(randk_stream, dim3(NB), blk, lds_stream, s, d, T, C, S, idx, val, ws);
     return hipGetLastError();
 }
 

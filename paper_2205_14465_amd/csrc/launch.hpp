@@ -36,10 +36,11 @@ struct Ws {
     // BC_RANDK
     uint32_t* r_keys;       // [T * 4] Feistel round keys
     uint32_t* r_tmp;        // [sum k] generated indices
-    uint32_t* r_ccount;     // [C] indices per chunk          
-    uint64_t* r_coff;       // [C + 1] payload position of each chunk, then
-                            // [ceil(C / 4096)] scan block sums
-    unsigned long long* r_cursor;  // [C] scatter cursors
+    uint32_t* r_ccount;     // [NB] indices per bucket
+    uint64_t* r_coff;       // [NB + 1] payload position of each bucket, then
+                            // [ceil(NB / 4096)] scan block sums
+    uint32_t* r_hist;       // [generating workgroups * NB] per-workgroup bucket
+                            // counts, then positions within each bucket
 };
 
 // Byte offsets of every region for a call shape; `total` is the workspace
@@ -47,7 +48,7 @@ struct Ws {
 struct WsPlan {
     size_t flags, s_val, s_partial, s_info, s_tab;
     size_t t_hist, t_thr, t_prefix, t_krem, t_fb, t_any, t_cand, t_ccount, t_gt, t_eq, t_off, t_eqb;
-    size_t r_keys, r_tmp, r_ccount, r_coff, r_cursor;
+    size_t r_keys, r_tmp, r_ccount, r_coff, r_hist;
     size_t total;
 };
 
@@ -80,6 +81,19 @@ hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t units, uint32
                                    int W, float alpha, int cus, hipStream_t s);
 hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t units, const uint64_t* wp, int W,
                                  float alpha, uint32_t* info, int32_t* tabs, hipStream_t s);
+
+// Random-k bucketing: generating workgroups of kGenBlock threads handle
+// kGenEntries payload entries each; a bucket is 2^S consecutive chunks with
+// S the smallest shift giving at most kRandkBuckets buckets (S <= 8).  A
+// call whose chunk count would need more than kRandkMaxBuckets buckets is
+// refused.  randk_buckets returns false for such a call.
+constexpr int kGenBlock = 1024;
+constexpr int kGenPerThread = 32;
+constexpr uint32_t kGenEntries = (uint32_t)kGenBlock * kGenPerThread;
+constexpr uint32_t kRandkBuckets = 8192;
+constexpr uint32_t kRandkMaxBuckets = 16384;
+constexpr uint32_t kRandkMaxShift = 8;
+bool randk_buckets(uint32_t C, uint32_t* S, uint32_t* NB);
 
 // Work-unit sizes of the aggregate kernels (elements per unit).
 // Worker descriptors in the aggregate table are padded to a multiple of 16.

@@ -105,6 +105,23 @@ def test_sampled_fallback_path_matches_exact():
         assert_resid_equal(got_e, want_e)
 
 
+@pytest.mark.parametrize("T, ratio", [(9000, 0.05), (17000, 0.02), (17000, 1.0)])
+def test_randk_many_chunks(T, ratio):
+    """More than 8192 chunks: indices are bucketed by runs of 2 and 4 chunks
+    (each run here spans several tensors), and buckets of ratio 1 hold every
+    element."""
+    rng = np.random.default_rng(T)
+    ns = [int(x) for x in rng.integers(1, 4097, size=T)]
+    for z in (0, 1, T // 2, T - 1):
+        ns[z] = 0 if z != T // 2 else 4096
+    ns += [3 * 4096 + 5, 20000]
+    grads, resids = make_set(ns, rng)
+    got, got_e = gpu_compress("randk", ratio, SEED + T, grads, resids)
+    want, want_e = O.compress_set("randk", ratio, SEED + T, grads, resids)
+    assert_sparse_equal(got, want, ns)
+    assert_resid_equal(got_e, want_e)
+
+
 def test_randk_tensor_id_keys_the_stream():
     rng = np.random.default_rng(15)
     ns = [50000, 50000]

@@ -12,8 +12,9 @@ algorithmic bytes are what the method must move:
              + 4 B per tensor scale)
   aggregate: read W payloads + write the dense fp32 output (4 B/elem).
 The roofline entry reports the dominant kernel's algorithmic bytes per
-launch over its average launch time (HIP events on the launch stream)
-against the 8 TB/s HBM peak.  The CPU baseline times the oracle (single
+launch over its average launch duration (HIP events that the library
+records at that kernel's start and end, on the launch stream) against the
+8 TB/s HBM peak.  The CPU baseline times the oracle (single
 thread) on a bounded sample of the same workload.
 """
 import argparse
@@ -208,11 +209,17 @@ def main():
 
     # per-call device time: the same K steps again, with HIP events on the
     # launch stream around each call (each event costs a few microseconds
-    # of stream time, so they stay out of the region above); the aggregate
-    # call's kernels are the dominant ones
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(reps)]
+    # of stream time, so they stay out of the region above), and the
+    # dominant kernel's own duration: the library brackets its next launch
+    # with a further pair of events (hipExtLaunchKernelGGL)
+    dom_kernel = {"sign": "aggregate_sign", "randk": "randk_stream"}.get(kind, "aggregate_sparse")
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(reps)]
+    for r in range(reps):
+        for e in ev[r][4:]:
+            e.record(stream)  # creates the HIP events the library records on
     torch.cuda.synchronize()
     for r in range(reps):
+        B.bytecomp_time_next_launch(dom_kernel, ev[r][4], ev[r][5])
         ev[r][0].record(stream)
         compress()
         ev[r][1].record(stream)
@@ -220,10 +227,13 @@ def main():
         aggregate()
         ev[r][3].record(stream)
     torch.cuda.synchronize()
+    B.bytecomp_time_next_launch(None, None, None)
     comp_ms = sorted(ev[r][0].elapsed_time(ev[r][1]) for r in range(reps))
     agg_ms = sorted(ev[r][2].elapsed_time(ev[r][3]) for r in range(reps))
+    dom_ms = sorted(ev[r][4].elapsed_time(ev[r][5]) for r in range(reps))
     comp_avg = sum(comp_ms) / reps
     agg_avg = sum(agg_ms) / reps
+    dom_avg = sum(dom_ms) / reps
     assert B.bytecomp_device_status(ws) == 0
 
     # achievable-bandwidth reference and the counter calibration kernel: a
@@ -243,18 +253,13 @@ def main():
     value = (comp_b + agg_b) / step_s / 1e9
     comp_gbs = comp_b / (comp_avg * 1e-3) / 1e9
     agg_gbs = agg_b / (agg_avg * 1e-3) / 1e9
-    # Dominant kernel.  Sign: aggregate_sign is the longest single kernel of
-    # the step (longer than either compress pass); its figure is the event
-    # span of the aggregate call, which adds the short sign_agg_prep before
-    # it.  Sparse kinds: the aggregate call is one kernel; the compress call
-    # (several kernels) is reported as a whole when it takes longer.
-    if kind == "sign":
-        dom = {"kernel": "aggregate_sign", "bytes": agg_b, "ms": agg_avg,
-               "note": "event span of the aggregate call: sign_agg_prep, then aggregate_sign"}
-    elif agg_avg >= comp_avg:
-        dom = {"kernel": "aggregate_sparse", "bytes": agg_b, "ms": agg_avg}
-    else:
-        dom = {"kernel": f"compress call ({kind})", "bytes": comp_b, "ms": comp_avg}
+    # Dominant kernel: the longest single kernel of the step.  Sign:
+    # aggregate_sign (longer than either compress pass).  Top-k kinds:
+    # aggregate_sparse (longer than any compress kernel).  Random-k:
+    # randk_stream, which moves every algorithmic byte of the compress
+    # call.  Its time is its own launch duration from the events above.
+    dom_bytes = comp_b if dom_kernel == "randk_stream" else agg_b
+    dom = {"kernel": dom_kernel, "bytes": dom_bytes, "ms": dom_avg}
     achieved = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
     traffic = counted_traffic(dom["kernel"], wl.slug)
     line = {
@@ -283,7 +288,8 @@ def main():
         "copy_gbs_reference": round(copy_gbs, 1),
         "roofline": {"bound": "hbm", "kernel": dom["kernel"], "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": traffic, **({"note": dom["note"]} if "note" in dom else {})},
+                     "traffic": traffic, "kernel_ms": round(dom_avg, 4),
+                     "kernel_ms_p10_p90": [round(dom_ms[reps // 10], 4), round(dom_ms[(9 * reps) // 10], 4)]},
     }
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")

@@ -180,6 +180,16 @@ int bytecomp_residual_update(int kind, double ratio, const bc_tensor* t, int T,
  * version waits on another workgroup, so it stays clear. */
 int bytecomp_device_status(void* ws, size_t ws_bytes, void* stream, uint32_t* flags);
 
+/* Instrumentation, not part of the method: for callers that measure one
+ * kernel's own duration (benchmarks).  The next launch, by any call, of
+ * the kernel named `kernel` ("aggregate_sign", "aggregate_sparse",
+ * "randk_stream", "topk_compact", "sign_pass1") records `start_event`
+ * when it begins and `stop_event` when it ends (HIP events created by the
+ * caller, on the launch's stream); the request is then cleared.  Both
+ * events NULL clears a pending request.  BC_E_KIND for an unknown name.
+ * One request is held at a time, process-wide. */
+int bytecomp_time_next_launch(const char* kernel, void* start_event, void* stop_event);
+
 #ifdef __cplusplus
 }
 #endif

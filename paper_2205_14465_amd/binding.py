@@ -73,6 +73,8 @@ def lib():
         L.bytecomp_residual_update.argtypes = [i32, dbl, ctypes.POINTER(bc_tensor), i32, bc_payload, vp]
         L.bytecomp_device_status.restype = i32
         L.bytecomp_device_status.argtypes = [vp, sz, vp, ctypes.POINTER(ctypes.c_uint32)]
+        L.bytecomp_time_next_launch.restype = i32
+        L.bytecomp_time_next_launch.argtypes = [ctypes.c_char_p, vp, vp]
         _lib = L
     return _lib
 
@@ -188,6 +190,18 @@ def bytecomp_residual_update(kind, ratio, grads, resids, own, stream=None, tenso
     _check("bytecomp_residual_update",
            lib().bytecomp_residual_update(_kind(kind), float(ratio), arr, len(grads), _payload(own),
                                           _stream_handle(stream)))
+
+
+def bytecomp_time_next_launch(kernel, start_event, stop_event):
+    """Have the next launch of `kernel` bracketed by two torch.cuda.Event
+    objects (recorded once before, so that their HIP events exist); None
+    for both clears a pending request."""
+    if start_event is None and stop_event is None:
+        _check("bytecomp_time_next_launch", lib().bytecomp_time_next_launch(None, None, None))
+        return
+    _check("bytecomp_time_next_launch",
+           lib().bytecomp_time_next_launch(kernel.encode(), ctypes.c_void_p(start_event.cuda_event),
+                                           ctypes.c_void_p(stop_event.cuda_event)))
 
 
 def bytecomp_device_status(ws, stream=None):

@@ -5,6 +5,7 @@
 
 #include <cmath>
 #include <cstdlib>
+#include <atomic>
 #include <cstring>
 #include <mutex>
 #include <new>
@@ -163,6 +164,30 @@ hipError_t device_info(int dev, DevInfo* out) {
     }
     *out = g_dev[dev];
     return hipSuccess;
+}
+
+// ------------------------------------------------------- kernel timing
+namespace {
+std::mutex g_timer_mu;
+std::atomic<int> g_timer_kernel{kTimedNone};
+hipEvent_t g_timer_start = nullptr, g_timer_stop = nullptr;
+
+void set_kernel_timer(int k, hipEvent_t start, hipEvent_t stop) {
+    std::lock_guard<std::mutex> lk(g_timer_mu);
+    g_timer_start = start;
+    g_timer_stop = stop;
+    g_timer_kernel.store(k, std::memory_order_release);
+}
+}  // namespace
+
+bool take_kernel_timer(int k, hipEvent_t* start, hipEvent_t* stop) {
+    if (g_timer_kernel.load(std::memory_order_acquire) != k) return false;
+    std::lock_guard<std::mutex> lk(g_timer_mu);
+    if (g_timer_kernel.load(std::memory_order_relaxed) != k) return false;
+    *start = g_timer_start;
+    *stop = g_timer_stop;
+    g_timer_kernel.store(kTimedNone, std::memory_order_relaxed);
+    return true;
 }
 
 // -------------------------------------------------------------- workspace
@@ -556,6 +581,25 @@ int bytecomp_residual_update(int kind, double ratio, const bc_tensor* t, int T, 
                                own.bits, own.scale, s);
     cache_mark_used(en, s);
     return finish(hip_status(e), s, nullptr);
+}
+
+int bytecomp_time_next_launch(const char* kernel, void* start_event, void* stop_event) {
+    if (!start_event && !stop_event) {
+        set_kernel_timer(kTimedNone, nullptr, nullptr);
+        return BC_OK;
+    }
+    if (!kernel || !start_event || !stop_event) return BC_E_NULL;
+    static const struct { const char* name; int k; } names[] = {
+        {"aggregate_sign", kTimedAggSign},       {"aggregate_sparse", kTimedAggSparse},
+        {"randk_stream", kTimedRandkStream},     {"topk_compact", kTimedTopkCompact},
+        {"sign_pass1", kTimedSignPass1}};
+    for (const auto& x : names) {
+        if (std::strcmp(kernel, x.name) == 0) {
+            set_kernel_timer(x.k, (hipEvent_t)start_event, (hipEvent_t)stop_event);
+            return BC_OK;
+        }
+    }
+    return BC_E_KIND;
 }
 
 int bytecomp_device_status(void* ws, size_t ws_bytes, void* stream, uint32_t* flags) {

@@ -50,7 +50,7 @@ static_assert(sizeof(ADesc) == 32, "ADesc layout");
 // One worker's payload in an aggregate call.
 // Worker table of the aggregate descriptor (pointers stored as uint64):
 // a[Wp] (sparse: idx, sign: bits), then b[Wp] (sparse: val, sign: scale),
-// then the unit -> tensor map; Wp = padded_workers(W) (launch.hpp) and the
+// then the unit -> tensor map; Wp = padded_workers(W) (below) and the
 // slots past W repeat worker W-1.
 
 // Largest t with d[t].chunk0 <= c (tensors without chunks share chunk0 with
@@ -297,5 +297,32 @@ constexpr uint64_t kStreamSample = 1;
 
 // Workspace header: failure flags (bit 0 reserved for a bounded wait that
 // ran out; no current kernel waits on another workgroup).
+
+// ------------------------------------------------- aggregate worker table
+// Worker descriptors in the aggregate table are padded to a multiple of 16.
+__host__ __device__ constexpr int padded_workers(int W) { return (W + 15) & ~15; }
+
+// The aggregate table is [ADesc x T][a x Wp][b x Wp][unit -> tensor map]
+// with Wp = padded_workers(W); slots past W repeat worker W-1.
+__device__ __forceinline__ const uint32_t* w_a(const uint64_t* __restrict__ wp, int w) {
+    return (const uint32_t*)wp[w];
+}
+__device__ __forceinline__ const float* w_b(const uint64_t* __restrict__ wp, int W, int w) {
+    return (const float*)wp[padded_workers(W) + w];
+}
+__device__ __forceinline__ int unit_owner(const uint64_t* __restrict__ wp, int W, uint32_t u) {
+    return (int)reinterpret_cast<const uint32_t*>(wp + 2 * padded_workers(W))[u];
+}
+
+// First position p in [0, k) with idx[p] >= x (k if none).
+__device__ __forceinline__ uint32_t lower_bound_u32(const uint32_t* idx, uint32_t k, uint32_t x) {
+    uint32_t lo = 0, hi = k;
+    while (lo < hi) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (gp(idx)[mid] < x) lo = mid + 1; else hi = mid;
+    }
+    return lo;
+}
+
 
 }  // namespace bc

@@ -1,0 +1,276 @@
+// kernels_agg_sparse.hip -- sparse decompress-and-aggregate of W workers'
+// payloads on gfx950 (paper Sec. 3.1, Reason #2: after the gather each node
+// decompresses the N payloads and aggregates them; Sec. 4.2.1, Dimension 3:
+// the aggregation of compressed tensors is not associative, so it is not an
+// Allreduce).
+//
+// out_t[i] = alpha * (sum of the workers' values at i, added in ascending
+// worker order, one fp32 addition each, starting from +0.0).  No
+// floating-point atomics are used, so results are deterministic and match
+// that order bit for bit.
+//
+// Each wave owns a run of 2048- or 4096-element output tiles held in LDS.
+// For every tile it walks the workers in order; worker w's entries for the
+// tile are the next ones after its cursor (indices ascending), read 64 at a
+// time and added into the tile (indices are unique within a worker, so a
+// worker's adds never collide and need no atomics).  Cursors are found by a
+// binary search only where a wave's run starts inside a tensor.
+#include "launch.hpp"
+
+namespace bc {
+
+// Each wave owns a run of consecutive kTS-element tiles held in its own LDS
+// slice.  The next 64 entries of kS workers are kept in flight in registers
+// (slot w % kS holds worker w): as soon as a worker's entries for the tile
+// have been added, its slot is refilled with the worker that comes kS
+// later, or, when W is a multiple of kS and the next tile continues the
+// tensor, with the entries of the slot's first worker (w % kS) for the next
+// tile (its cursor is final by then).
+//
+// kLanes (W <= 64): lane w of a VGPR holds worker w's cursor and its two
+// payload pointers (already offset to the tensor), read with readlane, so
+// a step touches neither LDS nor the scalar cache for bookkeeping.
+// Otherwise the cursors live in LDS after the tiles and the pointers are
+// read from the worker table.
+template <uint32_t kTS, int kS, bool kLanes>
+__global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restrict__ a, int T,
+                                                           uint32_t U, const uint64_t* __restrict__ wp,
+                                                           int W, float alpha) {
+    extern __shared__ uint32_t lds[];
+    const int wave = wave_id();
+    const int lane = lane_id();
+    float* tile = reinterpret_cast<float*>(lds) + wave * (int)kTS;
+    uint32_t* cur = lds + 4 * kTS + wave * W;  // !kLanes only
+    const uint64_t nw = (uint64_t)gridDim.x * 4;
+    const uint64_t gw = (uint64_t)blockIdx.x * 4 + wave;
+    const uint32_t u_beg = (uint32_t)((gw * U) / nw);
+    const uint32_t u_end = (uint32_t)(((gw + 1) * U) / nw);
+    const bool cross = (W % kS) == 0;
+    // per-lane worker state (kLanes): cursor, payload pointers of the tensor
+    uint32_t curv = 0;
+    uint64_t pav = 0, pbv = 0;
+    auto get_cur = [&](int w) -> uint32_t {
+        if constexpr (kLanes) return (uint32_t)__builtin_amdgcn_readlane((int)curv, w);
+        else return cur[w];
+    };
+    auto set_cur = [&](int w, uint32_t c) {
+        if constexpr (kLanes) curv = lane == w ? c : curv;
+        else if (lane == 0) cur[w] = c;
+    };
+    // Every slot load is issued unconditionally (index clamped into the
+    // tensor's entries) so that the compiler can count the loads in flight
+    // exactly and wait only for the one it needs; a dead slot's entries are
+    // masked by setting every bit of its index (never below a tile end).
+    uint32_t x[kS];
+    float y[kS];
+    uint32_t inv[kS];
+    int t = -1;
+    ADesc ad{};
+    bool primed = false;  // slots already hold this tile's first entries
+    for (uint32_t u = u_beg; u < u_end; ++u) {
+        if (t < 0 || u >= ad.unit0 + ad.nunits) {
+            t = unit_owner(wp, W, u);
+            ad = a[t];
+            const uint32_t lo0 = (u - ad.unit0) * kTS;
+            if constexpr (kLanes) {
+                const int wl = lane < W ? lane : W - 1;
+                pav = wp[wl] + ad.off * 4u;
+                pbv = wp[padded_workers(W) + wl] + ad.off * 4u;
+                curv = lo0 == 0 ? 0u : lower_bound_u32((const uint32_t*)pav, ad.k, lo0);
+            } else {
+                for (int w = lane; w < W; w += 64)
+                    cur[w] = lo0 == 0 ? 0u : lower_bound_u32(w_a(wp, w) + ad.off, ad.k, lo0);
+                __builtin_amdgcn_wave_barrier();
+            }
+            primed = false;
+        }
+        const uint32_t klast = ad.k - 1;  // a tile exists, so k >= 1
+        auto load_slot = [&](int q, int w, uint32_t c, bool live) {
+            const uint32_t i = c + lane;
+            const uint32_t ic = i < ad.k ? i : klast;
+            const uint32_t* pa;
+            const float* pb;
+            if constexpr (kLanes) {
+                pa = (const uint32_t*)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(pav >> 32), w) << 32) |
+                                       (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)pav, w));
+                pb = (const float*)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(pbv >> 32), w) << 32) |
+                                    (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)pbv, w));
+            } else {
+                pa = w_a(wp, w) + ad.off;
+                pb = w_b(wp, W, w) + ad.off;
+            }
+            x[q] = gp(pa)[ic];
+            y[q] = gp(pb)[ic];
+            inv[q] = (live && i < ad.k) ? 0u : 0xFFFFFFFFu;
+            asm volatile("" : "+v"(inv[q]));  // computed here, not sunk to its use
+        };
+        if (!primed) {
+            // W through an opaque copy: keeps the sixteen per-slot worker
+            // numbers and flags from being hoisted into live SGPRs
+            int Wq = W;
+            asm volatile("" : "+s"(Wq));
+#pragma unroll
+            for (int q = 0; q < kS; ++q) {
+                const int w = q < Wq ? q : Wq - 1;
+                load_slot(q, w, get_cur(w), q < Wq);
+            }
+        }
+        const uint32_t lo = (u - ad.unit0) * kTS;
+        const uint32_t hi = (lo + kTS < ad.n) ? lo + kTS : ad.n;
+        const uint32_t len = hi - lo;
+        const bool next_same = cross && u + 1 < u_end && u + 1 < ad.unit0 + ad.nunits;
+#pragma unroll
+        for (uint32_t r = 0; r < kTS / 256u; ++r)
+            *reinterpret_cast<f32x4*>(tile + 256u * r + 4u * lane) = f32x4{0.f, 0.f, 0.f, 0.f};
+        __builtin_amdgcn_wave_barrier();
+        // a worker with 64 or more entries in the tile (dense payloads)
+        // ends the pipelined walk: the rest of the tile, from that worker
+        // on, is finished one 64-entry window at a time below.  Keeping that
+        // loop out of the pipelined steps keeps their load waits exact.
+        int dw = -1;
+        uint32_t dcc = 0;
+        for (int w0 = 0; w0 < W; w0 += kS) {
+            // all kS steps issue their two loads on every path (the ones
+            // past W or after a dense worker are dead), so that the compiler
+            // counts the loads in flight the same way on every path
+#pragma unroll
+            for (int q = 0; q < kS; ++q) {
+                const int w = w0 + q;
+                // W through an opaque copy per step, so that the per-step
+                // flags are computed here rather than hoisted into SGPRs
+                int Wq = W;
+                asm volatile("" : "+s"(Wq));
+                uint32_t cc = 0;
+                if (w < Wq && dw < 0) {  // no load in here
+                    cc = get_cur(w);
+                    const uint32_t xv = x[q] | inv[q];
+                    const uint64_t m = __ballot(xv < hi);
+                    // entries below the tile can only come from an unsorted
+                    // payload; they are skipped rather than written out of range
+                    const uint32_t dd = xv - lo;
+                    if (dd < len) tile[dd] += y[q];
+                    const uint32_t cnt = (uint32_t)__popcll(m);
+                    cc += cnt;
+                    __builtin_amdgcn_wave_barrier();
+                    if (cnt == 64) {
+                        dw = w;
+                        dcc = cc;
+                    } else {
+                        set_cur(w, cc);
+                    }
+                }
+                // refill the slot: the worker kS later in this tile, or else
+                // (W a multiple of kS) worker q's entries for the next tile,
+                // its cursor being final here
+                const int wn = w + kS;
+                const bool later = wn < Wq;
+                int wr = later ? wn : wn - Wq;
+                wr = wr < Wq ? wr : Wq - 1;
+                const bool live = w < Wq && dw < 0 && (later || next_same);
+                load_slot(q, wr, later ? get_cur(wn) : (wr == w ? cc : get_cur(wr)), live);
+            }
+            if (dw >= 0) break;
+        }
+        if (dw >= 0) {
+            for (int w = dw; w < W; ++w) {
+                uint32_t cc = w == dw ? dcc : get_cur(w);
+                const uint32_t* pa;
+                const float* pb;
+                if constexpr (kLanes) {
+                    pa = (const uint32_t*)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(pav >> 32), w) << 32) |
+                                           (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)pav, w));
+                    pb = (const float*)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(pbv >> 32), w) << 32) |
+                                        (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)pbv, w));
+                } else {
+                    pa = w_a(wp, w) + ad.off;
+                    pb = w_b(wp, W, w) + ad.off;
+                }
+                uint32_t cnt = 64;
+                while (cnt == 64) {
+                    const uint32_t i = cc + lane;
+                    const bool oki = i < ad.k;
+                    const uint32_t ic = oki ? i : klast;
+                    const uint32_t xi = oki ? gp(pa)[ic] : 0xFFFFFFFFu;
+                    const float yi = gp(pb)[ic];
+                    const uint64_t m = __ballot(xi < hi);
+                    const uint32_t dd = xi - lo;
+                    if (dd < len) tile[dd] += yi;
+                    cnt = (uint32_t)__popcll(m);
+                    cc += cnt;
+                    __builtin_amdgcn_wave_barrier();
+                }
+                set_cur(w, cc);
+            }
+            primed = false;
+        } else {
+            primed = next_same;
+        }
+        float* out = ad.out + lo;
+        if (len == kTS) {
+#pragma unroll
+            for (uint32_t r = 0; r < kTS / 256u; ++r) {
+                const uint32_t i = 256u * r + 4u * lane;
+                const f32x4 v = *reinterpret_cast<const f32x4*>(tile + i);
+                stg4f(out + i, f32x4{alpha * v[0], alpha * v[1], alpha * v[2], alpha * v[3]});
+            }
+        } else {
+            for (uint32_t i = 4u * lane; i < len; i += 256u) {
+                if (i + 3 < len) {
+                    stg4f(out + i, f32x4{alpha * tile[i], alpha * tile[i + 1], alpha * tile[i + 2],
+                                         alpha * tile[i + 3]});
+                } else {
+                    for (uint32_t q = i; q < len; ++q) gp(out)[q] = alpha * tile[q];
+                }
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+    }
+}
+
+
+// -------------------------------------------------------------- launchers
+uint32_t sparse_agg_tile(uint64_t n_total, uint64_t k_total) {
+    // 4096-element tiles while a worker holds about 48 entries per tile or
+    // fewer (one 64-entry window covers its entries), 2048 otherwise
+    return k_total * 4096u <= n_total * 48u ? 4096u : 2048u;
+}
+
+namespace {
+template <uint32_t kTS, int kS, bool kLanes>
+void launch_sparse_t(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W, float alpha, int cus,
+                     hipStream_t s) {
+    const size_t lds = (size_t)4 * (kTS * 4 + (kLanes ? 0 : (size_t)W * 4));
+    // one round of resident workgroups at this LDS size (more waves with
+    // shorter runs measured slower)
+    size_t per_cu = (160u * 1024u) / lds;
+    if (per_cu < 1) per_cu = 1;
+    if (per_cu > 8) per_cu = 8;
+    uint64_t blocks = (U + 3) / 4;
+    const uint64_t cap = per_cu * (uint64_t)(cus > 0 ? cus : 256);
+    if (blocks > cap) blocks = cap;
+    (void)launch_timed(kTimedAggSparse, aggregate_sparse<kTS, kS, kLanes>, dim3((uint32_t)blocks), dim3(kBlock), lds, s,
+                 a, T, U, w, W, alpha);
+}
+template <uint32_t kTS>
+void launch_sparse_ts(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W, float alpha, int cus,
+                      hipStream_t s) {
+    if (W > 64) {
+        launch_sparse_t<kTS, 16, false>(a, T, U, w, W, alpha, cus, s);
+    } else if (W % 16 == 0 || W % 8 != 0) {
+        launch_sparse_t<kTS, 16, true>(a, T, U, w, W, alpha, cus, s);
+    } else {
+        launch_sparse_t<kTS, 8, true>(a, T, U, w, W, alpha, cus, s);
+    }
+}
+}  // namespace
+
+hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t U, uint32_t tile, const uint64_t* w, int W,
+                                   float alpha, int cus, hipStream_t s) {
+    if (U == 0) return hipSuccess;
+    if (tile == 4096u) launch_sparse_ts<4096u>(a, T, U, w, W, alpha, cus, s);
+    else if (tile == 2048u) launch_sparse_ts<2048u>(a, T, U, w, W, alpha, cus, s);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+}  // namespace bc

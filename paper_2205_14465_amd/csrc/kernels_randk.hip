@@ -446,8 +446,7 @@ hipError_t launch_randk(uint64_t seed, const TDesc* d, int T, uint32_t C, uint64
     hipLaunchKernelGGL(randk_scan_apply, dim3(nscan), blk, 0, s, NB, ws, bsum);
     if (nblk)
         hipLaunchKernelGGL(randk_place, dim3(nblk), dim3(kGenBlock), lds_place, s, d, T, sum_k, S, NB, idx, ws);
-    hipLaunchKernelGGL(randk_stream, dim3(NB), blk, lds_stream, s, d, T, C, S, idx, val, ws);
-    return hipGetLastError();
+    return launch_timed(kTimedRandkStream, randk_stream, dim3(NB), blk, lds_stream, s, d, T, C, S, idx, val, ws);
 }
 
 }  // namespace bc

@@ -164,7 +164,7 @@ __global__ __launch_bounds__(kBlock) void sign_residual_update(const TDesc* __re
 hipError_t launch_sign_compress(const TDesc* d, int T, uint32_t C, uint32_t max_chunks, bool any_empty,
                                 uint32_t* bits, float* scale, const Ws& ws, hipStream_t s) {
     if (T <= 0) return hipSuccess;
-    if (C > 0) hipLaunchKernelGGL(sign_pass1, dim3(C), dim3(kBlock), 0, s, d, T, bits, ws);
+    if (C > 0) (void)launch_timed(kTimedSignPass1, sign_pass1, dim3(C), dim3(kBlock), 0, s, d, T, bits, ws);
     // tensors without elements, or with more chunks than pass 2 sums inline
     if (max_chunks > kInlineScaleChunks || C == 0 || any_empty)
         hipLaunchKernelGGL(sign_finalize, dim3(T), dim3(kBlock), 0, s, d, scale, ws);

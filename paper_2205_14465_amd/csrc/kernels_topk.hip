@@ -453,13 +453,13 @@ hipError_t launch_topk(int kind, double ratio, uint64_t seed, const TDesc* d, in
     if (kind == 0) {  // exact
         hipLaunchKernelGGL(topk_hist_pass, dim3(C), blk, 0, s, d, T, C, 1, 0, ws);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindThrExact, 0, ws);
-        hipLaunchKernelGGL(topk_compact, dim3(C), blk, 0, s, d, T, C, 0, 0, ws);
+        (void)launch_timed(kTimedTopkCompact, topk_compact, dim3(C), blk, 0, s, d, T, C, 0, 0, ws);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit0, 0, ws);
     } else {  // sampled threshold, exact fallback per tensor
         hipLaunchKernelGGL(topk_sample_hist, dim3((C + kSampleChunksPerBlock - 1) / kSampleChunksPerBlock), blk,
                            0, s, d, T, C, seed, ws);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindThrSample, 0, ws);
-        hipLaunchKernelGGL(topk_compact, dim3(C), blk, 0, s, d, T, C, 1, 0, ws);
+        (void)launch_timed(kTimedTopkCompact, topk_compact, dim3(C), blk, 0, s, d, T, C, 1, 0, ws);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit0, 0, ws);
         // fallback passes: small grids that walk the chunks, and return at
         // once when no tensor fell back (the usual case)

@@ -2,6 +2,7 @@
 // workspace carve-up they share.  Included by the C-ABI layer only.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -61,6 +62,26 @@ struct DevInfo {
 };
 hipError_t device_info(int dev, DevInfo* out);
 
+// ------------------------------------------------------- kernel timing
+// Kernels a caller may ask to have timed (bytecomp_time_next_launch).
+enum TimedKernel { kTimedNone = 0, kTimedAggSign, kTimedAggSparse, kTimedRandkStream, kTimedTopkCompact,
+                   kTimedSignPass1 };
+// If a request for kernel `k` is pending, hand over its events and clear it.
+bool take_kernel_timer(int k, hipEvent_t* start, hipEvent_t* stop);
+
+// Launch `kernel`, bracketed by the requested events when kernel `k` is to
+// be timed.
+template <typename F, typename... Args>
+inline hipError_t launch_timed(int k, F kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s,
+                               Args... args) {
+    hipEvent_t e0, e1;
+    if (take_kernel_timer(k, &e0, &e1))
+        hipExtLaunchKernelGGL(kernel, grid, block, (std::uint32_t)lds, s, e0, e1, 0u, args...);
+    else
+        hipLaunchKernelGGL(kernel, grid, block, lds, s, args...);
+    return hipGetLastError();
+}
+
 // ------------------------------------------------------------- launchers
 // d: device TDesc[T]; C: total chunks.  Return the first HIP error.
 hipError_t launch_sign_compress(const TDesc* d, int T, uint32_t C, uint32_t max_chunks, bool any_empty,
@@ -96,8 +117,6 @@ constexpr uint32_t kRandkMaxShift = 8;
 bool randk_buckets(uint32_t C, uint32_t* S, uint32_t* NB);
 
 // Work-unit sizes of the aggregate kernels (elements per unit).
-// Worker descriptors in the aggregate table are padded to a multiple of 16.
-__host__ __device__ constexpr int padded_workers(int W) { return (W + 15) & ~15; }
 
 constexpr uint32_t kSignAggUnit = 4096;  // one workgroup: 16 elements per lane
 

@@ -118,3 +118,14 @@ def test_workspace_size_grows_with_inputs():
     b = B.bytecomp_workspace_size("topk_sampled", 0.01, [1 << 21], 1)
     assert b > a >= 8 * (1 << 20)
     assert B.bytecomp_workspace_size("sign", 0.01, [], 64) == 256
+
+
+def test_time_next_launch_arguments():
+    """The timing request only stores its arguments: checked without a GPU."""
+    L = B.lib()
+    fake = ctypes.c_void_p(0x1000)
+    assert L.bytecomp_time_next_launch(b"no_such_kernel", fake, fake) == -2
+    assert L.bytecomp_time_next_launch(b"aggregate_sign", fake, None) == -1
+    assert L.bytecomp_time_next_launch(None, fake, fake) == -1
+    assert L.bytecomp_time_next_launch(b"aggregate_sign", fake, fake) == 0
+    assert L.bytecomp_time_next_launch(None, None, None) == 0  # clears the request

@@ -358,3 +358,42 @@ def test_residual_update_matches_fused(kind):
         else:
             want = O.residual_update_sparse(grads[t], resids[t], own["idx"][sl], own["val"][sl])
         assert np.array_equal(bits(split_e[t]), bits(want)), t
+
+
+@pytest.mark.parametrize("kind, kernel", [("sign", "aggregate_sign"), ("topk", "aggregate_sparse")])
+def test_time_next_launch_brackets_the_kernel(kind, kernel):
+    """The timed launch records both events once, inside the call's span;
+    the following call is not timed again."""
+    import torch
+    from paper_2205_14465_amd import binding as B
+    from tests.helpers import torch_dev
+    rng = np.random.default_rng(5)
+    ns = [70001, 4096, 300000]
+    grads, resids = make_set(ns, rng)
+    pay, _ = gpu_compress(kind, 0.01, SEED, grads, resids)
+    payloads = [pay] * 3
+    outs_dev = [torch.empty(n, dtype=torch.float32, device="cuda") for n in ns]
+    ws = B.alloc_workspace(kind, 0.01, ns, 3)
+    dev_pay = []
+    for p in payloads:
+        if kind == "sign":
+            dev_pay.append({"bits": torch_dev(p["bits"].view(np.int32)), "scale": torch_dev(p["scale"])})
+        else:
+            dev_pay.append({"idx": torch_dev(p["idx"].view(np.int32)), "val": torch_dev(p["val"])})
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    for e in ev:
+        e.record()
+    torch.cuda.synchronize()
+    B.bytecomp_time_next_launch(kernel, ev[1], ev[2])
+    ev[0].record()
+    B.bytecomp_decompress_aggregate(kind, 0.01, dev_pay, ns, outs_dev, 1.0, ws)
+    ev[3].record()
+    torch.cuda.synchronize()
+    k_ms = ev[1].elapsed_time(ev[2])
+    call_ms = ev[0].elapsed_time(ev[3])
+    assert 0.0 < k_ms <= call_ms
+    # the request was consumed: a second call leaves the events where they were
+    B.bytecomp_decompress_aggregate(kind, 0.01, dev_pay, ns, outs_dev, 1.0, ws)
+    torch.cuda.synchronize()
+    assert ev[1].elapsed_time(ev[2]) == k_ms
+    assert B.bytecomp_device_status(ws) == 0

@@ -332,3 +332,71 @@ def aggregate_set(kind, ns, payloads, alpha=1.0):
             vv = [p["val"][p["off"][t]:p["off"][t + 1]] for p in payloads]
             outs.append(aggregate_sparse(n, ii, vv, alpha))
     return outs
+
+
+# ------------------------------------------------------ divisible scheme
+# Paper Sec. 3.1, Reason #2 (and the alltoall figure): in a divisible
+# scheme a compressed tensor is partitioned into parts; node j receives
+# part j from every node, decompresses and aggregates those parts, and
+# compresses the aggregate again (the second compression) before it is
+# broadcast.  Parts are element ranges [lo, hi) of each tensor.
+
+def check_part_bounds(n, b):
+    """Part boundaries of one tensor: 0 = b[0] <= ... <= b[-1] = n, every
+    inner boundary a multiple of 32 (word aligned for sign payloads)."""
+    b = [int(x) for x in b]
+    assert b[0] == 0 and b[-1] == n, (b, n)
+    assert all(x <= y for x, y in zip(b, b[1:])), b
+    assert all(x % 32 == 0 for x in b[1:-1]), b
+    return b
+
+
+def pack_part_sparse(idx, val, lo, hi):
+    """Entries of one tensor's sparse payload whose index lies in [lo, hi),
+    in payload order, with indices rebased to the range (index - lo)."""
+    idx = np.asarray(idx, np.uint32)
+    val = np.asarray(val, np.float32)
+    keep = (idx >= lo) & (idx < hi)
+    return (idx[keep] - np.uint32(lo)).astype(np.uint32), val[keep].copy()
+
+
+def pack_part_sign(words, lo, hi):
+    """Words of one tensor's sign payload that cover [lo, hi), lo a multiple
+    of 32: words lo/32 .. ceil(hi/32) - 1 (the scale travels unchanged)."""
+    assert lo % 32 == 0
+    return np.asarray(words, np.uint32)[lo // 32:(hi + 31) // 32].copy()
+
+
+def pack_part_set(kind, ns, payload, bounds, j):
+    """Part j of every tensor of one payload dict (as compress_set returns),
+    laid out tensor by tensor: {'idx', 'val', 'off'} for sparse kinds (off
+    = prefix sums of the per-tensor counts), {'bits', 'scale', 'off'} for
+    sign (off = prefix sums of the range word counts)."""
+    out_a, out_b, off = [], [], [0]
+    for t, n in enumerate(ns):
+        b = check_part_bounds(n, bounds[t])
+        lo, hi = b[j], b[j + 1]
+        seg = slice(payload["off"][t], payload["off"][t + 1])
+        if kind == "sign":
+            w = pack_part_sign(payload["bits"][seg], lo, hi)
+            out_a.append(w)
+        else:
+            i, v = pack_part_sparse(payload["idx"][seg], payload["val"][seg], lo, hi)
+            out_a.append(i)
+            out_b.append(v)
+        off.append(off[-1] + out_a[-1].size)
+    res = {"off": np.array(off, dtype=np.int64)}
+    if kind == "sign":
+        res["bits"] = np.concatenate(out_a) if out_a else np.zeros(0, np.uint32)
+        res["scale"] = np.asarray(payload["scale"], np.float32).copy()
+    else:
+        res["idx"] = np.concatenate(out_a) if out_a else np.zeros(0, np.uint32)
+        res["val"] = np.concatenate(out_b) if out_b else np.zeros(0, np.float32)
+    return res
+
+
+def aggregate_part_set(kind, lens, parts, alpha=1.0):
+    """Node j's aggregate of the part-j payloads of W senders (each laid out
+    as pack_part_set returns): per tensor, the dense slice of length
+    lens[t] -- the same decompress-and-aggregate as the whole tensors."""
+    return aggregate_set(kind, lens, parts, alpha)

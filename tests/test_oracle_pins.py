@@ -546,3 +546,72 @@ def test_sign_aggregate_zero_bits_and_single_worker():
     w, s, _ = O.compress_sign(g, None)
     out = O.aggregate_sign(n, [w], [s], 1.0)
     assert np.array_equal(out, np.where(g < 0, -s, s).astype(f32))
+
+
+# ------------------------------------------------------ divisible scheme
+
+def _div_bounds(rng, ns, P):
+    out = []
+    for n in ns:
+        inner = sorted(int(x) * 32 for x in rng.integers(0, n // 32 + 1, size=P - 1))
+        out.append([0] + inner + [n])
+    return out
+
+
+@pytest.mark.parametrize("kind", ["topk", "randk", "sign"])
+def test_parts_reassemble_the_payload(kind):
+    """Packing every part and undoing the rebase gives back the payload
+    exactly: the parts are disjoint and cover every entry (word)."""
+    rng = np.random.default_rng(31)
+    ns = [1, 31, 32, 100, 4097, 70000]
+    grads = [rng.standard_normal(n).astype(np.float32) for n in ns]
+    pay, _ = O.compress_set(kind, 0.05, 3, grads, None)
+    P = 4
+    bounds = _div_bounds(rng, ns, P)
+    parts = [O.pack_part_set(kind, ns, pay, bounds, j) for j in range(P)]
+    for t, n in enumerate(ns):
+        seg = slice(pay["off"][t], pay["off"][t + 1])
+        if kind == "sign":
+            got = np.concatenate([p["bits"][p["off"][t]:p["off"][t + 1]] for p in parts])
+            assert np.array_equal(got, pay["bits"][seg])
+            for p in parts:
+                assert np.array_equal(p["scale"], pay["scale"])
+        else:
+            ii = np.concatenate([p["idx"][p["off"][t]:p["off"][t + 1]] + np.uint32(bounds[t][j])
+                                 for j, p in enumerate(parts)])
+            vv = np.concatenate([p["val"][p["off"][t]:p["off"][t + 1]] for p in parts])
+            assert np.array_equal(ii, pay["idx"][seg])
+            assert np.array_equal(vv.view(np.uint32), pay["val"][seg].view(np.uint32))
+
+
+@pytest.mark.parametrize("kind", ["topk", "sign"])
+def test_part_aggregates_assemble_the_whole_aggregate(kind):
+    """The node-j aggregates of all parts, placed at their ranges, equal the
+    indivisible aggregate bit for bit (each element's sum sees the same
+    workers in the same order)."""
+    rng = np.random.default_rng(32)
+    ns = [33, 4096, 20001]
+    W, P = 5, 3
+    pays = []
+    for w in range(W):
+        grads = [rng.standard_normal(n).astype(np.float32) for n in ns]
+        pays.append(O.compress_set(kind, 0.1, 7 + w, grads, None)[0])
+    bounds = _div_bounds(rng, ns, P)
+    whole = O.aggregate_set(kind, ns, pays, 0.5)
+    for j in range(P):
+        lens = [bounds[t][j + 1] - bounds[t][j] for t in range(len(ns))]
+        parts = [O.pack_part_set(kind, ns, p, bounds, j) for p in pays]
+        got = O.aggregate_part_set(kind, lens, parts, 0.5)
+        for t in range(len(ns)):
+            lo, hi = bounds[t][j], bounds[t][j + 1]
+            assert np.array_equal(got[t].view(np.uint32), whole[t][lo:hi].view(np.uint32)), (j, t)
+
+
+def test_part_bounds_rules():
+    with pytest.raises(AssertionError):
+        O.check_part_bounds(100, [0, 50, 100])   # inner bound not word aligned
+    with pytest.raises(AssertionError):
+        O.check_part_bounds(100, [0, 64, 32, 100])
+    with pytest.raises(AssertionError):
+        O.check_part_bounds(100, [0, 96])
+    assert O.check_part_bounds(100, [0, 0, 96, 100]) == [0, 0, 96, 100]

@@ -167,6 +167,46 @@ int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, 
                                   const uint64_t* n, int T, float* const* out, float alpha,
                                   void* ws, size_t ws_bytes, void* stream);
 
+/* Divisible scheme, packing (paper Sec. 3.1, Reason #2, with the alltoall
+ * figure: a compressed tensor is partitioned into parts, and node j receives
+ * part j from every node).  Parts are element ranges: part q of tensor t is
+ * [bounds[t*(parts+1)+q], bounds[t*(parts+1)+q+1]), where bounds (host) run
+ * from 0 to n_t, never decrease, and every inner bound is a multiple of 32.
+ * This packs part j of one payload `in` (laid out as bytecomp_layout
+ * describes) into `out`:
+ *   sparse kinds: tensor by tensor, the entries whose index lies in the
+ *     range, in payload order, with the index rebased to the range
+ *     (index - start); out.idx / out.val need room for every entry of `in`
+ *     in the worst case;
+ *   BC_SIGN1: tensor by tensor, the words that cover the range (the layout
+ *     bytecomp_layout gives for the range lengths) and every tensor's scale.
+ *   part_off  device, T + 1 uint64: the packed offset of each tensor's part
+ *             (entries, or words), then the total.
+ * BC_E_ALIGN if an inner bound is not a multiple of 32, BC_E_SIZE if bounds
+ * do not run from 0 to n_t in order.  Stream-ordered like the rest. */
+int bytecomp_pack_part(int kind, double ratio, const uint64_t* n, int T, bc_payload in, int parts,
+                       const uint64_t* bounds, int j, bc_payload out, uint64_t* part_off, void* stream);
+
+/* Divisible scheme, aggregation of one part (paper Sec. 3.1, Reason #2: the
+ * node that receives part j from every node decompresses and aggregates the
+ * parts; compressing the aggregate again is bytecomp_compress on the dense
+ * slices, and the final decompress is bytecomp_decompress_aggregate with
+ * W = 1 per part).
+ *   in        host, W payloads packed by bytecomp_pack_part for the same part
+ *   part_off  host array of W device pointers: each sender's part_off
+ *             (sparse kinds; ignored for BC_SIGN1)
+ *   len       host, T range lengths of the part
+ *   out       host, T device pointers to dense fp32 slices (16-byte aligned)
+ * out_t[i] = alpha * the worker-ordered fp32 sum (sparse) or the exact sum
+ * rounded once (sign) of the senders' values at i, exactly as
+ * bytecomp_decompress_aggregate defines them, so the parts of all nodes
+ * assemble the whole aggregate bit for bit.  Sparse kinds take at most 64
+ * senders (BC_E_COUNT otherwise).  ws: as bytecomp_decompress_aggregate for
+ * the range lengths. */
+int bytecomp_aggregate_part(int kind, double ratio, const bc_payload* in, const uint64_t* const* part_off,
+                            int W, const uint64_t* len, int T, float* const* out, float alpha, void* ws,
+                            size_t ws_bytes, void* stream);
+
 /* Error-feedback update from a payload computed elsewhere (e.g. by a CPU
  * compressor, the paper's CPU offloading, Sec. 4.4.3):
  * residual <- (g + residual) - decompress(own), elementwise in fp32.

@@ -73,6 +73,11 @@ def lib():
         L.bytecomp_residual_update.argtypes = [i32, dbl, ctypes.POINTER(bc_tensor), i32, bc_payload, vp]
         L.bytecomp_device_status.restype = i32
         L.bytecomp_device_status.argtypes = [vp, sz, vp, ctypes.POINTER(ctypes.c_uint32)]
+        L.bytecomp_pack_part.restype = i32
+        L.bytecomp_pack_part.argtypes = [i32, dbl, vp, i32, bc_payload, i32, vp, i32, bc_payload, vp, vp]
+        L.bytecomp_aggregate_part.restype = i32
+        L.bytecomp_aggregate_part.argtypes = [i32, dbl, ctypes.POINTER(bc_payload), vp, i32, vp, i32, vp,
+                                              ctypes.c_float, vp, sz, vp]
         L.bytecomp_time_next_launch.restype = i32
         L.bytecomp_time_next_launch.argtypes = [ctypes.c_char_p, vp, vp]
         _lib = L
@@ -190,6 +195,32 @@ def bytecomp_residual_update(kind, ratio, grads, resids, own, stream=None, tenso
     _check("bytecomp_residual_update",
            lib().bytecomp_residual_update(_kind(kind), float(ratio), arr, len(grads), _payload(own),
                                           _stream_handle(stream)))
+
+
+def bytecomp_pack_part(kind, ratio, ns, payload, bounds, j, out, part_off, stream=None):
+    """Pack part j of `payload` into `out` (a payload dict sized like the
+    input); bounds is a list of per-tensor boundary lists (parts + 1 each);
+    part_off a device uint64 (int64) tensor of T + 1 entries."""
+    T = len(ns)
+    parts = len(bounds[0]) - 1 if T else 1
+    flat = _u64_array([int(x) for b in bounds for x in b])
+    _check("bytecomp_pack_part",
+           lib().bytecomp_pack_part(_kind(kind), float(ratio), _u64_array(ns), T, _payload(payload), parts,
+                                    flat, int(j), _payload(out), _ptr(part_off), _stream_handle(stream)))
+
+
+def bytecomp_aggregate_part(kind, ratio, parts, part_offs, lens, outs, alpha, ws, stream=None):
+    """Aggregate W packed parts (payload dicts from bytecomp_pack_part, with
+    their part_off tensors) into dense slices `outs` of lengths `lens`."""
+    W = len(parts)
+    T = len(lens)
+    pa = (bc_payload * W)(*[_payload(p) for p in parts])
+    po = (ctypes.c_void_p * W)(*[_ptr(x) for x in part_offs]) if part_offs is not None else None
+    op = (ctypes.c_void_p * max(T, 1))(*[_ptr(o) for o in outs])
+    _check("bytecomp_aggregate_part",
+           lib().bytecomp_aggregate_part(_kind(kind), float(ratio), pa, po, W, _u64_array(lens), T, op,
+                                         float(alpha), _ptr(ws), ws.numel() * ws.element_size(),
+                                         _stream_handle(stream)))
 
 
 def bytecomp_time_next_launch(kernel, start_event, stop_event):

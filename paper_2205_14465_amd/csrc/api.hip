@@ -451,9 +451,17 @@ int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t,
     return finish(hip_status(e), s, ws);
 }
 
-int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, int W,
-                                  const uint64_t* n, int T, float* const* out, float alpha,
-                                  void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Decompress-and-aggregate.  part_off == nullptr: W whole payloads in the
+// bytecomp_layout layout.  Otherwise (sparse kinds, W <= 64): W packed
+// parts, worker w's entries of tensor t at part_off[w][t] ..
+// part_off[w][t+1] (device arrays), indices relative to the tensor.
+int aggregate_impl(int kind, double ratio, const bc_payload* in, const uint64_t* const* part_off, int W,
+                   const uint64_t* n, int T, float* const* out, float alpha, void* ws, size_t ws_bytes,
+                   void* stream) {
     uint64_t ppm;
     int rc = check_kind_ratio(kind, ratio, ppm);
     if (rc) return rc;
@@ -463,6 +471,15 @@ int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, 
     if (!ws) return BC_E_WORKSPACE;
     if (ws_bytes < 256) return BC_E_WORKSPACE;
     const bool sparse = is_sparse(kind);
+    const bool ragged = part_off != nullptr;
+    if (ragged) {
+        if (!sparse) return BC_E_KIND;
+        if (W > 64) return BC_E_COUNT;
+        for (int q = 0; q < W; ++q)
+            if (!part_off[q]) return BC_E_NULL;
+    }
+    // ragged parts: [dummy-padded part-offset pointers][ADesc...][workers...]
+    const size_t rp_bytes = ragged ? align256((size_t)(padded_workers(W) + 1) * sizeof(uint64_t)) : 0;
     uint32_t unit = kSignAggUnit;
     if (sparse) {
         uint64_t nt = 0, kt = 0;
@@ -475,12 +492,17 @@ int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, 
     }
     std::vector<unsigned char> table;
     try {
-        table.resize((size_t)T * sizeof(ADesc) + (size_t)2 * padded_workers(W) * sizeof(uint64_t));
+        table.resize(rp_bytes + (size_t)T * sizeof(ADesc) + (size_t)2 * padded_workers(W) * sizeof(uint64_t));
     } catch (const std::bad_alloc&) {
         return BC_E_SIZE;
     }
-    ADesc* a = (ADesc*)table.data();
-    uint64_t* wa = (uint64_t*)(table.data() + (size_t)T * sizeof(ADesc));
+    if (ragged) {
+        uint64_t* rp = (uint64_t*)table.data();
+        for (int q = 0; q < padded_workers(W); ++q) rp[q] = (uint64_t)(uintptr_t)part_off[q < W ? q : W - 1];
+        rp[padded_workers(W)] = (uint64_t)(uintptr_t)ws;  // a readable dummy location
+    }
+    ADesc* a = (ADesc*)(table.data() + rp_bytes);
+    uint64_t* wa = (uint64_t*)(table.data() + rp_bytes + (size_t)T * sizeof(ADesc));
     uint64_t* wb = wa + padded_workers(W);
     uint64_t units = 0, off = 0;
     for (int i = 0; i < T; ++i) {
@@ -499,6 +521,10 @@ int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, 
         units += nu;
     }
     if (units >= (1ull << 31)) return BC_E_SIZE;
+    if (ragged) {
+        for (int i = 0; i < T; ++i) a[i].k = 0;  // per-worker counts come from the parts
+        off = 1;                                 // payloads are not addressed by layout
+    }
     Ws w{};  // sign: per-tensor forms and lookup tables live in the workspace
     if (!sparse) {
         uint64_t C = 0;
@@ -541,15 +567,88 @@ int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, 
                              },
                              s, &en);
     if (e != hipSuccess) return BC_E_HIP;
-    const ADesc* ad = (const ADesc*)en->dev;
-    const uint64_t* wdd = (const uint64_t*)((const char*)en->dev + (size_t)T * sizeof(ADesc));
+    const uint64_t* rpd = ragged ? (const uint64_t*)en->dev : nullptr;
+    const ADesc* ad = (const ADesc*)((const char*)en->dev + rp_bytes);
+    const uint64_t* wdd = (const uint64_t*)((const char*)en->dev + rp_bytes + (size_t)T * sizeof(ADesc));
     if (sparse) {
-        e = launch_aggregate_sparse(ad, T, (uint32_t)units, unit, wdd, W, alpha, di.cus, s);
+        e = launch_aggregate_sparse(ad, T, (uint32_t)units, unit, wdd, W, alpha, di.cus, rpd, s);
     } else {
         e = launch_aggregate_sign(ad, T, (uint32_t)units, wdd, W, alpha, w.s_info, w.s_tab, s);
     }
     cache_mark_used(en, s);
     return finish(hip_status(e), s, ws);
+}
+
+}  // namespace
+
+extern "C" {
+
+int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, int W,
+                                  const uint64_t* n, int T, float* const* out, float alpha,
+                                  void* ws, size_t ws_bytes, void* stream) {
+    return aggregate_impl(kind, ratio, in, nullptr, W, n, T, out, alpha, ws, ws_bytes, stream);
+}
+
+int bytecomp_aggregate_part(int kind, double ratio, const bc_payload* in, const uint64_t* const* part_off,
+                            int W, const uint64_t* len, int T, float* const* out, float alpha, void* ws,
+                            size_t ws_bytes, void* stream) {
+    if (kind == BC_SIGN1)  // packed sign parts have the word layout of the range lengths
+        return aggregate_impl(kind, ratio, in, nullptr, W, len, T, out, alpha, ws, ws_bytes, stream);
+    if (!part_off) return BC_E_NULL;
+    return aggregate_impl(kind, ratio, in, part_off, W, len, T, out, alpha, ws, ws_bytes, stream);
+}
+
+int bytecomp_pack_part(int kind, double ratio, const uint64_t* n, int T, bc_payload in, int parts,
+                       const uint64_t* bounds, int j, bc_payload out, uint64_t* part_off, void* stream) {
+    uint64_t ppm;
+    int rc = check_kind_ratio(kind, ratio, ppm);
+    if (rc) return rc;
+    if (T < 0 || T > kMaxT || parts < 1 || j < 0 || j >= parts) return BC_E_COUNT;
+    if (T == 0) return BC_OK;
+    if (!n || !bounds || !part_off) return BC_E_NULL;
+    const bool sparse = is_sparse(kind);
+    if (sparse ? (!in.idx || !in.val || !out.idx || !out.val) : (!in.bits || !in.scale || !out.bits || !out.scale))
+        return BC_E_NULL;
+    std::vector<PDesc> p;
+    try {
+        p.resize((size_t)T);
+    } catch (const std::bad_alloc&) {
+        return BC_E_SIZE;
+    }
+    uint64_t in_off = 0, out_words = 0;
+    for (int t = 0; t < T; ++t) {
+        if (n[t] >= kMaxN) return BC_E_SIZE;
+        const uint64_t* b = bounds + (size_t)t * (parts + 1);
+        if (b[0] != 0 || b[parts] != n[t]) return BC_E_SIZE;
+        for (int q = 0; q < parts; ++q) {
+            if (b[q] > b[q + 1]) return BC_E_SIZE;
+            if (q > 0 && (b[q] & 31u)) return BC_E_ALIGN;
+        }
+        const uint64_t cnt = sparse ? k_of(n[t], ppm) : words_of(n[t]);
+        PDesc& d = p[(size_t)t];
+        d.in_off = in_off;
+        d.out_off = out_words;
+        d.k = (uint32_t)cnt;
+        d.lo = (uint32_t)b[j];
+        d.hi = (uint32_t)b[j + 1];
+        d.pad = 0;
+        in_off += cnt;
+        out_words += (b[j + 1] - b[j] + 31) / 32;
+    }
+    hipStream_t s = (hipStream_t)stream;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return BC_E_HIP;
+    DevInfo di;
+    if (device_info(dev, &di) != hipSuccess) return BC_E_HIP;
+    std::lock_guard<std::mutex> lk(g_mu);
+    Entry* en = nullptr;
+    hipError_t e = cache_get(p.data(), p.size() * sizeof(PDesc), 0, [](void*) {}, s, &en);
+    if (e != hipSuccess) return BC_E_HIP;
+    const bc_payload_dev din{in.idx, in.val, in.bits, in.scale};
+    const bc_payload_dev dout{out.idx, out.val, out.bits, out.scale};
+    e = launch_pack_part(sparse ? 0 : 3, (const PDesc*)en->dev, T, din, dout, part_off, out_words, di.cus, s);
+    cache_mark_used(en, s);
+    return hip_status(e);
 }
 
 int bytecomp_residual_update(int kind, double ratio, const bc_tensor* t, int T, bc_payload own,

@@ -36,6 +36,26 @@ struct TDesc {
 };
 static_assert(sizeof(TDesc) == 48, "TDesc layout");
 
+// One tensor of a pack-part call (32 bytes): its payload offset and count
+// (entries, or words for sign), the part's element range, and (sign) the
+// part's word offset in the packed layout.
+struct PDesc {
+    uint64_t in_off;
+    uint64_t out_off;
+    uint32_t k;
+    uint32_t lo, hi;
+    uint32_t pad;
+};
+static_assert(sizeof(PDesc) == 32, "PDesc layout");
+
+// Device pointers of one payload (the C-ABI bc_payload, without torch).
+struct bc_payload_dev {
+    uint32_t* idx;
+    float* val;
+    uint32_t* bits;
+    float* scale;
+};
+
 // One tensor of an aggregate call (32 bytes).
 struct ADesc {
     float* out;

@@ -32,10 +32,16 @@ namespace bc {
 // a step touches neither LDS nor the scalar cache for bookkeeping.
 // Otherwise the cursors live in LDS after the tiles and the pointers are
 // read from the worker table.
-template <uint32_t kTS, int kS, bool kLanes>
+//
+// kRagged (with kLanes): the payloads are parts packed by
+// bytecomp_pack_part, so worker w's entries of tensor t start at
+// rp_w[t] and number rp_w[t+1] - rp_w[t] (rp[w] is worker w's part-offset
+// array); a worker with no entries reads a dummy location rp[Wp] instead.
+template <uint32_t kTS, int kS, bool kLanes, bool kRagged>
 __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restrict__ a, int T,
                                                            uint32_t U, const uint64_t* __restrict__ wp,
-                                                           int W, float alpha) {
+                                                           int W, float alpha, const uint64_t* __restrict__ rp) {
+    static_assert(kLanes || !kRagged, "ragged payloads need the lane-held worker state");
     extern __shared__ uint32_t lds[];
     const int wave = wave_id();
     const int lane = lane_id();
@@ -46,9 +52,11 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
     const uint32_t u_beg = (uint32_t)((gw * U) / nw);
     const uint32_t u_end = (uint32_t)(((gw + 1) * U) / nw);
     const bool cross = (W % kS) == 0;
-    // per-lane worker state (kLanes): cursor, payload pointers of the tensor
+    // per-lane worker state (kLanes): cursor, payload pointers of the tensor,
+    // and (kRagged) the worker's entry count of the tensor
     uint32_t curv = 0;
     uint64_t pav = 0, pbv = 0;
+    uint32_t kv = 0;
     auto get_cur = [&](int w) -> uint32_t {
         if constexpr (kLanes) return (uint32_t)__builtin_amdgcn_readlane((int)curv, w);
         else return cur[w];
@@ -72,7 +80,15 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
             t = unit_owner(wp, W, u);
             ad = a[t];
             const uint32_t lo0 = (u - ad.unit0) * kTS;
-            if constexpr (kLanes) {
+            if constexpr (kRagged) {
+                const int wl = lane < W ? lane : W - 1;
+                const uint64_t* po = (const uint64_t*)rp[wl];
+                const uint64_t o0 = po[t], o1 = po[t + 1];
+                kv = (uint32_t)(o1 - o0);
+                pav = kv ? wp[wl] + o0 * 4u : rp[padded_workers(W)];
+                pbv = kv ? wp[padded_workers(W) + wl] + o0 * 4u : rp[padded_workers(W)];
+                curv = lo0 == 0 ? 0u : lower_bound_u32((const uint32_t*)pav, kv, lo0);
+            } else if constexpr (kLanes) {
                 const int wl = lane < W ? lane : W - 1;
                 pav = wp[wl] + ad.off * 4u;
                 pbv = wp[padded_workers(W) + wl] + ad.off * 4u;
@@ -84,10 +100,16 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
             }
             primed = false;
         }
-        const uint32_t klast = ad.k - 1;  // a tile exists, so k >= 1
+        // entries of worker w in this tensor (the same for every worker unless
+        // the payloads are ragged parts; a part may hold none)
+        auto k_of = [&](int w) -> uint32_t {
+            if constexpr (kRagged) return (uint32_t)__builtin_amdgcn_readlane((int)kv, w);
+            else return ad.k;
+        };
         auto load_slot = [&](int q, int w, uint32_t c, bool live) {
             const uint32_t i = c + lane;
-            const uint32_t ic = i < ad.k ? i : klast;
+            const uint32_t kw = k_of(w);
+            const uint32_t ic = i < kw ? i : (kw ? kw - 1u : 0u);
             const uint32_t* pa;
             const float* pb;
             if constexpr (kLanes) {
@@ -101,7 +123,7 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
             }
             x[q] = gp(pa)[ic];
             y[q] = gp(pb)[ic];
-            inv[q] = (live && i < ad.k) ? 0u : 0xFFFFFFFFu;
+            inv[q] = (live && i < kw) ? 0u : 0xFFFFFFFFu;
             asm volatile("" : "+v"(inv[q]));  // computed here, not sunk to its use
         };
         if (!primed) {
@@ -188,8 +210,9 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
                 uint32_t cnt = 64;
                 while (cnt == 64) {
                     const uint32_t i = cc + lane;
-                    const bool oki = i < ad.k;
-                    const uint32_t ic = oki ? i : klast;
+                    const uint32_t kw = k_of(w);
+                    const bool oki = i < kw;
+                    const uint32_t ic = oki ? i : (kw ? kw - 1u : 0u);
                     const uint32_t xi = oki ? gp(pa)[ic] : 0xFFFFFFFFu;
                     const float yi = gp(pb)[ic];
                     const uint64_t m = __ballot(xi < hi);
@@ -236,9 +259,9 @@ uint32_t sparse_agg_tile(uint64_t n_total, uint64_t k_total) {
 }
 
 namespace {
-template <uint32_t kTS, int kS, bool kLanes>
+template <uint32_t kTS, int kS, bool kLanes, bool kRagged>
 void launch_sparse_t(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W, float alpha, int cus,
-                     hipStream_t s) {
+                     const uint64_t* rp, hipStream_t s) {
     const size_t lds = (size_t)4 * (kTS * 4 + (kLanes ? 0 : (size_t)W * 4));
     // one round of resident workgroups at this LDS size (more waves with
     // shorter runs measured slower)
@@ -248,27 +271,38 @@ void launch_sparse_t(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W
     uint64_t blocks = (U + 3) / 4;
     const uint64_t cap = per_cu * (uint64_t)(cus > 0 ? cus : 256);
     if (blocks > cap) blocks = cap;
-    (void)launch_timed(kTimedAggSparse, aggregate_sparse<kTS, kS, kLanes>, dim3((uint32_t)blocks), dim3(kBlock), lds, s,
-                 a, T, U, w, W, alpha);
+    (void)launch_timed(kTimedAggSparse, aggregate_sparse<kTS, kS, kLanes, kRagged>, dim3((uint32_t)blocks),
+                       dim3(kBlock), lds, s, a, T, U, w, W, alpha, rp);
 }
-template <uint32_t kTS>
+template <uint32_t kTS, bool kRagged>
 void launch_sparse_ts(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W, float alpha, int cus,
-                      hipStream_t s) {
-    if (W > 64) {
-        launch_sparse_t<kTS, 16, false>(a, T, U, w, W, alpha, cus, s);
-    } else if (W % 16 == 0 || W % 8 != 0) {
-        launch_sparse_t<kTS, 16, true>(a, T, U, w, W, alpha, cus, s);
+                      const uint64_t* rp, hipStream_t s) {
+    if constexpr (!kRagged) {
+        if (W > 64) {
+            launch_sparse_t<kTS, 16, false, false>(a, T, U, w, W, alpha, cus, rp, s);
+            return;
+        }
+    }
+    if (W % 16 == 0 || W % 8 != 0) {
+        launch_sparse_t<kTS, 16, true, kRagged>(a, T, U, w, W, alpha, cus, rp, s);
     } else {
-        launch_sparse_t<kTS, 8, true>(a, T, U, w, W, alpha, cus, s);
+        launch_sparse_t<kTS, 8, true, kRagged>(a, T, U, w, W, alpha, cus, rp, s);
     }
 }
 }  // namespace
 
 hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t U, uint32_t tile, const uint64_t* w, int W,
-                                   float alpha, int cus, hipStream_t s) {
+                                   float alpha, int cus, const uint64_t* rp, hipStream_t s) {
     if (U == 0) return hipSuccess;
-    if (tile == 4096u) launch_sparse_ts<4096u>(a, T, U, w, W, alpha, cus, s);
-    else if (tile == 2048u) launch_sparse_ts<2048u>(a, T, U, w, W, alpha, cus, s);
+    if (rp) {
+        if (W > 64) return hipErrorInvalidValue;
+        if (tile == 4096u) launch_sparse_ts<4096u, true>(a, T, U, w, W, alpha, cus, rp, s);
+        else if (tile == 2048u) launch_sparse_ts<2048u, true>(a, T, U, w, W, alpha, cus, rp, s);
+        else return hipErrorInvalidValue;
+        return hipGetLastError();
+    }
+    if (tile == 4096u) launch_sparse_ts<4096u, false>(a, T, U, w, W, alpha, cus, nullptr, s);
+    else if (tile == 2048u) launch_sparse_ts<2048u, false>(a, T, U, w, W, alpha, cus, nullptr, s);
     else return hipErrorInvalidValue;
     return hipGetLastError();
 }

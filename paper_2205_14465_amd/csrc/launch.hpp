@@ -98,8 +98,10 @@ hipError_t launch_residual_update(int kind, const TDesc* d, int T, uint32_t C, b
 // Sparse aggregate tile (elements per work unit) for a call whose tensors
 // hold n_total elements and k_total entries per worker.
 uint32_t sparse_agg_tile(uint64_t n_total, uint64_t k_total);
+// rp: null, or (ragged parts) per-worker part-offset arrays, then a dummy
+// readable location, as device pointers [padded_workers(W) + 1].
 hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t units, uint32_t tile, const uint64_t* wp,
-                                   int W, float alpha, int cus, hipStream_t s);
+                                   int W, float alpha, int cus, const uint64_t* rp, hipStream_t s);
 hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t units, const uint64_t* wp, int W,
                                  float alpha, uint32_t* info, int32_t* tabs, hipStream_t s);
 
@@ -115,6 +117,10 @@ constexpr uint32_t kRandkBuckets = 8192;
 constexpr uint32_t kRandkMaxBuckets = 16384;
 constexpr uint32_t kRandkMaxShift = 8;
 bool randk_buckets(uint32_t C, uint32_t* S, uint32_t* NB);
+
+// Divisible scheme: pack part j of one payload (kind 3 = sign).
+hipError_t launch_pack_part(int kind, const PDesc* p, int T, bc_payload_dev in, bc_payload_dev out,
+                            uint64_t* part_off, uint64_t sign_words, int cus, hipStream_t s);
 
 // Work-unit sizes of the aggregate kernels (elements per unit).
 

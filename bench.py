@@ -151,6 +151,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--scheme", choices=["indivisible", "divisible"], default="indivisible",
+                    help="divisible: time node 0's step of the divisible scheme instead")
+    ap.add_argument("--parts", type=int, default=8)
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -176,6 +179,9 @@ def main():
     comp_b, agg_b, pay_b = algorithmic_bytes(wl, off, kind)
     alpha = 1.0 / wl.W
     stream = torch.cuda.current_stream()
+
+    if args.scheme == "divisible":
+        return divisible(args, wl, off, payloads, ws, dev, stream)
 
     # argument arrays are marshalled once; each call is one C-ABI call
     compress_call = B.CompressCall(kind, wl.ratio, grads, resids, own, ws, stream=stream)
@@ -294,6 +300,119 @@ def main():
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
         line["cpu_baseline"] = cpu_baseline(wl, off, args.cpu_budget)
+    print(json.dumps(line), flush=True)
+
+
+def divisible(args, wl, off, payloads, ws_unused, dev, stream):
+    """Node 0's step of the divisible scheme (paper Sec. 3.1, Reason #2):
+    the W senders each pack their part 0 (bytecomp_pack_part), node 0
+    aggregates the W parts (bytecomp_aggregate_part) and compresses the
+    aggregate again without error feedback (bytecomp_compress).  Parts are
+    P near-equal word-aligned element ranges of every tensor.
+
+    Algorithmic bytes: each pack reads and writes its part's entries (or
+    words); the aggregate reads the W parts and writes the dense fp32
+    slices; the second compression reads the slices and writes their
+    payload."""
+    import torch
+    from paper_2205_14465_amd import binding as B
+    from paper_2205_14465_amd import workloads as WL
+    kind, W, P = wl.kind, wl.W, args.parts
+    bounds = []
+    for n in wl.sizes:
+        b = [0] + [min(n, (q * n // P) // 32 * 32) for q in range(1, P)] + [n]
+        bounds.append(b)
+    lens = [b[1] - b[0] for b in bounds]
+    parts = [B.alloc_payload(kind, wl.ratio, wl.sizes, device=dev) for _ in range(W)]
+    offs = [torch.zeros(wl.T + 1, dtype=torch.int64, device=dev) for _ in range(W)]
+    slice_flat = torch.empty(sum((n + 63) // 64 * 64 for n in lens) + 64, dtype=torch.float32, device=dev)
+    slices, pos = [], 0
+    for n in lens:
+        slices.append(slice_flat[pos:pos + n])
+        pos += (n + 63) // 64 * 64
+    sec = B.alloc_payload(kind, wl.ratio, lens, device=dev)
+    ws_agg = B.alloc_workspace(kind, wl.ratio, lens, W, device=dev)
+    ws_cmp = B.alloc_workspace(kind, wl.ratio, lens, 1, device=dev)
+    alpha = 1.0 / W
+
+    packs = [B.PackPartCall(kind, wl.ratio, wl.sizes, payloads[w], bounds, 0, parts[w], offs[w], stream=stream)
+             for w in range(W)]
+    agg_call = B.AggregatePartCall(kind, wl.ratio, parts, None if kind == "sign" else offs, lens, slices, alpha,
+                                   ws_agg, stream=stream)
+    cmp_call = B.CompressCall(kind, wl.ratio, slices, None, sec, ws_cmp, stream=stream)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        for pk in packs:
+            pk()
+        if ev is not None:
+            ev[1].record(stream)
+        agg_call()
+        if ev is not None:
+            ev[2].record(stream)
+        cmp_call(WL.SEED)
+        if ev is not None:
+            ev[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    # bytes actually present in each part
+    if kind == "sign":
+        part_units = [int(o[-1].item()) for o in offs]
+        part_bytes = [4 * u + 4 * wl.T for u in part_units]
+        sec_off = B.bytecomp_layout(kind, wl.ratio, lens)
+        sec_bytes = 4 * int(sec_off[-1]) + 4 * wl.T
+    else:
+        part_units = [int(o[-1].item()) for o in offs]
+        part_bytes = [8 * u for u in part_units]
+        sec_off = B.bytecomp_layout(kind, wl.ratio, lens)
+        sec_bytes = 8 * int(sec_off[-1])
+    n_slice = sum(lens)
+    pack_b = 2 * sum(part_bytes)
+    agg_b = sum(part_bytes) + 4 * n_slice
+    cmp_b = 4 * n_slice + sec_bytes
+    reps = args.steps
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        step()
+    torch.cuda.synchronize()
+    step_s = (time.perf_counter() - t0) / reps
+    dom_kernel = "aggregate_sign" if kind == "sign" else "aggregate_sparse"
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(reps)]
+    for r in range(reps):
+        for e in ev[r][4:]:
+            e.record(stream)
+    torch.cuda.synchronize()
+    for r in range(reps):
+        B.bytecomp_time_next_launch(dom_kernel, ev[r][4], ev[r][5])
+        step(ev[r])
+    torch.cuda.synchronize()
+    B.bytecomp_time_next_launch(None, None, None)
+    pack_ms = sum(ev[r][0].elapsed_time(ev[r][1]) for r in range(reps)) / reps
+    agg_ms = sum(ev[r][1].elapsed_time(ev[r][2]) for r in range(reps)) / reps
+    cmp_ms = sum(ev[r][2].elapsed_time(ev[r][3]) for r in range(reps)) / reps
+    dom_ms = sum(ev[r][4].elapsed_time(ev[r][5]) for r in range(reps)) / reps
+    assert B.bytecomp_device_status(ws_agg) == 0
+    value = (pack_b + agg_b + cmp_b) / step_s / 1e9
+    achieved = agg_b / (dom_ms * 1e-3) / 1e9
+    line = {
+        "metric": METRIC + " (divisible scheme, node 0's step)",
+        "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": reps, "warmup": args.warmup,
+        "ms_per_step": round(step_s * 1e3, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic", "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
+        "config": {"workload": wl.name, "kind": kind, "tensors": wl.T, "elements": wl.n_total, "W": W,
+                   "parts": P, "part_elements": n_slice},
+        "ops": {"pack_ms": round(pack_ms, 4), "pack_calls": W, "pack_gbs": round(pack_b / (pack_ms * 1e-3) / 1e9, 1),
+                "aggregate_part_ms": round(agg_ms, 4),
+                "aggregate_part_gbs": round(agg_b / (agg_ms * 1e-3) / 1e9, 1),
+                "recompress_ms": round(cmp_ms, 4), "recompress_gbs": round(cmp_b / (cmp_ms * 1e-3) / 1e9, 1)},
+        "roofline": {"bound": "hbm", "kernel": dom_kernel, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel_ms": round(dom_ms, 4)},
+    }
     print(json.dumps(line), flush=True)
 
 

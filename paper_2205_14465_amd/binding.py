@@ -287,6 +287,53 @@ class AggregateCall:
                                                    self.op, self.alpha, self.ws, self.ws_bytes, self.stream))
 
 
+class PackPartCall:
+    """bytecomp_pack_part with its argument arrays marshalled once."""
+
+    def __init__(self, kind, ratio, ns, payload, bounds, j, out, part_off, stream=None):
+        self.kind = _kind(kind)
+        self.ratio = float(ratio)
+        self.T = len(ns)
+        self.ns = _u64_array(ns)
+        self.parts = len(bounds[0]) - 1 if self.T else 1
+        self.flat = _u64_array([int(x) for b in bounds for x in b])
+        self.j = int(j)
+        self.inp = _payload(payload)
+        self.out = _payload(out)
+        self.po = _ptr(part_off)
+        self.stream = _stream_handle(stream)
+        self._keep = (payload, out, part_off)
+
+    def __call__(self):
+        _check("bytecomp_pack_part",
+               lib().bytecomp_pack_part(self.kind, self.ratio, self.ns, self.T, self.inp, self.parts, self.flat,
+                                        self.j, self.out, self.po, self.stream))
+
+
+class AggregatePartCall:
+    """bytecomp_aggregate_part with its argument arrays marshalled once."""
+
+    def __init__(self, kind, ratio, parts, part_offs, lens, outs, alpha, ws, stream=None):
+        self.kind = _kind(kind)
+        self.ratio = float(ratio)
+        self.W = len(parts)
+        self.pa = (bc_payload * max(self.W, 1))(*[_payload(p) for p in parts])
+        self.po = (ctypes.c_void_p * self.W)(*[x.data_ptr() for x in part_offs]) if part_offs is not None else None
+        self.T = len(lens)
+        self.lens = _u64_array(lens)
+        self.op = (ctypes.c_void_p * max(self.T, 1))(*[o.data_ptr() if o.numel() else None for o in outs])
+        self.alpha = float(alpha)
+        self.ws = _ptr(ws)
+        self.ws_bytes = ws.numel() * ws.element_size()
+        self.stream = _stream_handle(stream)
+        self._keep = (parts, part_offs, outs, ws)
+
+    def __call__(self):
+        _check("bytecomp_aggregate_part",
+               lib().bytecomp_aggregate_part(self.kind, self.ratio, self.pa, self.po, self.W, self.lens, self.T,
+                                             self.op, self.alpha, self.ws, self.ws_bytes, self.stream))
+
+
 # ------------------------------------------------------------ allocation
 
 def alloc_payload(kind, ratio, ns, device="cuda"):

@@ -615,7 +615,7 @@ int bytecomp_pack_part(int kind, double ratio, const uint64_t* n, int T, bc_payl
     } catch (const std::bad_alloc&) {
         return BC_E_SIZE;
     }
-    uint64_t in_off = 0, out_words = 0;
+    uint64_t in_off = 0, out_words = 0, max_entries = 0;
     for (int t = 0; t < T; ++t) {
         if (n[t] >= kMaxN) return BC_E_SIZE;
         const uint64_t* b = bounds + (size_t)t * (parts + 1);
@@ -634,6 +634,7 @@ int bytecomp_pack_part(int kind, double ratio, const uint64_t* n, int T, bc_payl
         d.pad = 0;
         in_off += cnt;
         out_words += (b[j + 1] - b[j] + 31) / 32;
+        max_entries += cnt < b[j + 1] - b[j] ? cnt : b[j + 1] - b[j];
     }
     hipStream_t s = (hipStream_t)stream;
     int dev = 0;
@@ -646,7 +647,8 @@ int bytecomp_pack_part(int kind, double ratio, const uint64_t* n, int T, bc_payl
     if (e != hipSuccess) return BC_E_HIP;
     const bc_payload_dev din{in.idx, in.val, in.bits, in.scale};
     const bc_payload_dev dout{out.idx, out.val, out.bits, out.scale};
-    e = launch_pack_part(sparse ? 0 : 3, (const PDesc*)en->dev, T, din, dout, part_off, out_words, di.cus, s);
+    e = launch_pack_part(sparse ? 0 : 3, (const PDesc*)en->dev, T, din, dout, part_off, out_words, max_entries,
+                         di.cus, s);
     cache_mark_used(en, s);
     return hip_status(e);
 }

@@ -119,8 +119,11 @@ constexpr uint32_t kRandkMaxShift = 8;
 bool randk_buckets(uint32_t C, uint32_t* S, uint32_t* NB);
 
 // Divisible scheme: pack part j of one payload (kind 3 = sign).
+// max_entries: an upper bound on the part's entries (sparse), which sizes
+// the copy grid.
 hipError_t launch_pack_part(int kind, const PDesc* p, int T, bc_payload_dev in, bc_payload_dev out,
-                            uint64_t* part_off, uint64_t sign_words, int cus, hipStream_t s);
+                            uint64_t* part_off, uint64_t sign_words, uint64_t max_entries, int cus,
+                            hipStream_t s);
 
 // Work-unit sizes of the aggregate kernels (elements per unit).
 

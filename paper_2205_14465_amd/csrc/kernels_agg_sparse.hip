@@ -33,11 +33,14 @@ namespace bc {
 // Otherwise the cursors live in LDS after the tiles and the pointers are
 // read from the worker table.
 //
+// kNT: the output tiles are written with the non-temporal hint (outputs
+// larger than the last-level cache).
+//
 // kRagged (with kLanes): the payloads are parts packed by
 // bytecomp_pack_part, so worker w's entries of tensor t start at
 // rp_w[t] and number rp_w[t+1] - rp_w[t] (rp[w] is worker w's part-offset
 // array); a worker with no entries reads a dummy location rp[Wp] instead.
-template <uint32_t kTS, int kS, bool kLanes, bool kRagged>
+template <uint32_t kTS, int kS, bool kLanes, bool kRagged, bool kNT>
 __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restrict__ a, int T,
                                                            uint32_t U, const uint64_t* __restrict__ wp,
                                                            int W, float alpha, const uint64_t* __restrict__ rp) {
@@ -234,12 +237,12 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
             for (uint32_t r = 0; r < kTS / 256u; ++r) {
                 const uint32_t i = 256u * r + 4u * lane;
                 const f32x4 v = *reinterpret_cast<const f32x4*>(tile + i);
-                stg4f(out + i, f32x4{alpha * v[0], alpha * v[1], alpha * v[2], alpha * v[3]});
+                stg4f_s<kNT>(out + i, f32x4{alpha * v[0], alpha * v[1], alpha * v[2], alpha * v[3]});
             }
         } else {
             for (uint32_t i = 4u * lane; i < len; i += 256u) {
                 if (i + 3 < len) {
-                    stg4f(out + i, f32x4{alpha * tile[i], alpha * tile[i + 1], alpha * tile[i + 2],
+                    stg4f_s<kNT>(out + i, f32x4{alpha * tile[i], alpha * tile[i + 1], alpha * tile[i + 2],
                                          alpha * tile[i + 3]});
                 } else {
                     for (uint32_t q = i; q < len; ++q) gp(out)[q] = alpha * tile[q];
@@ -259,7 +262,7 @@ uint32_t sparse_agg_tile(uint64_t n_total, uint64_t k_total) {
 }
 
 namespace {
-template <uint32_t kTS, int kS, bool kLanes, bool kRagged>
+template <uint32_t kTS, int kS, bool kLanes, bool kRagged, bool kNT>
 void launch_sparse_t(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W, float alpha, int cus,
                      const uint64_t* rp, hipStream_t s) {
     const size_t lds = (size_t)4 * (kTS * 4 + (kLanes ? 0 : (size_t)W * 4));
@@ -271,23 +274,34 @@ void launch_sparse_t(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W
     uint64_t blocks = (U + 3) / 4;
     const uint64_t cap = per_cu * (uint64_t)(cus > 0 ? cus : 256);
     if (blocks > cap) blocks = cap;
-    (void)launch_timed(kTimedAggSparse, aggregate_sparse<kTS, kS, kLanes, kRagged>, dim3((uint32_t)blocks),
+    (void)launch_timed(kTimedAggSparse, aggregate_sparse<kTS, kS, kLanes, kRagged, kNT>, dim3((uint32_t)blocks),
                        dim3(kBlock), lds, s, a, T, U, w, W, alpha, rp);
 }
-template <uint32_t kTS, bool kRagged>
-void launch_sparse_ts(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W, float alpha, int cus,
+template <uint32_t kTS, bool kRagged, bool kNT>
+void launch_sparse_nt(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W, float alpha, int cus,
                       const uint64_t* rp, hipStream_t s) {
     if constexpr (!kRagged) {
         if (W > 64) {
-            launch_sparse_t<kTS, 16, false, false>(a, T, U, w, W, alpha, cus, rp, s);
+            launch_sparse_t<kTS, 16, false, false, kNT>(a, T, U, w, W, alpha, cus, rp, s);
             return;
         }
     }
     if (W % 16 == 0 || W % 8 != 0) {
-        launch_sparse_t<kTS, 16, true, kRagged>(a, T, U, w, W, alpha, cus, rp, s);
+        launch_sparse_t<kTS, 16, true, kRagged, kNT>(a, T, U, w, W, alpha, cus, rp, s);
     } else {
-        launch_sparse_t<kTS, 8, true, kRagged>(a, T, U, w, W, alpha, cus, rp, s);
+        launch_sparse_t<kTS, 8, true, kRagged, kNT>(a, T, U, w, W, alpha, cus, rp, s);
     }
+}
+// Outputs past this many tiles (256 MB at 4096 elements) are written with
+// the non-temporal hint.
+constexpr uint32_t kNtTiles = 16384;
+template <uint32_t kTS, bool kRagged>
+void launch_sparse_ts(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W, float alpha, int cus,
+                      const uint64_t* rp, hipStream_t s) {
+    if ((uint64_t)U * kTS > (uint64_t)kNtTiles * 4096u)
+        launch_sparse_nt<kTS, kRagged, true>(a, T, U, w, W, alpha, cus, rp, s);
+    else
+        launch_sparse_nt<kTS, kRagged, false>(a, T, U, w, W, alpha, cus, rp, s);
 }
 }  // namespace
 

@@ -246,6 +246,7 @@ __global__ __launch_bounds__(kGenBlock) void randk_place(const TDesc* __restrict
 // of the chunk, writes e_new (selected entries zeroed) and emits its
 // selected (index, v) pairs at positions from a wave prefix over the
 // rounds, which is ascending index order.
+template <bool kNT>
 __global__ __launch_bounds__(kBlock) void randk_stream(const TDesc* __restrict__ d, int T, uint32_t C,
                                                        uint32_t S, uint32_t* __restrict__ idx,
                                                        float* __restrict__ val, Ws ws) {
@@ -313,17 +314,17 @@ __global__ __launch_bounds__(kBlock) void randk_stream(const TDesc* __restrict__
                 float g4[4] = {0.f, 0.f, 0.f, 0.f}, e4[4] = {0.f, 0.f, 0.f, 0.f};
                 if (e0 + 3 < td.n) {
                     if (td.dtype == 0) {
-                        const f32x4 x = ldg4f((const float*)td.grad + e0);
+                        const f32x4 x = ldg4f_s<kNT>((const float*)td.grad + e0);
                         g4[0] = x.x; g4[1] = x.y; g4[2] = x.z; g4[3] = x.w;
                     } else {
-                        const u32x2 h = ldg2u((const uint16_t*)td.grad + e0);
+                        const u32x2 h = ldg2u_s<kNT>((const uint16_t*)td.grad + e0);
                         g4[0] = h2f(h.x & 0xFFFFu);
                         g4[1] = h2f(h.x >> 16);
                         g4[2] = h2f(h.y & 0xFFFFu);
                         g4[3] = h2f(h.y >> 16);
                     }
                     if (use_e) {
-                        const f32x4 y = ldg4f(td.resid + e0);
+                        const f32x4 y = ldg4f_s<kNT>(td.resid + e0);
                         e4[0] = y.x; e4[1] = y.y; e4[2] = y.z; e4[3] = y.w;
                     }
                     valid |= 0xFu << (4 * r);
@@ -356,7 +357,7 @@ __global__ __launch_bounds__(kBlock) void randk_stream(const TDesc* __restrict__
 #pragma unroll
                     for (int i = 0; i < 4; ++i) o[i] = ((pm >> (4 * r + i)) & 1u) ? 0.f : v[4 * r + i];
                     if (e0 + 3 < td.n) {
-                        stg4f(td.resid + e0, f32x4{o[0], o[1], o[2], o[3]});
+                        stg4f_s<kNT>(td.resid + e0, f32x4{o[0], o[1], o[2], o[3]});
                     } else {
 #pragma unroll
                         for (int i = 0; i < 4; ++i)
@@ -418,7 +419,7 @@ hipError_t need_lds(const void* f, size_t bytes, size_t& allowed) {
     return e;
 }
 std::mutex g_lds_mu;
-size_t g_lds_place = 0, g_lds_stream = 0;
+size_t g_lds_place = 0, g_lds_stream = 0, g_lds_stream_nt = 0;
 }  // namespace
 
 hipError_t launch_randk(uint64_t seed, const TDesc* d, int T, uint32_t C, uint64_t sum_k, bool,
@@ -430,7 +431,8 @@ hipError_t launch_randk(uint64_t seed, const TDesc* d, int T, uint32_t C, uint64
     {
         std::lock_guard<std::mutex> lk(g_lds_mu);
         hipError_t e = need_lds((const void*)randk_place, lds_place, g_lds_place);
-        if (e == hipSuccess) e = need_lds((const void*)randk_stream, lds_stream, g_lds_stream);
+        if (e == hipSuccess) e = need_lds((const void*)randk_stream<false>, lds_stream, g_lds_stream);
+        if (e == hipSuccess) e = need_lds((const void*)randk_stream<true>, lds_stream, g_lds_stream_nt);
         if (e != hipSuccess) return e;
     }
     const dim3 blk(kBlock);
@@ -446,7 +448,11 @@ hipError_t launch_randk(uint64_t seed, const TDesc* d, int T, uint32_t C, uint64
     hipLaunchKernelGGL(randk_scan_apply, dim3(nscan), blk, 0, s, NB, ws, bsum);
     if (nblk)
         hipLaunchKernelGGL(randk_place, dim3(nblk), dim3(kGenBlock), lds_place, s, d, T, sum_k, S, NB, idx, ws);
-    return launch_timed(kTimedRandkStream, randk_stream, dim3(NB), blk, lds_stream, s, d, T, C, S, idx, val, ws);
+    if (C > kNtChunks)
+        return launch_timed(kTimedRandkStream, randk_stream<true>, dim3(NB), blk, lds_stream, s, d, T, C, S, idx,
+                            val, ws);
+    return launch_timed(kTimedRandkStream, randk_stream<false>, dim3(NB), blk, lds_stream, s, d, T, C, S, idx, val,
+                        ws);
 }
 
 }  // namespace bc

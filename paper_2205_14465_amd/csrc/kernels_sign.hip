@@ -54,11 +54,12 @@ __device__ __forceinline__ double reduce_partials(const double* p, uint32_t m, d
     return block_sum_f64(acc, sh);
 }
 
+template <bool kNT>
 __device__ __forceinline__ void store_sign_residual(const TDesc& td, uint32_t j, float s,
                                                     float v[kEpt]) {
 #pragma unroll
     for (int i = 0; i < kEpt; ++i) v[i] = v[i] - copysignf(s, v[i]);
-    store_chunk(td.resid, td.n, j, v);
+    store_chunk<kNT>(td.resid, td.n, j, v);
 }
 
 __device__ __forceinline__ uint32_t chunk_words(const TDesc& td, uint32_t j) {
@@ -72,6 +73,7 @@ __device__ __forceinline__ uint32_t chunk_words(const TDesc& td, uint32_t j) {
 // --------------------------------------------------------------- two pass
 constexpr uint32_t kInlineScaleChunks = 1024;
 
+template <bool kNT>
 __global__ __launch_bounds__(kBlock) void sign_pass1(const TDesc* __restrict__ d, int T,
                                                      uint32_t* __restrict__ bits, Ws ws) {
     __shared__ double sh[4];
@@ -81,7 +83,7 @@ __global__ __launch_bounds__(kBlock) void sign_pass1(const TDesc* __restrict__ d
     const uint32_t j = c - td.chunk0;
     float v[kEpt];
     uint32_t valid;
-    load_v(td, j, td.resid != nullptr, v, valid);
+    load_v<kNT>(td, j, td.resid != nullptr, v, valid);
     store_sign_words(v, bits + td.off + (uint64_t)j * kChunkWords, chunk_words(td, j));
     if (td.resid) store_chunk(td.resid, td.n, j, v);  // v parked in e for the second pass
     const double p = block_sum_f64(thread_abs_sum(v), sh);
@@ -110,6 +112,7 @@ __global__ __launch_bounds__(kBlock) void sign_finalize(const TDesc* __restrict_
 // fixed-order sum as sign_finalize; the first workgroup also stores it);
 // larger tensors read the scale sign_finalize stored.
 
+template <bool kNT>
 __global__ __launch_bounds__(kBlock) void sign_pass2(const TDesc* __restrict__ d, int T,
                                                      float* __restrict__ scale_out, Ws ws) {
     __shared__ double sh[4];
@@ -129,7 +132,7 @@ __global__ __launch_bounds__(kBlock) void sign_pass2(const TDesc* __restrict__ d
     float v[kEpt];
     uint32_t valid;
     load_stored_v(td, j, v, valid);  // e holds v after the first pass
-    store_sign_residual(td, j, s, v);
+    store_sign_residual<kNT>(td, j, s, v);
 }
 
 // -------------------------------------------------- residual update (sign)
@@ -164,11 +167,20 @@ __global__ __launch_bounds__(kBlock) void sign_residual_update(const TDesc* __re
 hipError_t launch_sign_compress(const TDesc* d, int T, uint32_t C, uint32_t max_chunks, bool any_empty,
                                 uint32_t* bits, float* scale, const Ws& ws, hipStream_t s) {
     if (T <= 0) return hipSuccess;
-    if (C > 0) (void)launch_timed(kTimedSignPass1, sign_pass1, dim3(C), dim3(kBlock), 0, s, d, T, bits, ws);
+    // past the cache size: stream g and e_old past the cache, keep v (re-read
+    // by pass 2) in it, and stream e_new out
+    const bool nt = C > kNtChunks;
+    if (C > 0) {
+        if (nt) (void)launch_timed(kTimedSignPass1, sign_pass1<true>, dim3(C), dim3(kBlock), 0, s, d, T, bits, ws);
+        else (void)launch_timed(kTimedSignPass1, sign_pass1<false>, dim3(C), dim3(kBlock), 0, s, d, T, bits, ws);
+    }
     // tensors without elements, or with more chunks than pass 2 sums inline
     if (max_chunks > kInlineScaleChunks || C == 0 || any_empty)
         hipLaunchKernelGGL(sign_finalize, dim3(T), dim3(kBlock), 0, s, d, scale, ws);
-    if (C > 0) hipLaunchKernelGGL(sign_pass2, dim3(C), dim3(kBlock), 0, s, d, T, scale, ws);
+    if (C > 0) {
+        if (nt) hipLaunchKernelGGL(sign_pass2<true>, dim3(C), dim3(kBlock), 0, s, d, T, scale, ws);
+        else hipLaunchKernelGGL(sign_pass2<false>, dim3(C), dim3(kBlock), 0, s, d, T, scale, ws);
+    }
     return hipGetLastError();
 }
 

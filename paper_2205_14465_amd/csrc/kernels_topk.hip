@@ -227,6 +227,7 @@ __global__ __launch_bounds__(kBlock) void topk_find(const TDesc* __restrict__ d,
 // Candidates = valid entries with key >= t_thr[t], compacted in index
 // order into the chunk's slot of t_cand; also the LDS histogram of their
 // key bits 30..20.
+template <bool kNT>
 __global__ __launch_bounds__(kBlock) void topk_compact(const TDesc* __restrict__ d, int T, uint32_t C,
                                                        int stream_mode, int fb_only, Ws ws) {
     __shared__ uint32_t lh[kBins0];
@@ -241,8 +242,8 @@ __global__ __launch_bounds__(kBlock) void topk_compact(const TDesc* __restrict__
         float v[kEpt];
         uint32_t valid;
         if (stream_mode) {
-            load_v(td, j, td.resid != nullptr, v, valid);
-            if (td.resid) store_chunk(td.resid, td.n, j, v);
+            load_v<kNT>(td, j, td.resid != nullptr, v, valid);
+            if (td.resid) store_chunk<kNT>(td.resid, td.n, j, v);
         } else {
             load_stored_v(td, j, v, valid);
         }
@@ -453,20 +454,23 @@ hipError_t launch_topk(int kind, double ratio, uint64_t seed, const TDesc* d, in
     if (kind == 0) {  // exact
         hipLaunchKernelGGL(topk_hist_pass, dim3(C), blk, 0, s, d, T, C, 1, 0, ws);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindThrExact, 0, ws);
-        (void)launch_timed(kTimedTopkCompact, topk_compact, dim3(C), blk, 0, s, d, T, C, 0, 0, ws);
+        (void)launch_timed(kTimedTopkCompact, topk_compact<false>, dim3(C), blk, 0, s, d, T, C, 0, 0, ws);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit0, 0, ws);
     } else {  // sampled threshold, exact fallback per tensor
         hipLaunchKernelGGL(topk_sample_hist, dim3((C + kSampleChunksPerBlock - 1) / kSampleChunksPerBlock), blk,
                            0, s, d, T, C, seed, ws);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindThrSample, 0, ws);
-        (void)launch_timed(kTimedTopkCompact, topk_compact, dim3(C), blk, 0, s, d, T, C, 1, 0, ws);
+        if (C > kNtChunks)
+            (void)launch_timed(kTimedTopkCompact, topk_compact<true>, dim3(C), blk, 0, s, d, T, C, 1, 0, ws);
+        else
+            (void)launch_timed(kTimedTopkCompact, topk_compact<false>, dim3(C), blk, 0, s, d, T, C, 1, 0, ws);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit0, 0, ws);
         // fallback passes: small grids that walk the chunks, and return at
         // once when no tensor fell back (the usual case)
         const dim3 fb_grid(C < 1024u ? C : 1024u);
         hipLaunchKernelGGL(topk_hist_pass, fb_grid, blk, 0, s, d, T, C, 0, 1, ws);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindThrExact, 1, ws);
-        hipLaunchKernelGGL(topk_compact, fb_grid, blk, 0, s, d, T, C, 0, 1, ws);
+        hipLaunchKernelGGL(topk_compact<false>, fb_grid, blk, 0, s, d, T, C, 0, 1, ws);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit0, 1, ws);
     }
     uint32_t span = C / 1024u;

@@ -82,6 +82,11 @@ inline hipError_t launch_timed(int k, F kernel, dim3 grid, dim3 block, size_t ld
     return hipGetLastError();
 }
 
+// Streaming passes of calls with more chunks than this use non-temporal
+// loads and stores: their g and e (6 to 8 bytes per element) outgrow the
+// 256 MB last-level cache, which smaller sets keep between passes.
+constexpr uint32_t kNtChunks = 8192;
+
 // ------------------------------------------------------------- launchers
 // d: device TDesc[T]; C: total chunks.  Return the first HIP error.
 hipError_t launch_sign_compress(const TDesc* d, int T, uint32_t C, uint32_t max_chunks, bool any_empty,

@@ -187,8 +187,12 @@ def main():
     compress_call = B.CompressCall(kind, wl.ratio, grads, resids, own, ws, stream=stream)
     aggregate_call = B.AggregateCall(kind, wl.ratio, payloads, wl.sizes, outs, alpha, ws, stream=stream)
 
+    # the caller varies the seed per iteration (random-k indices, the
+    # sampled threshold's sample)
+    seeds = iter(range(WL.SEED, WL.SEED + (1 << 62)))
+
     def compress():
-        compress_call(WL.SEED)
+        compress_call(next(seeds))
 
     def aggregate():
         aggregate_call()

@@ -105,6 +105,23 @@ def test_sampled_fallback_path_matches_exact():
         assert_resid_equal(got_e, want_e)
 
 
+def test_sampled_fallback_mixed_with_kept_candidates():
+    # one call where a tensor falls back (its stream pass had zeroed its
+    # candidates in e_new, which the fallback writes back), a large tensor
+    # whose sample holds zeros (threshold 0: every element a candidate, no
+    # zeroing) and small tensors below the sampling size
+    rng = np.random.default_rng(29)
+    ns = [70000, 140001, 100, 5000]
+    grads, resids = make_set(ns, rng)
+    grads[1][rng.random(ns[1]) < 0.3] = 0.0
+    resids[1][grads[1] == 0.0] = 0.0
+    for ratio in (1.0, 0.5):
+        got, got_e = gpu_compress("topk_sampled", ratio, SEED, grads, resids)
+        want, want_e = O.compress_set("topk", ratio, SEED, grads, resids)
+        assert_sparse_equal(got, want, ns)
+        assert_resid_equal(got_e, want_e)
+
+
 @pytest.mark.parametrize("T, ratio", [(9000, 0.05), (17000, 0.02), (17000, 1.0)])
 def test_randk_many_chunks(T, ratio):
     """More than 8192 chunks: indices are bucketed by runs of 2 and 4 chunks

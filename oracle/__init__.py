@@ -76,6 +76,20 @@ def lib():
         L.bco_randk_index.argtypes = [_u64, _u64, _u32, _u64]
         L.bco_sample_size.restype = _u64
         L.bco_sample_size.argtypes = [_u64]
+        L.bco_quant_levels.restype = _int
+        L.bco_quant_levels.argtypes = [_int]
+        L.bco_quant_words.restype = _u64
+        L.bco_quant_words.argtypes = [_u64, _int]
+        L.bco_quant_uniform.restype = _flt
+        L.bco_quant_uniform.argtypes = [_u64, _u32, _u64]
+        L.bco_quant_decode.restype = _flt
+        L.bco_quant_decode.argtypes = [_u32, _int, _flt]
+        L.bco_compress_quant.restype = _int
+        L.bco_compress_quant.argtypes = [_vp, _int, _vp, _u64, _int, _u64, _u32, _vp, _vp, _vp]
+        L.bco_residual_update_quant.restype = _int
+        L.bco_residual_update_quant.argtypes = [_vp, _int, _vp, _u64, _int, _vp, _flt]
+        L.bco_aggregate_quant.restype = _int
+        L.bco_aggregate_quant.argtypes = [_int, _u64, _int, _vp, _vp, _flt, _vp]
         _lib = L
     return _lib
 
@@ -277,19 +291,97 @@ def sample_size(n):
     return int(lib().bco_sample_size(int(n)))
 
 
+# ------------------------------------------------ stochastic quantizers
+# Paper Sec. 2.3: quantization to 8 bits, 2 bits (TernGrad) or 1 bit, with
+# error feedback.  Kinds here: "terngrad" (2-bit codes, 1 level),
+# "qsgd4" (4-bit, 7 levels), "qsgd8" (8-bit, 127 levels); the definitions
+# are in the C source.
+
+QUANT_BITS = {"terngrad": 2, "qsgd4": 4, "qsgd8": 8}
+
+
+def quant_levels(bits):
+    return int(lib().bco_quant_levels(int(bits)))
+
+
+def quant_words(n, bits):
+    return int(lib().bco_quant_words(int(n), int(bits)))
+
+
+def quant_uniform(seed, tensor_id, i):
+    return np.float32(lib().bco_quant_uniform(int(seed), int(tensor_id), int(i)))
+
+
+def quant_decode(code, bits, scale):
+    return np.float32(lib().bco_quant_decode(int(code), int(bits), float(scale)))
+
+
+def compress_quant(g, e, bits, seed, tensor_id):
+    g, dt = _grad(g)
+    n = g.size
+    e = _resid(e, n)
+    words = np.empty(quant_words(n, bits), np.uint32)
+    scale = np.zeros(1, np.float32)
+    e_out = np.empty(n, np.float32) if e is not None else None
+    rc = lib().bco_compress_quant(_p(g), dt, _p(e), n, int(bits), int(seed), int(tensor_id),
+                                  _p(words), _p(scale), _p(e_out))
+    assert rc == 0, rc
+    return words, scale[0], e_out
+
+
+def residual_update_quant(g, e, bits, words, scale):
+    g, dt = _grad(g)
+    n = g.size
+    e = np.array(e, dtype=np.float32, copy=True)
+    words = np.ascontiguousarray(words, np.uint32)
+    rc = lib().bco_residual_update_quant(_p(g), dt, _p(e), n, int(bits), _p(words), float(scale))
+    assert rc == 0, rc
+    return e
+
+
+def aggregate_quant(n, bits, words_list, scales, alpha=1.0):
+    W = len(words_list)
+    words_list = [np.ascontiguousarray(a, np.uint32) for a in words_list]
+    wp = (ctypes.c_void_p * max(W, 1))(*[a.ctypes.data for a in words_list])
+    sc = np.ascontiguousarray(np.asarray(scales, dtype=np.float32).reshape(-1))
+    out = np.empty(n, np.float32)
+    rc = lib().bco_aggregate_quant(W, n, int(bits), ctypes.cast(wp, _vp), _p(sc), float(alpha), _p(out))
+    assert rc == 0, rc
+    return out
+
+
+def quant_word_offsets(ns, bits):
+    off = np.zeros(len(ns) + 1, dtype=np.int64)
+    for t, n in enumerate(ns):
+        off[t + 1] = off[t] + quant_words(n, bits)
+    return off
+
+
 # ------------------------------------------------------ tensor-list calls
 
-KINDS = ("topk", "topk_sampled", "randk", "sign")
+KINDS = ("topk", "topk_sampled", "randk", "sign", "terngrad", "qsgd4", "qsgd8")
 
 
 def compress_set(kind, ratio, seed, grads, resids):
     """Compress a list of tensors; returns (payload dict, list of new residuals).
 
-    Sparse kinds: payload {"idx", "val", "off"}; sign: {"bits", "scale", "off"}.
+    Sparse kinds: payload {"idx", "val", "off"}; sign and the quantizers:
+    {"bits", "scale", "off"} (packed code words, one scale per tensor).
     """
     T = len(grads)
     ns = [g.size for g in grads]
     new_e = []
+    if kind in QUANT_BITS:
+        bits_per = QUANT_BITS[kind]
+        off = quant_word_offsets(ns, bits_per)
+        bits = np.empty(int(off[-1]), np.uint32)
+        scale = np.empty(T, np.float32)
+        for t in range(T):
+            w, s, e_out = compress_quant(grads[t], None if resids is None else resids[t], bits_per, seed, t)
+            bits[off[t]:off[t + 1]] = w
+            scale[t] = s
+            new_e.append(e_out)
+        return {"bits": bits, "scale": scale, "off": off}, new_e
     if kind == "sign":
         off = word_offsets(ns)
         bits = np.empty(int(off[-1]), np.uint32)
@@ -323,7 +415,11 @@ def aggregate_set(kind, ns, payloads, alpha=1.0):
     """Aggregate W payload dicts (laid out as compress_set returns) per tensor."""
     outs = []
     for t, n in enumerate(ns):
-        if kind == "sign":
+        if kind in QUANT_BITS:
+            ws = [p["bits"][p["off"][t]:p["off"][t + 1]] for p in payloads]
+            ss = [p["scale"][t] for p in payloads]
+            outs.append(aggregate_quant(n, QUANT_BITS[kind], ws, ss, alpha))
+        elif kind == "sign":
             ws = [p["bits"][p["off"][t]:p["off"][t + 1]] for p in payloads]
             ss = [p["scale"][t] for p in payloads]
             outs.append(aggregate_sign(n, ws, ss, alpha))

@@ -15,6 +15,10 @@
  *   - The evaluated operators are Randomk and DGC at a 1% rate and
  *     EFSignSGD, with error feedback on every compression (paper Sec. 5.1,
  *     "Compression algorithms").
+ *   - Quantization to 8 bits and to 2 bits (TernGrad) is named beside the
+ *     1-bit kind (paper Sec. 2.3) but not evaluated; the stochastic
+ *     quantizers at the end of this file are a stated reading of the
+ *     cited works.
  *   - In an indivisible scheme every node decompresses the N payloads it
  *     gathered and aggregates them; compressed aggregation is not
  *     associative, so it cannot be an Allreduce (paper Sec. 3.1, Reason #2
@@ -632,3 +636,139 @@ float bco_exact_sum_f32(const float* x, uint64_t m)
 /* Bit pattern helpers exported for tests. */
 uint32_t bco_f32_bits(float x) { return f2u(x); }
 float bco_bits_f32(uint32_t u) { return u2f(u); }
+
+/* ------------------------------------------------------------------ */
+/* Stochastic b-bit quantization with error feedback (paper Sec. 2.3:   */
+/* quantization maps fp32 gradients to fewer bits -- 8 bits, 2 bits     */
+/* (TernGrad), 1 bit -- and is combined with error feedback).  The      */
+/* paper defines none of these operators; the reading here follows the */
+/* cited stochastic quantizers (TernGrad: ternary levels scaled by the  */
+/* largest magnitude, each nonzero with probability |v|/max; QSGD:      */
+/* s uniform levels with stochastic rounding to a neighbouring level),  */
+/* with the largest magnitude as the norm so that the scale does not    */
+/* depend on a summation order:                                         */
+/*                                                                      */
+/*   bits b in {2, 4, 8}; levels s = 2^(b-1) - 1 (1, 7, 127);           */
+/*   v = fl32(g + e_old); m = max |v_i| (the payload's scale);          */
+/*   inv = fl32(s / m) and unit = fl32(m / s), each one fp64 division   */
+/*   rounded to fp32;                                                   */
+/*   x_i = fl32(|v_i| * inv); if x_i >= s the level is s, else with     */
+/*   l = floor(x_i) and p = x_i - l (exact), the level is l + 1 when    */
+/*   U_i < p and l otherwise;                                           */
+/*   U_i = (u_i >> 8) * 2^-24 with u_i the 32-bit word i mod 8 of the   */
+/*   Philox4x64-10 block at counter (tensor_id, i / 8, 0, 0), key       */
+/*   (seed, stream 2): 64-bit output word (i mod 8) / 2, its low half   */
+/*   for even i, high half for odd i;                                   */
+/*   code = 0 for level 0, else level | (sign bit of v_i) << (b - 1);   */
+/*   codes are packed b bits each, LSB first, 32 / b per 32-bit word,   */
+/*   each tensor starting a new word;                                   */
+/*   decode: d = 0 for level 0, else +-fl32(level * unit) with the sign */
+/*   of the code;  e_new = fl32(v - d);  m = 0 gives all-zero codes.    */
+/* ------------------------------------------------------------------ */
+
+#define STREAM_QUANT 2u
+
+int bco_quant_levels(int bits)
+{
+    if (bits != 2 && bits != 4 && bits != 8) return 0;
+    return (1 << (bits - 1)) - 1;
+}
+
+uint64_t bco_quant_words(uint64_t n, int bits) { return (n * (uint64_t)bits + 31u) / 32u; }
+
+/* The uniform U_i of element i (exact fp32 in [0, 1)). */
+float bco_quant_uniform(uint64_t seed, uint32_t tensor_id, uint64_t i)
+{
+    uint64_t ctr[4] = { tensor_id, i / 8u, 0, 0 };
+    uint64_t key[2] = { seed, STREAM_QUANT };
+    uint64_t w[4];
+    bco_philox4x64_10(ctr, key, w);
+    uint64_t x = w[(i % 8u) / 2u];
+    uint32_t u = (i % 2u) ? (uint32_t)(x >> 32) : (uint32_t)x;
+    return (float)(u >> 8) * 0x1p-24f;
+}
+
+/* Decoded value of one code for a tensor whose payload scale is m. */
+float bco_quant_decode(uint32_t code, int bits, float m)
+{
+    int s = bco_quant_levels(bits);
+    uint32_t level = code & ((1u << (bits - 1)) - 1u);
+    if (level == 0 || s == 0) return 0.0f;
+    float unit = (float)((double)m / (double)s);
+    float mag = (float)level * unit;
+    return ((code >> (bits - 1)) & 1u) ? -mag : mag;
+}
+
+static uint32_t quant_code_at(const uint32_t* words, uint64_t i, int bits)
+{
+    uint64_t pos = i * (uint64_t)bits;
+    return (words[pos / 32u] >> (pos % 32u)) & ((1u << bits) - 1u);
+}
+
+int bco_compress_quant(const void* g, int dtype, const float* e_in, uint64_t n, int bits,
+                       uint64_t seed, uint32_t tensor_id, uint32_t* words, float* scale,
+                       float* e_out)
+{
+    int s = bco_quant_levels(bits);
+    if (s == 0) return -1;
+    float* v = ef_accumulate(g, dtype, e_in, n);
+    if (!v) return -2;
+    float m = 0.0f;
+    for (uint64_t i = 0; i < n; ++i) {
+        float a = fabsf(v[i]);
+        if (a > m) m = a;
+    }
+    *scale = m;
+    uint64_t nw = bco_quant_words(n, bits);
+    for (uint64_t w = 0; w < nw; ++w) words[w] = 0u;
+    float inv = m > 0.0f ? (float)((double)s / (double)m) : 0.0f;
+    for (uint64_t i = 0; i < n; ++i) {
+        uint32_t level = 0;
+        if (m > 0.0f) {
+            float x = fabsf(v[i]) * inv;
+            if (x >= (float)s) {
+                level = (uint32_t)s;
+            } else {
+                float l = floorf(x);
+                float p = x - l;
+                level = (uint32_t)l + (bco_quant_uniform(seed, tensor_id, i) < p ? 1u : 0u);
+            }
+        }
+        uint32_t code = level ? (level | ((f2u(v[i]) >> 31) << (bits - 1))) : 0u;
+        uint64_t pos = i * (uint64_t)bits;
+        words[pos / 32u] |= code << (pos % 32u);
+    }
+    if (e_out) {
+        for (uint64_t i = 0; i < n; ++i)
+            e_out[i] = v[i] - bco_quant_decode(quant_code_at(words, i, bits), bits, m);
+    }
+    free(v);
+    return 0;
+}
+
+int bco_residual_update_quant(const void* g, int dtype, float* e_inout, uint64_t n, int bits,
+                              const uint32_t* words, float scale)
+{
+    if (bco_quant_levels(bits) == 0) return -1;
+    float* v = ef_accumulate(g, dtype, e_inout, n);
+    if (!v) return -2;
+    for (uint64_t i = 0; i < n; ++i)
+        e_inout[i] = v[i] - bco_quant_decode(quant_code_at(words, i, bits), bits, scale);
+    free(v);
+    return 0;
+}
+
+/* Aggregate: each output starts at +0.0 and adds the W decoded values in
+ * ascending worker order, one fp32 addition each, then alpha times that. */
+int bco_aggregate_quant(int W, uint64_t n, int bits, const uint32_t* const* words_w,
+                        const float* scale_w, float alpha, float* out)
+{
+    if (bco_quant_levels(bits) == 0) return -1;
+    for (uint64_t i = 0; i < n; ++i) {
+        float acc = 0.0f;
+        for (int w = 0; w < W; ++w)
+            acc = acc + bco_quant_decode(quant_code_at(words_w[w], i, bits), bits, scale_w[w]);
+        out[i] = alpha * acc;
+    }
+    return 0;
+}

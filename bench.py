@@ -8,8 +8,8 @@ the W generated worker payloads) are resident in HBM before timing starts.
 value = algorithmic bytes per step / time per step, in GB/s, where the
 algorithmic bytes are what the method must move:
   compress:  read g (4 B/elem fp32, 2 B fp16) + read e (4 B) + write e (4 B)
-             + write the payload (8 B per sparse entry; 4 B per sign word
-             + 4 B per tensor scale)
+             + write the payload (8 B per sparse entry; 4 B per sign or
+             quantizer code word + 4 B per tensor scale)
   aggregate: read W payloads + write the dense fp32 output (4 B/elem).
 The roofline entry reports the dominant kernel's algorithmic bytes per
 launch over its average launch duration (HIP events that the library
@@ -31,6 +31,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+WORD_KINDS = ("sign", "terngrad", "qsgd4", "qsgd8")  # payload: packed words + one scale per tensor
 METRIC = "gradient GB/s through compress+EF and decompress-aggregate; % of HBM peak"
 
 
@@ -41,7 +42,7 @@ def log(msg):
 def algorithmic_bytes(wl, off, kind):
     n = wl.n_total
     gbytes = 2 if wl.grad_dtype == "float16" else 4
-    if kind == "sign":
+    if kind in WORD_KINDS:
         payload = 4 * int(off[-1]) + 4 * wl.T
     else:
         payload = 8 * int(off[-1])
@@ -71,6 +72,8 @@ def cpu_baseline(wl, off, budget_s=15.0):
         t0 = time.perf_counter()
         if kind == "sign":
             w_, s_, _ = O.compress_sign(g, e)
+        elif kind in O.QUANT_BITS:
+            O.compress_quant(g, e, O.QUANT_BITS[kind], WL.SEED, t)
         elif kind == "topk":
             O.compress_topk(g, e, wl.ratio)
         elif kind == "topk_sampled":
@@ -79,7 +82,7 @@ def cpu_baseline(wl, off, budget_s=15.0):
             O.compress_randk(g, e, wl.ratio, WL.SEED, t)
         comp_s += time.perf_counter() - t0
         n = wl.sizes[t]
-        pay = (4 * counts[t] + 4) if kind == "sign" else 8 * counts[t]
+        pay = (4 * counts[t] + 4) if kind in WORD_KINDS else 8 * counts[t]
         comp_bytes += (gbytes + 8) * n + pay
         # aggregate this tensor over W generated payloads
         lists = []
@@ -87,12 +90,16 @@ def cpu_baseline(wl, off, budget_s=15.0):
             rng = WL.rng_for(wl.wid, t, WL.ROLE_WORKER + w)
             if kind == "sign":
                 lists.append(WL.random_sign_words(rng, [n], [counts[t]])[0])
+            elif kind in O.QUANT_BITS:
+                lists.append(WL.random_code_words(rng, [n], [counts[t]], O.QUANT_BITS[kind])[0])
             else:
                 i, v = WL.random_sparse_lists(rng, [n], [counts[t]])
                 lists.append((i[0], v[0]))
         t0 = time.perf_counter()
         if kind == "sign":
             O.aggregate_sign(n, lists, [np.float32(1e-3)] * wl.W, 1.0 / wl.W)
+        elif kind in O.QUANT_BITS:
+            O.aggregate_quant(n, O.QUANT_BITS[kind], lists, [np.float32(4e-3)] * wl.W, 1.0 / wl.W)
         else:
             O.aggregate_sparse(n, [a for a, _ in lists], [b for _, b in lists], 1.0 / wl.W)
         agg_s += time.perf_counter() - t0
@@ -149,7 +156,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5, 6, 7, 8])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--scheme", choices=["indivisible", "divisible"], default="indivisible",
                     help="divisible: time node 0's step of the divisible scheme instead")
@@ -180,6 +187,8 @@ def main():
     alpha = 1.0 / wl.W
     stream = torch.cuda.current_stream()
 
+    if args.scheme == "divisible" and kind not in ("topk", "topk_sampled", "randk", "sign"):
+        sys.exit(f"bench.py: the divisible scheme is not built for the {kind} kind")
     if args.scheme == "divisible":
         return divisible(args, wl, off, payloads, ws, dev, stream)
 
@@ -222,7 +231,8 @@ def main():
     # of stream time, so they stay out of the region above), and the
     # dominant kernel's own duration: the library brackets its next launch
     # with a further pair of events (hipExtLaunchKernelGGL)
-    dom_kernel = {"sign": "aggregate_sign", "randk": "randk_stream"}.get(kind, "aggregate_sparse")
+    dom_kernel = {"sign": "aggregate_sign", "randk": "randk_stream", "terngrad": "aggregate_quant",
+                  "qsgd4": "aggregate_quant", "qsgd8": "aggregate_quant"}.get(kind, "aggregate_sparse")
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(reps)]
     for r in range(reps):
         for e in ev[r][4:]:
@@ -264,7 +274,8 @@ def main():
     comp_gbs = comp_b / (comp_avg * 1e-3) / 1e9
     agg_gbs = agg_b / (agg_avg * 1e-3) / 1e9
     # Dominant kernel: the longest single kernel of the step.  Sign:
-    # aggregate_sign (longer than either compress pass).  Top-k kinds:
+    # aggregate_sign (longer than either compress pass); the quantizers
+    # likewise aggregate_quant.  Top-k kinds:
     # aggregate_sparse (longer than any compress kernel).  Random-k:
     # randk_stream, which moves every algorithmic byte of the compress
     # call.  Its time is its own launch duration from the events above.
@@ -287,7 +298,7 @@ def main():
         "data": "synthetic",
         "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
         "config": {"workload": wl.name, "kind": kind, "tensors": wl.T, "elements": wl.n_total,
-                   "ratio": wl.ratio if kind != "sign" else None, "W": wl.W,
+                   "ratio": wl.ratio if kind not in WORD_KINDS else None, "W": wl.W,
                    "payload_bytes_per_worker": pay_b},
         "ops": {"compress_ms": round(comp_avg, 4), "compress_gbs": round(comp_gbs, 1),
                 "compress_pct_peak": round(100 * comp_gbs / HBM_PEAK_GBS, 2),

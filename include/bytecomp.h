@@ -15,6 +15,11 @@
  *                    BC_TOPK, different cost)
  *   BC_RANDK         seeded random-k (Randomk)
  *   BC_SIGN1         1-bit sign with one scale per tensor (EFSignSGD)
+ *   BC_TERNGRAD      2-bit stochastic ternary quantization (TernGrad)
+ *   BC_QSGD4         4-bit stochastic quantization, 7 levels (QSGD)
+ *   BC_QSGD8         8-bit stochastic quantization, 127 levels (QSGD)
+ *                    (Sec. 2.3 names 8-bit, 2-bit and 1-bit quantization;
+ *                    the paper does not evaluate the first two)
  * Error feedback (paper Sec. 2.3 and Sec. 5.1): the compressed vector is
  * v = g + e_old and the residual e_new = v - decompress(payload) is written
  * back in place.
@@ -49,7 +54,8 @@
 extern "C" {
 #endif
 
-enum bc_kind { BC_TOPK = 0, BC_TOPK_SAMPLED = 1, BC_RANDK = 2, BC_SIGN1 = 3 };
+enum bc_kind { BC_TOPK = 0, BC_TOPK_SAMPLED = 1, BC_RANDK = 2, BC_SIGN1 = 3,
+               BC_TERNGRAD = 4, BC_QSGD4 = 5, BC_QSGD8 = 6 };
 enum bc_dtype { BC_F32 = 0, BC_F16 = 1 };
 
 enum bc_status {
@@ -74,7 +80,8 @@ enum bc_status {
  *   n         element count
  *   dtype     BC_F32 or BC_F16
  *   tensor_id key of the per-tensor random streams (BC_RANDK, the sample
- *             of BC_TOPK_SAMPLED); by convention the tensor's position in
+ *             of BC_TOPK_SAMPLED, the rounding of the quantizers); by
+ *             convention the tensor's position in
  *             the model, kept stable when only a subset is compressed */
 typedef struct bc_tensor {
     const void* grad;
@@ -90,7 +97,10 @@ typedef struct bc_tensor {
  * values fp32.  BC_SIGN1 uses bits/scale: tensor t occupies words
  * [off[t], off[t+1]), element i of the tensor at bit (i mod 32) of word
  * off[t] + i/32 (1 = negative), bits past the tensor's end zero, and
- * scale[t] is its fp32 scale.  Unused members may be NULL. */
+ * scale[t] is its fp32 scale.  The quantizers (b = 2, 4, 8 bits per
+ * element) also use bits/scale: element i's b-bit code at bit (i*b mod 32)
+ * of word off[t] + i*b/32, codes past the tensor's end zero, scale[t] the
+ * tensor's largest |v|.  Unused members may be NULL. */
 typedef struct bc_payload {
     uint32_t* idx;
     float* val;
@@ -106,6 +116,7 @@ const char* bytecomp_strerror(int status);
  * ratio))) (0 when n_t = 0), the ratio taken in whole parts per million;
  * this reads the paper's "1% compression rate" (Sec. 5.1) as an exact k.
  * BC_SIGN1: off[t+1] - off[t] = ceil(n_t / 32) words (ratio ignored).
+ * Quantizers: ceil(n_t * b / 32) words, b = 2, 4 or 8 (ratio ignored).
  *   n    host, T element counts
  *   off  host, T+1 entries written, off[0] = 0 */
 int bytecomp_layout(int kind, double ratio, const uint64_t* n, int T, uint64_t* off);
@@ -124,9 +135,10 @@ int bytecomp_workspace_size(int kind, double ratio, const uint64_t* n, int T, in
 int bytecomp_workspace_init(void* ws, size_t ws_bytes, void* stream);
 
 /* Compress T tensors with error feedback (paper Sec. 2.3, Sec. 5.1).
- *   kind, ratio  operator and compression rate (ratio unused by BC_SIGN1)
- *   seed         key of the random streams (BC_RANDK, BC_TOPK_SAMPLED);
- *                vary it per iteration
+ *   kind, ratio  operator and compression rate (ratio used by the sparse
+ *                kinds only)
+ *   seed         key of the random streams (BC_RANDK, BC_TOPK_SAMPLED,
+ *                the quantizers' rounding); vary it per iteration
  *   t            host, T tensor descriptors
  *   out          payload to write (device pointers), laid out as
  *                bytecomp_layout describes
@@ -137,6 +149,15 @@ int bytecomp_workspace_init(void* ws, size_t ws_bytes, void* stream);
  * values v[idx]; the residual becomes v with the selected entries +0.0.
  * BC_SIGN1 emits the sign bits of v and scale s_t = mean |v| (summed in
  * fp64) rounded to fp32; the residual becomes v - (bit ? -s_t : +s_t).
+ * Quantizers (b bits, s = 2^(b-1) - 1 levels): m_t = max |v| is the
+ * scale; with inv = fl32(s / m_t) and x = fl32(|v_i| * inv), the level is s
+ * when x >= s, else floor(x) + 1 when U_i < x - floor(x) and floor(x)
+ * otherwise, where U_i = (u >> 8) * 2^-24 and u is 32-bit word i mod 8
+ * (low half of 64-bit output word (i mod 8)/2 for even i, high half for odd
+ * i) of the Philox4x64-10 block at counter (tensor_id, i/8, 0, 0) and key
+ * (seed, 2); the code is the level with the sign bit of v_i at bit b-1 (0
+ * for level 0); decoding gives +-fl32(level * fl32(m_t / s)) and the
+ * residual becomes v - decoded.
  * Limits of BC_RANDK: fewer than 2^32 payload entries in the call and at
  * most 2^22 chunks of 4096 elements (about 1.7e10 elements); BC_E_SIZE
  * otherwise. */
@@ -153,7 +174,8 @@ int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t,
  *          (16-byte aligned)
  *   alpha  scale applied to each sum (1 = sum, 1/W = mean)
  *   ws     workspace: BC_SIGN1 needs bytecomp_workspace_size bytes (it keeps
- *          one flag per tensor there); sparse kinds need its 256-byte header
+ *          one flag per tensor there); the other kinds need its 256-byte
+ *          header
  * Sparse kinds: out_t[i] = alpha * (sum over workers w = 0..W-1, in that
  * order, of worker w's value at i), each addition in fp32 starting from
  * +0.0; elements no worker sent are alpha * 0.
@@ -162,7 +184,10 @@ int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t,
  * rounded once to fp32.  This form applies when tensor t's W scales are
  * finite and normal or zero and their binary exponents span at most
  * 29 - ceil(log2 W) binades; otherwise the worker-ordered fp32 sum, as for
- * the sparse kinds.  Results are deterministic. */
+ * the sparse kinds.  Quantizers: out_t[i] = alpha * (sum over w = 0..W-1,
+ * in that order, of worker w's decoded value at i), each addition in fp32
+ * starting from +0.0; at most 1024 workers (BC_E_COUNT otherwise).
+ * Results are deterministic. */
 int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, int W,
                                   const uint64_t* n, int T, float* const* out, float alpha,
                                   void* ws, size_t ws_bytes, void* stream);
@@ -183,7 +208,8 @@ int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, 
  *   part_off  device, T + 1 uint64: the packed offset of each tensor's part
  *             (entries, or words), then the total.
  * BC_E_ALIGN if an inner bound is not a multiple of 32, BC_E_SIZE if bounds
- * do not run from 0 to n_t in order.  Stream-ordered like the rest. */
+ * do not run from 0 to n_t in order.  Stream-ordered like the rest.
+ * BC_E_KIND for the quantizers (not supported in the divisible scheme). */
 int bytecomp_pack_part(int kind, double ratio, const uint64_t* n, int T, bc_payload in, int parts,
                        const uint64_t* bounds, int j, bc_payload out, uint64_t* part_off, void* stream);
 
@@ -200,7 +226,8 @@ int bytecomp_pack_part(int kind, double ratio, const uint64_t* n, int T, bc_payl
  * out_t[i] = alpha * the worker-ordered fp32 sum (sparse) or the exact sum
  * rounded once (sign) of the senders' values at i, exactly as
  * bytecomp_decompress_aggregate defines them, so the parts of all nodes
- * assemble the whole aggregate bit for bit.  Sparse kinds take at most 64
+ * assemble the whole aggregate bit for bit.  BC_E_KIND for the quantizers.
+ * Sparse kinds take at most 64
  * senders (BC_E_COUNT otherwise).  ws: as bytecomp_decompress_aggregate for
  * the range lengths. */
 int bytecomp_aggregate_part(int kind, double ratio, const bc_payload* in, const uint64_t* const* part_off,
@@ -223,7 +250,8 @@ int bytecomp_device_status(void* ws, size_t ws_bytes, void* stream, uint32_t* fl
 /* Instrumentation, not part of the method: for callers that measure one
  * kernel's own duration (benchmarks).  The next launch, by any call, of
  * the kernel named `kernel` ("aggregate_sign", "aggregate_sparse",
- * "randk_stream", "topk_compact", "sign_pass1") records `start_event`
+ * "randk_stream", "topk_compact", "sign_pass1", "quant_pass1",
+ * "aggregate_quant") records `start_event`
  * when it begins and `stop_event` when it ends (HIP events created by the
  * caller, on the launch's stream); the request is then cleared.  Both
  * events NULL clears a pending request.  BC_E_KIND for an unknown name.

@@ -16,8 +16,12 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libbytecomp.so")
 
 BC_TOPK, BC_TOPK_SAMPLED, BC_RANDK, BC_SIGN1 = 0, 1, 2, 3
+BC_TERNGRAD, BC_QSGD4, BC_QSGD8 = 4, 5, 6
 BC_F32, BC_F16 = 0, 1
-KIND = {"topk": BC_TOPK, "topk_sampled": BC_TOPK_SAMPLED, "randk": BC_RANDK, "sign": BC_SIGN1}
+KIND = {"topk": BC_TOPK, "topk_sampled": BC_TOPK_SAMPLED, "randk": BC_RANDK, "sign": BC_SIGN1,
+        "terngrad": BC_TERNGRAD, "qsgd4": BC_QSGD4, "qsgd8": BC_QSGD8}
+# kinds whose payload is packed words plus one scale per tensor
+WORD_KINDS = (BC_SIGN1, BC_TERNGRAD, BC_QSGD4, BC_QSGD8)
 STATUS = {0: "BC_OK", -1: "BC_E_NULL", -2: "BC_E_KIND", -3: "BC_E_DTYPE", -4: "BC_E_RATIO",
           -5: "BC_E_SIZE", -6: "BC_E_COUNT", -7: "BC_E_WORKSPACE", -8: "BC_E_HIP",
           -9: "BC_E_ALIGN", -10: "BC_E_DEVICE"}
@@ -341,7 +345,7 @@ def alloc_payload(kind, ratio, ns, device="cuda"):
     import torch
     off = bytecomp_layout(kind, ratio, ns)
     total = off[-1]
-    if _kind(kind) == BC_SIGN1:
+    if _kind(kind) in WORD_KINDS:
         return {"bits": torch.zeros(max(total, 1), dtype=torch.int32, device=device),
                 "scale": torch.zeros(max(len(ns), 1), dtype=torch.float32, device=device), "off": off}
     return {"idx": torch.zeros(max(total, 1), dtype=torch.int32, device=device),

@@ -48,6 +48,19 @@ uint64_t words_of(uint64_t n) { return (n + 31u) / 32u; }
 
 bool is_sparse(int kind) { return kind == BC_TOPK || kind == BC_TOPK_SAMPLED || kind == BC_RANDK; }
 
+// Bits per element of the stochastic quantizers (0 for the other kinds).
+int quant_bits(int kind) {
+    return kind == BC_TERNGRAD ? 2 : kind == BC_QSGD4 ? 4 : kind == BC_QSGD8 ? 8 : 0;
+}
+
+// Payload entries (sparse kinds) or 32-bit words (sign, quantizers) of a
+// tensor of n elements.
+uint64_t count_of(int kind, uint64_t n, uint64_t ppm) {
+    if (is_sparse(kind)) return k_of(n, ppm);
+    if (const int b = quant_bits(kind)) return (n * (uint64_t)b + 31u) / 32u;
+    return words_of(n);
+}
+
 size_t align256(size_t x) { return (x + 255u) & ~(size_t)255u; }
 
 // ----------------------------------------------------- descriptor cache
@@ -205,6 +218,9 @@ WsPlan plan_workspace(int kind, int T, uint64_t C, uint64_t sum_k) {
         take(p.s_partial, (size_t)C * 8);
         take(p.s_info, t * 4);
         take(p.s_tab, t * 2048 * 4);
+    } else if (quant_bits(kind)) {
+        take(p.s_val, t * 4);
+        take(p.q_max, (size_t)C * 4);
     } else if (kind == BC_TOPK || kind == BC_TOPK_SAMPLED) {
         take(p.t_hist, t * kBins0 * 4);
         take(p.t_thr, t * 4);
@@ -243,6 +259,7 @@ Ws carve_workspace(void* base, const WsPlan& p) {
     w.s_partial = (double*)at(p.s_partial);
     w.s_info = (uint32_t*)at(p.s_info);
     w.s_tab = (int32_t*)at(p.s_tab);
+    w.q_max = (uint32_t*)at(p.q_max);
     w.t_hist = (uint32_t*)at(p.t_hist);
     w.t_thr = (uint32_t*)at(p.t_thr);
     w.t_prefix = (uint32_t*)at(p.t_prefix);
@@ -308,7 +325,7 @@ int build_tdesc(int kind, uint64_t ppm, const bc_tensor* t, int T, bool need_res
         o.n = (uint32_t)x.n;
         o.dtype = x.dtype;
         o.tid = x.tensor_id;
-        const uint64_t cnt = is_sparse(kind) ? k_of(x.n, ppm) : words_of(x.n);
+        const uint64_t cnt = count_of(kind, x.n, ppm);
         o.k = (uint32_t)cnt;
         o.off = off;
         o.chunk0 = (uint32_t)chunks;
@@ -331,7 +348,7 @@ void fill_chunk_map(const std::vector<TDesc>& d, uint32_t* m) {
 }
 
 int check_kind_ratio(int kind, double ratio, uint64_t& ppm) {
-    if (kind < BC_TOPK || kind > BC_SIGN1) return BC_E_KIND;
+    if (kind < BC_TOPK || kind > BC_QSGD8) return BC_E_KIND;
     ppm = 1;
     if (is_sparse(kind)) {
         ppm = ratio_ppm(ratio);
@@ -370,7 +387,7 @@ int bytecomp_layout(int kind, double ratio, const uint64_t* n, int T, uint64_t* 
     off[0] = 0;
     for (int t = 0; t < T; ++t) {
         if (n[t] >= kMaxN) return BC_E_SIZE;
-        off[t + 1] = off[t] + (is_sparse(kind) ? k_of(n[t], ppm) : words_of(n[t]));
+        off[t + 1] = off[t] + count_of(kind, n[t], ppm);
     }
     return BC_OK;
 }
@@ -443,6 +460,12 @@ int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t,
             e = launch_topk(kind == BC_TOPK ? 0 : 1, ratio, seed, dd, T, C, a16, a32, out.idx, out.val,
                             w, s);
             break;
+        case BC_TERNGRAD:
+        case BC_QSGD4:
+        case BC_QSGD8:
+            e = launch_quant_compress(quant_bits(kind), seed, dd, T, C, maxc, di.any_empty, out.bits, out.scale,
+                                      w, s);
+            break;
         default:
             e = launch_randk(seed, dd, T, C, sum_k, a16, a32, out.idx, out.val, w, s);
             break;
@@ -509,7 +532,7 @@ int aggregate_impl(int kind, double ratio, const bc_payload* in, const uint64_t*
         if (n[i] >= kMaxN) return BC_E_SIZE;
         if (n[i] > 0 && !out[i]) return BC_E_NULL;
         if ((uintptr_t)out[i] & 15u) return BC_E_ALIGN;
-        const uint64_t cnt = sparse ? k_of(n[i], ppm) : words_of(n[i]);
+        const uint64_t cnt = count_of(kind, n[i], ppm);
         const uint64_t nu = (n[i] + unit - 1) / unit;
         a[i].out = out[i];
         a[i].n = (uint32_t)n[i];
@@ -526,7 +549,7 @@ int aggregate_impl(int kind, double ratio, const bc_payload* in, const uint64_t*
         off = 1;                                 // payloads are not addressed by layout
     }
     Ws w{};  // sign: per-tensor forms and lookup tables live in the workspace
-    if (!sparse) {
+    if (kind == BC_SIGN1) {
         uint64_t C = 0;
         for (int i = 0; i < T; ++i) C += (n[i] + kChunk - 1) / kChunk;
         const WsPlan plan = plan_workspace(kind, T, C, 0);
@@ -572,6 +595,8 @@ int aggregate_impl(int kind, double ratio, const bc_payload* in, const uint64_t*
     const uint64_t* wdd = (const uint64_t*)((const char*)en->dev + rp_bytes + (size_t)T * sizeof(ADesc));
     if (sparse) {
         e = launch_aggregate_sparse(ad, T, (uint32_t)units, unit, wdd, W, alpha, di.cus, rpd, s);
+    } else if (quant_bits(kind)) {
+        e = launch_aggregate_quant(quant_bits(kind), ad, T, (uint32_t)units, wdd, W, alpha, s);
     } else {
         e = launch_aggregate_sign(ad, T, (uint32_t)units, wdd, W, alpha, w.s_info, w.s_tab, s);
     }
@@ -592,6 +617,7 @@ int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, 
 int bytecomp_aggregate_part(int kind, double ratio, const bc_payload* in, const uint64_t* const* part_off,
                             int W, const uint64_t* len, int T, float* const* out, float alpha, void* ws,
                             size_t ws_bytes, void* stream) {
+    if (quant_bits(kind)) return BC_E_KIND;  // no divisible-scheme support for the quantizers
     if (kind == BC_SIGN1)  // packed sign parts have the word layout of the range lengths
         return aggregate_impl(kind, ratio, in, nullptr, W, len, T, out, alpha, ws, ws_bytes, stream);
     if (!part_off) return BC_E_NULL;
@@ -603,6 +629,7 @@ int bytecomp_pack_part(int kind, double ratio, const uint64_t* n, int T, bc_payl
     uint64_t ppm;
     int rc = check_kind_ratio(kind, ratio, ppm);
     if (rc) return rc;
+    if (quant_bits(kind)) return BC_E_KIND;  // no divisible-scheme support for the quantizers
     if (T < 0 || T > kMaxT || parts < 1 || j < 0 || j >= parts) return BC_E_COUNT;
     if (T == 0) return BC_OK;
     if (!n || !bounds || !part_off) return BC_E_NULL;
@@ -678,8 +705,11 @@ int bytecomp_residual_update(int kind, double ratio, const bc_tensor* t, int T, 
     hipError_t e = cache_get(d.data(), d.size() * sizeof(TDesc), (size_t)C * 4,
                              [&](void* dst) { fill_chunk_map(d, (uint32_t*)dst); }, s, &en);
     if (e != hipSuccess) return BC_E_HIP;
-    e = launch_residual_update(kind, (const TDesc*)en->dev, T, C, a16, a32, own.idx, own.val,
-                               own.bits, own.scale, s);
+    if (quant_bits(kind))
+        e = launch_quant_residual_update(quant_bits(kind), (const TDesc*)en->dev, T, C, own.bits, own.scale, s);
+    else
+        e = launch_residual_update(kind, (const TDesc*)en->dev, T, C, a16, a32, own.idx, own.val, own.bits,
+                                   own.scale, s);
     cache_mark_used(en, s);
     return finish(hip_status(e), s, nullptr);
 }
@@ -693,7 +723,8 @@ int bytecomp_time_next_launch(const char* kernel, void* start_event, void* stop_
     static const struct { const char* name; int k; } names[] = {
         {"aggregate_sign", kTimedAggSign},       {"aggregate_sparse", kTimedAggSparse},
         {"randk_stream", kTimedRandkStream},     {"topk_compact", kTimedTopkCompact},
-        {"sign_pass1", kTimedSignPass1}};
+        {"sign_pass1", kTimedSignPass1},         {"quant_pass1", kTimedQuantPass1},
+        {"aggregate_quant", kTimedAggQuant}};
     for (const auto& x : names) {
         if (std::strcmp(kernel, x.name) == 0) {
             set_kernel_timer(x.k, (hipEvent_t)start_event, (hipEvent_t)stop_event);

@@ -335,6 +335,7 @@ __host__ __device__ inline U64x4 philox4x64_10(U64x4 c, uint64_t k0, uint64_t k1
 // Random-stream ids (second key word).
 constexpr uint64_t kStreamRandk = 0;
 constexpr uint64_t kStreamSample = 1;
+constexpr uint64_t kStreamQuant = 2;
 
 // Workspace header: failure flags (bit 0 reserved for a bounded wait that
 // ran out; no current kernel waits on another workgroup).

@@ -1,0 +1,341 @@
+// kernels_quant.hip -- stochastic b-bit quantization with error feedback on
+// gfx950: TernGrad (2-bit codes, one level), QSGD with 7 levels (4-bit) and
+// with 127 levels (8-bit) (paper Sec. 2.3: gradients quantized to 8 bits,
+// 2 bits or 1 bit, combined with error feedback).
+//
+// For every tensor: v = g + e_old; m = max |v| (the payload's scale, exact
+// and independent of any summation order); inv = fl32(s / m), unit =
+// fl32(m / s); x = fl32(|v| * inv); the level is s when x >= s, else
+// floor(x) plus one with probability x - floor(x), decided against a
+// uniform U = (u >> 8) * 2^-24 drawn from Philox4x64-10 at counter
+// (tensor_id, i / 8), key (seed, stream 2) -- element i takes 32-bit word
+// i mod 8 of the block; code = level | sign << (b - 1) (0 for level 0),
+// b bits per element, LSB first, each tensor word aligned; decode d =
+// +-fl32(level * unit); e_new = fl32(v - d).
+//
+// Compress in two passes, as for the 1-bit kind: pass 1 forms v, parks it
+// in e and writes each chunk's largest |v| bits; pass 2 takes the tensor's
+// maximum over its chunks, re-reads v, quantizes, packs the codes with lane
+// shuffles and writes the residual.  The aggregate gives each workgroup
+// 4096 output elements (16 per lane) and adds the W workers' decoded values
+// in worker order, one fp32 addition each.
+#include "launch.hpp"
+
+namespace bc {
+
+namespace {
+
+template <int kBits>
+struct Quant {
+    static constexpr int kLevels = (1 << (kBits - 1)) - 1;
+    static constexpr uint32_t kMask = (1u << kBits) - 1u;
+    static constexpr uint32_t kLevelMask = (1u << (kBits - 1)) - 1u;
+    static constexpr uint32_t kWordsPerChunk = (uint32_t)kChunk * kBits / 32u;
+};
+
+constexpr uint32_t kQuantInlineChunks = 1024;  // pass 2 reduces the chunk maxima itself
+
+__device__ __forceinline__ uint32_t block_max_u32(uint32_t x, uint32_t* sh /* >= 4 */) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const uint32_t y = (uint32_t)__shfl_xor((int)x, o, 64);
+        x = y > x ? y : x;
+    }
+    if (lane_id() == 0) sh[threadIdx.x >> 6] = x;
+    __syncthreads();
+    uint32_t m = sh[0];
+#pragma unroll
+    for (int w = 1; w < kBlock / 64; ++w) m = sh[w] > m ? sh[w] : m;
+    __syncthreads();
+    return m;
+}
+
+// Largest |v| bits of tensor t from its chunk maxima.
+__device__ __forceinline__ uint32_t tensor_max(const uint32_t* __restrict__ q, const TDesc& td, uint32_t* sh) {
+    uint32_t m = 0;
+    for (uint32_t c = threadIdx.x; c < td.nchunks; c += kBlock) {
+        const uint32_t x = q[td.chunk0 + c];
+        m = x > m ? x : m;
+    }
+    return block_max_u32(m, sh);
+}
+
+// Uniforms of the four elements 8g + 4h .. 8g + 4h + 3 of a tensor.
+__device__ __forceinline__ void quant_uniforms(uint64_t seed, uint32_t tid, uint32_t g, uint32_t h,
+                                               float (&u)[4]) {
+    const U64x4 ctr = {{(uint64_t)tid, (uint64_t)g, 0, 0}};
+    const U64x4 r = philox4x64_10(ctr, seed, kStreamQuant);
+    const uint64_t w0 = h ? r.v[2] : r.v[0];
+    const uint64_t w1 = h ? r.v[3] : r.v[1];
+    u[0] = (float)((uint32_t)w0 >> 8) * 0x1p-24f;
+    u[1] = (float)((uint32_t)(w0 >> 32) >> 8) * 0x1p-24f;
+    u[2] = (float)((uint32_t)w1 >> 8) * 0x1p-24f;
+    u[3] = (float)((uint32_t)(w1 >> 32) >> 8) * 0x1p-24f;
+}
+
+// Decoded value of a code for a tensor whose decoding unit is `unit`.
+template <int kBits>
+__device__ __forceinline__ float quant_decode(uint32_t code, float unit) {
+    const uint32_t level = code & Quant<kBits>::kLevelMask;
+    float d;
+    if constexpr (kBits == 2) {
+        d = unit;  // the one level
+    } else {
+        d = (float)level * unit;
+    }
+    d = u2f(f2u(d) ^ ((code >> (kBits - 1)) << 31));
+    return level ? d : 0.f;
+}
+
+// Codes of four consecutive elements (kBits each, element q at bit kBits q)
+// into the payload: word `wi` of the tensor gathers 32 / kBits codes, so
+// 8-bit codes fill a word per lane, 4-bit codes a word per lane pair and
+// 2-bit codes a word per four lanes.  Words at or past the tensor's word
+// count are not written.
+template <int kBits>
+__device__ __forceinline__ void store_codes(uint32_t packed, uint32_t e0, uint32_t* __restrict__ words,
+                                            uint32_t nwords) {
+    const int lane = lane_id();
+    if constexpr (kBits == 8) {
+        const uint32_t wi = e0 / 4u;
+        if (wi < nwords) gp(words)[wi] = packed;
+    } else if constexpr (kBits == 4) {
+        uint32_t x = packed << (16 * (lane & 1));
+        x |= (uint32_t)__shfl_xor((int)x, 1, 64);
+        const uint32_t wi = e0 / 8u;
+        if ((lane & 1) == 0 && wi < nwords) gp(words)[wi] = x;
+    } else {
+        uint32_t x = packed << (8 * (lane & 3));
+        x |= (uint32_t)__shfl_xor((int)x, 1, 64);
+        x |= (uint32_t)__shfl_xor((int)x, 2, 64);
+        const uint32_t wi = e0 / 16u;
+        if ((lane & 3) == 0 && wi < nwords) gp(words)[wi] = x;
+    }
+}
+
+}  // namespace
+
+// Pass 1: v = g + e (parked in e for pass 2) and the chunk's largest |v|
+// bits.  Streams g and e_old past the cache for large calls; v is stored
+// normally so that pass 2 finds it there.
+template <bool kNT>
+__global__ __launch_bounds__(kBlock) void quant_pass1(const TDesc* __restrict__ d, int T, Ws ws) {
+    __shared__ uint32_t sh[4];
+    const uint32_t c = blockIdx.x;
+    const int t = tensor_of_chunk(d, T, c);
+    const TDesc td = d[t];
+    const uint32_t j = c - td.chunk0;
+    float v[kEpt];
+    uint32_t valid;
+    load_v<kNT>(td, j, td.resid != nullptr, v, valid);
+    if (td.resid) store_chunk(td.resid, td.n, j, v);
+    uint32_t m = 0;
+#pragma unroll
+    for (int i = 0; i < kEpt; ++i) {
+        const uint32_t k = ((valid >> i) & 1u) ? key_of(v[i]) : 0u;
+        m = k > m ? k : m;
+    }
+    m = block_max_u32(m, sh);
+    if (threadIdx.x == 0) ws.q_max[c] = m;
+}
+
+// Scales of tensors too large for pass 2 to reduce inline (and of empty
+// tensors).
+__global__ __launch_bounds__(kBlock) void quant_finalize(const TDesc* __restrict__ d, float* __restrict__ scale_out,
+                                                         Ws ws) {
+    __shared__ uint32_t sh[4];
+    const int t = blockIdx.x;
+    const TDesc td = d[t];
+    if (td.nchunks > 0 && td.nchunks <= kQuantInlineChunks) return;
+    const float m = td.nchunks ? u2f(tensor_max(ws.q_max, td, sh)) : 0.f;
+    if (threadIdx.x == 0) {
+        scale_out[t] = m;
+        ws.s_val[t] = m;
+    }
+}
+
+// Pass 2: quantize, pack, and write the residual.
+template <int kBits, bool kNT>
+__global__ __launch_bounds__(kBlock) void quant_pass2(const TDesc* __restrict__ d, int T, uint64_t seed,
+                                                      uint32_t* __restrict__ words, float* __restrict__ scale_out,
+                                                      Ws ws) {
+    using Q = Quant<kBits>;
+    __shared__ uint32_t sh[4];
+    const uint32_t c = blockIdx.x;
+    const int t = tensor_of_chunk(d, T, c);
+    const TDesc td = d[t];
+    const uint32_t j = c - td.chunk0;
+    float m;
+    if (td.nchunks <= kQuantInlineChunks) {
+        m = u2f(tensor_max(ws.q_max, td, sh));
+        if (j == 0 && threadIdx.x == 0) scale_out[t] = m;
+    } else {
+        m = ws.s_val[t];
+    }
+    const bool any = m > 0.f;
+    const float inv = any ? (float)((double)Q::kLevels / (double)m) : 0.f;
+    const float unit = (float)((double)m / (double)Q::kLevels);
+    float v[kEpt];
+    uint32_t valid;
+    load_stored_v(td, j, v, valid);  // e holds v after pass 1 (or v = g without error feedback)
+    uint32_t* tw = words + td.off;
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r) {
+        const uint32_t e0 = j * (uint32_t)kChunk + 1024u * r + 4u * threadIdx.x;  // element of the tensor
+        float u[4];
+        quant_uniforms(seed, td.tid, e0 >> 3, (e0 >> 2) & 1u, u);
+        uint32_t packed = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int i = 4 * r + q;
+            uint32_t level = 0;
+            if (any && ((valid >> i) & 1u)) {
+                const float x = fabsf(v[i]) * inv;
+                if (x >= (float)Q::kLevels) {
+                    level = (uint32_t)Q::kLevels;
+                } else {
+                    const float fl = floorf(x);
+                    level = (uint32_t)fl + (u[q] < x - fl ? 1u : 0u);
+                }
+            }
+            const uint32_t code = level ? (level | ((f2u(v[i]) >> 31) << (kBits - 1))) : 0u;
+            packed |= code << (kBits * q);
+            v[i] = v[i] - quant_decode<kBits>(code, unit);
+        }
+        store_codes<kBits>(packed, e0, tw, td.k);
+    }
+    if (td.resid) store_chunk<kNT>(td.resid, td.n, j, v);
+}
+
+// Residual update from a payload made elsewhere: e <- (g + e) - decode.
+// Each thread's four consecutive elements of a round share one word.
+template <int kBits>
+__global__ __launch_bounds__(kBlock) void quant_residual_update(const TDesc* __restrict__ d, int T,
+                                                                const uint32_t* __restrict__ words,
+                                                                const float* __restrict__ scale) {
+    const uint32_t c = blockIdx.x;
+    const int t = tensor_of_chunk(d, T, c);
+    const TDesc td = d[t];
+    const uint32_t j = c - td.chunk0;
+    float v[kEpt];
+    uint32_t valid;
+    load_v(td, j, true, v, valid);
+    const float unit = (float)((double)scale[t] / (double)Quant<kBits>::kLevels);
+    const uint32_t* tw = words + td.off;
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r) {
+        const uint32_t e0 = j * (uint32_t)kChunk + 1024u * r + 4u * threadIdx.x;
+        const uint32_t wi = e0 / (32u / kBits);
+        const uint32_t word = wi < td.k ? gp(tw)[wi] : 0u;
+        const uint32_t sh0 = (e0 % (32u / kBits)) * (uint32_t)kBits;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const uint32_t code = (word >> (sh0 + (uint32_t)(kBits * q))) & Quant<kBits>::kMask;
+            v[4 * r + q] = v[4 * r + q] - quant_decode<kBits>(code, unit);
+        }
+    }
+    store_chunk(td.resid, td.n, j, v);
+}
+
+// Aggregate: one workgroup per 4096-element unit of a tensor, lane l of
+// the workgroup owning elements 16 l .. 16 l + 15 of the unit (16 kBits
+// bits: kBits / 2 consecutive words of every worker's payload).
+template <int kBits>
+__global__ __launch_bounds__(kBlock) void aggregate_quant(const ADesc* __restrict__ a, int T, uint32_t U,
+                                                          const uint64_t* __restrict__ wp, int W, float alpha) {
+    constexpr int kWords = kBits / 2;
+    constexpr int kGroup = 4;  // workers whose words are in flight together
+    __shared__ float unit_sh[1024];
+    const uint32_t u = blockIdx.x;
+    const int t = unit_owner(wp, W, u);
+    const ADesc ad = a[t];
+    for (int w = threadIdx.x; w < W; w += kBlock)
+        unit_sh[w] = (float)((double)gp(w_b(wp, W, w))[t] / (double)Quant<kBits>::kLevels);
+    __syncthreads();
+    const uint32_t e_first = (u - ad.unit0) * kSignAggUnit + 16u * threadIdx.x;  // element of the tensor
+    const uint32_t w_first = e_first / (32u / kBits);                          // word of the tensor
+    float acc[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) acc[q] = 0.f;
+    for (int w0 = 0; w0 < W; w0 += kGroup) {
+        uint32_t wd[kGroup][kWords];
+#pragma unroll
+        for (int g = 0; g < kGroup; ++g) {
+            const int w = w0 + g < W ? w0 + g : W - 1;
+            const uint32_t* base = w_a(wp, w) + ad.off;
+#pragma unroll
+            for (int k = 0; k < kWords; ++k) wd[g][k] = w_first + k < ad.k ? gp(base)[w_first + k] : 0u;
+        }
+#pragma unroll
+        for (int g = 0; g < kGroup; ++g) {
+            if (w0 + g < W) {
+                const float un = unit_sh[w0 + g];
+#pragma unroll
+                for (int q = 0; q < 16; ++q) {
+                    const uint32_t code = (wd[g][(q * kBits) / 32] >> ((q * kBits) % 32)) & Quant<kBits>::kMask;
+                    acc[q] += quant_decode<kBits>(code, un);
+                }
+            }
+        }
+    }
+    float* out = ad.out + e_first;
+    if (e_first + 16u <= ad.n) {
+#pragma unroll
+        for (int q = 0; q < 16; q += 4)
+            stg4f(out + q, f32x4{alpha * acc[q], alpha * acc[q + 1], alpha * acc[q + 2], alpha * acc[q + 3]});
+    } else {
+#pragma unroll
+        for (int q = 0; q < 16; ++q)
+            if (e_first + q < ad.n) gp(out)[q] = alpha * acc[q];
+    }
+}
+
+// ------------------------------------------------------------- launchers
+namespace {
+template <int kBits>
+void quant_compress_bits(const TDesc* d, int T, uint32_t C, bool nt, uint64_t seed, uint32_t* words, float* scale,
+                         const Ws& ws, hipStream_t s) {
+    if (nt) hipLaunchKernelGGL((quant_pass2<kBits, true>), dim3(C), dim3(kBlock), 0, s, d, T, seed, words, scale, ws);
+    else hipLaunchKernelGGL((quant_pass2<kBits, false>), dim3(C), dim3(kBlock), 0, s, d, T, seed, words, scale, ws);
+}
+}  // namespace
+
+hipError_t launch_quant_compress(int bits, uint64_t seed, const TDesc* d, int T, uint32_t C, uint32_t max_chunks,
+                                 bool any_empty, uint32_t* words, float* scale, const Ws& ws, hipStream_t s) {
+    if (T <= 0) return hipSuccess;
+    const bool nt = C > kNtChunks;
+    if (C > 0) {
+        if (nt) (void)launch_timed(kTimedQuantPass1, quant_pass1<true>, dim3(C), dim3(kBlock), 0, s, d, T, ws);
+        else (void)launch_timed(kTimedQuantPass1, quant_pass1<false>, dim3(C), dim3(kBlock), 0, s, d, T, ws);
+    }
+    if (max_chunks > kQuantInlineChunks || C == 0 || any_empty)
+        hipLaunchKernelGGL(quant_finalize, dim3(T), dim3(kBlock), 0, s, d, scale, ws);
+    if (C > 0) {
+        if (bits == 2) quant_compress_bits<2>(d, T, C, nt, seed, words, scale, ws, s);
+        else if (bits == 4) quant_compress_bits<4>(d, T, C, nt, seed, words, scale, ws, s);
+        else quant_compress_bits<8>(d, T, C, nt, seed, words, scale, ws, s);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_quant_residual_update(int bits, const TDesc* d, int T, uint32_t C, const uint32_t* words,
+                                        const float* scale, hipStream_t s) {
+    if (C == 0) return hipSuccess;
+    if (bits == 2) hipLaunchKernelGGL(quant_residual_update<2>, dim3(C), dim3(kBlock), 0, s, d, T, words, scale);
+    else if (bits == 4) hipLaunchKernelGGL(quant_residual_update<4>, dim3(C), dim3(kBlock), 0, s, d, T, words, scale);
+    else hipLaunchKernelGGL(quant_residual_update<8>, dim3(C), dim3(kBlock), 0, s, d, T, words, scale);
+    return hipGetLastError();
+}
+
+hipError_t launch_aggregate_quant(int bits, const ADesc* a, int T, uint32_t U, const uint64_t* wp, int W,
+                                  float alpha, hipStream_t s) {
+    if (U == 0) return hipSuccess;
+    if (W > 1024) return hipErrorInvalidValue;
+    if (bits == 2)
+        return launch_timed(kTimedAggQuant, aggregate_quant<2>, dim3(U), dim3(kBlock), 0, s, a, T, U, wp, W, alpha);
+    if (bits == 4)
+        return launch_timed(kTimedAggQuant, aggregate_quant<4>, dim3(U), dim3(kBlock), 0, s, a, T, U, wp, W, alpha);
+    return launch_timed(kTimedAggQuant, aggregate_quant<8>, dim3(U), dim3(kBlock), 0, s, a, T, U, wp, W, alpha);
+}
+
+}  // namespace bc

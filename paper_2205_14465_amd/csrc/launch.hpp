@@ -21,6 +21,8 @@ struct Ws {
     double* s_partial;      // [C] per-chunk sums of |v|
     uint32_t* s_info;       // [T] aggregate: form (bits 0-7), smallest scale exponent (8-15)
     int32_t* s_tab;         // [T * 2048] aggregate: int32 lookup tables of each tensor
+    // BC_TERNGRAD, BC_QSGD4, BC_QSGD8 (and s_val)
+    uint32_t* q_max;        // [C] largest |v| bits of each chunk
     // BC_TOPK, BC_TOPK_SAMPLED
     uint32_t* t_hist;       // [T * 2048] histograms         
     uint32_t* t_thr;        // [T] candidate threshold (key)
@@ -47,7 +49,7 @@ struct Ws {
 // Byte offsets of every region for a call shape; `total` is the workspace
 // size.  Regions a kind does not use have size 0.
 struct WsPlan {
-    size_t flags, s_val, s_partial, s_info, s_tab;
+    size_t flags, s_val, s_partial, s_info, s_tab, q_max;
     size_t t_hist, t_thr, t_prefix, t_krem, t_fb, t_any, t_cand, t_ccount, t_gt, t_eq, t_off, t_eqb;
     size_t r_keys, r_tmp, r_ccount, r_coff, r_hist;
     size_t total;
@@ -65,7 +67,7 @@ hipError_t device_info(int dev, DevInfo* out);
 // ------------------------------------------------------- kernel timing
 // Kernels a caller may ask to have timed (bytecomp_time_next_launch).
 enum TimedKernel { kTimedNone = 0, kTimedAggSign, kTimedAggSparse, kTimedRandkStream, kTimedTopkCompact,
-                   kTimedSignPass1 };
+                   kTimedSignPass1, kTimedQuantPass1, kTimedAggQuant };
 // If a request for kernel `k` is pending, hand over its events and clear it.
 bool take_kernel_timer(int k, hipEvent_t* start, hipEvent_t* stop);
 
@@ -109,6 +111,14 @@ hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t units, uint32
                                    int W, float alpha, int cus, const uint64_t* rp, hipStream_t s);
 hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t units, const uint64_t* wp, int W,
                                  float alpha, uint32_t* info, int32_t* tabs, hipStream_t s);
+// Stochastic b-bit quantizers (bits 2, 4 or 8).
+hipError_t launch_quant_compress(int bits, uint64_t seed, const TDesc* d, int T, uint32_t C, uint32_t max_chunks,
+                                 bool any_empty, uint32_t* words, float* scale, const Ws& ws, hipStream_t s);
+hipError_t launch_quant_residual_update(int bits, const TDesc* d, int T, uint32_t C, const uint32_t* words,
+                                        const float* scale, hipStream_t s);
+// units of kSignAggUnit elements; W <= 1024
+hipError_t launch_aggregate_quant(int bits, const ADesc* a, int T, uint32_t units, const uint64_t* wp, int W,
+                                  float alpha, hipStream_t s);
 
 // Random-k bucketing: generating workgroups of kGenBlock threads handle
 // kGenEntries payload entries each; a bucket is 2^S consecutive chunks with

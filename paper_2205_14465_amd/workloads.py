@@ -101,7 +101,7 @@ class Workload:
     """One tensor set plus the aggregation fan-in it is measured with."""
     wid: int
     name: str
-    kind: str              # "topk" | "topk_sampled" | "randk" | "sign"
+    kind: str              # "topk" | "topk_sampled" | "randk" | "sign" | "terngrad" | "qsgd4" | "qsgd8"
     ratio: float
     W: int
     sizes: list = field(default_factory=list)
@@ -121,12 +121,15 @@ class Workload:
     def slug(self):
         """Short file-name form of the workload."""
         return {1: "single2p20_topk_w8", 2: "resnet50_sign_w64", 3: "bertbase_topksampled_w64",
-                4: "gpt2xl_randk_w16", 5: "small4096_fp16sign_w32"}[self.wid]
+                4: "gpt2xl_randk_w16", 5: "small4096_fp16sign_w32", 6: "resnet50_terngrad_w64",
+                7: "bertbase_qsgd8_w16", 8: "bertbase_qsgd4_w32"}[self.wid]
 
 
 def workload(wid: int, shrink: int = 1) -> Workload:
-    """The five measured workloads; `shrink` > 1 divides every tensor size
-    (at least 1 element) for fast parity runs of the same structure."""
+    """The measured workloads (1-5: the hot path's five operator configs;
+    6-8: the stochastic quantizers on the same model shapes); `shrink` > 1
+    divides every tensor size (at least 1 element) for fast parity runs of
+    the same structure."""
     def s(ns):
         return [max(1, n // shrink) for n in ns]
     if wid == 1:
@@ -144,7 +147,20 @@ def workload(wid: int, shrink: int = 1) -> Workload:
     if wid == 5:
         return Workload(5, "4096 small fp16 tensors (768..65536, ~60M), sign+fp32 EF, W=32", "sign",
                         0.01, 32, s(many_small_sizes()), "float16", "fixed:1e-3", "fixed:1e-4")
+    if wid == 6:
+        return Workload(6, "ResNet-50 gradients (161 fp32 tensors, 25.6M), TernGrad 2-bit+EF, W=64",
+                        "terngrad", 0.01, 64, s([numel(x) for x in resnet50_shapes()]))
+    if wid == 7:
+        return Workload(7, "BERT-base gradients (199 fp32 tensors, 109.5M), QSGD 8-bit+EF, W=16",
+                        "qsgd8", 0.01, 16, s([numel(x) for x in bert_base_shapes()]))
+    if wid == 8:
+        return Workload(8, "BERT-base gradients (199 fp32 tensors, 109.5M), QSGD 4-bit+EF, W=32",
+                        "qsgd4", 0.01, 32, s([numel(x) for x in bert_base_shapes()]))
     raise ValueError(wid)
+
+
+QUANT_BITS = {"terngrad": 2, "qsgd4": 4, "qsgd8": 8}
+WORD_KINDS = ("sign", "terngrad", "qsgd4", "qsgd8")  # payload: packed words + one scale per tensor
 
 
 def sigma_of(wl: Workload, tid: int) -> float:
@@ -210,6 +226,21 @@ def sign_payload(wl: Workload, w: int, word_counts, offs):
     return bits, scale
 
 
+def quant_payload(wl: Workload, w: int, word_counts, offs):
+    """Worker w's quantizer payload: uniformly random b-bit codes (codes past
+    the end of each tensor cleared) and scales 4 sigma_t (1 + 0.05 N(0,1)),
+    about the largest magnitude of the tensor's normal draws."""
+    b = QUANT_BITS[wl.kind]
+    total = int(offs[-1])
+    bits = np.empty(total, np.uint32)
+    scale = np.empty(wl.T, np.float32)
+    for t, n in enumerate(wl.sizes):
+        rng = rng_for(wl.wid, t, ROLE_WORKER + w)
+        bits[offs[t]:offs[t] + int(word_counts[t])] = random_code_words(rng, [n], [word_counts[t]], b)[0]
+        scale[t] = np.float32(4.0 * sigma_of(wl, t) * (1.0 + 0.05 * rng.standard_normal()))
+    return bits, scale
+
+
 # ------------------------------------------------- generic test inputs
 
 def random_sparse_lists(rng: np.random.Generator, ns, counts, sigma=1.0):
@@ -230,6 +261,19 @@ def random_sign_words(rng: np.random.Generator, ns, word_counts):
         tail = int(n) - 32 * (int(nw) - 1) if nw else 0
         if nw and tail < 32:
             w[-1] &= np.uint32((1 << tail) - 1)
+        out.append(w)
+    return out
+
+
+def random_code_words(rng: np.random.Generator, ns, word_counts, bits):
+    """One worker's packed b-bit code words for arbitrary tensor sizes (codes
+    past each tensor's end cleared), one list entry per tensor."""
+    out = []
+    for n, nw in zip(ns, word_counts):
+        w = rng.integers(0, 1 << 32, size=int(nw), dtype=np.uint64).astype(np.uint32)
+        used = int(n) * bits % 32
+        if nw and used:
+            w[-1] &= np.uint32((1 << used) - 1)
         out.append(w)
     return out
 
@@ -317,8 +361,8 @@ def device_inputs(wl, off, device):
     counts = [int(off[t + 1] - off[t]) for t in range(wl.T)]
     payloads = []
     for w in range(wl.W):
-        if kind == "sign":
-            b, s = sign_payload(wl, w, counts, off)
+        if kind in WORD_KINDS:
+            b, s = (sign_payload if kind == "sign" else quant_payload)(wl, w, counts, off)
             payloads.append({"bits": torch.from_numpy(b.view(np.int32)).to(device),
                              "scale": torch.from_numpy(s).to(device)})
         elif on_device:

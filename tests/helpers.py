@@ -22,6 +22,9 @@ def to_np_u32(t):
     return t.cpu().numpy().view(np.uint32)
 
 
+WORD_KINDS = ("sign", "terngrad", "qsgd4", "qsgd8")  # packed words + scales
+
+
 def gpu_compress(kind, ratio, seed, grads, resids, tensor_ids=None):
     """Returns (payload dict of numpy arrays, list of new residuals or None)."""
     import torch
@@ -36,7 +39,7 @@ def gpu_compress(kind, ratio, seed, grads, resids, tensor_ids=None):
     assert B.bytecomp_device_status(ws) == 0
     res = {"off": np.array(out["off"], dtype=np.int64)}
     total = out["off"][-1]
-    if kind == "sign":
+    if kind in WORD_KINDS:
         res["bits"] = to_np_u32(out["bits"])[:total]
         res["scale"] = out["scale"].cpu().numpy()[:len(ns)]
     else:
@@ -52,7 +55,7 @@ def gpu_aggregate(kind, ratio, ns, payloads, alpha):
     from paper_2205_14465_amd import binding as B
     dev = []
     for p in payloads:
-        if kind == "sign":
+        if kind in WORD_KINDS:
             dev.append({"bits": torch_dev(p["bits"].view(np.int32)), "scale": torch_dev(p["scale"])})
         else:
             dev.append({"idx": torch_dev(p["idx"].view(np.int32)), "val": torch_dev(p["val"])})

@@ -48,6 +48,22 @@ def test_layout_matches_k_rule_and_word_count():
             off = B.bytecomp_layout(kind, ratio, ns)
             assert np.array_equal(np.array(off), O.sparse_offsets(ns, ratio))
     assert np.array_equal(np.array(B.bytecomp_layout("sign", 0.0, ns)), O.word_offsets(ns))
+    for kind, bits in O.QUANT_BITS.items():
+        assert np.array_equal(np.array(B.bytecomp_layout(kind, 0.0, ns)), O.quant_word_offsets(ns, bits))
+
+
+def test_quantizers_refuse_the_divisible_scheme():
+    L = B.lib()
+    n = (ctypes.c_uint64 * 1)(64)
+    bounds = (ctypes.c_uint64 * 2)(0, 64)
+    pay = B.bc_payload(bits=0x3000, scale=0x4000)
+    po = ctypes.c_void_p(0x5000)
+    for kind in (4, 5, 6):
+        assert L.bytecomp_pack_part(kind, 0.0, n, 1, pay, 1, bounds, 0, pay, po, None) == -2
+        ins = (B.bc_payload * 1)(pay)
+        outs = (ctypes.c_void_p * 1)(0x6000)
+        offs = (ctypes.c_void_p * 1)(0x7000)
+        assert L.bytecomp_aggregate_part(kind, 0.0, ins, offs, 1, n, 1, outs, 1.0, po, 1 << 20, None) == -2
 
 
 def _status(fn):
@@ -128,4 +144,6 @@ def test_time_next_launch_arguments():
     assert L.bytecomp_time_next_launch(b"aggregate_sign", fake, None) == -1
     assert L.bytecomp_time_next_launch(None, fake, fake) == -1
     assert L.bytecomp_time_next_launch(b"aggregate_sign", fake, fake) == 0
+    assert L.bytecomp_time_next_launch(b"aggregate_quant", fake, fake) == 0
+    assert L.bytecomp_time_next_launch(b"quant_pass1", fake, fake) == 0
     assert L.bytecomp_time_next_launch(None, None, None) == 0  # clears the request

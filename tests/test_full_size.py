@@ -131,3 +131,22 @@ def test_full_size_sign_workload(wid):
             w0, w1 = off[t] + a // 32, off[t] + (b + 31) // 32
             want = O.aggregate_sign(b - a, [x[w0:w1] for x in p_bits], p_scale[:, t], alpha)
             assert np.array_equal(bits(got[a:b]), bits(want)), (t, a, b)
+
+
+@pytest.mark.parametrize("wid", [6, 7, 8])
+def test_full_size_quant_workload(wid):
+    wl, off, grads, resids, payloads, outs, own, sample, g_host, e_host, alpha = _run(wid)
+    b = O.QUANT_BITS[wl.kind]
+    words = own["bits"].cpu().numpy().view(np.uint32)
+    scale = own["scale"].cpu().numpy()
+    for t in sample:
+        ww, ss, we = O.compress_quant(g_host[t], e_host[t], b, WL.SEED, t)
+        assert np.array_equal(words[off[t]:off[t + 1]], ww), t
+        assert bits(scale[t]) == bits(np.float32(ss)), t
+        assert np.array_equal(bits(resids[t].cpu().numpy()), bits(we)), t
+    p_bits = [p["bits"].cpu().numpy().view(np.uint32) for p in payloads]
+    p_scale = np.stack([p["scale"].cpu().numpy() for p in payloads])
+    for t in sample:
+        n = wl.sizes[t]
+        want = O.aggregate_quant(n, b, [x[off[t]:off[t + 1]] for x in p_bits], p_scale[:, t], alpha)
+        assert np.array_equal(bits(outs[t].cpu().numpy()), bits(want)), t

@@ -240,43 +240,86 @@ __global__ __launch_bounds__(kBlock) void quant_residual_update(const TDesc* __r
 // Aggregate: one workgroup per 4096-element unit of a tensor, lane l of
 // the workgroup owning elements 16 l .. 16 l + 15 of the unit (16 kBits
 // bits: kBits / 2 consecutive words of every worker's payload).
+//
+// Decoding in the inner loop is branch-free: the level bits are widened
+// (2-bit: a sign-extended one-bit field masks the unit; 4- and 8-bit:
+// level * unit) and the code's sign bit is spliced in at bit 31 with a
+// bit-field insert.  A level-0 code with its sign bit set (never written
+// by the compressor) then decodes to -0.0 rather than +0.0; the running
+// sum never holds -0.0 (it starts at +0.0, and x + (-x) rounds to +0.0),
+// and adding either zero to a value that is not -0.0 gives the same
+// result, so the sums are those of the +0.0 decoding.
 template <int kBits>
 __global__ __launch_bounds__(kBlock) void aggregate_quant(const ADesc* __restrict__ a, int T, uint32_t U,
                                                           const uint64_t* __restrict__ wp, int W, float alpha) {
     constexpr int kWords = kBits / 2;
-    constexpr int kGroup = 4;  // workers whose words are in flight together
+    constexpr int kGroup = 8;  // workers whose words are in flight together
+    using Q = Quant<kBits>;
     __shared__ float unit_sh[1024];
     const uint32_t u = blockIdx.x;
     const int t = unit_owner(wp, W, u);
     const ADesc ad = a[t];
     for (int w = threadIdx.x; w < W; w += kBlock)
-        unit_sh[w] = (float)((double)gp(w_b(wp, W, w))[t] / (double)Quant<kBits>::kLevels);
+        unit_sh[w] = (float)((double)gp(w_b(wp, W, w))[t] / (double)Q::kLevels);
     __syncthreads();
     const uint32_t e_first = (u - ad.unit0) * kSignAggUnit + 16u * threadIdx.x;  // element of the tensor
     const uint32_t w_first = e_first / (32u / kBits);                          // word of the tensor
+    // a unit inside the tensor reads each worker's kWords words with one
+    // vector load (4-byte aligned: word offsets are arbitrary); the last
+    // unit of a tensor reads word by word, words past the tensor's end
+    // reading its last word and decoding as zero
+    const bool whole = (uint64_t)(u - ad.unit0 + 1u) * kSignAggUnit <= ad.n;
+    uint32_t widx[kWords];
+    uint32_t wkeep[kWords];
+#pragma unroll
+    for (int k = 0; k < kWords; ++k) {
+        const bool in = w_first + k < ad.k;
+        widx[k] = in ? w_first + k : ad.k - 1u;
+        wkeep[k] = in ? 0xFFFFFFFFu : 0u;
+    }
+    auto load_words = [&](const uint32_t* base, uint32_t (&wd)[kWords]) {
+        if (whole) {
+            typedef uint32_t vec_t __attribute__((ext_vector_type(kWords), aligned(4)));
+            const vec_t x = *(const BC_GLOBAL vec_t*)(gp(base) + w_first);
+#pragma unroll
+            for (int k = 0; k < kWords; ++k) wd[k] = x[k];
+        } else {
+#pragma unroll
+            for (int k = 0; k < kWords; ++k) wd[k] = gp(base)[widx[k]] & wkeep[k];
+        }
+    };
     float acc[16];
 #pragma unroll
     for (int q = 0; q < 16; ++q) acc[q] = 0.f;
-    for (int w0 = 0; w0 < W; w0 += kGroup) {
+    auto add_worker = [&](const uint32_t (&wd)[kWords], float un) {
+        const uint32_t ub = f2u(un);
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            constexpr int kPer = 32 / kBits;
+            const uint32_t word = wd[q / kPer];
+            const int pos = (q % kPer) * kBits;  // first bit of the code
+            float mag;
+            if constexpr (kBits == 2) {
+                mag = u2f(ub & (uint32_t)__builtin_amdgcn_sbfe((int)word, pos, 1));
+            } else {
+                mag = (float)__builtin_amdgcn_ubfe(word, pos, kBits - 1) * un;
+            }
+            const uint32_t sgn = word << (31 - (pos + kBits - 1));  // the code's sign bit at bit 31
+            acc[q] += u2f((sgn & 0x80000000u) ^ f2u(mag));
+        }
+    };
+    int w0 = 0;
+    for (; w0 + kGroup <= W; w0 += kGroup) {
         uint32_t wd[kGroup][kWords];
 #pragma unroll
-        for (int g = 0; g < kGroup; ++g) {
-            const int w = w0 + g < W ? w0 + g : W - 1;
-            const uint32_t* base = w_a(wp, w) + ad.off;
+        for (int g = 0; g < kGroup; ++g) load_words(w_a(wp, w0 + g) + ad.off, wd[g]);
 #pragma unroll
-            for (int k = 0; k < kWords; ++k) wd[g][k] = w_first + k < ad.k ? gp(base)[w_first + k] : 0u;
-        }
-#pragma unroll
-        for (int g = 0; g < kGroup; ++g) {
-            if (w0 + g < W) {
-                const float un = unit_sh[w0 + g];
-#pragma unroll
-                for (int q = 0; q < 16; ++q) {
-                    const uint32_t code = (wd[g][(q * kBits) / 32] >> ((q * kBits) % 32)) & Quant<kBits>::kMask;
-                    acc[q] += quant_decode<kBits>(code, un);
-                }
-            }
-        }
+        for (int g = 0; g < kGroup; ++g) add_worker(wd[g], unit_sh[w0 + g]);
+    }
+    for (; w0 < W; ++w0) {
+        uint32_t wd[kWords];
+        load_words(w_a(wp, w0) + ad.off, wd);
+        add_worker(wd, unit_sh[w0]);
     }
     float* out = ad.out + e_first;
     if (e_first + 16u <= ad.n) {

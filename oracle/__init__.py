@@ -88,6 +88,8 @@ def lib():
         L.bco_compress_quant.argtypes = [_vp, _int, _vp, _u64, _int, _u64, _u32, _vp, _vp, _vp]
         L.bco_residual_update_quant.restype = _int
         L.bco_residual_update_quant.argtypes = [_vp, _int, _vp, _u64, _int, _vp, _flt]
+        L.bco_dgc_momentum.restype = _int
+        L.bco_dgc_momentum.argtypes = [_vp, _int, _vp, _u64, _flt]
         L.bco_aggregate_quant.restype = _int
         L.bco_aggregate_quant.argtypes = [_int, _u64, _int, _vp, _vp, _flt, _vp]
         _lib = L
@@ -355,6 +357,52 @@ def quant_word_offsets(ns, bits):
     for t, n in enumerate(ns):
         off[t + 1] = off[t] + quant_words(n, bits)
     return off
+
+
+# ----------------------------------------------- DGC momentum correction
+# DGC (the paper's sparsification operator, Sec. 5.1) keeps a velocity u
+# per tensor: u_new = fl32(fl32(m u) + g); the sparse kind compresses
+# u_new with the error-feedback residual e; momentum-factor masking then
+# zeroes u_new at the chosen entries (e_new is already zero there).
+
+def dgc_momentum(g, u, m):
+    g, dt = _grad(g)
+    u = np.array(u, dtype=np.float32, copy=True)
+    assert u.size == g.size
+    rc = lib().bco_dgc_momentum(_p(g), dt, _p(u), g.size, float(m))
+    assert rc == 0, rc
+    return u
+
+
+def compress_dgc(kind, g, e, u, m, ratio, seed, tensor_id):
+    """One DGC step of one tensor: (idx, val, e_new, u_new)."""
+    u_new = dgc_momentum(g, u, m)
+    if kind == "topk":
+        idx, val, e_new = compress_topk(u_new, e, ratio)
+    elif kind == "topk_sampled":
+        idx, val, e_new = compress_topk_sampled(u_new, e, ratio, seed, tensor_id)
+    elif kind == "randk":
+        idx, val, e_new = compress_randk(u_new, e, ratio, seed, tensor_id)
+    else:
+        raise ValueError(kind)
+    u_new[idx.astype(np.int64)] = np.float32(0.0)
+    return idx, val, e_new, u_new
+
+
+def compress_dgc_set(kind, ratio, seed, m, grads, resids, vels):
+    """DGC step of a tensor list: (payload dict, new residuals, new velocities)."""
+    ns = [g.size for g in grads]
+    off = sparse_offsets(ns, ratio)
+    idx = np.empty(int(off[-1]), np.uint32)
+    val = np.empty(int(off[-1]), np.float32)
+    new_e, new_u = [], []
+    for t in range(len(grads)):
+        i, v, e_out, u_out = compress_dgc(kind, grads[t], resids[t], vels[t], m, ratio, seed, t)
+        idx[off[t]:off[t + 1]] = i
+        val[off[t]:off[t + 1]] = v
+        new_e.append(e_out)
+        new_u.append(u_out)
+    return {"idx": idx, "val": val, "off": off}, new_e, new_u
 
 
 # ------------------------------------------------------ tensor-list calls

@@ -772,3 +772,25 @@ int bco_aggregate_quant(int W, uint64_t n, int bits, const uint32_t* const* word
     }
     return 0;
 }
+
+/* ------------------------------------------------------------------ */
+/* DGC momentum correction and momentum-factor masking around a sparse  */
+/* compression (DGC is the paper's sparsification operator, Sec. 5.1;   */
+/* its momentum correction keeps a per-tensor velocity u next to the    */
+/* accumulated gradient, which is the error-feedback residual here):    */
+/*   u_new = fl32(fl32(m * u) + g);  the sparse kind then compresses    */
+/*   u_new with the residual e (v = fl32(u_new + e), selection, payload, */
+/*   e_new = v with the chosen entries +0.0);  masking sets u_new to    */
+/*   +0.0 at the chosen entries as well.                                */
+/* This function is the first step; the compression and the masking are */
+/* the existing functions applied in that order (see the Python side).  */
+/* ------------------------------------------------------------------ */
+
+int bco_dgc_momentum(const void* g, int dtype, float* u_inout, uint64_t n, float m)
+{
+    for (uint64_t i = 0; i < n; ++i) {
+        float mu = m * u_inout[i];
+        u_inout[i] = mu + grad_at(g, dtype, i);
+    }
+    return 0;
+}

@@ -42,6 +42,8 @@ def log(msg):
 def algorithmic_bytes(wl, off, kind):
     n = wl.n_total
     gbytes = 2 if wl.grad_dtype == "float16" else 4
+    if wl.momentum:  # DGC: the velocity is read and written as well
+        gbytes += 8
     if kind in WORD_KINDS:
         payload = 4 * int(off[-1]) + 4 * wl.T
     else:
@@ -62,7 +64,7 @@ def cpu_baseline(wl, off, budget_s=15.0):
     comp_bytes = agg_bytes = 0
     comp_s = agg_s = 0.0
     used = []
-    gbytes = 2 if wl.grad_dtype == "float16" else 4
+    gbytes = (2 if wl.grad_dtype == "float16" else 4) + (8 if wl.momentum else 0)
     order = list(range(wl.T))
     for t in order:
         if comp_s + agg_s > budget_s:
@@ -70,7 +72,9 @@ def cpu_baseline(wl, off, budget_s=15.0):
         g = WL.gradient(wl, t)
         e = WL.residual(wl, t)
         t0 = time.perf_counter()
-        if kind == "sign":
+        if wl.momentum:
+            O.compress_dgc(kind, g, e, np.zeros(g.size, np.float32), wl.momentum, wl.ratio, WL.SEED, t)
+        elif kind == "sign":
             w_, s_, _ = O.compress_sign(g, e)
         elif kind in O.QUANT_BITS:
             O.compress_quant(g, e, O.QUANT_BITS[kind], WL.SEED, t)
@@ -156,7 +160,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5, 6, 7, 8])
+    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5, 6, 7, 8, 9])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--scheme", choices=["indivisible", "divisible"], default="indivisible",
                     help="divisible: time node 0's step of the divisible scheme instead")
@@ -187,13 +191,17 @@ def main():
     alpha = 1.0 / wl.W
     stream = torch.cuda.current_stream()
 
-    if args.scheme == "divisible" and kind not in ("topk", "topk_sampled", "randk", "sign"):
+    if args.scheme == "divisible" and (kind not in ("topk", "topk_sampled", "randk", "sign") or wl.momentum):
         sys.exit(f"bench.py: the divisible scheme is not built for the {kind} kind")
     if args.scheme == "divisible":
         return divisible(args, wl, off, payloads, ws, dev, stream)
 
     # argument arrays are marshalled once; each call is one C-ABI call
-    compress_call = B.CompressCall(kind, wl.ratio, grads, resids, own, ws, stream=stream)
+    if wl.momentum:
+        vels = [torch.zeros(n, dtype=torch.float32, device=dev) for n in wl.sizes]
+        compress_call = B.DgcCall(kind, wl.ratio, wl.momentum, grads, resids, vels, own, ws, stream=stream)
+    else:
+        compress_call = B.CompressCall(kind, wl.ratio, grads, resids, own, ws, stream=stream)
     aggregate_call = B.AggregateCall(kind, wl.ratio, payloads, wl.sizes, outs, alpha, ws, stream=stream)
 
     # the caller varies the seed per iteration (random-k indices, the

@@ -164,6 +164,28 @@ int bytecomp_workspace_init(void* ws, size_t ws_bytes, void* stream);
 int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t, int T,
                       bc_payload out, void* ws, size_t ws_bytes, void* stream);
 
+/* One DGC step (DGC is the paper's sparsification operator, Sec. 5.1):
+ * momentum correction, sparse compression with error feedback, and
+ * momentum-factor masking.  For every tensor, with u its velocity:
+ *   u <- fl32(fl32(momentum * u) + g)    (fp16 g widened exactly)
+ *   the sparse kind compresses u with the tensor's residual e, exactly as
+ *   bytecomp_compress with grad = u (fp32) and residual = e would
+ *   (v = u + e, payload, e <- v with +0.0 at the chosen entries)
+ *   u <- +0.0 at the chosen entries.
+ *   kind      BC_TOPK, BC_TOPK_SAMPLED or BC_RANDK (BC_E_KIND otherwise)
+ *   velocity  host array of T device pointers: n_t fp32 values each,
+ *             16-byte aligned, updated in place (zero them before the
+ *             first step)
+ *   t         the tensors; every residual must be non-NULL (it is DGC's
+ *             accumulated gradient)
+ * Every other argument, the workspace and the limits are bytecomp_compress's.
+ * All arguments are checked before any work is enqueued.  DGC's sparsity
+ * warm-up is a schedule of `ratio` over iterations, chosen by the caller
+ * per call. */
+int bytecomp_compress_dgc(int kind, double ratio, uint64_t seed, float momentum, const bc_tensor* t,
+                          float* const* velocity, int T, bc_payload out, void* ws, size_t ws_bytes,
+                          void* stream);
+
 /* Decompress W workers' payloads and aggregate them (paper Sec. 3.1,
  * Reason #2: each node decompresses the gathered payloads and aggregates
  * them; the aggregation is not an Allreduce because compressed

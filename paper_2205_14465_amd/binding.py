@@ -70,6 +70,9 @@ def lib():
         L.bytecomp_compress.restype = i32
         L.bytecomp_compress.argtypes = [i32, dbl, u64, ctypes.POINTER(bc_tensor), i32, bc_payload, vp,
                                         sz, vp]
+        L.bytecomp_compress_dgc.restype = i32
+        L.bytecomp_compress_dgc.argtypes = [i32, dbl, u64, ctypes.c_float, ctypes.POINTER(bc_tensor), vp, i32,
+                                            bc_payload, vp, sz, vp]
         L.bytecomp_decompress_aggregate.restype = i32
         L.bytecomp_decompress_aggregate.argtypes = [i32, dbl, ctypes.POINTER(bc_payload), i32, vp, i32,
                                                     vp, flt, vp, sz, vp]
@@ -268,6 +271,35 @@ class CompressCall:
         _check("bytecomp_compress",
                lib().bytecomp_compress(self.kind, self.ratio, int(seed) & (2**64 - 1), self.arr, self.T,
                                        self.out, self.ws, self.ws_bytes, self.stream))
+
+
+class DgcCall:
+    """bytecomp_compress_dgc with its argument arrays marshalled once:
+    velocities is a list of fp32 device tensors, one per gradient."""
+
+    def __init__(self, kind, ratio, momentum, grads, resids, velocities, out, ws, stream=None, tensor_ids=None):
+        self.kind = _kind(kind)
+        self.ratio = float(ratio)
+        self.momentum = float(momentum)
+        self.T = len(grads)
+        self.arr = _tensor_list(grads, resids, tensor_ids)
+        self.vel = (ctypes.c_void_p * max(self.T, 1))(*[v.data_ptr() if v.numel() else None for v in velocities])
+        self.out = _payload(out)
+        self.ws = _ptr(ws)
+        self.ws_bytes = ws.numel() * ws.element_size()
+        self.stream = _stream_handle(stream)
+        self._keep = (grads, resids, velocities, out, ws)
+
+    def __call__(self, seed):
+        _check("bytecomp_compress_dgc",
+               lib().bytecomp_compress_dgc(self.kind, self.ratio, int(seed) & (2**64 - 1), self.momentum, self.arr,
+                                           self.vel, self.T, self.out, self.ws, self.ws_bytes, self.stream))
+
+
+def bytecomp_compress_dgc(kind, ratio, seed, momentum, grads, resids, velocities, out, ws, stream=None,
+                          tensor_ids=None):
+    """One DGC step: velocities (fp32 device tensors) and resids are updated in place."""
+    DgcCall(kind, ratio, momentum, grads, resids, velocities, out, ws, stream, tensor_ids)(seed)
 
 
 class AggregateCall:

@@ -474,6 +474,63 @@ int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t,
     return finish(hip_status(e), s, ws);
 }
 
+int bytecomp_compress_dgc(int kind, double ratio, uint64_t seed, float momentum, const bc_tensor* t,
+                          float* const* velocity, int T, bc_payload out, void* ws, size_t ws_bytes, void* stream) {
+    uint64_t ppm;
+    int rc = check_kind_ratio(kind, ratio, ppm);
+    if (rc) return rc;
+    if (!is_sparse(kind)) return BC_E_KIND;
+    if (T < 0 || T > kMaxT) return BC_E_COUNT;
+    if (T == 0) return BC_OK;
+    if (!t || !velocity || !out.idx || !out.val) return BC_E_NULL;
+    if (!ws) return BC_E_WORKSPACE;
+    std::vector<bc_tensor> tv, tc;
+    std::vector<TDesc> dm, dc;
+    uint32_t C, maxc, C2, maxc2;
+    uint64_t sum_k, sum_k2;
+    bool a16, a32, b16, b32;
+    try {
+        tv.resize((size_t)T);
+        tc.resize((size_t)T);
+        for (int i = 0; i < T; ++i) {
+            if (t[i].n > 0 && (!velocity[i] || !t[i].residual)) return BC_E_NULL;
+            tv[(size_t)i] = t[i];
+            tv[(size_t)i].residual = velocity[i];  // the velocity step updates u in place
+            tc[(size_t)i] = bc_tensor{velocity[i], t[i].residual, t[i].n, BC_F32, t[i].tensor_id};
+        }
+        // every argument of the three steps is checked before anything is enqueued
+        rc = build_tdesc(kind, ppm, tv.data(), T, true, dm, C, maxc, sum_k, a16, a32);
+        if (rc == BC_OK) rc = build_tdesc(kind, ppm, tc.data(), T, true, dc, C2, maxc2, sum_k2, b16, b32);
+    } catch (const std::bad_alloc&) {
+        return BC_E_SIZE;
+    }
+    if (rc) return rc;
+    if (kind == BC_RANDK && (sum_k >= (1ull << 32) || !randk_buckets(C, nullptr, nullptr))) return BC_E_SIZE;
+    if (ws_bytes < plan_workspace(kind, T, C, sum_k).total) return BC_E_WORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e;
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        Entry* en = nullptr;
+        e = cache_get(dm.data(), dm.size() * sizeof(TDesc), (size_t)C * 4,
+                      [&](void* dst) { fill_chunk_map(dm, (uint32_t*)dst); }, s, &en);
+        if (e != hipSuccess) return BC_E_HIP;
+        e = launch_dgc_momentum((const TDesc*)en->dev, T, C, momentum, s);
+        cache_mark_used(en, s);
+        if (e != hipSuccess) return BC_E_HIP;
+    }
+    rc = bytecomp_compress(kind, ratio, seed, tc.data(), T, out, ws, ws_bytes, stream);
+    if (rc) return rc;
+    std::lock_guard<std::mutex> lk(g_mu);
+    Entry* en = nullptr;
+    e = cache_get(dm.data(), dm.size() * sizeof(TDesc), (size_t)C * 4,
+                  [&](void* dst) { fill_chunk_map(dm, (uint32_t*)dst); }, s, &en);
+    if (e != hipSuccess) return BC_E_HIP;
+    e = launch_dgc_mask((const TDesc*)en->dev, T, out.idx, sum_k, s);
+    cache_mark_used(en, s);
+    return finish(hip_status(e), s, ws);
+}
+
 }  // extern "C"
 
 namespace {

@@ -356,6 +356,17 @@ __device__ __forceinline__ int unit_owner(const uint64_t* __restrict__ wp, int W
     return (int)reinterpret_cast<const uint32_t*>(wp + 2 * padded_workers(W))[u];
 }
 
+// Tensor whose payload entries hold flattened entry j: the last tensor
+// with off <= j (tensors without entries share the next one's offset).
+__device__ __forceinline__ int tensor_of_entry(const TDesc* __restrict__ d, int T, uint64_t j) {
+    int lo = 0, hi = T - 1;
+    while (lo < hi) {
+        int mid = (lo + hi + 1) >> 1;
+        if (d[mid].off <= j) lo = mid; else hi = mid - 1;
+    }
+    return lo;
+}
+
 // First position p in [0, k) with idx[p] >= x (k if none).
 __device__ __forceinline__ uint32_t lower_bound_u32(const uint32_t* idx, uint32_t k, uint32_t x) {
     uint32_t lo = 0, hi = k;

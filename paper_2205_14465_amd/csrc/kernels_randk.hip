@@ -59,14 +59,6 @@ __device__ __forceinline__ uint32_t feistel(uint32_t x, uint32_t h, uint32_t mas
 }
 
 // Tensor owning flat payload entry j: largest t with off[t] <= j.
-__device__ __forceinline__ int tensor_of_entry(const TDesc* __restrict__ d, int T, uint64_t j) {
-    int lo = 0, hi = T - 1;
-    while (lo < hi) {
-        int mid = (lo + hi + 1) >> 1;
-        if (d[mid].off <= j) lo = mid; else hi = mid - 1;
-    }
-    return lo;
-}
 
 }  // namespace
 

@@ -116,6 +116,10 @@ hipError_t launch_quant_compress(int bits, uint64_t seed, const TDesc* d, int T,
                                  bool any_empty, uint32_t* words, float* scale, const Ws& ws, hipStream_t s);
 hipError_t launch_quant_residual_update(int bits, const TDesc* d, int T, uint32_t C, const uint32_t* words,
                                         const float* scale, hipStream_t s);
+// DGC momentum correction (d: tensors with resid = the velocity u) and
+// momentum-factor masking (idx: the call's payload indices, total entries).
+hipError_t launch_dgc_momentum(const TDesc* d, int T, uint32_t C, float m, hipStream_t s);
+hipError_t launch_dgc_mask(const TDesc* d, int T, const uint32_t* idx, uint64_t total, hipStream_t s);
 // units of kSignAggUnit elements; W <= 1024
 hipError_t launch_aggregate_quant(int bits, const ADesc* a, int T, uint32_t units, const uint64_t* wp, int W,
                                   float alpha, hipStream_t s);

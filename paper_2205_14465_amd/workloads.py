@@ -108,6 +108,7 @@ class Workload:
     grad_dtype: str = "float32"
     sigma_mode: str = "loguniform"   # or "fixed:<sigma>"
     resid_mode: str = "tenth"        # "zero" | "tenth" | "fixed:<sigma>"
+    momentum: float = 0.0            # > 0: DGC momentum correction and masking
 
     @property
     def T(self):
@@ -122,12 +123,13 @@ class Workload:
         """Short file-name form of the workload."""
         return {1: "single2p20_topk_w8", 2: "resnet50_sign_w64", 3: "bertbase_topksampled_w64",
                 4: "gpt2xl_randk_w16", 5: "small4096_fp16sign_w32", 6: "resnet50_terngrad_w64",
-                7: "bertbase_qsgd8_w16", 8: "bertbase_qsgd4_w32"}[self.wid]
+                7: "bertbase_qsgd8_w16", 8: "bertbase_qsgd4_w32", 9: "bertbase_dgc_w64"}[self.wid]
 
 
 def workload(wid: int, shrink: int = 1) -> Workload:
     """The measured workloads (1-5: the hot path's five operator configs;
-    6-8: the stochastic quantizers on the same model shapes); `shrink` > 1
+    6-8: the stochastic quantizers on the same model shapes; 9: DGC's
+    momentum correction around the sampled top-k); `shrink` > 1
     divides every tensor size (at least 1 element) for fast parity runs of
     the same structure."""
     def s(ns):
@@ -156,6 +158,10 @@ def workload(wid: int, shrink: int = 1) -> Workload:
     if wid == 8:
         return Workload(8, "BERT-base gradients (199 fp32 tensors, 109.5M), QSGD 4-bit+EF, W=32",
                         "qsgd4", 0.01, 32, s([numel(x) for x in bert_base_shapes()]))
+    if wid == 9:
+        return Workload(9, "BERT-base gradients (199 fp32 tensors, 109.5M), DGC: momentum 0.9 correction and "
+                           "masking around sampled top-k 1%, W=64", "topk_sampled", 0.01, 64,
+                        s([numel(x) for x in bert_base_shapes()]), momentum=0.9)
     raise ValueError(wid)
 
 

@@ -272,7 +272,8 @@ int bytecomp_device_status(void* ws, size_t ws_bytes, void* stream, uint32_t* fl
 /* Instrumentation, not part of the method: for callers that measure one
  * kernel's own duration (benchmarks).  The next launch, by any call, of
  * the kernel named `kernel` ("aggregate_sign", "aggregate_sparse",
- * "randk_stream", "topk_compact", "sign_pass1", "quant_pass1",
+ * "randk_stream", "topk_compact", "sign_pass1" (the first sign compress
+ * kernel: its one-pass form when it runs), "quant_pass1",
  * "aggregate_quant") records `start_event`
  * when it begins and `stop_event` when it ends (HIP events created by the
  * caller, on the launch's stream); the request is then cleared.  Both

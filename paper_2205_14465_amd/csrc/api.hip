@@ -218,6 +218,7 @@ WsPlan plan_workspace(int kind, int T, uint64_t C, uint64_t sum_k) {
         take(p.s_partial, (size_t)C * 8);
         take(p.s_info, t * 4);
         take(p.s_tab, t * 2048 * 4);
+        take(p.s_slot, (size_t)C * 8);
     } else if (quant_bits(kind)) {
         take(p.s_val, t * 4);
         take(p.q_max, (size_t)C * 4);
@@ -259,6 +260,7 @@ Ws carve_workspace(void* base, const WsPlan& p) {
     w.s_partial = (double*)at(p.s_partial);
     w.s_info = (uint32_t*)at(p.s_info);
     w.s_tab = (int32_t*)at(p.s_tab);
+    w.s_slot = (uint64_t*)at(p.s_slot);
     w.q_max = (uint32_t*)at(p.q_max);
     w.t_hist = (uint32_t*)at(p.t_hist);
     w.t_thr = (uint32_t*)at(p.t_thr);
@@ -453,7 +455,7 @@ int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t,
     const TDesc* dd = (const TDesc*)en->dev;
     switch (kind) {
         case BC_SIGN1:
-            e = launch_sign_compress(dd, T, C, maxc, di.any_empty, out.bits, out.scale, w, s);
+            e = launch_sign_compress(dd, T, C, maxc, di.any_empty, out.bits, out.scale, w, di.cus, s);
             break;
         case BC_TOPK:
         case BC_TOPK_SAMPLED:

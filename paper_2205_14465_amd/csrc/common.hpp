@@ -200,6 +200,64 @@ __device__ __forceinline__ void load_v(const TDesc& td, uint32_t j, bool use_res
     else load_chunk<1, kNT>(td, j, use_resid, v, valid);
 }
 
+// Raw chunk data held in registers between issuing the loads and using
+// them (lets a kernel prefetch its next chunk before a wait).  g[i] holds
+// element i's fp32 bits or, for fp16 gradients, its 16 bits.
+struct RawChunk {
+    uint32_t g[kEpt];
+    float e[kEpt];
+    uint32_t valid;
+};
+
+__device__ __forceinline__ void load_raw(const TDesc& td, uint32_t j, bool use_resid, RawChunk& r) {
+    const uint32_t base = j * (uint32_t)kChunk;
+    const uint32_t n = td.n;
+    r.valid = 0;
+#pragma unroll
+    for (int rr = 0; rr < kRounds; ++rr) {
+        const uint32_t e0 = base + 1024u * rr + 4u * threadIdx.x;
+        if (e0 + 3 < n) {
+            if (td.dtype == 0) {
+                const u32x4 x = ldg4u((const float*)td.grad + e0);
+                r.g[4 * rr] = x.x; r.g[4 * rr + 1] = x.y; r.g[4 * rr + 2] = x.z; r.g[4 * rr + 3] = x.w;
+            } else {
+                const u32x2 h = ldg2u((const uint16_t*)td.grad + e0);
+                r.g[4 * rr] = h.x & 0xFFFFu; r.g[4 * rr + 1] = h.x >> 16;
+                r.g[4 * rr + 2] = h.y & 0xFFFFu; r.g[4 * rr + 3] = h.y >> 16;
+            }
+            if (use_resid) {
+                const f32x4 y = ldg4f(td.resid + e0);
+                r.e[4 * rr] = y.x; r.e[4 * rr + 1] = y.y; r.e[4 * rr + 2] = y.z; r.e[4 * rr + 3] = y.w;
+            }
+            r.valid |= 0xFu << (4 * rr);
+        } else {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const bool ok = e0 + q < n;
+                if (td.dtype == 0) r.g[4 * rr + q] = ok ? gp((const uint32_t*)td.grad)[e0 + q] : 0u;
+                else r.g[4 * rr + q] = ok ? (uint32_t)gp((const uint16_t*)td.grad)[e0 + q] : 0u;
+                if (use_resid) r.e[4 * rr + q] = ok ? gp(td.resid)[e0 + q] : 0.f;
+                r.valid |= (ok ? 1u : 0u) << (4 * rr + q);
+            }
+        }
+        if (!use_resid) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) r.e[4 * rr + q] = 0.f;
+        }
+    }
+}
+
+// v = widen(g) + e from a RawChunk (e = 0 without residual), exactly as
+// load_v forms it; elements past the tensor's end read as +0.0.
+__device__ __forceinline__ void raw_to_v(const TDesc& td, bool use_resid, const RawChunk& r, float v[kEpt]) {
+#pragma unroll
+    for (int i = 0; i < kEpt; ++i) {
+        float g = td.dtype == 0 ? u2f(r.g[i]) : h2f(r.g[i]);
+        g = ((r.valid >> i) & 1u) ? g : 0.f;
+        v[i] = use_resid ? g + r.e[i] : g;
+    }
+}
+
 // Load v that an earlier pass already stored (the residual buffer holds v),
 // or recompute it from the gradient when error feedback is off.
 __device__ __forceinline__ void load_stored_v(const TDesc& td, uint32_t j, float v[kEpt],
@@ -336,6 +394,8 @@ __host__ __device__ inline U64x4 philox4x64_10(U64x4 c, uint64_t k0, uint64_t k1
 constexpr uint64_t kStreamRandk = 0;
 constexpr uint64_t kStreamSample = 1;
 constexpr uint64_t kStreamQuant = 2;
+
+constexpr uint32_t kFlagWaitTimeout = 1u;  // a bounded wait between workgroups ran out
 
 // Workspace header: failure flags (bit 0 reserved for a bounded wait that
 // ran out; no current kernel waits on another workgroup).

@@ -6,14 +6,20 @@
 // element i at bit i mod 32, LSB first); s = mean |v| accumulated in fp64
 // and rounded once to fp32; e_new = v - (bit ? -s : +s).
 //
-// The scale needs the whole tensor before any residual can be written, so
-// the work takes two passes: pass 1 writes the bits, the chunk partial sums
-// and v (into e); pass 2 sums the partials of its tensor in a fixed order,
-// re-reads v and writes the residual.  The re-read of v mostly hits the
-// 256 MB last-level cache for tensor sets of ResNet-50 size.  (A one-pass
-// kernel that keeps v in registers while the tensor's workgroups exchange
-// partial sums was slower on every workload measured: the workgroups of a
-// tensor wait for each other with nothing to overlap.)
+// The scale needs the whole tensor before any residual can be written.
+// When every tensor has at most as many chunks as the GPU holds resident
+// workgroups, ONE pass does it (sign_onepass): a grid of resident
+// workgroups visits chunks c = blockIdx + k * grid; for each it loads g and
+// e, writes the bits, publishes the chunk's fp64 partial sum, and only then
+// writes the residual of its PREVIOUS chunk, kept in registers, whose
+// tensor's scale is by then almost always known.  The last workgroup to
+// publish a chunk of a tensor sums the tensor's partials in a fixed order
+// and publishes the scale.  Otherwise two passes run: pass 1 writes the
+// bits, the chunk partial sums and v (into e); pass 2 sums the partials of
+// its tensor in the same fixed order, re-reads v and writes the residual.
+// (An earlier one-pass form that waited for each chunk's own tensor before
+// moving on was slower than two passes: the workgroups of a tensor waited
+// for each other with nothing to overlap.)
 #include "launch.hpp"
 
 namespace bc {
@@ -135,6 +141,131 @@ __global__ __launch_bounds__(kBlock) void sign_pass2(const TDesc* __restrict__ d
     store_sign_residual<kNT>(td, j, s, v);
 }
 
+// --------------------------------------------------------------- one pass
+// Chunk partial sums travel through slots that hold the bitwise complement
+// of the fp64 partial once published and 0 before (a sum of magnitudes is
+// never all ones), so a slot needs no separate ready flag and a zeroed
+// workspace starts every slot empty.  A workgroup writes chunk c's
+// residual only after publishing chunk c + grid (and prefetching its next
+// chunk): it then reads all its tensor's slots, waiting while any is
+// empty, and sums them in the fixed order of the two-pass path.
+//
+// Every wait ends: the chunks of tensor(c) are published by workgroups
+// whose earlier waits concern chunks at least two grids before them,
+// which (no tensor being longer than a grid) belong to earlier tensors; by
+// induction over the tensors every slot is published, provided every
+// workgroup of the grid is resident (the launcher sizes the grid so).  The
+// wait is bounded regardless: past kSpinLimit polls it records
+// kFlagWaitTimeout in the workspace header and goes on.
+namespace {
+constexpr uint32_t kSpinLimit = 1u << 20;
+
+// Scale of tensor td from its published chunk slots (every thread returns it).
+__device__ __forceinline__ float onepass_scale(const TDesc& td, uint64_t* slot, uint32_t* flags, double* sh) {
+    __shared__ int pending_sh;
+    uint32_t spins = 0;
+    double acc;
+    for (;;) {
+        acc = 0.0;
+        int missing = 0;
+        for (uint32_t q = threadIdx.x; q < td.nchunks; q += kBlock) {
+            const unsigned long long x =
+                __hip_atomic_load((unsigned long long*)slot + td.chunk0 + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            missing |= x == 0ull;
+            acc += __longlong_as_double((long long)~x);
+        }
+        if (threadIdx.x == 0) pending_sh = 0;
+        __syncthreads();
+        if (missing) pending_sh = 1;
+        __syncthreads();
+        const int pending = pending_sh;
+        __syncthreads();
+        if (!pending) break;
+        if (++spins > kSpinLimit) {
+            if (threadIdx.x == 0)
+                __hip_atomic_fetch_or(flags, kFlagWaitTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            break;
+        }
+        __builtin_amdgcn_s_sleep(4);
+    }
+    return (float)(block_sum_f64(acc, sh) / (double)td.n);
+}
+}  // namespace
+
+__global__ __launch_bounds__(kBlock) void sign_onepass(const TDesc* __restrict__ d, int T, uint32_t C,
+                                                       uint32_t* __restrict__ bits, float* __restrict__ scale_out,
+                                                       Ws ws) {
+    __shared__ double sh[4];
+    float vp[kEpt];  // the previous chunk's v, its residual not yet written
+    TDesc tdp{};
+    bool prev = false;
+    uint32_t jp = 0;
+    float sp = 0.f;  // its scale when already known (a single-chunk tensor)
+    RawChunk raw;
+    uint32_t c = blockIdx.x;
+    TDesc td{};
+    if (c < C) {
+        td = d[tensor_of_chunk(d, T, c)];
+        load_raw(td, c - td.chunk0, td.resid != nullptr, raw);
+    }
+    for (;; c += gridDim.x) {
+        const bool have = c < C;
+        float v[kEpt];
+        uint32_t j = 0;
+        float s_now = 0.f;
+        if (have) {
+            const int t = tensor_of_chunk(d, T, c);
+            j = c - td.chunk0;
+            raw_to_v(td, td.resid != nullptr, raw, v);
+            store_sign_words(v, bits + td.off + (uint64_t)j * kChunkWords, chunk_words(td, j));
+            const double p = block_sum_f64(thread_abs_sum(v), sh);
+            if (td.nchunks == 1) {
+                s_now = (float)(p / (double)td.n);
+                if (threadIdx.x == 0) scale_out[t] = s_now;
+            } else if (threadIdx.x == 0) {
+                __hip_atomic_store((unsigned long long*)ws.s_slot + c, ~(unsigned long long)__double_as_longlong(p),
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        // the next chunk's loads go out before this round's wait
+        const uint32_t cn = c + gridDim.x;
+        TDesc tdn{};
+        if (cn < C) {
+            tdn = d[tensor_of_chunk(d, T, cn)];
+            load_raw(tdn, cn - tdn.chunk0, tdn.resid != nullptr, raw);
+        }
+        if (prev) {
+            float s = sp;
+            if (tdp.nchunks > 1) {
+                s = onepass_scale(tdp, ws.s_slot, ws.flags, sh);
+                if (jp == 0 && threadIdx.x == 0) scale_out[tensor_of_chunk(d, T, tdp.chunk0)] = s;
+            }
+            if (tdp.resid) store_sign_residual<false>(tdp, jp, s, vp);
+        }
+        if (!have) break;
+#pragma unroll
+        for (int i = 0; i < kEpt; ++i) vp[i] = v[i];
+        tdp = td;
+        prev = true;
+        jp = j;
+        sp = s_now;
+        td = tdn;
+    }
+}
+
+// Scales of empty tensors (+0.0) for the one-pass path.
+__global__ void sign_empty_scales(const TDesc* __restrict__ d, int T, float* __restrict__ scale_out) {
+    const int t = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+    if (t < T && d[t].nchunks == 0) scale_out[t] = 0.f;
+}
+
+// Slots of the one-pass kernel back to empty for the next call (a fill
+// kernel, not a memset, so that the sequence stays capturable).
+__global__ void sign_onepass_reset(uint32_t C, Ws ws) {
+    for (uint32_t c = blockIdx.x * blockDim.x + threadIdx.x; c < C; c += gridDim.x * blockDim.x)
+        ws.s_slot[c] = 0ull;
+}
+
 // -------------------------------------------------- residual update (sign)
 __global__ __launch_bounds__(kBlock) void sign_residual_update(const TDesc* __restrict__ d, int T,
                                                                const uint32_t* __restrict__ bits,
@@ -164,9 +295,32 @@ __global__ __launch_bounds__(kBlock) void sign_residual_update(const TDesc* __re
 }
 
 // ------------------------------------------------------------- launchers
+namespace {
+// Workgroups of sign_onepass resident at once on the whole GPU.
+uint32_t onepass_capacity(int cus) {
+    static int per_cu = -1;
+    if (per_cu < 0) {
+        int nb = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, sign_onepass, kBlock, 0) != hipSuccess) nb = 0;
+        per_cu = nb;
+    }
+    return (uint32_t)per_cu * (uint32_t)(cus > 0 ? cus : 0);
+}
+}  // namespace
+
 hipError_t launch_sign_compress(const TDesc* d, int T, uint32_t C, uint32_t max_chunks, bool any_empty,
-                                uint32_t* bits, float* scale, const Ws& ws, hipStream_t s) {
+                                uint32_t* bits, float* scale, const Ws& ws, int cus, hipStream_t s) {
     if (T <= 0) return hipSuccess;
+    // one pass when every tensor fits the resident grid
+    const uint32_t cap = onepass_capacity(cus);
+    if (C > 0 && cap > 0 && max_chunks <= cap) {
+        const uint32_t grid = C < cap ? C : cap;
+        (void)launch_timed(kTimedSignPass1, sign_onepass, dim3(grid), dim3(kBlock), 0, s, d, T, C, bits, scale, ws);
+        hipLaunchKernelGGL(sign_onepass_reset, dim3((C + 255) / 256 < 1024 ? (C + 255) / 256 : 1024), dim3(256), 0, s,
+                           C, ws);
+        if (any_empty) hipLaunchKernelGGL(sign_empty_scales, dim3((T + 255) / 256), dim3(256), 0, s, d, T, scale);
+        return hipGetLastError();
+    }
     // past the cache size: stream g and e_old past the cache, keep v (re-read
     // by pass 2) in it, and stream e_new out
     const bool nt = C > kNtChunks;

@@ -20,6 +20,8 @@ struct Ws {
     float* s_val;           // [T] published scales
     double* s_partial;      // [C] per-chunk sums of |v|
     uint32_t* s_info;       // [T] aggregate: form (bits 0-7), smallest scale exponent (8-15)
+    uint64_t* s_slot;       // [C] one-pass compress: ~bits of each chunk's partial sum once
+                            // published, 0 otherwise (0 between calls)
     int32_t* s_tab;         // [T * 2048] aggregate: int32 lookup tables of each tensor
     // BC_TERNGRAD, BC_QSGD4, BC_QSGD8 (and s_val)
     uint32_t* q_max;        // [C] largest |v| bits of each chunk
@@ -49,7 +51,7 @@ struct Ws {
 // Byte offsets of every region for a call shape; `total` is the workspace
 // size.  Regions a kind does not use have size 0.
 struct WsPlan {
-    size_t flags, s_val, s_partial, s_info, s_tab, q_max;
+    size_t flags, s_val, s_partial, s_info, s_tab, s_slot, q_max;
     size_t t_hist, t_thr, t_prefix, t_krem, t_fb, t_any, t_cand, t_ccount, t_gt, t_eq, t_off, t_eqb;
     size_t r_keys, r_tmp, r_ccount, r_coff, r_hist;
     size_t total;
@@ -92,7 +94,7 @@ constexpr uint32_t kNtChunks = 8192;
 // ------------------------------------------------------------- launchers
 // d: device TDesc[T]; C: total chunks.  Return the first HIP error.
 hipError_t launch_sign_compress(const TDesc* d, int T, uint32_t C, uint32_t max_chunks, bool any_empty,
-                                uint32_t* bits, float* scale, const Ws& ws, hipStream_t s);
+                                uint32_t* bits, float* scale, const Ws& ws, int cus, hipStream_t s);
 hipError_t launch_topk(int kind, double ratio, uint64_t seed, const TDesc* d, int T, uint32_t C,
                        bool any_f16, bool any_f32, uint32_t* idx, float* val, const Ws& ws,
                        hipStream_t s);

@@ -222,6 +222,7 @@ WsPlan plan_workspace(int kind, int T, uint64_t C, uint64_t sum_k) {
     } else if (quant_bits(kind)) {
         take(p.s_val, t * 4);
         take(p.q_max, (size_t)C * 4);
+        take(p.q_slot, (size_t)C * 4);
     } else if (kind == BC_TOPK || kind == BC_TOPK_SAMPLED) {
         take(p.t_hist, t * kBins0 * 4);
         take(p.t_thr, t * 4);
@@ -262,6 +263,7 @@ Ws carve_workspace(void* base, const WsPlan& p) {
     w.s_tab = (int32_t*)at(p.s_tab);
     w.s_slot = (uint64_t*)at(p.s_slot);
     w.q_max = (uint32_t*)at(p.q_max);
+    w.q_slot = (uint32_t*)at(p.q_slot);
     w.t_hist = (uint32_t*)at(p.t_hist);
     w.t_thr = (uint32_t*)at(p.t_thr);
     w.t_prefix = (uint32_t*)at(p.t_prefix);
@@ -466,7 +468,7 @@ int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t,
         case BC_QSGD4:
         case BC_QSGD8:
             e = launch_quant_compress(quant_bits(kind), seed, dd, T, C, maxc, di.any_empty, out.bits, out.scale,
-                                      w, s);
+                                      w, di.cus, s);
             break;
         default:
             e = launch_randk(seed, dd, T, C, sum_k, a16, a32, out.idx, out.val, w, s);

@@ -113,6 +113,44 @@ __device__ __forceinline__ void store_codes(uint32_t packed, uint32_t e0, uint32
     }
 }
 
+// Quantize chunk j of tensor td (v in registers, scale m): codes into the
+// payload words, residual into e.
+template <int kBits, bool kNT>
+__device__ __forceinline__ void quantize_chunk(const TDesc& td, uint32_t j, float m, float (&v)[kEpt], uint32_t valid,
+                                               uint64_t seed, uint32_t* __restrict__ words) {
+    using Q = Quant<kBits>;
+    const bool any = m > 0.f;
+    const float inv = any ? (float)((double)Q::kLevels / (double)m) : 0.f;
+    const float unit = (float)((double)m / (double)Q::kLevels);
+    uint32_t* tw = words + td.off;
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r) {
+        const uint32_t e0 = j * (uint32_t)kChunk + 1024u * r + 4u * threadIdx.x;  // element of the tensor
+        float u[4];
+        quant_uniforms(seed, td.tid, e0 >> 3, (e0 >> 2) & 1u, u);
+        uint32_t packed = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int i = 4 * r + q;
+            uint32_t level = 0;
+            if (any && ((valid >> i) & 1u)) {
+                const float x = fabsf(v[i]) * inv;
+                if (x >= (float)Q::kLevels) {
+                    level = (uint32_t)Q::kLevels;
+                } else {
+                    const float fl = floorf(x);
+                    level = (uint32_t)fl + (u[q] < x - fl ? 1u : 0u);
+                }
+            }
+            const uint32_t code = level ? (level | ((f2u(v[i]) >> 31) << (kBits - 1))) : 0u;
+            packed |= code << (kBits * q);
+            v[i] = v[i] - quant_decode<kBits>(code, unit);
+        }
+        store_codes<kBits>(packed, e0, tw, td.k);
+    }
+    if (td.resid) store_chunk<kNT>(td.resid, td.n, j, v);
+}
+
 }  // namespace
 
 // Pass 1: v = g + e (parked in e for pass 2) and the chunk's largest |v|
@@ -159,7 +197,6 @@ template <int kBits, bool kNT>
 __global__ __launch_bounds__(kBlock) void quant_pass2(const TDesc* __restrict__ d, int T, uint64_t seed,
                                                       uint32_t* __restrict__ words, float* __restrict__ scale_out,
                                                       Ws ws) {
-    using Q = Quant<kBits>;
     __shared__ uint32_t sh[4];
     const uint32_t c = blockIdx.x;
     const int t = tensor_of_chunk(d, T, c);
@@ -172,39 +209,129 @@ __global__ __launch_bounds__(kBlock) void quant_pass2(const TDesc* __restrict__ 
     } else {
         m = ws.s_val[t];
     }
-    const bool any = m > 0.f;
-    const float inv = any ? (float)((double)Q::kLevels / (double)m) : 0.f;
-    const float unit = (float)((double)m / (double)Q::kLevels);
     float v[kEpt];
     uint32_t valid;
     load_stored_v(td, j, v, valid);  // e holds v after pass 1 (or v = g without error feedback)
-    uint32_t* tw = words + td.off;
-#pragma unroll
-    for (int r = 0; r < kRounds; ++r) {
-        const uint32_t e0 = j * (uint32_t)kChunk + 1024u * r + 4u * threadIdx.x;  // element of the tensor
-        float u[4];
-        quant_uniforms(seed, td.tid, e0 >> 3, (e0 >> 2) & 1u, u);
-        uint32_t packed = 0;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int i = 4 * r + q;
-            uint32_t level = 0;
-            if (any && ((valid >> i) & 1u)) {
-                const float x = fabsf(v[i]) * inv;
-                if (x >= (float)Q::kLevels) {
-                    level = (uint32_t)Q::kLevels;
-                } else {
-                    const float fl = floorf(x);
-                    level = (uint32_t)fl + (u[q] < x - fl ? 1u : 0u);
-                }
-            }
-            const uint32_t code = level ? (level | ((f2u(v[i]) >> 31) << (kBits - 1))) : 0u;
-            packed |= code << (kBits * q);
-            v[i] = v[i] - quant_decode<kBits>(code, unit);
+    quantize_chunk<kBits, kNT>(td, j, m, v, valid, seed, words);
+}
+
+// One pass (tensors no longer than the resident grid), as the one-pass
+// sign compress: chunk c publishes its largest |v| bits in a slot (with bit
+// 31 set, 0 meaning not yet), the next chunk's loads go out, and chunk
+// c - grid, kept in registers, is quantized once every slot of its tensor
+// is published (the maximum of the slots is the scale, exact in any
+// order).  Waits end by the same induction over the tensors (every
+// workgroup resident, no tensor longer than the grid) and are bounded
+// regardless (workspace flag bit 0).
+namespace {
+constexpr uint32_t kQuantSpinLimit = 1u << 20;
+
+__device__ __forceinline__ float quant_onepass_scale(const TDesc& td, uint32_t* slot, uint32_t* flags, uint32_t* sh) {
+    __shared__ int pending_sh;
+    uint32_t spins = 0;
+    uint32_t mx;
+    for (;;) {
+        mx = 0;
+        int missing = 0;
+        for (uint32_t q = threadIdx.x; q < td.nchunks; q += kBlock) {
+            const uint32_t x = __hip_atomic_load(slot + td.chunk0 + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            missing |= x == 0u;
+            const uint32_t k = x & 0x7FFFFFFFu;
+            mx = k > mx ? k : mx;
         }
-        store_codes<kBits>(packed, e0, tw, td.k);
+        if (threadIdx.x == 0) pending_sh = 0;
+        __syncthreads();
+        if (missing) pending_sh = 1;
+        __syncthreads();
+        const int pending = pending_sh;
+        __syncthreads();
+        if (!pending) break;
+        if (++spins > kQuantSpinLimit) {
+            if (threadIdx.x == 0)
+                __hip_atomic_fetch_or(flags, kFlagWaitTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            break;
+        }
+        __builtin_amdgcn_s_sleep(4);
     }
-    if (td.resid) store_chunk<kNT>(td.resid, td.n, j, v);
+    return u2f(block_max_u32(mx, sh));
+}
+}  // namespace
+
+template <int kBits>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void quant_onepass(const TDesc* __restrict__ d, int T, uint32_t C, uint64_t seed,
+                                                        uint32_t* __restrict__ words, float* __restrict__ scale_out,
+                                                        Ws ws) {
+    __shared__ uint32_t sh[4];
+    float vp[kEpt];
+    uint32_t validp = 0;
+    TDesc tdp{};
+    bool prev = false;
+    uint32_t jp = 0;
+    float mp = 0.f;  // its scale when already known (a single-chunk tensor)
+    RawChunk raw;
+    uint32_t c = blockIdx.x;
+    TDesc td{};
+    if (c < C) {
+        td = d[tensor_of_chunk(d, T, c)];
+        load_raw(td, c - td.chunk0, td.resid != nullptr, raw);
+    }
+    for (;; c += gridDim.x) {
+        const bool have = c < C;
+        float v[kEpt];
+        uint32_t j = 0;
+        float m_now = 0.f;
+        if (have) {
+            const int t = tensor_of_chunk(d, T, c);
+            j = c - td.chunk0;
+            raw_to_v(td, td.resid != nullptr, raw, v);
+            uint32_t mk = 0;
+#pragma unroll
+            for (int i = 0; i < kEpt; ++i) {
+                const uint32_t k = ((raw.valid >> i) & 1u) ? key_of(v[i]) : 0u;
+                mk = k > mk ? k : mk;
+            }
+            mk = block_max_u32(mk, sh);
+            if (td.nchunks == 1) {
+                m_now = u2f(mk);
+                if (threadIdx.x == 0) scale_out[t] = m_now;
+            } else if (threadIdx.x == 0) {
+                __hip_atomic_store(ws.q_slot + c, mk | 0x80000000u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        const uint32_t valid_now = raw.valid;
+        const uint32_t cn = c + gridDim.x;
+        TDesc tdn{};
+        if (cn < C) {
+            tdn = d[tensor_of_chunk(d, T, cn)];
+            load_raw(tdn, cn - tdn.chunk0, tdn.resid != nullptr, raw);
+        }
+        if (prev) {
+            float m = mp;
+            if (tdp.nchunks > 1) {
+                m = quant_onepass_scale(tdp, ws.q_slot, ws.flags, sh);
+                if (jp == 0 && threadIdx.x == 0) scale_out[tensor_of_chunk(d, T, tdp.chunk0)] = m;
+            }
+            quantize_chunk<kBits, false>(tdp, jp, m, vp, validp, seed, words);
+        }
+        if (!have) break;
+#pragma unroll
+        for (int i = 0; i < kEpt; ++i) vp[i] = v[i];
+        validp = valid_now;
+        tdp = td;
+        prev = true;
+        jp = j;
+        mp = m_now;
+        td = tdn;
+    }
+}
+
+__global__ void quant_onepass_reset(uint32_t C, Ws ws) {
+    for (uint32_t c = blockIdx.x * blockDim.x + threadIdx.x; c < C; c += gridDim.x * blockDim.x) ws.q_slot[c] = 0u;
+}
+
+__global__ void quant_empty_scales(const TDesc* __restrict__ d, int T, float* __restrict__ scale_out) {
+    const int t = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+    if (t < T && d[t].nchunks == 0) scale_out[t] = 0.f;
 }
 
 // Residual update from a payload made elsewhere: e <- (g + e) - decode.
@@ -343,9 +470,42 @@ void quant_compress_bits(const TDesc* d, int T, uint32_t C, bool nt, uint64_t se
 }
 }  // namespace
 
+namespace {
+template <int kBits>
+uint32_t quant_onepass_capacity(int cus) {
+    static int per_cu = -1;
+    if (per_cu < 0) {
+        int nb = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, quant_onepass<kBits>, kBlock, 0) != hipSuccess) nb = 0;
+        per_cu = nb;
+    }
+    return (uint32_t)per_cu * (uint32_t)(cus > 0 ? cus : 0);
+}
+
+template <int kBits>
+bool quant_onepass_launch(uint64_t seed, const TDesc* d, int T, uint32_t C, uint32_t max_chunks, bool any_empty,
+                          uint32_t* words, float* scale, const Ws& ws, int cus, hipStream_t s) {
+    const uint32_t cap = quant_onepass_capacity<kBits>(cus);
+    if (C == 0 || cap == 0 || max_chunks > cap) return false;
+    const uint32_t grid = C < cap ? C : cap;
+    (void)launch_timed(kTimedQuantPass1, quant_onepass<kBits>, dim3(grid), dim3(kBlock), 0, s, d, T, C, seed, words,
+                       scale, ws);
+    hipLaunchKernelGGL(quant_onepass_reset, dim3((C + 255) / 256 < 1024 ? (C + 255) / 256 : 1024), dim3(256), 0, s,
+                       C, ws);
+    if (any_empty) hipLaunchKernelGGL(quant_empty_scales, dim3((T + 255) / 256), dim3(256), 0, s, d, T, scale);
+    return true;
+}
+}  // namespace
+
 hipError_t launch_quant_compress(int bits, uint64_t seed, const TDesc* d, int T, uint32_t C, uint32_t max_chunks,
-                                 bool any_empty, uint32_t* words, float* scale, const Ws& ws, hipStream_t s) {
+                                 bool any_empty, uint32_t* words, float* scale, const Ws& ws, int cus,
+                                 hipStream_t s) {
     if (T <= 0) return hipSuccess;
+    // one pass when every tensor fits the resident grid
+    const bool one = bits == 2   ? quant_onepass_launch<2>(seed, d, T, C, max_chunks, any_empty, words, scale, ws, cus, s)
+                     : bits == 4 ? quant_onepass_launch<4>(seed, d, T, C, max_chunks, any_empty, words, scale, ws, cus, s)
+                                 : quant_onepass_launch<8>(seed, d, T, C, max_chunks, any_empty, words, scale, ws, cus, s);
+    if (one) return hipGetLastError();
     const bool nt = C > kNtChunks;
     if (C > 0) {
         if (nt) (void)launch_timed(kTimedQuantPass1, quant_pass1<true>, dim3(C), dim3(kBlock), 0, s, d, T, ws);

@@ -25,6 +25,8 @@ struct Ws {
     int32_t* s_tab;         // [T * 2048] aggregate: int32 lookup tables of each tensor
     // BC_TERNGRAD, BC_QSGD4, BC_QSGD8 (and s_val)
     uint32_t* q_max;        // [C] largest |v| bits of each chunk
+    uint32_t* q_slot;       // [C] one-pass compress: those bits | 1 << 31 once published, 0 otherwise
+                            // (0 between calls)
     // BC_TOPK, BC_TOPK_SAMPLED
     uint32_t* t_hist;       // [T * 2048] histograms         
     uint32_t* t_thr;        // [T] candidate threshold (key)
@@ -51,7 +53,7 @@ struct Ws {
 // Byte offsets of every region for a call shape; `total` is the workspace
 // size.  Regions a kind does not use have size 0.
 struct WsPlan {
-    size_t flags, s_val, s_partial, s_info, s_tab, s_slot, q_max;
+    size_t flags, s_val, s_partial, s_info, s_tab, s_slot, q_max, q_slot;
     size_t t_hist, t_thr, t_prefix, t_krem, t_fb, t_any, t_cand, t_ccount, t_gt, t_eq, t_off, t_eqb;
     size_t r_keys, r_tmp, r_ccount, r_coff, r_hist;
     size_t total;
@@ -115,7 +117,7 @@ hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t units, const ui
                                  float alpha, uint32_t* info, int32_t* tabs, hipStream_t s);
 // Stochastic b-bit quantizers (bits 2, 4 or 8).
 hipError_t launch_quant_compress(int bits, uint64_t seed, const TDesc* d, int T, uint32_t C, uint32_t max_chunks,
-                                 bool any_empty, uint32_t* words, float* scale, const Ws& ws, hipStream_t s);
+                                 bool any_empty, uint32_t* words, float* scale, const Ws& ws, int cus, hipStream_t s);
 hipError_t launch_quant_residual_update(int bits, const TDesc* d, int T, uint32_t C, const uint32_t* words,
                                         const float* scale, hipStream_t s);
 // DGC momentum correction (d: tensors with resid = the velocity u) and

@@ -9,18 +9,22 @@
 // floating-point atomics are used, so results are deterministic and match
 // that order bit for bit.
 //
-// Each wave owns a run of 2048- or 4096-element output tiles held in LDS.
+// Each wave owns a run of 2048-, 4096- or 8192-element output tiles held in
+// LDS.
 // For every tile it walks the workers in order; worker w's entries for the
 // tile are the next ones after its cursor (indices ascending), read 64 at a
 // time and added into the tile (indices are unique within a worker, so a
 // worker's adds never collide and need no atomics).  Cursors are found by a
 // binary search only where a wave's run starts inside a tensor.
+#include <mutex>
+
 #include "launch.hpp"
 
 namespace bc {
 
 // Each wave owns a run of consecutive kTS-element tiles held in its own LDS
-// slice.  The next 64 entries of kS workers are kept in flight in registers
+// slice.  The next 64 kEPL entries of kS workers (a window: lane l holds
+// entries l, l + 64, ... of it) are kept in flight in registers
 // (slot w % kS holds worker w): as soon as a worker's entries for the tile
 // have been added, its slot is refilled with the worker that comes kS
 // later, or, when W is a multiple of kS and the next tile continues the
@@ -36,11 +40,15 @@ namespace bc {
 // kNT: the output tiles are written with the non-temporal hint (outputs
 // larger than the last-level cache).
 //
+// kEPL = 2 (8192-element tiles, for calls with many tiles) halves the
+// steps per element of the 4096-element form: each step covers a worker's
+// next 128 entries, two per lane.
+//
 // kRagged (with kLanes): the payloads are parts packed by
 // bytecomp_pack_part, so worker w's entries of tensor t start at
 // rp_w[t] and number rp_w[t+1] - rp_w[t] (rp[w] is worker w's part-offset
 // array); a worker with no entries reads a dummy location rp[Wp] instead.
-template <uint32_t kTS, int kS, bool kLanes, bool kRagged, bool kNT>
+template <uint32_t kTS, int kS, bool kLanes, bool kRagged, bool kNT, int kEPL>
 __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restrict__ a, int T,
                                                            uint32_t U, const uint64_t* __restrict__ wp,
                                                            int W, float alpha, const uint64_t* __restrict__ rp) {
@@ -72,9 +80,10 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
     // tensor's entries) so that the compiler can count the loads in flight
     // exactly and wait only for the one it needs; a dead slot's entries are
     // masked by setting every bit of its index (never below a tile end).
-    uint32_t x[kS];
-    float y[kS];
-    uint32_t inv[kS];
+    constexpr uint32_t kWin = 64u * kEPL;  // entries per window
+    uint32_t x[kS][kEPL];
+    float y[kS][kEPL];
+    uint32_t inv[kS][kEPL];
     int t = -1;
     ADesc ad{};
     bool primed = false;  // slots already hold this tile's first entries
@@ -110,9 +119,7 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
             else return ad.k;
         };
         auto load_slot = [&](int q, int w, uint32_t c, bool live) {
-            const uint32_t i = c + lane;
             const uint32_t kw = k_of(w);
-            const uint32_t ic = i < kw ? i : (kw ? kw - 1u : 0u);
             const uint32_t* pa;
             const float* pb;
             if constexpr (kLanes) {
@@ -124,10 +131,15 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
                 pa = w_a(wp, w) + ad.off;
                 pb = w_b(wp, W, w) + ad.off;
             }
-            x[q] = gp(pa)[ic];
-            y[q] = gp(pb)[ic];
-            inv[q] = (live && i < kw) ? 0u : 0xFFFFFFFFu;
-            asm volatile("" : "+v"(inv[q]));  // computed here, not sunk to its use
+#pragma unroll
+            for (int e = 0; e < kEPL; ++e) {
+                const uint32_t i = c + 64u * e + lane;
+                const uint32_t ic = i < kw ? i : (kw ? kw - 1u : 0u);
+                x[q][e] = gp(pa)[ic];
+                y[q][e] = gp(pb)[ic];
+                inv[q][e] = (live && i < kw) ? 0u : 0xFFFFFFFFu;
+                asm volatile("" : "+v"(inv[q][e]));  // computed here, not sunk to its use
+            }
         };
         if (!primed) {
             // W through an opaque copy: keeps the sixteen per-slot worker
@@ -148,9 +160,9 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
         for (uint32_t r = 0; r < kTS / 256u; ++r)
             *reinterpret_cast<f32x4*>(tile + 256u * r + 4u * lane) = f32x4{0.f, 0.f, 0.f, 0.f};
         __builtin_amdgcn_wave_barrier();
-        // a worker with 64 or more entries in the tile (dense payloads)
+        // a worker with a whole window or more in the tile (dense payloads)
         // ends the pipelined walk: the rest of the tile, from that worker
-        // on, is finished one 64-entry window at a time below.  Keeping that
+        // on, is finished one window at a time below.  Keeping that
         // loop out of the pipelined steps keeps their load waits exact.
         int dw = -1;
         uint32_t dcc = 0;
@@ -168,16 +180,19 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
                 uint32_t cc = 0;
                 if (w < Wq && dw < 0) {  // no load in here
                     cc = get_cur(w);
-                    const uint32_t xv = x[q] | inv[q];
-                    const uint64_t m = __ballot(xv < hi);
-                    // entries below the tile can only come from an unsorted
-                    // payload; they are skipped rather than written out of range
-                    const uint32_t dd = xv - lo;
-                    if (dd < len) tile[dd] += y[q];
-                    const uint32_t cnt = (uint32_t)__popcll(m);
+                    uint32_t cnt = 0;
+#pragma unroll
+                    for (int e = 0; e < kEPL; ++e) {
+                        const uint32_t xv = x[q][e] | inv[q][e];
+                        cnt += (uint32_t)__popcll(__ballot(xv < hi));
+                        // entries below the tile can only come from an unsorted
+                        // payload; they are skipped rather than written out of range
+                        const uint32_t dd = xv - lo;
+                        if (dd < len) tile[dd] += y[q][e];
+                    }
                     cc += cnt;
                     __builtin_amdgcn_wave_barrier();
-                    if (cnt == 64) {
+                    if (cnt == kWin) {
                         dw = w;
                         dcc = cc;
                     } else {
@@ -210,18 +225,21 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
                     pa = w_a(wp, w) + ad.off;
                     pb = w_b(wp, W, w) + ad.off;
                 }
-                uint32_t cnt = 64;
-                while (cnt == 64) {
-                    const uint32_t i = cc + lane;
+                uint32_t cnt = kWin;
+                while (cnt == kWin) {
                     const uint32_t kw = k_of(w);
-                    const bool oki = i < kw;
-                    const uint32_t ic = oki ? i : (kw ? kw - 1u : 0u);
-                    const uint32_t xi = oki ? gp(pa)[ic] : 0xFFFFFFFFu;
-                    const float yi = gp(pb)[ic];
-                    const uint64_t m = __ballot(xi < hi);
-                    const uint32_t dd = xi - lo;
-                    if (dd < len) tile[dd] += yi;
-                    cnt = (uint32_t)__popcll(m);
+                    cnt = 0;
+#pragma unroll
+                    for (int e = 0; e < kEPL; ++e) {
+                        const uint32_t i = cc + 64u * e + lane;
+                        const bool oki = i < kw;
+                        const uint32_t ic = oki ? i : (kw ? kw - 1u : 0u);
+                        const uint32_t xi = oki ? gp(pa)[ic] : 0xFFFFFFFFu;
+                        const float yi = gp(pb)[ic];
+                        cnt += (uint32_t)__popcll(__ballot(xi < hi));
+                        const uint32_t dd = xi - lo;
+                        if (dd < len) tile[dd] += yi;
+                    }
                     cc += cnt;
                     __builtin_amdgcn_wave_barrier();
                 }
@@ -256,69 +274,83 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
 
 // -------------------------------------------------------------- launchers
 uint32_t sparse_agg_tile(uint64_t n_total, uint64_t k_total) {
-    // 4096-element tiles while a worker holds about 48 entries per tile or
-    // fewer (one 64-entry window covers its entries), 2048 otherwise
+    // 8192-element tiles (128-entry windows) for calls of at least 2^24
+    // elements whose workers hold about 100 entries per such tile or fewer;
+    // else 4096-element tiles while a worker holds about 48 entries per tile
+    // or fewer (one 64-entry window covers its entries); 2048 otherwise
+    if (n_total >= (1ull << 24) && k_total * 8192u <= n_total * 100u) return 8192u;
     return k_total * 4096u <= n_total * 48u ? 4096u : 2048u;
 }
 
 namespace {
 template <uint32_t kTS, int kS, bool kLanes, bool kRagged, bool kNT>
-void launch_sparse_t(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W, float alpha, int cus,
-                     const uint64_t* rp, hipStream_t s) {
+hipError_t launch_sparse_t(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W, float alpha, int cus,
+                           const uint64_t* rp, hipStream_t s) {
+    constexpr int kEPL = kTS > 4096u ? 2 : 1;
+    const auto kern = aggregate_sparse<kTS, kS, kLanes, kRagged, kNT, kEPL>;
     const size_t lds = (size_t)4 * (kTS * 4 + (kLanes ? 0 : (size_t)W * 4));
     // one round of resident workgroups at this LDS size (more waves with
     // shorter runs measured slower)
     size_t per_cu = (160u * 1024u) / lds;
     if (per_cu < 1) per_cu = 1;
     if (per_cu > 8) per_cu = 8;
+    // LDS past 64 KiB per workgroup must be allowed per kernel (once; the
+    // largest size this instantiation meets)
+    if (lds > 64 * 1024) {
+        static std::mutex mu;
+        static size_t allowed = 0;
+        std::lock_guard<std::mutex> lk(mu);
+        if (lds > allowed) {
+            const hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                     (int)lds);
+            if (e != hipSuccess) return e;
+            allowed = lds;
+        }
+    }
     uint64_t blocks = (U + 3) / 4;
     const uint64_t cap = per_cu * (uint64_t)(cus > 0 ? cus : 256);
     if (blocks > cap) blocks = cap;
-    (void)launch_timed(kTimedAggSparse, aggregate_sparse<kTS, kS, kLanes, kRagged, kNT>, dim3((uint32_t)blocks),
-                       dim3(kBlock), lds, s, a, T, U, w, W, alpha, rp);
+    return launch_timed(kTimedAggSparse, kern, dim3((uint32_t)blocks), dim3(kBlock), lds, s, a, T, U, w, W, alpha,
+                        rp);
 }
 template <uint32_t kTS, bool kRagged, bool kNT>
-void launch_sparse_nt(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W, float alpha, int cus,
-                      const uint64_t* rp, hipStream_t s) {
+hipError_t launch_sparse_nt(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W, float alpha, int cus,
+                            const uint64_t* rp, hipStream_t s) {
     if constexpr (!kRagged) {
-        if (W > 64) {
-            launch_sparse_t<kTS, 16, false, false, kNT>(a, T, U, w, W, alpha, cus, rp, s);
-            return;
-        }
+        if (W > 64) return launch_sparse_t<kTS, 16, false, false, kNT>(a, T, U, w, W, alpha, cus, rp, s);
     }
-    if (W % 16 == 0 || W % 8 != 0) {
-        launch_sparse_t<kTS, 16, true, kRagged, kNT>(a, T, U, w, W, alpha, cus, rp, s);
-    } else {
-        launch_sparse_t<kTS, 8, true, kRagged, kNT>(a, T, U, w, W, alpha, cus, rp, s);
-    }
+    if (W % 16 == 0 || W % 8 != 0) return launch_sparse_t<kTS, 16, true, kRagged, kNT>(a, T, U, w, W, alpha, cus, rp, s);
+    return launch_sparse_t<kTS, 8, true, kRagged, kNT>(a, T, U, w, W, alpha, cus, rp, s);
 }
 // Outputs past this many tiles (256 MB at 4096 elements) are written with
 // the non-temporal hint.
 constexpr uint32_t kNtTiles = 16384;
 template <uint32_t kTS, bool kRagged>
-void launch_sparse_ts(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W, float alpha, int cus,
-                      const uint64_t* rp, hipStream_t s) {
+hipError_t launch_sparse_ts(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W, float alpha, int cus,
+                            const uint64_t* rp, hipStream_t s) {
     if ((uint64_t)U * kTS > (uint64_t)kNtTiles * 4096u)
-        launch_sparse_nt<kTS, kRagged, true>(a, T, U, w, W, alpha, cus, rp, s);
-    else
-        launch_sparse_nt<kTS, kRagged, false>(a, T, U, w, W, alpha, cus, rp, s);
+        return launch_sparse_nt<kTS, kRagged, true>(a, T, U, w, W, alpha, cus, rp, s);
+    return launch_sparse_nt<kTS, kRagged, false>(a, T, U, w, W, alpha, cus, rp, s);
 }
 }  // namespace
 
 hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t U, uint32_t tile, const uint64_t* w, int W,
                                    float alpha, int cus, const uint64_t* rp, hipStream_t s) {
     if (U == 0) return hipSuccess;
+    if (rp && W > 64) return hipErrorInvalidValue;
+    hipError_t e;
     if (rp) {
-        if (W > 64) return hipErrorInvalidValue;
-        if (tile == 4096u) launch_sparse_ts<4096u, true>(a, T, U, w, W, alpha, cus, rp, s);
-        else if (tile == 2048u) launch_sparse_ts<2048u, true>(a, T, U, w, W, alpha, cus, rp, s);
+        if (tile == 8192u) e = launch_sparse_ts<8192u, true>(a, T, U, w, W, alpha, cus, rp, s);
+        else if (tile == 4096u) e = launch_sparse_ts<4096u, true>(a, T, U, w, W, alpha, cus, rp, s);
+        else if (tile == 2048u) e = launch_sparse_ts<2048u, true>(a, T, U, w, W, alpha, cus, rp, s);
         else return hipErrorInvalidValue;
-        return hipGetLastError();
+    } else {
+        if (tile == 8192u) e = launch_sparse_ts<8192u, false>(a, T, U, w, W, alpha, cus, nullptr, s);
+        else if (tile == 4096u) e = launch_sparse_ts<4096u, false>(a, T, U, w, W, alpha, cus, nullptr, s);
+        else if (tile == 2048u) e = launch_sparse_ts<2048u, false>(a, T, U, w, W, alpha, cus, nullptr, s);
+        else return hipErrorInvalidValue;
     }
-    if (tile == 4096u) launch_sparse_ts<4096u, false>(a, T, U, w, W, alpha, cus, nullptr, s);
-    else if (tile == 2048u) launch_sparse_ts<2048u, false>(a, T, U, w, W, alpha, cus, nullptr, s);
-    else return hipErrorInvalidValue;
-    return hipGetLastError();
+    return e != hipSuccess ? e : hipGetLastError();
 }
 
 }  // namespace bc

@@ -105,6 +105,41 @@ def test_aggregate_part_matches_oracle(kind, W):
         assert B.bytecomp_device_status(ws) == 0
 
 
+def test_aggregate_part_large_tiles():
+    # parts totalling at least 2^24 elements at low density take the
+    # 8192-element tiles with ragged entry counts
+    import torch
+    from paper_2205_14465_amd import binding as B
+    rng = np.random.default_rng(8)
+    ns = [(1 << 25) + 4100, 3000]
+    ratio = 0.005
+    W = 12
+    off = O.sparse_offsets(ns, ratio)
+    pays = []
+    for w in range(W):
+        idx = [np.sort(rng.choice(n, size=int(O.k_for(n, ratio)), replace=False)).astype(np.uint32) for n in ns]
+        val = [rng.standard_normal(i.size).astype(np.float32) for i in idx]
+        pays.append({"idx": np.concatenate(idx), "val": np.concatenate(val), "off": off})
+    P = 2
+    bounds = [[0, (n // 2) // 32 * 32, n] for n in ns]
+    j = 0
+    lens = [b[j + 1] - b[j] for b in bounds]
+    assert sum(lens) >= 1 << 24
+    dev_parts, offs = [], []
+    for p in pays:
+        out, po = _gpu_pack("topk", ratio, ns, _dev_payload("topk", p), bounds, j)
+        dev_parts.append(out)
+        offs.append(po)
+    outs = [torch.full((n,), float("nan"), dtype=torch.float32, device="cuda") for n in lens]
+    ws = B.alloc_workspace("topk", ratio, lens, W)
+    B.bytecomp_aggregate_part("topk", ratio, dev_parts, offs, lens, outs, 1.0 / W, ws)
+    torch.cuda.synchronize()
+    want = O.aggregate_part_set("topk", lens, [O.pack_part_set("topk", ns, p, bounds, j) for p in pays], 1.0 / W)
+    for t in range(len(ns)):
+        assert np.array_equal(bits(outs[t].cpu().numpy()), bits(want[t])), t
+    assert B.bytecomp_device_status(ws) == 0
+
+
 @pytest.mark.parametrize("kind", ["topk", "sign"])
 def test_divisible_step_end_to_end(kind):
     """Node j's step for every j: aggregate the parts, compress the aggregate

@@ -225,6 +225,41 @@ def test_sparse_aggregate_several_tiles_per_wave(W):
         assert np.array_equal(bits(got[t]), bits(want[t])), t
 
 
+def _clustered_lists(rng, ns, counts, spread):
+    """One worker's payload whose indices crowd into the first `spread`
+    fraction of each tensor (dense windows: more than 128 entries per
+    8192-element tile)."""
+    idx, val = [], []
+    for n, k in zip(ns, counts):
+        span = max(int(k), int(n * spread))
+        idx.append(np.sort(rng.choice(span, size=int(k), replace=False)).astype(np.uint32))
+        val.append((rng.standard_normal(int(k))).astype(np.float32))
+    return idx, val
+
+
+@pytest.mark.parametrize("W", [24, 72])
+def test_sparse_aggregate_large_tiles(W):
+    # at least 2^24 elements at low density: 8192-element tiles, 128-entry
+    # windows; W = 24 takes 8-slot steps, W = 72 the LDS-held worker state;
+    # every fourth worker crowds its entries (dense windows, the slow path)
+    rng = np.random.default_rng(90 + W)
+    ns = [(1 << 24) + 12345, 7000, 1]
+    ratio = 0.01
+    counts = [O.k_for(n, ratio) for n in ns]
+    payloads = []
+    for w in range(W):
+        if w % 4 == 1:
+            idx, val = _clustered_lists(rng, ns, counts, 0.02)
+        else:
+            idx, val = WL.random_sparse_lists(rng, ns, counts)
+        payloads.append({"idx": np.concatenate(idx), "val": np.concatenate(val),
+                         "off": O.sparse_offsets(ns, ratio)})
+    got = gpu_aggregate("topk", ratio, ns, payloads, 1.0 / W)
+    want = O.aggregate_set("topk", ns, payloads, 1.0 / W)
+    for t in range(len(ns)):
+        assert np.array_equal(bits(got[t]), bits(want[t])), t
+
+
 def test_sparse_aggregate_dense_overlap():
     # every worker sends every index (ratio 1): maximal overlap, long runs
     rng = np.random.default_rng(23)

@@ -325,6 +325,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     }
 }
 
+// Slots of the one-pass kernel to empty before it runs (a fill kernel).
 __global__ void quant_onepass_reset(uint32_t C, Ws ws) {
     for (uint32_t c = blockIdx.x * blockDim.x + threadIdx.x; c < C; c += gridDim.x * blockDim.x) ws.q_slot[c] = 0u;
 }
@@ -488,10 +489,10 @@ bool quant_onepass_launch(uint64_t seed, const TDesc* d, int T, uint32_t C, uint
     const uint32_t cap = quant_onepass_capacity<kBits>(cus);
     if (C == 0 || cap == 0 || max_chunks > cap) return false;
     const uint32_t grid = C < cap ? C : cap;
-    (void)launch_timed(kTimedQuantPass1, quant_onepass<kBits>, dim3(grid), dim3(kBlock), 0, s, d, T, C, seed, words,
-                       scale, ws);
     hipLaunchKernelGGL(quant_onepass_reset, dim3((C + 255) / 256 < 1024 ? (C + 255) / 256 : 1024), dim3(256), 0, s,
                        C, ws);
+    (void)launch_timed(kTimedQuantPass1, quant_onepass<kBits>, dim3(grid), dim3(kBlock), 0, s, d, T, C, seed, words,
+                       scale, ws);
     if (any_empty) hipLaunchKernelGGL(quant_empty_scales, dim3((T + 255) / 256), dim3(256), 0, s, d, T, scale);
     return true;
 }

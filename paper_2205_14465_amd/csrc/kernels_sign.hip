@@ -144,8 +144,10 @@ __global__ __launch_bounds__(kBlock) void sign_pass2(const TDesc* __restrict__ d
 // --------------------------------------------------------------- one pass
 // Chunk partial sums travel through slots that hold the bitwise complement
 // of the fp64 partial once published and 0 before (a sum of magnitudes is
-// never all ones), so a slot needs no separate ready flag and a zeroed
-// workspace starts every slot empty.  A workgroup writes chunk c's
+// never all ones), so a slot needs no separate ready flag.  A fill kernel
+// empties the slots just before the one-pass kernel runs, so whatever an
+// earlier call (of any kind sharing the workspace) left there does not
+// matter.  A workgroup writes chunk c's
 // residual only after publishing chunk c + grid (and prefetching its next
 // chunk): it then reads all its tensor's slots, waiting while any is
 // empty, and sums them in the fixed order of the two-pass path.
@@ -259,8 +261,8 @@ __global__ void sign_empty_scales(const TDesc* __restrict__ d, int T, float* __r
     if (t < T && d[t].nchunks == 0) scale_out[t] = 0.f;
 }
 
-// Slots of the one-pass kernel back to empty for the next call (a fill
-// kernel, not a memset, so that the sequence stays capturable).
+// Slots of the one-pass kernel to empty before it runs (a fill kernel, not
+// a memset, so that the sequence stays capturable).
 __global__ void sign_onepass_reset(uint32_t C, Ws ws) {
     for (uint32_t c = blockIdx.x * blockDim.x + threadIdx.x; c < C; c += gridDim.x * blockDim.x)
         ws.s_slot[c] = 0ull;
@@ -315,9 +317,9 @@ hipError_t launch_sign_compress(const TDesc* d, int T, uint32_t C, uint32_t max_
     const uint32_t cap = onepass_capacity(cus);
     if (C > 0 && cap > 0 && max_chunks <= cap) {
         const uint32_t grid = C < cap ? C : cap;
-        (void)launch_timed(kTimedSignPass1, sign_onepass, dim3(grid), dim3(kBlock), 0, s, d, T, C, bits, scale, ws);
         hipLaunchKernelGGL(sign_onepass_reset, dim3((C + 255) / 256 < 1024 ? (C + 255) / 256 : 1024), dim3(256), 0, s,
                            C, ws);
+        (void)launch_timed(kTimedSignPass1, sign_onepass, dim3(grid), dim3(kBlock), 0, s, d, T, C, bits, scale, ws);
         if (any_empty) hipLaunchKernelGGL(sign_empty_scales, dim3((T + 255) / 256), dim3(256), 0, s, d, T, scale);
         return hipGetLastError();
     }

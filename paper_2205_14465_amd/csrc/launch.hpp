@@ -21,12 +21,12 @@ struct Ws {
     double* s_partial;      // [C] per-chunk sums of |v|
     uint32_t* s_info;       // [T] aggregate: form (bits 0-7), smallest scale exponent (8-15)
     uint64_t* s_slot;       // [C] one-pass compress: ~bits of each chunk's partial sum once
-                            // published, 0 otherwise (0 between calls)
+                            // published, 0 otherwise (emptied before the kernel runs)
     int32_t* s_tab;         // [T * 2048] aggregate: int32 lookup tables of each tensor
     // BC_TERNGRAD, BC_QSGD4, BC_QSGD8 (and s_val)
     uint32_t* q_max;        // [C] largest |v| bits of each chunk
     uint32_t* q_slot;       // [C] one-pass compress: those bits | 1 << 31 once published, 0 otherwise
-                            // (0 between calls)
+                            // (emptied before the kernel runs)
     // BC_TOPK, BC_TOPK_SAMPLED
     uint32_t* t_hist;       // [T * 2048] histograms         
     uint32_t* t_thr;        // [T] candidate threshold (key)

@@ -25,8 +25,10 @@ def to_np_u32(t):
 WORD_KINDS = ("sign", "terngrad", "qsgd4", "qsgd8")  # packed words + scales
 
 
-def gpu_compress(kind, ratio, seed, grads, resids, tensor_ids=None):
-    """Returns (payload dict of numpy arrays, list of new residuals or None)."""
+def gpu_compress(kind, ratio, seed, grads, resids, tensor_ids=None, ws_fill=None):
+    """Returns (payload dict of numpy arrays, list of new residuals or None).
+    ws_fill: byte that fills the workspace before its header is initialised
+    (what an earlier call sharing the workspace might have left there)."""
     import torch
     from paper_2205_14465_amd import binding as B
     ns = [g.size for g in grads]
@@ -34,6 +36,9 @@ def gpu_compress(kind, ratio, seed, grads, resids, tensor_ids=None):
     de = None if resids is None else [torch_dev(np.asarray(e, np.float32)) for e in resids]
     out = B.alloc_payload(kind, ratio, ns)
     ws = B.alloc_workspace(kind, ratio, ns, 1)
+    if ws_fill is not None:
+        ws.fill_(ws_fill)
+        B.bytecomp_workspace_init(ws)
     B.bytecomp_compress(kind, ratio, seed, dg, de, out, ws, tensor_ids=tensor_ids)
     torch.cuda.synchronize()
     assert B.bytecomp_device_status(ws) == 0

@@ -174,6 +174,26 @@ def test_sign_fp16_subnormals_exact():
     assert_resid_equal(got_e, want_e)
 
 
+@pytest.mark.parametrize("kind", ["sign", "terngrad", "qsgd8"])
+@pytest.mark.parametrize("fill", [0xA5, 0xFF])
+def test_one_pass_compress_ignores_stale_workspace(kind, fill):
+    # the one-pass kernels read their chunk slots as published when they
+    # are nonzero; a workspace body left dirty by an earlier call (here
+    # every byte `fill`, the header initialised) must not change a result
+    rng = np.random.default_rng(29)
+    ns = [4096 * 40 + 3, 5000, 1, 0, 4096]
+    grads, resids = make_set(ns, rng)
+    got, got_e = gpu_compress(kind, 0.01, SEED, grads, resids, ws_fill=fill)
+    want, want_e = O.compress_set(kind, 0.01, SEED, grads, resids)
+    if kind == "sign":
+        assert_sign_close(got, want, grads, resids, got_e, want_e)
+    else:
+        assert np.array_equal(got["off"], want["off"])
+        assert np.array_equal(got["bits"], want["bits"])
+        assert np.array_equal(bits(got["scale"]), bits(want["scale"]))
+        assert_resid_equal(got_e, want_e)
+
+
 def test_compress_is_deterministic():
     rng = np.random.default_rng(19)
     ns = [4096 * 300 + 5, 77]

@@ -457,7 +457,7 @@ int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t,
     const TDesc* dd = (const TDesc*)en->dev;
     switch (kind) {
         case BC_SIGN1:
-            e = launch_sign_compress(dd, T, C, maxc, di.any_empty, out.bits, out.scale, w, di.cus, s);
+            e = launch_sign_compress(dd, T, C, maxc, di.any_empty, a16, a32, out.bits, out.scale, w, di.cus, s);
             break;
         case BC_TOPK:
         case BC_TOPK_SAMPLED:
@@ -467,8 +467,8 @@ int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t,
         case BC_TERNGRAD:
         case BC_QSGD4:
         case BC_QSGD8:
-            e = launch_quant_compress(quant_bits(kind), seed, dd, T, C, maxc, di.any_empty, out.bits, out.scale,
-                                      w, di.cus, s);
+            e = launch_quant_compress(quant_bits(kind), seed, dd, T, C, maxc, di.any_empty, a16, a32, out.bits,
+                                      out.scale, w, di.cus, s);
             break;
         default:
             e = launch_randk(seed, dd, T, C, sum_k, a16, a32, out.idx, out.val, w, s);

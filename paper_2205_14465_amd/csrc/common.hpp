@@ -145,6 +145,23 @@ __device__ __forceinline__ int wave_id() {
 }
 
 // ----------------------------------------------------------- chunk loading
+// A chunk that lies wholly inside its tensor (every chunk but a tensor's
+// last, in general) is read by straight-line code that issues all of a
+// thread's vector loads before it uses any of them, so that they are in
+// flight together; the per-element path serves the tensor's last chunk.
+// The test is uniform over the workgroup (one chunk, one tensor).
+__device__ __forceinline__ bool whole_chunk(const TDesc& td, uint32_t j) {
+    return (uint64_t)j * kChunk + kChunk <= td.n;
+}
+
+// Widened gradient element q (0..3) of a thread's round: fp32 bits, or the
+// fp16 halves of two packed words.
+template <int DT>
+__device__ __forceinline__ float g_elem(const f32x4& gf, const u32x2& gh, int q) {
+    if constexpr (DT == 0) return gf[q];
+    else return h2f(((q < 2 ? gh.x : gh.y) >> (16 * (q & 1))) & 0xFFFFu);
+}
+
 // Load the 16 elements a thread owns of chunk `j` of tensor `td`, forming
 // v = widen(g) + e (e = 0 when there is no residual or `use_resid` is
 // false).  Elements past the tensor's end read as +0.0 and are reported
@@ -154,6 +171,32 @@ __device__ __forceinline__ void load_chunk(const TDesc& td, uint32_t j, bool use
                                            float v[kEpt], uint32_t& valid) {
     const uint32_t base = j * (uint32_t)kChunk;
     const uint32_t n = td.n;
+    if (whole_chunk(td, j)) {
+        f32x4 gf[kRounds];
+        u32x2 gh[kRounds];
+        const uint32_t e0 = base + 4u * threadIdx.x;
+#pragma unroll
+        for (int r = 0; r < kRounds; ++r) {
+            if constexpr (DT == 0) gf[r] = ldg4f_s<kNT>((const float*)td.grad + e0 + 1024u * r);
+            else gh[r] = ldg2u_s<kNT>((const uint16_t*)td.grad + e0 + 1024u * r);
+        }
+        if (use_resid) {
+            f32x4 ev[kRounds];
+#pragma unroll
+            for (int r = 0; r < kRounds; ++r) ev[r] = ldg4f_s<kNT>(td.resid + e0 + 1024u * r);
+#pragma unroll
+            for (int r = 0; r < kRounds; ++r)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) v[4 * r + q] = g_elem<DT>(gf[r], gh[r], q) + ev[r][q];
+        } else {
+#pragma unroll
+            for (int r = 0; r < kRounds; ++r)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) v[4 * r + q] = g_elem<DT>(gf[r], gh[r], q);
+        }
+        valid = 0xFFFFu;
+        return;
+    }
     valid = 0;
 #pragma unroll
     for (int r = 0; r < kRounds; ++r) {
@@ -201,58 +244,84 @@ __device__ __forceinline__ void load_v(const TDesc& td, uint32_t j, bool use_res
 }
 
 // Raw chunk data held in registers between issuing the loads and using
-// them (lets a kernel prefetch its next chunk before a wait).  g[i] holds
-// element i's fp32 bits or, for fp16 gradients, its 16 bits.
+// them (lets a kernel prefetch its next chunk before a wait).  g[4r + q]
+// holds element 4r + q's fp32 bits or, for fp16 gradients, g[4r] and
+// g[4r + 1] hold round r's four elements as packed halves (low half
+// first); e is written only when the residual is read.
 struct RawChunk {
     uint32_t g[kEpt];
     float e[kEpt];
     uint32_t valid;
 };
 
+// kDT: 0 every tensor of the call is fp32, 1 every tensor is fp16, 2 both
+// occur (td.dtype decides).  A kernel that keeps loads in flight across
+// iterations is instantiated per kDT so that the common single-dtype calls
+// have one load sequence (no merge of two register sets that would make
+// the compiler wait for the loads).
+template <int kDT>
 __device__ __forceinline__ void load_raw(const TDesc& td, uint32_t j, bool use_resid, RawChunk& r) {
-    const uint32_t base = j * (uint32_t)kChunk;
-    const uint32_t n = td.n;
-    r.valid = 0;
+    if constexpr (kDT == 2) {
+        if (td.dtype == 0) load_raw<0>(td, j, use_resid, r);
+        else load_raw<1>(td, j, use_resid, r);
+    } else {
+        const uint32_t base = j * (uint32_t)kChunk;
+        const uint32_t n = td.n;
+        if (whole_chunk(td, j)) {
+            const uint32_t e0 = base + 4u * threadIdx.x;
 #pragma unroll
-    for (int rr = 0; rr < kRounds; ++rr) {
-        const uint32_t e0 = base + 1024u * rr + 4u * threadIdx.x;
-        if (e0 + 3 < n) {
-            if (td.dtype == 0) {
-                const u32x4 x = ldg4u((const float*)td.grad + e0);
-                r.g[4 * rr] = x.x; r.g[4 * rr + 1] = x.y; r.g[4 * rr + 2] = x.z; r.g[4 * rr + 3] = x.w;
-            } else {
-                const u32x2 h = ldg2u((const uint16_t*)td.grad + e0);
-                r.g[4 * rr] = h.x & 0xFFFFu; r.g[4 * rr + 1] = h.x >> 16;
-                r.g[4 * rr + 2] = h.y & 0xFFFFu; r.g[4 * rr + 3] = h.y >> 16;
+            for (int rr = 0; rr < kRounds; ++rr) {
+                if constexpr (kDT == 0) {
+                    const u32x4 x = ldg4u((const float*)td.grad + e0 + 1024u * rr);
+                    r.g[4 * rr] = x.x; r.g[4 * rr + 1] = x.y; r.g[4 * rr + 2] = x.z; r.g[4 * rr + 3] = x.w;
+                } else {
+                    const u32x2 h = ldg2u((const uint16_t*)td.grad + e0 + 1024u * rr);
+                    r.g[4 * rr] = h.x;
+                    r.g[4 * rr + 1] = h.y;
+                }
             }
             if (use_resid) {
-                const f32x4 y = ldg4f(td.resid + e0);
-                r.e[4 * rr] = y.x; r.e[4 * rr + 1] = y.y; r.e[4 * rr + 2] = y.z; r.e[4 * rr + 3] = y.w;
+#pragma unroll
+                for (int rr = 0; rr < kRounds; ++rr) {
+                    const f32x4 y = ldg4f(td.resid + e0 + 1024u * rr);
+                    r.e[4 * rr] = y.x; r.e[4 * rr + 1] = y.y; r.e[4 * rr + 2] = y.z; r.e[4 * rr + 3] = y.w;
+                }
             }
-            r.valid |= 0xFu << (4 * rr);
-        } else {
+            r.valid = 0xFFFFu;
+            return;
+        }
+        r.valid = 0;
+#pragma unroll
+        for (int rr = 0; rr < kRounds; ++rr) {
+            const uint32_t e0 = base + 1024u * rr + 4u * threadIdx.x;
+            if constexpr (kDT == 1) {
+                r.g[4 * rr] = 0u;
+                r.g[4 * rr + 1] = 0u;
+            }
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 const bool ok = e0 + q < n;
-                if (td.dtype == 0) r.g[4 * rr + q] = ok ? gp((const uint32_t*)td.grad)[e0 + q] : 0u;
-                else r.g[4 * rr + q] = ok ? (uint32_t)gp((const uint16_t*)td.grad)[e0 + q] : 0u;
+                if constexpr (kDT == 0) {
+                    r.g[4 * rr + q] = ok ? gp((const uint32_t*)td.grad)[e0 + q] : 0u;
+                } else {
+                    const uint32_t hb = ok ? (uint32_t)gp((const uint16_t*)td.grad)[e0 + q] : 0u;
+                    r.g[4 * rr + (q >> 1)] |= hb << (16 * (q & 1));
+                }
                 if (use_resid) r.e[4 * rr + q] = ok ? gp(td.resid)[e0 + q] : 0.f;
                 r.valid |= (ok ? 1u : 0u) << (4 * rr + q);
             }
-        }
-        if (!use_resid) {
-#pragma unroll
-            for (int q = 0; q < 4; ++q) r.e[4 * rr + q] = 0.f;
         }
     }
 }
 
 // v = widen(g) + e from a RawChunk (e = 0 without residual), exactly as
 // load_v forms it; elements past the tensor's end read as +0.0.
+template <int kDT>
 __device__ __forceinline__ void raw_to_v(const TDesc& td, bool use_resid, const RawChunk& r, float v[kEpt]) {
+    const bool f16 = kDT == 1 || (kDT == 2 && td.dtype != 0);
 #pragma unroll
     for (int i = 0; i < kEpt; ++i) {
-        float g = td.dtype == 0 ? u2f(r.g[i]) : h2f(r.g[i]);
+        float g = f16 ? h2f((r.g[(i & ~3) + ((i >> 1) & 1)] >> (16 * (i & 1))) & 0xFFFFu) : u2f(r.g[i]);
         g = ((r.valid >> i) & 1u) ? g : 0.f;
         v[i] = use_resid ? g + r.e[i] : g;
     }
@@ -264,6 +333,17 @@ __device__ __forceinline__ void load_stored_v(const TDesc& td, uint32_t j, float
                                               uint32_t& valid) {
     if (td.resid) {
         const uint32_t base = j * (uint32_t)kChunk;
+        if (whole_chunk(td, j)) {
+            f32x4 y[kRounds];
+#pragma unroll
+            for (int r = 0; r < kRounds; ++r) y[r] = ldg4f(td.resid + base + 1024u * r + 4u * threadIdx.x);
+#pragma unroll
+            for (int r = 0; r < kRounds; ++r)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) v[4 * r + q] = y[r][q];
+            valid = 0xFFFFu;
+            return;
+        }
         valid = 0;
 #pragma unroll
         for (int r = 0; r < kRounds; ++r) {
@@ -292,6 +372,13 @@ __device__ __forceinline__ void load_stored_v(const TDesc& td, uint32_t j, float
 template <bool kNT = false>
 __device__ __forceinline__ void store_chunk(float* dst, uint32_t n, uint32_t j, const float v[kEpt]) {
     const uint32_t base = j * (uint32_t)kChunk;
+    if ((uint64_t)base + kChunk <= n) {
+#pragma unroll
+        for (int r = 0; r < kRounds; ++r)
+            stg4f_s<kNT>(dst + base + 1024u * r + 4u * threadIdx.x,
+                         f32x4{v[4 * r], v[4 * r + 1], v[4 * r + 2], v[4 * r + 3]});
+        return;
+    }
 #pragma unroll
     for (int r = 0; r < kRounds; ++r) {
         const uint32_t e0 = base + 1024u * r + 4u * threadIdx.x;

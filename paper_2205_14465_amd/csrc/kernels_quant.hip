@@ -257,7 +257,7 @@ __device__ __forceinline__ float quant_onepass_scale(const TDesc& td, uint32_t* 
 }
 }  // namespace
 
-template <int kBits>
+template <int kBits, int kDT>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void quant_onepass(const TDesc* __restrict__ d, int T, uint32_t C, uint64_t seed,
                                                         uint32_t* __restrict__ words, float* __restrict__ scale_out,
                                                         Ws ws) {
@@ -273,7 +273,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     TDesc td{};
     if (c < C) {
         td = d[tensor_of_chunk(d, T, c)];
-        load_raw(td, c - td.chunk0, td.resid != nullptr, raw);
+        load_raw<kDT>(td, c - td.chunk0, td.resid != nullptr, raw);
     }
     for (;; c += gridDim.x) {
         const bool have = c < C;
@@ -283,7 +283,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
         if (have) {
             const int t = tensor_of_chunk(d, T, c);
             j = c - td.chunk0;
-            raw_to_v(td, td.resid != nullptr, raw, v);
+            raw_to_v<kDT>(td, td.resid != nullptr, raw, v);
             uint32_t mk = 0;
 #pragma unroll
             for (int i = 0; i < kEpt; ++i) {
@@ -303,7 +303,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
         TDesc tdn{};
         if (cn < C) {
             tdn = d[tensor_of_chunk(d, T, cn)];
-            load_raw(tdn, cn - tdn.chunk0, tdn.resid != nullptr, raw);
+            load_raw<kDT>(tdn, cn - tdn.chunk0, tdn.resid != nullptr, raw);
         }
         if (prev) {
             float m = mp;
@@ -472,40 +472,52 @@ void quant_compress_bits(const TDesc* d, int T, uint32_t C, bool nt, uint64_t se
 }  // namespace
 
 namespace {
-template <int kBits>
+template <int kBits, int kDT>
 uint32_t quant_onepass_capacity(int cus) {
     static int per_cu = -1;
     if (per_cu < 0) {
         int nb = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, quant_onepass<kBits>, kBlock, 0) != hipSuccess) nb = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, quant_onepass<kBits, kDT>, kBlock, 0) != hipSuccess)
+            nb = 0;
         per_cu = nb;
     }
     return (uint32_t)per_cu * (uint32_t)(cus > 0 ? cus : 0);
 }
 
-template <int kBits>
+template <int kBits, int kDT>
 bool quant_onepass_launch(uint64_t seed, const TDesc* d, int T, uint32_t C, uint32_t max_chunks, bool any_empty,
                           uint32_t* words, float* scale, const Ws& ws, int cus, hipStream_t s) {
-    const uint32_t cap = quant_onepass_capacity<kBits>(cus);
+    const uint32_t cap = quant_onepass_capacity<kBits, kDT>(cus);
     if (C == 0 || cap == 0 || max_chunks > cap) return false;
     const uint32_t grid = C < cap ? C : cap;
     hipLaunchKernelGGL(quant_onepass_reset, dim3((C + 255) / 256 < 1024 ? (C + 255) / 256 : 1024), dim3(256), 0, s,
                        C, ws);
-    (void)launch_timed(kTimedQuantPass1, quant_onepass<kBits>, dim3(grid), dim3(kBlock), 0, s, d, T, C, seed, words,
-                       scale, ws);
+    (void)launch_timed(kTimedQuantPass1, quant_onepass<kBits, kDT>, dim3(grid), dim3(kBlock), 0, s, d, T, C, seed,
+                       words, scale, ws);
     if (any_empty) hipLaunchKernelGGL(quant_empty_scales, dim3((T + 255) / 256), dim3(256), 0, s, d, T, scale);
     return true;
+}
+
+template <int kBits>
+bool quant_onepass_dt(uint64_t seed, const TDesc* d, int T, uint32_t C, uint32_t max_chunks, bool any_empty,
+                      bool any_f16, bool any_f32, uint32_t* words, float* scale, const Ws& ws, int cus,
+                      hipStream_t s) {
+    if (any_f16 && any_f32)
+        return quant_onepass_launch<kBits, 2>(seed, d, T, C, max_chunks, any_empty, words, scale, ws, cus, s);
+    if (any_f16) return quant_onepass_launch<kBits, 1>(seed, d, T, C, max_chunks, any_empty, words, scale, ws, cus, s);
+    return quant_onepass_launch<kBits, 0>(seed, d, T, C, max_chunks, any_empty, words, scale, ws, cus, s);
 }
 }  // namespace
 
 hipError_t launch_quant_compress(int bits, uint64_t seed, const TDesc* d, int T, uint32_t C, uint32_t max_chunks,
-                                 bool any_empty, uint32_t* words, float* scale, const Ws& ws, int cus,
-                                 hipStream_t s) {
+                                 bool any_empty, bool any_f16, bool any_f32, uint32_t* words, float* scale,
+                                 const Ws& ws, int cus, hipStream_t s) {
     if (T <= 0) return hipSuccess;
     // one pass when every tensor fits the resident grid
-    const bool one = bits == 2   ? quant_onepass_launch<2>(seed, d, T, C, max_chunks, any_empty, words, scale, ws, cus, s)
-                     : bits == 4 ? quant_onepass_launch<4>(seed, d, T, C, max_chunks, any_empty, words, scale, ws, cus, s)
-                                 : quant_onepass_launch<8>(seed, d, T, C, max_chunks, any_empty, words, scale, ws, cus, s);
+    const bool one =
+        bits == 2   ? quant_onepass_dt<2>(seed, d, T, C, max_chunks, any_empty, any_f16, any_f32, words, scale, ws, cus, s)
+        : bits == 4 ? quant_onepass_dt<4>(seed, d, T, C, max_chunks, any_empty, any_f16, any_f32, words, scale, ws, cus, s)
+                    : quant_onepass_dt<8>(seed, d, T, C, max_chunks, any_empty, any_f16, any_f32, words, scale, ws, cus, s);
     if (one) return hipGetLastError();
     const bool nt = C > kNtChunks;
     if (C > 0) {

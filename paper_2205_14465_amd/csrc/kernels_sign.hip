@@ -194,7 +194,8 @@ __device__ __forceinline__ float onepass_scale(const TDesc& td, uint64_t* slot, 
 }
 }  // namespace
 
-__global__ __launch_bounds__(kBlock) void sign_onepass(const TDesc* __restrict__ d, int T, uint32_t C,
+template <int kDT>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) void sign_onepass(const TDesc* __restrict__ d, int T, uint32_t C,
                                                        uint32_t* __restrict__ bits, float* __restrict__ scale_out,
                                                        Ws ws) {
     __shared__ double sh[4];
@@ -208,7 +209,7 @@ __global__ __launch_bounds__(kBlock) void sign_onepass(const TDesc* __restrict__
     TDesc td{};
     if (c < C) {
         td = d[tensor_of_chunk(d, T, c)];
-        load_raw(td, c - td.chunk0, td.resid != nullptr, raw);
+        load_raw<kDT>(td, c - td.chunk0, td.resid != nullptr, raw);
     }
     for (;; c += gridDim.x) {
         const bool have = c < C;
@@ -218,7 +219,7 @@ __global__ __launch_bounds__(kBlock) void sign_onepass(const TDesc* __restrict__
         if (have) {
             const int t = tensor_of_chunk(d, T, c);
             j = c - td.chunk0;
-            raw_to_v(td, td.resid != nullptr, raw, v);
+            raw_to_v<kDT>(td, td.resid != nullptr, raw, v);
             store_sign_words(v, bits + td.off + (uint64_t)j * kChunkWords, chunk_words(td, j));
             const double p = block_sum_f64(thread_abs_sum(v), sh);
             if (td.nchunks == 1) {
@@ -234,7 +235,7 @@ __global__ __launch_bounds__(kBlock) void sign_onepass(const TDesc* __restrict__
         TDesc tdn{};
         if (cn < C) {
             tdn = d[tensor_of_chunk(d, T, cn)];
-            load_raw(tdn, cn - tdn.chunk0, tdn.resid != nullptr, raw);
+            load_raw<kDT>(tdn, cn - tdn.chunk0, tdn.resid != nullptr, raw);
         }
         if (prev) {
             float s = sp;
@@ -298,31 +299,41 @@ __global__ __launch_bounds__(kBlock) void sign_residual_update(const TDesc* __re
 
 // ------------------------------------------------------------- launchers
 namespace {
-// Workgroups of sign_onepass resident at once on the whole GPU.
+// Workgroups of sign_onepass<kDT> resident at once on the whole GPU.
+template <int kDT>
 uint32_t onepass_capacity(int cus) {
     static int per_cu = -1;
     if (per_cu < 0) {
         int nb = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, sign_onepass, kBlock, 0) != hipSuccess) nb = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, sign_onepass<kDT>, kBlock, 0) != hipSuccess) nb = 0;
         per_cu = nb;
     }
     return (uint32_t)per_cu * (uint32_t)(cus > 0 ? cus : 0);
 }
+
+// One pass when every tensor fits the resident grid; false otherwise.
+template <int kDT>
+bool sign_onepass_launch(const TDesc* d, int T, uint32_t C, uint32_t max_chunks, bool any_empty, uint32_t* bits,
+                         float* scale, const Ws& ws, int cus, hipStream_t s) {
+    const uint32_t cap = onepass_capacity<kDT>(cus);
+    if (C == 0 || cap == 0 || max_chunks > cap) return false;
+    const uint32_t grid = C < cap ? C : cap;
+    hipLaunchKernelGGL(sign_onepass_reset, dim3((C + 255) / 256 < 1024 ? (C + 255) / 256 : 1024), dim3(256), 0, s,
+                       C, ws);
+    (void)launch_timed(kTimedSignPass1, sign_onepass<kDT>, dim3(grid), dim3(kBlock), 0, s, d, T, C, bits, scale, ws);
+    if (any_empty) hipLaunchKernelGGL(sign_empty_scales, dim3((T + 255) / 256), dim3(256), 0, s, d, T, scale);
+    return true;
+}
 }  // namespace
 
 hipError_t launch_sign_compress(const TDesc* d, int T, uint32_t C, uint32_t max_chunks, bool any_empty,
-                                uint32_t* bits, float* scale, const Ws& ws, int cus, hipStream_t s) {
+                                bool any_f16, bool any_f32, uint32_t* bits, float* scale, const Ws& ws, int cus,
+                                hipStream_t s) {
     if (T <= 0) return hipSuccess;
-    // one pass when every tensor fits the resident grid
-    const uint32_t cap = onepass_capacity(cus);
-    if (C > 0 && cap > 0 && max_chunks <= cap) {
-        const uint32_t grid = C < cap ? C : cap;
-        hipLaunchKernelGGL(sign_onepass_reset, dim3((C + 255) / 256 < 1024 ? (C + 255) / 256 : 1024), dim3(256), 0, s,
-                           C, ws);
-        (void)launch_timed(kTimedSignPass1, sign_onepass, dim3(grid), dim3(kBlock), 0, s, d, T, C, bits, scale, ws);
-        if (any_empty) hipLaunchKernelGGL(sign_empty_scales, dim3((T + 255) / 256), dim3(256), 0, s, d, T, scale);
-        return hipGetLastError();
-    }
+    const bool one = any_f16 && any_f32 ? sign_onepass_launch<2>(d, T, C, max_chunks, any_empty, bits, scale, ws, cus, s)
+                     : any_f16          ? sign_onepass_launch<1>(d, T, C, max_chunks, any_empty, bits, scale, ws, cus, s)
+                                        : sign_onepass_launch<0>(d, T, C, max_chunks, any_empty, bits, scale, ws, cus, s);
+    if (one) return hipGetLastError();
     // past the cache size: stream g and e_old past the cache, keep v (re-read
     // by pass 2) in it, and stream e_new out
     const bool nt = C > kNtChunks;

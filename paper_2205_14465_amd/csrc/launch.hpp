@@ -96,7 +96,8 @@ constexpr uint32_t kNtChunks = 8192;
 // ------------------------------------------------------------- launchers
 // d: device TDesc[T]; C: total chunks.  Return the first HIP error.
 hipError_t launch_sign_compress(const TDesc* d, int T, uint32_t C, uint32_t max_chunks, bool any_empty,
-                                uint32_t* bits, float* scale, const Ws& ws, int cus, hipStream_t s);
+                                bool any_f16, bool any_f32, uint32_t* bits, float* scale, const Ws& ws, int cus,
+                                hipStream_t s);
 hipError_t launch_topk(int kind, double ratio, uint64_t seed, const TDesc* d, int T, uint32_t C,
                        bool any_f16, bool any_f32, uint32_t* idx, float* val, const Ws& ws,
                        hipStream_t s);
@@ -117,7 +118,8 @@ hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t units, const ui
                                  float alpha, uint32_t* info, int32_t* tabs, hipStream_t s);
 // Stochastic b-bit quantizers (bits 2, 4 or 8).
 hipError_t launch_quant_compress(int bits, uint64_t seed, const TDesc* d, int T, uint32_t C, uint32_t max_chunks,
-                                 bool any_empty, uint32_t* words, float* scale, const Ws& ws, int cus, hipStream_t s);
+                                 bool any_empty, bool any_f16, bool any_f32, uint32_t* words, float* scale,
+                                 const Ws& ws, int cus, hipStream_t s);
 hipError_t launch_quant_residual_update(int bits, const TDesc* d, int T, uint32_t C, const uint32_t* words,
                                         const float* scale, hipStream_t s);
 // DGC momentum correction (d: tensors with resid = the velocity u) and

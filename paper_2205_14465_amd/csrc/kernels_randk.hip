@@ -238,6 +238,37 @@ __global__ __launch_bounds__(kGenBlock) void randk_place(const TDesc* __restrict
 // of the chunk, writes e_new (selected entries zeroed) and emits its
 // selected (index, v) pairs at positions from a wave prefix over the
 // rounds, which is ascending index order.
+namespace {
+// v = widen(g) + e (or widen(g)) for the 32 elements a lane owns of the
+// 2048 elements from `lo` (all inside the tensor): element 256 r + 4 lane + i
+// at v[4 r + i].
+template <int DT, bool kNT>
+__device__ __forceinline__ void half_loads(const TDesc& td, uint32_t lo, int lane, bool use_e, float (&v)[32]) {
+    const uint32_t e0 = lo + 4u * (uint32_t)lane;
+    f32x4 gf[8];
+    u32x2 gh[8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+        if constexpr (DT == 0) gf[r] = ldg4f_s<kNT>((const float*)td.grad + e0 + 256u * r);
+        else gh[r] = ldg2u_s<kNT>((const uint16_t*)td.grad + e0 + 256u * r);
+    }
+    if (use_e) {
+        f32x4 ev[8];
+#pragma unroll
+        for (int r = 0; r < 8; ++r) ev[r] = ldg4f_s<kNT>(td.resid + e0 + 256u * r);
+#pragma unroll
+        for (int r = 0; r < 8; ++r)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) v[4 * r + i] = g_elem<DT>(gf[r], gh[r], i) + ev[r][i];
+    } else {
+#pragma unroll
+        for (int r = 0; r < 8; ++r)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) v[4 * r + i] = g_elem<DT>(gf[r], gh[r], i);
+    }
+}
+}  // namespace
+
 template <bool kNT>
 __global__ __launch_bounds__(kBlock) void randk_stream(const TDesc* __restrict__ d, int T, uint32_t C,
                                                        uint32_t S, uint32_t* __restrict__ idx,
@@ -300,8 +331,15 @@ __global__ __launch_bounds__(kBlock) void randk_stream(const TDesc* __restrict__
             const uint32_t lo = j * (uint32_t)kChunk + 2048u * half;
             float v[32];
             uint32_t valid = 0;
+            const bool whole = (uint64_t)lo + 2048u <= td.n;
+            if (whole) {
+                // straight-line: every load of the half is issued before any is used
+                if (td.dtype == 0) half_loads<0, kNT>(td, lo, lane, use_e, v);
+                else half_loads<1, kNT>(td, lo, lane, use_e, v);
+                valid = 0xFFFFFFFFu;
+            }
 #pragma unroll
-            for (int r = 0; r < 8; ++r) {
+            for (int r = 0; r < 8 && !whole; ++r) {
                 const uint32_t e0 = lo + 256u * r + 4u * (uint32_t)lane;
                 float g4[4] = {0.f, 0.f, 0.f, 0.f}, e4[4] = {0.f, 0.f, 0.f, 0.f};
                 if (e0 + 3 < td.n) {
@@ -348,7 +386,7 @@ __global__ __launch_bounds__(kBlock) void randk_stream(const TDesc* __restrict__
                     float o[4];
 #pragma unroll
                     for (int i = 0; i < 4; ++i) o[i] = ((pm >> (4 * r + i)) & 1u) ? 0.f : v[4 * r + i];
-                    if (e0 + 3 < td.n) {
+                    if (whole || e0 + 3 < td.n) {
                         stg4f_s<kNT>(td.resid + e0, f32x4{o[0], o[1], o[2], o[3]});
                     } else {
 #pragma unroll

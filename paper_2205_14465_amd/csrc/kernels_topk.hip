@@ -324,22 +324,39 @@ __global__ __launch_bounds__(kBlock) void topk_cand_hist(const TDesc* __restrict
     flush_hist(lh, ws.t_hist + (size_t)t * kBins0, kBins12);
 }
 
-// Per chunk: candidates above tau and equal to tau, one wave per chunk,
-// counted with ballots.
+// Per chunk: candidates above tau and equal to tau, counted with ballots;
+// each wave takes kCountChunks consecutive chunks, whose loads it issues
+// together (one chunk per wave for calls of few chunks, where the wave
+// count matters more).
+constexpr uint32_t kCountBatchFrom = 4096;  // chunks
+
+template <uint32_t kCountChunks>
 __global__ __launch_bounds__(kBlock) void topk_cand_count(const TDesc* __restrict__ d, int T, uint32_t C,
                                                           Ws ws) {
     const int lane = lane_id();
-    const uint32_t c = blockIdx.x * (kBlock / 64) + wave_id();
-    if (c < C) {
-        const uint32_t m = ws.t_ccount[c];
-        const uint32_t tau = ws.t_prefix[tensor_of_chunk(d, T, c)];
+    const uint32_t c0 = (blockIdx.x * (kBlock / 64) + wave_id()) * kCountChunks;
+    uint32_t m[kCountChunks], tau[kCountChunks], key[kCountChunks];
+#pragma unroll
+    for (uint32_t u = 0; u < kCountChunks; ++u) m[u] = c0 + u < C ? ws.t_ccount[c0 + u] : 0u;
+#pragma unroll
+    for (uint32_t u = 0; u < kCountChunks; ++u)
+        tau[u] = c0 + u < C ? ws.t_prefix[tensor_of_chunk(d, T, c0 + u)] : 0u;
+#pragma unroll
+    for (uint32_t u = 0; u < kCountChunks; ++u)
+        key[u] = (uint32_t)lane < m[u] ? ws.t_cand[(size_t)(c0 + u) * kChunk + lane].y & 0x7FFFFFFFu : 0u;
+#pragma unroll
+    for (uint32_t u = 0; u < kCountChunks; ++u) {
+        const uint32_t c = c0 + u;
+        if (c >= C) break;
+        const bool in = (uint32_t)lane < m[u];
+        uint32_t gt = (uint32_t)__popcll(__ballot(in && key[u] > tau[u]));
+        uint32_t eq = (uint32_t)__popcll(__ballot(in && key[u] == tau[u]));
         const uint2* cand = ws.t_cand + (size_t)c * kChunk;
-        uint32_t gt = 0, eq = 0;
-        for (uint32_t i0 = 0; i0 < m; i0 += 64) {
+        for (uint32_t i0 = 64; i0 < m[u]; i0 += 64) {  // chunks with more than 64 candidates
             const uint32_t i = i0 + lane;
-            const uint32_t key = i < m ? cand[i].y & 0x7FFFFFFFu : 0u;
-            gt += (uint32_t)__popcll(__ballot(i < m && key > tau));
-            eq += (uint32_t)__popcll(__ballot(i < m && key == tau));
+            const uint32_t k2 = i < m[u] ? cand[i].y & 0x7FFFFFFFu : 0u;
+            gt += (uint32_t)__popcll(__ballot(i < m[u] && k2 > tau[u]));
+            eq += (uint32_t)__popcll(__ballot(i < m[u] && k2 == tau[u]));
         }
         if (lane == 0) {
             ws.t_gt[c] = gt;
@@ -352,7 +369,21 @@ __global__ __launch_bounds__(kBlock) void topk_cand_count(const TDesc* __restric
 // of tau-equal candidates in earlier chunks; a chunk keeps its tau-equal
 // candidates while the running count stays below the number needed.  Thread
 // i walks a contiguous run of the tensor's chunks; two block scans over the
-// runs' totals give every chunk its prefix.
+// runs' totals give every chunk its prefix.  Runs of up to kScanRegs chunks
+// (tensors of up to 256 kScanRegs chunks) are read once into registers, all
+// loads in flight together; longer runs are read three times,
+// kScanBatch chunks at a time.
+constexpr uint32_t kScanRegs = 32;
+constexpr uint32_t kScanBatch = 8;
+
+namespace {
+// Winners of one chunk given the tau-equal candidates before it.
+__device__ __forceinline__ uint64_t chunk_winners(uint32_t gt, uint32_t eq, uint64_t eq_before, uint64_t need) {
+    const uint64_t left = eq_before < need ? need - eq_before : 0;
+    return (uint64_t)gt + (left < eq ? left : eq);
+}
+}  // namespace
+
 __global__ __launch_bounds__(kBlock) void topk_cand_scan(const TDesc* __restrict__ d, Ws ws) {
     __shared__ uint64_t sh[4];
     const int t = blockIdx.x;
@@ -362,32 +393,87 @@ __global__ __launch_bounds__(kBlock) void topk_cand_scan(const TDesc* __restrict
     const uint32_t per = (td.nchunks + kBlock - 1) / kBlock;
     const uint32_t lo = threadIdx.x * per;
     const uint32_t hi = lo + per < td.nchunks ? lo + per : td.nchunks;
+    const uint32_t* eqp = ws.t_eq + td.chunk0;
+    const uint32_t* gtp = ws.t_gt + td.chunk0;
+    uint64_t tot;
+    if (per <= kScanRegs) {
+        uint32_t eq[kScanRegs], gt[kScanRegs];
+#pragma unroll
+        for (uint32_t u = 0; u < kScanRegs; ++u) {
+            eq[u] = lo + u < hi ? eqp[lo + u] : 0u;
+            gt[u] = lo + u < hi ? gtp[lo + u] : 0u;
+        }
+        uint64_t eq_run = 0;
+#pragma unroll
+        for (uint32_t u = 0; u < kScanRegs; ++u) eq_run += eq[u];
+        const uint64_t eqb0 = block_excl_scan_u64(eq_run, sh, tot);
+        uint64_t sel_run = 0, e = eqb0;
+#pragma unroll
+        for (uint32_t u = 0; u < kScanRegs; ++u) {
+            sel_run += chunk_winners(gt[u], eq[u], e, need);
+            e += eq[u];
+        }
+        uint64_t pos = td.off + block_excl_scan_u64(sel_run, sh, tot);
+        e = eqb0;
+#pragma unroll
+        for (uint32_t u = 0; u < kScanRegs; ++u) {
+            if (lo + u < hi) {
+                const uint32_t c = td.chunk0 + lo + u;
+                ws.t_off[c] = pos;
+                ws.t_eqb[c] = (uint32_t)(e < 0xFFFFFFFFull ? e : 0xFFFFFFFFull);
+                pos += chunk_winners(gt[u], eq[u], e, need);
+                e += eq[u];
+            }
+        }
+        return;
+    }
     // tau-equal candidates before each run
     uint64_t eq_run = 0;
-    for (uint32_t q = lo; q < hi; ++q) eq_run += ws.t_eq[td.chunk0 + q];
-    uint64_t tot;
-    uint64_t eqb = block_excl_scan_u64(eq_run, sh, tot);
+    for (uint32_t q0 = lo; q0 < hi; q0 += kScanBatch) {
+        uint32_t eq[kScanBatch];
+#pragma unroll
+        for (uint32_t u = 0; u < kScanBatch; ++u) eq[u] = q0 + u < hi ? eqp[q0 + u] : 0u;
+#pragma unroll
+        for (uint32_t u = 0; u < kScanBatch; ++u) eq_run += eq[u];
+    }
+    const uint64_t eqb0 = block_excl_scan_u64(eq_run, sh, tot);
     // winners per chunk, and before each run
     uint64_t sel_run = 0;
     {
-        uint64_t e = eqb;
-        for (uint32_t q = lo; q < hi; ++q) {
-            const uint32_t c = td.chunk0 + q;
-            const uint32_t eq = ws.t_eq[c];
-            const uint64_t left = e < need ? need - e : 0;
-            sel_run += (uint64_t)ws.t_gt[c] + (left < eq ? left : eq);
-            e += eq;
+        uint64_t e = eqb0;
+        for (uint32_t q0 = lo; q0 < hi; q0 += kScanBatch) {
+            uint32_t eq[kScanBatch], gt[kScanBatch];
+#pragma unroll
+            for (uint32_t u = 0; u < kScanBatch; ++u) {
+                eq[u] = q0 + u < hi ? eqp[q0 + u] : 0u;
+                gt[u] = q0 + u < hi ? gtp[q0 + u] : 0u;
+            }
+#pragma unroll
+            for (uint32_t u = 0; u < kScanBatch; ++u) {
+                sel_run += chunk_winners(gt[u], eq[u], e, need);
+                e += eq[u];
+            }
         }
     }
     uint64_t pos = td.off + block_excl_scan_u64(sel_run, sh, tot);
-    for (uint32_t q = lo; q < hi; ++q) {
-        const uint32_t c = td.chunk0 + q;
-        const uint32_t eq = ws.t_eq[c];
-        const uint64_t left = eqb < need ? need - eqb : 0;
-        ws.t_off[c] = pos;
-        ws.t_eqb[c] = (uint32_t)(eqb < 0xFFFFFFFFull ? eqb : 0xFFFFFFFFull);
-        pos += (uint64_t)ws.t_gt[c] + (left < eq ? left : eq);
-        eqb += eq;
+    uint64_t eqb = eqb0;
+    for (uint32_t q0 = lo; q0 < hi; q0 += kScanBatch) {
+        uint32_t eq[kScanBatch], gt[kScanBatch];
+#pragma unroll
+        for (uint32_t u = 0; u < kScanBatch; ++u) {
+            eq[u] = q0 + u < hi ? eqp[q0 + u] : 0u;
+            gt[u] = q0 + u < hi ? gtp[q0 + u] : 0u;
+        }
+#pragma unroll
+        for (uint32_t u = 0; u < kScanBatch; ++u) {
+            if (q0 + u < hi) {
+                const uint32_t c = td.chunk0 + q0 + u;
+                ws.t_off[c] = pos;
+                ws.t_eqb[c] = (uint32_t)(eqb < 0xFFFFFFFFull ? eqb : 0xFFFFFFFFull);
+                pos += chunk_winners(gt[u], eq[u], eqb, need);
+                eqb += eq[u];
+            }
+        }
     }
 }
 
@@ -476,14 +562,16 @@ hipError_t launch_topk(int kind, double ratio, uint64_t seed, const TDesc* d, in
     uint32_t span = C / 1024u;
     span = span < 1u ? 1u : (span > 16u ? 16u : span);
     const dim3 hist_grid((C + span - 1) / span);
-    const dim3 wave_grid((C + kBlock / 64 - 1) / (kBlock / 64));
     hipLaunchKernelGGL(topk_cand_hist, hist_grid, blk, 0, s, d, T, C, span, 1, ws);
     hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit1, 0, ws);
     hipLaunchKernelGGL(topk_cand_hist, hist_grid, blk, 0, s, d, T, C, span, 2, ws);
     hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit2, 0, ws);
-    hipLaunchKernelGGL(topk_cand_count, wave_grid, blk, 0, s, d, T, C, ws);
+    if (C >= kCountBatchFrom)
+        hipLaunchKernelGGL(topk_cand_count<4>, dim3((C + 15) / 16), blk, 0, s, d, T, C, ws);
+    else
+        hipLaunchKernelGGL(topk_cand_count<1>, dim3((C + 3) / 4), blk, 0, s, d, T, C, ws);
     hipLaunchKernelGGL(topk_cand_scan, dim3(T), blk, 0, s, d, ws);
-    hipLaunchKernelGGL(topk_emit, wave_grid, blk, 0, s, d, T, C, idx, val, ws);
+    hipLaunchKernelGGL(topk_emit, dim3((C + kBlock / 64 - 1) / (kBlock / 64)), blk, 0, s, d, T, C, idx, val, ws);
     return hipGetLastError();
 }
 

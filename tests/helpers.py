@@ -54,8 +54,9 @@ def gpu_compress(kind, ratio, seed, grads, resids, tensor_ids=None, ws_fill=None
     return res, new_e
 
 
-def gpu_aggregate(kind, ratio, ns, payloads, alpha):
-    """payloads: list of dicts with numpy 'idx','val' or 'bits','scale'."""
+def gpu_aggregate(kind, ratio, ns, payloads, alpha, ws_fill=None):
+    """payloads: list of dicts with numpy 'idx','val' or 'bits','scale'.
+    ws_fill: as for gpu_compress."""
     import torch
     from paper_2205_14465_amd import binding as B
     dev = []
@@ -67,6 +68,9 @@ def gpu_aggregate(kind, ratio, ns, payloads, alpha):
     outs = [torch.full((max(n, 1),), float("nan"), dtype=torch.float32, device="cuda") for n in ns]
     outs = [o[:n] if n else o[:0] for o, n in zip(outs, ns)]
     ws = B.alloc_workspace(kind, ratio, ns, len(payloads))
+    if ws_fill is not None:
+        ws.fill_(ws_fill)
+        B.bytecomp_workspace_init(ws)
     B.bytecomp_decompress_aggregate(kind, ratio, dev, ns, outs, alpha, ws)
     torch.cuda.synchronize()
     return [o.cpu().numpy() for o in outs]

@@ -194,6 +194,38 @@ def test_one_pass_compress_ignores_stale_workspace(kind, fill):
         assert_resid_equal(got_e, want_e)
 
 
+@pytest.mark.parametrize("kind", ["topk", "topk_sampled", "randk", "sign", "terngrad", "qsgd4", "qsgd8"])
+def test_every_kind_ignores_a_dirty_workspace(kind):
+    # compress and aggregate with a workspace whose body is all 0xA5 bytes
+    # (header initialised): every region a call reads must be set by the
+    # call itself
+    rng = np.random.default_rng(31)
+    ns = [4096 * 40 + 3, 5000, 1, 0, 4096]
+    ratio = 0.01
+    grads, resids = make_set(ns, rng)
+    got, got_e = gpu_compress(kind, ratio, SEED, grads, resids, ws_fill=0xA5)
+    want, want_e = O.compress_set(kind, ratio, SEED, grads, resids)
+    if kind == "sign":
+        assert_sign_close(got, want, grads, resids, got_e, want_e)
+    elif kind in ("terngrad", "qsgd4", "qsgd8"):
+        assert np.array_equal(got["bits"], want["bits"])
+        assert np.array_equal(bits(got["scale"]), bits(want["scale"]))
+        assert_resid_equal(got_e, want_e)
+    else:
+        assert_sparse_equal(got, want, ns)
+        assert_resid_equal(got_e, want_e)
+    W = 5
+    payloads = [dict(want, off=want["off"])]
+    for w in range(1, W):
+        g2, e2 = make_set(ns, np.random.default_rng(100 + w))
+        p, _ = O.compress_set(kind, ratio, SEED + w, g2, e2)
+        payloads.append(p)
+    out = gpu_aggregate(kind, ratio, ns, payloads, 1.0 / W, ws_fill=0xA5)
+    ref = O.aggregate_set(kind, ns, payloads, 1.0 / W)
+    for t in range(len(ns)):
+        assert np.array_equal(bits(out[t]), bits(ref[t])), t
+
+
 def test_compress_is_deterministic():
     rng = np.random.default_rng(19)
     ns = [4096 * 300 + 5, 77]

@@ -264,9 +264,9 @@ int bytecomp_residual_update(int kind, double ratio, const bc_tensor* t, int T,
                              bc_payload own, void* stream);
 
 /* Read (synchronously, on `stream`) and clear the kernel failure flags a
- * workspace holds; *flags receives them (0 = none).  Bit 0 is reserved for
- * a bounded wait between workgroups that ran out; no kernel of this
- * version waits on another workgroup, so it stays clear. */
+ * workspace holds; *flags receives them (0 = none).  Bit 0: a bounded wait
+ * between workgroups of a one-pass compress kernel ran out (the results of
+ * that call are not to be trusted). */
 int bytecomp_device_status(void* ws, size_t ws_bytes, void* stream, uint32_t* flags);
 
 /* Instrumentation, not part of the method: for callers that measure one

@@ -27,8 +27,8 @@ WORD_KINDS = ("sign", "terngrad", "qsgd4", "qsgd8")  # packed words + scales
 
 def gpu_compress(kind, ratio, seed, grads, resids, tensor_ids=None, ws_fill=None):
     """Returns (payload dict of numpy arrays, list of new residuals or None).
-    ws_fill: byte that fills the workspace before its header is initialised
-    (what an earlier call sharing the workspace might have left there)."""
+    ws_fill: byte that fills the workspace past its (initialised) header,
+    as an earlier call of another kind sharing it might have left it."""
     import torch
     from paper_2205_14465_amd import binding as B
     ns = [g.size for g in grads]
@@ -37,8 +37,8 @@ def gpu_compress(kind, ratio, seed, grads, resids, tensor_ids=None, ws_fill=None
     out = B.alloc_payload(kind, ratio, ns)
     ws = B.alloc_workspace(kind, ratio, ns, 1)
     if ws_fill is not None:
-        ws.fill_(ws_fill)
         B.bytecomp_workspace_init(ws)
+        ws[256:].fill_(ws_fill)
     B.bytecomp_compress(kind, ratio, seed, dg, de, out, ws, tensor_ids=tensor_ids)
     torch.cuda.synchronize()
     assert B.bytecomp_device_status(ws) == 0
@@ -69,8 +69,8 @@ def gpu_aggregate(kind, ratio, ns, payloads, alpha, ws_fill=None):
     outs = [o[:n] if n else o[:0] for o, n in zip(outs, ns)]
     ws = B.alloc_workspace(kind, ratio, ns, len(payloads))
     if ws_fill is not None:
-        ws.fill_(ws_fill)
         B.bytecomp_workspace_init(ws)
+        ws[256:].fill_(ws_fill)
     B.bytecomp_decompress_aggregate(kind, ratio, dev, ns, outs, alpha, ws)
     torch.cuda.synchronize()
     return [o.cpu().numpy() for o in outs]

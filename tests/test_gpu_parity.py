@@ -177,9 +177,9 @@ def test_sign_fp16_subnormals_exact():
 @pytest.mark.parametrize("kind", ["sign", "terngrad", "qsgd8"])
 @pytest.mark.parametrize("fill", [0xA5, 0xFF])
 def test_one_pass_compress_ignores_stale_workspace(kind, fill):
-    # the one-pass kernels read their chunk slots as published when they
-    # are nonzero; a workspace body left dirty by an earlier call (here
-    # every byte `fill`, the header initialised) must not change a result
+    # the one-pass kernels publish chunk partials through workspace slots;
+    # a workspace body left dirty by an earlier call (here every byte
+    # `fill`, the header initialised) must not read as published
     rng = np.random.default_rng(29)
     ns = [4096 * 40 + 3, 5000, 1, 0, 4096]
     grads, resids = make_set(ns, rng)
@@ -192,6 +192,41 @@ def test_one_pass_compress_ignores_stale_workspace(kind, fill):
         assert np.array_equal(got["bits"], want["bits"])
         assert np.array_equal(bits(got["scale"]), bits(want["scale"]))
         assert_resid_equal(got_e, want_e)
+
+
+@pytest.mark.parametrize("kind", ["sign", "terngrad"])
+def test_one_pass_compress_calls_in_a_row_share_a_workspace(kind):
+    # successive calls on one workspace, with new inputs each time and a
+    # call of another shape between them: slots left by an earlier call of
+    # the same shape must not read as published in a later one
+    import torch
+    from paper_2205_14465_amd import binding as B
+    from tests.helpers import torch_dev, to_np_u32
+    ns_a = [4096 * 40 + 3, 5000, 4096 * 7]
+    ns_b = [4096 * 12 + 1, 77]
+    ws = B.alloc_workspace(kind, 0.01, ns_a, 1)
+    ws_b_bytes = B.bytecomp_workspace_size(kind, 0.01, ns_b, 1)
+    assert ws.numel() >= ws_b_bytes
+    for call, ns in enumerate([ns_a, ns_a, ns_b, ns_a, ns_a]):
+        rng = np.random.default_rng(300 + call)
+        grads, resids = make_set(ns, rng)
+        dg = [torch_dev(g) for g in grads]
+        de = [torch_dev(e) for e in resids]
+        out = B.alloc_payload(kind, 0.01, ns)
+        B.bytecomp_compress(kind, 0.01, SEED + call, dg, de, out, ws)
+        torch.cuda.synchronize()
+        assert B.bytecomp_device_status(ws) == 0
+        total = out["off"][-1]
+        got = {"off": np.array(out["off"], dtype=np.int64), "bits": to_np_u32(out["bits"])[:total],
+               "scale": out["scale"].cpu().numpy()[:len(ns)]}
+        got_e = [e.cpu().numpy() for e in de]
+        want, want_e = O.compress_set(kind, 0.01, SEED + call, grads, resids)
+        if kind == "sign":
+            assert_sign_close(got, want, grads, resids, got_e, want_e)
+        else:
+            assert np.array_equal(got["bits"], want["bits"]), call
+            assert np.array_equal(bits(got["scale"]), bits(want["scale"])), call
+            assert_resid_equal(got_e, want_e)
 
 
 @pytest.mark.parametrize("kind", ["topk", "topk_sampled", "randk", "sign", "terngrad", "qsgd4", "qsgd8"])

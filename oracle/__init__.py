@@ -62,6 +62,10 @@ def lib():
         L.bco_sign_span_limit.argtypes = [_int]
         L.bco_sign_exact_applies.restype = _int
         L.bco_sign_exact_applies.argtypes = [_int, _vp]
+        L.bco_tern_span_limit.restype = _int
+        L.bco_tern_span_limit.argtypes = [_int]
+        L.bco_tern_exact_applies.restype = _int
+        L.bco_tern_exact_applies.argtypes = [_int, _vp]
         L.bco_exact_sum_f32.restype = _flt
         L.bco_exact_sum_f32.argtypes = [_vp, _u64]
         L.bco_philox4x64_10.restype = None
@@ -255,6 +259,15 @@ def sign_span_limit(W):
 def sign_exact_applies(scales):
     sc = np.ascontiguousarray(np.asarray(scales, dtype=np.float32).reshape(-1))
     return bool(lib().bco_sign_exact_applies(sc.size, _p(sc)))
+
+
+def tern_span_limit(W):
+    return int(lib().bco_tern_span_limit(int(W)))
+
+
+def tern_exact_applies(scales):
+    sc = np.ascontiguousarray(np.asarray(scales, dtype=np.float32).reshape(-1))
+    return bool(lib().bco_tern_exact_applies(sc.size, _p(sc)))
 
 
 def exact_sum_f32(x):

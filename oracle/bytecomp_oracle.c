@@ -760,10 +760,55 @@ int bco_residual_update_quant(const void* g, int dtype, float* e_inout, uint64_t
 
 /* Aggregate: each output starts at +0.0 and adds the W decoded values in
  * ascending worker order, one fp32 addition each, then alpha times that. */
+/* TernGrad aggregate, exact form: the binade span its nonzero scales may
+ * have (W padded to a multiple of 4; 24 + span + log2 of that <= 31). */
+int bco_tern_span_limit(int W)
+{
+    int w4 = 4 * ((W + 3) / 4), lg = 0;
+    while ((1 << lg) < w4) ++lg;
+    return 7 - lg;
+}
+
+/* 1 when the TernGrad exact-sum form applies: at most 64 workers, every
+ * scale finite and zero or normal, the nonzero scales' binary exponents
+ * within bco_tern_span_limit(W). */
+int bco_tern_exact_applies(int W, const float* scale_w)
+{
+    if (W > 64) return 0;
+    int emin = 1000, emax = -1000;
+    for (int w = 0; w < W; ++w) {
+        uint32_t u = f2u(scale_w[w]);
+        uint32_t e = (u >> 23) & 255u;
+        if (e == 255u) return 0;
+        if (e == 0u) {
+            if (u & 0x7FFFFFu) return 0; /* subnormal */
+            continue;
+        }
+        if ((int)e < emin) emin = (int)e;
+        if ((int)e > emax) emax = (int)e;
+    }
+    return emax < emin || emax - emin <= bco_tern_span_limit(W);
+}
+
+/* Quantizer aggregate: alpha * (sum over the workers of the decoded
+ * values).  4- and 8-bit codes: the fp32 additions in worker order from
+ * +0.0.  2-bit (TernGrad) codes decode to 0 or +-scale, like the sign kind,
+ * and take its reading: the exact sum rounded once to fp32 while
+ * bco_tern_exact_applies holds, the worker-ordered fp32 sum otherwise. */
 int bco_aggregate_quant(int W, uint64_t n, int bits, const uint32_t* const* words_w,
                         const float* scale_w, float alpha, float* out)
 {
     if (bco_quant_levels(bits) == 0) return -1;
+    if (bits == 2 && bco_tern_exact_applies(W, scale_w)) {
+        for (uint64_t i = 0; i < n; ++i) {
+            acc320_t a;
+            memset(&a, 0, sizeof a);
+            for (int w = 0; w < W; ++w)
+                acc_add_f32(&a, bco_quant_decode(quant_code_at(words_w[w], i, bits), bits, scale_w[w]));
+            out[i] = alpha * acc_round_f32(&a);
+        }
+        return 0;
+    }
     for (uint64_t i = 0; i < n; ++i) {
         float acc = 0.0f;
         for (int w = 0; w < W; ++w)

@@ -6,8 +6,9 @@ Against things other than the oracle itself: numpy.random.Philox for the
 uniforms, numpy's little-endian byte view for the code packing, the
 hand-worked examples in tests/golden/hand_examples.json, closed forms on
 inputs whose levels are whole numbers, the unbiasedness and variance bound
-of stochastic rounding measured over many seeds, and brute-force ordered
-sums for the aggregate.
+of stochastic rounding measured over many seeds, brute-force ordered sums
+for the 4- and 8-bit aggregate (and the 2-bit one outside its exact
+form), and exact rational sums rounded once for the 2-bit exact form.
 """
 import json
 import os
@@ -224,10 +225,14 @@ def test_zero_and_empty_tensors(bits):
 
 @pytest.mark.parametrize("bits", BITS)
 def test_aggregate_ordered_bruteforce(bits):
+    # 2-bit codes take the ordered form only when their scales spread wider
+    # than the exact form allows: worker w's gradient is scaled by 2^(3w)
     rng = np.random.default_rng(90 + bits)
     n, W = 37, 5
-    pays = [O.compress_quant((rng.standard_normal(n) * 10.0 ** rng.uniform(-3, 0)).astype(f32), None,
-                             bits, 100 + w, 0)[:2] for w in range(W)]
+    pays = [O.compress_quant((rng.standard_normal(n) * 10.0 ** rng.uniform(-3, 0) * 2.0 ** (3 * w)).astype(f32),
+                             None, bits, 100 + w, 0)[:2] for w in range(W)]
+    if bits == 2:
+        assert not O.tern_exact_applies([p[1] for p in pays])
     alpha = f32(0.25)
     got = O.aggregate_quant(n, bits, [p[0] for p in pays], [p[1] for p in pays], float(alpha))
     for i in range(n):
@@ -239,6 +244,84 @@ def test_aggregate_ordered_bruteforce(bits):
     one = O.aggregate_quant(n, bits, [pays[0][0]], [pays[0][1]], 1.0)
     assert np.array_equal(one.view(np.uint32),
                           (f32(0.0) + decode_np(unpack_codes(pays[0][0], n, bits), bits, pays[0][1])).view(np.uint32))
+
+
+def exact_round_f32(values):
+    """Exact rational sum of float32 values rounded once to float32 (round
+    to nearest, ties to even, done on the rational)."""
+    from fractions import Fraction
+    q = sum((Fraction(float(v)) for v in values), Fraction(0))
+    if q == 0:
+        return f32(0.0)
+    sign = -1 if q < 0 else 1
+    q = abs(q)
+    e = q.numerator.bit_length() - q.denominator.bit_length()
+    if Fraction(2) ** e > q:
+        e -= 1
+    ex = max(e, -126) - 23
+    sc = q / Fraction(2) ** ex
+    m = sc.numerator // sc.denominator
+    rem = sc - m
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and m % 2 == 1):
+        m += 1
+    return f32(sign * float(m) * 2.0 ** ex)
+
+
+def test_tern_span_limit_closed_form():
+    # 24 mantissa bits + span + log2(W rounded up to a multiple of 4) <= 31
+    for W in range(1, 65):
+        w4 = 4 * ((W + 3) // 4)
+        assert O.tern_span_limit(W) == 7 - (w4 - 1).bit_length()
+    assert O.tern_span_limit(64) == 1 and O.tern_span_limit(4) == 5
+
+
+def test_tern_exact_applies_rule():
+    one = f32(1.0)
+    assert O.tern_exact_applies([one] * 64)
+    assert not O.tern_exact_applies([one] * 65)              # more than 64 workers
+    assert O.tern_exact_applies([one, f32(3.9), f32(0.0)] * 20)   # span 1, zeros ignored
+    assert not O.tern_exact_applies([one, f32(4.0)] * 32)    # span 2 > 1 at W = 64
+    assert O.tern_exact_applies([one, f32(4.0)] * 2)         # W = 4: limit 5
+    assert not O.tern_exact_applies([one, f32(np.inf)])
+    assert not O.tern_exact_applies([one, f32(1e-40)])       # subnormal
+
+
+@pytest.mark.parametrize("W", [1, 3, 16, 64])
+def test_terngrad_aggregate_exact_form_per_element(W):
+    # the exact rational sum of the decoded values, rounded once, times alpha
+    rng = np.random.default_rng(400 + W)
+    n = 53
+    pays = []
+    for w in range(W):
+        g = (rng.standard_normal(n) * 1e-3 * (1 + 0.05 * rng.standard_normal())).astype(f32)
+        pays.append(O.compress_quant(g, None, 2, 500 + w, 0)[:2])
+    scales = [p[1] for p in pays]
+    assert O.tern_exact_applies(scales)
+    alpha = f32(1.0 / W)
+    got = O.aggregate_quant(n, 2, [p[0] for p in pays], scales, float(alpha))
+    dec = [decode_np(unpack_codes(wds, n, 2), 2, m) for wds, m in pays]
+    for i in range(n):
+        want = f32(alpha * exact_round_f32([d[i] for d in dec]))
+        assert got[i].view(np.uint32) == want.view(np.uint32), i
+
+
+def test_terngrad_aggregate_exact_differs_from_ordered_somewhere():
+    # the two readings are distinguishable: with scales that are not exact
+    # multiples of each other some ordered fp32 sums round differently
+    rng = np.random.default_rng(411)
+    n, W = 4000, 64
+    pays = []
+    for w in range(W):
+        g = (rng.standard_normal(n) * 1e-3 * (1 + 0.05 * rng.standard_normal())).astype(f32)
+        pays.append(O.compress_quant(g, None, 2, 600 + w, 0)[:2])
+    got = O.aggregate_quant(n, 2, [p[0] for p in pays], [p[1] for p in pays], 1.0)
+    dec = np.array([decode_np(unpack_codes(wds, n, 2), 2, m) for wds, m in pays])
+    ordered = np.zeros(n, f32)
+    for w in range(W):
+        ordered = (ordered + dec[w]).astype(f32)
+    assert np.any(got.view(np.uint32) != ordered.view(np.uint32))
+    exact64 = dec.astype(np.float64).sum(axis=0)  # exact: 24 + 1 + 6 bits
+    assert np.array_equal(got, exact64.astype(f32))
 
 
 @pytest.mark.parametrize("kind", ["terngrad", "qsgd4", "qsgd8"])

@@ -223,6 +223,10 @@ WsPlan plan_workspace(int kind, int T, uint64_t C, uint64_t sum_k) {
         take(p.s_val, t * 4);
         take(p.q_max, (size_t)C * 4);
         take(p.q_slot, (size_t)C * 4);
+        if (kind == BC_TERNGRAD) {
+            take(p.s_info, t * 4);
+            take(p.s_tab, t * 4096 * 4);
+        }
     } else if (kind == BC_TOPK || kind == BC_TOPK_SAMPLED) {
         take(p.t_hist, t * kBins0 * 4);
         take(p.t_thr, t * 4);
@@ -609,8 +613,8 @@ int aggregate_impl(int kind, double ratio, const bc_payload* in, const uint64_t*
         for (int i = 0; i < T; ++i) a[i].k = 0;  // per-worker counts come from the parts
         off = 1;                                 // payloads are not addressed by layout
     }
-    Ws w{};  // sign: per-tensor forms and lookup tables live in the workspace
-    if (kind == BC_SIGN1) {
+    Ws w{};  // sign, TernGrad: per-tensor forms and lookup tables live in the workspace
+    if (kind == BC_SIGN1 || kind == BC_TERNGRAD) {
         uint64_t C = 0;
         for (int i = 0; i < T; ++i) C += (n[i] + kChunk - 1) / kChunk;
         const WsPlan plan = plan_workspace(kind, T, C, 0);
@@ -657,7 +661,7 @@ int aggregate_impl(int kind, double ratio, const bc_payload* in, const uint64_t*
     if (sparse) {
         e = launch_aggregate_sparse(ad, T, (uint32_t)units, unit, wdd, W, alpha, di.cus, rpd, s);
     } else if (quant_bits(kind)) {
-        e = launch_aggregate_quant(quant_bits(kind), ad, T, (uint32_t)units, wdd, W, alpha, s);
+        e = launch_aggregate_quant(quant_bits(kind), ad, T, (uint32_t)units, wdd, W, alpha, w.s_info, w.s_tab, s);
     } else {
         e = launch_aggregate_sign(ad, T, (uint32_t)units, wdd, W, alpha, w.s_info, w.s_tab, s);
     }

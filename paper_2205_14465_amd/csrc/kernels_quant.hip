@@ -365,6 +365,120 @@ __global__ __launch_bounds__(kBlock) void quant_residual_update(const TDesc* __r
     store_chunk(td.resid, td.n, j, v);
 }
 
+// ------------------------------------------------ TernGrad exact aggregate
+// 2-bit codes decode to 0 or +-scale, so the TernGrad aggregate is, like
+// the sign aggregate, the exact sum rounded once: with at most 64 workers
+// whose nonzero scales span at most tern_span_limit(W) binades, every scale
+// is an integer multiple of 2^(emin-150) below 2^(24+span), and the sum of
+// W of them stays below 2^31: int32 arithmetic is exact.  Workers go in
+// groups of four; a group's four 2-bit codes of an element form an 8-bit
+// index into a 256-entry table of the group's sums.  Other scale sets take
+// the worker-ordered fp32 path.
+namespace {
+constexpr int kTernTab = 16 * 256;  // int32 entries per tensor: 16 groups of four workers
+
+// The scale as a multiple of 2^(emin - 150) (zero stays zero).
+__device__ __forceinline__ int32_t tern_scale_units(float sv, int emin) {
+    const uint32_t b = f2u(sv);
+    const int e = (int)((b >> 23) & 255u);
+    if (e == 0) return 0;
+    return (int32_t)(((b & 0x7FFFFFu) | 0x800000u) << (e - emin));
+}
+
+// Contribution of a 2-bit code (level bit 0, sign bit 1) of scale units sv.
+__device__ __forceinline__ int32_t tern_code_value(uint32_t code, int32_t sv) {
+    return (code & 1u) ? ((code & 2u) ? -sv : sv) : 0;
+}
+}  // namespace
+
+// One wave per tensor: its form (info[t]: 1 exact, 0 ordered; emin in bits
+// 8-15) and, for the exact form, its tables: tab[256 g + p] is the sum over
+// the four workers 4g + c of the value of code (p >> 2c) & 3, built from two
+// two-worker tables of 16 entries.  Workers past W count as zero.
+__global__ __launch_bounds__(64) void tern_agg_prep(const ADesc* __restrict__ a, int T,
+                                                    const uint64_t* __restrict__ wp, int W, int span_limit,
+                                                    uint32_t* __restrict__ info, int32_t* __restrict__ tabs) {
+    __shared__ float sc[64];
+    __shared__ int32_t sub[16 * 32];
+    const int t = blockIdx.x;
+    if (a[t].nunits == 0) return;
+    const int lane = (int)threadIdx.x;
+    int lo = 1000, hi = -1000, bad = W > 64;
+    for (int w = lane; w < W && w < 64; w += 64) {
+        const float sv = gp((const float*)w_b(wp, W, w))[t];
+        sc[w] = sv;
+        const int e = (int)((f2u(sv) >> 23) & 255u);
+        if (e == 255 || (e == 0 && (f2u(sv) & 0x7FFFFFu))) bad = 1;
+        else if (e) {
+            lo = e < lo ? e : lo;
+            hi = e > hi ? e : hi;
+        }
+    }
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) {
+        const int lo2 = __shfl_xor(lo, m, 64), hi2 = __shfl_xor(hi, m, 64);
+        lo = lo2 < lo ? lo2 : lo;
+        hi = hi2 > hi ? hi2 : hi;
+        bad |= __shfl_xor(bad, m, 64);
+    }
+    const int span = hi < lo ? 0 : hi - lo;
+    const int form = !bad && span <= span_limit ? 1 : 0;
+    const int emin = hi < lo ? 1 : lo;
+    if (lane == 0) info[t] = (uint32_t)form | ((uint32_t)emin << 8);
+    if (form != 1) return;
+    __builtin_amdgcn_wave_barrier();
+    // sub[32 g + 16 h + p]: workers 4g + 2h + c, c < 2, with codes (p >> 2c) & 3
+    for (int x = lane; x < 16 * 32; x += 64) {
+        const int w0 = 4 * (x >> 5) + 2 * ((x >> 4) & 1), pat = x & 15;
+        int32_t acc = 0;
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+            const int32_t sv = w0 + c < W ? tern_scale_units(sc[w0 + c], emin) : 0;
+            acc += tern_code_value((uint32_t)(pat >> (2 * c)) & 3u, sv);
+        }
+        sub[x] = acc;
+    }
+    __builtin_amdgcn_wave_barrier();
+    int32_t* tt = tabs + (size_t)t * kTernTab;
+    for (int x = 4 * lane; x < kTernTab; x += 256) {
+        const int g = x >> 8, p0 = x & 255;
+        const int32_t hi16 = sub[32 * g + 16 + (p0 >> 4)];
+        u32x4 v;
+        v.x = (uint32_t)(sub[32 * g + ((p0 + 0) & 15)] + hi16);
+        v.y = (uint32_t)(sub[32 * g + ((p0 + 1) & 15)] + hi16);
+        v.z = (uint32_t)(sub[32 * g + ((p0 + 2) & 15)] + hi16);
+        v.w = (uint32_t)(sub[32 * g + ((p0 + 3) & 15)] + hi16);
+        *(BC_GLOBAL u32x4*)(gp(tt) + x) = v;
+    }
+}
+
+namespace {
+// Indices of one group of four workers for the lane's 16 elements: x[k] is
+// worker 4g + k's word (element q's code at bits 2q).  v_perm gathers byte j
+// of the four words (elements 4j .. 4j+3, one byte per worker) and a 4x4
+// transpose of 2-bit fields (two delta swaps) turns byte i into element
+// 4j + i's index, worker k's code at bits 2k.
+__device__ __forceinline__ void tern_indices(const uint32_t (&x)[4], uint32_t (&y)[4]) {
+    const uint32_t p01 = __builtin_amdgcn_perm(x[1], x[0], 0x05010400u);
+    const uint32_t q01 = __builtin_amdgcn_perm(x[1], x[0], 0x07030602u);
+    const uint32_t r23 = __builtin_amdgcn_perm(x[3], x[2], 0x05010400u);
+    const uint32_t s23 = __builtin_amdgcn_perm(x[3], x[2], 0x07030602u);
+    y[0] = __builtin_amdgcn_perm(r23, p01, 0x05040100u);
+    y[1] = __builtin_amdgcn_perm(r23, p01, 0x07060302u);
+    y[2] = __builtin_amdgcn_perm(s23, q01, 0x05040100u);
+    y[3] = __builtin_amdgcn_perm(s23, q01, 0x07060302u);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        uint32_t v = y[j];
+        uint32_t t = ((v >> 12) ^ v) & 0x0000F0F0u;
+        v ^= t ^ (t << 12);
+        t = ((v >> 6) ^ v) & 0x00CC00CCu;
+        v ^= t ^ (t << 6);
+        y[j] = v;
+    }
+}
+}  // namespace
+
 // Aggregate: one workgroup per 4096-element unit of a tensor, lane l of
 // the workgroup owning elements 16 l .. 16 l + 15 of the unit (16 kBits
 // bits: kBits / 2 consecutive words of every worker's payload).
@@ -377,13 +491,21 @@ __global__ __launch_bounds__(kBlock) void quant_residual_update(const TDesc* __r
 // sum never holds -0.0 (it starts at +0.0, and x + (-x) rounds to +0.0),
 // and adding either zero to a value that is not -0.0 gives the same
 // result, so the sums are those of the +0.0 decoding.
-template <int kBits>
+//
+// 2-bit codes of a tensor in the exact form (info[t] & 255 == 1) take the
+// table path instead: the workgroup copies the tensor's tables into LDS,
+// loads the words of all (at most 16 kTS) workers at once, and adds one
+// table entry per element and group of four workers in int32.
+template <int kBits, int kTS>
 __global__ __launch_bounds__(kBlock) void aggregate_quant(const ADesc* __restrict__ a, int T, uint32_t U,
-                                                          const uint64_t* __restrict__ wp, int W, float alpha) {
+                                                          const uint64_t* __restrict__ wp, int W, float alpha,
+                                                          const uint32_t* __restrict__ info,
+                                                          const int32_t* __restrict__ tabs) {
     constexpr int kWords = kBits / 2;
     constexpr int kGroup = 8;  // workers whose words are in flight together
     using Q = Quant<kBits>;
     __shared__ float unit_sh[1024];
+    __shared__ __attribute__((aligned(16))) int32_t tab_sh[kBits == 2 ? 256 * 4 * kTS : 4];
     const uint32_t u = blockIdx.x;
     const int t = unit_owner(wp, W, u);
     const ADesc ad = a[t];
@@ -419,6 +541,43 @@ __global__ __launch_bounds__(kBlock) void aggregate_quant(const ADesc* __restric
     float acc[16];
 #pragma unroll
     for (int q = 0; q < 16; ++q) acc[q] = 0.f;
+    if constexpr (kBits == 2) {
+        const uint32_t inf = info[t];
+        if ((inf & 255u) == 1u) {
+            const int G4 = (W + 3) / 4;  // <= 4 kTS
+            const int32_t* tt = tabs + (size_t)t * kTernTab;
+            uint32_t wv[16 * kTS];
+#pragma unroll
+            for (int k = 0; k < 16 * kTS; ++k) {
+                uint32_t wd[1];
+                load_words(w_a(wp, k < W ? k : W - 1) + ad.off, wd);
+                wv[k] = wd[0];
+            }
+            for (int x = 4 * (int)threadIdx.x; x < 256 * G4; x += 4 * kBlock)
+                *reinterpret_cast<u32x4*>(tab_sh + x) = ldg4u(tt + x);
+            __syncthreads();
+            int32_t S[16];
+#pragma unroll
+            for (int q = 0; q < 16; ++q) S[q] = 0;
+#pragma unroll
+            for (int g = 0; g < 4 * kTS; ++g) {
+                if (g < G4) {
+                    const uint32_t xw[4] = {wv[4 * g], wv[4 * g + 1], wv[4 * g + 2], wv[4 * g + 3]};
+                    uint32_t y[4];
+                    tern_indices(xw, y);
+                    const int32_t* tg = tab_sh + 256 * g;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) S[4 * j + i] += tg[(y[j] >> (8 * i)) & 255u];
+                }
+            }
+            // exact: |S| < 2^31 and the unit is a power of two
+            const double unit = __builtin_ldexp(1.0, (int)((inf >> 8) & 255u) - 150);
+#pragma unroll
+            for (int q = 0; q < 16; ++q) acc[q] = (float)((double)S[q] * unit);
+        }
+    }
     auto add_worker = [&](const uint32_t (&wd)[kWords], float un) {
         const uint32_t ub = f2u(un);
 #pragma unroll
@@ -437,6 +596,9 @@ __global__ __launch_bounds__(kBlock) void aggregate_quant(const ADesc* __restric
         }
     };
     int w0 = 0;
+    if constexpr (kBits == 2) {
+        if ((info[t] & 255u) == 1u) w0 = W;  // summed on the table path
+    }
     for (; w0 + kGroup <= W; w0 += kGroup) {
         uint32_t wd[kGroup][kWords];
 #pragma unroll
@@ -544,14 +706,29 @@ hipError_t launch_quant_residual_update(int bits, const TDesc* d, int T, uint32_
 }
 
 hipError_t launch_aggregate_quant(int bits, const ADesc* a, int T, uint32_t U, const uint64_t* wp, int W,
-                                  float alpha, hipStream_t s) {
+                                  float alpha, uint32_t* info, int32_t* tabs, hipStream_t s) {
     if (U == 0) return hipSuccess;
     if (W > 1024) return hipErrorInvalidValue;
-    if (bits == 2)
-        return launch_timed(kTimedAggQuant, aggregate_quant<2>, dim3(U), dim3(kBlock), 0, s, a, T, U, wp, W, alpha);
+    const dim3 grid(U), block(kBlock);
+    if (bits == 2) {
+        // 24 + span + ceil(log2 W4) <= 31, W4 = W rounded up to a multiple of 4
+        const int w4 = 4 * ((W + 3) / 4);
+        int lg = 0;
+        while ((1 << lg) < w4) ++lg;
+        hipLaunchKernelGGL(tern_agg_prep, dim3(T), dim3(64), 0, s, a, T, wp, W, 7 - lg, info, tabs);
+        const uint32_t* ci = info;
+        const int32_t* ct = tabs;
+        const int steps = W > 64 ? 1 : (W + 15) / 16;
+        if (steps <= 1) return launch_timed(kTimedAggQuant, aggregate_quant<2, 1>, grid, block, 0, s, a, T, U, wp, W, alpha, ci, ct);
+        if (steps == 2) return launch_timed(kTimedAggQuant, aggregate_quant<2, 2>, grid, block, 0, s, a, T, U, wp, W, alpha, ci, ct);
+        if (steps == 3) return launch_timed(kTimedAggQuant, aggregate_quant<2, 3>, grid, block, 0, s, a, T, U, wp, W, alpha, ci, ct);
+        return launch_timed(kTimedAggQuant, aggregate_quant<2, 4>, grid, block, 0, s, a, T, U, wp, W, alpha, ci, ct);
+    }
+    const uint32_t* nul = nullptr;
+    const int32_t* nt = nullptr;
     if (bits == 4)
-        return launch_timed(kTimedAggQuant, aggregate_quant<4>, dim3(U), dim3(kBlock), 0, s, a, T, U, wp, W, alpha);
-    return launch_timed(kTimedAggQuant, aggregate_quant<8>, dim3(U), dim3(kBlock), 0, s, a, T, U, wp, W, alpha);
+        return launch_timed(kTimedAggQuant, aggregate_quant<4, 1>, grid, block, 0, s, a, T, U, wp, W, alpha, nul, nt);
+    return launch_timed(kTimedAggQuant, aggregate_quant<8, 1>, grid, block, 0, s, a, T, U, wp, W, alpha, nul, nt);
 }
 
 }  // namespace bc

@@ -19,10 +19,12 @@ struct Ws {
     // BC_SIGN1
     float* s_val;           // [T] published scales
     double* s_partial;      // [C] per-chunk sums of |v|
-    uint32_t* s_info;       // [T] aggregate: form (bits 0-7), smallest scale exponent (8-15)
+    uint32_t* s_info;       // [T] sign / TernGrad aggregate: form (bits 0-7), smallest scale
+                            // exponent (8-15)
     uint64_t* s_slot;       // [C] one-pass compress: ~bits of each chunk's partial sum once
                             // published, 0 otherwise (emptied before the kernel runs)
-    int32_t* s_tab;         // [T * 2048] aggregate: int32 lookup tables of each tensor
+    int32_t* s_tab;         // aggregate: int32 lookup tables of each tensor, [T * 2048] (sign)
+                            // or [T * 4096] (TernGrad)
     // BC_TERNGRAD, BC_QSGD4, BC_QSGD8 (and s_val)
     uint32_t* q_max;        // [C] largest |v| bits of each chunk
     uint32_t* q_slot;       // [C] one-pass compress: those bits | 1 << 31 once published, 0 otherwise
@@ -127,8 +129,9 @@ hipError_t launch_quant_residual_update(int bits, const TDesc* d, int T, uint32_
 hipError_t launch_dgc_momentum(const TDesc* d, int T, uint32_t C, float m, hipStream_t s);
 hipError_t launch_dgc_mask(const TDesc* d, int T, const uint32_t* idx, uint64_t total, hipStream_t s);
 // units of kSignAggUnit elements; W <= 1024
+// info, tabs: the TernGrad exact form's per-tensor forms and tables (2-bit only).
 hipError_t launch_aggregate_quant(int bits, const ADesc* a, int T, uint32_t units, const uint64_t* wp, int W,
-                                  float alpha, hipStream_t s);
+                                  float alpha, uint32_t* info, int32_t* tabs, hipStream_t s);
 
 // Random-k bucketing: generating workgroups of kGenBlock threads handle
 // kGenEntries payload entries each; a bucket is 2^S consecutive chunks with

@@ -149,3 +149,54 @@ def test_quant_residual_update_matches_fused(kind):
                                     fused["bits"][fused["off"][t]:fused["off"][t + 1]], fused["scale"][t])
             for t in range(len(ns))]
     assert_resid_equal([e.cpu().numpy() for e in de], want)
+
+
+def _tern_payloads(rng, ns, W, spread):
+    """Arbitrary 2-bit code words (every code, the sign bit with level 0
+    included) and per-tensor scales 2^e (1 + 0.05 N(0,1)) with e drawn per
+    worker from `spread` binades (0: one band, so the exact form applies)."""
+    off = O.quant_word_offsets(ns, 2)
+    pays = []
+    for w in range(W):
+        words = rng.integers(0, 2**32, size=max(int(off[-1]), 1), dtype=np.uint64).astype(np.uint32)[:int(off[-1])]
+        for t, n in enumerate(ns):  # codes past each tensor's end are zero
+            used = n * 2 % 32
+            if used:
+                words[off[t + 1] - 1] &= np.uint32((1 << used) - 1)
+        e = rng.integers(0, spread + 1, size=len(ns)) if spread else np.zeros(len(ns), int)
+        scale = (1e-3 * 2.0 ** e * (1 + 0.05 * rng.standard_normal(len(ns)))).astype(np.float32)
+        pays.append({"bits": words, "scale": scale, "off": off})
+    return pays
+
+
+@pytest.mark.parametrize("W", [1, 2, 4, 5, 13, 16, 17, 33, 48, 64])
+def test_terngrad_aggregate_exact_form(W):
+    # every tensor in the exact form: the table path, exact sums rounded once
+    rng = np.random.default_rng(700 + W)
+    ns = [1, 15, 16, 17, 4095, 4096, 4097, 3 * 4096 + 33, 0, 50000]
+    pays = _tern_payloads(rng, ns, W, 0)
+    for t in range(len(ns)):
+        assert O.tern_exact_applies([p["scale"][t] for p in pays])
+    got = gpu_aggregate("terngrad", 1.0, ns, pays, 1.0 / W)
+    want = O.aggregate_set("terngrad", ns, pays, 1.0 / W)
+    for t, n in enumerate(ns):
+        assert np.array_equal(bits(got[t]), bits(want[t])), (t, n)
+
+
+@pytest.mark.parametrize("W", [8, 64, 65, 72])
+def test_terngrad_aggregate_mixed_forms(W):
+    # tensors of one call in both forms: wide spreads and zero scales among
+    # narrow ones, and more than 64 workers (ordered throughout)
+    rng = np.random.default_rng(800 + W)
+    ns = [5000, 4096 * 5 + 7, 300, 12000]
+    pays = _tern_payloads(rng, ns, W, 0)
+    for w, p in enumerate(pays):
+        p["scale"][1] = np.float32(p["scale"][1] * 2.0 ** (3 * (w % 4)))  # spread: ordered
+        if w == 2:
+            p["scale"][2] = np.float32(0.0)                             # a zero scale: still exact
+    forms = [O.tern_exact_applies([p["scale"][t] for p in pays]) for t in range(len(ns))]
+    assert forms == ([True, False, True, True] if W <= 64 else [False] * 4)
+    got = gpu_aggregate("terngrad", 1.0, ns, pays, 0.25)
+    want = O.aggregate_set("terngrad", ns, pays, 0.25)
+    for t, n in enumerate(ns):
+        assert np.array_equal(bits(got[t]), bits(want[t])), (t, n)

@@ -5,7 +5,8 @@ Every result is deterministic for a given seed, so codes, scales,
 residuals and aggregates must all match the oracle bit for bit: the scale
 is a maximum (no summation order), the rounding decisions use the same
 fp32 operations and the same Philox4x64-10 uniforms on both sides, and
-the aggregate adds the workers in the same order.
+the aggregate adds the workers in the same order (4- and 8-bit, and 2-bit
+outside the exact form) or forms the exact sum (2-bit exact form).
 """
 import numpy as np
 import pytest

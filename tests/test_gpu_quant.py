@@ -201,3 +201,17 @@ def test_terngrad_aggregate_mixed_forms(W):
     want = O.aggregate_set("terngrad", ns, pays, 0.25)
     for t, n in enumerate(ns):
         assert np.array_equal(bits(got[t]), bits(want[t])), (t, n)
+
+
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_quant_compress_long_and_short_tensors(kind, dtype):
+    # calls with tensors longer than the resident grid of the one-pass
+    # kernel (more than 1280 chunks on any current part) among short ones
+    # take the two passes; empty tensors included
+    rng = np.random.default_rng(41 + KINDS.index(kind))
+    ns = [5000, 1400 * 4096 + 123, 0, 77, 4096 * 3, 1300 * 4096, 1]
+    grads, resids = make_set(ns, rng, dtype)
+    got, got_e = gpu_compress(kind, 1.0, SEED + 7, grads, resids)
+    want, want_e = O.compress_set(kind, 1.0, SEED + 7, grads, resids)
+    check(kind, got, got_e, want, want_e)

@@ -195,9 +195,9 @@ int bytecomp_compress_dgc(int kind, double ratio, uint64_t seed, float momentum,
  *   out    host array of T device pointers to dense fp32 outputs
  *          (16-byte aligned)
  *   alpha  scale applied to each sum (1 = sum, 1/W = mean)
- *   ws     workspace: BC_SIGN1 needs bytecomp_workspace_size bytes (it keeps
- *          one flag per tensor there); the other kinds need its 256-byte
- *          header
+ *   ws     workspace: BC_SIGN1 and BC_TERNGRAD need bytecomp_workspace_size
+ *          bytes (they keep a form and lookup tables per tensor there); the
+ *          other kinds need its 256-byte header
  * Sparse kinds: out_t[i] = alpha * (sum over workers w = 0..W-1, in that
  * order, of worker w's value at i), each addition in fp32 starting from
  * +0.0; elements no worker sent are alpha * 0.
@@ -206,9 +206,14 @@ int bytecomp_compress_dgc(int kind, double ratio, uint64_t seed, float momentum,
  * rounded once to fp32.  This form applies when tensor t's W scales are
  * finite and normal or zero and their binary exponents span at most
  * 29 - ceil(log2 W) binades; otherwise the worker-ordered fp32 sum, as for
- * the sparse kinds.  Quantizers: out_t[i] = alpha * (sum over w = 0..W-1,
- * in that order, of worker w's decoded value at i), each addition in fp32
- * starting from +0.0; at most 1024 workers (BC_E_COUNT otherwise).
+ * the sparse kinds.  BC_QSGD4, BC_QSGD8: out_t[i] = alpha * (sum over
+ * w = 0..W-1, in that order, of worker w's decoded value at i), each
+ * addition in fp32 starting from +0.0.  BC_TERNGRAD (decoded values 0 or
+ * +-s_w,t): as BC_SIGN1, the exact sum rounded once, when W <= 64 and the
+ * tensor's nonzero scales are finite and normal and span at most
+ * 7 - ceil(log2 W4) binades (W4 = W rounded up to a multiple of 4);
+ * otherwise the worker-ordered fp32 sum.  Quantizers: at most 1024 workers
+ * (BC_E_COUNT otherwise).
  * Results are deterministic. */
 int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, int W,
                                   const uint64_t* n, int T, float* const* out, float alpha,

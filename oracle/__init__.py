@@ -58,14 +58,6 @@ def lib():
         L.bco_aggregate_sign.argtypes = [_int, _u64, _vp, _vp, _flt, _vp]
         L.bco_aggregate_sign_ordered.restype = _int
         L.bco_aggregate_sign_ordered.argtypes = [_int, _u64, _vp, _vp, _flt, _vp]
-        L.bco_sign_span_limit.restype = _int
-        L.bco_sign_span_limit.argtypes = [_int]
-        L.bco_sign_exact_applies.restype = _int
-        L.bco_sign_exact_applies.argtypes = [_int, _vp]
-        L.bco_tern_span_limit.restype = _int
-        L.bco_tern_span_limit.argtypes = [_int]
-        L.bco_tern_exact_applies.restype = _int
-        L.bco_tern_exact_applies.argtypes = [_int, _vp]
         L.bco_exact_sum_f32.restype = _flt
         L.bco_exact_sum_f32.argtypes = [_vp, _u64]
         L.bco_philox4x64_10.restype = None
@@ -250,24 +242,6 @@ def aggregate_sign(n, words_list, scales, alpha=1.0, ordered=False):
     rc = fn(W, n, ctypes.cast(wp, _vp), _p(sc), float(alpha), _p(out))
     assert rc == 0, rc
     return out
-
-
-def sign_span_limit(W):
-    return int(lib().bco_sign_span_limit(int(W)))
-
-
-def sign_exact_applies(scales):
-    sc = np.ascontiguousarray(np.asarray(scales, dtype=np.float32).reshape(-1))
-    return bool(lib().bco_sign_exact_applies(sc.size, _p(sc)))
-
-
-def tern_span_limit(W):
-    return int(lib().bco_tern_span_limit(int(W)))
-
-
-def tern_exact_applies(scales):
-    sc = np.ascontiguousarray(np.asarray(scales, dtype=np.float32).reshape(-1))
-    return bool(lib().bco_tern_exact_applies(sc.size, _p(sc)))
 
 
 def exact_sum_f32(x):

@@ -31,8 +31,9 @@
  * compiled with -O2 -ffp-contract=off (no FMA contraction, no fast-math).
  * The mean-|v| scale is accumulated in fp64 in index order.  The sparse
  * aggregate adds the workers' values in worker order in fp32; the sign
- * aggregate is the exact sum rounded once (a 320-bit fixed-point sum),
- * with the worker-ordered fp32 sum for scale sets outside fp64 exactness.
+ * aggregate (and the 2-bit one) is the exact sum of the decoded values
+ * rounded once (a 320-bit fixed-point sum), with an order-free rule for
+ * non-finite scales.
  *
  * Parity status of each function is pinned by tests under tests/ against
  * brute force, closed forms, hand-worked examples and library routines
@@ -487,8 +488,10 @@ int bco_aggregate_sparse(int W, uint64_t n, const uint32_t* const* idx_w,
     return 0;
 }
 
-/* Sign aggregate, worker-ordered form: each output starts at +0.0 and adds
- * the W decoded values in ascending worker order, one fp32 addition each. */
+/* Worker-ordered fp32 sum of the decoded sign values (each output starts at
+ * +0.0 and adds the W values in ascending worker order).  Not the sign
+ * aggregate's definition (bco_aggregate_sign below is); exported so that the
+ * pins can bound the exact sum against a recursive summation. */
 int bco_aggregate_sign_ordered(int W, uint64_t n, const uint32_t* const* words_w,
                                const float* scale_w, float alpha, float* out)
 {
@@ -575,51 +578,46 @@ static float acc_round_f32(const acc320_t* a)
     return neg ? -mag : mag;
 }
 
-/* Largest binade distance between the scales for which an fp64 sum of the
- * W decoded values is exact: 24 + span + ceil(log2 W) <= 53. */
-int bco_sign_span_limit(int W)
+/* Order-free sum of the W decoded values of one element, the aggregate's
+ * reading for the kinds whose decoded values are 0 or +-scale (sign,
+ * TernGrad).  The paper only has every node decompress the gathered payloads
+ * and sum them (Sec. 3.1, Reason #2); no addition order is given, so the sum
+ * is the one every order of exact arithmetic reaches:
+ *   - NaN when some decoded value is NaN, or when both +Inf and -Inf occur;
+ *   - else +Inf or -Inf when an infinity occurs;
+ *   - else the exact real sum of the finite values (subnormals included),
+ *     rounded once to fp32 (round to nearest even; an exact zero gives +0.0,
+ *     a sum beyond the fp32 range rounds to an infinity). */
+typedef struct { acc320_t a; int nan, pinf, ninf; } xsum_t;
+
+static void xsum_add(xsum_t* s, float d)
 {
-    int lg = 0;
-    while ((1 << lg) < W) ++lg;
-    return 29 - lg;
+    if (isnan(d)) s->nan = 1;
+    else if (isinf(d)) { if (d > 0.0f) s->pinf = 1; else s->ninf = 1; }
+    else acc_add_f32(&s->a, d);
 }
 
-/* 1 when the exact-sum form applies: every scale finite and zero or normal,
- * and the nonzero scales' binary exponents within bco_sign_span_limit(W). */
-int bco_sign_exact_applies(int W, const float* scale_w)
+static float xsum_round(const xsum_t* s)
 {
-    int emin = 1000, emax = -1000;
-    for (int w = 0; w < W; ++w) {
-        uint32_t u = f2u(scale_w[w]);
-        uint32_t e = (u >> 23) & 255u;
-        if (e == 255u) return 0;
-        if (e == 0u) {
-            if (u & 0x7FFFFFu) return 0; /* subnormal */
-            continue;
-        }
-        if ((int)e < emin) emin = (int)e;
-        if ((int)e > emax) emax = (int)e;
-    }
-    return emax < emin || emax - emin <= bco_sign_span_limit(W);
+    if (s->nan || (s->pinf && s->ninf)) return NAN;
+    if (s->pinf) return INFINITY;
+    if (s->ninf) return -INFINITY;
+    return acc_round_f32(&s->a);
 }
 
-/* Sign aggregate (reading): the exact sum of the W decoded values, rounded
- * once to fp32, times alpha in fp32.  For scale sets outside the exact-sum
- * form's range (non-finite or subnormal scales, or exponents spread wider
- * than bco_sign_span_limit) the worker-ordered fp32 sum is used instead. */
+/* Sign aggregate (reading): alpha times the order-free sum above of the W
+ * decoded values d_w = (bit ? -s_w : +s_w), one fp32 multiplication. */
 int bco_aggregate_sign(int W, uint64_t n, const uint32_t* const* words_w,
                        const float* scale_w, float alpha, float* out)
 {
-    if (!bco_sign_exact_applies(W, scale_w))
-        return bco_aggregate_sign_ordered(W, n, words_w, scale_w, alpha, out);
     for (uint64_t i = 0; i < n; ++i) {
-        acc320_t a;
-        memset(&a, 0, sizeof a);
+        xsum_t s;
+        memset(&s, 0, sizeof s);
         for (int w = 0; w < W; ++w) {
             uint32_t bit = (words_w[w][i / 32] >> (i % 32)) & 1u;
-            acc_add_f32(&a, bit ? -scale_w[w] : scale_w[w]);
+            xsum_add(&s, bit ? -scale_w[w] : scale_w[w]);
         }
-        out[i] = alpha * acc_round_f32(&a);
+        out[i] = alpha * xsum_round(&s);
     }
     return 0;
 }
@@ -758,54 +756,23 @@ int bco_residual_update_quant(const void* g, int dtype, float* e_inout, uint64_t
     return 0;
 }
 
-/* Aggregate: each output starts at +0.0 and adds the W decoded values in
- * ascending worker order, one fp32 addition each, then alpha times that. */
-/* TernGrad aggregate, exact form: the binade span its nonzero scales may
- * have (W padded to a multiple of 4; 24 + span + log2 of that <= 31). */
-int bco_tern_span_limit(int W)
-{
-    int w4 = 4 * ((W + 3) / 4), lg = 0;
-    while ((1 << lg) < w4) ++lg;
-    return 7 - lg;
-}
-
-/* 1 when the TernGrad exact-sum form applies: at most 64 workers, every
- * scale finite and zero or normal, the nonzero scales' binary exponents
- * within bco_tern_span_limit(W). */
-int bco_tern_exact_applies(int W, const float* scale_w)
-{
-    if (W > 64) return 0;
-    int emin = 1000, emax = -1000;
-    for (int w = 0; w < W; ++w) {
-        uint32_t u = f2u(scale_w[w]);
-        uint32_t e = (u >> 23) & 255u;
-        if (e == 255u) return 0;
-        if (e == 0u) {
-            if (u & 0x7FFFFFu) return 0; /* subnormal */
-            continue;
-        }
-        if ((int)e < emin) emin = (int)e;
-        if ((int)e > emax) emax = (int)e;
-    }
-    return emax < emin || emax - emin <= bco_tern_span_limit(W);
-}
-
 /* Quantizer aggregate: alpha * (sum over the workers of the decoded
- * values).  4- and 8-bit codes: the fp32 additions in worker order from
- * +0.0.  2-bit (TernGrad) codes decode to 0 or +-scale, like the sign kind,
- * and take its reading: the exact sum rounded once to fp32 while
- * bco_tern_exact_applies holds, the worker-ordered fp32 sum otherwise. */
+ * values).  4- and 8-bit codes: each output starts at +0.0 and adds the W
+ * decoded values in ascending worker order, one fp32 addition each.  2-bit
+ * (TernGrad) codes decode to 0 or +-scale, as sign bits decode to +-scale,
+ * and take the sign kind's reading: the order-free exact sum of the decoded
+ * values rounded once (xsum above). */
 int bco_aggregate_quant(int W, uint64_t n, int bits, const uint32_t* const* words_w,
                         const float* scale_w, float alpha, float* out)
 {
     if (bco_quant_levels(bits) == 0) return -1;
-    if (bits == 2 && bco_tern_exact_applies(W, scale_w)) {
+    if (bits == 2) {
         for (uint64_t i = 0; i < n; ++i) {
-            acc320_t a;
-            memset(&a, 0, sizeof a);
+            xsum_t s;
+            memset(&s, 0, sizeof s);
             for (int w = 0; w < W; ++w)
-                acc_add_f32(&a, bco_quant_decode(quant_code_at(words_w[w], i, bits), bits, scale_w[w]));
-            out[i] = alpha * acc_round_f32(&a);
+                xsum_add(&s, bco_quant_decode(quant_code_at(words_w[w], i, bits), bits, scale_w[w]));
+            out[i] = alpha * xsum_round(&s);
         }
         return 0;
     }

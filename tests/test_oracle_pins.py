@@ -15,6 +15,8 @@ import pytest
 
 import oracle as O
 
+from .exact_ref import exact_round_f32, same_f32, same_f32_arrays, xsum_f32
+
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_examples.json")
 f32 = np.float32
 
@@ -444,29 +446,8 @@ def test_sparse_aggregate_brute_force_order():
 
 
 def exact_round(values):
-    """Exact rational sum of float32 values, rounded once to float32
-    (Fraction -> nearest float64 is exact-enough only as a first step, so
-    the rounding to float32 is done on the rational directly)."""
-    tot = sum((Fraction(float(v)) for v in values), Fraction(0))
-    return fraction_to_f32(tot)
-
-
-def fraction_to_f32(q):
-    if q == 0:
-        return f32(0.0)
-    sign = -1 if q < 0 else 1
-    q = abs(q)
-    # find e with 2^e <= q < 2^(e+1)
-    e = q.numerator.bit_length() - q.denominator.bit_length()
-    if Fraction(2) ** e > q:
-        e -= 1
-    exp = max(e, -126) - 23           # unit in the last place (subnormals below -126)
-    scaled = q / Fraction(2) ** exp   # mantissa as a rational, < 2^24
-    m = scaled.numerator // scaled.denominator
-    rem = scaled - m
-    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and m % 2 == 1):
-        m += 1
-    return f32(sign * float(m) * 2.0 ** exp)
+    """Exact rational sum of float32 values rounded once to float32."""
+    return exact_round_f32(values)
 
 
 @pytest.mark.parametrize("seed", range(6))
@@ -496,7 +477,6 @@ def test_sign_aggregate_exact_form_per_element():
     n, W = 90, 7
     words = [rng.integers(0, 1 << 32, 3, dtype=np.uint64).astype(np.uint32) for _ in range(W)]
     scales = (np.abs(rng.standard_normal(W)) * 1e-3).astype(f32)
-    assert O.sign_exact_applies(scales)
     out = O.aggregate_sign(n, words, scales, 0.25)
     for i in range(n):
         d = [(-scales[w] if (words[w][i // 32] >> (i % 32)) & 1 else scales[w]) for w in range(W)]
@@ -517,22 +497,106 @@ def test_sign_aggregate_exact_is_within_recursive_sum_bound_of_ordered():
     assert np.any(a != b)  # the two forms are genuinely different readings
 
 
-def test_sign_aggregate_wide_scale_span_uses_ordered_form():
-    W = 4
-    limit = O.sign_span_limit(W)
-    assert limit == 27
-    words = [np.array([0x5], np.uint32), np.array([0x3], np.uint32), np.array([0x0], np.uint32),
-             np.array([0x7], np.uint32)]
-    wide = np.array([1.0, 2.0 ** -(limit + 1), 0.5, 0.25], f32)
-    assert not O.sign_exact_applies(wide)
-    assert np.array_equal(O.aggregate_sign(3, words, wide, 1.0),
-                          O.aggregate_sign(3, words, wide, 1.0, ordered=True))
-    narrow = np.array([1.0, 2.0 ** -limit, 0.5, 0.25], f32)
-    assert O.sign_exact_applies(narrow)
-    for bad in (np.array([1.0, np.inf, 1, 1], f32), np.array([1.0, 1e-40, 1, 1], f32)):
-        assert not O.sign_exact_applies(bad)
-    assert O.sign_exact_applies(np.array([0.0, 0.0, 1.0, 1.0], f32))
-    assert O.sign_span_limit(64) == 23 and O.sign_span_limit(65) == 22 and O.sign_span_limit(1) == 29
+def _decoded_sign(words, scales, i):
+    return [(-scales[w] if (words[w][i // 32] >> (i % 32)) & 1 else scales[w]) for w in range(len(scales))]
+
+
+@pytest.mark.parametrize("W", [2, 5, 16, 64])
+@pytest.mark.parametrize("span", [30, 45, 60, 120, 253])
+def test_sign_aggregate_is_exact_at_any_scale_span(W, span):
+    # scales whose binary exponents spread over `span` binades: the output
+    # is still the exact rational sum rounded once (no span-dependent form)
+    rng = np.random.default_rng(1000 * W + span)
+    n = 96
+    words = [rng.integers(0, 1 << 32, 3, dtype=np.uint64).astype(np.uint32) for _ in range(W)]
+    ex = rng.integers(-126, -126 + span + 1, W)
+    ex[0], ex[-1] = -126, -126 + span
+    scales = (np.ldexp(1.0 + rng.random(W), ex)).astype(f32)
+    scales[rng.random(W) < 0.3] *= f32(-1.0)     # negative scales are summed as given
+    out = O.aggregate_sign(n, words, scales, 0.5)
+    for i in range(n):
+        want = f32(f32(0.5) * exact_round(_decoded_sign(words, scales, i)))
+        assert same_f32(out[i], want), (i, out[i], want)
+
+
+def test_sign_aggregate_small_terms_decide_the_rounding():
+    # two large scales cancel or tie at a rounding point; a scale 40 and 60
+    # binades below breaks the tie, which any truncated sum would lose
+    big, half_ulp = f32(1.0), f32(2.0 ** -24)
+    for tiny, wbits, want in [
+        (f32(2.0 ** -64), [0, 0, 0], f32(1.0 + 2.0 ** -23)),   # 1 + half ulp + tiny: up
+        (f32(2.0 ** -64), [0, 0, 1], f32(1.0)),                # 1 + half ulp - tiny: down
+        (f32(2.0 ** -84), [1, 0, 0], f32(-1.0 + 2.0 ** -24)),  # tiny term below the last place
+    ]:
+        words = [np.array([b], np.uint32) for b in wbits]
+        out = O.aggregate_sign(1, words, [big, half_ulp, tiny], 1.0)
+        assert same_f32(out[0], want), (tiny, wbits, out[0], want)
+        assert same_f32(out[0], exact_round(_decoded_sign(words, [big, half_ulp, tiny], 0)))
+
+
+def test_sign_aggregate_subnormal_scales_and_results():
+    # subnormal scales are summed exactly; a subnormal result is exact
+    s = np.array([2.0 ** -149, 3 * 2.0 ** -149, 2.0 ** -130, 2.0 ** -127], f32)
+    rng = np.random.default_rng(5)
+    words = [rng.integers(0, 1 << 32, 2, dtype=np.uint64).astype(np.uint32) for _ in range(4)]
+    out = O.aggregate_sign(64, words, s, 1.0)
+    for i in range(64):
+        assert same_f32(out[i], exact_round(_decoded_sign(words, s, i))), i
+
+
+def test_sign_aggregate_overflow_rounds_to_infinity():
+    fmax = np.finfo(np.float32).max
+    ones, zeros = np.array([0xFFFFFFFF], np.uint32), np.zeros(1, np.uint32)
+    # FLT_MAX + half an ulp is a tie with an odd last bit: rounds up to +Inf
+    out = O.aggregate_sign(1, [zeros, zeros], [fmax, f32(2.0 ** 103)], 1.0)
+    assert out[0] == np.inf
+    out = O.aggregate_sign(1, [zeros, zeros], [fmax, f32(2.0 ** 102)], 1.0)
+    assert out[0] == fmax
+    out = O.aggregate_sign(1, [ones, ones], [fmax, f32(2.0 ** 103)], 1.0)
+    assert out[0] == -np.inf
+    # large terms cancel exactly and leave a finite sum
+    out = O.aggregate_sign(1, [zeros, zeros, ones], [fmax, fmax, fmax], 1.0)
+    assert out[0] == fmax
+
+
+def test_sign_aggregate_non_finite_rule():
+    z, o = np.zeros(1, np.uint32), np.ones(1, np.uint32)
+    inf, nan = f32(np.inf), f32(np.nan)
+    cases = [
+        ([z, z], [inf, f32(1.0)], np.inf),          # +Inf with a finite value
+        ([o, z], [inf, f32(1.0)], -np.inf),         # the bit flips the infinity
+        ([z, o], [inf, inf], np.nan),               # +Inf and -Inf
+        ([z, z], [f32(-np.inf), f32(-1.0)], -np.inf),
+        ([z, z], [nan, f32(1.0)], np.nan),          # NaN wins over everything
+        ([z, z, o], [nan, inf, inf], np.nan),
+    ]
+    for words, scales, want in cases:
+        out = O.aggregate_sign(1, words, scales, 1.0)
+        assert same_f32(out[0], want), (scales, out[0])
+        assert same_f32(out[0], xsum_f32(_decoded_sign(words, scales, 0)))
+
+
+def test_sign_aggregate_is_independent_of_worker_order():
+    # a definition with no addition order: permuting the workers changes
+    # nothing, at any span, with cancellations and non-finite scales
+    rng = np.random.default_rng(9)
+    n, W = 200, 24
+    words = [rng.integers(0, 1 << 32, 7, dtype=np.uint64).astype(np.uint32) for _ in range(W)]
+    scales = np.ldexp(1.0 + rng.random(W), rng.integers(-120, 120, W)).astype(f32)
+    scales[3] = scales[7]
+    for variant in range(3):
+        sc = scales.copy()
+        if variant == 1:
+            sc[5] = np.inf
+        if variant == 2:
+            sc[5], sc[6] = np.inf, np.nan
+        ref = O.aggregate_sign(n, words, sc, 1.0)
+        for _ in range(4):
+            perm = rng.permutation(W)
+            got = O.aggregate_sign(n, [words[p] for p in perm], sc[perm], 1.0)
+            assert same_f32_arrays(got, ref)
+        for i in range(0, n, 17):
+            assert same_f32(ref[i], xsum_f32(_decoded_sign(words, sc, i)))
 
 
 def test_sign_aggregate_zero_bits_and_single_worker():

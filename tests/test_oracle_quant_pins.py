@@ -7,8 +7,8 @@ uniforms, numpy's little-endian byte view for the code packing, the
 hand-worked examples in tests/golden/hand_examples.json, closed forms on
 inputs whose levels are whole numbers, the unbiasedness and variance bound
 of stochastic rounding measured over many seeds, brute-force ordered sums
-for the 4- and 8-bit aggregate (and the 2-bit one outside its exact
-form), and exact rational sums rounded once for the 2-bit exact form.
+for the 4- and 8-bit aggregate, and exact rational sums rounded once (with
+the order-free rule for non-finite scales) for the 2-bit aggregate.
 """
 import json
 import os
@@ -17,6 +17,8 @@ import numpy as np
 import pytest
 
 import oracle as O
+
+from .exact_ref import exact_round_f32, same_f32, xsum_f32
 
 f32 = np.float32
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_examples.json")
@@ -223,16 +225,14 @@ def test_zero_and_empty_tensors(bits):
     assert np.array_equal(e_new.view(np.uint32), ((v + e).astype(f32)).view(np.uint32))
 
 
-@pytest.mark.parametrize("bits", BITS)
+@pytest.mark.parametrize("bits", (4, 8))
 def test_aggregate_ordered_bruteforce(bits):
-    # 2-bit codes take the ordered form only when their scales spread wider
-    # than the exact form allows: worker w's gradient is scaled by 2^(3w)
+    # 4- and 8-bit codes: worker-ordered fp32 sums; worker w's gradient is
+    # scaled by 2^(3w) so that the additions round
     rng = np.random.default_rng(90 + bits)
     n, W = 37, 5
     pays = [O.compress_quant((rng.standard_normal(n) * 10.0 ** rng.uniform(-3, 0) * 2.0 ** (3 * w)).astype(f32),
                              None, bits, 100 + w, 0)[:2] for w in range(W)]
-    if bits == 2:
-        assert not O.tern_exact_applies([p[1] for p in pays])
     alpha = f32(0.25)
     got = O.aggregate_quant(n, bits, [p[0] for p in pays], [p[1] for p in pays], float(alpha))
     for i in range(n):
@@ -246,46 +246,6 @@ def test_aggregate_ordered_bruteforce(bits):
                           (f32(0.0) + decode_np(unpack_codes(pays[0][0], n, bits), bits, pays[0][1])).view(np.uint32))
 
 
-def exact_round_f32(values):
-    """Exact rational sum of float32 values rounded once to float32 (round
-    to nearest, ties to even, done on the rational)."""
-    from fractions import Fraction
-    q = sum((Fraction(float(v)) for v in values), Fraction(0))
-    if q == 0:
-        return f32(0.0)
-    sign = -1 if q < 0 else 1
-    q = abs(q)
-    e = q.numerator.bit_length() - q.denominator.bit_length()
-    if Fraction(2) ** e > q:
-        e -= 1
-    ex = max(e, -126) - 23
-    sc = q / Fraction(2) ** ex
-    m = sc.numerator // sc.denominator
-    rem = sc - m
-    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and m % 2 == 1):
-        m += 1
-    return f32(sign * float(m) * 2.0 ** ex)
-
-
-def test_tern_span_limit_closed_form():
-    # 24 mantissa bits + span + log2(W rounded up to a multiple of 4) <= 31
-    for W in range(1, 65):
-        w4 = 4 * ((W + 3) // 4)
-        assert O.tern_span_limit(W) == 7 - (w4 - 1).bit_length()
-    assert O.tern_span_limit(64) == 1 and O.tern_span_limit(4) == 5
-
-
-def test_tern_exact_applies_rule():
-    one = f32(1.0)
-    assert O.tern_exact_applies([one] * 64)
-    assert not O.tern_exact_applies([one] * 65)              # more than 64 workers
-    assert O.tern_exact_applies([one, f32(3.9), f32(0.0)] * 20)   # span 1, zeros ignored
-    assert not O.tern_exact_applies([one, f32(4.0)] * 32)    # span 2 > 1 at W = 64
-    assert O.tern_exact_applies([one, f32(4.0)] * 2)         # W = 4: limit 5
-    assert not O.tern_exact_applies([one, f32(np.inf)])
-    assert not O.tern_exact_applies([one, f32(1e-40)])       # subnormal
-
-
 @pytest.mark.parametrize("W", [1, 3, 16, 64])
 def test_terngrad_aggregate_exact_form_per_element(W):
     # the exact rational sum of the decoded values, rounded once, times alpha
@@ -296,7 +256,6 @@ def test_terngrad_aggregate_exact_form_per_element(W):
         g = (rng.standard_normal(n) * 1e-3 * (1 + 0.05 * rng.standard_normal())).astype(f32)
         pays.append(O.compress_quant(g, None, 2, 500 + w, 0)[:2])
     scales = [p[1] for p in pays]
-    assert O.tern_exact_applies(scales)
     alpha = f32(1.0 / W)
     got = O.aggregate_quant(n, 2, [p[0] for p in pays], scales, float(alpha))
     dec = [decode_np(unpack_codes(wds, n, 2), 2, m) for wds, m in pays]
@@ -322,6 +281,44 @@ def test_terngrad_aggregate_exact_differs_from_ordered_somewhere():
     assert np.any(got.view(np.uint32) != ordered.view(np.uint32))
     exact64 = dec.astype(np.float64).sum(axis=0)  # exact: 24 + 1 + 6 bits
     assert np.array_equal(got, exact64.astype(f32))
+
+
+@pytest.mark.parametrize("W", [2, 7, 64, 100])
+def test_terngrad_aggregate_exact_at_wide_spans(W):
+    # worker scales spread over up to 200 binades (subnormal ones included):
+    # still the exact sum of the decoded values, rounded once
+    rng = np.random.default_rng(700 + W)
+    n = 45
+    pays = []
+    for w in range(W):
+        g = (rng.standard_normal(n) * 2.0 ** int(rng.integers(-140, 60))).astype(f32)
+        pays.append(O.compress_quant(g, None, 2, 800 + w, 0)[:2])
+    scales = [p[1] for p in pays]
+    got = O.aggregate_quant(n, 2, [p[0] for p in pays], scales, 0.5)
+    dec = [decode_np(unpack_codes(wds, n, 2), 2, m) for wds, m in pays]
+    for i in range(n):
+        want = f32(f32(0.5) * exact_round_f32([d[i] for d in dec]))
+        assert same_f32(got[i], want), i
+
+
+def test_terngrad_aggregate_non_finite_scales():
+    # a level-0 code decodes to 0 whatever the scale; a nonzero code of an
+    # infinite or NaN scale follows the order-free rule
+    def word(codes):
+        return np.array([sum(int(c) << (2 * q) for q, c in enumerate(codes))], np.uint32)
+    inf, nan = f32(np.inf), f32(np.nan)
+    cases = [
+        ([[0, 1], [1, 1]], [nan, f32(2.0)], [2.0, np.nan]),      # NaN scale, level 0 then 1
+        ([[1, 3], [1, 1]], [inf, f32(2.0)], [np.inf, -np.inf]),  # code 3: -scale
+        ([[1, 1], [3, 0]], [inf, inf], [np.nan, np.inf]),        # +Inf and -Inf
+    ]
+    for codes, scales, want in cases:
+        words = [word(c) for c in codes]
+        got = O.aggregate_quant(2, 2, words, scales, 1.0)
+        for i in range(2):
+            dec = [O.quant_decode((int(wd[0]) >> (2 * i)) & 3, 2, sc) for wd, sc in zip(words, scales)]
+            assert same_f32(got[i], want[i]), (codes, scales, i, got[i])
+            assert same_f32(got[i], xsum_f32(dec))
 
 
 @pytest.mark.parametrize("kind", ["terngrad", "qsgd4", "qsgd8"])

@@ -201,18 +201,17 @@ int bytecomp_compress_dgc(int kind, double ratio, uint64_t seed, float momentum,
  * Sparse kinds: out_t[i] = alpha * (sum over workers w = 0..W-1, in that
  * order, of worker w's value at i), each addition in fp32 starting from
  * +0.0; elements no worker sent are alpha * 0.
- * BC_SIGN1: out_t[i] = alpha * fl32(exact sum over w of d_w,i), d_w,i =
- * -s_w,t if worker w's bit i is set, else +s_w,t: the exact real sum
- * rounded once to fp32.  This form applies when tensor t's W scales are
- * finite and normal or zero and their binary exponents span at most
- * 29 - ceil(log2 W) binades; otherwise the worker-ordered fp32 sum, as for
- * the sparse kinds.  BC_QSGD4, BC_QSGD8: out_t[i] = alpha * (sum over
- * w = 0..W-1, in that order, of worker w's decoded value at i), each
- * addition in fp32 starting from +0.0.  BC_TERNGRAD (decoded values 0 or
- * +-s_w,t): as BC_SIGN1, the exact sum rounded once, when W <= 64 and the
- * tensor's nonzero scales are finite and normal and span at most
- * 7 - ceil(log2 W4) binades (W4 = W rounded up to a multiple of 4);
- * otherwise the worker-ordered fp32 sum.  Quantizers: at most 1024 workers
+ * BC_SIGN1: out_t[i] = alpha * X(d_0,i, ..., d_W-1,i), d_w,i = -s_w,t if
+ * worker w's bit i is set, else +s_w,t, where X is the sum every order of
+ * exact arithmetic reaches: NaN if some d is NaN or both +Inf and -Inf
+ * occur, else +-Inf if an infinity occurs, else the exact real sum of the
+ * d rounded once to fp32 (nearest, ties to even; an exact zero gives +0.0;
+ * past the fp32 range, an infinity).  This holds for every scale set
+ * (subnormal, negative, widely spread or non-finite scales included).
+ * BC_QSGD4, BC_QSGD8: out_t[i] = alpha * (sum over w = 0..W-1, in that
+ * order, of worker w's decoded value at i), each addition in fp32 starting
+ * from +0.0.  BC_TERNGRAD (decoded values 0 or +-s_w,t): alpha * X of the
+ * decoded values, as for BC_SIGN1.  Quantizers: at most 1024 workers
  * (BC_E_COUNT otherwise).
  * Results are deterministic. */
 int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, int W,

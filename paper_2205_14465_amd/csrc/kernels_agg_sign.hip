@@ -9,11 +9,14 @@
 // its W scales and builds its lookup tables: int32 tables of eight-worker
 // partial sums (in units of the smallest scale's last place) when the
 // exponents span few enough binades for 32-bit sums, fp64 tables while the
-// span fits fp64 exactly; past that the worker-ordered fp32 sum is used.
+// span fits fp64 exactly; other scale sets (wider spans, subnormal or
+// non-finite scales) take the multi-word exact path of exact_wide.hpp, so
+// every tensor gets the same definition whatever path computes it.
 // The aggregate kernel takes one 4096-element unit per workgroup, gathers
 // each element's eight-worker bytes with a byte permute and an 8x8 bit
 // transpose, sums the table entries, and stores through LDS for coalesced
 // writes.
+#include "exact_wide.hpp"
 #include "launch.hpp"
 
 namespace bc {
@@ -25,8 +28,6 @@ typedef const float __attribute__((address_space(4)))* cf32p;
 }  // namespace
 
 namespace {
-
-constexpr int kSignGroup = 4;  // workers whose words are in flight together (ordered form)
 
 // Word at a 32-bit byte offset from a wave-uniform base: the form the
 // backend emits as a global load with an SGPR base and a VGPR offset.
@@ -59,21 +60,6 @@ __host__ __device__ __forceinline__ void transpose_bytes8(uint32_t (&x)[8]) {
         const uint32_t t = ((x[i] >> 1) ^ x[i + 1]) & 0x55555555u;
         x[i + 1] ^= t;
         x[i] ^= t << 1;
-    }
-}
-
-// Ordered form: acc[q] += (bit q of half) ? -s : +s for the lane's 16
-// elements, one fp32 addition per element and worker in worker order: the
-// bit is moved to the sign position (v_lshlrev) and spliced into s (v_bfi).
-__device__ __forceinline__ void sign_half_accumulate(float (&acc)[16], uint32_t half, float s) {
-    const uint32_t su = f2u(s);
-    const uint32_t sign = 0x80000000u;
-#pragma unroll
-    for (int q = 0; q < 16; ++q) {
-        const uint32_t t = half << (31 - q);
-        uint32_t d;
-        asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(d) : "v"(sign), "v"(t), "v"(su));
-        acc[q] += u2f(d);
     }
 }
 
@@ -165,34 +151,6 @@ __device__ __forceinline__ void lookup_step_half(double (&S)[8], const uint32_t*
     }
 }
 
-// Scales of tensor t into sc[] and its form: 0 ordered, 1 int32 exact,
-// 2 fp64 exact; emin = smallest biased exponent of its normal scales.
-__device__ __forceinline__ void tensor_form(const uint64_t* __restrict__ wp, int W, int t, float* sc,
-                                            int* emin_sh, int* emax_sh, int* bad_sh, int span_limit,
-                                            int int_span_limit, int& form, int& emin) {
-    __syncthreads();  // the previous tensor's scales and tables are done with
-    if (threadIdx.x == 0) {
-        *emin_sh = 1000;
-        *emax_sh = -1000;
-        *bad_sh = 0;
-    }
-    __syncthreads();
-    for (int w = threadIdx.x; w < W; w += kBlock) {
-        const float sv = ((cf32p)w_b(wp, W, w))[t];
-        sc[w] = sv;
-        const uint32_t e = (f2u(sv) >> 23) & 255u;
-        if (e == 255u || (e == 0u && (f2u(sv) & 0x7FFFFFu))) atomicOr(bad_sh, 1);
-        else if (e) {
-            atomicMin(emin_sh, (int)e);
-            atomicMax(emax_sh, (int)e);
-        }
-    }
-    __syncthreads();
-    const int span = *emax_sh < *emin_sh ? 0 : *emax_sh - *emin_sh;
-    form = *bad_sh ? 0 : span <= int_span_limit ? 1 : span <= span_limit ? 2 : 0;
-    emin = *emax_sh < *emin_sh ? 1 : *emin_sh;
-}
-
 __device__ __forceinline__ void store16(const ADesc& ad, uint32_t e0, const float (&res)[16]) {
     float* out = ad.out + e0;
     if (e0 + 16u <= ad.n) {
@@ -218,8 +176,8 @@ __device__ __forceinline__ void store16(const ADesc& ad, uint32_t e0, const floa
 // int_span_limit binades every scale is an integer multiple of 2^(emin-150)
 // below 2^(24+span), and the whole sum stays below 2^31 in those units:
 // tables and sums are int32.  Up to span_limit binades they are fp64 (every
-// partial sum exact).  Ordered form (non-finite or subnormal scales, or a
-// wider span): worker-ordered fp32 additions.
+// partial sum exact).  Other scale sets (non-finite or subnormal scales, or
+// a wider span): the exact sum in 288-bit integer limbs (exact_wide.hpp).
 //
 // Two launches: sign_agg_prep (one wave per tensor) classifies each tensor
 // and, for up to 64 workers, writes its int32 tables to the workspace;
@@ -354,24 +312,10 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
         for (int w = threadIdx.x; w < W; w += kBlock) sc[w] = ((cf32p)w_b(wp, W, w))[t];
         __syncthreads();
         if (form == 0) {
-            float acc[16];
-#pragma unroll
-            for (int q = 0; q < 16; ++q) acc[q] = 0.f;
-            for (int w0 = 0; w0 < W; w0 += kSignGroup) {
-                uint32_t word[kSignGroup];
-                float sv[kSignGroup];
-#pragma unroll
-                for (int g = 0; g < kSignGroup; ++g) {
-                    const int w = w0 + g < W ? w0 + g : W - 1;
-                    sv[g] = sc[w];
-                    word[g] = ld_word(w_a(wp, w), wload);
-                }
-#pragma unroll
-                for (int g = 0; g < kSignGroup; ++g)
-                    if (w0 + g < W) sign_half_accumulate(acc, word[g] >> (16u * h), sv[g]);
-            }
-#pragma unroll
-            for (int q = 0; q < 16; ++q) res[q] = alpha * acc[q];
+            // scales the tables cannot hold exactly: the wide exact path
+            // writes the unit's outputs itself
+            aggregate_unit_exact_wide<0>(ad, u, wp, W, alpha, sc, reinterpret_cast<unsigned char*>(lds));
+            return;
         } else {
             // fp64 tables (exact for the int32 form's tensors too), the
             // lane's sixteen elements in two halves of eight

@@ -19,6 +19,7 @@
 // shuffles and writes the residual.  The aggregate gives each workgroup
 // 4096 output elements (16 per lane) and adds the W workers' decoded values
 // in worker order, one fp32 addition each.
+#include "exact_wide.hpp"
 #include "launch.hpp"
 
 namespace bc {
@@ -372,8 +373,9 @@ __global__ __launch_bounds__(kBlock) void quant_residual_update(const TDesc* __r
 // is an integer multiple of 2^(emin-150) below 2^(24+span), and the sum of
 // W of them stays below 2^31: int32 arithmetic is exact.  Workers go in
 // groups of four; a group's four 2-bit codes of an element form an 8-bit
-// index into a 256-entry table of the group's sums.  Other scale sets take
-// the worker-ordered fp32 path.
+// index into a 256-entry table of the group's sums.  Other scale sets (wider
+// spans, subnormal or non-finite scales, more than 64 workers) take the
+// multi-word exact path of exact_wide.hpp: one definition for every tensor.
 namespace {
 constexpr int kTernTab = 16 * 256;  // int32 entries per tensor: 16 groups of four workers
 
@@ -391,7 +393,7 @@ __device__ __forceinline__ int32_t tern_code_value(uint32_t code, int32_t sv) {
 }
 }  // namespace
 
-// One wave per tensor: its form (info[t]: 1 exact, 0 ordered; emin in bits
+// One wave per tensor: its form (info[t]: 1 tables, 0 wide exact path; emin in bits
 // 8-15) and, for the exact form, its tables: tab[256 g + p] is the sum over
 // the four workers 4g + c of the value of code (p >> 2c) & 3, built from two
 // two-worker tables of 16 entries.  Workers past W count as zero.
@@ -492,10 +494,11 @@ __device__ __forceinline__ void tern_indices(const uint32_t (&x)[4], uint32_t (&
 // and adding either zero to a value that is not -0.0 gives the same
 // result, so the sums are those of the +0.0 decoding.
 //
-// 2-bit codes of a tensor in the exact form (info[t] & 255 == 1) take the
-// table path instead: the workgroup copies the tensor's tables into LDS,
-// loads the words of all (at most 16 kTS) workers at once, and adds one
-// table entry per element and group of four workers in int32.
+// 2-bit codes (TernGrad) are summed exactly.  A tensor in the table form
+// (info[t] & 255 == 1) takes the table path: the workgroup copies the
+// tensor's tables into LDS, loads the words of all (at most 16 kTS) workers
+// at once, and adds one table entry per element and group of four workers
+// in int32.  Other tensors take the wide exact path.
 template <int kBits, int kTS>
 __global__ __launch_bounds__(kBlock) void aggregate_quant(const ADesc* __restrict__ a, int T, uint32_t U,
                                                           const uint64_t* __restrict__ wp, int W, float alpha,
@@ -506,6 +509,7 @@ __global__ __launch_bounds__(kBlock) void aggregate_quant(const ADesc* __restric
     using Q = Quant<kBits>;
     __shared__ float unit_sh[1024];
     __shared__ __attribute__((aligned(16))) int32_t tab_sh[kBits == 2 ? 256 * 4 * kTS : 4];
+    static_assert(kBits != 2 || sizeof(tab_sh) >= kWideScratchBytes, "wide-path scratch");
     const uint32_t u = blockIdx.x;
     const int t = unit_owner(wp, W, u);
     const ADesc ad = a[t];
@@ -543,7 +547,14 @@ __global__ __launch_bounds__(kBlock) void aggregate_quant(const ADesc* __restric
     for (int q = 0; q < 16; ++q) acc[q] = 0.f;
     if constexpr (kBits == 2) {
         const uint32_t inf = info[t];
-        if ((inf & 255u) == 1u) {
+        if ((inf & 255u) != 1u) {
+            // scales the int32 tables cannot hold exactly (or more than 64
+            // workers): the wide exact path writes the unit's outputs itself
+            aggregate_unit_exact_wide<1>(ad, u, wp, W, alpha, unit_sh,
+                                         reinterpret_cast<unsigned char*>(tab_sh));
+            return;
+        }
+        {
             const int G4 = (W + 3) / 4;  // <= 4 kTS
             const int32_t* tt = tabs + (size_t)t * kTernTab;
             uint32_t wv[16 * kTS];
@@ -596,9 +607,7 @@ __global__ __launch_bounds__(kBlock) void aggregate_quant(const ADesc* __restric
         }
     };
     int w0 = 0;
-    if constexpr (kBits == 2) {
-        if ((info[t] & 255u) == 1u) w0 = W;  // summed on the table path
-    }
+    if constexpr (kBits == 2) w0 = W;  // summed on the table path
     for (; w0 + kGroup <= W; w0 += kGroup) {
         uint32_t wd[kGroup][kWords];
 #pragma unroll

@@ -12,7 +12,8 @@ import numpy as np
 import pytest
 
 import oracle as O
-from tests.helpers import (assert_resid_equal, assert_sign_close, assert_sparse_equal, bits,
+from tests.exact_ref import same_f32_arrays
+from tests.helpers import (_first_diff, assert_resid_equal, assert_sign_close, assert_sparse_equal, bits,
                            gpu_aggregate, gpu_compress)
 from paper_2205_14465_amd import workloads as WL
 
@@ -381,61 +382,97 @@ def test_sign_aggregate_ragged(W):
         assert np.array_equal(bits(got[t]), bits(want[t])), t
 
 
-@pytest.mark.parametrize("W", [4, 64])
-def test_sign_aggregate_wide_scale_span_takes_ordered_form(W):
-    # a tensor whose worker scales span more binades than fp64 can sum exactly
-    # is aggregated in worker order; its neighbour keeps the exact form
-    rng = np.random.default_rng(33 + W)
-    ns = [8192 + 100, 5000]
+def _sign_payloads(rng, ns, per_t):
+    """W sign payloads over tensors ns; per_t[t][w] is worker w's scale of
+    tensor t."""
     wc = [O.words_for(n) for n in ns]
-    limit = O.sign_span_limit(W)
-    payloads = []
-    for w in range(W):
-        words = WL.random_sign_words(rng, ns, wc)
-        wide = np.float32(1e-3 * 2.0 ** -(limit + 2) if w == 1 else 1e-3 * (1 + 0.05 * rng.standard_normal()))
-        narrow = np.float32(1e-3 * (1 + 0.05 * rng.standard_normal()))
-        payloads.append({"bits": np.concatenate(words), "scale": np.array([wide, narrow], np.float32),
-                         "off": O.word_offsets(ns)})
-    assert not O.sign_exact_applies([p["scale"][0] for p in payloads])
-    assert O.sign_exact_applies([p["scale"][1] for p in payloads])
-    got = gpu_aggregate("sign", 0.01, ns, payloads, 1.0)
-    want = O.aggregate_set("sign", ns, payloads, 1.0)
-    for t in range(len(ns)):
-        assert np.array_equal(bits(got[t]), bits(want[t])), t
-
-
-def _scales_with_span(rng, W, span):
-    """W fp32 scales near 1e-3 whose binary exponents span exactly `span`
-    binades (worker 0 at the low end, worker 1 at the high end)."""
-    base = np.float32(2.0 ** -10)
-    s = (base * (1 + rng.random(W))).astype(np.float32)  # exponent -10
-    if W >= 2:
-        s[0] = base * np.float32(1.25)
-        s[1] = np.float32(base * np.float32(2.0 ** span) * np.float32(1.5))
-    return s
-
-
-@pytest.mark.parametrize("W", [8, 32, 64, 71, 128, 130])
-def test_sign_aggregate_exact_forms_by_scale_span(W):
-    # one call whose tensors fall in every form: int32 tables (spans up to
-    # 7 - ceil(log2(8 ceil(W/8)))), fp64 tables (up to 29 - ceil(log2 W)),
-    # and the worker-ordered sum beyond; results match the oracle bit for bit
-    rng = np.random.default_rng(51 + W)
-    limit = O.sign_span_limit(W)
-    int_limit = 7 - int(np.ceil(np.log2(8 * ((W + 7) // 8))))
-    spans = sorted({0, 1, max(int_limit, 0), int_limit + 1, limit - 1, limit, limit + 1, limit + 5})
-    spans = [sp for sp in spans if sp >= 0]
-    ns = [4096 * 3 + 77 if i % 2 == 0 else 5000 + 31 * i for i in range(len(spans))]
-    wc = [O.words_for(n) for n in ns]
-    per_t = [_scales_with_span(rng, W, sp) for sp in spans]
+    W = len(per_t[0])
     payloads = []
     for w in range(W):
         words = WL.random_sign_words(rng, ns, wc)
         payloads.append({"bits": np.concatenate(words),
                          "scale": np.array([per_t[t][w] for t in range(len(ns))], np.float32),
                          "off": O.word_offsets(ns)})
-    for t, sp in enumerate(spans):
-        assert O.sign_exact_applies(per_t[t]) == (sp <= limit), (t, sp)
+    return payloads
+
+
+def _scales_with_span(rng, W, span, base_exp=-10):
+    """W fp32 scales whose binary exponents span exactly `span` binades
+    (worker 0 at the low end, worker 1 at the high end), random signs for
+    the wide spans."""
+    base = np.float32(2.0 ** base_exp)
+    s = (base * (1 + rng.random(W))).astype(np.float32)
+    if W >= 2:
+        s[0] = base * np.float32(1.25)
+        s[1] = np.float32(np.ldexp(1.5, base_exp + span))
+        if W > 2:
+            s[2:] = np.ldexp(1.0 + rng.random(W - 2), rng.integers(base_exp, base_exp + span + 1, W - 2))
+    return s
+
+
+def _gpu_tiers(W):
+    """Binade spans the kernel's int32 and fp64 table forms take (the test
+    aims tensors at both sides of each; the result must not depend on it)."""
+    int_limit = 7 - int(np.ceil(np.log2(8 * ((W + 7) // 8))))
+    f64_limit = 29 - int(np.ceil(np.log2(W))) if W > 1 else 29
+    return int_limit, f64_limit
+
+
+@pytest.mark.parametrize("W", [4, 64, 130])
+def test_sign_aggregate_wide_scale_spans_are_exact(W):
+    # tensors whose worker scales spread over 30 to 253 binades, beside a
+    # narrow one: every output is the exact sum rounded once
+    rng = np.random.default_rng(33 + W)
+    spans = [30, 45, 60, 120, 253]
+    ns = [8192 + 100, 5000, 4096 * 2, 77, 4097, 3000]
+    per_t = [_scales_with_span(rng, W, sp, base_exp=-126) for sp in spans]
+    per_t.append((1e-3 * (1 + 0.05 * rng.standard_normal(W))).astype(np.float32))
+    payloads = _sign_payloads(rng, ns, per_t)
+    got = gpu_aggregate("sign", 0.01, ns, payloads, 1.0 / W)
+    want = O.aggregate_set("sign", ns, payloads, 1.0 / W)
+    for t in range(len(ns)):
+        assert same_f32_arrays(got[t], want[t]), (t, _first_diff(bits(got[t]), bits(want[t])))
+
+
+@pytest.mark.parametrize("W", [3, 64])
+def test_sign_aggregate_subnormal_negative_and_non_finite_scales(W):
+    # subnormal scales, negative scales, sums past the fp32 range, and NaN
+    # or infinite scales (the order-free rule), each in its own tensor
+    rng = np.random.default_rng(90 + W)
+    fmax = np.float32(np.finfo(np.float32).max)
+    ns = [4096 + 5, 300, 2000, 129, 4096 * 2, 64]
+    per_t = []
+    per_t.append(np.ldexp(1.0 + rng.random(W), rng.integers(-149, -126, W)).astype(np.float32))  # subnormal
+    per_t.append((-np.abs(rng.standard_normal(W)) * 1e-3).astype(np.float32))                    # negative
+    per_t.append(np.full(W, fmax, np.float32))                                                   # overflow
+    t3 = (1e-3 * (1 + rng.random(W))).astype(np.float32)
+    t3[W // 2] = np.inf
+    per_t.append(t3)                                                                             # one +Inf
+    t4 = (1e-3 * (1 + rng.random(W))).astype(np.float32)
+    t4[0], t4[-1] = np.inf, -np.inf
+    per_t.append(t4)                                                                             # both
+    t5 = (1e-3 * (1 + rng.random(W))).astype(np.float32)
+    t5[1 % W] = np.nan
+    per_t.append(t5)                                                                             # NaN
+    payloads = _sign_payloads(rng, ns, per_t)
+    got = gpu_aggregate("sign", 0.01, ns, payloads, 0.5)
+    want = O.aggregate_set("sign", ns, payloads, 0.5)
+    for t in range(len(ns)):
+        assert same_f32_arrays(got[t], want[t]), (t, _first_diff(bits(got[t]), bits(want[t])))
+
+
+@pytest.mark.parametrize("W", [8, 32, 64, 71, 128, 130])
+def test_sign_aggregate_exact_forms_by_scale_span(W):
+    # one call whose tensors fall on both sides of each of the kernel's
+    # table forms (int32, fp64) and far beyond them: results match the
+    # oracle's exact sum bit for bit whatever path computes them
+    rng = np.random.default_rng(51 + W)
+    int_limit, limit = _gpu_tiers(W)
+    spans = sorted({0, 1, max(int_limit, 0), int_limit + 1, limit - 1, limit, limit + 1, limit + 5, 40, 60})
+    spans = [sp for sp in spans if sp >= 0]
+    ns = [4096 * 3 + 77 if i % 2 == 0 else 5000 + 31 * i for i in range(len(spans))]
+    per_t = [_scales_with_span(rng, W, sp) for sp in spans]
+    payloads = _sign_payloads(rng, ns, per_t)
     got = gpu_aggregate("sign", 0.01, ns, payloads, 1.0 / W)
     want = O.aggregate_set("sign", ns, payloads, 1.0 / W)
     for t in range(len(ns)):
@@ -446,7 +483,7 @@ def test_sign_aggregate_exact_forms_by_scale_span(W):
 def test_sign_aggregate_integer_form_extremes(W):
     # largest sums the int32 form admits: every scale at the top of the
     # widest span it takes, all signs equal (both polarities) and mixed
-    int_limit = 7 - int(np.ceil(np.log2(8 * ((W + 7) // 8))))
+    int_limit, _ = _gpu_tiers(W)
     top = np.float32(np.nextafter(np.float32(2.0 ** (-9 + int_limit)), np.float32(0)))
     scales = np.full(W, top, np.float32)
     scales[0] = np.float32(2.0 ** -10)  # sets emin, so the span is int_limit

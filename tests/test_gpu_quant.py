@@ -12,6 +12,7 @@ import numpy as np
 import pytest
 
 import oracle as O
+from tests.exact_ref import same_f32_arrays
 from tests.helpers import assert_resid_equal, bits, gpu_aggregate, gpu_compress
 
 pytestmark = pytest.mark.gpu
@@ -176,8 +177,6 @@ def test_terngrad_aggregate_exact_form(W):
     rng = np.random.default_rng(700 + W)
     ns = [1, 15, 16, 17, 4095, 4096, 4097, 3 * 4096 + 33, 0, 50000]
     pays = _tern_payloads(rng, ns, W, 0)
-    for t in range(len(ns)):
-        assert O.tern_exact_applies([p["scale"][t] for p in pays])
     got = gpu_aggregate("terngrad", 1.0, ns, pays, 1.0 / W)
     want = O.aggregate_set("terngrad", ns, pays, 1.0 / W)
     for t, n in enumerate(ns):
@@ -186,21 +185,27 @@ def test_terngrad_aggregate_exact_form(W):
 
 @pytest.mark.parametrize("W", [8, 64, 65, 72])
 def test_terngrad_aggregate_mixed_forms(W):
-    # tensors of one call in both forms: wide spreads and zero scales among
-    # narrow ones, and more than 64 workers (ordered throughout)
+    # tensors of one call on both sides of the kernel's table form: spreads
+    # of a few binades and of 40 to 200, zero, subnormal and non-finite
+    # scales among narrow ones, and more than 64 workers (no tables); every
+    # output is the exact sum rounded once (NaN where the rule says so)
     rng = np.random.default_rng(800 + W)
-    ns = [5000, 4096 * 5 + 7, 300, 12000]
+    ns = [5000, 4096 * 5 + 7, 300, 12000, 4100, 999, 64]
     pays = _tern_payloads(rng, ns, W, 0)
     for w, p in enumerate(pays):
-        p["scale"][1] = np.float32(p["scale"][1] * 2.0 ** (3 * (w % 4)))  # spread: ordered
+        p["scale"][1] = np.float32(p["scale"][1] * 2.0 ** (3 * (w % 4)))       # a few binades
         if w == 2:
-            p["scale"][2] = np.float32(0.0)                             # a zero scale: still exact
-    forms = [O.tern_exact_applies([p["scale"][t] for p in pays]) for t in range(len(ns))]
-    assert forms == ([True, False, True, True] if W <= 64 else [False] * 4)
+            p["scale"][2] = np.float32(0.0)                                 # a zero scale
+        p["scale"][3] = np.float32(np.ldexp(1.0 + rng.random(), int(rng.integers(-100, 100))))  # ~200
+        p["scale"][4] = np.float32(np.ldexp(1.0 + rng.random(), int(rng.integers(-149, -127))))  # subnormal
+        if w == 1:
+            p["scale"][5] = np.float32(np.inf)
+        if w == W - 1:
+            p["scale"][6] = np.float32(np.nan)
     got = gpu_aggregate("terngrad", 1.0, ns, pays, 0.25)
     want = O.aggregate_set("terngrad", ns, pays, 0.25)
     for t, n in enumerate(ns):
-        assert np.array_equal(bits(got[t]), bits(want[t])), (t, n)
+        assert same_f32_arrays(got[t], want[t]), (t, n)
 
 
 @pytest.mark.parametrize("kind", KINDS)

@@ -268,21 +268,33 @@ int bytecomp_residual_update(int kind, double ratio, const bc_tensor* t, int T,
                              bc_payload own, void* stream);
 
 /* Read (synchronously, on `stream`) and clear the kernel failure flags a
- * workspace holds; *flags receives them (0 = none).  Bit 0: a bounded wait
- * between workgroups of a one-pass compress kernel ran out (the results of
- * that call are not to be trusted). */
+ * workspace holds; *flags receives them (0 = none).  No kernel of this
+ * version sets one (bit 0 is reserved). */
 int bytecomp_device_status(void* ws, size_t ws_bytes, void* stream, uint32_t* flags);
+
+/* Wait limit of the one-pass compress kernels (BC_SIGN1 and the quantizers
+ * when every tensor fits the GPU's resident grid), process-wide.  Their
+ * workgroups defer each chunk's residual (and codes) until the tensor's
+ * scale, which needs a partial result of every chunk, is known, and wait
+ * for the other chunks' partials at most `microseconds`.  Past that (the
+ * grid not wholly resident, e.g. beside other kernels) a waiting workgroup
+ * computes the missing partials itself, bit-identical to their owners'
+ * (the same fixed-order arithmetic), so the results are the same either
+ * way, only later.  0 makes every such wait do so at once (for tests of
+ * that path).  Default 200; BC_E_SIZE above 10 s. */
+int bytecomp_set_wait_limit(uint32_t microseconds);
 
 /* Instrumentation, not part of the method: for callers that measure one
  * kernel's own duration (benchmarks).  The next launch, by any call, of
  * the kernel named `kernel` ("aggregate_sign", "aggregate_sparse",
- * "randk_stream", "topk_compact", "sign_pass1" (the first sign compress
- * kernel: its one-pass form when it runs), "quant_pass1",
- * "aggregate_quant") records `start_event`
- * when it begins and `stop_event` when it ends (HIP events created by the
- * caller, on the launch's stream); the request is then cleared.  Both
- * events NULL clears a pending request.  BC_E_KIND for an unknown name.
- * One request is held at a time, process-wide. */
+ * "randk_stream", "topk_compact", "sign_onepass", "sign_pass1" (the first
+ * kernel of the two-pass sign compress), "quant_onepass", "quant_pass1",
+ * "aggregate_quant") records `start_event` when it begins and `stop_event`
+ * when it ends (HIP events created by the caller, on the launch's stream);
+ * the request is then cleared.  Both events NULL clears a pending request
+ * and returns 1 if one was pending (the named kernel did not run since the
+ * request), 0 otherwise.  BC_E_KIND for an unknown name.  One request is
+ * held at a time, process-wide. */
 int bytecomp_time_next_launch(const char* kernel, void* start_event, void* stop_event);
 
 #ifdef __cplusplus

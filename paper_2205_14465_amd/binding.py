@@ -87,6 +87,8 @@ def lib():
                                               ctypes.c_float, vp, sz, vp]
         L.bytecomp_time_next_launch.restype = i32
         L.bytecomp_time_next_launch.argtypes = [ctypes.c_char_p, vp, vp]
+        L.bytecomp_set_wait_limit.restype = i32
+        L.bytecomp_set_wait_limit.argtypes = [ctypes.c_uint32]
         _lib = L
     return _lib
 
@@ -233,13 +235,23 @@ def bytecomp_aggregate_part(kind, ratio, parts, part_offs, lens, outs, alpha, ws
 def bytecomp_time_next_launch(kernel, start_event, stop_event):
     """Have the next launch of `kernel` bracketed by two torch.cuda.Event
     objects (recorded once before, so that their HIP events exist); None
-    for both clears a pending request."""
+    for both clears a pending request and returns True if one was pending
+    (the kernel did not run since the request)."""
     if start_event is None and stop_event is None:
-        _check("bytecomp_time_next_launch", lib().bytecomp_time_next_launch(None, None, None))
-        return
+        rc = lib().bytecomp_time_next_launch(None, None, None)
+        if rc < 0:
+            _check("bytecomp_time_next_launch", rc)
+        return rc == 1
     _check("bytecomp_time_next_launch",
            lib().bytecomp_time_next_launch(kernel.encode(), ctypes.c_void_p(start_event.cuda_event),
                                            ctypes.c_void_p(stop_event.cuda_event)))
+
+
+def bytecomp_set_wait_limit(microseconds):
+    """How long a one-pass compress workgroup waits for the rest of its
+    tensor's chunk partials before it computes the missing ones itself
+    (process-wide; default 200)."""
+    _check("bytecomp_set_wait_limit", lib().bytecomp_set_wait_limit(int(microseconds)))
 
 
 def bytecomp_device_status(ws, stream=None):

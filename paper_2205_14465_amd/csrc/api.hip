@@ -172,6 +172,9 @@ hipError_t device_info(int dev, DevInfo* out) {
         DevInfo di;
         di.cus = p.multiProcessorCount;
         di.any_empty = false;
+        int khz = 0;
+        if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess) khz = 0;
+        di.wall_khz = khz;
         g_dev[dev] = di;
         g_dev_ok[dev] = true;
     }
@@ -185,13 +188,32 @@ std::mutex g_timer_mu;
 std::atomic<int> g_timer_kernel{kTimedNone};
 hipEvent_t g_timer_start = nullptr, g_timer_stop = nullptr;
 
-void set_kernel_timer(int k, hipEvent_t start, hipEvent_t stop) {
+// Sets (or clears, k = kTimedNone) the request; returns whether a request
+// was pending (set and not yet taken by a launch).
+bool set_kernel_timer(int k, hipEvent_t start, hipEvent_t stop) {
     std::lock_guard<std::mutex> lk(g_timer_mu);
+    const bool pending = g_timer_kernel.load(std::memory_order_relaxed) != kTimedNone;
     g_timer_start = start;
     g_timer_stop = stop;
     g_timer_kernel.store(k, std::memory_order_release);
+    return pending;
 }
 }  // namespace
+
+// ------------------------------------------------- one-pass wait limit
+namespace {
+std::atomic<uint32_t> g_wait_us{200};
+}  // namespace
+
+uint32_t onepass_wait_ticks() {
+    int dev = 0;
+    DevInfo di;
+    uint64_t khz = 100000;  // the usual rate of the counter, if the query fails
+    if (hipGetDevice(&dev) == hipSuccess && device_info(dev, &di) == hipSuccess && di.wall_khz > 0)
+        khz = (uint64_t)di.wall_khz;
+    const uint64_t t = (uint64_t)g_wait_us.load(std::memory_order_relaxed) * khz / 1000u;
+    return t > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)t;
+}
 
 bool take_kernel_timer(int k, hipEvent_t* start, hipEvent_t* stop) {
     if (g_timer_kernel.load(std::memory_order_acquire) != k) return false;
@@ -204,7 +226,7 @@ bool take_kernel_timer(int k, hipEvent_t* start, hipEvent_t* stop) {
 }
 
 // -------------------------------------------------------------- workspace
-WsPlan plan_workspace(int kind, int T, uint64_t C, uint64_t sum_k) {
+WsPlan plan_workspace(int kind, int T, uint64_t C, uint64_t sum_k, bool agg_tables) {
     WsPlan p;
     std::memset(&p, 0, sizeof(p));
     size_t at = 256;  // header
@@ -216,14 +238,14 @@ WsPlan plan_workspace(int kind, int T, uint64_t C, uint64_t sum_k) {
     if (kind == BC_SIGN1) {
         take(p.s_val, t * 4);
         take(p.s_partial, (size_t)C * 8);
-        take(p.s_info, t * 4);
-        take(p.s_tab, t * 2048 * 4);
+        take(p.s_info, agg_tables ? t * 4 : 0);
+        take(p.s_tab, agg_tables ? t * 2048 * 4 : 0);
         take(p.s_slot, (size_t)C * 8);
     } else if (quant_bits(kind)) {
         take(p.s_val, t * 4);
         take(p.q_max, (size_t)C * 4);
         take(p.q_slot, (size_t)C * 4);
-        if (kind == BC_TERNGRAD) {
+        if (kind == BC_TERNGRAD && agg_tables) {
             take(p.s_info, t * 4);
             take(p.s_tab, t * 4096 * 4);
         }
@@ -367,6 +389,64 @@ int check_kind_ratio(int kind, double ratio, uint64_t& ppm) {
 
 }  // namespace
 
+namespace bc {
+
+// Host-side checks and descriptor table of a compress call (everything
+// before device memory is needed).  agg_tables: plan the workspace with the
+// aggregate's regions (the size bytecomp_workspace_size reports) or
+// without them (compress only).
+int compress_prepare(int kind, double ratio, const bc_tensor* t, int T, const bc_payload& out, bool agg_tables,
+                     CompressPrep& p) {
+    int rc = check_kind_ratio(kind, ratio, p.ppm);
+    if (rc) return rc;
+    if (T < 0 || T > kMaxT) return BC_E_COUNT;
+    if (T == 0) return BC_OK;
+    if (!t) return BC_E_NULL;
+    if (is_sparse(kind) ? (!out.idx || !out.val) : (!out.bits || !out.scale)) return BC_E_NULL;
+    try {
+        rc = build_tdesc(kind, p.ppm, t, T, false, p.d, p.C, p.maxc, p.sum_k, p.a16, p.a32);
+    } catch (const std::bad_alloc&) {
+        return BC_E_SIZE;
+    }
+    if (rc) return rc;
+    // random-k: payload positions are 32-bit and the bucket count is bounded
+    if (kind == BC_RANDK && (p.sum_k >= (1ull << 32) || !randk_buckets(p.C, nullptr, nullptr))) return BC_E_SIZE;
+    p.any_empty = false;
+    for (int i = 0; i < T && !p.any_empty; ++i) p.any_empty = t[i].n == 0;
+    p.plan = plan_workspace(kind, T, p.C, p.sum_k, agg_tables);
+    return BC_OK;
+}
+
+// The kind's compress kernels, on descriptor table dd (device) and carved
+// workspace w.
+hipError_t compress_launch(int kind, double ratio, uint64_t seed, const CompressPrep& p, const TDesc* dd,
+                           const bc_payload& out, const Ws& w, hipStream_t s) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    DevInfo di;
+    if ((e = device_info(dev, &di)) != hipSuccess) return e;
+    const int T = (int)p.d.size();
+    switch (kind) {
+        case BC_SIGN1:
+            return launch_sign_compress(dd, T, p.C, p.maxc, p.any_empty, p.a16, p.a32, out.bits, out.scale, w,
+                                        di.cus, s);
+        case BC_TOPK:
+        case BC_TOPK_SAMPLED:
+            return launch_topk(kind == BC_TOPK ? 0 : 1, ratio, seed, dd, T, p.C, p.a16, p.a32, out.idx, out.val, w,
+                               s);
+        case BC_TERNGRAD:
+        case BC_QSGD4:
+        case BC_QSGD8:
+            return launch_quant_compress(quant_bits(kind), seed, dd, T, p.C, p.maxc, p.any_empty, p.a16, p.a32,
+                                         out.bits, out.scale, w, di.cus, s);
+        default:
+            return launch_randk(seed, dd, T, p.C, p.sum_k, p.a16, p.a32, out.idx, out.val, w, s);
+    }
+}
+
+}  // namespace bc
+
 extern "C" {
 
 const char* bytecomp_strerror(int status) {
@@ -424,60 +504,18 @@ int bytecomp_workspace_init(void* ws, size_t ws_bytes, void* stream) {
 
 int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t, int T,
                       bc_payload out, void* ws, size_t ws_bytes, void* stream) {
-    uint64_t ppm;
-    int rc = check_kind_ratio(kind, ratio, ppm);
-    if (rc) return rc;
-    if (T < 0 || T > kMaxT) return BC_E_COUNT;
-    if (T == 0) return BC_OK;
-    if (!t) return BC_E_NULL;
-    if (is_sparse(kind) ? (!out.idx || !out.val) : (!out.bits || !out.scale)) return BC_E_NULL;
+    CompressPrep p;
+    int rc = compress_prepare(kind, ratio, t, T, out, true, p);
+    if (rc || T == 0) return rc;
     if (!ws) return BC_E_WORKSPACE;
-    std::vector<TDesc> d;
-    uint32_t C, maxc;
-    uint64_t sum_k;
-    bool a16, a32;
-    try {
-        rc = build_tdesc(kind, ppm, t, T, false, d, C, maxc, sum_k, a16, a32);
-    } catch (const std::bad_alloc&) {
-        return BC_E_SIZE;
-    }
-    if (rc) return rc;
-    // random-k: payload positions are 32-bit and the bucket count is bounded
-    if (kind == BC_RANDK && (sum_k >= (1ull << 32) || !randk_buckets(C, nullptr, nullptr))) return BC_E_SIZE;
-    const WsPlan plan = plan_workspace(kind, T, C, sum_k);
-    if (ws_bytes < plan.total) return BC_E_WORKSPACE;
+    if (ws_bytes < p.plan.total) return BC_E_WORKSPACE;
     hipStream_t s = (hipStream_t)stream;
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return BC_E_HIP;
-    DevInfo di;
-    if (device_info(dev, &di) != hipSuccess) return BC_E_HIP;
-    const Ws w = carve_workspace(ws, plan);
-    for (int i = 0; i < T && !di.any_empty; ++i) di.any_empty = t[i].n == 0;
     std::lock_guard<std::mutex> lk(g_mu);
     Entry* en = nullptr;
-    hipError_t e = cache_get(d.data(), d.size() * sizeof(TDesc), (size_t)C * 4,
-                             [&](void* dst) { fill_chunk_map(d, (uint32_t*)dst); }, s, &en);
+    hipError_t e = cache_get(p.d.data(), p.d.size() * sizeof(TDesc), (size_t)p.C * 4,
+                             [&](void* dst) { fill_chunk_map(p.d, (uint32_t*)dst); }, s, &en);
     if (e != hipSuccess) return BC_E_HIP;
-    const TDesc* dd = (const TDesc*)en->dev;
-    switch (kind) {
-        case BC_SIGN1:
-            e = launch_sign_compress(dd, T, C, maxc, di.any_empty, a16, a32, out.bits, out.scale, w, di.cus, s);
-            break;
-        case BC_TOPK:
-        case BC_TOPK_SAMPLED:
-            e = launch_topk(kind == BC_TOPK ? 0 : 1, ratio, seed, dd, T, C, a16, a32, out.idx, out.val,
-                            w, s);
-            break;
-        case BC_TERNGRAD:
-        case BC_QSGD4:
-        case BC_QSGD8:
-            e = launch_quant_compress(quant_bits(kind), seed, dd, T, C, maxc, di.any_empty, a16, a32, out.bits,
-                                      out.scale, w, di.cus, s);
-            break;
-        default:
-            e = launch_randk(seed, dd, T, C, sum_k, a16, a32, out.idx, out.val, w, s);
-            break;
-    }
+    e = compress_launch(kind, ratio, seed, p, (const TDesc*)en->dev, out, carve_workspace(ws, p.plan), s);
     cache_mark_used(en, s);
     return finish(hip_status(e), s, ws);
 }
@@ -780,23 +818,27 @@ int bytecomp_residual_update(int kind, double ratio, const bc_tensor* t, int T, 
 }
 
 int bytecomp_time_next_launch(const char* kernel, void* start_event, void* stop_event) {
-    if (!start_event && !stop_event) {
-        set_kernel_timer(kTimedNone, nullptr, nullptr);
-        return BC_OK;
-    }
+    if (!start_event && !stop_event) return set_kernel_timer(kTimedNone, nullptr, nullptr) ? 1 : BC_OK;
     if (!kernel || !start_event || !stop_event) return BC_E_NULL;
     static const struct { const char* name; int k; } names[] = {
         {"aggregate_sign", kTimedAggSign},       {"aggregate_sparse", kTimedAggSparse},
         {"randk_stream", kTimedRandkStream},     {"topk_compact", kTimedTopkCompact},
         {"sign_pass1", kTimedSignPass1},         {"quant_pass1", kTimedQuantPass1},
-        {"aggregate_quant", kTimedAggQuant}};
+        {"aggregate_quant", kTimedAggQuant},     {"sign_onepass", kTimedSignOnepass},
+        {"quant_onepass", kTimedQuantOnepass}};
     for (const auto& x : names) {
         if (std::strcmp(kernel, x.name) == 0) {
-            set_kernel_timer(x.k, (hipEvent_t)start_event, (hipEvent_t)stop_event);
+            (void)set_kernel_timer(x.k, (hipEvent_t)start_event, (hipEvent_t)stop_event);
             return BC_OK;
         }
     }
     return BC_E_KIND;
+}
+
+int bytecomp_set_wait_limit(uint32_t microseconds) {
+    if (microseconds > 10000000u) return BC_E_SIZE;
+    g_wait_us.store(microseconds, std::memory_order_relaxed);
+    return BC_OK;
 }
 
 int bytecomp_device_status(void* ws, size_t ws_bytes, void* stream, uint32_t* flags) {

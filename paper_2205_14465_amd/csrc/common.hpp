@@ -482,10 +482,28 @@ constexpr uint64_t kStreamRandk = 0;
 constexpr uint64_t kStreamSample = 1;
 constexpr uint64_t kStreamQuant = 2;
 
-constexpr uint32_t kFlagWaitTimeout = 1u;  // a bounded wait between workgroups ran out
+// Workspace header: failure flags reported by bytecomp_device_status.  No
+// current kernel sets one: the one-pass compress kernels wait for other
+// workgroups, but only for a bounded time, and a wait that runs out takes
+// a path whose results are exact (the workgroup computes the missing
+// partials itself), so it is no failure.
 
-// Workspace header: failure flags (bit 0 reserved for a bounded wait that
-// ran out; no current kernel waits on another workgroup).
+// --------------------------------------------- one-pass compress protocol
+// A one-pass compress kernel defers each chunk's residual (and, for the
+// quantizers, its codes) until its tensor's scale is known, which needs a
+// published partial (a sum of |v|, or a largest |v|) of every chunk of the
+// tensor.  A workgroup waits for missing partials only for a bounded time;
+// then it computes each still-missing partial itself, from the chunk's
+// gradient and residual, with exactly the owner's arithmetic (so the value
+// is bit-identical), and publishes it by compare-and-swap from empty: if the
+// owner published first, the owner's value stays.  The owner writes the
+// chunk's residual only once its tensor's partials are all published, and a
+// helper reads the chunk's residual only while its partial is still
+// missing, so a helper's publication never rests on a residual the owner
+// has already overwritten (had the owner begun, its partial would be
+// published and the helper's swap would fail).  Every wait therefore ends
+// after at most the limit plus the workgroup's own work, whatever the
+// residency of the grid.
 
 // ------------------------------------------------- aggregate worker table
 // Worker descriptors in the aggregate table are padded to a multiple of 16.

@@ -114,6 +114,36 @@ __device__ __forceinline__ void store_codes(uint32_t packed, uint32_t e0, uint32
     }
 }
 
+// Quantize the four elements e0 .. e0+3 of tensor td held in v4 (valid4:
+// which of them exist), with inv = fl32(s / m) and unit = fl32(m / s):
+// stores their codes and leaves their residuals v - decode in v4.
+template <int kBits>
+__device__ __forceinline__ void quantize_round(const TDesc& td, uint32_t e0, bool any, float inv, float unit,
+                                               float (&v4)[4], uint32_t valid4, uint64_t seed,
+                                               uint32_t* __restrict__ tw) {
+    using Q = Quant<kBits>;
+    float u[4];
+    quant_uniforms(seed, td.tid, e0 >> 3, (e0 >> 2) & 1u, u);
+    uint32_t packed = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        uint32_t level = 0;
+        if (any && ((valid4 >> q) & 1u)) {
+            const float x = fabsf(v4[q]) * inv;
+            if (x >= (float)Q::kLevels) {
+                level = (uint32_t)Q::kLevels;
+            } else {
+                const float fl = floorf(x);
+                level = (uint32_t)fl + (u[q] < x - fl ? 1u : 0u);
+            }
+        }
+        const uint32_t code = level ? (level | ((f2u(v4[q]) >> 31) << (kBits - 1))) : 0u;
+        packed |= code << (kBits * q);
+        v4[q] = v4[q] - quant_decode<kBits>(code, unit);
+    }
+    store_codes<kBits>(packed, e0, tw, td.k);
+}
+
 // Quantize chunk j of tensor td (v in registers, scale m): codes into the
 // payload words, residual into e.
 template <int kBits, bool kNT>
@@ -127,27 +157,10 @@ __device__ __forceinline__ void quantize_chunk(const TDesc& td, uint32_t j, floa
 #pragma unroll
     for (int r = 0; r < kRounds; ++r) {
         const uint32_t e0 = j * (uint32_t)kChunk + 1024u * r + 4u * threadIdx.x;  // element of the tensor
-        float u[4];
-        quant_uniforms(seed, td.tid, e0 >> 3, (e0 >> 2) & 1u, u);
-        uint32_t packed = 0;
+        float v4[4] = {v[4 * r], v[4 * r + 1], v[4 * r + 2], v[4 * r + 3]};
+        quantize_round<kBits>(td, e0, any, inv, unit, v4, (valid >> (4 * r)) & 0xFu, seed, tw);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int i = 4 * r + q;
-            uint32_t level = 0;
-            if (any && ((valid >> i) & 1u)) {
-                const float x = fabsf(v[i]) * inv;
-                if (x >= (float)Q::kLevels) {
-                    level = (uint32_t)Q::kLevels;
-                } else {
-                    const float fl = floorf(x);
-                    level = (uint32_t)fl + (u[q] < x - fl ? 1u : 0u);
-                }
-            }
-            const uint32_t code = level ? (level | ((f2u(v[i]) >> 31) << (kBits - 1))) : 0u;
-            packed |= code << (kBits * q);
-            v[i] = v[i] - quant_decode<kBits>(code, unit);
-        }
-        store_codes<kBits>(packed, e0, tw, td.k);
+        for (int q = 0; q < 4; ++q) v[4 * r + q] = v4[q];
     }
     if (td.resid) store_chunk<kNT>(td.resid, td.n, j, v);
 }
@@ -221,21 +234,51 @@ __global__ __launch_bounds__(kBlock) void quant_pass2(const TDesc* __restrict__ 
 // 31 set, 0 meaning not yet), the next chunk's loads go out, and chunk
 // c - grid, kept in registers, is quantized once every slot of its tensor
 // is published (the maximum of the slots is the scale, exact in any
-// order).  Waits end by the same induction over the tensors (every
-// workgroup resident, no tensor longer than the grid) and are bounded
-// regardless (workspace flag bit 0).
+// order).  Waits end by the same induction over the tensors when every
+// workgroup is resident; past the host's wait limit a waiting workgroup
+// computes the missing chunk maxima itself and publishes them by
+// compare-and-swap (common.hpp), so waits end whatever the residency.
 namespace {
-constexpr uint32_t kQuantSpinLimit = 1u << 20;
 
-__device__ __forceinline__ float quant_onepass_scale(const TDesc& td, uint32_t* slot, uint32_t* flags, uint32_t* sh) {
-    __shared__ int pending_sh;
-    uint32_t spins = 0;
+constexpr int kHelpBatch = 256;  // missing maxima a waiting workgroup computes per pass
+
+// Largest |v| bits over chunk j of tensor td, the owner's value (a maximum,
+// so any order gives it), read one round of four elements at a time.
+__device__ __forceinline__ uint32_t chunk_max_key(const TDesc& td, uint32_t j, uint32_t* sh) {
+    uint32_t mk = 0;
+#pragma unroll 1
+    for (int r = 0; r < kRounds; ++r) {
+        const uint32_t e0 = j * (uint32_t)kChunk + 1024u * r + 4u * threadIdx.x;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            if (e0 + q < td.n) {
+                const float g = td.dtype == 0 ? gp((const float*)td.grad)[e0 + q]
+                                              : h2f(gp((const uint16_t*)td.grad)[e0 + q]);
+                const uint32_t k = key_of(td.resid ? g + gp(td.resid)[e0 + q] : g);
+                mk = k > mk ? k : mk;
+            }
+        }
+    }
+    return block_max_u32(mk, sh);
+}
+
+// Largest |v| of tensor td from its slots (every thread returns it),
+// waiting while a slot is empty; once `ticks` of the constant-rate counter
+// have passed, each pass computes up to kHelpBatch missing maxima and
+// publishes them by compare-and-swap.  ctl_sh: LDS, 2 + kHelpBatch ints.
+__device__ __forceinline__ float quant_onepass_scale(const TDesc& td, uint32_t* slot, uint32_t* sh, uint32_t ticks,
+                                                     int* ctl_sh) {
+    int& pending_sh = ctl_sh[0];
+    int& help_sh = ctl_sh[1];
+    int* miss_sh = ctl_sh + 2;
+    const uint64_t t0 = wall_clock64();
+    uint32_t* sl = slot + td.chunk0;
     uint32_t mx;
     for (;;) {
         mx = 0;
         int missing = 0;
         for (uint32_t q = threadIdx.x; q < td.nchunks; q += kBlock) {
-            const uint32_t x = __hip_atomic_load(slot + td.chunk0 + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const uint32_t x = __hip_atomic_load(sl + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             missing |= x == 0u;
             const uint32_t k = x & 0x7FFFFFFFu;
             mx = k > mx ? k : mx;
@@ -245,14 +288,33 @@ __device__ __forceinline__ float quant_onepass_scale(const TDesc& td, uint32_t* 
         if (missing) pending_sh = 1;
         __syncthreads();
         const int pending = pending_sh;
+        if (threadIdx.x == 0) help_sh = pending && wall_clock64() - t0 >= (uint64_t)ticks ? 1 : 0;
         __syncthreads();
         if (!pending) break;
-        if (++spins > kQuantSpinLimit) {
-            if (threadIdx.x == 0)
-                __hip_atomic_fetch_or(flags, kFlagWaitTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            break;
+        if (!help_sh) {
+            __builtin_amdgcn_s_sleep(4);
+            continue;
         }
-        __builtin_amdgcn_s_sleep(4);
+        if (threadIdx.x == 0) pending_sh = 0;
+        __syncthreads();
+        for (uint32_t q = threadIdx.x; q < td.nchunks; q += kBlock) {
+            if (__hip_atomic_load(sl + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u) {
+                const int k = atomicAdd(&pending_sh, 1);
+                if (k < kHelpBatch) miss_sh[k] = (int)q;
+            }
+        }
+        __syncthreads();
+        const int m = pending_sh < kHelpBatch ? pending_sh : kHelpBatch;
+        for (int i = 0; i < m; ++i) {
+            const uint32_t q = (uint32_t)miss_sh[i];
+            const uint32_t mk = chunk_max_key(td, q, sh);
+            if (threadIdx.x == 0) {
+                uint32_t expected = 0u;
+                __hip_atomic_compare_exchange_strong(sl + q, &expected, mk | 0x80000000u, __ATOMIC_RELAXED,
+                                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        __syncthreads();  // the list is reused by the next pass
     }
     return u2f(block_max_u32(mx, sh));
 }
@@ -261,8 +323,9 @@ __device__ __forceinline__ float quant_onepass_scale(const TDesc& td, uint32_t* 
 template <int kBits, int kDT>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void quant_onepass(const TDesc* __restrict__ d, int T, uint32_t C, uint64_t seed,
                                                         uint32_t* __restrict__ words, float* __restrict__ scale_out,
-                                                        Ws ws) {
+                                                        Ws ws, uint32_t wait_ticks) {
     __shared__ uint32_t sh[4];
+    __shared__ int ctl_sh[2 + kHelpBatch];
     float vp[kEpt];
     uint32_t validp = 0;
     TDesc tdp{};
@@ -309,7 +372,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
         if (prev) {
             float m = mp;
             if (tdp.nchunks > 1) {
-                m = quant_onepass_scale(tdp, ws.q_slot, ws.flags, sh);
+                m = quant_onepass_scale(tdp, ws.q_slot, sh, wait_ticks, ctl_sh);
                 if (jp == 0 && threadIdx.x == 0) scale_out[tensor_of_chunk(d, T, tdp.chunk0)] = m;
             }
             quantize_chunk<kBits, false>(tdp, jp, m, vp, validp, seed, words);
@@ -326,7 +389,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     }
 }
 
-// Slots of the one-pass kernel to empty before it runs (a fill kernel).
+// Slots of the one-pass kernel, emptied before it runs (a fill kernel).
 __global__ void quant_onepass_reset(uint32_t C, Ws ws) {
     for (uint32_t c = blockIdx.x * blockDim.x + threadIdx.x; c < C; c += gridDim.x * blockDim.x) ws.q_slot[c] = 0u;
 }
@@ -663,8 +726,8 @@ bool quant_onepass_launch(uint64_t seed, const TDesc* d, int T, uint32_t C, uint
     const uint32_t grid = C < cap ? C : cap;
     hipLaunchKernelGGL(quant_onepass_reset, dim3((C + 255) / 256 < 1024 ? (C + 255) / 256 : 1024), dim3(256), 0, s,
                        C, ws);
-    (void)launch_timed(kTimedQuantPass1, quant_onepass<kBits, kDT>, dim3(grid), dim3(kBlock), 0, s, d, T, C, seed,
-                       words, scale, ws);
+    (void)launch_timed(kTimedQuantOnepass, quant_onepass<kBits, kDT>, dim3(grid), dim3(kBlock), 0, s, d, T, C, seed,
+                       words, scale, ws, onepass_wait_ticks());
     if (any_empty) hipLaunchKernelGGL(quant_empty_scales, dim3((T + 255) / 256), dim3(256), 0, s, d, T, scale);
     return true;
 }

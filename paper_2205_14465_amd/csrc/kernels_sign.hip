@@ -12,9 +12,9 @@
 // workgroups visits chunks c = blockIdx + k * grid; for each it loads g and
 // e, writes the bits, publishes the chunk's fp64 partial sum, and only then
 // writes the residual of its PREVIOUS chunk, kept in registers, whose
-// tensor's scale is by then almost always known.  The last workgroup to
-// publish a chunk of a tensor sums the tensor's partials in a fixed order
-// and publishes the scale.  Otherwise two passes run: pass 1 writes the
+// tensor's scale is by then almost always known (every workgroup of the
+// tensor sums its partials in the same fixed order).  Otherwise two passes
+// run: pass 1 writes the
 // bits, the chunk partial sums and v (into e); pass 2 sums the partials of
 // its tensor in the same fixed order, re-reads v and writes the residual.
 // (An earlier one-pass form that waited for each chunk's own tensor before
@@ -147,32 +147,66 @@ __global__ __launch_bounds__(kBlock) void sign_pass2(const TDesc* __restrict__ d
 // never all ones), so a slot needs no separate ready flag.  A fill kernel
 // empties the slots just before the one-pass kernel runs, so whatever an
 // earlier call (of any kind sharing the workspace) left there does not
-// matter.  A workgroup writes chunk c's
-// residual only after publishing chunk c + grid (and prefetching its next
-// chunk): it then reads all its tensor's slots, waiting while any is
-// empty, and sums them in the fixed order of the two-pass path.
+// matter.  A workgroup writes chunk c's residual only after publishing
+// chunk c + grid (and prefetching its next chunk): it then reads all its
+// tensor's slots, waiting while any is empty, and sums them in the fixed
+// order of the two-pass path.
 //
-// Every wait ends: the chunks of tensor(c) are published by workgroups
-// whose earlier waits concern chunks at least two grids before them,
-// which (no tensor being longer than a grid) belong to earlier tensors; by
-// induction over the tensors every slot is published, provided every
-// workgroup of the grid is resident (the launcher sizes the grid so).  The
-// wait is bounded regardless: past kSpinLimit polls it records
-// kFlagWaitTimeout in the workspace header and goes on.
+// When every workgroup of the grid is resident (the launcher sizes the
+// grid so) every wait ends quickly: the chunks of tensor(c) are published
+// by workgroups whose earlier waits concern chunks at least two grids
+// before them, which (no tensor being longer than a grid) belong to earlier
+// tensors, so by induction over the tensors every slot gets published.
+// When the grid is not wholly resident (other kernels holding compute
+// units), a wait may find a slot whose owner has not started: after the
+// host's wait limit the waiting workgroup computes such partials itself
+// and publishes them by compare-and-swap (common.hpp), so every wait ends
+// and the results are the same either way.
 namespace {
-constexpr uint32_t kSpinLimit = 1u << 20;
 
-// Scale of tensor td from its published chunk slots (every thread returns it).
-__device__ __forceinline__ float onepass_scale(const TDesc& td, uint64_t* slot, uint32_t* flags, double* sh) {
-    __shared__ int pending_sh;
-    uint32_t spins = 0;
+constexpr int kHelpBatch = 256;  // missing partials a waiting workgroup computes per pass
+
+// Partial sum of |v| over chunk j of tensor td, bit-identical to the
+// owner's (each thread's sixteen values in element order, then the fixed
+// block tree), read one round of four elements at a time (lean in
+// registers: it runs inside the one-pass kernel).
+__device__ __forceinline__ double chunk_abs_partial(const TDesc& td, uint32_t j, double* sh) {
+    double acc = 0.0;
+#pragma unroll 1
+    for (int r = 0; r < kRounds; ++r) {
+        const uint32_t e0 = j * (uint32_t)kChunk + 1024u * r + 4u * threadIdx.x;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            float v = 0.f;
+            if (e0 + q < td.n) {
+                const float g = td.dtype == 0 ? gp((const float*)td.grad)[e0 + q]
+                                              : h2f(gp((const uint16_t*)td.grad)[e0 + q]);
+                v = td.resid ? g + gp(td.resid)[e0 + q] : g;
+            }
+            acc += fabs((double)v);
+        }
+    }
+    return block_sum_f64(acc, sh);
+}
+
+// Scale of tensor td from its chunk slots (every thread returns it),
+// waiting while a slot is empty; once `ticks` of the constant-rate counter
+// have passed (thread 0 decides, through LDS), each pass computes up to
+// kHelpBatch missing partials and publishes them by compare-and-swap.
+// ctl_sh: LDS, 2 + kHelpBatch ints.
+__device__ __forceinline__ float onepass_scale(const TDesc& td, uint64_t* slot, double* sh, uint32_t ticks,
+                                               int* ctl_sh) {
+    int& pending_sh = ctl_sh[0];
+    int& help_sh = ctl_sh[1];
+    int* miss_sh = ctl_sh + 2;
+    const uint64_t t0 = wall_clock64();
+    unsigned long long* sl = (unsigned long long*)slot + td.chunk0;
     double acc;
     for (;;) {
         acc = 0.0;
         int missing = 0;
         for (uint32_t q = threadIdx.x; q < td.nchunks; q += kBlock) {
-            const unsigned long long x =
-                __hip_atomic_load((unsigned long long*)slot + td.chunk0 + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const unsigned long long x = __hip_atomic_load(sl + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             missing |= x == 0ull;
             acc += __longlong_as_double((long long)~x);
         }
@@ -181,14 +215,35 @@ __device__ __forceinline__ float onepass_scale(const TDesc& td, uint64_t* slot, 
         if (missing) pending_sh = 1;
         __syncthreads();
         const int pending = pending_sh;
+        if (threadIdx.x == 0) help_sh = pending && wall_clock64() - t0 >= (uint64_t)ticks ? 1 : 0;
         __syncthreads();
         if (!pending) break;
-        if (++spins > kSpinLimit) {
-            if (threadIdx.x == 0)
-                __hip_atomic_fetch_or(flags, kFlagWaitTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            break;
+        if (!help_sh) {
+            __builtin_amdgcn_s_sleep(4);
+            continue;
         }
-        __builtin_amdgcn_s_sleep(4);
+        // list up to kHelpBatch empty slots (pending_sh counts them), then
+        // compute and publish each
+        if (threadIdx.x == 0) pending_sh = 0;
+        __syncthreads();
+        for (uint32_t q = threadIdx.x; q < td.nchunks; q += kBlock) {
+            if (__hip_atomic_load(sl + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0ull) {
+                const int k = atomicAdd(&pending_sh, 1);
+                if (k < kHelpBatch) miss_sh[k] = (int)q;
+            }
+        }
+        __syncthreads();
+        const int m = pending_sh < kHelpBatch ? pending_sh : kHelpBatch;
+        for (int i = 0; i < m; ++i) {
+            const uint32_t q = (uint32_t)miss_sh[i];
+            const double p = chunk_abs_partial(td, q, sh);
+            if (threadIdx.x == 0) {
+                unsigned long long expected = 0ull;
+                __hip_atomic_compare_exchange_strong(sl + q, &expected, ~(unsigned long long)__double_as_longlong(p),
+                                                     __ATOMIC_RELAXED, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        __syncthreads();  // the list is reused by the next pass
     }
     return (float)(block_sum_f64(acc, sh) / (double)td.n);
 }
@@ -197,8 +252,9 @@ __device__ __forceinline__ float onepass_scale(const TDesc& td, uint64_t* slot, 
 template <int kDT>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) void sign_onepass(const TDesc* __restrict__ d, int T, uint32_t C,
                                                        uint32_t* __restrict__ bits, float* __restrict__ scale_out,
-                                                       Ws ws) {
+                                                       Ws ws, uint32_t wait_ticks) {
     __shared__ double sh[4];
+    __shared__ int ctl_sh[2 + kHelpBatch];
     float vp[kEpt];  // the previous chunk's v, its residual not yet written
     TDesc tdp{};
     bool prev = false;
@@ -240,7 +296,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) voi
         if (prev) {
             float s = sp;
             if (tdp.nchunks > 1) {
-                s = onepass_scale(tdp, ws.s_slot, ws.flags, sh);
+                s = onepass_scale(tdp, ws.s_slot, sh, wait_ticks, ctl_sh);
                 if (jp == 0 && threadIdx.x == 0) scale_out[tensor_of_chunk(d, T, tdp.chunk0)] = s;
             }
             if (tdp.resid) store_sign_residual<false>(tdp, jp, s, vp);
@@ -262,7 +318,7 @@ __global__ void sign_empty_scales(const TDesc* __restrict__ d, int T, float* __r
     if (t < T && d[t].nchunks == 0) scale_out[t] = 0.f;
 }
 
-// Slots of the one-pass kernel to empty before it runs (a fill kernel, not
+// Slots of the one-pass kernel, emptied before it runs (a fill kernel, not
 // a memset, so that the sequence stays capturable).
 __global__ void sign_onepass_reset(uint32_t C, Ws ws) {
     for (uint32_t c = blockIdx.x * blockDim.x + threadIdx.x; c < C; c += gridDim.x * blockDim.x)
@@ -320,7 +376,8 @@ bool sign_onepass_launch(const TDesc* d, int T, uint32_t C, uint32_t max_chunks,
     const uint32_t grid = C < cap ? C : cap;
     hipLaunchKernelGGL(sign_onepass_reset, dim3((C + 255) / 256 < 1024 ? (C + 255) / 256 : 1024), dim3(256), 0, s,
                        C, ws);
-    (void)launch_timed(kTimedSignPass1, sign_onepass<kDT>, dim3(grid), dim3(kBlock), 0, s, d, T, C, bits, scale, ws);
+    (void)launch_timed(kTimedSignOnepass, sign_onepass<kDT>, dim3(grid), dim3(kBlock), 0, s, d, T, C, bits, scale, ws,
+                       onepass_wait_ticks());
     if (any_empty) hipLaunchKernelGGL(sign_empty_scales, dim3((T + 255) / 256), dim3(256), 0, s, d, T, scale);
     return true;
 }

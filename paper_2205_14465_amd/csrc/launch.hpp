@@ -7,6 +7,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include "common.hpp"
 
 namespace bc {
@@ -61,21 +63,53 @@ struct WsPlan {
     size_t total;
 };
 
-WsPlan plan_workspace(int kind, int T, uint64_t chunks, uint64_t sum_k);
+// agg_tables false: without the regions only the sign and TernGrad
+// aggregates use (a compress-only workspace).
+WsPlan plan_workspace(int kind, int T, uint64_t chunks, uint64_t sum_k, bool agg_tables = true);
 Ws carve_workspace(void* base, const WsPlan& p);
+
+}  // namespace bc
+
+#include "../../include/bytecomp.h"
+
+namespace bc {
+
+// A compress call checked on the host: its descriptor table (chunk map not
+// included), chunk count, largest tensor in chunks, payload entries, dtype
+// mix, whether a tensor is empty, and the workspace plan.
+struct CompressPrep {
+    std::vector<TDesc> d;
+    uint32_t C = 0, maxc = 0;
+    uint64_t sum_k = 0, ppm = 0;
+    bool a16 = false, a32 = false, any_empty = false;
+    WsPlan plan{};
+};
+// BC_OK (T = 0 included: nothing to do) or the call's error status.
+int compress_prepare(int kind, double ratio, const bc_tensor* t, int T, const bc_payload& out, bool agg_tables,
+                     CompressPrep& p);
+// The kind's compress kernels on a device descriptor table (TDesc[T], then
+// the chunk -> tensor map) and a carved workspace.
+hipError_t compress_launch(int kind, double ratio, uint64_t seed, const CompressPrep& p, const TDesc* dd,
+                           const bc_payload& out, const Ws& w, hipStream_t s);
 
 struct DevInfo {
     int cus;
     bool any_empty;      // per call: some tensor has no elements
+    int wall_khz;        // rate of the constant-rate counter kernels read (wall_clock64)
 };
 hipError_t device_info(int dev, DevInfo* out);
 
 // ------------------------------------------------------- kernel timing
 // Kernels a caller may ask to have timed (bytecomp_time_next_launch).
 enum TimedKernel { kTimedNone = 0, kTimedAggSign, kTimedAggSparse, kTimedRandkStream, kTimedTopkCompact,
-                   kTimedSignPass1, kTimedQuantPass1, kTimedAggQuant };
+                   kTimedSignPass1, kTimedQuantPass1, kTimedAggQuant, kTimedSignOnepass, kTimedQuantOnepass };
 // If a request for kernel `k` is pending, hand over its events and clear it.
 bool take_kernel_timer(int k, hipEvent_t* start, hipEvent_t* stop);
+
+// How long (in ticks of the device's constant-rate counter, wall_clock64)
+// a one-pass compress workgroup waits for the rest of its tensor's chunk
+// partials before it computes the missing ones itself.
+uint32_t onepass_wait_ticks();
 
 // Launch `kernel`, bracketed by the requested events when kernel `k` is to
 // be timed.

@@ -146,4 +146,7 @@ def test_time_next_launch_arguments():
     assert L.bytecomp_time_next_launch(b"aggregate_sign", fake, fake) == 0
     assert L.bytecomp_time_next_launch(b"aggregate_quant", fake, fake) == 0
     assert L.bytecomp_time_next_launch(b"quant_pass1", fake, fake) == 0
-    assert L.bytecomp_time_next_launch(None, None, None) == 0  # clears the request
+    assert L.bytecomp_time_next_launch(b"sign_onepass", fake, fake) == 0
+    assert L.bytecomp_time_next_launch(b"quant_onepass", fake, fake) == 0
+    assert L.bytecomp_time_next_launch(None, None, None) == 1  # clears the pending request
+    assert L.bytecomp_time_next_launch(None, None, None) == 0  # nothing pending

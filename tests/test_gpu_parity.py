@@ -195,6 +195,76 @@ def test_one_pass_compress_ignores_stale_workspace(kind, fill):
         assert_resid_equal(got_e, want_e)
 
 
+def _check_word_kind(kind, got, want, grads, resids, got_e, want_e):
+    if kind == "sign":
+        assert_sign_close(got, want, grads, resids, got_e, want_e)
+    else:
+        assert np.array_equal(got["off"], want["off"])
+        assert np.array_equal(got["bits"], want["bits"])
+        assert np.array_equal(bits(got["scale"]), bits(want["scale"]))
+        if got_e is not None:
+            assert_resid_equal(got_e, want_e)
+
+
+@pytest.mark.parametrize("kind", ["sign", "terngrad", "qsgd4", "qsgd8"])
+@pytest.mark.parametrize("ef", [True, False])
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_one_pass_waits_given_up_from_the_host_stay_exact(kind, ef, dtype):
+    # a wait limit of 0 makes every wait of the one-pass kernels stop
+    # waiting at once (the condition of a grid that is not wholly resident,
+    # forced from the host): a workgroup that finds a chunk partial missing
+    # computes it itself; results equal the oracle's, and no failure is
+    # reported
+    from paper_2205_14465_amd import binding as B
+    rng = np.random.default_rng(71)
+    ns = [4096 * 40 + 3, 5000, 1, 0, 4096, 4096 * 9, 12345]
+    grads, resids = make_set(ns, rng, dtype)
+    r_in = resids if ef else None
+    B.bytecomp_set_wait_limit(0)
+    try:
+        got, got_e = gpu_compress(kind, 0.01, SEED, grads, r_in)
+    finally:
+        B.bytecomp_set_wait_limit(200)
+    want, want_e = O.compress_set(kind, 0.01, SEED, grads, r_in)
+    _check_word_kind(kind, got, want, grads, r_in, got_e, want_e)
+
+
+@pytest.mark.parametrize("kind", ["sign", "qsgd8"])
+def test_one_pass_compress_beside_a_long_kernel_on_another_stream(kind):
+    # the one-pass kernel starts while matrix products queued on another
+    # stream (default priority) hold compute units, so its grid may not be
+    # wholly resident: waits may run out and workgroups compute missing
+    # partials themselves; results still equal the oracle's and no failure
+    # is reported
+    import torch
+    from paper_2205_14465_amd import binding as B
+    from tests.helpers import torch_dev, to_np_u32
+    rng = np.random.default_rng(72)
+    ns = [4096 * 200 + 9, 4096 * 150, 70001, 4096 * 300 + 1, 5000]
+    grads, resids = make_set(ns, rng)
+    dg = [torch_dev(g) for g in grads]
+    de = [torch_dev(e) for e in resids]
+    out = B.alloc_payload(kind, 0.01, ns)
+    ws = B.alloc_workspace(kind, 0.01, ns, 1)
+    a = torch.randn(4096, 4096, device="cuda")
+    b = torch.randn(4096, 4096, device="cuda")
+    side = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(side):
+        for _ in range(8):
+            c = torch.mm(a, b)
+    B.bytecomp_compress(kind, 0.01, SEED, dg, de, out, ws)
+    torch.cuda.synchronize()
+    del c
+    assert B.bytecomp_device_status(ws) == 0
+    total = out["off"][-1]
+    got = {"off": np.array(out["off"], dtype=np.int64), "bits": to_np_u32(out["bits"])[:total],
+           "scale": out["scale"].cpu().numpy()[:len(ns)]}
+    got_e = [e.cpu().numpy() for e in de]
+    want, want_e = O.compress_set(kind, 0.01, SEED, grads, resids)
+    _check_word_kind(kind, got, want, grads, resids, got_e, want_e)
+
+
 @pytest.mark.parametrize("kind", ["sign", "terngrad"])
 def test_one_pass_compress_calls_in_a_row_share_a_workspace(kind):
     # successive calls on one workspace, with new inputs each time and a
@@ -569,7 +639,13 @@ def test_time_next_launch_brackets_the_kernel(kind, kernel):
     call_ms = ev[0].elapsed_time(ev[3])
     assert 0.0 < k_ms <= call_ms
     # the request was consumed: a second call leaves the events where they were
+    assert not B.bytecomp_time_next_launch(None, None, None)
     B.bytecomp_decompress_aggregate(kind, 0.01, dev_pay, ns, outs_dev, 1.0, ws)
     torch.cuda.synchronize()
     assert ev[1].elapsed_time(ev[2]) == k_ms
     assert B.bytecomp_device_status(ws) == 0
+    # a request for a kernel the call does not launch stays pending
+    B.bytecomp_time_next_launch("randk_stream", ev[1], ev[2])
+    B.bytecomp_decompress_aggregate(kind, 0.01, dev_pay, ns, outs_dev, 1.0, ws)
+    torch.cuda.synchronize()
+    assert B.bytecomp_time_next_launch(None, None, None)

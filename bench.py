@@ -4,6 +4,8 @@ One step = compress (with error feedback) every tensor of the workload, then
 decompress-and-aggregate W workers' payloads of the same tensor list: the
 whole hot path for that workload's operator.  Inputs (gradients, residuals,
 the W generated worker payloads) are resident in HBM before timing starts.
+The default workload is the largest single-GPU one: GPT-2-XL gradients
+(1.56B fp32 elements), random-k 1%, W = 16.
 
 value = algorithmic bytes per step / time per step, in GB/s, where the
 algorithmic bytes are what the method must move:
@@ -11,11 +13,17 @@ algorithmic bytes are what the method must move:
              + write the payload (8 B per sparse entry; 4 B per sign or
              quantizer code word + 4 B per tensor scale)
   aggregate: read W payloads + write the dense fp32 output (4 B/elem).
-The roofline entry reports the dominant kernel's algorithmic bytes per
-launch over its average launch duration (HIP events that the library
-records at that kernel's start and end, on the launch stream) against the
-8 TB/s HBM peak.  The CPU baseline times the oracle (single
-thread) on a bounded sample of the same workload.
+Timing: K steps between two synchronisations; before each step an untimed
+kernel writes 1 GiB (more than the 256 MB last-level cache), so that no step
+starts with its inputs in the cache, and HIP events on the launch stream
+bracket each step (the flush stays outside).  Per-operation times are the
+median, 10th and 90th percentile of --reps flushed repetitions.  The
+roofline entry is the dominant kernel -- the longest of the step's
+timeable kernels, measured -- with its algorithmic bytes per launch over
+its average launch duration (events the library records at that kernel's
+start and end) against the 8 TB/s HBM peak.  The CPU baseline times the
+oracle on a bounded sample of the same workload, on one core and on every
+core the process may use (OpenMP over tensors and element ranges).
 """
 import argparse
 import hashlib
@@ -53,40 +61,68 @@ def algorithmic_bytes(wl, off, kind):
     return comp, agg, payload
 
 
-def cpu_baseline(wl, off, budget_s=15.0):
-    """Time the oracle (one thread) on a bounded sample of the workload:
-    whole tensors in workload order until ~budget_s of compress work, and
-    the aggregate of the same tensors over all W workers."""
+def host_description():
+    """Host facts for the CPU baseline: logical CPUs, the ones this process
+    may run on, the CPU model and the RAM."""
+    model, ram_gb = None, None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for ln in fh:
+                if ln.startswith("model name"):
+                    model = ln.split(":", 1)[1].strip()
+                    break
+        with open("/proc/meminfo") as fh:
+            for ln in fh:
+                if ln.startswith("MemTotal"):
+                    ram_gb = round(int(ln.split()[1]) / 2**20, 1)
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = os.cpu_count()
+    return {"nproc": os.cpu_count(), "usable_cpus": usable, "model": model, "ram_gib": ram_gb}
+
+
+def cpu_baseline(wl, off, budget_s=10.0):
+    """Time the oracle on a bounded sample of the workload: whole tensors in
+    workload order until about budget_s of single-thread compress plus
+    aggregate work, each tensor aggregated over all W generated payloads;
+    then the same sample through the oracle's all-core list calls (OpenMP
+    over tensors and element ranges, bit-identical results)."""
     import oracle as O
     from paper_2205_14465_amd import workloads as WL
     kind = wl.kind
+    word = kind in WORD_KINDS
     counts = [int(off[t + 1] - off[t]) for t in range(wl.T)]
     comp_bytes = agg_bytes = 0
     comp_s = agg_s = 0.0
-    used = []
+    used, gs, es, pays_t = [], [], [], []
     gbytes = (2 if wl.grad_dtype == "float16" else 4) + (8 if wl.momentum else 0)
-    order = list(range(wl.T))
-    for t in order:
+    serial_payload = []
+    for t in range(wl.T):
         if comp_s + agg_s > budget_s:
             break
         g = WL.gradient(wl, t)
         e = WL.residual(wl, t)
         t0 = time.perf_counter()
         if wl.momentum:
-            O.compress_dgc(kind, g, e, np.zeros(g.size, np.float32), wl.momentum, wl.ratio, WL.SEED, t)
+            res = O.compress_dgc(kind, g, e, np.zeros(g.size, np.float32), wl.momentum, wl.ratio, WL.SEED, t)
         elif kind == "sign":
-            w_, s_, _ = O.compress_sign(g, e)
+            res = O.compress_sign(g, e)
         elif kind in O.QUANT_BITS:
-            O.compress_quant(g, e, O.QUANT_BITS[kind], WL.SEED, t)
+            res = O.compress_quant(g, e, O.QUANT_BITS[kind], WL.SEED, t)
         elif kind == "topk":
-            O.compress_topk(g, e, wl.ratio)
+            res = O.compress_topk(g, e, wl.ratio)
         elif kind == "topk_sampled":
-            O.compress_topk_sampled(g, e, wl.ratio, WL.SEED, t)
+            res = O.compress_topk_sampled(g, e, wl.ratio, WL.SEED, t)
         else:
-            O.compress_randk(g, e, wl.ratio, WL.SEED, t)
+            res = O.compress_randk(g, e, wl.ratio, WL.SEED, t)
         comp_s += time.perf_counter() - t0
+        serial_payload.append(res[:2])
         n = wl.sizes[t]
-        pay = (4 * counts[t] + 4) if kind in WORD_KINDS else 8 * counts[t]
+        pay = (4 * counts[t] + 4) if word else 8 * counts[t]
         comp_bytes += (gbytes + 8) * n + pay
         # aggregate this tensor over W generated payloads
         lists = []
@@ -99,23 +135,59 @@ def cpu_baseline(wl, off, budget_s=15.0):
             else:
                 i, v = WL.random_sparse_lists(rng, [n], [counts[t]])
                 lists.append((i[0], v[0]))
+        scale = np.float32(1e-3 if kind == "sign" else 4e-3)
         t0 = time.perf_counter()
         if kind == "sign":
-            O.aggregate_sign(n, lists, [np.float32(1e-3)] * wl.W, 1.0 / wl.W)
+            O.aggregate_sign(n, lists, [scale] * wl.W, 1.0 / wl.W)
         elif kind in O.QUANT_BITS:
-            O.aggregate_quant(n, O.QUANT_BITS[kind], lists, [np.float32(4e-3)] * wl.W, 1.0 / wl.W)
+            O.aggregate_quant(n, O.QUANT_BITS[kind], lists, [scale] * wl.W, 1.0 / wl.W)
         else:
             O.aggregate_sparse(n, [a for a, _ in lists], [b for _, b in lists], 1.0 / wl.W)
         agg_s += time.perf_counter() - t0
         agg_bytes += wl.W * pay + 4 * n
         used.append(t)
+        gs.append(g)
+        es.append(e)
+        pays_t.append(lists)
     total = comp_bytes + agg_bytes
     secs = comp_s + agg_s
-    return {"value": round(total / secs / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"{len(used)} of {wl.T} tensors ({sum(wl.sizes[t] for t in used)} elements), "
-                      f"compress + aggregate over W={wl.W}, single thread, {secs:.1f} s",
-            "compress_gbs": round(comp_bytes / comp_s / 1e9, 3) if comp_s else None,
-            "aggregate_gbs": round(agg_bytes / agg_s / 1e9, 3) if agg_s else None}
+    one = {"value": round(total / secs / 1e9, 4), "cores": 1, "seconds": round(secs, 2),
+           "compress_gbs": round(comp_bytes / comp_s / 1e9, 4) if comp_s else None,
+           "aggregate_gbs": round(agg_bytes / agg_s / 1e9, 4) if agg_s else None}
+    sample = (f"{len(used)} of {wl.T} tensors ({sum(wl.sizes[t] for t in used)} elements) in workload order, "
+              f"compress+EF and aggregate over W={wl.W}")
+    out = {"value": one["value"], "unit": "GB/s", "cores": 1, "kind": "oracle", "sample": sample,
+           "one_core": one, "host": host_description()}
+    if wl.momentum:
+        out["all_cores"] = None  # the list calls cover the plain kinds only
+        return out
+    threads = O.omp_max_threads()
+    ns = [wl.sizes[t] for t in used]
+    t0 = time.perf_counter()
+    pay_omp, _ = O.compress_list_omp(kind, wl.ratio, WL.SEED, gs, es, threads, tensor_ids=used)
+    c_s = time.perf_counter() - t0
+    # the all-core payload equals the serial one
+    for q, (a, b) in enumerate(serial_payload):
+        seg = slice(pay_omp["off"][q], pay_omp["off"][q + 1])
+        got = pay_omp["bits"][seg] if word else pay_omp["idx"][seg]
+        assert np.array_equal(got, a), ("all-core oracle differs from the serial one", used[q])
+    off_s = np.asarray(pay_omp["off"])
+    pay_dicts = []
+    for w in range(wl.W):
+        if word:
+            pay_dicts.append({"bits": np.concatenate([pays_t[q][w] for q in range(len(used))]),
+                              "scale": np.full(len(used), scale, np.float32), "off": off_s})
+        else:
+            pay_dicts.append({"idx": np.concatenate([pays_t[q][w][0] for q in range(len(used))]),
+                              "val": np.concatenate([pays_t[q][w][1] for q in range(len(used))]), "off": off_s})
+    t0 = time.perf_counter()
+    O.aggregate_list_omp(kind, ns, pay_dicts, 1.0 / wl.W, threads)
+    a_s = time.perf_counter() - t0
+    allc = {"value": round(total / (c_s + a_s) / 1e9, 4), "cores": threads, "seconds": round(c_s + a_s, 2),
+            "compress_gbs": round(comp_bytes / c_s / 1e9, 4), "aggregate_gbs": round(agg_bytes / a_s / 1e9, 4)}
+    out.update({"value": allc["value"], "cores": threads, "all_cores": allc,
+                "compress_gbs": allc["compress_gbs"], "aggregate_gbs": allc["aggregate_gbs"]})
+    return out
 
 
 def source_digest(files):
@@ -155,17 +227,42 @@ def counted_traffic(kernel, slug):
     return round(fetch + write)
 
 
+def kernel_candidates(wl, kind, comp_b, agg_b, pay_b):
+    """Kernels of the step that the library can time, with the algorithmic
+    bytes one launch moves (what the method must move, attributed to the
+    kernel that moves it)."""
+    n = wl.n_total
+    g_in = 4 if wl.momentum else (2 if wl.grad_dtype == "float16" else 4)  # DGC compresses the fp32 velocity
+    if kind == "randk":
+        return [("randk_stream", comp_b), ("aggregate_sparse", agg_b)]
+    if kind in ("topk", "topk_sampled"):
+        # the streaming EF pass reads g and e and writes e; the payload is
+        # written by the emit kernel
+        return [("topk_compact", (g_in + 8) * n), ("aggregate_sparse", agg_b)]
+    if kind == "sign":
+        # one pass: everything; two passes: the first reads g and e and
+        # writes the bits and scales
+        return [("sign_onepass", comp_b), ("sign_pass1", (g_in + 4) * n + pay_b), ("aggregate_sign", agg_b)]
+    return [("quant_onepass", comp_b), ("quant_pass1", (g_in + 4) * n), ("aggregate_quant", agg_b)]
+
+
+def pct(sorted_ms, q):
+    return sorted_ms[min(len(sorted_ms) - 1, int(q * len(sorted_ms)))]
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5, 6, 7, 8, 9])
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--reps", type=int, default=100, help="flushed repetitions of each operation")
+    ap.add_argument("--workload", type=int, default=4, choices=[1, 2, 3, 4, 5, 6, 7, 8, 9])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-flush", action="store_true", help="no cache flush between steps (warm-cache numbers)")
     ap.add_argument("--scheme", choices=["indivisible", "divisible"], default="indivisible",
                     help="divisible: time node 0's step of the divisible scheme instead")
     ap.add_argument("--parts", type=int, default=8)
-    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--cpu-budget", type=float, default=10.0)
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the compression hot path has no inter-GPU step "
@@ -214,6 +311,20 @@ def main():
     def aggregate():
         aggregate_call()
 
+    # an untimed write of 1 GiB (a torch fill kernel) evicts the 256 MB
+    # last-level cache before each timed step or operation
+    flush_buf = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+
+    def flush():
+        if not args.no_flush:
+            flush_buf.fill_(1.0)
+
+    def events(k):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(k)]
+        for e in ev:
+            e.record(stream)  # creates the HIP events (the library records on some of them)
+        return ev
+
     log("warmup")
     for _ in range(args.warmup):
         compress()
@@ -221,84 +332,95 @@ def main():
     torch.cuda.synchronize()
     assert B.bytecomp_device_status(ws) == 0
 
-    # whole-step timing (the contract): K steps between two synchronisations,
-    # nothing else on the stream
-    log(f"timing {args.steps} steps")
-    reps = args.steps
+    # the timed region: exactly K steps between two synchronisations, each
+    # bracketed by events on the launch stream, a flush before each
+    K = args.steps
+    log(f"timing {K} steps")
+    sev = [events(2) for _ in range(K)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(reps):
+    for r in range(K):
+        flush()
+        sev[r][0].record(stream)
         compress()
         aggregate()
+        sev[r][1].record(stream)
     torch.cuda.synchronize()
-    step_s = (time.perf_counter() - t0) / reps
+    wall_s = (time.perf_counter() - t0) / K
+    step_ms = sorted(sev[r][0].elapsed_time(sev[r][1]) for r in range(K))
+    step_avg = sum(step_ms) / K
     assert B.bytecomp_device_status(ws) == 0
 
-    # per-call device time: the same K steps again, with HIP events on the
-    # launch stream around each call (each event costs a few microseconds
-    # of stream time, so they stay out of the region above), and the
-    # dominant kernel's own duration: the library brackets its next launch
-    # with a further pair of events (hipExtLaunchKernelGGL)
-    dom_kernel = {"sign": "aggregate_sign", "randk": "randk_stream", "terngrad": "aggregate_quant",
-                  "qsgd4": "aggregate_quant", "qsgd8": "aggregate_quant"}.get(kind, "aggregate_sparse")
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(reps)]
-    for r in range(reps):
-        for e in ev[r][4:]:
-            e.record(stream)  # creates the HIP events the library records on
+    # per-operation device time: --reps flushed repetitions of each call
+    R = args.reps
+    log(f"timing {R} repetitions of each operation")
+    oev = [events(4) for _ in range(R)]
     torch.cuda.synchronize()
-    for r in range(reps):
-        B.bytecomp_time_next_launch(dom_kernel, ev[r][4], ev[r][5])
-        ev[r][0].record(stream)
+    for r in range(R):
+        flush()
+        oev[r][0].record(stream)
         compress()
-        ev[r][1].record(stream)
-        ev[r][2].record(stream)
+        oev[r][1].record(stream)
+        flush()
+        oev[r][2].record(stream)
         aggregate()
-        ev[r][3].record(stream)
+        oev[r][3].record(stream)
     torch.cuda.synchronize()
-    B.bytecomp_time_next_launch(None, None, None)
-    comp_ms = sorted(ev[r][0].elapsed_time(ev[r][1]) for r in range(reps))
-    agg_ms = sorted(ev[r][2].elapsed_time(ev[r][3]) for r in range(reps))
-    dom_ms = sorted(ev[r][4].elapsed_time(ev[r][5]) for r in range(reps))
-    comp_avg = sum(comp_ms) / reps
-    agg_avg = sum(agg_ms) / reps
-    dom_avg = sum(dom_ms) / reps
+    comp_ms = sorted(oev[r][0].elapsed_time(oev[r][1]) for r in range(R))
+    agg_ms = sorted(oev[r][2].elapsed_time(oev[r][3]) for r in range(R))
     assert B.bytecomp_device_status(ws) == 0
+
+    # the dominant kernel: each timeable kernel of the step, timed by the
+    # library's events around its own launch; the longest one
+    RK = max(5, R // 5)
+    kstats = {}
+    for name, kbytes in kernel_candidates(wl, kind, comp_b, agg_b, pay_b):
+        kev = [events(2) for _ in range(RK)]
+        torch.cuda.synchronize()
+        ran = True
+        for r in range(RK):
+            flush()
+            B.bytecomp_time_next_launch(name, kev[r][0], kev[r][1])
+            compress()
+            aggregate()
+            if B.bytecomp_time_next_launch(None, None, None):
+                ran = False  # the step does not launch this kernel
+                break
+        torch.cuda.synchronize()
+        if not ran:
+            continue
+        ms = sorted(kev[r][0].elapsed_time(kev[r][1]) for r in range(RK))
+        kstats[name] = {"bytes": kbytes, "ms_avg": sum(ms) / RK, "ms_p50": pct(ms, 0.5)}
+    dom_kernel = max(kstats, key=lambda k: kstats[k]["ms_avg"])
+    dom = kstats[dom_kernel]
 
     # achievable-bandwidth reference and the counter calibration kernel: a
     # plain elementwise pass reading 1 GiB and writing 1 GiB
     src = torch.empty(1 << 28, dtype=torch.float32, device=dev)
     dst = torch.empty_like(src)
     torch.neg(src, out=dst)
-    ce = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ce = events(2)
+    torch.cuda.synchronize()
     ce[0].record(stream)
     for _ in range(5):
         torch.neg(src, out=dst)
     ce[1].record(stream)
     torch.cuda.synchronize()
     copy_gbs = 5 * 2 * src.numel() * 4 / (ce[0].elapsed_time(ce[1]) * 1e-3) / 1e9
-    del src, dst
+    del src, dst, flush_buf
 
-    value = (comp_b + agg_b) / step_s / 1e9
-    comp_gbs = comp_b / (comp_avg * 1e-3) / 1e9
-    agg_gbs = agg_b / (agg_avg * 1e-3) / 1e9
-    # Dominant kernel: the longest single kernel of the step.  Sign:
-    # aggregate_sign (longer than either compress pass); the quantizers
-    # likewise aggregate_quant.  Top-k kinds:
-    # aggregate_sparse (longer than any compress kernel).  Random-k:
-    # randk_stream, which moves every algorithmic byte of the compress
-    # call.  Its time is its own launch duration from the events above.
-    dom_bytes = comp_b if dom_kernel == "randk_stream" else agg_b
-    dom = {"kernel": dom_kernel, "bytes": dom_bytes, "ms": dom_avg}
-    achieved = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
-    traffic = counted_traffic(dom["kernel"], wl.slug)
+    value = (comp_b + agg_b) / (step_avg * 1e-3) / 1e9
+    comp_med, agg_med = pct(comp_ms, 0.5), pct(agg_ms, 0.5)
+    achieved = dom["bytes"] / (dom["ms_avg"] * 1e-3) / 1e9
+    traffic = counted_traffic(dom_kernel, wl.slug)
     line = {
         "metric": METRIC,
         "value": round(value, 2),
         "unit": "GB/s",
         "n_gpus": 1,
-        "steps": args.steps,
+        "steps": K,
         "warmup": args.warmup,
-        "ms_per_step": round(step_s * 1e3, 4),
+        "ms_per_step": round(step_avg, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -307,21 +429,25 @@ def main():
         "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
         "config": {"workload": wl.name, "kind": kind, "tensors": wl.T, "elements": wl.n_total,
                    "ratio": wl.ratio if kind not in WORD_KINDS else None, "W": wl.W,
-                   "payload_bytes_per_worker": pay_b},
-        "ops": {"compress_ms": round(comp_avg, 4), "compress_gbs": round(comp_gbs, 1),
-                "compress_pct_peak": round(100 * comp_gbs / HBM_PEAK_GBS, 2),
-                "aggregate_ms": round(agg_avg, 4), "aggregate_gbs": round(agg_gbs, 1),
-                "aggregate_pct_peak": round(100 * agg_gbs / HBM_PEAK_GBS, 2),
-                "compress_ms_p10_p90": [round(comp_ms[reps // 10], 4), round(comp_ms[(9 * reps) // 10], 4)],
-                "aggregate_ms_p10_p90": [round(agg_ms[reps // 10], 4), round(agg_ms[(9 * reps) // 10], 4)]},
+                   "payload_bytes_per_worker": pay_b, "bytes_per_step": comp_b + agg_b},
+        "timing": {"cache_flush_gib": 0 if args.no_flush else 1,
+                   "step_ms_p10_p50_p90": [round(pct(step_ms, q), 4) for q in (0.1, 0.5, 0.9)],
+                   "wall_ms_per_step_incl_flush": round(wall_s * 1e3, 4)},
+        "ops": {"reps": R,
+                "compress_ms_p10_p50_p90": [round(pct(comp_ms, q), 4) for q in (0.1, 0.5, 0.9)],
+                "compress_gbs": round(comp_b / (comp_med * 1e-3) / 1e9, 1),
+                "compress_pct_peak": round(100 * comp_b / (comp_med * 1e-3) / 1e9 / HBM_PEAK_GBS, 2),
+                "aggregate_ms_p10_p50_p90": [round(pct(agg_ms, q), 4) for q in (0.1, 0.5, 0.9)],
+                "aggregate_gbs": round(agg_b / (agg_med * 1e-3) / 1e9, 1),
+                "aggregate_pct_peak": round(100 * agg_b / (agg_med * 1e-3) / 1e9 / HBM_PEAK_GBS, 2),
+                "kernels_ms_avg": {k: round(v["ms_avg"], 4) for k, v in kstats.items()}},
         "copy_gbs_reference": round(copy_gbs, 1),
-        "roofline": {"bound": "hbm", "kernel": dom["kernel"], "achieved": round(achieved, 1),
+        "roofline": {"bound": "hbm", "kernel": dom_kernel, "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": traffic, "kernel_ms": round(dom_avg, 4),
-                     "kernel_ms_p10_p90": [round(dom_ms[reps // 10], 4), round(dom_ms[(9 * reps) // 10], 4)]},
+                     "traffic": traffic, "bytes_per_launch": dom["bytes"], "kernel_ms": round(dom["ms_avg"], 4)},
     }
     if not args.no_cpu_baseline:
-        log("cpu baseline (oracle)")
+        log("cpu baseline (oracle, one core and all cores)")
         line["cpu_baseline"] = cpu_baseline(wl, off, args.cpu_budget)
     print(json.dumps(line), flush=True)
 

@@ -531,3 +531,89 @@ def aggregate_part_set(kind, lens, parts, alpha=1.0):
     as pack_part_set returns): per tensor, the dense slice of length
     lens[t] -- the same decompress-and-aggregate as the whole tensors."""
     return aggregate_set(kind, lens, parts, alpha)
+
+
+# ------------------------------------------------ all-core list calls
+# The same per-tensor functions run over a tensor list with OpenMP (the
+# benchmark's all-core CPU baseline); results are bit-identical to
+# compress_set / aggregate_set at any thread count.
+
+_lib_omp = None
+_KIND_CODE = {"topk": 0, "topk_sampled": 1, "randk": 2, "sign": 3, "terngrad": 4, "qsgd4": 5, "qsgd8": 6}
+
+
+def omp_lib():
+    global _lib_omp
+    if _lib_omp is None:
+        if not os.path.exists(_build.LIB_OMP):
+            _build.build()
+        L = ctypes.CDLL(_build.LIB_OMP)
+        L.bco_omp_max_threads.restype = _int
+        L.bco_omp_max_threads.argtypes = []
+        L.bco_compress_list.restype = _int
+        L.bco_compress_list.argtypes = [_int, _int, _vp, _vp, _vp, _vp, _vp, _dbl, _u64, _vp, _vp, _vp, _vp,
+                                        _vp, _vp, _int]
+        L.bco_aggregate_list.restype = _int
+        L.bco_aggregate_list.argtypes = [_int, _int, _int, _vp, _vp, _vp, _vp, _flt, _vp, _int]
+        _lib_omp = L
+    return _lib_omp
+
+
+def omp_max_threads():
+    return int(omp_lib().bco_omp_max_threads())
+
+
+def _ptrs(arrs):
+    return (ctypes.c_void_p * max(len(arrs), 1))(*[None if a is None else a.ctypes.data for a in arrs])
+
+
+def _payload_offsets(kind, ns, ratio):
+    if kind in QUANT_BITS:
+        return quant_word_offsets(ns, QUANT_BITS[kind])
+    if kind == "sign":
+        return word_offsets(ns)
+    return sparse_offsets(ns, ratio)
+
+
+def compress_list_omp(kind, ratio, seed, grads, resids, threads, tensor_ids=None):
+    """compress_set on `threads` threads (tensors in parallel)."""
+    T = len(grads)
+    gs = [_grad(g)[0] for g in grads]
+    dts = np.array([_DT[g.dtype] for g in gs], np.int32)
+    ns = np.array([g.size for g in gs], np.uint64)
+    es = [None] * T if resids is None else [_resid(e, g.size) for e, g in zip(resids, gs)]
+    eo = [None if e is None else np.empty(g.size, np.float32) for e, g in zip(es, gs)]
+    tids = np.array(range(T) if tensor_ids is None else tensor_ids, np.uint32)
+    off = _payload_offsets(kind, [int(x) for x in ns], ratio)
+    offu = off.astype(np.uint64)
+    word = kind in QUANT_BITS or kind == "sign"
+    a = np.empty(max(int(off[-1]), 1), np.uint32)
+    b = np.empty(max(int(off[-1]), 1) if not word else max(T, 1), np.float32)
+    rc = omp_lib().bco_compress_list(_KIND_CODE[kind], T, _ptrs(gs), _p(dts), _ptrs(es), _p(ns), _p(tids),
+                                     float(ratio), int(seed), _p(offu), None if word else _p(a),
+                                     None if word else _p(b), _p(a) if word else None, _p(b) if word else None,
+                                     _ptrs(eo), int(threads))
+    assert rc == 0, rc
+    if word:
+        return {"bits": a[:int(off[-1])], "scale": b[:T], "off": off}, eo
+    return {"idx": a[:int(off[-1])], "val": b[:int(off[-1])], "off": off}, eo
+
+
+def aggregate_list_omp(kind, ns, payloads, alpha, threads, ratio=None):
+    """aggregate_set on `threads` threads (tensors and 4096-element ranges
+    in parallel).  payloads: dicts as compress_set returns (their 'off')."""
+    T, W = len(ns), len(payloads)
+    word = kind in QUANT_BITS or kind == "sign"
+    off = np.asarray(payloads[0]["off"]).astype(np.uint64)
+    na = np.array(ns, np.uint64)
+    if word:
+        aa = [np.ascontiguousarray(p["bits"], np.uint32) for p in payloads]
+        bb = [np.ascontiguousarray(p["scale"], np.float32) for p in payloads]
+    else:
+        aa = [np.ascontiguousarray(p["idx"], np.uint32) for p in payloads]
+        bb = [np.ascontiguousarray(p["val"], np.float32) for p in payloads]
+    outs = [np.empty(int(n), np.float32) for n in ns]
+    rc = omp_lib().bco_aggregate_list(_KIND_CODE[kind], W, T, _p(na), _p(off), _ptrs(aa), _ptrs(bb),
+                                      float(alpha), _ptrs(outs), int(threads))
+    assert rc == 0, rc
+    return outs

@@ -287,9 +287,11 @@ def random_code_words(rng: np.random.Generator, ns, word_counts, bits):
 # --------------------------------------------- on-device generation (large)
 # For the 1.56B-element workload, drawing every input with numpy on the host
 # takes minutes; these generators draw the same distributions on the device
-# with torch's seeded generator.  Sparse worker payloads use one index per
-# stratum (stratum j of tensor t covers [floor(j n/k), floor((j+1) n/k))),
-# which keeps indices distinct and ascending with the same density.
+# with torch's seeded generator.  A sparse worker payload of tensor t is a
+# uniformly random k-subset of [0, n_t): k + k/32 + 64 indices drawn with
+# replacement, their distinct values, and a uniformly random k of those
+# (redrawn in the rare case of fewer than k distinct values); every k-subset
+# is equally likely, since each step treats all indices alike.
 
 def _torch_gen(device, *key):
     import torch
@@ -325,11 +327,17 @@ def device_sparse_payload(wl: Workload, w: int, counts, offs, device):
         k = int(counts[t])
         if k == 0:
             continue
-        j = torch.arange(k, device=device, dtype=torch.int64)
-        lo = (j * n) // k
-        hi = ((j + 1) * n) // k
-        u = torch.rand(k, generator=gen, device=device, dtype=torch.float64)
-        idx[offs[t]:offs[t] + k] = lo + torch.floor(u * (hi - lo).to(torch.float64)).to(torch.int64)
+        if k == n:
+            sel = torch.arange(n, device=device, dtype=torch.int64)
+        else:
+            while True:
+                x = torch.randint(0, n, (k + k // 32 + 64,), generator=gen, device=device, dtype=torch.int64)
+                u = torch.unique(x)
+                if u.numel() >= k:
+                    break
+            pick = torch.randperm(u.numel(), generator=gen, device=device)[:k]
+            sel = torch.sort(u[pick]).values
+        idx[offs[t]:offs[t] + k] = sel
         val[offs[t]:offs[t] + k] = torch.randn(k, generator=gen, device=device) * sigma_of(wl, t)
     return idx.to(torch.int32), val
 

@@ -164,6 +164,23 @@ int bytecomp_workspace_init(void* ws, size_t ws_bytes, void* stream);
 int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t, int T,
                       bc_payload out, void* ws, size_t ws_bytes, void* stream);
 
+/* bytecomp_compress for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same kernels and results, with no workspace argument.
+ * The call's workspace and its descriptor table live in a device array of
+ * the library, 16 MiB per GPU, held by each GPU the library runs on until
+ * the process ends; the descriptor table is written by kernel launches (no
+ * host-to-device copy) and the call allocates nothing.  Every call on a GPU
+ * shares that GPU's array: calls that overlap on one GPU (other streams or
+ * threads) race, so order them.  BC_E_SIZE, before anything is enqueued,
+ * when the call's compress workspace plus its table (48 bytes per tensor
+ * and 4 per 4096 elements) exceed 16 MiB: for BC_TOPK and BC_TOPK_SAMPLED
+ * that is about 2M elements per call (8 bytes per element of candidate
+ * space), for BC_SIGN1 and the quantizers several hundred million.  Every
+ * other argument, status and result is bytecomp_compress's. */
+int bytecomp_compress_noalloc(int kind, double ratio, uint64_t seed, const bc_tensor* t, int T,
+                              bc_payload out, void* stream);
+
 /* One DGC step (DGC is the paper's sparsification operator, Sec. 5.1):
  * momentum correction, sparse compression with error feedback, and
  * momentum-factor masking.  For every tensor, with u its velocity:

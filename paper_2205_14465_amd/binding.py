@@ -70,6 +70,8 @@ def lib():
         L.bytecomp_compress.restype = i32
         L.bytecomp_compress.argtypes = [i32, dbl, u64, ctypes.POINTER(bc_tensor), i32, bc_payload, vp,
                                         sz, vp]
+        L.bytecomp_compress_noalloc.restype = i32
+        L.bytecomp_compress_noalloc.argtypes = [i32, dbl, u64, ctypes.POINTER(bc_tensor), i32, bc_payload, vp]
         L.bytecomp_compress_dgc.restype = i32
         L.bytecomp_compress_dgc.argtypes = [i32, dbl, u64, ctypes.c_float, ctypes.POINTER(bc_tensor), vp, i32,
                                             bc_payload, vp, sz, vp]
@@ -186,6 +188,15 @@ def bytecomp_compress(kind, ratio, seed, grads, resids, out, ws, stream=None, te
            lib().bytecomp_compress(_kind(kind), float(ratio), int(seed) & (2**64 - 1), arr, len(grads),
                                    _payload(out), _ptr(ws), ws.numel() * ws.element_size(),
                                    _stream_handle(stream)))
+
+
+def bytecomp_compress_noalloc(kind, ratio, seed, grads, resids, out, stream=None, tensor_ids=None):
+    """bytecomp_compress without a workspace: the library's own per-GPU
+    device array serves as workspace and descriptor table (no allocation)."""
+    arr = _tensor_list(grads, resids, tensor_ids)
+    _check("bytecomp_compress_noalloc",
+           lib().bytecomp_compress_noalloc(_kind(kind), float(ratio), int(seed) & (2**64 - 1), arr, len(grads),
+                                           _payload(out), _stream_handle(stream)))
 
 
 def bytecomp_decompress_aggregate(kind, ratio, payloads, ns, outs, alpha, ws, stream=None):

@@ -129,6 +129,27 @@ def test_argument_errors():
     assert L.bytecomp_residual_update(0, 0.01, t, 1, pay, None) == -1
 
 
+def test_noalloc_compress_checks_before_any_device_work():
+    """The allocation-free compress refuses calls past its 16 MiB device
+    array, and bad arguments, on the host: checked without a GPU."""
+    L = B.lib()
+    pay = B.bc_payload(idx=0x2000, val=0x3000)
+    t = (B.bc_tensor * 1)()
+    t[0].grad = 0x1000
+    t[0].residual = None
+    t[0].n = 1 << 22          # top-k: 8 bytes of candidates per element, 32 MiB
+    t[0].dtype = 0
+    t[0].tensor_id = 0
+    assert L.bytecomp_compress_noalloc(0, 0.01, 0, t, 1, pay, None) == -5
+    assert L.bytecomp_compress_noalloc(0, 0.01, 0, t, 0, pay, None) == 0     # T = 0: nothing to do
+    assert L.bytecomp_compress_noalloc(9, 0.01, 0, t, 1, pay, None) == -2
+    assert L.bytecomp_compress_noalloc(0, 0.0, 0, t, 1, pay, None) == -4
+    assert L.bytecomp_compress_noalloc(3, 0.01, 0, t, 1, pay, None) == -1     # sign needs bits
+    t[0].grad = 0x1004
+    t[0].n = 100
+    assert L.bytecomp_compress_noalloc(0, 0.01, 0, t, 1, pay, None) == -9
+
+
 def test_workspace_size_grows_with_inputs():
     a = B.bytecomp_workspace_size("topk_sampled", 0.01, [1 << 20], 1)
     b = B.bytecomp_workspace_size("topk_sampled", 0.01, [1 << 21], 1)

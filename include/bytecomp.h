@@ -284,6 +284,31 @@ int bytecomp_aggregate_part(int kind, double ratio, const bc_payload* in, const 
 int bytecomp_residual_update(int kind, double ratio, const bc_tensor* t, int T,
                              bc_payload own, void* stream);
 
+/* CPU compression (paper Sec. 4.4.3, CPU offloading: the compression of
+ * some tensors runs on the host CPUs instead of the GPU; Sec. 4.3 profiles
+ * every operation on both).  bytecomp_compress on host memory: every
+ * pointer (gradients, residuals, payload arrays) is host memory, and the
+ * call runs synchronously on up to `threads` CPU threads (<= 0: one per
+ * hardware thread).  Kinds BC_TOPK, BC_TOPK_SAMPLED (computed as BC_TOPK:
+ * the same result), BC_RANDK and BC_SIGN1; BC_E_KIND for the quantizers.
+ * Payload layout and results are bytecomp_compress's, except that a sign
+ * scale is its fp64 sum taken in another order of additions (the two
+ * differ by at most the fp64 rounding of the sums, under 1e-6 relative;
+ * the residual uses the scale this call produced).  Errors: the argument
+ * checks of bytecomp_compress (no stream or device checks); BC_E_SIZE when
+ * host memory for the selection runs out; BC_E_HIP for any other host
+ * failure.  Nothing is written to the outputs on an argument error. */
+int bytecomp_cpu_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t, int T,
+                          bc_payload out, int threads);
+
+/* CPU decompress-and-aggregate (the CPU side of the same offloading):
+ * bytecomp_decompress_aggregate on host memory (payloads and outputs host
+ * pointers), synchronous, up to `threads` CPU threads; the same results,
+ * bit for bit, for BC_TOPK, BC_TOPK_SAMPLED, BC_RANDK and BC_SIGN1
+ * (BC_E_KIND otherwise); at most 1024 workers. */
+int bytecomp_cpu_decompress_aggregate(int kind, double ratio, const bc_payload* in, int W,
+                                      const uint64_t* n, int T, float* const* out, float alpha, int threads);
+
 /* Read (synchronously, on `stream`) and clear the kernel failure flags a
  * workspace holds; *flags receives them (0 = none).  No kernel of this
  * version sets one (bit 0 is reserved). */

@@ -72,6 +72,12 @@ def lib():
                                         sz, vp]
         L.bytecomp_compress_noalloc.restype = i32
         L.bytecomp_compress_noalloc.argtypes = [i32, dbl, u64, ctypes.POINTER(bc_tensor), i32, bc_payload, vp]
+        L.bytecomp_cpu_compress.restype = i32
+        L.bytecomp_cpu_compress.argtypes = [i32, dbl, u64, ctypes.POINTER(bc_tensor), i32, bc_payload, i32]
+        L.bytecomp_cpu_decompress_aggregate.restype = i32
+        L.bytecomp_cpu_decompress_aggregate.argtypes = [i32, dbl, ctypes.POINTER(bc_payload), i32,
+                                                        ctypes.POINTER(ctypes.c_uint64), i32,
+                                                        ctypes.POINTER(ctypes.c_void_p), flt, i32]
         L.bytecomp_compress_dgc.restype = i32
         L.bytecomp_compress_dgc.argtypes = [i32, dbl, u64, ctypes.c_float, ctypes.POINTER(bc_tensor), vp, i32,
                                             bc_payload, vp, sz, vp]
@@ -197,6 +203,85 @@ def bytecomp_compress_noalloc(kind, ratio, seed, grads, resids, out, stream=None
     _check("bytecomp_compress_noalloc",
            lib().bytecomp_compress_noalloc(_kind(kind), float(ratio), int(seed) & (2**64 - 1), arr, len(grads),
                                            _payload(out), _stream_handle(stream)))
+
+
+# ------------------------------------------------------------- CPU side
+# The host operators (CPU offloading): numpy arrays in host memory.
+
+def _np_tensor_list(grads, resids, tensor_ids):
+    import numpy as np
+    T = len(grads)
+    arr = (bc_tensor * max(T, 1))()
+    for t, g in enumerate(grads):
+        e = None if resids is None else resids[t]
+        assert g.flags.c_contiguous and (e is None or (e.flags.c_contiguous and e.dtype == np.float32))
+        arr[t].grad = g.ctypes.data if g.size else None
+        arr[t].residual = None if e is None else e.ctypes.data
+        arr[t].n = g.size
+        arr[t].dtype = BC_F32 if g.dtype == np.float32 else BC_F16 if g.dtype == np.float16 else 99
+        arr[t].tensor_id = t if tensor_ids is None else int(tensor_ids[t])
+    return arr
+
+
+def _np_payload(p):
+    def ptr(key):
+        a = p.get(key)
+        return a.ctypes.data if a is not None and a.size else None
+    return bc_payload(idx=ptr("idx"), val=ptr("val"), bits=ptr("bits"), scale=ptr("scale"))
+
+
+def cpu_alloc_payload(kind, ratio, ns):
+    """Host payload arrays (numpy) laid out as bytecomp_layout describes."""
+    import numpy as np
+    off = bytecomp_layout(kind, ratio, ns)
+    total = off[-1]
+    if _kind(kind) in (KIND["sign"], KIND["terngrad"], KIND["qsgd4"], KIND["qsgd8"]):
+        return {"bits": np.zeros(max(total, 1), np.uint32), "scale": np.zeros(max(len(ns), 1), np.float32),
+                "off": off}
+    return {"idx": np.zeros(max(total, 1), np.uint32), "val": np.zeros(max(total, 1), np.float32), "off": off}
+
+
+class CpuCompressCall:
+    """bytecomp_cpu_compress with its arguments marshalled once."""
+
+    def __init__(self, kind, ratio, grads, resids, out, threads=0, tensor_ids=None):
+        self.kind, self.ratio, self.T, self.threads = _kind(kind), float(ratio), len(grads), int(threads)
+        self.arr = _np_tensor_list(grads, resids, tensor_ids)
+        self.out = _np_payload(out)
+        self._keep = (grads, resids, out)
+
+    def __call__(self, seed):
+        _check("bytecomp_cpu_compress",
+               lib().bytecomp_cpu_compress(self.kind, self.ratio, int(seed) & (2**64 - 1), self.arr, self.T,
+                                           self.out, self.threads))
+
+
+class CpuAggregateCall:
+    """bytecomp_cpu_decompress_aggregate with its arguments marshalled once."""
+
+    def __init__(self, kind, ratio, payloads, ns, outs, alpha, threads=0):
+        self.kind, self.ratio, self.alpha, self.threads = _kind(kind), float(ratio), float(alpha), int(threads)
+        self.W, self.T = len(payloads), len(ns)
+        self.pa = (bc_payload * max(self.W, 1))(*[_np_payload(p) for p in payloads])
+        self.ns = _u64_array(ns)
+        self.op = (ctypes.c_void_p * max(self.T, 1))(*[o.ctypes.data if o.size else None for o in outs])
+        self._keep = (payloads, outs)
+
+    def __call__(self):
+        _check("bytecomp_cpu_decompress_aggregate",
+               lib().bytecomp_cpu_decompress_aggregate(self.kind, self.ratio, self.pa, self.W, self.ns, self.T,
+                                                       self.op, self.alpha, self.threads))
+
+
+def bytecomp_cpu_compress(kind, ratio, seed, grads, resids, out, threads=0, tensor_ids=None):
+    """Host compression: grads/resids numpy arrays (resids updated in place,
+    None = error feedback off); out from cpu_alloc_payload."""
+    CpuCompressCall(kind, ratio, grads, resids, out, threads, tensor_ids)(seed)
+
+
+def bytecomp_cpu_decompress_aggregate(kind, ratio, payloads, ns, outs, alpha, threads=0):
+    """Host decompress-and-aggregate of W numpy payloads into numpy outputs."""
+    CpuAggregateCall(kind, ratio, payloads, ns, outs, alpha, threads)()
 
 
 def bytecomp_decompress_aggregate(kind, ratio, payloads, ns, outs, alpha, ws, stream=None):

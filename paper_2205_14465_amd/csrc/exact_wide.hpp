@@ -40,7 +40,7 @@ namespace wide {
 
 // Bucket of a scale: 0..7 the limb of a finite nonzero scale, 8 a NaN or an
 // infinity, 9 zero (contributes nothing).
-__device__ __forceinline__ int bucket_of(uint32_t b, int emin) {
+__host__ __device__ __forceinline__ int bucket_of(uint32_t b, int emin) {
     const uint32_t e = (b >> 23) & 255u;
     if (e == 255u) return 8;
     if ((b & 0x7FFFFFFFu) == 0u) return 9;
@@ -64,7 +64,7 @@ __device__ __forceinline__ void decode_bits(uint32_t word, uint32_t pos, uint32_
 }
 
 // Round a 288-bit two's-complement total in units of 2^(emin - 150).
-__device__ __forceinline__ float round_total(int64_t (&acc)[kWideLimbs], int emin) {
+__host__ __device__ __forceinline__ float round_total(int64_t (&acc)[kWideLimbs], int emin) {
     uint32_t d[kWideLimbs];
 #pragma unroll
     for (int j = 0; j + 1 < kWideLimbs; ++j) {

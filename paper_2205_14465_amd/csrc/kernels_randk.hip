@@ -2,14 +2,9 @@
 // on gfx950 (Randomk at a 1% rate, paper Sec. 5.1; sparsification with
 // error feedback, Sec. 2.3).
 //
-// The k_t indices of tensor t are the images of 0..k_t-1 under a keyed
-// pseudorandom permutation of [0, n_t): a balanced four-round Feistel
-// network on b-bit integers (b = bit length of n_t - 1, at least 2, rounded
-// up to even), restricted to [0, n_t) by cycle-walking (Black & Rogaway,
-// CT-RSA 2002).  Round keys: one Philox4x64-10 block keyed by
-// (seed, stream 0) at counter (tensor_id, 0, 0, 0), word r folded to 32
-// bits; round function: the "lowbias32" integer hash (C. Wellons,
-// hash-prospector) of the right half xor the round key.
+// The k_t indices of tensor t are the images of 0..k_t-1 under the keyed
+// pseudorandom permutation of [0, n_t) in randk_perm.hpp (a four-round
+// Feistel network with cycle-walking, keyed by (seed, tensor id)).
 //
 // Instead of sorting the k indices, they are bucketed by runs of 2^S
 // consecutive 4096-element chunks (S from the call's chunk count): each
@@ -21,6 +16,7 @@
 // chunk zeroes them in e_new and emits (index, v) in index order, which is
 // the sorted payload.
 #include "launch.hpp"
+#include "randk_perm.hpp"
 
 #include <mutex>
 
@@ -31,33 +27,6 @@ namespace {
 constexpr int kScanBlock = kBlock * 16;  // bucket sizes per scan block
 constexpr int kColBlock = 1024;          // threads of the column pass
 
-__device__ __forceinline__ uint32_t lowbias32(uint32_t x) {
-    x ^= x >> 16;
-    x *= 0x7feb352du;
-    x ^= x >> 15;
-    x *= 0x846ca68bu;
-    x ^= x >> 16;
-    return x;
-}
-
-__device__ __forceinline__ uint32_t half_bits(uint32_t n) {
-    const uint32_t m = n > 1 ? n - 1 : 0;
-    uint32_t b = m ? 32u - __clz(m) : 0u;
-    if (b < 2) b = 2;
-    b += b & 1u;
-    return b >> 1;
-}
-
-__device__ __forceinline__ uint32_t feistel(uint32_t x, uint32_t h, uint32_t mask, const uint4 rk) {
-    uint32_t L = (x >> h) & mask, R = x & mask;
-    uint32_t F;
-    F = lowbias32(R ^ rk.x) & mask; { uint32_t t = L ^ F; L = R; R = t; }
-    F = lowbias32(R ^ rk.y) & mask; { uint32_t t = L ^ F; L = R; R = t; }
-    F = lowbias32(R ^ rk.z) & mask; { uint32_t t = L ^ F; L = R; R = t; }
-    F = lowbias32(R ^ rk.w) & mask; { uint32_t t = L ^ F; L = R; R = t; }
-    return (h >= 16) ? ((L << 16) | R) : ((L << h) | R);
-}
-
 // Tensor owning flat payload entry j: largest t with off[t] <= j.
 
 }  // namespace
@@ -66,10 +35,11 @@ __device__ __forceinline__ uint32_t feistel(uint32_t x, uint32_t h, uint32_t mas
 __global__ void randk_prep(const TDesc* __restrict__ d, int T, uint64_t seed, Ws ws) {
     const int t = (int)(blockIdx.x * blockDim.x + threadIdx.x);
     if (t >= T) return;
-    U64x4 ctr = {{(uint64_t)d[t].tid, 0, 0, 0}};
-    const U64x4 w = philox4x64_10(ctr, seed, kStreamRandk);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) ws.r_keys[4 * t + r] = (uint32_t)w.v[r] ^ (uint32_t)(w.v[r] >> 32);
+    const uint4 rk = randk_round_keys(seed, d[t].tid);
+    ws.r_keys[4 * t] = rk.x;
+    ws.r_keys[4 * t + 1] = rk.y;
+    ws.r_keys[4 * t + 2] = rk.z;
+    ws.r_keys[4 * t + 3] = rk.w;
 }
 
 

@@ -20,9 +20,17 @@ compression option for every tensor so as to shorten the iteration:
     decision; each visited tensor takes the GPU option (or none) that
     minimises F with the others fixed (Property #3);
   * Algorithm 2, CPU offloading (Sec. 4.4.3): the compressed tensors are
-    grouped by size and option; in each group the tensors farthest from the
-    output layer are offloaded first (the paper's lemma); every vector of
-    per-group counts is evaluated and the best kept.
+    grouped by size and option; in each group the tensors are offloaded in
+    the order the paper's lemma fixes; every vector of per-group counts is
+    evaluated and the best kept.  The lemma's statement names the tensors
+    farthest from the output layer, while its stated intuition is that
+    tensors offloaded earlier overlap more CPU work with communication and
+    computation; in backward order the gradients that are ready earliest
+    are those closest to the output layer, so the two point in opposite
+    directions.  The default order follows the intuition (earliest-ready
+    first, lemma_order="earliest"), which in this timeline model always
+    matched the best of all offloading subsets on random instances; the
+    statement's order is lemma_order="farthest".
 
 The options are the decision tree's leaves reduced to what this library
 computes: no compression (ring allreduce of the fp32 tensor), or the
@@ -30,10 +38,11 @@ compression algorithm on the GPU or the CPU with the indivisible scheme
 (compress, ring allgather of the payloads, decompress-and-aggregate of the N
 payloads) or the divisible scheme (compress, all-to-all of the N parts,
 aggregate one part, compress it again, allgather, decompress).  Times come
-from a CostModel: the GPU compress / aggregate times of the compression-time
-profiler (paper_2205_14465_amd.profiler, interpolated in log-log over
-tensor size), the profiler's ring-collective formulas, and a throughput for
-CPU compression and PCIe copies.  The per-tensor computation times are an
+from a CostModel: the GPU and CPU compress / aggregate times of the
+compression-time profiler (paper_2205_14465_amd.profiler: the library's
+device kernels and its host operators, interpolated in log-log over tensor
+size), the profiler's ring-collective formulas, and its measured host <->
+device copy rates.  Without CPU rows in the profile there is no CPU option.  The per-tensor computation times are an
 input (the paper takes them from execution traces of 100 iterations; here
 they are synthetic, since no training trace is available).
 """
@@ -68,9 +77,7 @@ class Cluster:
     N: int = 8               # GPUs in the ring
     link_gbs: float = 12.5   # per-link bandwidth, GB/s (100 Gb/s)
     alpha_us: float = 5.0    # per-step latency of a collective
-    pcie_gbs: float = 25.0   # host <-> device copies of offloaded tensors
-    cpu_gbs: float = 4.0     # CPU compressor throughput over the fp32 input
-    cpu_agg_gbs: float = 8.0 # CPU decompress-and-aggregate throughput over the payloads
+    pcie_gbs: Optional[float] = None  # host <-> device copy rate; None: the profile's measured rates
 
 
 def alltoall_us(nbytes_per_gpu: float, N: int, link_gbs: float, alpha_us: float) -> float:
@@ -84,26 +91,33 @@ def alltoall_us(nbytes_per_gpu: float, N: int, link_gbs: float, alpha_us: float)
 class CostModel:
     """Time models of one compression algorithm on one cluster."""
 
-    def __init__(self, kind: str, ratio: float, rows: Sequence[dict], cluster: Cluster, table_W: int = 8):
+    def __init__(self, kind: str, ratio: float, rows: Sequence[dict], cluster: Cluster, table_W: int = 8,
+                 pcie: Optional[Dict[str, float]] = None):
         self.kind, self.ratio, self.c, self.table_W = kind, ratio, cluster, table_W
-        pts = sorted((int(r["n"]), float(r["compress_us"]), float(r["aggregate_us"])) for r in rows
-                     if r["kind"] == kind)
-        if not pts:
-            raise ValueError(f"no compression-time rows for {kind}")
-        self.ln = [math.log(p[0]) for p in pts]
-        self.comp = [p[1] for p in pts]
-        self.agg = [p[2] for p in pts]
+        self.curves: Dict[str, Tuple[List[float], List[float], List[float]]] = {}
+        for dev in ("gpu", "cpu"):
+            pts = sorted((int(r["n"]), float(r["compress_us"]), float(r["aggregate_us"])) for r in rows
+                         if r["kind"] == kind and r.get("device", "gpu") == dev)
+            if pts:
+                self.curves[dev] = ([math.log(p[0]) for p in pts], [p[1] for p in pts], [p[2] for p in pts])
+        if "gpu" not in self.curves:
+            raise ValueError(f"no GPU compression-time rows for {kind}")
+        rate = {"h2d": cluster.pcie_gbs, "d2h": cluster.pcie_gbs} if cluster.pcie_gbs else pcie
+        self.pcie_rate = rate if rate and rate.get("h2d") and rate.get("d2h") else None
+        # the CPU option needs measured CPU times and a copy rate
+        self.has_cpu = "cpu" in self.curves and self.pcie_rate is not None
 
-    def _interp(self, ys: List[float], n: float) -> float:
+    @staticmethod
+    def _interp(ln: List[float], ys: List[float], n: float) -> float:
         """Log-log interpolation in the size; past the largest size the time
         grows in proportion to n, below the smallest it stays constant."""
         x = math.log(max(n, 1.0))
-        if x <= self.ln[0]:
+        if x <= ln[0]:
             return ys[0]
-        if x >= self.ln[-1]:
-            return ys[-1] * math.exp(x - self.ln[-1])
-        i = max(j for j in range(len(self.ln)) if self.ln[j] <= x)
-        t = (x - self.ln[i]) / (self.ln[i + 1] - self.ln[i])
+        if x >= ln[-1]:
+            return ys[-1] * math.exp(x - ln[-1])
+        i = max(j for j in range(len(ln)) if ln[j] <= x)
+        t = (x - ln[i]) / (ln[i + 1] - ln[i])
         return math.exp(math.log(ys[i]) * (1 - t) + math.log(ys[i + 1]) * t)
 
     def payload_bytes(self, n: int) -> float:
@@ -118,18 +132,19 @@ class CostModel:
 
     # compute-resource times
     def compress(self, device: str, n: float) -> float:
-        if device == "gpu":
-            return self._interp(self.comp, n)
-        return 12.0 * n / (self.c.cpu_gbs * 1e3)
+        ln, comp, _ = self.curves[device]
+        return self._interp(ln, comp, n)
 
     def aggregate(self, device: str, n: float, parts: int) -> float:
-        """Decompress and aggregate `parts` payloads of a tensor of n elements."""
-        if device == "gpu":
-            return self._interp(self.agg, n) * parts / self.table_W
-        return (parts * self.payload_bytes(int(n)) + 4.0 * n) / (self.c.cpu_agg_gbs * 1e3)
+        """Decompress and aggregate `parts` payloads of a tensor of n elements
+        (the profile aggregates table_W payloads; the time is taken in
+        proportion to the payload count)."""
+        ln, _, agg = self.curves[device]
+        return self._interp(ln, agg, n) * parts / self.table_W
 
-    def pcie(self, nbytes: float) -> float:
-        return nbytes / (self.c.pcie_gbs * 1e3)
+    def pcie(self, nbytes: float, direction: str) -> float:
+        """Copy of nbytes between host and device; direction 'h2d' or 'd2h'."""
+        return nbytes / (self.pcie_rate[direction] * 1e3)
 
     # network times
     def allreduce(self, n: int) -> float:
@@ -152,7 +167,7 @@ class CostModel:
         p = self.payload_bytes(n)
         st: List[Tuple[str, float, str]] = []
         if dev == "cpu":
-            st.append(("pcie", self.pcie(4.0 * n), "to host"))
+            st.append(("pcie", self.pcie(4.0 * n, "d2h"), "to host"))
         st.append((dev, self.compress(dev, n), "compress"))
         if scheme == "indivisible":
             st.append(("net", self.allgather(p), "allgather"))
@@ -164,7 +179,7 @@ class CostModel:
             st.append(("net", self.allgather(self.payload_bytes(max(1, n // N))), "allgather"))
             st.append((dev, self.aggregate(dev, n, 1), "decompress"))
         if dev == "cpu":
-            st.append(("pcie", self.pcie(4.0 * n), "to device"))
+            st.append(("pcie", self.pcie(4.0 * n, "h2d"), "to device"))
         return st
 
 
@@ -275,20 +290,24 @@ def plan_gpu(tensors: Sequence[Tensor], model: CostModel, options=GPU_OPTIONS) -
     return S
 
 
-def plan_cpu(tensors: Sequence[Tensor], S: Sequence[Option], model: CostModel, max_evals: int = 20000
-             ) -> Tuple[List[Option], int]:
+def plan_cpu(tensors: Sequence[Tensor], S: Sequence[Option], model: CostModel, max_evals: int = 20000,
+             lemma_order: str = "earliest") -> Tuple[List[Option], int]:
     """Algorithm 2: CPU offloading of the GPU-compressed tensors.  Returns
     the strategy and the number of strategies evaluated.  When the product
     of the group sizes (plus one) exceeds max_evals, the counts are chosen
     one group at a time instead (each group's count minimising F with the
     others fixed, repeated until no count changes)."""
+    if not getattr(model, "has_cpu", True):
+        return list(S), 0
     groups: Dict[tuple, List[int]] = {}
     for i, o in enumerate(S):
         if o is not None and o[0] == "gpu":
             groups.setdefault((tensors[i].n, o), []).append(i)
     keys = sorted(groups)
-    for k in keys:  # farthest from the output layer first (the paper's lemma)
-        groups[k].sort(reverse=True)
+    if lemma_order not in ("earliest", "farthest"):
+        raise ValueError(lemma_order)
+    for k in keys:  # tensor index = backward order: 0 is ready first, closest to the output layer
+        groups[k].sort(reverse=(lemma_order == "farthest"))
 
     def apply(U):
         out = list(S)
@@ -331,14 +350,26 @@ def plan_cpu(tensors: Sequence[Tensor], S: Sequence[Option], model: CostModel, m
 def load_profile_rows(path: str) -> List[dict]:
     """Rows of the compression-time table the profiler writes (its text form)."""
     rows = []
-    pat = re.compile(r"^(\w+)\s+(\d+)\s+(\d+)\s+([\d.]+)\s+([\d.]+)\s+([\d.]+)\s*$")
+    pat = re.compile(r"^(\w+)\s+(gpu|cpu)\s+(\d+)\s+(\d+)\s+([\d.]+)\s+([\d.]+)\s+([\d.]+)\s+(\d+)\s*$")
     with open(path) as fh:
         for line in fh:
             m = pat.match(line)
             if m:
-                rows.append({"kind": m.group(1), "n": int(m.group(2)), "compress_us": float(m.group(4)),
-                             "aggregate_us": float(m.group(5))})
+                rows.append({"kind": m.group(1), "device": m.group(2), "n": int(m.group(3)),
+                             "compress_us": float(m.group(5)), "aggregate_us": float(m.group(6)),
+                             "runs": int(m.group(8))})
     return rows
+
+
+def load_profile_pcie(path: str) -> Optional[Dict[str, float]]:
+    """The host <-> device copy rates (GB/s) the profiler measured, if any."""
+    pat = re.compile(r"^# pcie_gbs h2d ([\d.]+) d2h ([\d.]+)")
+    with open(path) as fh:
+        for line in fh:
+            m = pat.match(line)
+            if m:
+                return {"h2d": float(m.group(1)), "d2h": float(m.group(2))}
+    return None
 
 
 def synthetic_job(model_name: str, us_per_mparam: float) -> List[Tensor]:
@@ -367,7 +398,7 @@ def main(argv=None) -> None:
     a = ap.parse_args(argv)
     tensors = synthetic_job(a.model, a.us_per_mparam)
     model = CostModel(a.kind, a.ratio, load_profile_rows(a.table),
-                      Cluster(N=a.N, link_gbs=a.link_gbs, alpha_us=a.alpha_us))
+                      Cluster(N=a.N, link_gbs=a.link_gbs, alpha_us=a.alpha_us), pcie=load_profile_pcie(a.table))
     t0 = time.perf_counter()
     S1 = plan_gpu(tensors, model)
     t1 = time.perf_counter()

@@ -70,19 +70,43 @@ def test_bubble_rule_keeps_earlier_tensors_uncompressed():
 
 def _instances(count, seed=0):
     rows = P.load_profile_rows(TABLE)
+    pcie = P.load_profile_pcie(TABLE)
     for trial in range(count):
         rnd = random.Random(seed + trial)
         T = rnd.randint(3, 6)
         tensors = [P.Tensor(rnd.choice([1 << 16, 1 << 20, 1 << 22]), rnd.uniform(50, 2000)) for _ in range(T)]
-        cl = P.Cluster(N=rnd.choice([4, 8, 16]), link_gbs=rnd.choice([3.0, 12.5]), cpu_gbs=rnd.choice([2.0, 8.0]))
-        yield tensors, P.CostModel(rnd.choice(["sign", "topk", "randk"]), 0.01, rows, cl)
+        cl = P.Cluster(N=rnd.choice([4, 8, 16]), link_gbs=rnd.choice([3.0, 12.5]))
+        # the measured CPU times, and hosts 4x faster or slower than the one profiled
+        f = rnd.choice([0.25, 1.0, 4.0])
+        scaled = [dict(r, compress_us=r["compress_us"] * f, aggregate_us=r["aggregate_us"] * f)
+                  if r["device"] == "cpu" else r for r in rows]
+        yield tensors, P.CostModel(rnd.choice(["sign", "topk", "randk"]), 0.01, scaled, cl, pcie=pcie)
 
 
 def test_profile_table_loads():
     rows = P.load_profile_rows(TABLE)
-    kinds = {r["kind"] for r in rows}
-    assert {"topk", "topk_sampled", "randk", "sign"} <= kinds
-    assert all(r["compress_us"] > 0 and r["aggregate_us"] > 0 for r in rows)
+    for dev in ("gpu", "cpu"):
+        kinds = {r["kind"] for r in rows if r["device"] == dev}
+        assert {"topk", "topk_sampled", "randk", "sign"} <= kinds, dev
+    assert all(r["compress_us"] > 0 and r["aggregate_us"] > 0 and r["runs"] >= 3 for r in rows)
+    pcie = P.load_profile_pcie(TABLE)
+    assert pcie and pcie["h2d"] > 1.0 and pcie["d2h"] > 1.0
+    m = P.CostModel("topk", 0.01, rows, P.Cluster(), pcie=pcie)
+    assert m.has_cpu
+    # the CPU curve is the measured one: at a profiled size it returns the row
+    r = next(r for r in rows if r["device"] == "cpu" and r["kind"] == "topk" and r["n"] == 1 << 20)
+    assert m.compress("cpu", 1 << 20) == pytest.approx(r["compress_us"])
+    assert m.aggregate("cpu", 1 << 20, 8) == pytest.approx(r["aggregate_us"])
+
+
+def test_no_cpu_option_without_measured_cpu_times():
+    rows = [r for r in P.load_profile_rows(TABLE) if r["device"] == "gpu"]
+    m = P.CostModel("sign", 0.01, rows, P.Cluster(), pcie=P.load_profile_pcie(TABLE))
+    assert not m.has_cpu
+    tensors = [P.Tensor(1 << 20, 500.0) for _ in range(4)]
+    S1 = P.plan_gpu(tensors, m)
+    S2, evals = P.plan_cpu(tensors, S1, m)
+    assert S2 == S1 and evals == 0
 
 
 def test_algorithm1_never_worse_than_no_compression():
@@ -92,51 +116,68 @@ def test_algorithm1_never_worse_than_no_compression():
         assert all(o is None or o[0] == "gpu" for o in S)
 
 
-def test_algorithm2_is_the_best_lemma_restricted_offloading():
+def _group_offload(S1, groups, U, farthest):
+    S = list(S1)
+    for g, u in zip(groups.values(), U):
+        for i in sorted(g, reverse=farthest)[:u]:
+            S[i] = ("cpu", S[i][1])
+    return S
+
+
+@pytest.mark.parametrize("order", ["earliest", "farthest"])
+def test_algorithm2_is_the_best_lemma_restricted_offloading(order):
     # Algorithm 2 against brute force over its own search space: in each
-    # (size, option) group, offload the u tensors farthest from the output
+    # (size, option) group, offload the first u tensors in the lemma's order
     for tensors, m in _instances(25, seed=100):
         S1 = P.plan_gpu(tensors, m)
-        S2, evals = P.plan_cpu(tensors, S1, m)
+        S2, evals = P.plan_cpu(tensors, S1, m, lemma_order=order)
         groups = {}
         for i, o in enumerate(S1):
             if o:
                 groups.setdefault((tensors[i].n, o), []).append(i)
         best = math.inf
         for U in itertools.product(*[range(len(g) + 1) for g in groups.values()]):
-            S = list(S1)
-            for g, u in zip(groups.values(), U):
-                for i in sorted(g, reverse=True)[:u]:
-                    S[i] = ("cpu", S[i][1])
-            best = min(best, P.simulate(tensors, S, m).iteration_us)
+            best = min(best, P.simulate(tensors, _group_offload(S1, groups, U, order == "farthest"), m).iteration_us)
         f2 = P.simulate(tensors, S2, m).iteration_us
         assert f2 == pytest.approx(best, abs=1e-9)
         assert f2 <= P.simulate(tensors, S1, m).iteration_us
 
 
+def _best_subset(tensors, S1, m):
+    comp = [i for i, o in enumerate(S1) if o]
+    best = math.inf
+    for mask in range(1 << len(comp)):
+        S = list(S1)
+        for b, i in enumerate(comp):
+            if mask >> b & 1:
+                S[i] = ("cpu", S[i][1])
+        best = min(best, P.simulate(tensors, S, m).iteration_us)
+    return best
+
+
 def test_algorithm2_against_every_offloading_subset():
-    # the paper's lemma (offload the farthest tensors of a group first) is
-    # exact under its own model; in this timeline model it is not always:
-    # over random instances Algorithm 2 finds the best of all 2^|T_gpu|
-    # subsets in most of them and is never far from it
-    hit, total, worst = 0, 0, 0.0
-    for tensors, m in _instances(40, seed=200):
+    # the lemma restricts each group to offloading its first u tensors; in
+    # this timeline model, with the measured GPU and CPU times, the
+    # earliest-ready-first order reaches the best of all 2^|T_gpu| subsets
+    # on every random instance
+    for tensors, m in _instances(60, seed=200):
         S1 = P.plan_gpu(tensors, m)
         S2, _ = P.plan_cpu(tensors, S1, m)
-        comp = [i for i, o in enumerate(S1) if o]
-        best = math.inf
-        for mask in range(1 << len(comp)):
-            S = list(S1)
-            for b, i in enumerate(comp):
-                if mask >> b & 1:
-                    S[i] = ("cpu", S[i][1])
-            best = min(best, P.simulate(tensors, S, m).iteration_us)
+        assert P.simulate(tensors, S2, m).iteration_us <= _best_subset(tensors, S1, m) + 1e-9
+
+
+def test_lemma_statement_order_is_not_always_best_here():
+    # the statement's order (farthest from the output layer first) misses
+    # the best subset on some instances of this model (the reading the
+    # default order takes); it is never worse than GPU-only compression
+    miss = 0
+    for tensors, m in _instances(60, seed=200):
+        S1 = P.plan_gpu(tensors, m)
+        S2, _ = P.plan_cpu(tensors, S1, m, lemma_order="farthest")
         f2 = P.simulate(tensors, S2, m).iteration_us
-        total += 1
-        hit += f2 <= best + 1e-9
-        worst = max(worst, f2 / best - 1.0)
-    assert hit >= 0.9 * total
-    assert worst < 0.02
+        assert f2 <= P.simulate(tensors, S1, m).iteration_us
+        miss += f2 > _best_subset(tensors, S1, m) + 1e-9
+    assert miss > 0
 
 
 def test_cli_runs_on_the_committed_table(capsys):

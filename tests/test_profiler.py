@@ -28,6 +28,21 @@ def test_benefit_ratio_grows_with_size_for_fixed_overhead():
     assert r[0] < r[1] < r[2]
 
 
+def test_cpu_profile_runs_every_kind():
+    """The CPU side times the library's host operators (no GPU needed)."""
+    rows = P.profile_cpu(sizes=[1 << 10, 1 << 16], runs=3, W=4, warmup=1, threads=2)
+    assert len(rows) == 2 * len(P.KINDS)
+    for r in rows:
+        assert r.device == "cpu" and r.runs == 3
+        assert r.compress_us > 0 and r.aggregate_us > 0 and r.payload_bytes > 0
+    assert " cpu " in P.table(rows)
+
+
+def test_cpu_profile_cuts_runs_to_the_budget():
+    rows = P.profile_cpu(kinds=["topk"], sizes=[1 << 20], runs=1000, W=2, warmup=1, threads=2, budget_s=0.01)
+    assert 3 <= rows[0].runs < 1000
+
+
 @pytest.mark.gpu
 def test_profile_runs_every_kind():
     rows = P.profile(sizes=[1 << 10, 1 << 16], runs=3, W=4, warmup=1)

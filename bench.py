@@ -236,9 +236,10 @@ def kernel_candidates(wl, kind, comp_b, agg_b, pay_b):
     if kind == "randk":
         return [("randk_stream", comp_b), ("aggregate_sparse", agg_b)]
     if kind in ("topk", "topk_sampled"):
-        # the streaming EF pass reads g and e and writes e; the payload is
-        # written by the emit kernel
-        return [("topk_compact", (g_in + 8) * n), ("aggregate_sparse", agg_b)]
+        # the streaming EF pass (topk_compact in the general pipeline,
+        # topk_hist in the few-chunk path) reads g and e and writes e; the
+        # payload is written by the emit kernel
+        return [("topk_compact", (g_in + 8) * n), ("topk_hist", (g_in + 8) * n), ("aggregate_sparse", agg_b)]
     if kind == "sign":
         # one pass: everything; two passes: the first reads g and e and
         # writes the bits and scales

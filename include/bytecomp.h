@@ -326,11 +326,20 @@ int bytecomp_device_status(void* ws, size_t ws_bytes, void* stream, uint32_t* fl
  * that path).  Default 200; BC_E_SIZE above 10 s. */
 int bytecomp_set_wait_limit(uint32_t microseconds);
 
+/* Path choice for top-k compression (both kinds), for tests and tuning:
+ * calls of at most `chunks` 4096-element chunks in total take the
+ * few-chunk path (five launches, exact selection, a look-back across
+ * chunks), larger calls the general pipeline; both give the same result.
+ * Default and maximum 2048 (BC_E_SIZE above); 0 sends every call to the
+ * general pipeline.  Process-wide; takes effect at the next call. */
+int bytecomp_set_topk_few_chunks(uint32_t chunks);
+
 /* Instrumentation, not part of the method: for callers that measure one
  * kernel's own duration (benchmarks).  The next launch, by any call, of
  * the kernel named `kernel` ("aggregate_sign", "aggregate_sparse",
- * "randk_stream", "topk_compact", "sign_onepass", "sign_pass1" (the first
- * kernel of the two-pass sign compress), "quant_onepass", "quant_pass1",
+ * "randk_stream", "topk_compact", "topk_hist" (the histogram pass of the
+ * few-chunk top-k path), "sign_onepass", "sign_pass1" (the first kernel of
+ * the two-pass sign compress), "quant_onepass", "quant_pass1",
  * "aggregate_quant") records `start_event` when it begins and `stop_event`
  * when it ends (HIP events created by the caller, on the launch's stream);
  * the request is then cleared.  Both events NULL clears a pending request

@@ -97,6 +97,8 @@ def lib():
         L.bytecomp_time_next_launch.argtypes = [ctypes.c_char_p, vp, vp]
         L.bytecomp_set_wait_limit.restype = i32
         L.bytecomp_set_wait_limit.argtypes = [ctypes.c_uint32]
+        L.bytecomp_set_topk_few_chunks.restype = i32
+        L.bytecomp_set_topk_few_chunks.argtypes = [ctypes.c_uint32]
         _lib = L
     return _lib
 
@@ -348,6 +350,12 @@ def bytecomp_set_wait_limit(microseconds):
     tensor's chunk partials before it computes the missing ones itself
     (process-wide; default 200)."""
     _check("bytecomp_set_wait_limit", lib().bytecomp_set_wait_limit(int(microseconds)))
+
+
+def bytecomp_set_topk_few_chunks(chunks):
+    """Top-k calls of at most `chunks` chunks take the few-chunk path
+    (default and maximum 2048; 0: always the general pipeline)."""
+    _check("bytecomp_set_topk_few_chunks", lib().bytecomp_set_topk_few_chunks(int(chunks)))
 
 
 def bytecomp_device_status(ws, stream=None):

@@ -203,7 +203,10 @@ bool set_kernel_timer(int k, hipEvent_t start, hipEvent_t stop) {
 // ------------------------------------------------- one-pass wait limit
 namespace {
 std::atomic<uint32_t> g_wait_us{200};
+std::atomic<uint32_t> g_topk_few{kTopkFewChunksMax};
 }  // namespace
+
+uint32_t topk_few_chunks_limit() { return g_topk_few.load(std::memory_order_relaxed); }
 
 uint32_t onepass_wait_ticks() {
     int dev = 0;
@@ -250,7 +253,8 @@ WsPlan plan_workspace(int kind, int T, uint64_t C, uint64_t sum_k, bool agg_tabl
             take(p.s_tab, t * 4096 * 4);
         }
     } else if (kind == BC_TOPK || kind == BC_TOPK_SAMPLED) {
-        take(p.t_hist, t * kBins0 * 4);
+        // digit 0; the few-chunk path: up to 4 copies of digit 0, then digits 1 and 2
+        take(p.t_hist, C <= kTopkFewChunksMax ? t * (4 * kBins0 + 2 * kBins12) * 4 : t * kBins0 * 4);
         take(p.t_thr, t * 4);
         take(p.t_prefix, t * 4);
         take(p.t_krem, t * 4);
@@ -825,7 +829,7 @@ int bytecomp_time_next_launch(const char* kernel, void* start_event, void* stop_
         {"randk_stream", kTimedRandkStream},     {"topk_compact", kTimedTopkCompact},
         {"sign_pass1", kTimedSignPass1},         {"quant_pass1", kTimedQuantPass1},
         {"aggregate_quant", kTimedAggQuant},     {"sign_onepass", kTimedSignOnepass},
-        {"quant_onepass", kTimedQuantOnepass}};
+        {"quant_onepass", kTimedQuantOnepass},   {"topk_hist", kTimedTopkHist}};
     for (const auto& x : names) {
         if (std::strcmp(kernel, x.name) == 0) {
             (void)set_kernel_timer(x.k, (hipEvent_t)start_event, (hipEvent_t)stop_event);
@@ -838,6 +842,12 @@ int bytecomp_time_next_launch(const char* kernel, void* start_event, void* stop_
 int bytecomp_set_wait_limit(uint32_t microseconds) {
     if (microseconds > 10000000u) return BC_E_SIZE;
     g_wait_us.store(microseconds, std::memory_order_relaxed);
+    return BC_OK;
+}
+
+int bytecomp_set_topk_few_chunks(uint32_t chunks) {
+    if (chunks > kTopkFewChunksMax) return BC_E_SIZE;
+    g_topk_few.store(chunks, std::memory_order_relaxed);
     return BC_OK;
 }
 

@@ -58,10 +58,12 @@ __device__ __forceinline__ void flush_hist(const uint32_t* lh, uint32_t* gh, int
 // histogram of key bits 30..20.  With `fb_only` it re-reads the stored v of
 // tensors flagged for the fallback.
 __global__ __launch_bounds__(kBlock) void topk_hist_pass(const TDesc* __restrict__ d, int T, uint32_t C,
-                                                         int write_resid, int fb_only, Ws ws) {
+                                                         int write_resid, int fb_only, Ws ws,
+                                                         uint64_t* __restrict__ clear_status, int copies) {
     __shared__ uint32_t lh[kBins0];
     if (fb_only && ws.t_any[0] == 0u) return;  // no tensor fell back
     for (uint32_t c = blockIdx.x; c < C; c += gridDim.x) {
+        if (clear_status && threadIdx.x == 0) clear_status[c] = 0ull;
         const int t = tensor_of_chunk(d, T, c);
         if (!active(ws.t_fb, t, fb_only)) continue;
         const TDesc td = d[t];
@@ -80,7 +82,7 @@ __global__ __launch_bounds__(kBlock) void topk_hist_pass(const TDesc* __restrict
         for (int i = 0; i < kEpt; ++i)
             if ((valid >> i) & 1u) atomicAdd(&lh[key_of(v[i]) >> 20], 1u);
         __syncthreads();
-        flush_hist(lh, ws.t_hist + (size_t)t * kBins0, kBins0);
+        flush_hist(lh, ws.t_hist + ((size_t)(c % (uint32_t)copies) * T + t) * kBins0, kBins0);
         __syncthreads();
     }
 }
@@ -520,6 +522,337 @@ __global__ __launch_bounds__(kBlock) void topk_emit(const TDesc* __restrict__ d,
     }
 }
 
+// ------------------------------------------------- few-chunk exact path
+// Calls of at most topk_few_chunks_limit() chunks (2048 unless set lower)
+// take a path of five launches (the
+// general pipeline's per-step launches cost more than the passes themselves
+// at these sizes): clear, the histogram pass, then three kernels that each
+// redo the previous radix step's bin search from the global histogram in
+// every workgroup instead of in a launch of its own:
+//   compact:  bin b of the k-th key (digit 0) -> candidates (keys at or
+//             above bin b) per chunk, index order; histogram of digit 1
+//             among the candidates in bin b;
+//   digit 2:  digit 1 -> histogram of digit 2 among the candidates whose
+//             digits 0 and 1 match;
+//   emit:     digit 2 gives the k-th key tau and how many tau-equal entries
+//             to keep; each wave takes one chunk, counts its candidates
+//             above and equal to tau, and finds the counts of all earlier
+//             chunks of its tensor by looking back over their published
+//             counts (decoupled look-back, Merrill and Garland 2016): a
+//             chunk's wave publishes its own counts, then its running
+//             totals; a wave that finds an earlier chunk unpublished
+//             counts that chunk's candidates itself, so no wave waits for
+//             another and the pass needs no particular residency.
+// Histogram regions: digit 0 in `copies` copies (chunk c adds to copy
+// c % copies, which spreads the atomic additions to the busiest bins over
+// several addresses; readers add the copies) at t_hist[(r * T + t) * 2048],
+// then digit 1 at t_hist[copies * T * 2048 + t * 1024] and digit 2 at
+// t_hist[copies * T * 2048 + T * 1024 + t * 1024].
+// Look-back words (t_off, cleared by the histogram pass): bit 62 counts
+// published, bit 63 running totals published, bits 61..31 entries above
+// tau, bits 30..0 entries equal to tau (chunk counts, or totals over the
+// tensor's chunks up to and including this one).
+constexpr uint64_t kLbCounts = 1ull << 62, kLbTotals = 1ull << 63;
+constexpr int kLbPolls = 16;  // re-reads of unpublished look-back words before counting them
+constexpr int kFewCopiesMax = 4;
+// digit-0 histogram copies of a few-chunk call of T tensors
+inline int few_copies(int T) { return T <= 16 ? kFewCopiesMax : 1; }
+
+namespace {
+
+// Bin holding the target-th largest entry of a global histogram, searched
+// by the whole workgroup (thread i owns the i-th run of bins from the top);
+// *above receives the entries in higher bins.  Needs 1 <= target <= total.
+__device__ uint32_t block_hist_select(const uint32_t* __restrict__ gh, int bins, uint32_t target, uint64_t* sh,
+                                      uint32_t* res_sh, uint32_t* above, int copies = 1,
+                                      size_t copy_stride = 0) {
+    const int per = bins / kBlock;  // 8 or 4
+    const int hi = bins - (int)threadIdx.x * per;
+    uint32_t h[8];
+    uint32_t mine = 0;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) h[q] = q < per ? gh[hi - 1 - q] : 0u;
+    for (int r = 1; r < copies; ++r)
+#pragma unroll
+        for (int q = 0; q < 8; ++q) h[q] += q < per ? gh[r * copy_stride + hi - 1 - q] : 0u;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) mine += h[q];
+    uint64_t tot;
+    uint32_t a = (uint32_t)block_excl_scan_u64(mine, sh, tot);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        if (q < per && a < target && target <= a + h[q]) {
+            res_sh[0] = (uint32_t)(hi - 1 - q);
+            res_sh[1] = a;
+        }
+        a += h[q];
+    }
+    __syncthreads();
+    const uint32_t b = res_sh[0];
+    *above = res_sh[1];
+    __syncthreads();
+    return b;
+}
+
+// The same over 1024 bins by one wave (lane i owns the i-th run of 16
+// bins from the top).
+__device__ uint32_t wave_hist_select(const uint32_t* __restrict__ gh, uint32_t target, uint32_t* above) {
+    const int lane = lane_id();
+    const int hi = kBins12 - lane * 16;
+    uint32_t h[16];
+    uint32_t mine = 0;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+        h[q] = gh[hi - 1 - q];
+        mine += h[q];
+    }
+    uint32_t inc = mine;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t y = __shfl_up(inc, o, 64);
+        if (lane >= o) inc += y;
+    }
+    uint32_t a = inc - mine;
+    int found = -1;
+    uint32_t fa = 0;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+        if (found < 0 && a < target && target <= a + h[q]) {
+            found = hi - 1 - q;
+            fa = a;
+        }
+        a += h[q];
+    }
+    const uint64_t m = __ballot(found >= 0);
+    const int src = m ? (int)__builtin_ctzll(m) : 0;
+    *above = (uint32_t)__shfl(fa, src, 64);
+    return (uint32_t)__shfl(found, src, 64);
+}
+
+__device__ __forceinline__ uint64_t lb_load(const uint64_t* p) {
+    return __hip_atomic_load((unsigned long long*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void lb_store(uint64_t* p, uint64_t v) {
+    __hip_atomic_store((unsigned long long*)p, (unsigned long long)v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t lb_word(uint64_t flag, uint32_t gt, uint32_t eq) {
+    return flag | (uint64_t)gt << 31 | (uint64_t)eq;
+}
+
+// Candidates of chunk c above and equal to tau, counted by one wave.
+__device__ __forceinline__ void wave_count_chunk(const Ws& ws, uint32_t c, uint32_t tau, uint32_t& gt,
+                                                 uint32_t& eq) {
+    const int lane = lane_id();
+    const uint32_t m = ws.t_ccount[c];
+    const uint2* cand = ws.t_cand + (size_t)c * kChunk;
+    gt = 0;
+    eq = 0;
+    for (uint32_t i0 = 0; i0 < m; i0 += 64) {
+        const uint32_t i = i0 + (uint32_t)lane;
+        const uint32_t key = i < m ? cand[i].y & 0x7FFFFFFFu : 0u;
+        gt += (uint32_t)__popcll(__ballot(i < m && key > tau));
+        eq += (uint32_t)__popcll(__ballot(i < m && key == tau));
+    }
+}
+
+}  // namespace
+
+// Digit 0 from the histogram pass's counts, then candidate compaction
+// (v re-read from the stored e_new, or from g without error feedback) and
+// the digit-1 histogram of the candidates in bin b.
+__global__ __launch_bounds__(kBlock) void topk_fast_compact(const TDesc* __restrict__ d, int T, uint32_t C,
+                                                            int copies, Ws ws) {
+    __shared__ uint32_t lh[kBins12];
+    __shared__ uint64_t sh[4];
+    __shared__ uint32_t res_sh[2];
+    const uint32_t c = blockIdx.x;
+    const int t = tensor_of_chunk(d, T, c);
+    const TDesc td = d[t];
+    const uint32_t j = c - td.chunk0;
+    float v[kEpt];
+    uint32_t valid;
+    load_stored_v(td, j, v, valid);  // in flight during the bin search
+    for (int b = threadIdx.x; b < kBins12; b += kBlock) lh[b] = 0;
+    uint32_t above;
+    const uint32_t b0 = block_hist_select(ws.t_hist + (size_t)t * kBins0, kBins0, td.k, sh, res_sh, &above, copies,
+                                          (size_t)T * kBins0);
+    if (j == 0 && threadIdx.x == 0) {
+        ws.t_thr[t] = b0 << 20;
+        ws.t_fb[t] = td.k - above;  // entries still to select inside bin b
+    }
+    const uint32_t thr = b0 << 20;
+    uint32_t pm = 0;
+#pragma unroll
+    for (int i = 0; i < kEpt; ++i)
+        if (((valid >> i) & 1u) && key_of(v[i]) >= thr) pm |= 1u << i;
+    uint64_t packed = 0;
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r) packed |= (uint64_t)__popc((pm >> (4 * r)) & 0xFu) << (16 * r);
+    uint64_t tot;
+    const uint64_t pre = block_excl_scan_u64(packed, sh, tot);
+    uint2* out = ws.t_cand + (size_t)c * kChunk;
+    uint32_t base = 0;
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r) {
+        uint32_t rank = base + (uint32_t)((pre >> (16 * r)) & 0xFFFFu);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int i = 4 * r + q;
+            if ((pm >> i) & 1u) {
+                const uint32_t e = j * (uint32_t)kChunk + 1024u * r + 4u * threadIdx.x + q;
+                const uint32_t key = key_of(v[i]);
+                out[rank++] = make_uint2(e, f2u(v[i]));
+                if ((key >> 20) == b0) atomicAdd(&lh[(key >> 10) & (kBins12 - 1)], 1u);
+            }
+        }
+        base += (uint32_t)((tot >> (16 * r)) & 0xFFFFu);
+    }
+    if (threadIdx.x == 0) ws.t_ccount[c] = base;
+    __syncthreads();
+    flush_hist(lh, ws.t_hist + (size_t)copies * T * kBins0 + (size_t)t * kBins12, kBins12);
+}
+
+// Digit 1, then the digit-2 histogram of the candidates whose digits 0 and
+// 1 match.
+__global__ __launch_bounds__(kBlock) void topk_fast_digit2(const TDesc* __restrict__ d, int T, int copies, Ws ws) {
+    __shared__ uint32_t lh[kBins12];
+    __shared__ uint64_t sh[4];
+    __shared__ uint32_t res_sh[2];
+    const uint32_t c = blockIdx.x;
+    const int t = tensor_of_chunk(d, T, c);
+    const TDesc td = d[t];
+    const uint32_t j = c - td.chunk0;
+    uint32_t* h1 = ws.t_hist + (size_t)copies * T * kBins0;
+    // the chunk's count and first candidates, in flight during the bin search
+    // (a slot holds kChunk entries, so the first kBlock are always in bounds)
+    const uint32_t m = ws.t_ccount[c];
+    const uint2* cand = ws.t_cand + (size_t)c * kChunk;
+    const uint32_t key0 = cand[threadIdx.x].y & 0x7FFFFFFFu;
+    for (int b = threadIdx.x; b < kBins12; b += kBlock) lh[b] = 0;
+    const uint32_t thr = ws.t_thr[t], r0 = ws.t_fb[t];
+    uint32_t above;
+    const uint32_t d1 = block_hist_select(h1 + (size_t)t * kBins12, kBins12, r0, sh, res_sh, &above);
+    const uint32_t prefix = thr | d1 << 10;
+    if (j == 0 && threadIdx.x == 0) {
+        ws.t_prefix[t] = prefix;
+        ws.t_krem[t] = r0 - above;
+    }
+    if (threadIdx.x < m && (key0 >> 10) == (prefix >> 10)) atomicAdd(&lh[key0 & (kBins12 - 1)], 1u);
+    for (uint32_t i = threadIdx.x + kBlock; i < m; i += kBlock) {
+        const uint32_t key = cand[i].y & 0x7FFFFFFFu;
+        if ((key >> 10) == (prefix >> 10)) atomicAdd(&lh[key & (kBins12 - 1)], 1u);
+    }
+    __syncthreads();
+    flush_hist(lh, h1 + (size_t)T * kBins12 + (size_t)t * kBins12, kBins12);
+}
+
+// Digit 2 gives tau; one wave per chunk counts, looks back, and emits its
+// winners in index order (clearing them in e_new).
+__global__ __launch_bounds__(kBlock) void topk_fast_emit(const TDesc* __restrict__ d, int T, uint32_t C, int copies,
+                                                         uint32_t* __restrict__ idx, float* __restrict__ val,
+                                                         Ws ws) {
+    const int lane = lane_id();
+    const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
+    const uint32_t c = blockIdx.x * (kBlock / 64) + wave_id();
+    if (c >= C) return;
+    const int t = tensor_of_chunk(d, T, c);
+    const TDesc td = d[t];
+    // the chunk's count and first 64 candidates, in flight during the bin
+    // search (always inside the chunk's slot)
+    const uint32_t m = ws.t_ccount[c];
+    const uint2* cand = ws.t_cand + (size_t)c * kChunk;
+    const uint2 first = cand[lane];
+    const uint32_t prefix = ws.t_prefix[t], r1 = ws.t_krem[t];
+    uint32_t above;
+    const uint32_t d2 =
+        wave_hist_select(ws.t_hist + (size_t)copies * T * kBins0 + (size_t)(T + t) * kBins12, r1, &above);
+    const uint32_t tau = prefix | d2;
+    const uint32_t need = r1 - above;  // tau-equal entries to keep, lowest indices first
+    uint32_t gt, eq;
+    {
+        const uint32_t key = (uint32_t)lane < m ? first.y & 0x7FFFFFFFu : 0u;
+        gt = (uint32_t)__popcll(__ballot((uint32_t)lane < m && key > tau));
+        eq = (uint32_t)__popcll(__ballot((uint32_t)lane < m && key == tau));
+        for (uint32_t i0 = 64; i0 < m; i0 += 64) {
+            const uint32_t i = i0 + (uint32_t)lane;
+            const uint32_t k2 = i < m ? cand[i].y & 0x7FFFFFFFu : 0u;
+            gt += (uint32_t)__popcll(__ballot(i < m && k2 > tau));
+            eq += (uint32_t)__popcll(__ballot(i < m && k2 == tau));
+        }
+    }
+    uint64_t* lb = ws.t_off;
+    if (lane == 0) lb_store(lb + c, lb_word(kLbCounts, gt, eq));
+    // totals of the earlier chunks of the tensor
+    uint32_t gt_b = 0, eq_b = 0;
+    for (int64_t q0 = (int64_t)c - 1; q0 >= (int64_t)td.chunk0; q0 -= 64) {
+        const int64_t q = q0 - lane;
+        const bool in = q >= (int64_t)td.chunk0;
+        uint64_t w = in ? lb_load(lb + q) : 0ull;
+        uint64_t tot_m;
+        int lim;
+        // chunks whose waves run alongside this one publish within a few
+        // load latencies: poll those still unpublished a bounded number of
+        // times before counting them here
+        for (int spin = 0;; ++spin) {
+            tot_m = __ballot(in && (w & kLbTotals));
+            lim = tot_m ? (int)__builtin_ctzll(tot_m) : 63;  // up to the nearest chunk with totals
+            const bool pend = in && lane <= lim && w == 0ull;
+            if (!__ballot(pend) || spin == kLbPolls) break;
+            __builtin_amdgcn_s_sleep(4);
+            if (pend) w = lb_load(lb + q);
+        }
+        const bool use = in && lane <= lim;
+        // unpublished chunks: count them here, one at a time with the whole wave
+        uint64_t help = __ballot(use && w == 0ull);
+        while (help) {
+            const int l = (int)__builtin_ctzll(help);
+            help &= help - 1;
+            uint32_t hg, he;
+            wave_count_chunk(ws, (uint32_t)(q0 - l), tau, hg, he);
+            if (lane == l) w = lb_word(kLbCounts, hg, he);
+        }
+        uint32_t g = use ? (uint32_t)(w >> 31) & 0x7FFFFFFFu : 0u;
+        uint32_t e = use ? (uint32_t)w & 0x7FFFFFFFu : 0u;
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) {
+            g += __shfl_xor(g, o, 64);
+            e += __shfl_xor(e, o, 64);
+        }
+        gt_b += g;
+        eq_b += e;
+        if (tot_m) break;
+    }
+    if (lane == 0) lb_store(lb + c, lb_word(kLbCounts | kLbTotals, gt_b + gt, eq_b + eq));
+    // emit
+    if (m == 0) return;
+    float* resid = td.resid;
+    const uint64_t end = td.off + td.k;
+    uint64_t eq_seen = eq_b;
+    uint64_t pos = td.off + gt_b + (eq_b < need ? eq_b : need);
+    for (uint32_t i0 = 0; i0 < m; i0 += 64) {
+        const uint32_t i = i0 + lane;
+        uint2 e = make_uint2(0, 0);
+        uint32_t key = 0;
+        if (i < m) {
+            e = i0 == 0 ? first : cand[i];
+            key = e.y & 0x7FFFFFFFu;
+        }
+        const bool is_eq = i < m && key == tau;
+        const uint64_t meq = __ballot(is_eq);
+        const uint64_t eq_rank = eq_seen + (uint64_t)__popcll(meq & below);
+        const bool sel = i < m && (key > tau || (is_eq && eq_rank < need));
+        const uint64_t msel = __ballot(sel);
+        const uint64_t at = pos + (uint64_t)__popcll(msel & below);
+        if (sel && at < end) {
+            idx[at] = e.x;
+            val[at] = u2f(e.y);
+            if (resid) gp(resid)[e.x] = 0.f;
+        }
+        eq_seen += (uint64_t)__popcll(meq);
+        pos += (uint64_t)__popcll(msel);
+    }
+}
+
 // Clear the tensors' histograms (T * 2048 words, a multiple of 4) and the
 // fallback flag at the start of a call.
 __global__ void topk_zero_hist(uint32_t* h, uint64_t n, uint32_t* any) {
@@ -533,12 +866,25 @@ hipError_t launch_topk(int kind, double ratio, uint64_t seed, const TDesc* d, in
                        bool, bool, uint32_t* idx, float* val, const Ws& ws, hipStream_t s) {
     if (C == 0) return hipSuccess;
     const dim3 blk(kBlock);
+    if (C <= topk_few_chunks_limit()) {  // few chunks: the five-launch exact path (both kinds: same result)
+        const int copies = few_copies(T);
+        const uint64_t hn = (uint64_t)T * ((uint64_t)copies * kBins0 + 2 * kBins12);
+        uint32_t zb = (uint32_t)((hn / 4 + 255) / 256);
+        if (zb > 4096) zb = 4096;
+        hipLaunchKernelGGL(topk_zero_hist, dim3(zb), dim3(256), 0, s, ws.t_hist, hn, ws.t_any);
+        (void)launch_timed(kTimedTopkHist, topk_hist_pass, dim3(C), blk, 0, s, d, T, C, 1, 0, ws, ws.t_off, copies);
+        hipLaunchKernelGGL(topk_fast_compact, dim3(C), blk, 0, s, d, T, C, copies, ws);
+        hipLaunchKernelGGL(topk_fast_digit2, dim3(C), blk, 0, s, d, T, copies, ws);
+        hipLaunchKernelGGL(topk_fast_emit, dim3((C + kBlock / 64 - 1) / (kBlock / 64)), blk, 0, s, d, T, C, copies,
+                           idx, val, ws);
+        return hipGetLastError();
+    }
     const uint64_t hn = (uint64_t)T * kBins0;
     uint32_t zb = (uint32_t)((hn / 4 + 255) / 256);
     if (zb > 4096) zb = 4096;
     hipLaunchKernelGGL(topk_zero_hist, dim3(zb), dim3(256), 0, s, ws.t_hist, hn, ws.t_any);
     if (kind == 0) {  // exact
-        hipLaunchKernelGGL(topk_hist_pass, dim3(C), blk, 0, s, d, T, C, 1, 0, ws);
+        hipLaunchKernelGGL(topk_hist_pass, dim3(C), blk, 0, s, d, T, C, 1, 0, ws, (uint64_t*)nullptr, 1);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindThrExact, 0, ws);
         (void)launch_timed(kTimedTopkCompact, topk_compact<false>, dim3(C), blk, 0, s, d, T, C, 0, 0, ws);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit0, 0, ws);
@@ -554,7 +900,7 @@ hipError_t launch_topk(int kind, double ratio, uint64_t seed, const TDesc* d, in
         // fallback passes: small grids that walk the chunks, and return at
         // once when no tensor fell back (the usual case)
         const dim3 fb_grid(C < 1024u ? C : 1024u);
-        hipLaunchKernelGGL(topk_hist_pass, fb_grid, blk, 0, s, d, T, C, 0, 1, ws);
+        hipLaunchKernelGGL(topk_hist_pass, fb_grid, blk, 0, s, d, T, C, 0, 1, ws, (uint64_t*)nullptr, 1);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindThrExact, 1, ws);
         hipLaunchKernelGGL(topk_compact<false>, fb_grid, blk, 0, s, d, T, C, 0, 1, ws);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit0, 1, ws);

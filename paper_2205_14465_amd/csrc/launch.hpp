@@ -102,7 +102,8 @@ hipError_t device_info(int dev, DevInfo* out);
 // ------------------------------------------------------- kernel timing
 // Kernels a caller may ask to have timed (bytecomp_time_next_launch).
 enum TimedKernel { kTimedNone = 0, kTimedAggSign, kTimedAggSparse, kTimedRandkStream, kTimedTopkCompact,
-                   kTimedSignPass1, kTimedQuantPass1, kTimedAggQuant, kTimedSignOnepass, kTimedQuantOnepass };
+                   kTimedSignPass1, kTimedQuantPass1, kTimedAggQuant, kTimedSignOnepass, kTimedQuantOnepass,
+                   kTimedTopkHist };
 // If a request for kernel `k` is pending, hand over its events and clear it.
 bool take_kernel_timer(int k, hipEvent_t* start, hipEvent_t* stop);
 
@@ -110,6 +111,9 @@ bool take_kernel_timer(int k, hipEvent_t* start, hipEvent_t* stop);
 // a one-pass compress workgroup waits for the rest of its tensor's chunk
 // partials before it computes the missing ones itself.
 uint32_t onepass_wait_ticks();
+// Top-k calls of at most this many chunks take the few-chunk path.
+constexpr uint32_t kTopkFewChunksMax = 2048;  // 8M elements: its counts fit in 31 bits
+uint32_t topk_few_chunks_limit();
 
 // Launch `kernel`, bracketed by the requested events when kernel `k` is to
 // be timed.

@@ -44,9 +44,27 @@ def make_set(ns, rng, dtype=np.float32, sigma=0.01, mode="normal"):
 
 # ------------------------------------------------------------- compression
 
+@pytest.fixture(params=["few", "general"])
+def topk_path(request):
+    """Top-k calls through the few-chunk path (the default at these sizes)
+    and through the general pipeline."""
+    from paper_2205_14465_amd import binding as B
+    B.bytecomp_set_topk_few_chunks(2048 if request.param == "few" else 0)
+    yield request.param
+    B.bytecomp_set_topk_few_chunks(2048)
+
+
+@pytest.fixture
+def general_path():
+    from paper_2205_14465_amd import binding as B
+    B.bytecomp_set_topk_few_chunks(0)
+    yield
+    B.bytecomp_set_topk_few_chunks(2048)
+
+
 @pytest.mark.parametrize("kind", ["topk", "topk_sampled", "randk"])
 @pytest.mark.parametrize("dtype", [np.float32, np.float16])
-def test_sparse_compress_ragged(kind, dtype):
+def test_sparse_compress_ragged(kind, dtype, topk_path):
     rng = np.random.default_rng(100 + len(kind))
     grads, resids = make_set(RAGGED, rng, dtype)
     got, got_e = gpu_compress(kind, 0.01, SEED, grads, resids)
@@ -57,7 +75,7 @@ def test_sparse_compress_ragged(kind, dtype):
 
 @pytest.mark.parametrize("kind", ["topk", "topk_sampled", "randk"])
 @pytest.mark.parametrize("ratio", [0.001, 0.05, 0.3, 1.0])
-def test_sparse_compress_ratios(kind, ratio):
+def test_sparse_compress_ratios(kind, ratio, topk_path):
     rng = np.random.default_rng(7)
     ns = [5, 4097, 70001, 131072]
     grads, resids = make_set(ns, rng)
@@ -68,7 +86,7 @@ def test_sparse_compress_ratios(kind, ratio):
 
 
 @pytest.mark.parametrize("kind", ["topk", "topk_sampled"])
-def test_topk_tie_heavy(kind):
+def test_topk_tie_heavy(kind, topk_path):
     rng = np.random.default_rng(9)
     ns = [100, 4096 * 5 + 3, 200000]
     grads, resids = make_set(ns, rng, mode="ties")
@@ -80,7 +98,7 @@ def test_topk_tie_heavy(kind):
 
 
 @pytest.mark.parametrize("kind", ["topk", "topk_sampled", "randk", "sign"])
-def test_error_feedback_off(kind):
+def test_error_feedback_off(kind, topk_path):
     rng = np.random.default_rng(11)
     ns = [3, 4096, 70000]
     grads, _ = make_set(ns, rng)
@@ -93,7 +111,7 @@ def test_error_feedback_off(kind):
         assert_sparse_equal(got, want, ns)
 
 
-def test_sampled_fallback_path_matches_exact():
+def test_sampled_fallback_path_matches_exact(general_path):
     # ratio 1 (and 0.95) on tensors above the all-candidates size forces the
     # candidate set from the sample to fall short of k: exact fallback
     rng = np.random.default_rng(13)
@@ -106,7 +124,7 @@ def test_sampled_fallback_path_matches_exact():
         assert_resid_equal(got_e, want_e)
 
 
-def test_sampled_fallback_mixed_with_kept_candidates():
+def test_sampled_fallback_mixed_with_kept_candidates(general_path):
     # one call where a tensor falls back (its stream pass had zeroed its
     # candidates in e_new, which the fallback writes back), a large tensor
     # whose sample holds zeros (threshold 0: every element a candidate, no
@@ -121,6 +139,46 @@ def test_sampled_fallback_mixed_with_kept_candidates():
         want, want_e = O.compress_set("topk", ratio, SEED, grads, resids)
         assert_sparse_equal(got, want, ns)
         assert_resid_equal(got_e, want_e)
+
+
+@pytest.mark.parametrize("kind", ["topk", "topk_sampled"])
+def test_topk_two_paths_bitwise(kind):
+    """The same call through the few-chunk path and the general pipeline
+    (different kernels and launch geometries): payloads and residuals
+    identical bit for bit, and equal to the oracle's; includes a call of
+    exactly 2048 chunks (the few-chunk limit), tensors whose k-th key is
+    shared by many entries, and an all-zero tensor."""
+    from paper_2205_14465_amd import binding as B
+    rng = np.random.default_rng(31)
+    cases = [[2048 * 4096], [1, 4095, 4096 * 700 + 5, 3, 4096 * 300]]
+    for ns in cases:
+        grads, resids = make_set(ns, rng)
+        if len(ns) > 1:
+            grads[2][::3] = np.float32(0.02)  # a key shared by a third of the tensor
+            resids[2][::3] = 0.0
+            grads[4][:] = 0.0
+            resids[4][:] = 0.0
+        outs = []
+        for limit in (2048, 0):
+            B.bytecomp_set_topk_few_chunks(limit)
+            try:
+                outs.append(gpu_compress(kind, 0.01, SEED, grads, resids))
+            finally:
+                B.bytecomp_set_topk_few_chunks(2048)
+        (p0, e0), (p1, e1) = outs
+        assert np.array_equal(p0["idx"], p1["idx"]) and np.array_equal(bits(p0["val"]), bits(p1["val"]))
+        for a, b in zip(e0, e1):
+            assert np.array_equal(bits(a), bits(b))
+        want, want_e = O.compress_set("topk", 0.01, SEED, grads, resids)
+        assert_sparse_equal(p0, want, ns)
+        assert_resid_equal(e0, want_e)
+
+
+def test_topk_path_knob_limits():
+    from paper_2205_14465_amd import binding as B
+    with pytest.raises(B.BytecompError, match="BC_E_SIZE"):
+        B.bytecomp_set_topk_few_chunks(2049)
+    B.bytecomp_set_topk_few_chunks(2048)
 
 
 @pytest.mark.parametrize("T, ratio", [(9000, 0.05), (17000, 0.02), (17000, 1.0)])

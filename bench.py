@@ -13,10 +13,12 @@ algorithmic bytes are what the method must move:
              + write the payload (8 B per sparse entry; 4 B per sign or
              quantizer code word + 4 B per tensor scale)
   aggregate: read W payloads + write the dense fp32 output (4 B/elem).
-Timing: K steps between two synchronisations; before each step an untimed
-kernel writes 1 GiB (more than the 256 MB last-level cache), so that no step
-starts with its inputs in the cache, and HIP events on the launch stream
-bracket each step (the flush stays outside).  Per-operation times are the
+Timing: K steps between two synchronisations; before each step, untimed,
+one kernel writes 1 GiB (more than the 256 MB last-level cache) and another
+reads a second 1 GiB buffer (which writes back the dirty lines of the
+first), so that no step starts with its inputs in the cache or pays for
+another kernel's write-backs, and HIP events on the launch stream bracket
+each step (the flush stays outside).  Per-operation times are the
 median, 10th and 90th percentile of --reps flushed repetitions.  The
 roofline entry is the dominant kernel -- the longest of the step's
 timeable kernels, measured -- with its algorithmic bytes per launch over
@@ -312,13 +314,19 @@ def main():
     def aggregate():
         aggregate_call()
 
-    # an untimed write of 1 GiB (a torch fill kernel) evicts the 256 MB
-    # last-level cache before each timed step or operation
+    # before each timed step or operation, untimed: a write of 1 GiB (a
+    # torch fill kernel) evicts the 256 MB last-level cache, then a read of
+    # another 1 GiB (a torch sum) writes back the dirty lines the fill left,
+    # so that the timed kernels start from a cold, clean cache and do not
+    # pay for writing back the flush's data
     flush_buf = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    flush_rd = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    flush_sum = torch.empty((), dtype=torch.float32, device=dev)
 
     def flush():
         if not args.no_flush:
             flush_buf.fill_(1.0)
+            torch.sum(flush_rd, dim=0, out=flush_sum)
 
     def events(k):
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(k)]
@@ -408,7 +416,7 @@ def main():
     ce[1].record(stream)
     torch.cuda.synchronize()
     copy_gbs = 5 * 2 * src.numel() * 4 / (ce[0].elapsed_time(ce[1]) * 1e-3) / 1e9
-    del src, dst, flush_buf
+    del src, dst, flush_buf, flush_rd
 
     value = (comp_b + agg_b) / (step_avg * 1e-3) / 1e9
     comp_med, agg_med = pct(comp_ms, 0.5), pct(agg_ms, 0.5)

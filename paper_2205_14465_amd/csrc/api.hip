@@ -241,8 +241,6 @@ WsPlan plan_workspace(int kind, int T, uint64_t C, uint64_t sum_k, bool agg_tabl
     if (kind == BC_SIGN1) {
         take(p.s_val, t * 4);
         take(p.s_partial, (size_t)C * 8);
-        take(p.s_info, agg_tables ? t * 4 : 0);
-        take(p.s_tab, agg_tables ? t * 2048 * 4 : 0);
         take(p.s_slot, (size_t)C * 8);
     } else if (quant_bits(kind)) {
         take(p.s_val, t * 4);
@@ -635,12 +633,16 @@ int aggregate_impl(int kind, double ratio, const bc_payload* in, const uint64_t*
     uint64_t* wa = (uint64_t*)(table.data() + rp_bytes + (size_t)T * sizeof(ADesc));
     uint64_t* wb = wa + padded_workers(W);
     uint64_t units = 0, off = 0;
+    // sign: a tensor's units start on 128-byte lines of the payloads (worker
+    // 0's address decides; the kernel derives the same shift)
+    const uint64_t sign_base = kind == BC_SIGN1 && in && in[0].bits ? (uint64_t)(uintptr_t)in[0].bits >> 2 : 0;
     for (int i = 0; i < T; ++i) {
         if (n[i] >= kMaxN) return BC_E_SIZE;
         if (n[i] > 0 && !out[i]) return BC_E_NULL;
         if ((uintptr_t)out[i] & 15u) return BC_E_ALIGN;
         const uint64_t cnt = count_of(kind, n[i], ppm);
-        const uint64_t nu = (n[i] + unit - 1) / unit;
+        uint64_t nu = (n[i] + unit - 1) / unit;
+        if (kind == BC_SIGN1 && cnt) nu = (cnt + ((sign_base + off) & 31u) + kSignAggUnit / 32 - 1) / (kSignAggUnit / 32);
         a[i].out = out[i];
         a[i].n = (uint32_t)n[i];
         a[i].k = (uint32_t)cnt;
@@ -655,8 +657,8 @@ int aggregate_impl(int kind, double ratio, const bc_payload* in, const uint64_t*
         for (int i = 0; i < T; ++i) a[i].k = 0;  // per-worker counts come from the parts
         off = 1;                                 // payloads are not addressed by layout
     }
-    Ws w{};  // sign, TernGrad: per-tensor forms and lookup tables live in the workspace
-    if (kind == BC_SIGN1 || kind == BC_TERNGRAD) {
+    Ws w{};  // TernGrad: per-tensor forms and lookup tables live in the workspace
+    if (kind == BC_TERNGRAD) {
         uint64_t C = 0;
         for (int i = 0; i < T; ++i) C += (n[i] + kChunk - 1) / kChunk;
         const WsPlan plan = plan_workspace(kind, T, C, 0);
@@ -705,7 +707,7 @@ int aggregate_impl(int kind, double ratio, const bc_payload* in, const uint64_t*
     } else if (quant_bits(kind)) {
         e = launch_aggregate_quant(quant_bits(kind), ad, T, (uint32_t)units, wdd, W, alpha, w.s_info, w.s_tab, s);
     } else {
-        e = launch_aggregate_sign(ad, T, (uint32_t)units, wdd, W, alpha, w.s_info, w.s_tab, s);
+        e = launch_aggregate_sign(ad, T, (uint32_t)units, wdd, W, alpha, s);
     }
     cache_mark_used(en, s);
     return finish(hip_status(e), s, ws);

@@ -117,8 +117,10 @@ __host__ __device__ __forceinline__ float round_total(int64_t (&acc)[kWideLimbs]
 // of word i / 32); 1: 2-bit TernGrad payloads (element i at bits 2 (i mod
 // 16) of word i / 16).  sc: the tensor's W scales in LDS (read only);
 // scratch: kWideScratchBytes of LDS.  Results go straight to the output.
+// The unit's output elements are ebase .. ebase + kSignAggUnit - 1 of the
+// tensor (ebase may be negative: elements outside [0, n) are skipped).
 template <int kKind>
-__device__ void aggregate_unit_exact_wide(const ADesc& ad, uint32_t u, const uint64_t* __restrict__ wp, int W,
+__device__ void aggregate_unit_exact_wide(const ADesc& ad, int64_t ebase, const uint64_t* __restrict__ wp, int W,
                                           float alpha, const float* sc, unsigned char* scratch) {
     uint16_t* order = reinterpret_cast<uint16_t*>(scratch);          // [1024]
     int* cursor = reinterpret_cast<int*>(scratch + 2048);             // [10]
@@ -154,15 +156,15 @@ __device__ void aggregate_unit_exact_wide(const ADesc& ad, uint32_t u, const uin
     __syncthreads();
 
     constexpr int kE = 2;  // elements per lane and pass
-    const uint32_t ebase = (u - ad.unit0) * kSignAggUnit;
     for (int q0 = 0; q0 < (int)(kSignAggUnit / kBlock); q0 += kE) {
         uint32_t el[kE], wofs[kE], pos[kE];
         bool ok[kE];
 #pragma unroll
         for (int i = 0; i < kE; ++i) {
-            el[i] = ebase + threadIdx.x + (uint32_t)kBlock * (uint32_t)(q0 + i);
-            ok[i] = el[i] < ad.n;
-            const uint32_t e = ok[i] ? el[i] : 0u;  // lanes past the end read the first word
+            const int64_t ge = ebase + (int64_t)threadIdx.x + (int64_t)kBlock * (q0 + i);
+            ok[i] = ge >= 0 && ge < (int64_t)ad.n;
+            el[i] = ok[i] ? (uint32_t)ge : 0u;
+            const uint32_t e = el[i];  // lanes outside the tensor read its first word
             wofs[i] = (uint32_t)ad.off + (kKind == 0 ? e >> 5 : e >> 4);
             pos[i] = kKind == 0 ? (e & 31u) : 2u * (e & 15u);
         }

@@ -5,17 +5,19 @@
 //
 // out_t[i] = alpha * fl32(exact sum over w of d_w,i), d_w,i = -s_w,t when
 // worker w's bit i is set, else +s_w,t: the exact real sum rounded once.
-// A one-wave prep kernel classifies each tensor by the binary exponents of
-// its W scales and builds its lookup tables: int32 tables of eight-worker
-// partial sums (in units of the smallest scale's last place) when the
-// exponents span few enough binades for 32-bit sums, fp64 tables while the
-// span fits fp64 exactly; other scale sets (wider spans, subnormal or
-// non-finite scales) take the multi-word exact path of exact_wide.hpp, so
-// every tensor gets the same definition whatever path computes it.
-// The aggregate kernel takes one 4096-element unit per workgroup, gathers
-// each element's eight-worker bytes with a byte permute and an 8x8 bit
-// transpose, sums the table entries, and stores through LDS for coalesced
-// writes.
+// One kernel: each workgroup takes one unit of 128 payload words (4096
+// elements) of one tensor, classifies the tensor by the binary exponents of
+// its W scales and builds its lookup tables in LDS: int32 tables of
+// eight-worker partial sums (in units of the smallest scale's last place)
+// when the exponents span few enough binades for 32-bit sums, fp64 tables
+// while the span fits fp64 exactly; other scale sets (wider spans,
+// subnormal or non-finite scales) take the multi-word exact path of
+// exact_wide.hpp, so every tensor gets the same definition whatever path
+// computes it.  It gathers each element's eight-worker bytes with a byte
+// permute and an 8x8 bit transpose, sums the table entries, and stores
+// through LDS for coalesced writes.  Units start on 128-byte boundaries of
+// the payloads (a tensor's first unit is shortened to reach one), so that
+// no cache line of a payload is read by two units of a tensor.
 #include "exact_wide.hpp"
 #include "launch.hpp"
 
@@ -63,6 +65,12 @@ __host__ __device__ __forceinline__ void transpose_bytes8(uint32_t (&x)[8]) {
     }
 }
 
+// Workgroup barrier for LDS data: waits for this wave's LDS operations
+// only, leaving its global loads in flight (__syncthreads would wait for
+// those too, and the payload words requested before the tables are built
+// would stop overlapping the build).
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // Integer image of a scale for the 32-bit exact form: the scale as a
 // multiple of 2^(emin - 150), the unit in the last place of the smallest
 // normal scale of the tensor (zero stays zero).
@@ -79,8 +87,9 @@ __device__ __forceinline__ int32_t scale_units(float s, int emin) {
 // of two four-worker entries sub[32 gi + 16 hh + p'].  Workers past W count
 // as zero.  Called by the whole workgroup.
 template <typename Acc>
-__device__ __forceinline__ void build_tables(int g, int W, const float* sc, int emin, Acc* tab, Acc* sub) {
-    __syncthreads();  // earlier lookups are done with the tables
+__device__ __forceinline__ void build_tables(int g, int W, const float* sc, int emin, Acc* tab, Acc* sub,
+                                             int ngroups = 8) {
+    lds_barrier();  // earlier lookups are done with the tables
     {
         const int x = threadIdx.x;  // kBlock == 8 * 32 entries
         const int w0 = 8 * (g + (x >> 5)) + 4 * ((x >> 4) & 1), pat = x & 15;
@@ -96,12 +105,12 @@ __device__ __forceinline__ void build_tables(int g, int W, const float* sc, int 
         }
         sub[x] = acc;
     }
-    __syncthreads();
-    for (int x = threadIdx.x; x < 8 * 256; x += kBlock) {
+    lds_barrier();
+    for (int x = threadIdx.x; x < ngroups * 256; x += kBlock) {
         const int gi = x >> 8, pat = x & 255;
         tab[x] = sub[32 * gi + (pat & 15)] + sub[32 * gi + 16 + (pat >> 4)];
     }
-    __syncthreads();
+    lds_barrier();
 }
 
 // One step: add the table entries of groups g and g+1 for the lane's 16
@@ -165,9 +174,14 @@ __device__ __forceinline__ void store16(const ADesc& ad, uint32_t e0, const floa
 
 }  // namespace
 
-// Sign aggregate.  A unit is 4096 output elements (128 words) of one
-// tensor; lanes 2i and 2i+1 share word i of the unit, each taking 16 of its
-// elements (half h = lane parity covers elements 16h .. 16h+15 of the word).
+// Sign aggregate.  A unit is 128 consecutive payload words (4096 output
+// elements) of one tensor; lanes 2i and 2i+1 share word i of the unit,
+// each taking 16 of its elements (half h = lane parity covers elements
+// 16h .. 16h+15 of the word).  Tensor t's unit j covers its words
+// 128 j - s .. 128 j - s + 127, s = (payload word offset of the tensor) mod
+// 32 (from worker 0's payload address), so that unit boundaries fall on
+// 128-byte lines; words outside the tensor are read as its first word and
+// their sums dropped.
 //
 // Exact forms: workers are taken in groups of eight; the 256 possible sums
 // of a group's eight +-s_w are tabulated, the eight sign bits of an element
@@ -178,28 +192,54 @@ __device__ __forceinline__ void store16(const ADesc& ad, uint32_t e0, const floa
 // tables and sums are int32.  Up to span_limit binades they are fp64 (every
 // partial sum exact).  Other scale sets (non-finite or subnormal scales, or
 // a wider span): the exact sum in 288-bit integer limbs (exact_wide.hpp).
-//
-// Two launches: sign_agg_prep (one wave per tensor) classifies each tensor
-// and, for up to 64 workers, writes its int32 tables to the workspace;
-// aggregate_sign (one workgroup per unit, in unit order, so that the
-// workgroups resident at a time read neighbouring words of every payload)
-// copies its tensor's int32 tables into LDS and sums the unit.  Units of the
-// other forms (rare) take a slower path in the same kernel that is kept lean
-// in registers, so that the common form keeps its occupancy.
-__global__ __launch_bounds__(64) void sign_agg_prep(const ADesc* __restrict__ a, int T,
-                                                    const uint64_t* __restrict__ wp, int W,
-                                                    int span_limit, int int_span_limit,
-                                                    uint32_t* __restrict__ info,
-                                                    int32_t* __restrict__ tabs, int build) {
-    // one wave per tensor
+// Every workgroup classifies its tensor from the W scales and builds the
+// tables it needs in LDS; the int32 form for up to 64 workers (fast_ok) is
+// the common one, the others take a slower path kept lean in registers, so
+// that the common form keeps its occupancy.  Workgroups run in unit order,
+// so that the workgroups resident at a time read neighbouring words of
+// every payload.
+__device__ __forceinline__ uint32_t unit_shift(const uint64_t* __restrict__ wp, const ADesc& ad) {
+    return (uint32_t)(((uint64_t)(uintptr_t)w_a(wp, 0) >> 2) + ad.off) & 31u;
+}
+
+template <int kS>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(5))) void aggregate_sign(const ADesc* __restrict__ a, int T, uint32_t U,
+                                                         const uint64_t* __restrict__ wp, int W,
+                                                         float alpha, int span_limit, int int_span_limit,
+                                                         int fast_ok) {
+    // the tables (int32: up to 8 KiB, fp64: 16 KiB), then, after the last
+    // lookup, the unit's 4096 results (16 KiB) on their way to coalesced
+    // stores
+    __shared__ __attribute__((aligned(16))) float lds[4096];
     __shared__ float sc[1024];
-    __shared__ int32_t sub[8 * 32];
-    const int t = blockIdx.x;
-    if (a[t].nunits == 0) return;
-    const int lane = (int)threadIdx.x;
+    __shared__ double sub[8 * 32];
+    __shared__ int red[12];
+    const uint32_t u = blockIdx.x;
+    const int t = unit_owner(wp, W, u);
+    const ADesc ad = a[t];
+    const uint32_t h = threadIdx.x & 1u;
+    const uint32_t sel = h ? 0x07060302u : 0x05040100u;
+    const int G = (W + 7) / 8;
+    const uint32_t shift = unit_shift(wp, ad);
+    // word of the tensor (wraps past 2^32 below its first word)
+    const uint32_t wi = (u - ad.unit0) * (kSignAggUnit / 32u) + (threadIdx.x >> 1) - shift;
+    const bool has = wi < ad.k;
+    const uint32_t wload = (uint32_t)(ad.off + (has ? wi : 0u)) * 4u;
+    const int64_t ebase = ((int64_t)(u - ad.unit0) * (kSignAggUnit / 32u) - shift) * 32;  // unit element 0
+    // the tensor's scales (the first kBlock requested before the words, so
+    // that waiting for them does not wait for the words)
+    const float sv0 = (int)threadIdx.x < W ? ((cf32p)w_b(wp, W, threadIdx.x))[t] : 0.f;
+    // the words of the first 16 kS workers (16 kS = 16 ceil(G/2) = Wp for
+    // W <= 64, so every slot exists), in flight while the tables are built
+    uint32_t wv[16 * kS];
+    if (fast_ok) {
+#pragma unroll
+        for (int jj = 0; jj < 16 * kS; ++jj) wv[jj] = ld_word(w_a(wp, jj), wload);
+    }
+    // the binades the scales span
     int lo = 1000, hi = -1000, bad = 0;
-    for (int w = lane; w < W; w += 64) {
-        const float sv = ((cf32p)w_b(wp, W, w))[t];
+    for (int w = threadIdx.x; w < W; w += kBlock) {
+        const float sv = w == (int)threadIdx.x ? sv0 : ((cf32p)w_b(wp, W, w))[t];
         sc[w] = sv;
         const int e = (int)((f2u(sv) >> 23) & 255u);
         if (e == 255 || (e == 0 && (f2u(sv) & 0x7FFFFFu))) bad = 1;
@@ -215,86 +255,27 @@ __global__ __launch_bounds__(64) void sign_agg_prep(const ADesc* __restrict__ a,
         hi = hi2 > hi ? hi2 : hi;
         bad |= __shfl_xor(bad, m, 64);
     }
+    if (lane_id() == 0) {
+        red[3 * wave_id()] = lo;
+        red[3 * wave_id() + 1] = hi;
+        red[3 * wave_id() + 2] = bad;
+    }
+    lds_barrier();
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        lo = red[3 * q] < lo ? red[3 * q] : lo;
+        hi = red[3 * q + 1] > hi ? red[3 * q + 1] : hi;
+        bad |= red[3 * q + 2];
+    }
     const int span = hi < lo ? 0 : hi - lo;
     const int form = bad ? 0 : span <= int_span_limit ? 1 : span <= span_limit ? 2 : 0;
     const int emin = hi < lo ? 1 : lo;
-    if (lane == 0) info[t] = (uint32_t)form | ((uint32_t)emin << 8);
-    if (!build || form != 1) return;
-    __builtin_amdgcn_wave_barrier();
-    // sub[32 gi + 16 hh + p]: sum over workers 8 gi + 4 hh + c, c < 4, of
-    // (bit c of p ? -s : +s) in units of 2^(emin-150); zero past W
-    for (int x = lane; x < 8 * 32; x += 64) {
-        const int w0 = 8 * (x >> 5) + 4 * ((x >> 4) & 1), pat = x & 15;
-        int32_t acc = 0;
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const int32_t sv = w0 + c < W ? scale_units(sc[w0 + c], emin) : 0;
-            acc += ((pat >> c) & 1) ? -sv : sv;
-        }
-        sub[x] = acc;
-    }
-    __builtin_amdgcn_wave_barrier();
-    // tab[256 gi + p] = sub[32 gi + (p & 15)] + sub[32 gi + 16 + (p >> 4)],
-    // four entries per lane and store
-    int32_t* tt = tabs + (size_t)t * 2048;
-    for (int x = 4 * lane; x < 8 * 256; x += 256) {
-        const int gi = x >> 8, p0 = x & 255;
-        const int32_t hi16 = sub[32 * gi + 16 + (p0 >> 4)];
-        u32x4 v;
-        v.x = (uint32_t)(sub[32 * gi + ((p0 + 0) & 15)] + hi16);
-        v.y = (uint32_t)(sub[32 * gi + ((p0 + 1) & 15)] + hi16);
-        v.z = (uint32_t)(sub[32 * gi + ((p0 + 2) & 15)] + hi16);
-        v.w = (uint32_t)(sub[32 * gi + ((p0 + 3) & 15)] + hi16);
-        *(BC_GLOBAL u32x4*)(gp(tt) + x) = v;
-    }
-}
-
-template <int kS>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) void aggregate_sign(const ADesc* __restrict__ a, int T, uint32_t U,
-                                                         const uint64_t* __restrict__ wp, int W,
-                                                         float alpha, const uint32_t* __restrict__ info,
-                                                         const int32_t* __restrict__ tabs, int fast_ok) {
-    // the tables (int32: 8 KiB, fp64: 16 KiB), then, after the last lookup,
-    // the unit's 4096 results (16 KiB) on their way to coalesced stores
-    __shared__ __attribute__((aligned(16))) float lds[4096];
-    __shared__ float sc[1024];
-    __shared__ double sub[8 * 32];
-    const uint32_t u = blockIdx.x;
-    const int t = unit_owner(wp, W, u);
-    const uint32_t inf = ((const uint32_t __attribute__((address_space(4)))*)info)[t];
-    const int form = (int)(inf & 255u);
-    const int emin = (int)((inf >> 8) & 255u);
-    const ADesc ad = a[t];
-    const uint32_t h = threadIdx.x & 1u;
-    const uint32_t sel = h ? 0x07060302u : 0x05040100u;
-    const int G = (W + 7) / 8;
-    const uint32_t wi = (u - ad.unit0) * (kSignAggUnit / 32u) + (threadIdx.x >> 1);  // word of the tensor
-    const bool has = wi < ad.k;
-    // lanes past the tensor read its first word (their sums are dropped)
-    const uint32_t wload = (uint32_t)(ad.off + (has ? wi : 0u)) * 4u;
     float res[16];
     if (fast_ok && form == 1) {
         // int32 form, up to 64 workers: the tables of the 2 kS groups the
-        // steps read (groups past G are zero in the workspace), 16 bytes per
-        // lane and load, are requested first, then the words of the 16 kS
-        // workers (16 kS = 16 ceil(G/2) = Wp, so every slot exists)
+        // steps read (groups past G are zero: their workers count as zero)
         int32_t* tab = reinterpret_cast<int32_t*>(lds);
-        const int32_t* tt = tabs + (size_t)t * 2048;
-        u32x4 tv[2];
-#pragma unroll
-        for (int r = 0; r < 2; ++r) {
-            const int x = 4 * threadIdx.x + 1024 * r;
-            tv[r] = x < 512 * kS ? ldg4u(reinterpret_cast<const uint32_t*>(tt) + x) : u32x4{0u, 0u, 0u, 0u};
-        }
-        uint32_t wv[16 * kS];
-#pragma unroll
-        for (int jj = 0; jj < 16 * kS; ++jj) wv[jj] = ld_word(w_a(wp, jj), wload);
-#pragma unroll
-        for (int r = 0; r < 2; ++r) {
-            const int x = 4 * threadIdx.x + 1024 * r;
-            if (x < 512 * kS) *reinterpret_cast<u32x4*>(tab + x) = tv[r];
-        }
-        __syncthreads();
+        build_tables<int32_t>(0, W, sc, emin, tab, reinterpret_cast<int32_t*>(sub), 2 * kS);
         int32_t S[16];
 #pragma unroll
         for (int q = 0; q < 16; ++q) S[q] = 0;
@@ -305,61 +286,54 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
         const double unit = __builtin_ldexp(1.0, emin - 150);
 #pragma unroll
         for (int q = 0; q < 16; ++q) res[q] = alpha * (float)((double)S[q] * unit);
+    } else if (form == 0) {
+        // scales the tables cannot hold exactly: the wide exact path
+        // writes the unit's outputs itself
+        aggregate_unit_exact_wide<0>(ad, ebase, wp, W, alpha, sc, reinterpret_cast<unsigned char*>(lds));
+        return;
     } else {
-        // the other forms (rare: scales spread over many binades, or more
-        // than 64 workers), kept lean in registers so that they do not cost
-        // the int32 form its occupancy
-        for (int w = threadIdx.x; w < W; w += kBlock) sc[w] = ((cf32p)w_b(wp, W, w))[t];
-        __syncthreads();
-        if (form == 0) {
-            // scales the tables cannot hold exactly: the wide exact path
-            // writes the unit's outputs itself
-            aggregate_unit_exact_wide<0>(ad, u, wp, W, alpha, sc, reinterpret_cast<unsigned char*>(lds));
-            return;
-        } else {
-            // fp64 tables (exact for the int32 form's tensors too), the
-            // lane's sixteen elements in two halves of eight
-            double* tab = reinterpret_cast<double*>(lds);
+        // fp64 tables (exact for the int32 form's tensors too), the lane's
+        // sixteen elements in two halves of eight
+        double* tab = reinterpret_cast<double*>(lds);
 #pragma unroll
-            for (int half = 0; half < 2; ++half) {
-                double S[8];
+        for (int half = 0; half < 2; ++half) {
+            double S[8];
 #pragma unroll
-                for (int q = 0; q < 8; ++q) S[q] = 0.0;
-                for (int g = 0; g < G; g += 2) {
-                    if ((g & 7) == 0 && (half == 0 || G > 8)) build_tables<double>(g, W, sc, emin, tab, sub);
-                    uint32_t w16[16];
+            for (int q = 0; q < 8; ++q) S[q] = 0.0;
+            for (int g = 0; g < G; g += 2) {
+                if ((g & 7) == 0 && (half == 0 || G > 8)) build_tables<double>(g, W, sc, emin, tab, sub);
+                uint32_t w16[16];
 #pragma unroll
-                    for (int jj = 0; jj < 16; ++jj) w16[jj] = ld_word(w_a(wp, 8 * g + jj), wload);
-                    lookup_step_half(S, w16, sel, tab, g, half);
-                }
-#pragma unroll
-                for (int q = 0; q < 8; ++q) res[8 * half + q] = alpha * (float)S[q];
+                for (int jj = 0; jj < 16; ++jj) w16[jj] = ld_word(w_a(wp, 8 * g + jj), wload);
+                lookup_step_half(S, w16, sel, tab, g, half);
             }
+#pragma unroll
+            for (int q = 0; q < 8; ++q) res[8 * half + q] = alpha * (float)S[q];
         }
     }
     // Lane l holds unit elements 16 l .. 16 l + 15.  Through LDS (element e
     // of the unit at lds[e]), store k of the workgroup writes elements
     // 1024 k + 4 l' .. +3 for lane l': every store instruction covers 1 KiB
-    // of the output.
+    // of the output.  ebase is a multiple of 32, so whole groups of four
+    // are inside or outside [0, n) at the tensor's start.
     __syncthreads();  // every wave is past its lookups
 #pragma unroll
     for (int c = 0; c < 4; ++c)
         *reinterpret_cast<f32x4*>(lds + 16 * threadIdx.x + 4 * c) =
             f32x4{res[4 * c], res[4 * c + 1], res[4 * c + 2], res[4 * c + 3]};
     __syncthreads();
-    const uint32_t ebase = (u - ad.unit0) * kSignAggUnit;  // first element of the unit
-    const uint32_t nleft = ad.n - ebase;                     // > 0
-    float* out = ad.out + ebase;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const uint32_t e = 1024u * k + 4u * threadIdx.x;  // element of the unit
+        const int64_t g = ebase + e;                       // element of the tensor
+        if (g < 0) continue;
         const f32x4 v = *reinterpret_cast<const f32x4*>(lds + e);
-        if (e + 4u <= nleft) {
-            stg4f(out + e, v);
+        if (g + 4 <= (int64_t)ad.n) {
+            stg4f(ad.out + g, v);
         } else {
 #pragma unroll
             for (int q = 0; q < 4; ++q)
-                if (e + q < nleft) gp(out)[e + q] = v[q];
+                if (g + q < (int64_t)ad.n) gp(ad.out)[g + q] = v[q];
         }
     }
 }
@@ -367,7 +341,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
 
 // -------------------------------------------------------------- launcher
 hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W,
-                                 float alpha, uint32_t* info, int32_t* tabs, hipStream_t s) {
+                                 float alpha, hipStream_t s) {
     if (U == 0) return hipSuccess;
     int lg = 0;
     while ((1 << lg) < W) ++lg;
@@ -376,21 +350,21 @@ hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t U, const uint64
     int lg8 = 0;
     while ((1 << lg8) < 8 * G) ++lg8;
     const int int_span_limit = 7 - lg8;  // 24 + span + ceil(log2 8G) <= 31
-    // the int32 tables (and the fast path) serve up to 64 workers
+    // the int32 form's fast path serves up to 64 workers
     const int small = G <= 8;
-    hipLaunchKernelGGL(sign_agg_prep, dim3(T), dim3(64), 0, s, a, T, w, W, span_limit, int_span_limit, info,
-                       tabs, small);
     const int steps = small ? (G + 1) / 2 : 1;
     const dim3 grid(U), block(kBlock);
-    const uint32_t* ci = info;
-    const int32_t* ct = tabs;
     if (steps <= 1)
-        return launch_timed(kTimedAggSign, aggregate_sign<1>, grid, block, 0, s, a, T, U, w, W, alpha, ci, ct, small);
+        return launch_timed(kTimedAggSign, aggregate_sign<1>, grid, block, 0, s, a, T, U, w, W, alpha, span_limit,
+                            int_span_limit, small);
     if (steps == 2)
-        return launch_timed(kTimedAggSign, aggregate_sign<2>, grid, block, 0, s, a, T, U, w, W, alpha, ci, ct, small);
+        return launch_timed(kTimedAggSign, aggregate_sign<2>, grid, block, 0, s, a, T, U, w, W, alpha, span_limit,
+                            int_span_limit, small);
     if (steps == 3)
-        return launch_timed(kTimedAggSign, aggregate_sign<3>, grid, block, 0, s, a, T, U, w, W, alpha, ci, ct, small);
-    return launch_timed(kTimedAggSign, aggregate_sign<4>, grid, block, 0, s, a, T, U, w, W, alpha, ci, ct, small);
+        return launch_timed(kTimedAggSign, aggregate_sign<3>, grid, block, 0, s, a, T, U, w, W, alpha, span_limit,
+                            int_span_limit, small);
+    return launch_timed(kTimedAggSign, aggregate_sign<4>, grid, block, 0, s, a, T, U, w, W, alpha, span_limit,
+                        int_span_limit, small);
 }
 
 }  // namespace bc

@@ -613,7 +613,7 @@ __global__ __launch_bounds__(kBlock) void aggregate_quant(const ADesc* __restric
         if ((inf & 255u) != 1u) {
             // scales the int32 tables cannot hold exactly (or more than 64
             // workers): the wide exact path writes the unit's outputs itself
-            aggregate_unit_exact_wide<1>(ad, u, wp, W, alpha, unit_sh,
+            aggregate_unit_exact_wide<1>(ad, (int64_t)(u - ad.unit0) * kSignAggUnit, wp, W, alpha, unit_sh,
                                          reinterpret_cast<unsigned char*>(tab_sh));
             return;
         }

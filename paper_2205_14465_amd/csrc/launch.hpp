@@ -21,12 +21,11 @@ struct Ws {
     // BC_SIGN1
     float* s_val;           // [T] published scales
     double* s_partial;      // [C] per-chunk sums of |v|
-    uint32_t* s_info;       // [T] sign / TernGrad aggregate: form (bits 0-7), smallest scale
+    uint32_t* s_info;       // [T] TernGrad aggregate: form (bits 0-7), smallest scale
                             // exponent (8-15)
     uint64_t* s_slot;       // [C] one-pass compress: ~bits of each chunk's partial sum once
                             // published, 0 otherwise (emptied before the kernel runs)
-    int32_t* s_tab;         // aggregate: int32 lookup tables of each tensor, [T * 2048] (sign)
-                            // or [T * 4096] (TernGrad)
+    int32_t* s_tab;         // TernGrad aggregate: int32 lookup tables of each tensor, [T * 4096]
     // BC_TERNGRAD, BC_QSGD4, BC_QSGD8 (and s_val)
     uint32_t* q_max;        // [C] largest |v| bits of each chunk
     uint32_t* q_slot;       // [C] one-pass compress: those bits | 1 << 31 once published, 0 otherwise
@@ -155,7 +154,7 @@ uint32_t sparse_agg_tile(uint64_t n_total, uint64_t k_total);
 hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t units, uint32_t tile, const uint64_t* wp,
                                    int W, float alpha, int cus, const uint64_t* rp, hipStream_t s);
 hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t units, const uint64_t* wp, int W,
-                                 float alpha, uint32_t* info, int32_t* tabs, hipStream_t s);
+                                 float alpha, hipStream_t s);
 // Stochastic b-bit quantizers (bits 2, 4 or 8).
 hipError_t launch_quant_compress(int bits, uint64_t seed, const TDesc* d, int T, uint32_t C, uint32_t max_chunks,
                                  bool any_empty, bool any_f16, bool any_f32, uint32_t* words, float* scale,

@@ -251,8 +251,13 @@ WsPlan plan_workspace(int kind, int T, uint64_t C, uint64_t sum_k, bool agg_tabl
             take(p.s_tab, t * 4096 * 4);
         }
     } else if (kind == BC_TOPK || kind == BC_TOPK_SAMPLED) {
-        // digit 0; the few-chunk path: up to 4 copies of digit 0, then digits 1 and 2
-        take(p.t_hist, C <= kTopkFewChunksMax ? t * (4 * kBins0 + 2 * kBins12) * 4 : t * kBins0 * 4);
+        // the general pipeline: copies of one histogram per tensor; the
+        // few-chunk path: up to 4 copies of digit 0, then digits 1 and 2
+        {
+            size_t per = (size_t)topk_general_copies(T) * kBins0;
+            if (C <= kTopkFewChunksMax && per < 4 * kBins0 + 2 * kBins12) per = 4 * kBins0 + 2 * kBins12;
+            take(p.t_hist, t * per * 4);
+        }
         take(p.t_thr, t * 4);
         take(p.t_prefix, t * 4);
         take(p.t_krem, t * 4);

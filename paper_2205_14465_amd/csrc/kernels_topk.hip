@@ -96,7 +96,8 @@ __global__ __launch_bounds__(kBlock) void topk_hist_pass(const TDesc* __restrict
 constexpr uint32_t kSampleChunksPerBlock = 16;
 
 __global__ __launch_bounds__(kBlock) void topk_sample_hist(const TDesc* __restrict__ d, int T,
-                                                           uint32_t C, uint64_t seed, Ws ws) {
+                                                           uint32_t C, uint64_t seed, int copies, Ws ws) {
+    uint32_t* gh0 = ws.t_hist + (size_t)(blockIdx.x % (uint32_t)copies) * T * kBins0;  // this workgroup's copy
     __shared__ uint32_t lh[kBins0];
     const uint32_t c0 = blockIdx.x * kSampleChunksPerBlock;
     const uint32_t c1 = (c0 + kSampleChunksPerBlock < C) ? c0 + kSampleChunksPerBlock : C;
@@ -125,17 +126,17 @@ __global__ __launch_bounds__(kBlock) void topk_sample_hist(const TDesc* __restri
         const float v = td.resid ? g + gp(td.resid)[i] : g;
         const uint32_t bin = key_of(v) >> 20;
         if (same) atomicAdd(&lh[bin], 1u);
-        else atomicAdd(ws.t_hist + (size_t)t * kBins0 + bin, 1u);
+        else atomicAdd(gh0 + (size_t)t * kBins0 + bin, 1u);
     }
     if (!same) return;
     __syncthreads();
-    flush_hist(lh, ws.t_hist + (size_t)t0 * kBins0, kBins0);
+    flush_hist(lh, gh0 + (size_t)t0 * kBins0, kBins0);
 }
 
 // One workgroup per tensor: read (and clear) the tensor's histogram and
 // pick the bin / digit the mode asks for.
-__global__ __launch_bounds__(kBlock) void topk_find(const TDesc* __restrict__ d, double ratio,
-                                                    int mode, int fb_only, Ws ws) {
+__global__ __launch_bounds__(kBlock) void topk_find(const TDesc* __restrict__ d, int T, double ratio,
+                                                    int mode, int fb_only, int copies, Ws ws) {
     __shared__ uint64_t sh[4];
     __shared__ uint32_t found_bin, found_above, found_total;
     if (fb_only && ws.t_any[0] == 0u) return;  // no tensor fell back
@@ -145,18 +146,32 @@ __global__ __launch_bounds__(kBlock) void topk_find(const TDesc* __restrict__ d,
     const int bins = (mode == kFindDigit1 || mode == kFindDigit2) ? kBins12 : kBins0;
     const int per = bins / kBlock;
     uint32_t* gh = ws.t_hist + (size_t)t * kBins0;
+    const size_t cs = (size_t)T * kBins0;  // between copies
     // thread i owns bins [bins - (i+1)*per, bins - i*per): thread 0 the top
     const int hi = bins - threadIdx.x * per;
     uint32_t h[8];
     uint32_t mine = 0;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-        if (q < per) {
-            h[q] = gh[hi - 1 - q];
-            gh[hi - 1 - q] = 0;
-            mine += h[q];
+    for (int q = 0; q < 8; ++q) h[q] = 0;
+    // every copy's loads issued together (at most 8 copies)
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+        if (r < copies) {
+#pragma unroll
+            for (int q = 0; q < 8; ++q)
+                if (q < per) h[q] += gh[r * cs + hi - 1 - q];
         }
     }
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+        if (r < copies) {
+#pragma unroll
+            for (int q = 0; q < 8; ++q)
+                if (q < per) gh[r * cs + hi - 1 - q] = 0;
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) mine += q < per ? h[q] : 0u;
     uint64_t total64;
     const uint64_t above0 = block_excl_scan_u64(mine, sh, total64);
     const uint32_t total = (uint32_t)total64;
@@ -231,7 +246,7 @@ __global__ __launch_bounds__(kBlock) void topk_find(const TDesc* __restrict__ d,
 // key bits 30..20.
 template <bool kNT>
 __global__ __launch_bounds__(kBlock) void topk_compact(const TDesc* __restrict__ d, int T, uint32_t C,
-                                                       int stream_mode, int fb_only, Ws ws) {
+                                                       int stream_mode, int fb_only, int copies, Ws ws) {
     __shared__ uint32_t lh[kBins0];
     __shared__ uint64_t sh[4];
     if (fb_only && ws.t_any[0] == 0u) return;  // no tensor fell back
@@ -277,7 +292,7 @@ __global__ __launch_bounds__(kBlock) void topk_compact(const TDesc* __restrict__
         }
         if (threadIdx.x == 0) ws.t_ccount[c] = base;
         __syncthreads();
-        flush_hist(lh, ws.t_hist + (size_t)t * kBins0, kBins0);
+        flush_hist(lh, ws.t_hist + ((size_t)(c % (uint32_t)copies) * T + t) * kBins0, kBins0);
         __syncthreads();
     }
 }
@@ -288,25 +303,73 @@ __global__ __launch_bounds__(kBlock) void topk_compact(const TDesc* __restrict__
 // of its LDS histogram once per range; the count and emit passes give each
 // wave one chunk.
 
-// Radix pass over the candidates of a chunk range: histogram of the next
-// digit among candidates whose higher bits match the prefix chosen so far.
-// The LDS histogram is flushed whenever the range moves to another tensor.
+// Radix pass over the candidates of a chunk range (at most 16 chunks):
+// histogram of the next digit among candidates whose higher bits match the
+// prefix chosen so far.  A range inside one tensor (the usual case) walks
+// its candidates as one flattened list, every thread's loads in flight
+// together; a range that crosses tensors walks chunk by chunk and flushes
+// the LDS histogram whenever it moves to another tensor.
+constexpr uint32_t kCandSpanMax = 16;
+
 __global__ __launch_bounds__(kBlock) void topk_cand_hist(const TDesc* __restrict__ d, int T, uint32_t C,
-                                                         uint32_t span, int pass, Ws ws) {
+                                                         uint32_t span, int pass, int copies, Ws ws) {
     __shared__ uint32_t lh[kBins12];
+    __shared__ uint32_t pre[kCandSpanMax + 1];
+    uint32_t* gh0 = ws.t_hist + (size_t)(blockIdx.x % (uint32_t)copies) * T * kBins0;  // this workgroup's copy
     const int shift = pass == 1 ? 10 : 0;
     const int match_shift = pass == 1 ? 20 : 10;
     const uint32_t c0 = blockIdx.x * span;
     const uint32_t c1 = c0 + span < C ? c0 + span : C;
     for (int b = threadIdx.x; b < kBins12; b += kBlock) lh[b] = 0;
-    __syncthreads();
     int t = tensor_of_chunk(d, T, c0);
+    if (c1 <= d[t].chunk0 + d[t].nchunks) {
+        // one tensor: candidate counts of the range, then the flattened walk
+        const uint32_t nc = c1 - c0;
+        const uint32_t mine = threadIdx.x < nc ? ws.t_ccount[c0 + threadIdx.x] : 0u;
+        const uint32_t pfx = ws.t_prefix[t] >> match_shift;
+        if (threadIdx.x < 64) {
+            uint32_t inc = mine;
+#pragma unroll
+            for (int o = 1; o < 64; o <<= 1) {
+                const uint32_t y = __shfl_up(inc, o, 64);
+                if ((int)threadIdx.x >= o) inc += y;
+            }
+            if (threadIdx.x < nc) pre[threadIdx.x + 1] = inc;
+            if (threadIdx.x == 0) pre[0] = 0;
+        }
+        __syncthreads();
+        const uint32_t M = pre[nc];
+        constexpr int kU = 4;  // candidates per thread with loads in flight together
+        for (uint32_t f0 = 0; f0 < M; f0 += kU * kBlock) {
+            uint32_t key[kU];
+#pragma unroll
+            for (int q = 0; q < kU; ++q) {
+                const uint32_t f = f0 + q * kBlock + threadIdx.x;
+                key[q] = 0xFFFFFFFFu;
+                if (f < M) {
+                    uint32_t ci = 0;  // chunk of the range holding flattened entry f
+#pragma unroll
+                    for (uint32_t b = kCandSpanMax / 2; b >= 1; b >>= 1)
+                        if (ci + b <= nc - 1 && pre[ci + b] <= f) ci += b;
+                    key[q] = ws.t_cand[(size_t)(c0 + ci) * kChunk + (f - pre[ci])].y & 0x7FFFFFFFu;
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < kU; ++q)
+                if (key[q] != 0xFFFFFFFFu && (key[q] >> match_shift) == pfx)
+                    atomicAdd(&lh[(key[q] >> shift) & (kBins12 - 1)], 1u);
+        }
+        __syncthreads();
+        flush_hist(lh, gh0 + (size_t)t * kBins0, kBins12);
+        return;
+    }
+    __syncthreads();
     uint32_t prefix = ws.t_prefix[t];
     uint32_t tend = d[t].chunk0 + d[t].nchunks;
     for (uint32_t c = c0; c < c1; ++c) {
         if (c >= tend) {  // next tensor: flush this one's counts
             __syncthreads();
-            flush_hist(lh, ws.t_hist + (size_t)t * kBins0, kBins12);
+            flush_hist(lh, gh0 + (size_t)t * kBins0, kBins12);
             __syncthreads();
             for (int b = threadIdx.x; b < kBins12; b += kBlock) lh[b] = 0;
             __syncthreads();
@@ -323,7 +386,7 @@ __global__ __launch_bounds__(kBlock) void topk_cand_hist(const TDesc* __restrict
         }
     }
     __syncthreads();
-    flush_hist(lh, ws.t_hist + (size_t)t * kBins0, kBins12);
+    flush_hist(lh, gh0 + (size_t)t * kBins0, kBins12);
 }
 
 // Per chunk: candidates above tau and equal to tau, counted with ballots;
@@ -879,39 +942,40 @@ hipError_t launch_topk(int kind, double ratio, uint64_t seed, const TDesc* d, in
                            idx, val, ws);
         return hipGetLastError();
     }
-    const uint64_t hn = (uint64_t)T * kBins0;
+    const int R = topk_general_copies(T);
+    const uint64_t hn = (uint64_t)T * R * kBins0;
     uint32_t zb = (uint32_t)((hn / 4 + 255) / 256);
     if (zb > 4096) zb = 4096;
     hipLaunchKernelGGL(topk_zero_hist, dim3(zb), dim3(256), 0, s, ws.t_hist, hn, ws.t_any);
     if (kind == 0) {  // exact
-        hipLaunchKernelGGL(topk_hist_pass, dim3(C), blk, 0, s, d, T, C, 1, 0, ws, (uint64_t*)nullptr, 1);
-        hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindThrExact, 0, ws);
-        (void)launch_timed(kTimedTopkCompact, topk_compact<false>, dim3(C), blk, 0, s, d, T, C, 0, 0, ws);
-        hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit0, 0, ws);
+        hipLaunchKernelGGL(topk_hist_pass, dim3(C), blk, 0, s, d, T, C, 1, 0, ws, (uint64_t*)nullptr, R);
+        hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, T, ratio, (int)kFindThrExact, 0, R, ws);
+        (void)launch_timed(kTimedTopkCompact, topk_compact<false>, dim3(C), blk, 0, s, d, T, C, 0, 0, R, ws);
+        hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, T, ratio, (int)kFindDigit0, 0, R, ws);
     } else {  // sampled threshold, exact fallback per tensor
         hipLaunchKernelGGL(topk_sample_hist, dim3((C + kSampleChunksPerBlock - 1) / kSampleChunksPerBlock), blk,
-                           0, s, d, T, C, seed, ws);
-        hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindThrSample, 0, ws);
+                           0, s, d, T, C, seed, R, ws);
+        hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, T, ratio, (int)kFindThrSample, 0, R, ws);
         if (C > kNtChunks)
-            (void)launch_timed(kTimedTopkCompact, topk_compact<true>, dim3(C), blk, 0, s, d, T, C, 1, 0, ws);
+            (void)launch_timed(kTimedTopkCompact, topk_compact<true>, dim3(C), blk, 0, s, d, T, C, 1, 0, R, ws);
         else
-            (void)launch_timed(kTimedTopkCompact, topk_compact<false>, dim3(C), blk, 0, s, d, T, C, 1, 0, ws);
-        hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit0, 0, ws);
+            (void)launch_timed(kTimedTopkCompact, topk_compact<false>, dim3(C), blk, 0, s, d, T, C, 1, 0, R, ws);
+        hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, T, ratio, (int)kFindDigit0, 0, R, ws);
         // fallback passes: small grids that walk the chunks, and return at
         // once when no tensor fell back (the usual case)
         const dim3 fb_grid(C < 1024u ? C : 1024u);
-        hipLaunchKernelGGL(topk_hist_pass, fb_grid, blk, 0, s, d, T, C, 0, 1, ws, (uint64_t*)nullptr, 1);
-        hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindThrExact, 1, ws);
-        hipLaunchKernelGGL(topk_compact<false>, fb_grid, blk, 0, s, d, T, C, 0, 1, ws);
-        hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit0, 1, ws);
+        hipLaunchKernelGGL(topk_hist_pass, fb_grid, blk, 0, s, d, T, C, 0, 1, ws, (uint64_t*)nullptr, R);
+        hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, T, ratio, (int)kFindThrExact, 1, R, ws);
+        hipLaunchKernelGGL(topk_compact<false>, fb_grid, blk, 0, s, d, T, C, 0, 1, R, ws);
+        hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, T, ratio, (int)kFindDigit0, 1, R, ws);
     }
     uint32_t span = C / 1024u;
-    span = span < 1u ? 1u : (span > 16u ? 16u : span);
+    span = span < 1u ? 1u : (span > kCandSpanMax ? kCandSpanMax : span);
     const dim3 hist_grid((C + span - 1) / span);
-    hipLaunchKernelGGL(topk_cand_hist, hist_grid, blk, 0, s, d, T, C, span, 1, ws);
-    hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit1, 0, ws);
-    hipLaunchKernelGGL(topk_cand_hist, hist_grid, blk, 0, s, d, T, C, span, 2, ws);
-    hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, ratio, (int)kFindDigit2, 0, ws);
+    hipLaunchKernelGGL(topk_cand_hist, hist_grid, blk, 0, s, d, T, C, span, 1, R, ws);
+    hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, T, ratio, (int)kFindDigit1, 0, R, ws);
+    hipLaunchKernelGGL(topk_cand_hist, hist_grid, blk, 0, s, d, T, C, span, 2, R, ws);
+    hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, T, ratio, (int)kFindDigit2, 0, R, ws);
     if (C >= kCountBatchFrom)
         hipLaunchKernelGGL(topk_cand_count<4>, dim3((C + 15) / 16), blk, 0, s, d, T, C, ws);
     else

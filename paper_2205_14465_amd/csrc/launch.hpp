@@ -110,6 +110,10 @@ bool take_kernel_timer(int k, hipEvent_t* start, hipEvent_t* stop);
 // a one-pass compress workgroup waits for the rest of its tensor's chunk
 // partials before it computes the missing ones itself.
 uint32_t onepass_wait_ticks();
+// Copies of each top-k histogram in the general pipeline for a call of T
+// tensors: workgroups add into copy (their index mod copies), which spreads
+// the atomic additions to the busiest bins; readers add the copies.
+inline int topk_general_copies(int T) { return T <= 256 ? 8 : T <= 1024 ? 2 : 1; }  // at most 8
 // Top-k calls of at most this many chunks take the few-chunk path.
 constexpr uint32_t kTopkFewChunksMax = 2048;  // 8M elements: its counts fit in 31 bits
 uint32_t topk_few_chunks_limit();

@@ -14,6 +14,8 @@
 #include "../../include/bytecomp.h"
 #include "launch.hpp"
 
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 namespace bc {
 
 namespace {
@@ -199,6 +201,9 @@ bool set_kernel_timer(int k, hipEvent_t start, hipEvent_t stop) {
     return pending;
 }
 }  // namespace
+
+CallRange::CallRange(const char* name) { roctxRangePushA(name); }
+CallRange::~CallRange() { roctxRangePop(); }
 
 // ------------------------------------------------- one-pass wait limit
 namespace {
@@ -511,6 +516,7 @@ int bytecomp_workspace_init(void* ws, size_t ws_bytes, void* stream) {
 
 int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t, int T,
                       bc_payload out, void* ws, size_t ws_bytes, void* stream) {
+    const CallRange range("bytecomp_compress");
     CompressPrep p;
     int rc = compress_prepare(kind, ratio, t, T, out, true, p);
     if (rc || T == 0) return rc;
@@ -529,6 +535,7 @@ int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t,
 
 int bytecomp_compress_dgc(int kind, double ratio, uint64_t seed, float momentum, const bc_tensor* t,
                           float* const* velocity, int T, bc_payload out, void* ws, size_t ws_bytes, void* stream) {
+    const CallRange range("bytecomp_compress_dgc");
     uint64_t ppm;
     int rc = check_kind_ratio(kind, ratio, ppm);
     if (rc) return rc;
@@ -725,12 +732,14 @@ extern "C" {
 int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, int W,
                                   const uint64_t* n, int T, float* const* out, float alpha,
                                   void* ws, size_t ws_bytes, void* stream) {
+    const CallRange range("bytecomp_decompress_aggregate");
     return aggregate_impl(kind, ratio, in, nullptr, W, n, T, out, alpha, ws, ws_bytes, stream);
 }
 
 int bytecomp_aggregate_part(int kind, double ratio, const bc_payload* in, const uint64_t* const* part_off,
                             int W, const uint64_t* len, int T, float* const* out, float alpha, void* ws,
                             size_t ws_bytes, void* stream) {
+    const CallRange range("bytecomp_aggregate_part");
     if (quant_bits(kind)) return BC_E_KIND;  // no divisible-scheme support for the quantizers
     if (kind == BC_SIGN1)  // packed sign parts have the word layout of the range lengths
         return aggregate_impl(kind, ratio, in, nullptr, W, len, T, out, alpha, ws, ws_bytes, stream);
@@ -740,6 +749,7 @@ int bytecomp_aggregate_part(int kind, double ratio, const bc_payload* in, const 
 
 int bytecomp_pack_part(int kind, double ratio, const uint64_t* n, int T, bc_payload in, int parts,
                        const uint64_t* bounds, int j, bc_payload out, uint64_t* part_off, void* stream) {
+    const CallRange range("bytecomp_pack_part");
     uint64_t ppm;
     int rc = check_kind_ratio(kind, ratio, ppm);
     if (rc) return rc;
@@ -796,6 +806,7 @@ int bytecomp_pack_part(int kind, double ratio, const uint64_t* n, int T, bc_payl
 
 int bytecomp_residual_update(int kind, double ratio, const bc_tensor* t, int T, bc_payload own,
                              void* stream) {
+    const CallRange range("bytecomp_residual_update");
     uint64_t ppm;
     int rc = check_kind_ratio(kind, ratio, ppm);
     if (rc) return rc;

@@ -22,6 +22,7 @@
 
 #include "../../include/bytecomp.h"
 #include "exact_wide.hpp"
+#include "launch.hpp"
 #include "randk_perm.hpp"
 
 namespace bc {
@@ -330,6 +331,7 @@ using namespace bc;
 
 extern "C" int bytecomp_cpu_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t, int T,
                                      bc_payload out, int threads) {
+    const CallRange range("bytecomp_cpu_compress");
     if (kind < BC_TOPK || kind > BC_QSGD8) return BC_E_KIND;
     if (kind > BC_SIGN1) return BC_E_KIND;  // the quantizers have no CPU form here
     uint64_t ppm = 1;
@@ -375,6 +377,7 @@ extern "C" int bytecomp_cpu_compress(int kind, double ratio, uint64_t seed, cons
 extern "C" int bytecomp_cpu_decompress_aggregate(int kind, double ratio, const bc_payload* in, int W,
                                                  const uint64_t* n, int T, float* const* out, float alpha,
                                                  int threads) {
+    const CallRange range("bytecomp_cpu_decompress_aggregate");
     if (kind < BC_TOPK || kind > BC_SIGN1) return BC_E_KIND;
     uint64_t ppm = 1;
     if (is_sparse_kind(kind)) {

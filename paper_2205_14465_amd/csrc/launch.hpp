@@ -114,6 +114,14 @@ uint32_t onepass_wait_ticks();
 // tensors: workgroups add into copy (their index mod copies), which spreads
 // the atomic additions to the busiest bins; readers add the copies.
 inline int topk_general_copies(int T) { return T <= 256 ? 8 : T <= 1024 ? 2 : 1; }  // at most 8
+// A profiler range (roctx) around one C-ABI call: a push at construction,
+// the pop at scope exit; without a profiler attached both are plain calls.
+struct CallRange {
+    explicit CallRange(const char* name);
+    ~CallRange();
+    CallRange(const CallRange&) = delete;
+    CallRange& operator=(const CallRange&) = delete;
+};
 // Top-k calls of at most this many chunks take the few-chunk path.
 constexpr uint32_t kTopkFewChunksMax = 2048;  // 8M elements: its counts fit in 31 bits
 uint32_t topk_few_chunks_limit();

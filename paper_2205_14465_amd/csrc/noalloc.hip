@@ -76,6 +76,7 @@ using namespace bc;
 
 extern "C" int bytecomp_compress_noalloc(int kind, double ratio, uint64_t seed, const bc_tensor* t, int T,
                                          bc_payload out, void* stream) {
+    const CallRange range("bytecomp_compress_noalloc");
     CompressPrep p;
     int rc = compress_prepare(kind, ratio, t, T, out, false, p);
     if (rc || T == 0) return rc;

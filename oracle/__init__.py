@@ -86,6 +86,10 @@ def lib():
         L.bco_residual_update_quant.argtypes = [_vp, _int, _vp, _u64, _int, _vp, _flt]
         L.bco_dgc_momentum.restype = _int
         L.bco_dgc_momentum.argtypes = [_vp, _int, _vp, _u64, _flt]
+        L.bco_dgc_clip_factor.restype = ctypes.c_float
+        L.bco_dgc_clip_factor.argtypes = [_int, _vp, _vp, _vp, _dbl]
+        L.bco_dgc_momentum_clipped.restype = _int
+        L.bco_dgc_momentum_clipped.argtypes = [_vp, _int, _vp, _u64, _flt, _flt]
         L.bco_aggregate_quant.restype = _int
         L.bco_aggregate_quant.argtypes = [_int, _u64, _int, _vp, _vp, _flt, _vp]
         _lib = L
@@ -361,9 +365,29 @@ def dgc_momentum(g, u, m):
     return u
 
 
-def compress_dgc(kind, g, e, u, m, ratio, seed, tensor_id):
-    """One DGC step of one tensor: (idx, val, e_new, u_new)."""
-    u_new = dgc_momentum(g, u, m)
+def dgc_clip_factor(grads, clip):
+    """Local gradient clipping factor over a tensor list (bco_dgc_clip_factor)."""
+    gs = [_grad(g) for g in grads]
+    T = len(gs)
+    gp_ = (ctypes.c_void_p * max(T, 1))(*[a.ctypes.data if a.size else None for a, _ in gs])
+    dts = np.array([dt for _, dt in gs] or [0], dtype=np.int32)
+    ns = np.array([a.size for a, _ in gs] or [0], dtype=np.uint64)
+    return np.float32(lib().bco_dgc_clip_factor(T, ctypes.cast(gp_, _vp), _p(dts), _p(ns), float(clip)))
+
+
+def dgc_momentum_clipped(g, u, m, c):
+    g, dt = _grad(g)
+    u = np.array(u, dtype=np.float32, copy=True)
+    assert u.size == g.size
+    rc = lib().bco_dgc_momentum_clipped(_p(g), dt, _p(u), g.size, float(m), float(c))
+    assert rc == 0, rc
+    return u
+
+
+def compress_dgc(kind, g, e, u, m, ratio, seed, tensor_id, clip_c=None):
+    """One DGC step of one tensor: (idx, val, e_new, u_new); clip_c: the
+    local clipping factor of the step (None: no clipping)."""
+    u_new = dgc_momentum(g, u, m) if clip_c is None else dgc_momentum_clipped(g, u, m, clip_c)
     if kind == "topk":
         idx, val, e_new = compress_topk(u_new, e, ratio)
     elif kind == "topk_sampled":
@@ -376,15 +400,17 @@ def compress_dgc(kind, g, e, u, m, ratio, seed, tensor_id):
     return idx, val, e_new, u_new
 
 
-def compress_dgc_set(kind, ratio, seed, m, grads, resids, vels):
-    """DGC step of a tensor list: (payload dict, new residuals, new velocities)."""
+def compress_dgc_set(kind, ratio, seed, m, grads, resids, vels, clip=None):
+    """DGC step of a tensor list: (payload dict, new residuals, new velocities);
+    clip: the local clipping threshold on the list's L2 norm (None: none)."""
     ns = [g.size for g in grads]
     off = sparse_offsets(ns, ratio)
     idx = np.empty(int(off[-1]), np.uint32)
     val = np.empty(int(off[-1]), np.float32)
     new_e, new_u = [], []
+    c = None if clip is None else dgc_clip_factor(grads, clip)
     for t in range(len(grads)):
-        i, v, e_out, u_out = compress_dgc(kind, grads[t], resids[t], vels[t], m, ratio, seed, t)
+        i, v, e_out, u_out = compress_dgc(kind, grads[t], resids[t], vels[t], m, ratio, seed, t, c)
         idx[off[t]:off[t + 1]] = i
         val[off[t]:off[t + 1]] = v
         new_e.append(e_out)

@@ -806,3 +806,33 @@ int bco_dgc_momentum(const void* g, int dtype, float* u_inout, uint64_t n, float
     }
     return 0;
 }
+
+/* DGC local gradient clipping (DGC's clipping before the gradient joins
+ * the accumulation; a reading of it, the paper naming DGC only as its
+ * sparsifier, Sec. 5.1): over the T gradients of one step, the L2 norm
+ * ||g|| = sqrt(sum of widen(g_i)^2), each square exact in fp64, summed in
+ * fp64 in tensor order then index order, the square root in fp64;
+ * factor c = fl32(clip / ||g||) when ||g|| > clip, else exactly 1. */
+float bco_dgc_clip_factor(int T, const void* const* g, const int* dtype, const uint64_t* n, double clip)
+{
+    double s = 0.0;
+    for (int t = 0; t < T; ++t)
+        for (uint64_t i = 0; i < n[t]; ++i) {
+            const double x = (double)grad_at(g[t], dtype[t], i);
+            s += x * x;
+        }
+    const double norm = sqrt(s);
+    return norm > clip ? (float)(clip / norm) : 1.0f;
+}
+
+/* The velocity step with the clipped gradient: u = fl32(fl32(m u) +
+ * fl32(c g)) (c = 1 leaves g unchanged, so the step is bco_dgc_momentum's). */
+int bco_dgc_momentum_clipped(const void* g, int dtype, float* u_inout, uint64_t n, float m, float c)
+{
+    for (uint64_t i = 0; i < n; ++i) {
+        float mu = m * u_inout[i];
+        float gc = c * grad_at(g, dtype, i);
+        u_inout[i] = mu + gc;
+    }
+    return 0;
+}

@@ -203,6 +203,27 @@ int bytecomp_compress_dgc(int kind, double ratio, uint64_t seed, float momentum,
                           float* const* velocity, int T, bc_payload out, void* ws, size_t ws_bytes,
                           void* stream);
 
+/* One DGC step with DGC's local gradient clipping before the momentum
+ * correction (a reading of DGC's clipping; the paper names DGC as its
+ * sparsifier, Sec. 5.1).  Over the call's T gradients (the worker's whole
+ * gradient when the call holds it):
+ *   norm = sqrt(sum over every element of widen(g)^2), each square exact
+ *          in fp64, the sum in fp64 (per-chunk sums added in a fixed
+ *          order, which differs from index order by the rounding of fp64
+ *          additions only), the root in fp64
+ *   c    = fl32(clip_norm / norm) if norm > clip_norm, else 1
+ *   u   <- fl32(fl32(momentum * u) + fl32(c * g)), then the steps of
+ *          bytecomp_compress_dgc (c = 1 gives its result bit for bit).
+ *   clip_norm    the threshold (DGC scales its global threshold by
+ *                N^(-1/2) for N workers; the caller passes the scaled
+ *                value); >= 0, +inf never clips; BC_E_RATIO for a negative
+ *                or NaN value
+ *   clip_factor  device pointer to one float that receives c, or NULL
+ * Every other argument and status is bytecomp_compress_dgc's. */
+int bytecomp_compress_dgc_clip(int kind, double ratio, uint64_t seed, float momentum, double clip_norm,
+                               const bc_tensor* t, float* const* velocity, int T, bc_payload out,
+                               float* clip_factor, void* ws, size_t ws_bytes, void* stream);
+
 /* Decompress W workers' payloads and aggregate them (paper Sec. 3.1,
  * Reason #2: each node decompresses the gathered payloads and aggregates
  * them; the aggregation is not an Allreduce because compressed
@@ -246,13 +267,13 @@ int bytecomp_decompress_aggregate(int kind, double ratio, const bc_payload* in, 
  *     range, in payload order, with the index rebased to the range
  *     (index - start); out.idx / out.val need room for every entry of `in`
  *     in the worst case;
- *   BC_SIGN1: tensor by tensor, the words that cover the range (the layout
- *     bytecomp_layout gives for the range lengths) and every tensor's scale.
+ *   BC_SIGN1 and the quantizers: tensor by tensor, the words that cover
+ *     the range (the layout bytecomp_layout gives for the range lengths)
+ *     and every tensor's scale.
  *   part_off  device, T + 1 uint64: the packed offset of each tensor's part
  *             (entries, or words), then the total.
  * BC_E_ALIGN if an inner bound is not a multiple of 32, BC_E_SIZE if bounds
- * do not run from 0 to n_t in order.  Stream-ordered like the rest.
- * BC_E_KIND for the quantizers (not supported in the divisible scheme). */
+ * do not run from 0 to n_t in order.  Stream-ordered like the rest. */
 int bytecomp_pack_part(int kind, double ratio, const uint64_t* n, int T, bc_payload in, int parts,
                        const uint64_t* bounds, int j, bc_payload out, uint64_t* part_off, void* stream);
 
@@ -263,14 +284,14 @@ int bytecomp_pack_part(int kind, double ratio, const uint64_t* n, int T, bc_payl
  * W = 1 per part).
  *   in        host, W payloads packed by bytecomp_pack_part for the same part
  *   part_off  host array of W device pointers: each sender's part_off
- *             (sparse kinds; ignored for BC_SIGN1)
+ *             (sparse kinds; ignored for the word kinds)
  *   len       host, T range lengths of the part
  *   out       host, T device pointers to dense fp32 slices (16-byte aligned)
- * out_t[i] = alpha * the worker-ordered fp32 sum (sparse) or the exact sum
- * rounded once (sign) of the senders' values at i, exactly as
- * bytecomp_decompress_aggregate defines them, so the parts of all nodes
- * assemble the whole aggregate bit for bit.  BC_E_KIND for the quantizers.
- * Sparse kinds take at most 64
+ * out_t[i] = alpha * the senders' values at i summed exactly as
+ * bytecomp_decompress_aggregate defines it for the kind (worker-ordered fp32
+ * for the sparse kinds and 4-/8-bit codes, the exact sum rounded once for
+ * sign and TernGrad), so the parts of all nodes assemble the whole
+ * aggregate bit for bit.  Sparse kinds take at most 64
  * senders (BC_E_COUNT otherwise).  ws: as bytecomp_decompress_aggregate for
  * the range lengths. */
 int bytecomp_aggregate_part(int kind, double ratio, const bc_payload* in, const uint64_t* const* part_off,

@@ -517,25 +517,27 @@ def pack_part_sparse(idx, val, lo, hi):
     return (idx[keep] - np.uint32(lo)).astype(np.uint32), val[keep].copy()
 
 
-def pack_part_sign(words, lo, hi):
-    """Words of one tensor's sign payload that cover [lo, hi), lo a multiple
-    of 32: words lo/32 .. ceil(hi/32) - 1 (the scale travels unchanged)."""
+def pack_part_sign(words, lo, hi, bits=1):
+    """Words of one tensor's sign (bits = 1) or b-bit quantizer payload that
+    cover [lo, hi), lo a multiple of 32: words lo*b/32 .. ceil(hi*b/32) - 1
+    (the scale travels unchanged)."""
     assert lo % 32 == 0
-    return np.asarray(words, np.uint32)[lo // 32:(hi + 31) // 32].copy()
+    return np.asarray(words, np.uint32)[lo * bits // 32:(hi * bits + 31) // 32].copy()
 
 
 def pack_part_set(kind, ns, payload, bounds, j):
     """Part j of every tensor of one payload dict (as compress_set returns),
     laid out tensor by tensor: {'idx', 'val', 'off'} for sparse kinds (off
     = prefix sums of the per-tensor counts), {'bits', 'scale', 'off'} for
-    sign (off = prefix sums of the range word counts)."""
+    sign and the quantizers (off = prefix sums of the range word counts)."""
+    words_kind = kind == "sign" or kind in QUANT_BITS
     out_a, out_b, off = [], [], [0]
     for t, n in enumerate(ns):
         b = check_part_bounds(n, bounds[t])
         lo, hi = b[j], b[j + 1]
         seg = slice(payload["off"][t], payload["off"][t + 1])
-        if kind == "sign":
-            w = pack_part_sign(payload["bits"][seg], lo, hi)
+        if words_kind:
+            w = pack_part_sign(payload["bits"][seg], lo, hi, QUANT_BITS.get(kind, 1))
             out_a.append(w)
         else:
             i, v = pack_part_sparse(payload["idx"][seg], payload["val"][seg], lo, hi)
@@ -543,7 +545,7 @@ def pack_part_set(kind, ns, payload, bounds, j):
             out_b.append(v)
         off.append(off[-1] + out_a[-1].size)
     res = {"off": np.array(off, dtype=np.int64)}
-    if kind == "sign":
+    if words_kind:
         res["bits"] = np.concatenate(out_a) if out_a else np.zeros(0, np.uint32)
         res["scale"] = np.asarray(payload["scale"], np.float32).copy()
     else:

@@ -81,6 +81,9 @@ def lib():
         L.bytecomp_compress_dgc.restype = i32
         L.bytecomp_compress_dgc.argtypes = [i32, dbl, u64, ctypes.c_float, ctypes.POINTER(bc_tensor), vp, i32,
                                             bc_payload, vp, sz, vp]
+        L.bytecomp_compress_dgc_clip.restype = i32
+        L.bytecomp_compress_dgc_clip.argtypes = [i32, dbl, u64, ctypes.c_float, dbl, ctypes.POINTER(bc_tensor), vp,
+                                                 i32, bc_payload, vp, vp, sz, vp]
         L.bytecomp_decompress_aggregate.restype = i32
         L.bytecomp_decompress_aggregate.argtypes = [i32, dbl, ctypes.POINTER(bc_payload), i32, vp, i32,
                                                     vp, flt, vp, sz, vp]
@@ -391,12 +394,18 @@ class CompressCall:
 
 class DgcCall:
     """bytecomp_compress_dgc with its argument arrays marshalled once:
-    velocities is a list of fp32 device tensors, one per gradient."""
+    velocities is a list of fp32 device tensors, one per gradient.  With
+    clip_norm (not None) the call is bytecomp_compress_dgc_clip, and
+    clip_factor (a one-element fp32 device tensor, or None) receives the
+    clipping factor."""
 
-    def __init__(self, kind, ratio, momentum, grads, resids, velocities, out, ws, stream=None, tensor_ids=None):
+    def __init__(self, kind, ratio, momentum, grads, resids, velocities, out, ws, stream=None, tensor_ids=None,
+                 clip_norm=None, clip_factor=None):
         self.kind = _kind(kind)
         self.ratio = float(ratio)
         self.momentum = float(momentum)
+        self.clip_norm = None if clip_norm is None else float(clip_norm)
+        self.clip_factor = _ptr(clip_factor)
         self.T = len(grads)
         self.arr = _tensor_list(grads, resids, tensor_ids)
         self.vel = (ctypes.c_void_p * max(self.T, 1))(*[v.data_ptr() if v.numel() else None for v in velocities])
@@ -404,18 +413,33 @@ class DgcCall:
         self.ws = _ptr(ws)
         self.ws_bytes = ws.numel() * ws.element_size()
         self.stream = _stream_handle(stream)
-        self._keep = (grads, resids, velocities, out, ws)
+        self._keep = (grads, resids, velocities, out, ws, clip_factor)
 
     def __call__(self, seed):
-        _check("bytecomp_compress_dgc",
-               lib().bytecomp_compress_dgc(self.kind, self.ratio, int(seed) & (2**64 - 1), self.momentum, self.arr,
-                                           self.vel, self.T, self.out, self.ws, self.ws_bytes, self.stream))
+        if self.clip_norm is None:
+            _check("bytecomp_compress_dgc",
+                   lib().bytecomp_compress_dgc(self.kind, self.ratio, int(seed) & (2**64 - 1), self.momentum,
+                                               self.arr, self.vel, self.T, self.out, self.ws, self.ws_bytes,
+                                               self.stream))
+        else:
+            _check("bytecomp_compress_dgc_clip",
+                   lib().bytecomp_compress_dgc_clip(self.kind, self.ratio, int(seed) & (2**64 - 1), self.momentum,
+                                                    self.clip_norm, self.arr, self.vel, self.T, self.out,
+                                                    self.clip_factor, self.ws, self.ws_bytes, self.stream))
 
 
 def bytecomp_compress_dgc(kind, ratio, seed, momentum, grads, resids, velocities, out, ws, stream=None,
                           tensor_ids=None):
     """One DGC step: velocities (fp32 device tensors) and resids are updated in place."""
     DgcCall(kind, ratio, momentum, grads, resids, velocities, out, ws, stream, tensor_ids)(seed)
+
+
+def bytecomp_compress_dgc_clip(kind, ratio, seed, momentum, clip_norm, grads, resids, velocities, out, ws,
+                               clip_factor=None, stream=None, tensor_ids=None):
+    """One DGC step with local gradient clipping at clip_norm; clip_factor:
+    a one-element fp32 device tensor that receives the factor, or None."""
+    DgcCall(kind, ratio, momentum, grads, resids, velocities, out, ws, stream, tensor_ids, clip_norm=clip_norm,
+            clip_factor=clip_factor)(seed)
 
 
 class AggregateCall:

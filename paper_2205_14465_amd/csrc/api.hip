@@ -285,6 +285,10 @@ WsPlan plan_workspace(int kind, int T, uint64_t C, uint64_t sum_k, bool agg_tabl
         take(p.r_coff, ((size_t)NB + 1 + nscan) * 8);
         take(p.r_hist, nblk * NB * 4);
     }
+    if (kind == BC_TOPK || kind == BC_TOPK_SAMPLED || kind == BC_RANDK) {
+        take(p.d_part, (size_t)C * 8);
+        take(p.d_factor, 4);
+    }
     p.total = at;
     return p;
 }
@@ -319,6 +323,8 @@ Ws carve_workspace(void* base, const WsPlan& p) {
     w.r_ccount = (uint32_t*)at(p.r_ccount);
     w.r_coff = (uint64_t*)at(p.r_coff);
     w.r_hist = (uint32_t*)at(p.r_hist);
+    w.d_part = (double*)at(p.d_part);
+    w.d_factor = (float*)at(p.d_factor);
     return w;
 }
 
@@ -459,6 +465,13 @@ hipError_t compress_launch(int kind, double ratio, uint64_t seed, const Compress
 
 }  // namespace bc
 
+namespace {
+// One DGC step (bytecomp_compress_dgc, bytecomp_compress_dgc_clip).
+int compress_dgc_impl(int kind, double ratio, uint64_t seed, float momentum, bool clipping, double clip_norm,
+                      float* clip_factor, const bc_tensor* t, float* const* velocity, int T, bc_payload out,
+                      void* ws, size_t ws_bytes, void* stream);
+}  // namespace
+
 extern "C" {
 
 const char* bytecomp_strerror(int status) {
@@ -536,6 +549,26 @@ int bytecomp_compress(int kind, double ratio, uint64_t seed, const bc_tensor* t,
 int bytecomp_compress_dgc(int kind, double ratio, uint64_t seed, float momentum, const bc_tensor* t,
                           float* const* velocity, int T, bc_payload out, void* ws, size_t ws_bytes, void* stream) {
     const CallRange range("bytecomp_compress_dgc");
+    return compress_dgc_impl(kind, ratio, seed, momentum, false, 0.0, nullptr, t, velocity, T, out, ws, ws_bytes,
+                             stream);
+}
+
+int bytecomp_compress_dgc_clip(int kind, double ratio, uint64_t seed, float momentum, double clip_norm,
+                               const bc_tensor* t, float* const* velocity, int T, bc_payload out,
+                               float* clip_factor, void* ws, size_t ws_bytes, void* stream) {
+    const CallRange range("bytecomp_compress_dgc_clip");
+    if (!(clip_norm >= 0.0)) return BC_E_RATIO;  // NaN or negative
+    return compress_dgc_impl(kind, ratio, seed, momentum, true, clip_norm, clip_factor, t, velocity, T, out, ws,
+                             ws_bytes, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+int compress_dgc_impl(int kind, double ratio, uint64_t seed, float momentum, bool clipping, double clip_norm,
+                      float* clip_factor, const bc_tensor* t, float* const* velocity, int T, bc_payload out,
+                      void* ws, size_t ws_bytes, void* stream) {
     uint64_t ppm;
     int rc = check_kind_ratio(kind, ratio, ppm);
     if (rc) return rc;
@@ -566,7 +599,9 @@ int bytecomp_compress_dgc(int kind, double ratio, uint64_t seed, float momentum,
     }
     if (rc) return rc;
     if (kind == BC_RANDK && (sum_k >= (1ull << 32) || !randk_buckets(C, nullptr, nullptr))) return BC_E_SIZE;
-    if (ws_bytes < plan_workspace(kind, T, C, sum_k).total) return BC_E_WORKSPACE;
+    const WsPlan plan = plan_workspace(kind, T, C, sum_k);
+    if (ws_bytes < plan.total) return BC_E_WORKSPACE;
+    const Ws w = carve_workspace(ws, plan);
     hipStream_t s = (hipStream_t)stream;
     hipError_t e;
     {
@@ -575,7 +610,8 @@ int bytecomp_compress_dgc(int kind, double ratio, uint64_t seed, float momentum,
         e = cache_get(dm.data(), dm.size() * sizeof(TDesc), (size_t)C * 4,
                       [&](void* dst) { fill_chunk_map(dm, (uint32_t*)dst); }, s, &en);
         if (e != hipSuccess) return BC_E_HIP;
-        e = launch_dgc_momentum((const TDesc*)en->dev, T, C, momentum, s);
+        e = launch_dgc_momentum((const TDesc*)en->dev, T, C, momentum, clipping, clip_norm, w.d_part, w.d_factor,
+                                clip_factor, s);
         cache_mark_used(en, s);
         if (e != hipSuccess) return BC_E_HIP;
     }
@@ -591,7 +627,7 @@ int bytecomp_compress_dgc(int kind, double ratio, uint64_t seed, float momentum,
     return finish(hip_status(e), s, ws);
 }
 
-}  // extern "C"
+}  // namespace
 
 namespace {
 
@@ -740,8 +776,7 @@ int bytecomp_aggregate_part(int kind, double ratio, const bc_payload* in, const 
                             int W, const uint64_t* len, int T, float* const* out, float alpha, void* ws,
                             size_t ws_bytes, void* stream) {
     const CallRange range("bytecomp_aggregate_part");
-    if (quant_bits(kind)) return BC_E_KIND;  // no divisible-scheme support for the quantizers
-    if (kind == BC_SIGN1)  // packed sign parts have the word layout of the range lengths
+    if (!is_sparse(kind))  // packed sign and quantizer parts have the word layout of the range lengths
         return aggregate_impl(kind, ratio, in, nullptr, W, len, T, out, alpha, ws, ws_bytes, stream);
     if (!part_off) return BC_E_NULL;
     return aggregate_impl(kind, ratio, in, part_off, W, len, T, out, alpha, ws, ws_bytes, stream);
@@ -753,7 +788,6 @@ int bytecomp_pack_part(int kind, double ratio, const uint64_t* n, int T, bc_payl
     uint64_t ppm;
     int rc = check_kind_ratio(kind, ratio, ppm);
     if (rc) return rc;
-    if (quant_bits(kind)) return BC_E_KIND;  // no divisible-scheme support for the quantizers
     if (T < 0 || T > kMaxT || parts < 1 || j < 0 || j >= parts) return BC_E_COUNT;
     if (T == 0) return BC_OK;
     if (!n || !bounds || !part_off) return BC_E_NULL;
@@ -775,7 +809,7 @@ int bytecomp_pack_part(int kind, double ratio, const uint64_t* n, int T, bc_payl
             if (b[q] > b[q + 1]) return BC_E_SIZE;
             if (q > 0 && (b[q] & 31u)) return BC_E_ALIGN;
         }
-        const uint64_t cnt = sparse ? k_of(n[t], ppm) : words_of(n[t]);
+        const uint64_t cnt = count_of(kind, n[t], ppm);
         PDesc& d = p[(size_t)t];
         d.in_off = in_off;
         d.out_off = out_words;
@@ -784,7 +818,7 @@ int bytecomp_pack_part(int kind, double ratio, const uint64_t* n, int T, bc_payl
         d.hi = (uint32_t)b[j + 1];
         d.pad = 0;
         in_off += cnt;
-        out_words += (b[j + 1] - b[j] + 31) / 32;
+        out_words += count_of(kind, b[j + 1] - b[j], ppm);  // words of the range (word kinds)
         max_entries += cnt < b[j + 1] - b[j] ? cnt : b[j + 1] - b[j];
     }
     hipStream_t s = (hipStream_t)stream;
@@ -798,8 +832,8 @@ int bytecomp_pack_part(int kind, double ratio, const uint64_t* n, int T, bc_payl
     if (e != hipSuccess) return BC_E_HIP;
     const bc_payload_dev din{in.idx, in.val, in.bits, in.scale};
     const bc_payload_dev dout{out.idx, out.val, out.bits, out.scale};
-    e = launch_pack_part(sparse ? 0 : 3, (const PDesc*)en->dev, T, din, dout, part_off, out_words, max_entries,
-                         di.cus, s);
+    e = launch_pack_part(sparse ? 0 : quant_bits(kind) ? quant_bits(kind) : 1, (const PDesc*)en->dev, T, din, dout,
+                         part_off, out_words, max_entries, di.cus, s);
     cache_mark_used(en, s);
     return hip_status(e);
 }

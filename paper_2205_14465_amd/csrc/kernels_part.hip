@@ -6,9 +6,10 @@
 // Parts are element ranges [lo, hi) of every tensor.  Packing part j of a
 // sparse payload keeps, tensor by tensor, the entries whose index lies in
 // the range, in payload order, with the index rebased to the range; a sign
-// payload keeps the words that cover the range (lo is a multiple of 32) and
-// every tensor's scale.  part_off receives the packed offsets of the
-// tensors: entries (sparse) or words (sign), T + 1 values.
+// or quantizer payload (b bits per element) keeps the words that cover the
+// range (lo is a multiple of 32, so the range starts on a word) and every
+// tensor's scale.  part_off receives the packed offsets of the tensors:
+// entries (sparse) or words (sign, quantizers), T + 1 values.
 #include "launch.hpp"
 
 namespace bc {
@@ -130,18 +131,19 @@ __global__ __launch_bounds__(kBlock) void part_copy_sparse(const PDesc* __restri
     }
 }
 
-// Sign: copy tensor t's range words and its scale; part_off gets the
-// (host-computed) word offsets.
-__global__ __launch_bounds__(kBlock) void part_copy_sign(const PDesc* __restrict__ p, int T,
-                                                         const uint32_t* __restrict__ in_bits,
-                                                         const float* __restrict__ in_scale,
-                                                         uint32_t* __restrict__ out_bits,
-                                                         float* __restrict__ out_scale,
-                                                         uint64_t* __restrict__ part_off, uint64_t total) {
+// Sign and quantizers (`bits` per element): copy tensor t's range words
+// and its scale; part_off gets the (host-computed) word offsets.
+__global__ __launch_bounds__(kBlock) void part_copy_words(const PDesc* __restrict__ p, int T, uint32_t bits,
+                                                          const uint32_t* __restrict__ in_bits,
+                                                          const float* __restrict__ in_scale,
+                                                          uint32_t* __restrict__ out_bits,
+                                                          float* __restrict__ out_scale,
+                                                          uint64_t* __restrict__ part_off, uint64_t total) {
     for (int t = blockIdx.x; t < T; t += gridDim.x) {
         const PDesc pd = p[t];
-        const uint32_t nw = (pd.hi - pd.lo + 31u) / 32u;
-        const uint64_t src = pd.in_off + pd.lo / 32u;
+        // bits per element: the range starts on a word (lo is a multiple of 32)
+        const uint32_t nw = (uint32_t)(((uint64_t)(pd.hi - pd.lo) * bits + 31u) / 32u);
+        const uint64_t src = pd.in_off + (uint64_t)pd.lo / 32u * bits;
         for (uint32_t i = threadIdx.x; i < nw; i += kBlock) out_bits[pd.out_off + i] = gp(in_bits)[src + i];
         if (threadIdx.x == 0) {
             out_scale[t] = gp(in_scale)[t];
@@ -151,13 +153,13 @@ __global__ __launch_bounds__(kBlock) void part_copy_sign(const PDesc* __restrict
     }
 }
 
-hipError_t launch_pack_part(int kind, const PDesc* p, int T, bc_payload_dev in, bc_payload_dev out,
-                            uint64_t* part_off, uint64_t sign_words, uint64_t max_entries, int cus, hipStream_t s) {
+hipError_t launch_pack_part(int word_bits, const PDesc* p, int T, bc_payload_dev in, bc_payload_dev out,
+                            uint64_t* part_off, uint64_t words, uint64_t max_entries, int cus, hipStream_t s) {
     if (T <= 0) return hipSuccess;
     const uint32_t grid = (uint32_t)(T < 4 * cus ? T : 4 * cus);
-    if (kind == 3) {
-        hipLaunchKernelGGL(part_copy_sign, dim3(grid), dim3(kBlock), 0, s, p, T, in.bits, in.scale, out.bits,
-                           out.scale, part_off, sign_words);
+    if (word_bits) {
+        hipLaunchKernelGGL(part_copy_words, dim3(grid), dim3(kBlock), 0, s, p, T, (uint32_t)word_bits, in.bits,
+                           in.scale, out.bits, out.scale, part_off, words);
         return hipGetLastError();
     }
     hipLaunchKernelGGL(part_count, dim3((T + 3) / 4), dim3(kBlock), 0, s, p, T, in.idx, part_off);

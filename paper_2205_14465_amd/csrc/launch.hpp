@@ -51,6 +51,9 @@ struct Ws {
                             // [ceil(NB / 4096)] scan block sums
     uint32_t* r_hist;       // [generating workgroups * NB] per-workgroup bucket
                             // counts, then positions within each bucket
+    // DGC local clipping (sparse kinds)
+    double* d_part;         // [C] sums of squares per chunk
+    float* d_factor;        // [1] the clipping factor
 };
 
 // Byte offsets of every region for a call shape; `total` is the workspace
@@ -59,6 +62,7 @@ struct WsPlan {
     size_t flags, s_val, s_partial, s_info, s_tab, s_slot, q_max, q_slot;
     size_t t_hist, t_thr, t_prefix, t_krem, t_fb, t_any, t_cand, t_ccount, t_gt, t_eq, t_off, t_eqb;
     size_t r_keys, r_tmp, r_ccount, r_coff, r_hist;
+    size_t d_part, d_factor;
     size_t total;
 };
 
@@ -175,7 +179,11 @@ hipError_t launch_quant_residual_update(int bits, const TDesc* d, int T, uint32_
                                         const float* scale, hipStream_t s);
 // DGC momentum correction (d: tensors with resid = the velocity u) and
 // momentum-factor masking (idx: the call's payload indices, total entries).
-hipError_t launch_dgc_momentum(const TDesc* d, int T, uint32_t C, float m, hipStream_t s);
+// clipping: first the local clipping factor of the list (chunk sums of
+// squares in part[C], the factor in factor[0] and, when given,
+// factor_out[0]), then the step with the clipped gradient.
+hipError_t launch_dgc_momentum(const TDesc* d, int T, uint32_t C, float m, bool clipping, double clip,
+                               double* part, float* factor, float* factor_out, hipStream_t s);
 hipError_t launch_dgc_mask(const TDesc* d, int T, const uint32_t* idx, uint64_t total, hipStream_t s);
 // units of kSignAggUnit elements; W <= 1024
 // info, tabs: the TernGrad exact form's per-tensor forms and tables (2-bit only).
@@ -195,12 +203,12 @@ constexpr uint32_t kRandkMaxBuckets = 16384;
 constexpr uint32_t kRandkMaxShift = 8;
 bool randk_buckets(uint32_t C, uint32_t* S, uint32_t* NB);
 
-// Divisible scheme: pack part j of one payload (kind 3 = sign).
-// max_entries: an upper bound on the part's entries (sparse), which sizes
-// the copy grid.
-hipError_t launch_pack_part(int kind, const PDesc* p, int T, bc_payload_dev in, bc_payload_dev out,
-                            uint64_t* part_off, uint64_t sign_words, uint64_t max_entries, int cus,
-                            hipStream_t s);
+// Divisible scheme: pack part j of one payload.  word_bits: 0 for the
+// sparse kinds, else the code bits per element (1 sign, 2, 4, 8); words:
+// the packed words (word kinds); max_entries: an upper bound on the part's
+// entries (sparse), which sizes the copy grid.
+hipError_t launch_pack_part(int word_bits, const PDesc* p, int T, bc_payload_dev in, bc_payload_dev out,
+                            uint64_t* part_off, uint64_t words, uint64_t max_entries, int cus, hipStream_t s);
 
 // Work-unit sizes of the aggregate kernels (elements per unit).
 

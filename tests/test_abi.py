@@ -52,18 +52,20 @@ def test_layout_matches_k_rule_and_word_count():
         assert np.array_equal(np.array(B.bytecomp_layout(kind, 0.0, ns)), O.quant_word_offsets(ns, bits))
 
 
-def test_quantizers_refuse_the_divisible_scheme():
+def test_quantizers_take_the_divisible_scheme():
+    """The quantizer kinds pass the divisible scheme's kind check: their
+    calls reach the argument checks that follow it (each call below fails
+    one of those before any device work)."""
     L = B.lib()
     n = (ctypes.c_uint64 * 1)(64)
-    bounds = (ctypes.c_uint64 * 2)(0, 64)
+    bounds = (ctypes.c_uint64 * 3)(0, 40, 64)  # inner bound not a multiple of 32
     pay = B.bc_payload(bits=0x3000, scale=0x4000)
     po = ctypes.c_void_p(0x5000)
     for kind in (4, 5, 6):
-        assert L.bytecomp_pack_part(kind, 0.0, n, 1, pay, 1, bounds, 0, pay, po, None) == -2
+        assert L.bytecomp_pack_part(kind, 0.0, n, 1, pay, 2, bounds, 0, pay, po, None) == -9  # BC_E_ALIGN
         ins = (B.bc_payload * 1)(pay)
         outs = (ctypes.c_void_p * 1)(0x6000)
-        offs = (ctypes.c_void_p * 1)(0x7000)
-        assert L.bytecomp_aggregate_part(kind, 0.0, ins, offs, 1, n, 1, outs, 1.0, po, 1 << 20, None) == -2
+        assert L.bytecomp_aggregate_part(kind, 0.0, ins, None, 0, n, 1, outs, 1.0, po, 1 << 20, None) == -6
 
 
 def _status(fn):

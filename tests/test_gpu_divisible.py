@@ -23,8 +23,11 @@ def _bounds(rng, ns, P, empty_part=False):
     return out
 
 
+WORD_KINDS = ("sign", "terngrad", "qsgd4", "qsgd8")
+
+
 def _dev_payload(kind, p):
-    if kind == "sign":
+    if kind in WORD_KINDS:
         return {"bits": torch_dev(p["bits"].view(np.int32)), "scale": torch_dev(p["scale"])}
     return {"idx": torch_dev(p["idx"].view(np.int32)), "val": torch_dev(p["val"])}
 
@@ -47,7 +50,7 @@ def _gpu_pack(kind, ratio, ns, dev_pay, bounds, j):
     return out, po
 
 
-@pytest.mark.parametrize("kind", ["topk", "randk", "sign"])
+@pytest.mark.parametrize("kind", ["topk", "randk", "sign", "terngrad", "qsgd4", "qsgd8"])
 @pytest.mark.parametrize("empty_part", [False, True])
 def test_pack_part_matches_oracle(kind, empty_part):
     rng = np.random.default_rng(41 + empty_part)
@@ -63,7 +66,7 @@ def test_pack_part_matches_oracle(kind, empty_part):
         got_off = po.cpu().numpy()
         assert np.array_equal(got_off, want["off"]), (j, got_off, want["off"])
         tot = int(want["off"][-1])
-        if kind == "sign":
+        if kind in WORD_KINDS:
             assert np.array_equal(out["bits"].cpu().numpy().view(np.uint32)[:tot], want["bits"]), j
             assert np.array_equal(bits(out["scale"].cpu().numpy()[:len(ns)]), bits(want["scale"]))
         else:
@@ -71,7 +74,7 @@ def test_pack_part_matches_oracle(kind, empty_part):
             assert np.array_equal(bits(out["val"].cpu().numpy()[:tot]), bits(want["val"])), j
 
 
-@pytest.mark.parametrize("kind", ["topk", "randk", "sign"])
+@pytest.mark.parametrize("kind", ["topk", "randk", "sign", "terngrad", "qsgd4", "qsgd8"])
 @pytest.mark.parametrize("W", [1, 3, 16, 64])
 def test_aggregate_part_matches_oracle(kind, W):
     import torch
@@ -92,7 +95,7 @@ def test_aggregate_part_matches_oracle(kind, W):
             offs.append(po)
         outs = [torch.full((max(n, 1),), float("nan"), dtype=torch.float32, device="cuda")[:n] for n in lens]
         ws = B.alloc_workspace(kind, ratio, lens, W)
-        B.bytecomp_aggregate_part(kind, ratio, dev_parts, None if kind == "sign" else offs, lens, outs,
+        B.bytecomp_aggregate_part(kind, ratio, dev_parts, None if kind in WORD_KINDS else offs, lens, outs,
                                   1.0 / W, ws)
         torch.cuda.synchronize()
         want_parts = O.aggregate_part_set(kind, lens, [O.pack_part_set(kind, ns, p, bounds, j) for p in pays],
@@ -140,7 +143,7 @@ def test_aggregate_part_large_tiles():
     assert B.bytecomp_device_status(ws) == 0
 
 
-@pytest.mark.parametrize("kind", ["topk", "sign"])
+@pytest.mark.parametrize("kind", ["topk", "sign", "terngrad", "qsgd8"])
 def test_divisible_step_end_to_end(kind):
     """Node j's step for every j: aggregate the parts, compress the aggregate
     again (no error feedback), and decompress every node's result into the
@@ -163,7 +166,7 @@ def test_divisible_step_end_to_end(kind):
             offs.append(po)
         slices = [torch.empty(max(n, 1), dtype=torch.float32, device="cuda")[:n] for n in lens]
         ws = B.alloc_workspace(kind, ratio, lens, W)
-        B.bytecomp_aggregate_part(kind, ratio, dev_parts, None if kind == "sign" else offs, lens, slices,
+        B.bytecomp_aggregate_part(kind, ratio, dev_parts, None if kind in WORD_KINDS else offs, lens, slices,
                                   1.0 / W, ws)
         # second compression of node j's aggregate (no residual)
         sec = B.alloc_payload(kind, ratio, lens)
@@ -182,9 +185,6 @@ def test_divisible_step_end_to_end(kind):
             want_finals[t][bounds[t][j]:bounds[t][j + 1]] = dec[t]
     for t in range(len(ns)):
         got = finals[t].cpu().numpy()
-        if kind == "sign":
-            # scales of the second compression: fp64 sums in the same order
-            # on both sides, bit-exact in practice
-            assert np.array_equal(bits(got), bits(want_finals[t])), t
-        else:
-            assert np.array_equal(bits(got), bits(want_finals[t])), t
+        # sign: the second compression's scales are fp64 sums in different
+        # orders on the two sides, equal in practice at these sizes
+        assert np.array_equal(bits(got), bits(want_finals[t])), t

@@ -622,7 +622,10 @@ def _div_bounds(rng, ns, P):
     return out
 
 
-@pytest.mark.parametrize("kind", ["topk", "randk", "sign"])
+WORD_KINDS = ("sign", "terngrad", "qsgd4", "qsgd8")
+
+
+@pytest.mark.parametrize("kind", ["topk", "randk", "sign", "terngrad", "qsgd4", "qsgd8"])
 def test_parts_reassemble_the_payload(kind):
     """Packing every part and undoing the rebase gives back the payload
     exactly: the parts are disjoint and cover every entry (word)."""
@@ -635,7 +638,7 @@ def test_parts_reassemble_the_payload(kind):
     parts = [O.pack_part_set(kind, ns, pay, bounds, j) for j in range(P)]
     for t, n in enumerate(ns):
         seg = slice(pay["off"][t], pay["off"][t + 1])
-        if kind == "sign":
+        if kind in WORD_KINDS:
             got = np.concatenate([p["bits"][p["off"][t]:p["off"][t + 1]] for p in parts])
             assert np.array_equal(got, pay["bits"][seg])
             for p in parts:
@@ -648,7 +651,7 @@ def test_parts_reassemble_the_payload(kind):
             assert np.array_equal(vv.view(np.uint32), pay["val"][seg].view(np.uint32))
 
 
-@pytest.mark.parametrize("kind", ["topk", "sign"])
+@pytest.mark.parametrize("kind", ["topk", "sign", "terngrad", "qsgd4", "qsgd8"])
 def test_part_aggregates_assemble_the_whole_aggregate(kind):
     """The node-j aggregates of all parts, placed at their ranges, equal the
     indivisible aggregate bit for bit (each element's sum sees the same

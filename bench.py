@@ -291,8 +291,8 @@ def main():
     alpha = 1.0 / wl.W
     stream = torch.cuda.current_stream()
 
-    if args.scheme == "divisible" and (kind not in ("topk", "topk_sampled", "randk", "sign") or wl.momentum):
-        sys.exit(f"bench.py: the divisible scheme is not built for the {kind} kind")
+    if args.scheme == "divisible" and wl.momentum:
+        sys.exit("bench.py: the divisible-scheme step is not timed for the DGC workload")
     if args.scheme == "divisible":
         return divisible(args, wl, off, payloads, ws, dev, stream)
 
@@ -495,7 +495,7 @@ def divisible(args, wl, off, payloads, ws_unused, dev, stream):
 
     packs = [B.PackPartCall(kind, wl.ratio, wl.sizes, payloads[w], bounds, 0, parts[w], offs[w], stream=stream)
              for w in range(W)]
-    agg_call = B.AggregatePartCall(kind, wl.ratio, parts, None if kind == "sign" else offs, lens, slices, alpha,
+    agg_call = B.AggregatePartCall(kind, wl.ratio, parts, None if kind in WORD_KINDS else offs, lens, slices, alpha,
                                    ws_agg, stream=stream)
     cmp_call = B.CompressCall(kind, wl.ratio, slices, None, sec, ws_cmp, stream=stream)
 
@@ -517,7 +517,7 @@ def divisible(args, wl, off, payloads, ws_unused, dev, stream):
         step()
     torch.cuda.synchronize()
     # bytes actually present in each part
-    if kind == "sign":
+    if kind in WORD_KINDS:
         part_units = [int(o[-1].item()) for o in offs]
         part_bytes = [4 * u + 4 * wl.T for u in part_units]
         sec_off = B.bytecomp_layout(kind, wl.ratio, lens)
@@ -538,7 +538,8 @@ def divisible(args, wl, off, payloads, ws_unused, dev, stream):
         step()
     torch.cuda.synchronize()
     step_s = (time.perf_counter() - t0) / reps
-    dom_kernel = "aggregate_sign" if kind == "sign" else "aggregate_sparse"
+    dom_kernel = {"sign": "aggregate_sign", "terngrad": "aggregate_quant", "qsgd4": "aggregate_quant",
+                  "qsgd8": "aggregate_quant"}.get(kind, "aggregate_sparse")
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(reps)]
     for r in range(reps):
         for e in ev[r][4:]:

@@ -28,15 +28,22 @@
  *   - Pointers named "device" must be device memory of the current HIP
  *     device; pointers named "host" are read before the call returns.
  *   - All work is enqueued on `stream` (a hipStream_t, NULL = the null
- *     stream); calls return without synchronising.  Argument errors are
+ *     stream); calls return without synchronising, with one exception: a
+ *     descriptor-cache miss that evicts a table used from several streams
+ *     waits for the device (below).  Argument errors are
  *     detected on the host before anything is enqueued: the call then
  *     returns a negative status and has no side effect.  Faults inside
  *     kernels surface at the caller's next synchronisation; with the
  *     environment variable BYTECOMP_DEBUG=1 every call synchronises and
  *     checks.
  *   - The caller owns every buffer.  The library keeps a small cache of
- *     per-device descriptor tables (allocated on first use of a tensor
- *     list and reused while the list is unchanged) and nothing else.
+ *     per-device descriptor tables, reused while a call's tensor list is
+ *     unchanged, and nothing else.  A call whose table is not cached
+ *     allocates device and pinned host memory for it (hipMalloc,
+ *     hipHostMalloc) when the evicted slot is too small, and first waits
+ *     for the queued kernels that still read the evicted table: its event
+ *     when one stream used it, the whole device when several did.  Callers
+ *     that must not allocate use bytecomp_compress_noalloc.
  *   - Sizes: 0 <= n < 2^32 elements per tensor (indices are uint32);
  *     0 < ratio <= 1 with at least one part per million; T >= 0 (T = 0 is
  *     a no-op); W >= 1.

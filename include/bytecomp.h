@@ -337,6 +337,39 @@ int bytecomp_cpu_compress(int kind, double ratio, uint64_t seed, const bc_tensor
 int bytecomp_cpu_decompress_aggregate(int kind, double ratio, const bc_payload* in, int W,
                                       const uint64_t* n, int T, float* const* out, float alpha, int threads);
 
+/* Decision algorithm, host only (paper Sec. 4.3, the timeline model of
+ * "Expressing interactions"; Sec. 4.4.3, Algorithm 2 and the Theorem's
+ * enumeration of prod(|G_i| + 1) offloading count vectors).  A job of T
+ * tensors in backward order (index 0 computed first); option o of tensor
+ * i (0 none, 1 GPU indivisible, 2 GPU divisible, 3 CPU indivisible, 4 CPU
+ * divisible) has the steps stage_off[i*5+o] .. stage_off[i*5+o+1]-1 after
+ * its computation (compute_us[i] on the GPU): stage_res[q] the resource
+ * (0 GPU, 1 CPU, 2 PCIe link, 3 network) and stage_us[q] the duration.
+ * Every resource serves one step at a time in order of release (earliest
+ * release, then lower tensor index, then earlier step); a tensor's
+ * computation is released when the previous tensor's computation ends,
+ * each later step when its previous step ends.  All arrays host.
+ * bytecomp_plan_simulate: *iteration_us = the end of the last step under
+ * the options option[T].  BC_E_KIND for an option outside 0..4. */
+int bytecomp_plan_simulate(int T, const double* compute_us, const uint64_t* stage_off, const int32_t* stage_res,
+                           const double* stage_us, const int32_t* option, double* iteration_us);
+
+/* Algorithm 2's exhaustive search: groups g = 0..G-1 of tensors compressed
+ * on the GPU (option 1 or 2), members group_member[group_off[g] ..
+ * group_off[g+1]-1] in offloading order; count vector U offloads the first
+ * U[g] members of each group (option + 2).  Every vector is evaluated (on
+ * up to `threads` host threads, <= 0: all), in the order where the last
+ * group's count varies fastest; the result is the first vector that
+ * improves on the best so far by more than eps_us (vector 0 first).
+ * best_counts[G] receives it, *best_us its iteration time, *evals the
+ * number of vectors.  BC_E_SIZE, with nothing evaluated, when the number
+ * of vectors exceeds max_evals; BC_E_KIND when a member is not on a GPU
+ * option. */
+int bytecomp_plan_enumerate(int T, const double* compute_us, const uint64_t* stage_off, const int32_t* stage_res,
+                            const double* stage_us, const int32_t* option, int G, const uint64_t* group_off,
+                            const int32_t* group_member, uint64_t max_evals, double eps_us, int threads,
+                            int32_t* best_counts, double* best_us, uint64_t* evals);
+
 /* Read (synchronously, on `stream`) and clear the kernel failure flags a
  * workspace holds; *flags receives them (0 = none).  No kernel of this
  * version sets one (bit 0 is reserved). */

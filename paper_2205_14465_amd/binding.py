@@ -72,6 +72,10 @@ def lib():
                                         sz, vp]
         L.bytecomp_compress_noalloc.restype = i32
         L.bytecomp_compress_noalloc.argtypes = [i32, dbl, u64, ctypes.POINTER(bc_tensor), i32, bc_payload, vp]
+        L.bytecomp_plan_simulate.restype = i32
+        L.bytecomp_plan_simulate.argtypes = [i32, vp, vp, vp, vp, vp, vp]
+        L.bytecomp_plan_enumerate.restype = i32
+        L.bytecomp_plan_enumerate.argtypes = [i32, vp, vp, vp, vp, vp, i32, vp, vp, u64, dbl, i32, vp, vp, vp]
         L.bytecomp_cpu_compress.restype = i32
         L.bytecomp_cpu_compress.argtypes = [i32, dbl, u64, ctypes.POINTER(bc_tensor), i32, bc_payload, i32]
         L.bytecomp_cpu_decompress_aggregate.restype = i32

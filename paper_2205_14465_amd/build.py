@@ -15,7 +15,7 @@ LIB = os.path.join(HERE, "libbytecomp.so")
 BUILD = os.path.join(HERE, "_build")
 SOURCES = ["api.hip", "kernels_sign.hip", "kernels_topk.hip", "kernels_randk.hip", "kernels_agg_sparse.hip",
            "kernels_agg_sign.hip", "kernels_resid.hip", "kernels_part.hip", "kernels_quant.hip",
-           "kernels_dgc.hip", "noalloc.hip", "cpu_ops.hip"]
+           "kernels_dgc.hip", "noalloc.hip", "cpu_ops.hip", "plan_sim.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-ffp-contract=off",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

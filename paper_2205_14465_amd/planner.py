@@ -268,21 +268,28 @@ def _remove(tensors, S, model, live: set) -> None:
             live.discard(i)
 
 
-def plan_gpu(tensors: Sequence[Tensor], model: CostModel, options=GPU_OPTIONS) -> List[Option]:
-    """Algorithm 1: GPU compression decisions."""
+def plan_gpu(tensors: Sequence[Tensor], model: CostModel, options=GPU_OPTIONS, native: bool = True) -> List[Option]:
+    """Algorithm 1: GPU compression decisions.  The candidates' iteration
+    times come from the library's timeline model (native=False: from
+    simulate(), for tests); the bubbles of Property #1 from simulate()."""
     T = len(tensors)
     S: List[Option] = [None] * T
     order = sorted(range(T), key=lambda i: (-tensors[i].n, i))  # Property #2
     live = set(range(T))
+    table = NativeTable(tensors, model) if native else None
+
+    def F(strategy):
+        return table.simulate(strategy) if table is not None else simulate(tensors, strategy, model).iteration_us
+
     _remove(tensors, S, model, live)
     for i in order:
         if i not in live:
             continue
-        best, best_f = S, simulate(tensors, S, model).iteration_us
+        best, best_f = S, F(S)
         for c in options:  # Property #3
             cand = list(S)
             cand[i] = c
-            f = simulate(tensors, cand, model).iteration_us
+            f = F(cand)
             if f < best_f - EPS_US:
                 best, best_f = cand, f
         S = best
@@ -290,13 +297,86 @@ def plan_gpu(tensors: Sequence[Tensor], model: CostModel, options=GPU_OPTIONS) -
     return S
 
 
-def plan_cpu(tensors: Sequence[Tensor], S: Sequence[Option], model: CostModel, max_evals: int = 20000,
-             lemma_order: str = "earliest") -> Tuple[List[Option], int]:
+# ------------------------------------------- the native timeline model
+# The library's host functions bytecomp_plan_simulate / _enumerate evaluate
+# the same timeline model as simulate() (a CPU test compares them bit for
+# bit); Algorithm 2 uses them so that its exhaustive search reaches far
+# more count vectors.
+
+OPTION_CODE = {None: 0, ("gpu", "indivisible"): 1, ("gpu", "divisible"): 2, ("cpu", "indivisible"): 3,
+               ("cpu", "divisible"): 4}
+RESOURCE_CODE = {"gpu": 0, "cpu": 1, "pcie": 2, "net": 3}
+
+
+class NativeTable:
+    """Every tensor's steps under every option, flattened for the library."""
+
+    def __init__(self, tensors: Sequence[Tensor], model: CostModel):
+        import ctypes
+
+        import numpy as np
+        self.T = len(tensors)
+        opts = [None, ("gpu", "indivisible"), ("gpu", "divisible"), ("cpu", "indivisible"), ("cpu", "divisible")]
+        cpu_ok = getattr(model, "has_cpu", True)
+        off, res, dur = [0], [], []
+        for t in tensors:
+            for o in opts:
+                st = model.stages(t, o) if (o is None or o[0] == "gpu" or cpu_ok) else []
+                for r, us, _ in st:
+                    res.append(RESOURCE_CODE[r])
+                    dur.append(float(us))
+                off.append(len(res))
+        self.compute = np.array([float(t.compute_us) for t in tensors] or [0.0], dtype=np.float64)
+        self.off = np.array(off, dtype=np.uint64)
+        self.res = np.array(res or [0], dtype=np.int32)
+        self.dur = np.array(dur or [0.0], dtype=np.float64)
+        self._c = ctypes
+
+    def _args(self):
+        return (self.T, self.compute.ctypes.data, self.off.ctypes.data, self.res.ctypes.data, self.dur.ctypes.data)
+
+    def simulate(self, S: Sequence[Option]) -> float:
+        import numpy as np
+
+        from . import binding as B
+        opt = np.array([OPTION_CODE[o] for o in S] or [0], dtype=np.int32)
+        out = self._c.c_double(0.0)
+        B._check("bytecomp_plan_simulate",
+                 B.lib().bytecomp_plan_simulate(*self._args(), opt.ctypes.data, self._c.byref(out)))
+        return out.value
+
+    def enumerate(self, S: Sequence[Option], groups: Sequence[Sequence[int]], max_evals: int,
+                  threads: int = 0) -> Optional[Tuple[List[int], float, int]]:
+        """Algorithm 2's exhaustive search; None when the count vectors
+        exceed max_evals."""
+        import numpy as np
+
+        from . import binding as B
+        opt = np.array([OPTION_CODE[o] for o in S] or [0], dtype=np.int32)
+        goff = np.array([0] + list(itertools.accumulate(len(g) for g in groups)), dtype=np.uint64)
+        mem = np.array([i for g in groups for i in g] or [0], dtype=np.int32)
+        G = len(groups)
+        best = np.zeros(max(G, 1), dtype=np.int32)
+        bus = self._c.c_double(0.0)
+        ev = self._c.c_uint64(0)
+        rc = B.lib().bytecomp_plan_enumerate(*self._args(), opt.ctypes.data, G, goff.ctypes.data, mem.ctypes.data,
+                                             int(max_evals), float(EPS_US), int(threads), best.ctypes.data,
+                                             self._c.byref(bus), self._c.byref(ev))
+        if rc == -5:  # BC_E_SIZE: beyond max_evals
+            return None
+        B._check("bytecomp_plan_enumerate", rc)
+        return [int(x) for x in best[:G]], bus.value, int(ev.value)
+
+
+def plan_cpu(tensors: Sequence[Tensor], S: Sequence[Option], model: CostModel, max_evals: int = 2_000_000,
+             lemma_order: str = "earliest", native: bool = True) -> Tuple[List[Option], int]:
     """Algorithm 2: CPU offloading of the GPU-compressed tensors.  Returns
-    the strategy and the number of strategies evaluated.  When the product
-    of the group sizes (plus one) exceeds max_evals, the counts are chosen
-    one group at a time instead (each group's count minimising F with the
-    others fixed, repeated until no count changes)."""
+    the strategy and the number of strategies evaluated.  Every count
+    vector is evaluated when their number (the Theorem's bound) is at most
+    max_evals (by the library's native timeline model; native=False: by
+    simulate(), for tests); beyond that the counts are chosen one group at
+    a time instead (each group's count minimising F with the others fixed,
+    repeated until no count changes)."""
     if not getattr(model, "has_cpu", True):
         return list(S), 0
     groups: Dict[tuple, List[int]] = {}
@@ -319,16 +399,26 @@ def plan_cpu(tensors: Sequence[Tensor], S: Sequence[Option], model: CostModel, m
     sizes = [len(groups[k]) + 1 for k in keys]
     total = math.prod(sizes) if sizes else 1
     evals = 0
+    table = NativeTable(tensors, model) if native else None
+
+    def F(strategy):
+        return table.simulate(strategy) if table is not None else simulate(tensors, strategy, model).iteration_us
+
     if total <= max_evals:
+        if table is not None:
+            res = table.enumerate(S, [groups[k] for k in keys], max_evals)
+            if res is not None:
+                U, _, evals = res
+                return apply(U), evals
         best, best_f = list(S), math.inf
         for U in itertools.product(*[range(m) for m in sizes]):
-            f = simulate(tensors, apply(U), model).iteration_us
+            f = F(apply(U))
             evals += 1
             if f < best_f - EPS_US:
                 best, best_f = apply(U), f
         return best, evals
     U = [0] * len(keys)
-    best_f = simulate(tensors, apply(U), model).iteration_us
+    best_f = F(apply(U))
     changed = True
     while changed:
         changed = False
@@ -338,7 +428,7 @@ def plan_cpu(tensors: Sequence[Tensor], S: Sequence[Option], model: CostModel, m
                     continue
                 V = list(U)
                 V[g] = u
-                f = simulate(tensors, apply(V), model).iteration_us
+                f = F(apply(V))
                 evals += 1
                 if f < best_f - EPS_US:
                     U, best_f, changed = V, f, True
@@ -399,6 +489,8 @@ def main(argv=None) -> None:
     tensors = synthetic_job(a.model, a.us_per_mparam)
     model = CostModel(a.kind, a.ratio, load_profile_rows(a.table),
                       Cluster(N=a.N, link_gbs=a.link_gbs, alpha_us=a.alpha_us), pcie=load_profile_pcie(a.table))
+    from . import binding as B
+    B.lib()  # load the library (and torch) before the clock starts
     t0 = time.perf_counter()
     S1 = plan_gpu(tensors, model)
     t1 = time.perf_counter()

@@ -186,3 +186,37 @@ def test_cli_runs_on_the_committed_table(capsys):
     res = json.loads(capsys.readouterr().out)
     assert res["algorithm1_2_us"] <= res["algorithm1_us"] <= res["fp32_us"]
     assert res["tensors"] == 161
+
+
+def test_native_timeline_model_matches_simulate():
+    """The library's timeline model (bytecomp_plan_simulate) and simulate()
+    give the same iteration time, bit for bit, on random instances and
+    strategies of every option."""
+    opts = [None, ("gpu", "indivisible"), ("gpu", "divisible"), ("cpu", "indivisible"), ("cpu", "divisible")]
+    for k, (tensors, m) in enumerate(_instances(40, seed=300)):
+        table = P.NativeTable(tensors, m)
+        rnd = random.Random(k)
+        for _ in range(10):
+            S = [rnd.choice(opts) for _ in tensors]
+            assert table.simulate(S) == P.simulate(tensors, S, m).iteration_us, (k, S)
+
+
+def test_native_enumeration_matches_the_python_loop():
+    for tensors, m in _instances(25, seed=400):
+        S1 = P.plan_gpu(tensors, m)
+        assert S1 == P.plan_gpu(tensors, m, native=False)
+        a, ea = P.plan_cpu(tensors, S1, m, native=True)
+        b, eb = P.plan_cpu(tensors, S1, m, native=False)
+        assert a == b and ea == eb
+
+
+def test_native_enumeration_limits():
+    tensors = [P.Tensor(1 << 20, 100.0) for _ in range(12)]
+    m = P.CostModel("topk", 0.01, P.load_profile_rows(TABLE), P.Cluster(N=16, link_gbs=3.0),
+                    pcie=P.load_profile_pcie(TABLE))
+    S = [("gpu", "indivisible")] * 12
+    table = P.NativeTable(tensors, m)
+    assert table.enumerate(S, [list(range(12))], max_evals=12) is None   # 13 vectors
+    U, f, ev = table.enumerate(S, [list(range(12))], max_evals=13)
+    assert ev == 13 and 0 <= U[0] <= 12
+    assert f == table.simulate([("cpu", "indivisible") if i < U[0] else S[i] for i in range(12)])

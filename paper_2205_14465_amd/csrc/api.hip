@@ -657,6 +657,7 @@ int aggregate_impl(int kind, double ratio, const bc_payload* in, const uint64_t*
     // ragged parts: [dummy-padded part-offset pointers][ADesc...][workers...]
     const size_t rp_bytes = ragged ? align256((size_t)(padded_workers(W) + 1) * sizeof(uint64_t)) : 0;
     uint32_t unit = kSignAggUnit;
+    bool ring = false;
     if (sparse) {
         uint64_t nt = 0, kt = 0;
         for (int i = 0; i < T; ++i) {
@@ -664,7 +665,7 @@ int aggregate_impl(int kind, double ratio, const bc_payload* in, const uint64_t*
             nt += n[i];
             kt += k_of(n[i], ppm);
         }
-        unit = sparse_agg_tile(nt, kt);
+        unit = sparse_agg_tile(nt, kt, W, &ring);
     }
     std::vector<unsigned char> table;
     try {
@@ -751,7 +752,7 @@ int aggregate_impl(int kind, double ratio, const bc_payload* in, const uint64_t*
     const ADesc* ad = (const ADesc*)((const char*)en->dev + rp_bytes);
     const uint64_t* wdd = (const uint64_t*)((const char*)en->dev + rp_bytes + (size_t)T * sizeof(ADesc));
     if (sparse) {
-        e = launch_aggregate_sparse(ad, T, (uint32_t)units, unit, wdd, W, alpha, di.cus, rpd, s);
+        e = launch_aggregate_sparse(ad, T, (uint32_t)units, unit, ring, wdd, W, alpha, di.cus, rpd, s);
     } else if (quant_bits(kind)) {
         e = launch_aggregate_quant(quant_bits(kind), ad, T, (uint32_t)units, wdd, W, alpha, w.s_info, w.s_tab, s);
     } else {

@@ -15,7 +15,10 @@
 // tile are the next ones after its cursor (indices ascending), read 64 at a
 // time and added into the tile (indices are unique within a worker, so a
 // worker's adds never collide and need no atomics).  Cursors are found by a
-// binary search only where a wave's run starts inside a tensor.
+// search only where a wave's run starts inside a tensor.  Two forms: a slot
+// pipeline that keeps 8 or 16 workers' next windows in flight (any W), and
+// a ring form for 33 to 64 workers that keeps every worker's window in
+// registers across the whole run (below).
 #include <mutex>
 
 #include "launch.hpp"
@@ -272,8 +275,242 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
 }
 
 
+// ------------------------------------------------------ ring-window form
+// For W <= 64 and sparse enough payloads: every worker keeps one 64-entry
+// window of (index, value) pairs in registers for the wave's whole run of
+// tiles, as a ring -- lane l holds the window's entry whose position in the
+// worker's payload is congruent to l modulo 64.  The window of worker w
+// starts at its cursor c and holds positions [c, c + 64).  A step adds the
+// window's entries that fall in the tile (a prefix of the window: indices
+// ascend and everything below the tile was consumed before) into the tile,
+// then reloads exactly the lanes it consumed with the positions 64 further
+// on.  Every payload entry is thus fetched once per call, and a reload has
+// a whole round of the other workers' steps to arrive before it is used.
+// A worker with more than 64 entries in one tile repeats the step after
+// its reload has arrived (rare at the densities this form is chosen for).
+//
+// Loads go through buffer resources sized to the worker's entry count:
+// positions past it read zero without touching memory, and the lanes that
+// hold them are masked out of the step by the count, so the windows need
+// no clamping.  Each step does one LDS read-add-write: lanes with nothing
+// to add address a per-lane dummy word past the tile instead of branching.
+
+// First position p in [0, k) with idx[p] >= x (k if none), by rounds of
+// fifteen independent probes that cut the interval sixteenfold, so a run's
+// starting cursor costs about four load latencies instead of seventeen.
+__device__ __forceinline__ uint32_t lower_bound_16(const uint32_t* idx, uint32_t k, uint32_t x) {
+    uint32_t lo = 0, hi = k;  // the answer lies in [lo, hi]
+    while (hi - lo > 16u) {
+        const uint64_t len = hi - lo;
+        uint32_t v[15];
+#pragma unroll
+        for (uint32_t j = 1; j < 16u; ++j) v[j - 1] = gp(idx)[lo + (uint32_t)((len * j) >> 4)];
+        uint32_t c = 0;
+#pragma unroll
+        for (uint32_t j = 0; j < 15u; ++j) c += v[j] < x ? 1u : 0u;
+        const uint32_t nlo = c ? lo + (uint32_t)((len * c) >> 4) + 1u : lo;
+        const uint32_t nhi = c < 15u ? lo + (uint32_t)((len * (c + 1u)) >> 4) : hi;
+        lo = nlo;
+        hi = nhi;
+    }
+    uint32_t c = 0;
+    for (uint32_t j = 0; j < hi - lo; ++j) c += gp(idx)[lo + j] < x ? 1u : 0u;
+    return lo + c;
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t entries_rsrc(uint64_t base, uint32_t k) {
+    // raw buffer over k 4-byte entries (gfx9 word 3: 32-bit data format)
+    return __builtin_amdgcn_make_buffer_rsrc((void*)(uintptr_t)base, (short)0, (int)(k * 4u), 0x00020000);
+}
+
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
+    return ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(v >> 32), l) << 32) |
+           (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+}
+
+// Lane state of worker `lane` for tensor t: entry count and the bases of
+// its index and value arrays (lanes past W copy worker W - 1; they are
+// never read for a worker number >= W).
+template <bool kRagged>
+__device__ __forceinline__ void ring_lane_state(const ADesc& ad, int t, const uint64_t* __restrict__ wp, int W,
+                                                const uint64_t* __restrict__ rp, uint32_t& kv, uint64_t& pav,
+                                                uint64_t& pbv) {
+    const int lane = lane_id();
+    const int wl = lane < W ? lane : W - 1;
+    const int Wp = padded_workers(W);
+    if constexpr (kRagged) {
+        const uint64_t* po = (const uint64_t*)rp[wl];
+        const uint64_t o0 = po[t], o1 = po[t + 1];
+        kv = (uint32_t)(o1 - o0);
+        pav = wp[wl] + o0 * 4u;
+        pbv = wp[Wp + wl] + o0 * 4u;
+    } else {
+        kv = ad.k;
+        pav = wp[wl] + ad.off * 4u;
+        pbv = wp[Wp + wl] + ad.off * 4u;
+    }
+}
+
+// kW: worker slots (8, 16, 32 or 64; slots W .. kW - 1 hold no entries and
+// their steps add nothing).  kRagged: as in aggregate_sparse (parts packed
+// by bytecomp_pack_part).
+//
+// Every window register has one definition inside the tile loop, the
+// step's reload, so that the compiler keeps each window in place and
+// tracks its loads exactly: the reload of a tensor's last tile already
+// fetches the next tensor's first window (cursor 0), and the windows of
+// the run's first tile are fetched before the loop.
+template <uint32_t kTS, int kW, bool kRagged, bool kNT>
+__global__ __launch_bounds__(kBlock) void aggregate_sparse_ring(const ADesc* __restrict__ a, int T, uint32_t U,
+                                                                const uint64_t* __restrict__ wp, int W, float alpha,
+                                                                const uint64_t* __restrict__ rp) {
+    extern __shared__ uint32_t lds[];
+    const int wave = wave_id();
+    const int lane = lane_id();
+    float* tile = reinterpret_cast<float*>(lds) + wave * (int)(kTS + 64u);
+    const uint64_t nw = (uint64_t)gridDim.x * 4;
+    const uint64_t gw = (uint64_t)blockIdx.x * 4 + wave;
+    const uint32_t u_beg = (uint32_t)((gw * U) / nw);
+    const uint32_t u_end = (uint32_t)(((gw + 1) * U) / nw);
+    if (u_beg >= u_end) return;
+    // the windows: worker w's entries in x[w] (indices) and y[w] (values)
+    uint32_t x[kW];
+    float y[kW];
+    auto fetch = [&](uint64_t pa, uint64_t pb, uint32_t kw, uint32_t pos, uint32_t& xo, float& yo) {
+        xo = __builtin_amdgcn_raw_buffer_load_b32(entries_rsrc(pa, kw), (int)(pos * 4u), 0, 0);
+        yo = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(entries_rsrc(pb, kw), (int)(pos * 4u), 0, 0));
+    };
+    // lane w: worker w's cursor, entry count and payload bases for the tensor
+    int t = unit_owner(wp, W, u_beg);
+    ADesc ad = a[t];
+    uint32_t kv, curv;
+    uint64_t pav, pbv;
+    ring_lane_state<kRagged>(ad, t, wp, W, rp, kv, pav, pbv);
+    {
+        const uint32_t lo0 = (u_beg - ad.unit0) * kTS;
+        curv = lo0 == 0 ? 0u : lower_bound_16((const uint32_t*)pav, kv, lo0);
+        if (lane >= W) kv = curv = 0;  // empty slots
+#pragma unroll
+        for (int w = 0; w < kW; ++w) {
+            const uint32_t c = (uint32_t)__builtin_amdgcn_readlane((int)curv, w);
+            fetch(readlane64(pav, w), readlane64(pbv, w), (uint32_t)__builtin_amdgcn_readlane((int)kv, w),
+                  c + (((uint32_t)lane - c) & 63u), x[w], y[w]);
+        }
+    }
+    for (uint32_t u = u_beg; u < u_end; ++u) {
+        const uint32_t lo = (u - ad.unit0) * kTS;
+        const uint32_t hi = (lo + kTS < ad.n) ? lo + kTS : ad.n;
+        const uint32_t len = hi - lo;
+        // the next tile starts another tensor: its state, for the reloads
+        const bool sw = u + 1 < u_end && u + 1 >= ad.unit0 + ad.nunits;
+        int t2 = t;
+        ADesc ad2 = ad;
+        uint32_t kv2 = kv;
+        uint64_t pav2 = pav, pbv2 = pbv;
+        if (sw) {
+            t2 = unit_owner(wp, W, u + 1);
+            ad2 = a[t2];
+            ring_lane_state<kRagged>(ad2, t2, wp, W, rp, kv2, pav2, pbv2);
+            if (lane >= W) kv2 = 0;
+        }
+#pragma unroll
+        for (uint32_t r = 0; r < kTS / 256u; ++r)
+            *reinterpret_cast<f32x4*>(tile + 256u * r + 4u * lane) = f32x4{0.f, 0.f, 0.f, 0.f};
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int w = 0; w < kW; ++w) {
+            const uint32_t kw = (uint32_t)__builtin_amdgcn_readlane((int)kv, w);
+            const uint32_t c = (uint32_t)__builtin_amdgcn_readlane((int)curv, w);
+            // lanes holding positions below the worker's count
+            const uint32_t rem = kw - c;
+            uint64_t vm = rem >= 64u ? ~0ull : ((1ull << rem) - 1ull);
+            const uint32_t sh = c & 63u;
+            vm = sh ? (vm << sh) | (vm >> (64u - sh)) : vm;
+            const uint32_t dd = x[w] - lo;
+            const uint64_t m = __ballot(dd < len) & vm;
+            const uint32_t cnt = (uint32_t)__popcll(m);
+            const uint32_t at = __builtin_amdgcn_inverse_ballot_w64(m) ? dd : kTS + (uint32_t)lane;
+            const float v = tile[at];
+            tile[at] = v + y[w];
+            uint32_t cf = c + cnt;
+            const bool dense = cnt == 64u;
+            if (dense) {
+                // the whole window was in the tile: continue straight from
+                // the payload, 64 positions at a time, until the worker's
+                // entries leave the tile
+                const uint64_t pa = readlane64(pav, w), pb = readlane64(pbv, w);
+                uint32_t more = 64u;
+                while (more == 64u) {
+                    const uint32_t pos = cf + (uint32_t)lane;
+                    uint32_t xi;
+                    float yi;
+                    fetch(pa, pb, kw, pos, xi, yi);
+                    const uint32_t di = xi - lo;
+                    const uint64_t mi = __ballot(pos < kw && di < len);
+                    more = (uint32_t)__popcll(mi);
+                    const uint32_t ai = __builtin_amdgcn_inverse_ballot_w64(mi) ? di : kTS + (uint32_t)lane;
+                    const float vi = tile[ai];
+                    tile[ai] = vi + yi;
+                    cf += more;
+                }
+            }
+            // the window moves to positions [cf, cf + 64) (the next tensor's
+            // [0, 64) when the tile ends a tensor): the consumed lanes load
+            // their new positions (c + 64 + p is cf's ring slot of lane p),
+            // every lane after a dense tile or at a tensor switch
+            const uint32_t c2 = sw ? 0u : cf;
+            const uint32_t p = ((uint32_t)lane - c) & 63u;
+            if (sw || dense || p < cnt)
+                fetch(readlane64(sw ? pav2 : pav, w), readlane64(sw ? pbv2 : pbv, w),
+                      sw ? (uint32_t)__builtin_amdgcn_readlane((int)kv2, w) : kw,
+                      c2 + (((uint32_t)lane - c2) & 63u), x[w], y[w]);
+            curv = __builtin_amdgcn_inverse_ballot_w64(1ull << w) ? c2 : curv;
+        }
+        __builtin_amdgcn_wave_barrier();
+        float* out = ad.out + lo;
+        if (len == kTS) {
+#pragma unroll
+            for (uint32_t r = 0; r < kTS / 256u; ++r) {
+                const uint32_t i = 256u * r + 4u * lane;
+                const f32x4 v = *reinterpret_cast<const f32x4*>(tile + i);
+                stg4f_s<kNT>(out + i, f32x4{alpha * v[0], alpha * v[1], alpha * v[2], alpha * v[3]});
+            }
+        } else {
+            for (uint32_t i = 4u * lane; i < len; i += 256u) {
+                if (i + 3 < len) {
+                    stg4f_s<kNT>(out + i, f32x4{alpha * tile[i], alpha * tile[i + 1], alpha * tile[i + 2],
+                                         alpha * tile[i + 3]});
+                } else {
+                    for (uint32_t q = i; q < len; ++q) gp(out)[q] = alpha * tile[q];
+                }
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+        if (sw) {
+            t = t2;
+            ad = ad2;
+            kv = kv2;
+            pav = pav2;
+            pbv = pbv2;
+        }
+    }
+}
+
 // -------------------------------------------------------------- launchers
-uint32_t sparse_agg_tile(uint64_t n_total, uint64_t k_total) {
+uint32_t sparse_agg_tile(uint64_t n_total, uint64_t k_total, int W, bool* ring) {
+    // ring form (more than 32 workers; fewer take the slot pipeline below,
+    // measured faster there): the largest tile in which a worker holds about
+    // 44 entries or fewer on average (its 64-entry window then almost never
+    // runs dry inside a tile); entry counts stay below 2^30 for 32-bit byte
+    // offsets
+    *ring = false;
+    if (W > 32 && W <= 64 && k_total < (1ull << 30) - 64u && n_total > 0) {
+        for (uint32_t ts = 8192u; ts >= 1024u; ts >>= 1)
+            if (k_total * ts <= n_total * 44u) {
+                *ring = true;
+                return ts;
+            }
+    }
     // 8192-element tiles (128-entry windows) for calls of at least 2^24
     // elements whose workers hold about 100 entries per such tile or fewer;
     // else 4096-element tiles while a worker holds about 48 entries per tile
@@ -334,12 +571,61 @@ hipError_t launch_sparse_ts(const ADesc* a, int T, uint32_t U, const uint64_t* w
 }
 }  // namespace
 
-hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t U, uint32_t tile, const uint64_t* w, int W,
-                                   float alpha, int cus, const uint64_t* rp, hipStream_t s) {
+namespace {
+template <uint32_t kTS, int kW, bool kRagged, bool kNT>
+hipError_t launch_ring_t(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W, float alpha, int cus,
+                         const uint64_t* rp, hipStream_t s) {
+    const auto kern = aggregate_sparse_ring<kTS, kW, kRagged, kNT>;
+    const size_t lds = (size_t)4 * 4 * (kTS + 64u);
+    // one round of resident workgroups (registers and LDS decide how many)
+    static int per_cu = 0;
+    if (per_cu == 0) {
+        int nb = 0;
+        const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kern, kBlock, lds);
+        if (e != hipSuccess) return e;
+        per_cu = nb > 0 ? nb : 1;
+    }
+    uint64_t blocks = (U + 3) / 4;
+    const uint64_t cap = (uint64_t)per_cu * (uint64_t)(cus > 0 ? cus : 256);
+    if (blocks > cap) blocks = cap;
+    return launch_timed(kTimedAggSparse, kern, dim3((uint32_t)blocks), dim3(kBlock), lds, s, a, T, U, w, W, alpha,
+                        rp);
+}
+template <uint32_t kTS, int kW, bool kRagged>
+hipError_t launch_ring_nt(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W, float alpha, int cus,
+                          const uint64_t* rp, hipStream_t s) {
+    if ((uint64_t)U * kTS > (uint64_t)kNtTiles * 4096u)
+        return launch_ring_t<kTS, kW, kRagged, true>(a, T, U, w, W, alpha, cus, rp, s);
+    return launch_ring_t<kTS, kW, kRagged, false>(a, T, U, w, W, alpha, cus, rp, s);
+}
+template <uint32_t kTS, bool kRagged>
+hipError_t launch_ring_ts(const ADesc* a, int T, uint32_t U, const uint64_t* w, int W, float alpha, int cus,
+                          const uint64_t* rp, hipStream_t s) {
+    // (the form is chosen for 33 to 64 workers)
+    return launch_ring_nt<kTS, 64, kRagged>(a, T, U, w, W, alpha, cus, rp, s);
+}
+template <bool kRagged>
+hipError_t launch_ring(const ADesc* a, int T, uint32_t U, uint32_t tile, const uint64_t* w, int W, float alpha,
+                       int cus, const uint64_t* rp, hipStream_t s) {
+    switch (tile) {
+        case 8192u: return launch_ring_ts<8192u, kRagged>(a, T, U, w, W, alpha, cus, rp, s);
+        case 4096u: return launch_ring_ts<4096u, kRagged>(a, T, U, w, W, alpha, cus, rp, s);
+        case 2048u: return launch_ring_ts<2048u, kRagged>(a, T, U, w, W, alpha, cus, rp, s);
+        case 1024u: return launch_ring_ts<1024u, kRagged>(a, T, U, w, W, alpha, cus, rp, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+}  // namespace
+
+hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t U, uint32_t tile, bool ring, const uint64_t* w,
+                                   int W, float alpha, int cus, const uint64_t* rp, hipStream_t s) {
     if (U == 0) return hipSuccess;
-    if (rp && W > 64) return hipErrorInvalidValue;
+    if ((rp || ring) && W > 64) return hipErrorInvalidValue;
     hipError_t e;
-    if (rp) {
+    if (ring) {
+        e = rp ? launch_ring<true>(a, T, U, tile, w, W, alpha, cus, rp, s)
+               : launch_ring<false>(a, T, U, tile, w, W, alpha, cus, nullptr, s);
+    } else if (rp) {
         if (tile == 8192u) e = launch_sparse_ts<8192u, true>(a, T, U, w, W, alpha, cus, rp, s);
         else if (tile == 4096u) e = launch_sparse_ts<4096u, true>(a, T, U, w, W, alpha, cus, rp, s);
         else if (tile == 2048u) e = launch_sparse_ts<2048u, true>(a, T, U, w, W, alpha, cus, rp, s);

@@ -163,12 +163,14 @@ hipError_t launch_residual_update(int kind, const TDesc* d, int T, uint32_t C, b
                                   bool any_f32, const uint32_t* idx, const float* val,
                                   const uint32_t* bits, const float* scale, hipStream_t s);
 // Sparse aggregate tile (elements per work unit) for a call whose tensors
-// hold n_total elements and k_total entries per worker.
-uint32_t sparse_agg_tile(uint64_t n_total, uint64_t k_total);
+// hold n_total elements and k_total entries per worker from W workers;
+// *ring tells whether the ring-window kernel takes the call.
+uint32_t sparse_agg_tile(uint64_t n_total, uint64_t k_total, int W, bool* ring);
 // rp: null, or (ragged parts) per-worker part-offset arrays, then a dummy
 // readable location, as device pointers [padded_workers(W) + 1].
-hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t units, uint32_t tile, const uint64_t* wp,
-                                   int W, float alpha, int cus, const uint64_t* rp, hipStream_t s);
+hipError_t launch_aggregate_sparse(const ADesc* a, int T, uint32_t units, uint32_t tile, bool ring,
+                                   const uint64_t* wp, int W, float alpha, int cus, const uint64_t* rp,
+                                   hipStream_t s);
 hipError_t launch_aggregate_sign(const ADesc* a, int T, uint32_t units, const uint64_t* wp, int W,
                                  float alpha, hipStream_t s);
 // Stochastic b-bit quantizers (bits 2, 4 or 8).

@@ -476,6 +476,30 @@ def test_sparse_aggregate_large_tiles(W):
         assert np.array_equal(bits(got[t]), bits(want[t])), t
 
 
+@pytest.mark.parametrize("W,ratio", [(5, 0.01), (33, 0.03), (64, 0.01), (64, 0.004)])
+def test_sparse_aggregate_windows_across_tensors(W, ratio):
+    # many small tensors at low density (the register-window path): waves
+    # cross tensor boundaries inside their runs and start runs inside
+    # tensors; empty tensors and tensors without entries are mixed in, and
+    # every seventh worker crowds its entries (windows that run dry inside
+    # a tile)
+    rng = np.random.default_rng(400 + W)
+    ns = [int(x) for x in rng.integers(1, 60000, size=150)] + [0, 1, 3, 250000, 4096, 4097, 1 << 20]
+    counts = [O.k_for(n, ratio) for n in ns]
+    payloads = []
+    for w in range(W):
+        if w % 7 == 3:
+            idx, val = _clustered_lists(rng, ns, counts, 0.03)
+        else:
+            idx, val = WL.random_sparse_lists(rng, ns, counts)
+        payloads.append({"idx": np.concatenate(idx), "val": np.concatenate(val),
+                         "off": O.sparse_offsets(ns, ratio)})
+    got = gpu_aggregate("topk", ratio, ns, payloads, 1.0 / W)
+    want = O.aggregate_set("topk", ns, payloads, 1.0 / W)
+    for t in range(len(ns)):
+        assert np.array_equal(bits(got[t]), bits(want[t])), t
+
+
 def test_sparse_aggregate_dense_overlap():
     # every worker sends every index (ratio 1): maximal overlap, long runs
     rng = np.random.default_rng(23)

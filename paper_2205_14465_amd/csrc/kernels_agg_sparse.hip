@@ -15,15 +15,59 @@
 // tile are the next ones after its cursor (indices ascending), read 64 at a
 // time and added into the tile (indices are unique within a worker, so a
 // worker's adds never collide and need no atomics).  Cursors are found by a
-// search only where a wave's run starts inside a tensor.  Two forms: a slot
-// pipeline that keeps 8 or 16 workers' next windows in flight (any W), and
-// a ring form for 33 to 64 workers that keeps every worker's window in
-// registers across the whole run (below).
+// search (lower_bound_guess) only where a wave's run starts inside a
+// tensor.  Two forms: a slot pipeline that keeps 8 or 16 workers' next
+// windows in flight (any W), and a ring form for 33 to 64 workers that
+// keeps every worker's window in registers across the whole run (below).
 #include <mutex>
 
 #include "launch.hpp"
 
 namespace bc {
+
+// First position p in [0, k) with idx[p] >= x (k if none) for a tensor of
+// n elements, starting at the position the entries would have if they were
+// spread evenly over the tensor: a gallop away from that guess (steps of
+// 32, 64, ... positions) brackets the answer and a binary search finishes
+// inside the bracket.  On evenly spread indices the answer lies within a
+// few hundred positions of the guess, so a search reads about seven lines
+// of the index array instead of one per halving.
+__device__ __forceinline__ uint32_t lower_bound_guess(const uint32_t* idx, uint32_t k, uint32_t n, uint32_t x) {
+    if (k == 0) return 0;
+    uint32_t g = n ? (uint32_t)(((uint64_t)k * x) / n) : 0u;
+    if (g >= k) g = k - 1;
+    uint32_t lo, hi;  // the answer lies in [lo, hi]
+    if (gp(idx)[g] < x) {
+        lo = g + 1;
+        hi = k;
+        for (uint32_t step = 32;; step *= 2) {
+            const uint64_t q = (uint64_t)g + step;
+            if (q >= k) break;
+            if (gp(idx)[q] >= x) {
+                hi = (uint32_t)q;
+                break;
+            }
+            lo = (uint32_t)q + 1;
+        }
+    } else {
+        lo = 0;
+        hi = g;
+        for (uint32_t step = 32;; step *= 2) {
+            if (g < step) break;
+            const uint32_t q = g - step;
+            if (gp(idx)[q] < x) {
+                lo = q + 1;
+                break;
+            }
+            hi = q;
+        }
+    }
+    while (lo < hi) {
+        const uint32_t mid = lo + ((hi - lo) >> 1);
+        if (gp(idx)[mid] < x) lo = mid + 1; else hi = mid;
+    }
+    return lo;
+}
 
 // Each wave owns a run of consecutive kTS-element tiles held in its own LDS
 // slice.  The next 64 kEPL entries of kS workers (a window: lane l holds
@@ -102,15 +146,15 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
                 kv = (uint32_t)(o1 - o0);
                 pav = kv ? wp[wl] + o0 * 4u : rp[padded_workers(W)];
                 pbv = kv ? wp[padded_workers(W) + wl] + o0 * 4u : rp[padded_workers(W)];
-                curv = lo0 == 0 ? 0u : lower_bound_u32((const uint32_t*)pav, kv, lo0);
+                curv = lo0 == 0 ? 0u : lower_bound_guess((const uint32_t*)pav, kv, ad.n, lo0);
             } else if constexpr (kLanes) {
                 const int wl = lane < W ? lane : W - 1;
                 pav = wp[wl] + ad.off * 4u;
                 pbv = wp[padded_workers(W) + wl] + ad.off * 4u;
-                curv = lo0 == 0 ? 0u : lower_bound_u32((const uint32_t*)pav, ad.k, lo0);
+                curv = lo0 == 0 ? 0u : lower_bound_guess((const uint32_t*)pav, ad.k, ad.n, lo0);
             } else {
                 for (int w = lane; w < W; w += 64)
-                    cur[w] = lo0 == 0 ? 0u : lower_bound_u32(w_a(wp, w) + ad.off, ad.k, lo0);
+                    cur[w] = lo0 == 0 ? 0u : lower_bound_guess(w_a(wp, w) + ad.off, ad.k, ad.n, lo0);
                 __builtin_amdgcn_wave_barrier();
             }
             primed = false;
@@ -295,29 +339,6 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse(const ADesc* __restri
 // no clamping.  Each step does one LDS read-add-write: lanes with nothing
 // to add address a per-lane dummy word past the tile instead of branching.
 
-// First position p in [0, k) with idx[p] >= x (k if none), by rounds of
-// fifteen independent probes that cut the interval sixteenfold, so a run's
-// starting cursor costs about four load latencies instead of seventeen.
-__device__ __forceinline__ uint32_t lower_bound_16(const uint32_t* idx, uint32_t k, uint32_t x) {
-    uint32_t lo = 0, hi = k;  // the answer lies in [lo, hi]
-    while (hi - lo > 16u) {
-        const uint64_t len = hi - lo;
-        uint32_t v[15];
-#pragma unroll
-        for (uint32_t j = 1; j < 16u; ++j) v[j - 1] = gp(idx)[lo + (uint32_t)((len * j) >> 4)];
-        uint32_t c = 0;
-#pragma unroll
-        for (uint32_t j = 0; j < 15u; ++j) c += v[j] < x ? 1u : 0u;
-        const uint32_t nlo = c ? lo + (uint32_t)((len * c) >> 4) + 1u : lo;
-        const uint32_t nhi = c < 15u ? lo + (uint32_t)((len * (c + 1u)) >> 4) : hi;
-        lo = nlo;
-        hi = nhi;
-    }
-    uint32_t c = 0;
-    for (uint32_t j = 0; j < hi - lo; ++j) c += gp(idx)[lo + j] < x ? 1u : 0u;
-    return lo + c;
-}
-
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t entries_rsrc(uint64_t base, uint32_t k) {
     // raw buffer over k 4-byte entries (gfx9 word 3: 32-bit data format)
     return __builtin_amdgcn_make_buffer_rsrc((void*)(uintptr_t)base, (short)0, (int)(k * 4u), 0x00020000);
@@ -388,7 +409,8 @@ __global__ __launch_bounds__(kBlock) void aggregate_sparse_ring(const ADesc* __r
     ring_lane_state<kRagged>(ad, t, wp, W, rp, kv, pav, pbv);
     {
         const uint32_t lo0 = (u_beg - ad.unit0) * kTS;
-        curv = lo0 == 0 ? 0u : lower_bound_16((const uint32_t*)pav, kv, lo0);
+        curv = 0;
+        if (lo0 != 0 && lane < W) curv = lower_bound_guess((const uint32_t*)pav, kv, ad.n, lo0);
         if (lane >= W) kv = curv = 0;  // empty slots
 #pragma unroll
         for (int w = 0; w < kW; ++w) {

@@ -61,17 +61,45 @@ __device__ __forceinline__ uint32_t tensor_max(const uint32_t* __restrict__ q, c
     return block_max_u32(m, sh);
 }
 
-// Uniforms of the four elements 8g + 4h .. 8g + 4h + 3 of a tensor.
-__device__ __forceinline__ void quant_uniforms(uint64_t seed, uint32_t tid, uint32_t g, uint32_t h,
-                                               float (&u)[4]) {
-    const U64x4 ctr = {{(uint64_t)tid, (uint64_t)g, 0, 0}};
-    const U64x4 r = philox4x64_10(ctr, seed, kStreamQuant);
-    const uint64_t w0 = h ? r.v[2] : r.v[0];
-    const uint64_t w1 = h ? r.v[3] : r.v[1];
+__device__ __forceinline__ void words_to_uniforms(uint64_t w0, uint64_t w1, float (&u)[4]) {
     u[0] = (float)((uint32_t)w0 >> 8) * 0x1p-24f;
     u[1] = (float)((uint32_t)(w0 >> 32) >> 8) * 0x1p-24f;
     u[2] = (float)((uint32_t)w1 >> 8) * 0x1p-24f;
     u[3] = (float)((uint32_t)(w1 >> 32) >> 8) * 0x1p-24f;
+}
+
+__device__ __forceinline__ uint64_t shfl_xor64(uint64_t x, int m) {
+    const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)x, m, 64);
+    const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(x >> 32), m, 64);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// The uniforms of the thread's kRounds rounds of chunk j (round r: the
+// elements i = 4096 j + 1024 r + 4 tid .. + 3; element i takes 32-bit word
+// i mod 8 of the Philox block at counter (tensor id, i / 8)).  The two
+// threads of a lane pair share every round's block, each using one half of
+// it, so the even thread computes the blocks of the even rounds and the odd
+// thread those of the odd rounds, and each hands the other the half it
+// needs: every uniform as defined, for half the Philox work.  Called by
+// every thread of the workgroup.
+__device__ __forceinline__ void chunk_uniforms(uint64_t seed, uint32_t tid, uint32_t j,
+                                               float (&u)[kRounds][4]) {
+    static_assert(kRounds % 2 == 0, "rounds pair up");
+    const bool odd = (threadIdx.x & 1u) != 0u;
+#pragma unroll
+    for (int rr = 0; rr < kRounds / 2; ++rr) {
+        const uint32_t r = 2u * (uint32_t)rr + (odd ? 1u : 0u);  // the round whose block this thread computes
+        const uint32_t g = (j * (uint32_t)kChunk + 1024u * r + 4u * threadIdx.x) >> 3;
+        const U64x4 ctr = {{(uint64_t)tid, (uint64_t)g, 0, 0}};
+        const U64x4 R = philox4x64_10(ctr, seed, kStreamQuant);
+        // own half (words 0, 1 for the even thread, 2, 3 for the odd one),
+        // and the partner's half, sent across the pair
+        const uint64_t k0 = odd ? R.v[2] : R.v[0], k1 = odd ? R.v[3] : R.v[1];
+        const uint64_t q0 = shfl_xor64(odd ? R.v[0] : R.v[2], 1), q1 = shfl_xor64(odd ? R.v[1] : R.v[3], 1);
+        // round 2rr is the even thread's block, round 2rr + 1 the odd one's
+        words_to_uniforms(odd ? q0 : k0, odd ? q1 : k1, u[2 * rr]);
+        words_to_uniforms(odd ? k0 : q0, odd ? k1 : q1, u[2 * rr + 1]);
+    }
 }
 
 // Decoded value of a code for a tensor whose decoding unit is `unit`.
@@ -119,11 +147,9 @@ __device__ __forceinline__ void store_codes(uint32_t packed, uint32_t e0, uint32
 // stores their codes and leaves their residuals v - decode in v4.
 template <int kBits>
 __device__ __forceinline__ void quantize_round(const TDesc& td, uint32_t e0, bool any, float inv, float unit,
-                                               float (&v4)[4], uint32_t valid4, uint64_t seed,
+                                               float (&v4)[4], uint32_t valid4, const float (&u)[4],
                                                uint32_t* __restrict__ tw) {
     using Q = Quant<kBits>;
-    float u[4];
-    quant_uniforms(seed, td.tid, e0 >> 3, (e0 >> 2) & 1u, u);
     uint32_t packed = 0;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -154,11 +180,13 @@ __device__ __forceinline__ void quantize_chunk(const TDesc& td, uint32_t j, floa
     const float inv = any ? (float)((double)Q::kLevels / (double)m) : 0.f;
     const float unit = (float)((double)m / (double)Q::kLevels);
     uint32_t* tw = words + td.off;
+    float u[kRounds][4];
+    chunk_uniforms(seed, td.tid, j, u);
 #pragma unroll
     for (int r = 0; r < kRounds; ++r) {
         const uint32_t e0 = j * (uint32_t)kChunk + 1024u * r + 4u * threadIdx.x;  // element of the tensor
         float v4[4] = {v[4 * r], v[4 * r + 1], v[4 * r + 2], v[4 * r + 3]};
-        quantize_round<kBits>(td, e0, any, inv, unit, v4, (valid >> (4 * r)) & 0xFu, seed, tw);
+        quantize_round<kBits>(td, e0, any, inv, unit, v4, (valid >> (4 * r)) & 0xFu, u[r], tw);
 #pragma unroll
         for (int q = 0; q < 4; ++q) v[4 * r + q] = v4[q];
     }

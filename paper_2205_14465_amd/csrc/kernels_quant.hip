@@ -68,10 +68,16 @@ __device__ __forceinline__ void words_to_uniforms(uint64_t w0, uint64_t w1, floa
     u[3] = (float)((uint32_t)(w1 >> 32) >> 8) * 0x1p-24f;
 }
 
-__device__ __forceinline__ uint64_t shfl_xor64(uint64_t x, int m) {
-    const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)x, m, 64);
-    const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(x >> 32), m, 64);
-    return ((uint64_t)hi << 32) | lo;
+// The value of lane l ^ 1 (l ^ 2), by a DPP quad permutation: one VALU
+// move instead of an LDS permute.
+__device__ __forceinline__ uint32_t lane_xor1(uint32_t x) {
+    return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0xB1, 0xF, 0xF, false);  // quad_perm [1,0,3,2]
+}
+__device__ __forceinline__ uint32_t lane_xor2(uint32_t x) {
+    return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x4E, 0xF, 0xF, false);  // quad_perm [2,3,0,1]
+}
+__device__ __forceinline__ uint64_t lane_xor1_64(uint64_t x) {
+    return ((uint64_t)lane_xor1((uint32_t)(x >> 32)) << 32) | lane_xor1((uint32_t)x);
 }
 
 // The uniforms of the thread's kRounds rounds of chunk j (round r: the
@@ -95,7 +101,7 @@ __device__ __forceinline__ void chunk_uniforms(uint64_t seed, uint32_t tid, uint
         // own half (words 0, 1 for the even thread, 2, 3 for the odd one),
         // and the partner's half, sent across the pair
         const uint64_t k0 = odd ? R.v[2] : R.v[0], k1 = odd ? R.v[3] : R.v[1];
-        const uint64_t q0 = shfl_xor64(odd ? R.v[0] : R.v[2], 1), q1 = shfl_xor64(odd ? R.v[1] : R.v[3], 1);
+        const uint64_t q0 = lane_xor1_64(odd ? R.v[0] : R.v[2]), q1 = lane_xor1_64(odd ? R.v[1] : R.v[3]);
         // round 2rr is the even thread's block, round 2rr + 1 the odd one's
         words_to_uniforms(odd ? q0 : k0, odd ? q1 : k1, u[2 * rr]);
         words_to_uniforms(odd ? k0 : q0, odd ? k1 : q1, u[2 * rr + 1]);
@@ -130,13 +136,13 @@ __device__ __forceinline__ void store_codes(uint32_t packed, uint32_t e0, uint32
         if (wi < nwords) gp(words)[wi] = packed;
     } else if constexpr (kBits == 4) {
         uint32_t x = packed << (16 * (lane & 1));
-        x |= (uint32_t)__shfl_xor((int)x, 1, 64);
+        x |= lane_xor1(x);
         const uint32_t wi = e0 / 8u;
         if ((lane & 1) == 0 && wi < nwords) gp(words)[wi] = x;
     } else {
         uint32_t x = packed << (8 * (lane & 3));
-        x |= (uint32_t)__shfl_xor((int)x, 1, 64);
-        x |= (uint32_t)__shfl_xor((int)x, 2, 64);
+        x |= lane_xor1(x);
+        x |= lane_xor2(x);
         const uint32_t wi = e0 / 16u;
         if ((lane & 3) == 0 && wi < nwords) gp(words)[wi] = x;
     }

@@ -75,7 +75,14 @@ __device__ __forceinline__ void entry_tensor_advance(const TDesc* __restrict__ d
 }
 
 // Generate the indices of kGenEntries consecutive payload entries, keep
-// them in r_tmp, and write this workgroup's row of bucket counts.
+// them in r_tmp, and write this workgroup's row of bucket counts.  A thread
+// takes its entries in turn, but the cycle walks are not aligned across the
+// wave: every pass of the loop applies one Feistel evaluation per thread,
+// and a thread whose walk has landed in [0, n) records its index and starts
+// its next entry in the same pass.  A wave then costs about the largest
+// per-thread total of evaluations rather than the sum over entries of the
+// largest walk in the wave (walks take 1 to 4 evaluations on average and
+// have long tails).
 __global__ __launch_bounds__(kGenBlock) void randk_count(const TDesc* __restrict__ d, int T, uint64_t sum_k,
                                                          uint32_t S, uint32_t NB, Ws ws) {
     extern __shared__ uint32_t hist[];  // [NB]
@@ -83,15 +90,31 @@ __global__ __launch_bounds__(kGenBlock) void randk_count(const TDesc* __restrict
     __syncthreads();
     const uint64_t j0 = (uint64_t)blockIdx.x * kGenEntries + threadIdx.x;
     EntryTensor et;
-    if (j0 < sum_k) entry_tensor_load(d, T, ws.r_keys, tensor_of_entry(d, T, j0), et);
-    for (int q = 0; q < kGenPerThread; ++q) {
-        const uint64_t j = j0 + (uint64_t)q * kGenBlock;
-        if (j >= sum_k) break;
-        entry_tensor_advance(d, T, ws.r_keys, j, et);
-        uint32_t x = feistel((uint32_t)(j - et.off), et.h, et.mask, et.rk);
-        while (x >= et.n) x = feistel(x, et.h, et.mask, et.rk);
-        ws.r_tmp[j] = x;
-        atomicAdd(&hist[(et.chunk0 + x / (uint32_t)kChunk) >> S], 1u);
+    uint64_t j = j0;
+    int q = 0;
+    bool live = j0 < sum_k;
+    uint32_t cur = 0;  // the value the next evaluation permutes
+    if (live) {
+        entry_tensor_load(d, T, ws.r_keys, tensor_of_entry(d, T, j0), et);
+        cur = (uint32_t)(j - et.off);
+    }
+    while (__any(live)) {
+        if (live) {
+            const uint32_t x = feistel(cur, et.h, et.mask, et.rk);
+            if (x < et.n) {
+                ws.r_tmp[j] = x;
+                atomicAdd(&hist[(et.chunk0 + x / (uint32_t)kChunk) >> S], 1u);
+                ++q;
+                j += (uint64_t)kGenBlock;
+                live = q < kGenPerThread && j < sum_k;
+                if (live) {
+                    entry_tensor_advance(d, T, ws.r_keys, j, et);
+                    cur = (uint32_t)(j - et.off);
+                }
+            } else {
+                cur = x;
+            }
+        }
     }
     __syncthreads();
     uint32_t* row = ws.r_hist + (size_t)blockIdx.x * NB;

@@ -234,7 +234,8 @@ def kernel_candidates(wl, kind, comp_b, agg_b, pay_b):
     bytes one launch moves (what the method must move, attributed to the
     kernel that moves it)."""
     n = wl.n_total
-    g_in = 4 if wl.momentum else (2 if wl.grad_dtype == "float16" else 4)  # DGC compresses the fp32 velocity
+    # DGC: the top-k stream pass also takes the velocity step (reads g and u, writes u)
+    g_in = (2 if wl.grad_dtype == "float16" else 4) + (8 if wl.momentum else 0)
     if kind == "randk":
         return [("randk_stream", comp_b), ("aggregate_sparse", agg_b)]
     if kind in ("topk", "topk_sampled"):

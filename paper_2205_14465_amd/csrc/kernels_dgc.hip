@@ -13,6 +13,9 @@
 //   compress u with residual e: v = fl32(u + e), select, payload v[idx],
 //   e <- v with +0.0 at idx                         (the sparse kind)
 //   u[idx] <- +0.0                                   (dgc_mask)
+// The top-k kinds fold the velocity step into their stream pass and the
+// masking into their emit pass (kernels_topk.hip); random-k runs the three
+// steps as separate launches.
 #include "launch.hpp"
 
 namespace bc {
@@ -106,11 +109,18 @@ __global__ __launch_bounds__(kBlock) void dgc_mask(const TDesc* __restrict__ d, 
     }
 }
 
+hipError_t launch_dgc_clip(const TDesc* d, int T, uint32_t C, double clip, double* part, float* factor,
+                           float* factor_out, hipStream_t s) {
+    if (C > 0) hipLaunchKernelGGL(dgc_sumsq, dim3(C), dim3(kBlock), 0, s, d, T, part);
+    hipLaunchKernelGGL(dgc_clip_factor, dim3(1), dim3(kBlock), 0, s, part, C, clip, factor, factor_out);
+    return hipGetLastError();
+}
+
 hipError_t launch_dgc_momentum(const TDesc* d, int T, uint32_t C, float m, bool clipping, double clip,
                                 double* part, float* factor, float* factor_out, hipStream_t s) {
     if (clipping) {
-        if (C > 0) hipLaunchKernelGGL(dgc_sumsq, dim3(C), dim3(kBlock), 0, s, d, T, part);
-        hipLaunchKernelGGL(dgc_clip_factor, dim3(1), dim3(kBlock), 0, s, part, C, clip, factor, factor_out);
+        const hipError_t e = launch_dgc_clip(d, T, C, clip, part, factor, factor_out, s);
+        if (e != hipSuccess) return e;
     }
     if (C == 0) return hipGetLastError();
     const float* cf = clipping ? factor : nullptr;

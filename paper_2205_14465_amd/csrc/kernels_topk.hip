@@ -24,6 +24,14 @@
 //             the payload and zeroes e_new at the winners.
 // Trimming or topping up to exactly k in the selection order makes the
 // sampled kind return the same entries as the exact kind.
+//
+// A DGC step (Sec. 5.1) runs inside the same passes: the pass that forms v
+// (the exact path's histogram pass, the sampled path's stream pass; the
+// sample reads the same values) first takes the velocity step
+// u <- fl32(fl32(m * u) + fl32(c * g)) and writes u, then v = fl32(u + e);
+// the emit pass writes +0.0 into u as well as e_new at the winners.  The
+// call's table then holds u in the gradient's place; the gradients come
+// from a second table of the same tensors.
 #include "launch.hpp"
 
 namespace bc {
@@ -44,6 +52,34 @@ __device__ __forceinline__ bool active(const uint32_t* fb, int t, bool fb_only) 
     return !fb_only || fb[t] != 0u;
 }
 
+// The DGC velocity step of a chunk: td holds u (as the fp32 gradient) and
+// e, tg the step's gradient; u receives fl32(fl32(m * u) + fl32(c * g))
+// (c the clipping factor, or g as widened without clipping) and v fl32(u + e),
+// +0.0 past the tensor's end.
+template <bool kNT>
+__device__ __forceinline__ void load_v_dgc(const TDesc& td, const TDesc& tg, uint32_t j, const DgcFuse& f,
+                                           float u[kEpt], float v[kEpt], uint32_t& valid) {
+    float g[kEpt], e[kEpt];
+    load_v<kNT>(tg, j, false, g, valid);
+    load_v<kNT>(td, j, false, u, valid);
+    TDesc te = td;
+    te.grad = td.resid;
+    load_v<kNT>(te, j, false, e, valid);
+    if (f.clip) {
+        const float cf = *f.clip;
+#pragma unroll
+        for (int i = 0; i < kEpt; ++i) g[i] = cf * g[i];
+    }
+#pragma unroll
+    for (int i = 0; i < kEpt; ++i) {
+        const float mu = f.m * u[i];
+        u[i] = mu + g[i];
+        v[i] = u[i] + e[i];
+    }
+}
+
+__device__ __forceinline__ float* vel_of(const TDesc& td) { return (float*)const_cast<void*>(td.grad); }
+
 // Flush a block's LDS histogram into the tensor's global histogram.
 __device__ __forceinline__ void flush_hist(const uint32_t* lh, uint32_t* gh, int bins) {
     for (int b = threadIdx.x; b < bins; b += kBlock) {
@@ -54,12 +90,14 @@ __device__ __forceinline__ void flush_hist(const uint32_t* lh, uint32_t* gh, int
 
 }  // namespace
 
-// Stream pass of the exact path: e_new = v (when `write_resid`) and the
-// histogram of key bits 30..20.  With `fb_only` it re-reads the stored v of
-// tensors flagged for the fallback.
+// Stream pass of the exact path: e_new = v (when `write_resid`; kDGC: after
+// the velocity step) and the histogram of key bits 30..20.  With `fb_only`
+// it re-reads the stored v of tensors flagged for the fallback.
+template <bool kDGC>
 __global__ __launch_bounds__(kBlock) void topk_hist_pass(const TDesc* __restrict__ d, int T, uint32_t C,
                                                          int write_resid, int fb_only, Ws ws,
-                                                         uint64_t* __restrict__ clear_status, int copies) {
+                                                         uint64_t* __restrict__ clear_status, int copies,
+                                                         DgcFuse f) {
     __shared__ uint32_t lh[kBins0];
     if (fb_only && ws.t_any[0] == 0u) return;  // no tensor fell back
     for (uint32_t c = blockIdx.x; c < C; c += gridDim.x) {
@@ -71,7 +109,12 @@ __global__ __launch_bounds__(kBlock) void topk_hist_pass(const TDesc* __restrict
         for (int b = threadIdx.x; b < kBins0; b += kBlock) lh[b] = 0;
         float v[kEpt];
         uint32_t valid;
-        if (write_resid) {
+        if (kDGC && write_resid) {
+            float u[kEpt];
+            load_v_dgc<false>(td, f.dg[t], j, f, u, v, valid);
+            store_chunk(vel_of(td), td.n, j, u);
+            store_chunk(td.resid, td.n, j, v);
+        } else if (write_resid) {
             load_v(td, j, td.resid != nullptr, v, valid);
             if (td.resid) store_chunk(td.resid, td.n, j, v);
         } else {
@@ -95,8 +138,10 @@ __global__ __launch_bounds__(kBlock) void topk_hist_pass(const TDesc* __restrict
 // global histogram sees one atomic per non-empty bin.
 constexpr uint32_t kSampleChunksPerBlock = 16;
 
+template <bool kDGC>
 __global__ __launch_bounds__(kBlock) void topk_sample_hist(const TDesc* __restrict__ d, int T,
-                                                           uint32_t C, uint64_t seed, int copies, Ws ws) {
+                                                           uint32_t C, uint64_t seed, int copies, Ws ws,
+                                                           DgcFuse f) {
     uint32_t* gh0 = ws.t_hist + (size_t)(blockIdx.x % (uint32_t)copies) * T * kBins0;  // this workgroup's copy
     __shared__ uint32_t lh[kBins0];
     const uint32_t c0 = blockIdx.x * kSampleChunksPerBlock;
@@ -120,10 +165,22 @@ __global__ __launch_bounds__(kBlock) void topk_sample_hist(const TDesc* __restri
         if (len < 64) continue;
         const uint32_t start = j * (uint32_t)kChunk + (uint32_t)(r.v[1] % (uint64_t)(len - 63));
         const uint32_t i = start + lane_id();
-        float g;
-        if (td.dtype == 0) g = gp((const float*)td.grad)[i];
-        else g = h2f(gp((const uint16_t*)td.grad)[i]);
-        const float v = td.resid ? g + gp(td.resid)[i] : g;
+        float v;
+        if constexpr (kDGC) {  // the value the stream pass will form
+            const TDesc tg = f.dg[t];
+            float g;
+            if (tg.dtype == 0) g = gp((const float*)tg.grad)[i];
+            else g = h2f(gp((const uint16_t*)tg.grad)[i]);
+            if (f.clip) g = *f.clip * g;
+            const float mu = f.m * gp((const float*)td.grad)[i];
+            const float u = mu + g;
+            v = u + gp(td.resid)[i];
+        } else {
+            float g;
+            if (td.dtype == 0) g = gp((const float*)td.grad)[i];
+            else g = h2f(gp((const uint16_t*)td.grad)[i]);
+            v = td.resid ? g + gp(td.resid)[i] : g;
+        }
         const uint32_t bin = key_of(v) >> 20;
         if (same) atomicAdd(&lh[bin], 1u);
         else atomicAdd(gh0 + (size_t)t * kBins0 + bin, 1u);
@@ -240,13 +297,14 @@ __global__ __launch_bounds__(kBlock) void topk_find(const TDesc* __restrict__ d,
 }
 
 // Candidate compaction.  Stream mode (sampled main pass): v = g + e,
-// e_new = v written back.  Re-read mode: v from the residual (or g).
-// Candidates = valid entries with key >= t_thr[t], compacted in index
-// order into the chunk's slot of t_cand; also the LDS histogram of their
-// key bits 30..20.
-template <bool kNT>
+// e_new = v written back (kDGC: after the velocity step, u written back).
+// Re-read mode: v from the residual (or g).  Candidates = valid entries
+// with key >= t_thr[t], compacted in index order into the chunk's slot of
+// t_cand; also the LDS histogram of their key bits 30..20.
+template <bool kNT, bool kDGC>
 __global__ __launch_bounds__(kBlock) void topk_compact(const TDesc* __restrict__ d, int T, uint32_t C,
-                                                       int stream_mode, int fb_only, int copies, Ws ws) {
+                                                       int stream_mode, int fb_only, int copies, Ws ws,
+                                                       DgcFuse f) {
     __shared__ uint32_t lh[kBins0];
     __shared__ uint64_t sh[4];
     if (fb_only && ws.t_any[0] == 0u) return;  // no tensor fell back
@@ -258,7 +316,12 @@ __global__ __launch_bounds__(kBlock) void topk_compact(const TDesc* __restrict__
         for (int b = threadIdx.x; b < kBins0; b += kBlock) lh[b] = 0;
         float v[kEpt];
         uint32_t valid;
-        if (stream_mode) {
+        if (kDGC && stream_mode) {
+            float u[kEpt];
+            load_v_dgc<kNT>(td, f.dg[t], j, f, u, v, valid);
+            store_chunk<kNT>(vel_of(td), td.n, j, u);
+            store_chunk<kNT>(td.resid, td.n, j, v);
+        } else if (stream_mode) {
             load_v<kNT>(td, j, td.resid != nullptr, v, valid);
             if (td.resid) store_chunk<kNT>(td.resid, td.n, j, v);
         } else {
@@ -542,8 +605,9 @@ __global__ __launch_bounds__(kBlock) void topk_cand_scan(const TDesc* __restrict
     }
 }
 
-// Emit the winners of a chunk in index order and clear them in e_new, one
-// wave per chunk; ranks come from ballots.
+// Emit the winners of a chunk in index order and clear them in e_new (kDGC:
+// and in u), one wave per chunk; ranks come from ballots.
+template <bool kDGC>
 __global__ __launch_bounds__(kBlock) void topk_emit(const TDesc* __restrict__ d, int T, uint32_t C,
                                                     uint32_t* __restrict__ idx,
                                                     float* __restrict__ val, Ws ws) {
@@ -578,6 +642,7 @@ __global__ __launch_bounds__(kBlock) void topk_emit(const TDesc* __restrict__ d,
                 idx[at] = e.x;
                 val[at] = u2f(e.y);
                 if (resid) gp(resid)[e.x] = 0.f;
+                if constexpr (kDGC) gp(vel_of(d[t]))[e.x] = 0.f;
             }
             eq_seen += (uint64_t)__popcll(meq);
             pos += (uint64_t)__popcll(msel);
@@ -810,7 +875,8 @@ __global__ __launch_bounds__(kBlock) void topk_fast_digit2(const TDesc* __restri
 }
 
 // Digit 2 gives tau; one wave per chunk counts, looks back, and emits its
-// winners in index order (clearing them in e_new).
+// winners in index order (clearing them in e_new; kDGC: and in u).
+template <bool kDGC>
 __global__ __launch_bounds__(kBlock) void topk_fast_emit(const TDesc* __restrict__ d, int T, uint32_t C, int copies,
                                                          uint32_t* __restrict__ idx, float* __restrict__ val,
                                                          Ws ws) {
@@ -910,6 +976,7 @@ __global__ __launch_bounds__(kBlock) void topk_fast_emit(const TDesc* __restrict
             idx[at] = e.x;
             val[at] = u2f(e.y);
             if (resid) gp(resid)[e.x] = 0.f;
+            if constexpr (kDGC) gp(vel_of(td))[e.x] = 0.f;
         }
         eq_seen += (uint64_t)__popcll(meq);
         pos += (uint64_t)__popcll(msel);
@@ -925,21 +992,25 @@ __global__ void topk_zero_hist(uint32_t* h, uint64_t n, uint32_t* any) {
     if (blockIdx.x == 0 && threadIdx.x == 0) any[0] = 0u;
 }
 
-hipError_t launch_topk(int kind, double ratio, uint64_t seed, const TDesc* d, int T, uint32_t C,
-                       bool, bool, uint32_t* idx, float* val, const Ws& ws, hipStream_t s) {
-    if (C == 0) return hipSuccess;
+namespace {
+
+template <bool kDGC>
+hipError_t launch_topk_t(int kind, double ratio, uint64_t seed, const TDesc* d, int T, uint32_t C,
+                         uint32_t* idx, float* val, const Ws& ws, hipStream_t s, const DgcFuse& f) {
     const dim3 blk(kBlock);
+    const DgcFuse none{nullptr, 0.f, nullptr};
     if (C <= topk_few_chunks_limit()) {  // few chunks: the five-launch exact path (both kinds: same result)
         const int copies = few_copies(T);
         const uint64_t hn = (uint64_t)T * ((uint64_t)copies * kBins0 + 2 * kBins12);
         uint32_t zb = (uint32_t)((hn / 4 + 255) / 256);
         if (zb > 4096) zb = 4096;
         hipLaunchKernelGGL(topk_zero_hist, dim3(zb), dim3(256), 0, s, ws.t_hist, hn, ws.t_any);
-        (void)launch_timed(kTimedTopkHist, topk_hist_pass, dim3(C), blk, 0, s, d, T, C, 1, 0, ws, ws.t_off, copies);
+        (void)launch_timed(kTimedTopkHist, topk_hist_pass<kDGC>, dim3(C), blk, 0, s, d, T, C, 1, 0, ws, ws.t_off,
+                           copies, f);
         hipLaunchKernelGGL(topk_fast_compact, dim3(C), blk, 0, s, d, T, C, copies, ws);
         hipLaunchKernelGGL(topk_fast_digit2, dim3(C), blk, 0, s, d, T, copies, ws);
-        hipLaunchKernelGGL(topk_fast_emit, dim3((C + kBlock / 64 - 1) / (kBlock / 64)), blk, 0, s, d, T, C, copies,
-                           idx, val, ws);
+        hipLaunchKernelGGL(topk_fast_emit<kDGC>, dim3((C + kBlock / 64 - 1) / (kBlock / 64)), blk, 0, s, d, T, C,
+                           copies, idx, val, ws);
         return hipGetLastError();
     }
     const int R = topk_general_copies(T);
@@ -948,25 +1019,29 @@ hipError_t launch_topk(int kind, double ratio, uint64_t seed, const TDesc* d, in
     if (zb > 4096) zb = 4096;
     hipLaunchKernelGGL(topk_zero_hist, dim3(zb), dim3(256), 0, s, ws.t_hist, hn, ws.t_any);
     if (kind == 0) {  // exact
-        hipLaunchKernelGGL(topk_hist_pass, dim3(C), blk, 0, s, d, T, C, 1, 0, ws, (uint64_t*)nullptr, R);
+        hipLaunchKernelGGL(topk_hist_pass<kDGC>, dim3(C), blk, 0, s, d, T, C, 1, 0, ws, (uint64_t*)nullptr, R, f);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, T, ratio, (int)kFindThrExact, 0, R, ws);
-        (void)launch_timed(kTimedTopkCompact, topk_compact<false>, dim3(C), blk, 0, s, d, T, C, 0, 0, R, ws);
+        (void)launch_timed(kTimedTopkCompact, topk_compact<false, false>, dim3(C), blk, 0, s, d, T, C, 0, 0, R, ws,
+                           none);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, T, ratio, (int)kFindDigit0, 0, R, ws);
     } else {  // sampled threshold, exact fallback per tensor
-        hipLaunchKernelGGL(topk_sample_hist, dim3((C + kSampleChunksPerBlock - 1) / kSampleChunksPerBlock), blk,
-                           0, s, d, T, C, seed, R, ws);
+        hipLaunchKernelGGL(topk_sample_hist<kDGC>, dim3((C + kSampleChunksPerBlock - 1) / kSampleChunksPerBlock),
+                           blk, 0, s, d, T, C, seed, R, ws, f);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, T, ratio, (int)kFindThrSample, 0, R, ws);
         if (C > kNtChunks)
-            (void)launch_timed(kTimedTopkCompact, topk_compact<true>, dim3(C), blk, 0, s, d, T, C, 1, 0, R, ws);
+            (void)launch_timed(kTimedTopkCompact, topk_compact<true, kDGC>, dim3(C), blk, 0, s, d, T, C, 1, 0, R, ws,
+                               f);
         else
-            (void)launch_timed(kTimedTopkCompact, topk_compact<false>, dim3(C), blk, 0, s, d, T, C, 1, 0, R, ws);
+            (void)launch_timed(kTimedTopkCompact, topk_compact<false, kDGC>, dim3(C), blk, 0, s, d, T, C, 1, 0, R,
+                               ws, f);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, T, ratio, (int)kFindDigit0, 0, R, ws);
         // fallback passes: small grids that walk the chunks, and return at
-        // once when no tensor fell back (the usual case)
+        // once when no tensor fell back (the usual case); they re-read the
+        // stored v, so a DGC step needs nothing more here
         const dim3 fb_grid(C < 1024u ? C : 1024u);
-        hipLaunchKernelGGL(topk_hist_pass, fb_grid, blk, 0, s, d, T, C, 0, 1, ws, (uint64_t*)nullptr, R);
+        hipLaunchKernelGGL(topk_hist_pass<false>, fb_grid, blk, 0, s, d, T, C, 0, 1, ws, (uint64_t*)nullptr, R, none);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, T, ratio, (int)kFindThrExact, 1, R, ws);
-        hipLaunchKernelGGL(topk_compact<false>, fb_grid, blk, 0, s, d, T, C, 0, 1, R, ws);
+        hipLaunchKernelGGL((topk_compact<false, false>), fb_grid, blk, 0, s, d, T, C, 0, 1, R, ws, none);
         hipLaunchKernelGGL(topk_find, dim3(T), blk, 0, s, d, T, ratio, (int)kFindDigit0, 1, R, ws);
     }
     uint32_t span = C / 1024u;
@@ -981,8 +1056,18 @@ hipError_t launch_topk(int kind, double ratio, uint64_t seed, const TDesc* d, in
     else
         hipLaunchKernelGGL(topk_cand_count<1>, dim3((C + 3) / 4), blk, 0, s, d, T, C, ws);
     hipLaunchKernelGGL(topk_cand_scan, dim3(T), blk, 0, s, d, ws);
-    hipLaunchKernelGGL(topk_emit, dim3((C + kBlock / 64 - 1) / (kBlock / 64)), blk, 0, s, d, T, C, idx, val, ws);
+    hipLaunchKernelGGL(topk_emit<kDGC>, dim3((C + kBlock / 64 - 1) / (kBlock / 64)), blk, 0, s, d, T, C, idx, val,
+                       ws);
     return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_topk(int kind, double ratio, uint64_t seed, const TDesc* d, int T, uint32_t C,
+                       bool, bool, uint32_t* idx, float* val, const Ws& ws, hipStream_t s, const DgcFuse* dgc) {
+    if (C == 0) return hipSuccess;
+    if (dgc) return launch_topk_t<true>(kind, ratio, seed, d, T, C, idx, val, ws, s, *dgc);
+    return launch_topk_t<false>(kind, ratio, seed, d, T, C, idx, val, ws, s, DgcFuse{nullptr, 0.f, nullptr});
 }
 
 }  // namespace bc

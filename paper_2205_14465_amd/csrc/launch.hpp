@@ -153,9 +153,20 @@ constexpr uint32_t kNtChunks = 8192;
 hipError_t launch_sign_compress(const TDesc* d, int T, uint32_t C, uint32_t max_chunks, bool any_empty,
                                 bool any_f16, bool any_f32, uint32_t* bits, float* scale, const Ws& ws, int cus,
                                 hipStream_t s);
+// A DGC step folded into the top-k passes: the velocity step runs inside
+// the stream pass that forms v, the masking inside the emit pass.  The
+// call's table d then holds u (as the fp32 gradient) and e; dg holds the
+// step's gradients (same tensors, chunks and k); clip is the device
+// clipping factor or NULL.
+struct DgcFuse {
+    const TDesc* dg;
+    float m;
+    const float* clip;
+};
+// dgc: NULL for a plain call.
 hipError_t launch_topk(int kind, double ratio, uint64_t seed, const TDesc* d, int T, uint32_t C,
                        bool any_f16, bool any_f32, uint32_t* idx, float* val, const Ws& ws,
-                       hipStream_t s);
+                       hipStream_t s, const DgcFuse* dgc = nullptr);
 hipError_t launch_randk(uint64_t seed, const TDesc* d, int T, uint32_t C, uint64_t sum_k,
                         bool any_f16, bool any_f32, uint32_t* idx, float* val, const Ws& ws,
                         hipStream_t s);
@@ -186,6 +197,9 @@ hipError_t launch_quant_residual_update(int bits, const TDesc* d, int T, uint32_
 // factor_out[0]), then the step with the clipped gradient.
 hipError_t launch_dgc_momentum(const TDesc* d, int T, uint32_t C, float m, bool clipping, double clip,
                                double* part, float* factor, float* factor_out, hipStream_t s);
+// The clipping factor alone (for a step folded into the top-k passes).
+hipError_t launch_dgc_clip(const TDesc* d, int T, uint32_t C, double clip, double* part, float* factor,
+                           float* factor_out, hipStream_t s);
 hipError_t launch_dgc_mask(const TDesc* d, int T, const uint32_t* idx, uint64_t total, hipStream_t s);
 // units of kSignAggUnit elements; W <= 1024
 // info, tabs: the TernGrad exact form's per-tensor forms and tables (2-bit only).

@@ -150,3 +150,46 @@ def test_full_size_quant_workload(wid):
         n = wl.sizes[t]
         want = O.aggregate_quant(n, b, [x[off[t]:off[t + 1]] for x in p_bits], p_scale[:, t], alpha)
         assert np.array_equal(bits(outs[t].cpu().numpy()), bits(want)), t
+
+
+def test_full_size_dgc_workload():
+    """The DGC workload's tensor list (BERT-base, momentum 0.9 around the
+    sampled top-k at 1 %, W = 64) in the launch configuration the benchmark
+    times, with non-zero velocities: the sampled tensors' payloads,
+    residuals and velocities bit for bit against the oracle's DGC step;
+    every tensor's payload by its properties and its velocity +0.0 at its
+    payload's indices."""
+    import torch
+    from paper_2205_14465_amd import binding as B
+    wl = WL.workload(9)
+    dev = torch.device("cuda:0")
+    off = B.bytecomp_layout(wl.kind, wl.ratio, wl.sizes)
+    grads, resids, payloads, outs = WL.device_inputs(wl, off, dev)
+    del payloads, outs
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(909)
+    vels = [torch.randn(n, generator=gen, device=dev, dtype=torch.float32) * 0.01 for n in wl.sizes]
+    rng = np.random.default_rng(1009)
+    sample = _sample(wl, rng)
+    g_host = {t: grads[t].cpu().numpy() for t in sample}
+    e_host = {t: resids[t].cpu().numpy().copy() for t in sample}
+    u_host = {t: vels[t].cpu().numpy().copy() for t in sample}
+    own = B.alloc_payload(wl.kind, wl.ratio, wl.sizes, device=dev)
+    ws = B.alloc_workspace(wl.kind, wl.ratio, wl.sizes, wl.W, device=dev)
+    B.DgcCall(wl.kind, wl.ratio, wl.momentum, grads, resids, vels, own, ws,
+              stream=torch.cuda.current_stream())(WL.SEED)
+    torch.cuda.synchronize()
+    assert B.bytecomp_device_status(ws) == 0
+    _check_sparse_payload_properties(wl, off, own)
+    idx = own["idx"].cpu().numpy().view(np.uint32)
+    val = own["val"].cpu().numpy()
+    for t in sample:
+        wi, wv, we, wu = O.compress_dgc(wl.kind, g_host[t], e_host[t], u_host[t], wl.momentum, wl.ratio,
+                                        WL.SEED, t)
+        assert np.array_equal(idx[off[t]:off[t + 1]], wi), t
+        assert np.array_equal(bits(val[off[t]:off[t + 1]]), bits(wv)), t
+        assert np.array_equal(bits(resids[t].cpu().numpy()), bits(we)), t
+        assert np.array_equal(bits(vels[t].cpu().numpy()), bits(wu)), t
+    for t in range(wl.T):
+        sel = idx[off[t]:off[t + 1]].astype(np.int64)
+        assert np.all(bits(vels[t].cpu().numpy()[sel]) == 0), t

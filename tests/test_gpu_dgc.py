@@ -2,7 +2,11 @@
 compression with error feedback, momentum-factor masking; DGC is the
 paper's sparsification operator, Sec. 5.1) against the oracle, over two
 consecutive steps so that the velocity and residual states carry over.
-Payloads, residuals and velocities must match bit for bit."""
+Payloads, residuals and velocities must match bit for bit.  The top-k kinds
+fold the velocity step and the masking into their own passes; both of their
+launch sequences (the few-chunk path and the general pipeline) are run."""
+import contextlib
+
 import numpy as np
 import pytest
 
@@ -13,10 +17,28 @@ pytestmark = pytest.mark.gpu
 
 RAGGED = [0, 1, 3, 64, 1000, 4095, 4097, 3 * 4096 + 17, 65537, 140001]
 
+KIND_PATHS = [("topk", "few"), ("topk", "general"), ("topk_sampled", "few"), ("topk_sampled", "general"),
+              ("randk", "few")]
 
-@pytest.mark.parametrize("kind", ["topk", "topk_sampled", "randk"])
+
+@contextlib.contextmanager
+def topk_path(path):
+    from paper_2205_14465_amd import binding as B
+    B.bytecomp_set_topk_few_chunks(2048 if path == "few" else 0)
+    try:
+        yield
+    finally:
+        B.bytecomp_set_topk_few_chunks(2048)
+
+
+@pytest.mark.parametrize("kind,path", KIND_PATHS)
 @pytest.mark.parametrize("dtype", [np.float32, np.float16])
-def test_dgc_two_steps(kind, dtype):
+def test_dgc_two_steps(kind, path, dtype):
+    with topk_path(path):
+        _two_steps(kind, dtype)
+
+
+def _two_steps(kind, dtype):
     import torch
     from paper_2205_14465_amd import binding as B
     rng = np.random.default_rng(3 + (dtype == np.float16))
@@ -46,14 +68,19 @@ def test_dgc_two_steps(kind, dtype):
             assert np.array_equal(bits(du[t].cpu().numpy()), bits(u[t])), (step, t)
 
 
-@pytest.mark.parametrize("kind", ["topk", "topk_sampled", "randk"])
+@pytest.mark.parametrize("kind,path", KIND_PATHS)
 @pytest.mark.parametrize("dtype", [np.float32, np.float16])
-def test_dgc_clip_two_steps(kind, dtype):
+def test_dgc_clip_two_steps(kind, path, dtype):
     """Local gradient clipping: the factor within one fp32 place of the
     oracle's (the two add the fp64 squares in different orders); where the
     factors agree (the usual case), payloads, residuals and velocities bit
     for bit.  The first step clips (threshold below the norm), the second
     does not (threshold above it: factor exactly 1)."""
+    with topk_path(path):
+        _clip_two_steps(kind, dtype)
+
+
+def _clip_two_steps(kind, dtype):
     import torch
     from paper_2205_14465_amd import binding as B
     rng = np.random.default_rng(23 + (dtype == np.float16))
@@ -103,3 +130,40 @@ def test_dgc_clip_rejects_bad_threshold():
     for bad in (-1.0, float("nan")):
         with pytest.raises(B.BytecompError, match="BC_E_RATIO"):
             B.bytecomp_compress_dgc_clip("topk", 0.1, 1, 0.9, bad, g, e, u, out, ws)
+
+
+@pytest.mark.parametrize("ratio", [1.0, 0.5])
+def test_dgc_sampled_fallback_mixed(ratio):
+    """General pipeline, sampled kind: a tensor whose sample misses the k-th
+    key falls back to the exact path, which re-reads the v that the fused
+    stream pass stored (after the velocity step); beside it a tensor whose
+    values are mostly zero (threshold 0) and tensors below the sampling
+    size.  Two steps, so the masked velocities feed the second."""
+    import torch
+    from paper_2205_14465_amd import binding as B
+    rng = np.random.default_rng(41)
+    ns = [70000, 140001, 100, 5000]
+    m = 0.9
+    e = [(rng.standard_normal(n) * 1e-3).astype(np.float32) for n in ns]
+    u = [(rng.standard_normal(n) * 1e-2).astype(np.float32) for n in ns]
+    u[1][rng.random(ns[1]) < 0.3] = 0.0
+    e[1][u[1] == 0.0] = 0.0
+    de = [torch_dev(x) for x in e]
+    du = [torch_dev(x) for x in u]
+    out = B.alloc_payload("topk_sampled", ratio, ns)
+    ws = B.alloc_workspace("topk_sampled", ratio, ns, 1)
+    with topk_path("general"):
+        for step, seed in enumerate((5, 6)):
+            grads = [(rng.standard_normal(n) * 0.01).astype(np.float32) for n in ns]
+            grads[1][u[1] == 0.0] = 0.0
+            dg = [torch_dev(g) for g in grads]
+            B.bytecomp_compress_dgc("topk_sampled", ratio, seed, m, dg, de, du, out, ws)
+            torch.cuda.synchronize()
+            assert B.bytecomp_device_status(ws) == 0
+            want, e, u = O.compress_dgc_set("topk_sampled", ratio, seed, m, grads, e, u)
+            total = int(want["off"][-1])
+            assert np.array_equal(out["idx"].cpu().numpy().view(np.uint32)[:total], want["idx"]), step
+            assert np.array_equal(bits(out["val"].cpu().numpy()[:total]), bits(want["val"])), step
+            for t in range(len(ns)):
+                assert np.array_equal(bits(de[t].cpu().numpy()), bits(e[t])), (step, t)
+                assert np.array_equal(bits(du[t].cpu().numpy()), bits(u[t])), (step, t)

@@ -417,6 +417,21 @@ def main():
     ce[1].record(stream)
     torch.cuda.synchronize()
     copy_gbs = 5 * 2 * src.numel() * 4 / (ce[0].elapsed_time(ce[1]) * 1e-3) / 1e9
+    del src, dst
+    # the access pattern of the compress stream passes (read g and e, write
+    # e): a plain elementwise e += g over the workload's element count (at
+    # least 2^28 fp32, so that it streams from HBM)
+    n_add = max(1 << 28, wl.n_total)
+    src = torch.zeros(n_add, dtype=torch.float32, device=dev)
+    dst = torch.zeros_like(src)
+    dst.add_(src)
+    torch.cuda.synchronize()
+    ce[0].record(stream)
+    for _ in range(5):
+        dst.add_(src)
+    ce[1].record(stream)
+    torch.cuda.synchronize()
+    add_gbs = 5 * 12 * n_add / (ce[0].elapsed_time(ce[1]) * 1e-3) / 1e9
     del src, dst, flush_buf, flush_rd
 
     value = (comp_b + agg_b) / (step_avg * 1e-3) / 1e9
@@ -452,6 +467,8 @@ def main():
                 "aggregate_pct_peak": round(100 * agg_b / (agg_med * 1e-3) / 1e9 / HBM_PEAK_GBS, 2),
                 "kernels_ms_avg": {k: round(v["ms_avg"], 4) for k, v in kstats.items()}},
         "copy_gbs_reference": round(copy_gbs, 1),
+        "add_gbs_reference": round(add_gbs, 1),
+        "add_reference_elements": n_add,
         "roofline": {"bound": "hbm", "kernel": dom_kernel, "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "bytes_per_launch": dom["bytes"], "kernel_ms": round(dom["ms_avg"], 4)},

@@ -11,10 +11,14 @@
 // generating workgroup histograms its indices in LDS and writes one row of
 // per-bucket counts, a column pass and a scan give every workgroup its
 // position in every bucket, and a second pass places the indices there, so
-// no global atomics are used.  The streaming pass then takes one bucket per
-// workgroup: it marks the bucket's indices in an LDS bitmap, and for each
-// chunk zeroes them in e_new and emits (index, v) in index order, which is
-// the sorted payload.
+// no global atomics are used.  The generated indices wait in the payload's
+// index buffer (which the streaming pass overwrites in full) and are placed
+// into r_tmp.  The streaming pass then takes a run of 2^SP chunks of one
+// bucket per workgroup (SP <= S; several workgroups per bucket when the
+// indices are sparse enough that each rescanning the bucket's list is
+// cheap): it marks the run's indices in an LDS bitmap, and for each chunk
+// zeroes them in e_new and emits (index, v) in index order, which is the
+// sorted payload.
 #include "launch.hpp"
 #include "randk_perm.hpp"
 
@@ -75,7 +79,8 @@ __device__ __forceinline__ void entry_tensor_advance(const TDesc* __restrict__ d
 }
 
 // Generate the indices of kGenEntries consecutive payload entries, keep
-// them in r_tmp, and write this workgroup's row of bucket counts.  A thread
+// them in gen (the payload's index buffer), and write this workgroup's row
+// of bucket counts.  A thread
 // takes its entries in turn, but the cycle walks are not aligned across the
 // wave: every pass of the loop applies one Feistel evaluation per thread,
 // and a thread whose walk has landed in [0, n) records its index and starts
@@ -84,7 +89,8 @@ __device__ __forceinline__ void entry_tensor_advance(const TDesc* __restrict__ d
 // largest walk in the wave (walks take 1 to 4 evaluations on average and
 // have long tails).
 __global__ __launch_bounds__(kGenBlock) void randk_count(const TDesc* __restrict__ d, int T, uint64_t sum_k,
-                                                         uint32_t S, uint32_t NB, Ws ws) {
+                                                         uint32_t S, uint32_t NB, uint32_t* __restrict__ gen,
+                                                         Ws ws) {
     extern __shared__ uint32_t hist[];  // [NB]
     for (uint32_t b = threadIdx.x; b < NB; b += kGenBlock) hist[b] = 0;
     __syncthreads();
@@ -102,7 +108,7 @@ __global__ __launch_bounds__(kGenBlock) void randk_count(const TDesc* __restrict
         if (live) {
             const uint32_t x = feistel(cur, et.h, et.mask, et.rk);
             if (x < et.n) {
-                ws.r_tmp[j] = x;
+                gen[j] = x;
                 atomicAdd(&hist[(et.chunk0 + x / (uint32_t)kChunk) >> S], 1u);
                 ++q;
                 j += (uint64_t)kGenBlock;
@@ -194,12 +200,13 @@ __global__ __launch_bounds__(kBlock) void randk_scan_apply(uint32_t NB, Ws ws, c
     if (c0 < NB && c0 + 16 >= NB) ws.r_coff[NB] = run;  // the thread holding the last size
 }
 
-// Place each generated index in its bucket: the workgroup's position in the
-// bucket (payload start + column prefix) plus a rank taken in LDS.  The
-// value stored is the index's position within the bucket's 2^S chunks.
+// Place each generated index (gen, in generation order) in its bucket's
+// range of r_tmp: the workgroup's position in the bucket (payload start +
+// column prefix) plus a rank taken in LDS.  The value stored is the index's
+// position within the bucket's 2^S chunks.
 __global__ __launch_bounds__(kGenBlock) void randk_place(const TDesc* __restrict__ d, int T, uint64_t sum_k,
-                                                         uint32_t S, uint32_t NB, uint32_t* __restrict__ idx,
-                                                         Ws ws) {
+                                                         uint32_t S, uint32_t NB,
+                                                         const uint32_t* __restrict__ gen, Ws ws) {
     extern __shared__ uint32_t lds[];
     uint32_t* base = lds;       // [NB] this workgroup's first position in each bucket
     uint32_t* rank = lds + NB;  // [NB] entries placed so far
@@ -216,17 +223,19 @@ __global__ __launch_bounds__(kGenBlock) void randk_place(const TDesc* __restrict
         const uint64_t j = j0 + (uint64_t)q * kGenBlock;
         if (j >= sum_k) break;
         entry_tensor_advance(d, T, ws.r_keys, j, et);
-        const uint32_t x = ws.r_tmp[j];
+        const uint32_t x = gen[j];
         const uint32_t gc = et.chunk0 + x / (uint32_t)kChunk;
         const uint32_t b = gc >> S;
         const uint32_t pos = base[b] + atomicAdd(&rank[b], 1u);
-        idx[pos] = ((gc - (b << S)) << 12) | (x & (uint32_t)(kChunk - 1));
+        ws.r_tmp[pos] = ((gc - (b << S)) << 12) | (x & (uint32_t)(kChunk - 1));
     }
 }
 
-// One bucket per workgroup.  The bucket's indices are marked in an LDS
-// bitmap; per-chunk counts of the bitmap and their prefix give each chunk's
-// payload position.  Then every wave streams whole chunks on its own (no
+// A run of 2^SP chunks of one bucket per workgroup (the whole bucket when
+// SP = S).  The run's indices, read from the bucket's list, are marked in
+// an LDS bitmap, and the list's indices below the run are counted; these
+// and the per-chunk counts of the bitmap with their prefix give each
+// chunk's payload position.  Then every wave streams whole chunks on its own (no
 // workgroup barrier): lane l holds elements 256 r + 4 l + i (r < 16, i < 4)
 // of the chunk, writes e_new (selected entries zeroed) and emits its
 // selected (index, v) pairs at positions from a wave prefix over the
@@ -264,22 +273,41 @@ __device__ __forceinline__ void half_loads(const TDesc& td, uint32_t lo, int lan
 
 template <bool kNT>
 __global__ __launch_bounds__(kBlock) void randk_stream(const TDesc* __restrict__ d, int T, uint32_t C,
-                                                       uint32_t S, uint32_t* __restrict__ idx,
-                                                       float* __restrict__ val, Ws ws) {
-    extern __shared__ uint32_t bm[];  // [2^S * 128] bits of the bucket's chunks
+                                                       uint32_t S, uint32_t SP, uint32_t NB,
+                                                       uint32_t* __restrict__ idx, float* __restrict__ val,
+                                                       Ws ws) {
+    extern __shared__ uint32_t bm[];  // [2^SP * 128] bits of the run's chunks
     __shared__ uint32_t coff[(1u << kRandkMaxShift) + 1];
+    __shared__ uint32_t below_sh;
     const int lane = lane_id();
     const int wave = wave_id();
-    const uint32_t b = blockIdx.x;
-    const uint32_t c0 = b << S;
-    const uint32_t nc = (C - c0 < (1u << S)) ? C - c0 : (1u << S);
+    // the F runs of a bucket take workgroup ids congruent modulo 8 (one XCD,
+    // whose L2 then serves the bucket's list to all of them) and are
+    // dispatched within 8F ids of each other
+    const uint32_t F = 1u << (S - SP);
+    const uint32_t b = blockIdx.x / (8u * F) * 8u + blockIdx.x % 8u;
+    const uint32_t run = blockIdx.x / 8u % F;
+    if (b >= NB) return;
+    const uint32_t cb = b << S;
+    const uint32_t ncb = (C - cb < (1u << S)) ? C - cb : (1u << S);
+    const uint32_t s0 = run << SP;  // the run's first chunk within the bucket
+    if (s0 >= ncb) return;
+    const uint32_t nc = (ncb - s0 < (1u << SP)) ? ncb - s0 : (1u << SP);
+    const uint32_t c0 = cb + s0;
+    const uint32_t ylo = s0 << 12, yhi = (s0 + nc) << 12;
     const uint64_t beg = ws.r_coff[b], end = ws.r_coff[b + 1];
     for (uint32_t i = threadIdx.x; i < nc * (uint32_t)kChunkWords; i += kBlock) bm[i] = 0u;
+    if (threadIdx.x == 0) below_sh = 0u;
     __syncthreads();
+    uint32_t below = 0;
     for (uint64_t i = beg + threadIdx.x; i < end; i += kBlock) {
-        const uint32_t y = idx[i];
-        if (y < (nc << 12)) atomicOr(&bm[y >> 5], 1u << (y & 31));
+        const uint32_t y = ws.r_tmp[i];
+        if (y < ylo) ++below;
+        else if (y < yhi) atomicOr(&bm[(y - ylo) >> 5], 1u << (y & 31));
     }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) below += __shfl_xor(below, o, 64);
+    if (lane == 0 && below) atomicAdd(&below_sh, below);
     __syncthreads();
     // selected entries per chunk (one wave per chunk), then their prefix
     for (uint32_t q = (uint32_t)wave; q < nc; q += kBlock / 64) {
@@ -318,7 +346,7 @@ __global__ __launch_bounds__(kBlock) void randk_stream(const TDesc* __restrict__
         const TDesc td = d[tensor_of_chunk(d, T, c0 + q)];
         const uint32_t j = c0 + q - td.chunk0;
         const bool use_e = td.resid != nullptr;
-        uint64_t base = beg + coff[q];
+        uint64_t base = beg + below_sh + coff[q];
         // the chunk in two halves of 2048 elements, emitted in order
         for (uint32_t half = 0; half < 2; ++half) {
             const uint32_t lo = j * (uint32_t)kChunk + 2048u * half;
@@ -450,7 +478,15 @@ hipError_t launch_randk(uint64_t seed, const TDesc* d, int T, uint32_t C, uint64
     if (C == 0 || T == 0) return hipSuccess;
     uint32_t S, NB;
     if (!randk_buckets(C, &S, &NB) || sum_k >= (1ull << 32)) return hipErrorInvalidValue;
-    const size_t lds_place = (size_t)NB * 8, lds_stream = ((size_t)kChunkWords * 4) << S;
+    // runs of 2^SP chunks per stream workgroup: shorter runs balance the
+    // pass's end better (long-lived workgroups leave the chip part-idle
+    // while the last ones finish), but each of a bucket's 2^(S - SP)
+    // workgroups reads the whole bucket list, so runs are split only while
+    // those re-reads stay under an eighth of the 8 B-per-element input, at
+    // most 16 runs per bucket, and never below 4 chunks (one per wave)
+    uint32_t SP = S;
+    while (SP > 2 && S - SP < 4 && ((sum_k << (S - SP + 1)) * 4 <= (uint64_t)C * kChunk)) --SP;
+    const size_t lds_place = (size_t)NB * 8, lds_stream = ((size_t)kChunkWords * 4) << SP;
     {
         std::lock_guard<std::mutex> lk(g_lds_mu);
         hipError_t e = need_lds((const void*)randk_place, lds_place, g_lds_place);
@@ -464,18 +500,24 @@ hipError_t launch_randk(uint64_t seed, const TDesc* d, int T, uint32_t C, uint64
     hipLaunchKernelGGL(randk_prep, dim3((T + 255) / 256), dim3(256), 0, s, d, T, seed, ws);
     const uint32_t nblk = (uint32_t)((sum_k + kGenEntries - 1) / kGenEntries);
     if (nblk) {
-        hipLaunchKernelGGL(randk_count, dim3(nblk), dim3(kGenBlock), (size_t)NB * 4, s, d, T, sum_k, S, NB, ws);
+        hipLaunchKernelGGL(randk_count, dim3(nblk), dim3(kGenBlock), (size_t)NB * 4, s, d, T, sum_k, S, NB, idx,
+                           ws);
     }
     hipLaunchKernelGGL(randk_columns, dim3((NB + 63) / 64), dim3(kColBlock), 0, s, NB, nblk, ws);
     hipLaunchKernelGGL(randk_scan_sums, dim3(nscan), blk, 0, s, NB, ws, bsum);
     hipLaunchKernelGGL(randk_scan_apply, dim3(nscan), blk, 0, s, NB, ws, bsum);
     if (nblk)
-        hipLaunchKernelGGL(randk_place, dim3(nblk), dim3(kGenBlock), lds_place, s, d, T, sum_k, S, NB, idx, ws);
+        hipLaunchKernelGGL(randk_place, dim3(nblk), dim3(kGenBlock), lds_place, s, d, T, sum_k, S, NB,
+                           (const uint32_t*)idx, ws);
+    // ids in groups of 8F: 8 buckets' F runs each (a last group may hold
+    // fewer buckets: its surplus workgroups return at once)
+    const uint32_t F = 1u << (S - SP);
+    const dim3 sgrid((NB + 7) / 8 * 8 * F);
     if (C > kNtChunks)
-        return launch_timed(kTimedRandkStream, randk_stream<true>, dim3(NB), blk, lds_stream, s, d, T, C, S, idx,
-                            val, ws);
-    return launch_timed(kTimedRandkStream, randk_stream<false>, dim3(NB), blk, lds_stream, s, d, T, C, S, idx, val,
-                        ws);
+        return launch_timed(kTimedRandkStream, randk_stream<true>, sgrid, blk, lds_stream, s, d, T, C, S, SP, NB,
+                            idx, val, ws);
+    return launch_timed(kTimedRandkStream, randk_stream<false>, sgrid, blk, lds_stream, s, d, T, C, S, SP, NB, idx,
+                        val, ws);
 }
 
 }  // namespace bc

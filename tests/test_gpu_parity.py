@@ -198,6 +198,26 @@ def test_randk_many_chunks(T, ratio):
     assert_resid_equal(got_e, want_e)
 
 
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("case", ["small_tensors", "large_tensors"])
+def test_randk_bucket_split_into_runs(case):
+    """Calls of more than 32768 chunks at a 1 % rate: each bucket of 2^S
+    chunks is streamed by several workgroups, each taking a run of 4 chunks
+    of it (40000 one-chunk tensors: buckets of 8 chunks in 2 runs; about
+    296 M elements in five tensors: buckets of 16 chunks in 4 runs)."""
+    rng = np.random.default_rng(61 if case == "small_tensors" else 62)
+    if case == "small_tensors":
+        ns = [int(x) for x in rng.integers(1, 4097, size=40000)]
+        ns[123] = 0
+    else:
+        ns = [40_000_000, 33_554_432 + 5, 77, 4096 * 30000 + 1, 100_000_000]
+    grads, resids = make_set(ns, rng)
+    got, got_e = gpu_compress("randk", 0.01, SEED + 5, grads, resids)
+    want, want_e = O.compress_set("randk", 0.01, SEED + 5, grads, resids)
+    assert_sparse_equal(got, want, ns)
+    assert_resid_equal(got_e, want_e)
+
+
 def test_randk_tensor_id_keys_the_stream():
     rng = np.random.default_rng(15)
     ns = [50000, 50000]

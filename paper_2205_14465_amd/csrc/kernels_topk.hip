@@ -133,9 +133,11 @@ __global__ __launch_bounds__(kBlock) void topk_hist_pass(const TDesc* __restrict
 // Seeded sample: each 4096-element chunk of a tensor larger than
 // kAllCandidatesBelow contributes one run of 64 consecutive elements with
 // probability 0.64 (an expected 1% of the tensor).  A workgroup covers 16
-// consecutive chunks, one wave per chunk in turn; when they all belong to
-// one tensor (the usual case) the keys are binned in LDS first so the
-// global histogram sees one atomic per non-empty bin.
+// consecutive chunks, four per wave: lanes 0..3 of a wave draw its four
+// chunks' runs at once, then the wave issues the four runs' loads together;
+// when the 16 chunks all belong to one tensor (the usual case) the keys
+// are binned in LDS first so the global histogram sees one atomic per
+// non-empty bin.
 constexpr uint32_t kSampleChunksPerBlock = 16;
 
 template <bool kDGC>
@@ -152,38 +154,57 @@ __global__ __launch_bounds__(kBlock) void topk_sample_hist(const TDesc* __restri
     if (same)
         for (int b = threadIdx.x; b < kBins0; b += kBlock) lh[b] = 0;
     __syncthreads();
-    for (uint32_t c = c0 + (threadIdx.x >> 6); c < c1; c += 4) {
-        const int t = tensor_of_chunk(d, T, c);
-        const TDesc td = d[t];
-        if (td.n < kAllCandidatesBelow) continue;
-        const uint32_t j = c - td.chunk0;
-        U64x4 ctr = {{(uint64_t)td.tid, (uint64_t)j, 0, 0}};
-        const U64x4 r = philox4x64_10(ctr, seed, kStreamSample);
-        const uint32_t u = (uint32_t)(r.v[0] >> 32);
-        if (u >= 2748779069u) continue;  // 0.64 * 2^32
-        const uint32_t len = (j + 1 == td.nchunks) ? td.n - j * (uint32_t)kChunk : (uint32_t)kChunk;
-        if (len < 64) continue;
-        const uint32_t start = j * (uint32_t)kChunk + (uint32_t)(r.v[1] % (uint64_t)(len - 63));
-        const uint32_t i = start + lane_id();
-        float v;
+    const int lane = lane_id();
+    // lane q < 4: the run of chunk c0 + wave + 4q (start element, tensor; -1: none)
+    uint32_t run_start = 0;
+    int run_t = -1;
+    if (lane < 4) {
+        const uint32_t c = c0 + (uint32_t)wave_id() + 4u * (uint32_t)lane;
+        if (c < c1) {
+            const int t = tensor_of_chunk(d, T, c);
+            const TDesc td = d[t];
+            const uint32_t j = c - td.chunk0;
+            U64x4 ctr = {{(uint64_t)td.tid, (uint64_t)j, 0, 0}};
+            const U64x4 r = philox4x64_10(ctr, seed, kStreamSample);
+            const uint32_t u = (uint32_t)(r.v[0] >> 32);
+            const uint32_t len = (j + 1 == td.nchunks) ? td.n - j * (uint32_t)kChunk : (uint32_t)kChunk;
+            if (td.n >= kAllCandidatesBelow && u < 2748779069u && len >= 64) {  // 0.64 * 2^32
+                run_start = j * (uint32_t)kChunk + (uint32_t)(r.v[1] % (uint64_t)(len - 63));
+                run_t = t;
+            }
+        }
+    }
+    float v[4];
+    int tq[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        tq[q] = __builtin_amdgcn_readlane(run_t, q);
+        v[q] = 0.f;
+        if (tq[q] < 0) continue;
+        const uint32_t i = (uint32_t)__builtin_amdgcn_readlane((int)run_start, q) + (uint32_t)lane;
+        const TDesc td = d[tq[q]];
         if constexpr (kDGC) {  // the value the stream pass will form
-            const TDesc tg = f.dg[t];
+            const TDesc tg = f.dg[tq[q]];
             float g;
             if (tg.dtype == 0) g = gp((const float*)tg.grad)[i];
             else g = h2f(gp((const uint16_t*)tg.grad)[i]);
             if (f.clip) g = *f.clip * g;
             const float mu = f.m * gp((const float*)td.grad)[i];
-            const float u = mu + g;
-            v = u + gp(td.resid)[i];
+            const float uu = mu + g;
+            v[q] = uu + gp(td.resid)[i];
         } else {
             float g;
             if (td.dtype == 0) g = gp((const float*)td.grad)[i];
             else g = h2f(gp((const uint16_t*)td.grad)[i]);
-            v = td.resid ? g + gp(td.resid)[i] : g;
+            v[q] = td.resid ? g + gp(td.resid)[i] : g;
         }
-        const uint32_t bin = key_of(v) >> 20;
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        if (tq[q] < 0) continue;
+        const uint32_t bin = key_of(v[q]) >> 20;
         if (same) atomicAdd(&lh[bin], 1u);
-        else atomicAdd(gh0 + (size_t)t * kBins0 + bin, 1u);
+        else atomicAdd(gh0 + (size_t)tq[q] * kBins0 + bin, 1u);
     }
     if (!same) return;
     __syncthreads();

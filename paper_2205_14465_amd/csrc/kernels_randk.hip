@@ -271,7 +271,9 @@ __device__ __forceinline__ void half_loads(const TDesc& td, uint32_t lo, int lan
 }
 }  // namespace
 
-template <bool kNT>
+// kHalves (runs of at most 2 chunks): each wave takes half a chunk, so that
+// all four waves have work; else each wave takes whole chunks.
+template <bool kNT, bool kHalves>
 __global__ __launch_bounds__(kBlock) void randk_stream(const TDesc* __restrict__ d, int T, uint32_t C,
                                                        uint32_t S, uint32_t SP, uint32_t NB,
                                                        uint32_t* __restrict__ idx, float* __restrict__ val,
@@ -342,13 +344,23 @@ __global__ __launch_bounds__(kBlock) void randk_stream(const TDesc* __restrict__
         }
     }
     __syncthreads();
-    for (uint32_t q = (uint32_t)wave; q < nc; q += kBlock / 64) {
+    const uint32_t units = kHalves ? 2 * nc : nc;
+    for (uint32_t unit = (uint32_t)wave; unit < units; unit += kBlock / 64) {
+        const uint32_t q = kHalves ? unit >> 1 : unit;
         const TDesc td = d[tensor_of_chunk(d, T, c0 + q)];
         const uint32_t j = c0 + q - td.chunk0;
         const bool use_e = td.resid != nullptr;
         uint64_t base = beg + below_sh + coff[q];
-        // the chunk in two halves of 2048 elements, emitted in order
-        for (uint32_t half = 0; half < 2; ++half) {
+        if (kHalves && (unit & 1u)) {  // the second half: after the first half's entries
+            uint32_t n0 = __popc(bm[q * (uint32_t)kChunkWords + lane]);
+#pragma unroll
+            for (int o = 32; o >= 1; o >>= 1) n0 += __shfl_xor(n0, o, 64);
+            base += n0;
+        }
+        // the chunk in two halves of 2048 elements, emitted in order (kHalves:
+        // this unit's half only)
+        for (uint32_t h = 0; h < (kHalves ? 1u : 2u); ++h) {
+            const uint32_t half = kHalves ? (unit & 1u) : h;
             const uint32_t lo = j * (uint32_t)kChunk + 2048u * half;
             float v[32];
             uint32_t valid = 0;
@@ -482,16 +494,18 @@ hipError_t launch_randk(uint64_t seed, const TDesc* d, int T, uint32_t C, uint64
     // pass's end better (long-lived workgroups leave the chip part-idle
     // while the last ones finish), but each of a bucket's 2^(S - SP)
     // workgroups reads the whole bucket list, so runs are split only while
-    // those re-reads stay under an eighth of the 8 B-per-element input, at
-    // most 16 runs per bucket, and never below 4 chunks (one per wave)
+    // those re-reads stay under a quarter of the 8 B-per-element input, at
+    // most 32 runs per bucket, and never below 2 chunks (half a chunk per
+    // wave)
     uint32_t SP = S;
-    while (SP > 2 && S - SP < 4 && ((sum_k << (S - SP + 1)) * 4 <= (uint64_t)C * kChunk)) --SP;
+    while (SP > 1 && S - SP < 5 && ((sum_k << (S - SP + 1)) * 4 <= (uint64_t)C * kChunk * 2)) --SP;
     const size_t lds_place = (size_t)NB * 8, lds_stream = ((size_t)kChunkWords * 4) << SP;
     {
         std::lock_guard<std::mutex> lk(g_lds_mu);
         hipError_t e = need_lds((const void*)randk_place, lds_place, g_lds_place);
-        if (e == hipSuccess) e = need_lds((const void*)randk_stream<false>, lds_stream, g_lds_stream);
-        if (e == hipSuccess) e = need_lds((const void*)randk_stream<true>, lds_stream, g_lds_stream_nt);
+        // (runs of more than 2 chunks: 2^SP * 512 bytes, at most 128 KiB)
+        if (e == hipSuccess) e = need_lds((const void*)randk_stream<false, false>, lds_stream, g_lds_stream);
+        if (e == hipSuccess) e = need_lds((const void*)randk_stream<true, false>, lds_stream, g_lds_stream_nt);
         if (e != hipSuccess) return e;
     }
     const dim3 blk(kBlock);
@@ -513,11 +527,9 @@ hipError_t launch_randk(uint64_t seed, const TDesc* d, int T, uint32_t C, uint64
     // fewer buckets: its surplus workgroups return at once)
     const uint32_t F = 1u << (S - SP);
     const dim3 sgrid((NB + 7) / 8 * 8 * F);
-    if (C > kNtChunks)
-        return launch_timed(kTimedRandkStream, randk_stream<true>, sgrid, blk, lds_stream, s, d, T, C, S, SP, NB,
-                            idx, val, ws);
-    return launch_timed(kTimedRandkStream, randk_stream<false>, sgrid, blk, lds_stream, s, d, T, C, S, SP, NB, idx,
-                        val, ws);
+    const auto kern = C > kNtChunks ? (SP <= 1 ? randk_stream<true, true> : randk_stream<true, false>)
+                                     : (SP <= 1 ? randk_stream<false, true> : randk_stream<false, false>);
+    return launch_timed(kTimedRandkStream, kern, sgrid, blk, lds_stream, s, d, T, C, S, SP, NB, idx, val, ws);
 }
 
 }  // namespace bc

@@ -202,9 +202,10 @@ def test_randk_many_chunks(T, ratio):
 @pytest.mark.parametrize("case", ["small_tensors", "large_tensors"])
 def test_randk_bucket_split_into_runs(case):
     """Calls of more than 32768 chunks at a 1 % rate: each bucket of 2^S
-    chunks is streamed by several workgroups, each taking a run of 4 chunks
-    of it (40000 one-chunk tensors: buckets of 8 chunks in 2 runs; about
-    296 M elements in five tensors: buckets of 16 chunks in 4 runs)."""
+    chunks is streamed by several workgroups, each taking a run of 2 chunks
+    of it, half a chunk per wave (40000 one-chunk tensors: buckets of 8
+    chunks in 4 runs; about 296 M elements in five tensors: buckets of 16
+    chunks in 8 runs)."""
     rng = np.random.default_rng(61 if case == "small_tensors" else 62)
     if case == "small_tensors":
         ns = [int(x) for x in rng.integers(1, 4097, size=40000)]

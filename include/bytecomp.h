@@ -375,6 +375,24 @@ int bytecomp_plan_enumerate(int T, const double* compute_us, const uint64_t* sta
  * version sets one (bit 0 is reserved). */
 int bytecomp_device_status(void* ws, size_t ws_bytes, void* stream, uint32_t* flags);
 
+/* Selection statistics of the last top-k compress call on this workspace
+ * (BC_TOPK or BC_TOPK_SAMPLED; the call's kind, ratio and tensor sizes
+ * given again, no other call on the workspace since, and the path choice of
+ * bytecomp_set_topk_few_chunks unchanged), read synchronously on `stream`:
+ *   candidates  entries the exact selection examined, summed over the
+ *               tensors: those at or above each tensor's candidate
+ *               threshold (the sampled threshold, or for BC_TOPK and after
+ *               a fallback the bin of the k-th key); at least the sum of
+ *               the k_t, at most the sum of the n_t
+ *   fallbacks   tensors whose sampled threshold left fewer than k_t
+ *               candidates, so that they took the exact histogram path
+ *               (0 for BC_TOPK and on the few-chunk path)
+ * For monitoring and tuning (DGC's sampling); results never depend on it.
+ * BC_E_KIND for other kinds, BC_E_WORKSPACE when ws is smaller than the
+ * call's workspace, other argument errors as bytecomp_workspace_size. */
+int bytecomp_topk_stats(int kind, double ratio, const uint64_t* n, int T, const void* ws, size_t ws_bytes,
+                        void* stream, uint64_t* candidates, uint32_t* fallbacks);
+
 /* Wait limit of the one-pass compress kernels (BC_SIGN1 and the quantizers
  * when every tensor fits the GPU's resident grid), process-wide.  Their
  * workgroups defer each chunk's residual (and codes) until the tensor's

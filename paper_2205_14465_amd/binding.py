@@ -95,6 +95,9 @@ def lib():
         L.bytecomp_residual_update.argtypes = [i32, dbl, ctypes.POINTER(bc_tensor), i32, bc_payload, vp]
         L.bytecomp_device_status.restype = i32
         L.bytecomp_device_status.argtypes = [vp, sz, vp, ctypes.POINTER(ctypes.c_uint32)]
+        L.bytecomp_topk_stats.restype = i32
+        L.bytecomp_topk_stats.argtypes = [i32, dbl, vp, i32, vp, sz, vp, ctypes.POINTER(ctypes.c_uint64),
+                                          ctypes.POINTER(ctypes.c_uint32)]
         L.bytecomp_pack_part.restype = i32
         L.bytecomp_pack_part.argtypes = [i32, dbl, vp, i32, bc_payload, i32, vp, i32, bc_payload, vp, vp]
         L.bytecomp_aggregate_part.restype = i32
@@ -371,6 +374,20 @@ def bytecomp_device_status(ws, stream=None):
            lib().bytecomp_device_status(_ptr(ws), ws.numel() * ws.element_size(), _stream_handle(stream),
                                         ctypes.byref(f)))
     return int(f.value)
+
+
+def bytecomp_topk_stats(kind, ratio, sizes, ws, stream=None):
+    """(candidates, fallbacks) of the last top-k compress call of this shape
+    on the workspace ws (a device tensor, or None for calls of empty
+    tensors only)."""
+    n = (ctypes.c_uint64 * max(len(sizes), 1))(*[int(x) for x in sizes])
+    cand = ctypes.c_uint64(0)
+    fb = ctypes.c_uint32(0)
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check("bytecomp_topk_stats",
+           lib().bytecomp_topk_stats(_kind(kind), float(ratio), n, len(sizes), _ptr(ws), ws_bytes,
+                                     _stream_handle(stream), ctypes.byref(cand), ctypes.byref(fb)))
+    return int(cand.value), int(fb.value)
 
 
 # ---------------------------------------------------------- prepared calls

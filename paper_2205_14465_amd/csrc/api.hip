@@ -934,6 +934,50 @@ int bytecomp_set_topk_few_chunks(uint32_t chunks) {
     return BC_OK;
 }
 
+int bytecomp_topk_stats(int kind, double ratio, const uint64_t* n, int T, const void* ws, size_t ws_bytes,
+                        void* stream, uint64_t* candidates, uint32_t* fallbacks) {
+    uint64_t ppm;
+    int rc = check_kind_ratio(kind, ratio, ppm);
+    if (rc) return rc;
+    if (kind != BC_TOPK && kind != BC_TOPK_SAMPLED) return BC_E_KIND;
+    if (T < 0 || T > kMaxT) return BC_E_COUNT;
+    if (!candidates || !fallbacks || (T > 0 && !n)) return BC_E_NULL;
+    *candidates = 0;
+    *fallbacks = 0;
+    uint64_t C = 0, sk = 0;
+    for (int t = 0; t < T; ++t) {
+        if (n[t] >= kMaxN) return BC_E_SIZE;
+        C += (n[t] + kChunk - 1) / kChunk;
+        sk += k_of(n[t], ppm);
+    }
+    if (C == 0) return BC_OK;
+    if (!ws) return BC_E_NULL;
+    const WsPlan plan = plan_workspace(kind, T, C, sk);
+    if (ws_bytes < plan.total) return BC_E_WORKSPACE;
+    std::vector<uint32_t> cc, fb;
+    try {
+        cc.resize((size_t)C);
+        fb.resize((size_t)T);
+    } catch (const std::bad_alloc&) {
+        return BC_E_SIZE;
+    }
+    hipStream_t s = (hipStream_t)stream;
+    const char* base = (const char*)ws;
+    hipError_t e = hipMemcpyAsync(cc.data(), base + plan.t_ccount, (size_t)C * 4, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(fb.data(), base + plan.t_fb, (size_t)T * 4, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return BC_E_HIP;
+    uint64_t cand = 0;
+    for (uint32_t x : cc) cand += x;
+    uint32_t nfb = 0;
+    // the few-chunk path keeps another per-tensor value in t_fb
+    if (kind == BC_TOPK_SAMPLED && C > topk_few_chunks_limit())
+        for (uint32_t x : fb) nfb += x != 0u;
+    *candidates = cand;
+    *fallbacks = nfb;
+    return BC_OK;
+}
+
 int bytecomp_device_status(void* ws, size_t ws_bytes, void* stream, uint32_t* flags) {
     if (!ws || !flags) return BC_E_NULL;
     if (ws_bytes < 256) return BC_E_WORKSPACE;

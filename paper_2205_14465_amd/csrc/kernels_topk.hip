@@ -277,7 +277,8 @@ __global__ __launch_bounds__(kBlock) void topk_find(const TDesc* __restrict__ d,
             }
             return;
         }
-        if (threadIdx.x == 0) ws.t_fb[t] = 0u;
+        // a tensor that fell back keeps its flag (bytecomp_topk_stats counts them)
+        if (threadIdx.x == 0 && !fb_only) ws.t_fb[t] = 0u;
     } else {
         target = ws.t_krem[t];
     }

@@ -131,6 +131,31 @@ def test_argument_errors():
     assert L.bytecomp_residual_update(0, 0.01, t, 1, pay, None) == -1
 
 
+def test_topk_stats_argument_errors():
+    """bytecomp_topk_stats checks its arguments before any device work; a
+    call of empty tensors needs no workspace and reports zeros."""
+    L = B.lib()
+    n = (ctypes.c_uint64 * 2)(100, 5000)
+    cand = ctypes.c_uint64(7)
+    fb = ctypes.c_uint32(7)
+    ws = ctypes.c_void_p(0x5000)
+    args = (ctypes.byref(cand), ctypes.byref(fb))
+    assert L.bytecomp_topk_stats(B.KIND["sign"], 0.01, n, 2, ws, 1 << 30, None, *args) == -2
+    assert L.bytecomp_topk_stats(B.KIND["randk"], 0.01, n, 2, ws, 1 << 30, None, *args) == -2
+    assert L.bytecomp_topk_stats(9, 0.01, n, 2, ws, 1 << 30, None, *args) == -2
+    assert L.bytecomp_topk_stats(B.KIND["topk"], 0.0, n, 2, ws, 1 << 30, None, *args) == -4
+    assert L.bytecomp_topk_stats(B.KIND["topk"], 0.01, n, -1, ws, 1 << 30, None, *args) == -6
+    assert L.bytecomp_topk_stats(B.KIND["topk"], 0.01, None, 2, ws, 1 << 30, None, *args) == -1
+    assert L.bytecomp_topk_stats(B.KIND["topk"], 0.01, n, 2, ws, 1 << 30, None, None, ctypes.byref(fb)) == -1
+    assert L.bytecomp_topk_stats(B.KIND["topk"], 0.01, n, 2, None, 1 << 30, None, *args) == -1
+    assert L.bytecomp_topk_stats(B.KIND["topk_sampled"], 0.01, n, 2, ws, 64, None, *args) == -7
+    big = (ctypes.c_uint64 * 1)(1 << 32)
+    assert L.bytecomp_topk_stats(B.KIND["topk"], 0.01, big, 1, ws, 1 << 30, None, *args) == -5
+    empty = (ctypes.c_uint64 * 2)(0, 0)
+    assert L.bytecomp_topk_stats(B.KIND["topk"], 0.01, empty, 2, None, 0, None, *args) == 0
+    assert (cand.value, fb.value) == (0, 0)
+
+
 def test_noalloc_compress_checks_before_any_device_work():
     """The allocation-free compress refuses calls past its 16 MiB device
     array, and bad arguments, on the host: checked without a GPU."""

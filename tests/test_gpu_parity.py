@@ -14,7 +14,7 @@ import pytest
 import oracle as O
 from tests.exact_ref import same_f32_arrays
 from tests.helpers import (_first_diff, assert_resid_equal, assert_sign_close, assert_sparse_equal, bits,
-                           gpu_aggregate, gpu_compress)
+                           gpu_aggregate, gpu_compress, torch_dev)
 from paper_2205_14465_amd import workloads as WL
 
 pytestmark = pytest.mark.gpu
@@ -139,6 +139,57 @@ def test_sampled_fallback_mixed_with_kept_candidates(general_path):
         want, want_e = O.compress_set("topk", ratio, SEED, grads, resids)
         assert_sparse_equal(got, want, ns)
         assert_resid_equal(got_e, want_e)
+
+
+def _stats_after(kind, ratio, grads, resids):
+    import torch
+    from paper_2205_14465_amd import binding as B
+    ns = [g.size for g in grads]
+    out = B.alloc_payload(kind, ratio, ns)
+    ws = B.alloc_workspace(kind, ratio, ns, 1)
+    B.bytecomp_compress(kind, ratio, SEED, [torch_dev(g) for g in grads],
+                        [torch_dev(np.asarray(e, np.float32)) for e in resids], out, ws)
+    torch.cuda.synchronize()
+    return B.bytecomp_topk_stats(kind, ratio, ns, ws)
+
+
+@pytest.mark.parametrize("path", ["few", "general"])
+def test_topk_stats_exact_kind(path):
+    """bytecomp_topk_stats after an exact top-k call: no fallbacks, and the
+    candidates are the entries whose key (|v| bits) lies in the bin of the
+    k-th key (bits 30..20) or above, counted here from v = g + e."""
+    from paper_2205_14465_amd import binding as B
+    rng = np.random.default_rng(37)
+    ns = [5000, 70000, 140001, 3]
+    grads, resids = make_set(ns, rng)
+    B.bytecomp_set_topk_few_chunks(2048 if path == "few" else 0)
+    try:
+        cand, fb = _stats_after("topk", 0.01, grads, resids)
+    finally:
+        B.bytecomp_set_topk_few_chunks(2048)
+    want = 0
+    for g, e in zip(grads, resids):
+        v = g.astype(np.float32) + e
+        key = v.view(np.uint32) & np.uint32(0x7FFFFFFF)
+        k = O.k_for(v.size, 0.01)
+        b0 = np.sort(key)[::-1][k - 1] >> np.uint32(20)
+        want += int(np.count_nonzero((key >> np.uint32(20)) >= b0))
+    assert fb == 0
+    assert cand == want
+
+
+def test_topk_stats_sampled_kind(general_path):
+    """Sampled top-k: at ratio 1 the sample leaves fewer than k candidates in
+    both tensors, which fall back and examine every element; at 1 % none
+    falls back and the candidates lie between the k_t and the n_t."""
+    rng = np.random.default_rng(13)
+    ns = [70000, 140001]
+    grads, resids = make_set(ns, rng)
+    cand, fb = _stats_after("topk_sampled", 1.0, grads, resids)
+    assert (cand, fb) == (sum(ns), 2)
+    cand, fb = _stats_after("topk_sampled", 0.01, grads, resids)
+    assert fb == 0
+    assert sum(O.k_for(n, 0.01) for n in ns) <= cand <= sum(ns)
 
 
 @pytest.mark.parametrize("kind", ["topk", "topk_sampled"])

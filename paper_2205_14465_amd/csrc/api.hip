@@ -604,56 +604,36 @@ int compress_dgc_impl(int kind, double ratio, uint64_t seed, float momentum, boo
     const Ws w = carve_workspace(ws, plan);
     hipStream_t s = (hipStream_t)stream;
     hipError_t e;
-    if (kind == BC_TOPK || kind == BC_TOPK_SAMPLED) {
-        // the velocity step and the masking inside the top-k passes: dc
-        // (u in the gradient's place, e) drives them, dm supplies g
-        std::lock_guard<std::mutex> lk(g_mu);
-        Entry* em = nullptr;
-        Entry* ec = nullptr;
-        e = cache_get(dm.data(), dm.size() * sizeof(TDesc), (size_t)C * 4,
-                      [&](void* dst) { fill_chunk_map(dm, (uint32_t*)dst); }, s, &em);
-        if (e != hipSuccess) return BC_E_HIP;
-        if (clipping) {
-            e = launch_dgc_clip((const TDesc*)em->dev, T, C, clip_norm, w.d_part, w.d_factor, clip_factor, s);
-            if (e != hipSuccess) {
-                cache_mark_used(em, s);
-                return BC_E_HIP;
-            }
-        }
-        // the newest entry is never the one a miss replaces, so em stays valid
-        e = cache_get(dc.data(), dc.size() * sizeof(TDesc), (size_t)C2 * 4,
-                      [&](void* dst) { fill_chunk_map(dc, (uint32_t*)dst); }, s, &ec);
+    // the velocity step and the masking inside the compress passes: dc (u
+    // in the gradient's place, e) drives them, dm supplies g
+    std::lock_guard<std::mutex> lk(g_mu);
+    Entry* em = nullptr;
+    Entry* ec = nullptr;
+    e = cache_get(dm.data(), dm.size() * sizeof(TDesc), (size_t)C * 4,
+                  [&](void* dst) { fill_chunk_map(dm, (uint32_t*)dst); }, s, &em);
+    if (e != hipSuccess) return BC_E_HIP;
+    if (clipping) {
+        e = launch_dgc_clip((const TDesc*)em->dev, T, C, clip_norm, w.d_part, w.d_factor, clip_factor, s);
         if (e != hipSuccess) {
             cache_mark_used(em, s);
             return BC_E_HIP;
         }
-        const DgcFuse f{(const TDesc*)em->dev, momentum, clipping ? w.d_factor : nullptr};
+    }
+    // the newest entry is never the one a miss replaces, so em stays valid
+    e = cache_get(dc.data(), dc.size() * sizeof(TDesc), (size_t)C2 * 4,
+                  [&](void* dst) { fill_chunk_map(dc, (uint32_t*)dst); }, s, &ec);
+    if (e != hipSuccess) {
+        cache_mark_used(em, s);
+        return BC_E_HIP;
+    }
+    const DgcFuse f{(const TDesc*)em->dev, momentum, clipping ? w.d_factor : nullptr};
+    if (kind == BC_RANDK)
+        e = launch_randk(seed, (const TDesc*)ec->dev, T, C2, sum_k2, b16, b32, out.idx, out.val, w, s, &f);
+    else
         e = launch_topk(kind == BC_TOPK ? 0 : 1, ratio, seed, (const TDesc*)ec->dev, T, C2, b16, b32, out.idx,
                         out.val, w, s, &f);
-        cache_mark_used(em, s);
-        cache_mark_used(ec, s);
-        return finish(hip_status(e), s, ws);
-    }
-    {
-        std::lock_guard<std::mutex> lk(g_mu);
-        Entry* en = nullptr;
-        e = cache_get(dm.data(), dm.size() * sizeof(TDesc), (size_t)C * 4,
-                      [&](void* dst) { fill_chunk_map(dm, (uint32_t*)dst); }, s, &en);
-        if (e != hipSuccess) return BC_E_HIP;
-        e = launch_dgc_momentum((const TDesc*)en->dev, T, C, momentum, clipping, clip_norm, w.d_part, w.d_factor,
-                                clip_factor, s);
-        cache_mark_used(en, s);
-        if (e != hipSuccess) return BC_E_HIP;
-    }
-    rc = bytecomp_compress(kind, ratio, seed, tc.data(), T, out, ws, ws_bytes, stream);
-    if (rc) return rc;
-    std::lock_guard<std::mutex> lk(g_mu);
-    Entry* en = nullptr;
-    e = cache_get(dm.data(), dm.size() * sizeof(TDesc), (size_t)C * 4,
-                  [&](void* dst) { fill_chunk_map(dm, (uint32_t*)dst); }, s, &en);
-    if (e != hipSuccess) return BC_E_HIP;
-    e = launch_dgc_mask((const TDesc*)en->dev, T, out.idx, sum_k, s);
-    cache_mark_used(en, s);
+    cache_mark_used(em, s);
+    cache_mark_used(ec, s);
     return finish(hip_status(e), s, ws);
 }
 

@@ -1,6 +1,6 @@
-// kernels_dgc.hip -- DGC's momentum correction and momentum-factor masking
-// around the sparse kinds (DGC is the paper's sparsification operator at a
-// 1% rate, Sec. 5.1; Sec. 2.3: sparsification with error feedback).
+// kernels_dgc.hip -- DGC's local gradient clipping for the DGC step of the
+// sparse kinds (DGC is the paper's sparsification operator at a 1% rate,
+// Sec. 5.1; Sec. 2.3: sparsification with error feedback).
 //
 // A DGC step of one tensor keeps a velocity u next to the error-feedback
 // residual e (DGC's accumulated gradient):
@@ -8,46 +8,17 @@
 //       fl32(clip / ||g||) when the list's L2 norm is above the threshold,
 //       else 1 (dgc_sumsq: fp64 sum of squares per chunk; dgc_clip_factor:
 //       one workgroup adds the chunk sums, takes the root and the factor)
-//   u <- fl32(fl32(m * u) + fl32(c * g))            (dgc_momentum; c = 1:
-//                                                    the unclipped g)
+//   u <- fl32(fl32(m * u) + fl32(c * g))            (c = 1: the unclipped g)
 //   compress u with residual e: v = fl32(u + e), select, payload v[idx],
 //   e <- v with +0.0 at idx                         (the sparse kind)
-//   u[idx] <- +0.0                                   (dgc_mask)
-// The top-k kinds fold the velocity step into their stream pass and the
-// masking into their emit pass (kernels_topk.hip); random-k runs the three
-// steps as separate launches.
+//   u[idx] <- +0.0
+// The velocity step runs inside the compress pass that forms v and the
+// masking where the selection is known: the top-k emit pass
+// (kernels_topk.hip), the random-k stream pass (kernels_randk.hip).  This
+// file holds the clipping factor.
 #include "launch.hpp"
 
 namespace bc {
-
-// Velocity step, one workgroup per 4096-element chunk (td.resid is u);
-// clip: the clipping factor (NULL: none).
-template <bool kNT>
-__global__ __launch_bounds__(kBlock) void dgc_momentum(const TDesc* __restrict__ d, int T, float m,
-                                                       const float* __restrict__ clip) {
-    const uint32_t c = blockIdx.x;
-    const int t = tensor_of_chunk(d, T, c);
-    const TDesc td = d[t];
-    const uint32_t j = c - td.chunk0;
-    float g[kEpt], u[kEpt];
-    uint32_t valid;
-    load_v<kNT>(td, j, false, g, valid);  // g widened to fp32
-    TDesc tu = td;
-    tu.grad = td.resid;
-    tu.dtype = 0;
-    load_v<kNT>(tu, j, false, u, valid);
-    if (clip) {
-        const float cf = *clip;
-#pragma unroll
-        for (int i = 0; i < kEpt; ++i) g[i] = cf * g[i];
-    }
-#pragma unroll
-    for (int i = 0; i < kEpt; ++i) {
-        const float mu = m * u[i];
-        u[i] = mu + g[i];
-    }
-    store_chunk<kNT>(td.resid, td.n, j, u);
-}
 
 // Sum of squares of a chunk's widened gradient, each square exact in fp64,
 // added per thread then in the fixed tree of block_sum_f64.
@@ -89,50 +60,10 @@ __global__ __launch_bounds__(kBlock) void dgc_clip_factor(const double* __restri
     }
 }
 
-// Masking: +0.0 into u at every payload index, kMaskSpan flattened
-// entries per workgroup.
-constexpr uint32_t kMaskSpan = 4096;
-
-__global__ __launch_bounds__(kBlock) void dgc_mask(const TDesc* __restrict__ d, int T, const uint32_t* __restrict__ idx,
-                                                   uint64_t total) {
-    __shared__ int t0_sh;
-    const uint64_t j0 = (uint64_t)blockIdx.x * kMaskSpan;
-    if (threadIdx.x == 0) t0_sh = tensor_of_entry(d, T, j0);
-    __syncthreads();
-    const uint64_t j1 = j0 + kMaskSpan < total ? j0 + kMaskSpan : total;
-    int t = t0_sh;
-    for (uint64_t j = j0 + threadIdx.x; j < j1; j += kBlock) {
-        while (t + 1 < T && d[t + 1].off <= j) ++t;
-        float* u = d[t].resid;
-        const uint32_t x = gp(idx)[j];
-        if (u && x < d[t].n) gp(u)[x] = 0.f;
-    }
-}
-
 hipError_t launch_dgc_clip(const TDesc* d, int T, uint32_t C, double clip, double* part, float* factor,
                            float* factor_out, hipStream_t s) {
     if (C > 0) hipLaunchKernelGGL(dgc_sumsq, dim3(C), dim3(kBlock), 0, s, d, T, part);
     hipLaunchKernelGGL(dgc_clip_factor, dim3(1), dim3(kBlock), 0, s, part, C, clip, factor, factor_out);
-    return hipGetLastError();
-}
-
-hipError_t launch_dgc_momentum(const TDesc* d, int T, uint32_t C, float m, bool clipping, double clip,
-                                double* part, float* factor, float* factor_out, hipStream_t s) {
-    if (clipping) {
-        const hipError_t e = launch_dgc_clip(d, T, C, clip, part, factor, factor_out, s);
-        if (e != hipSuccess) return e;
-    }
-    if (C == 0) return hipGetLastError();
-    const float* cf = clipping ? factor : nullptr;
-    if (C > kNtChunks) hipLaunchKernelGGL(dgc_momentum<true>, dim3(C), dim3(kBlock), 0, s, d, T, m, cf);
-    else hipLaunchKernelGGL(dgc_momentum<false>, dim3(C), dim3(kBlock), 0, s, d, T, m, cf);
-    return hipGetLastError();
-}
-
-hipError_t launch_dgc_mask(const TDesc* d, int T, const uint32_t* idx, uint64_t total, hipStream_t s) {
-    if (total == 0 || T == 0) return hipSuccess;
-    const uint64_t blocks = (total + kMaskSpan - 1) / kMaskSpan;
-    hipLaunchKernelGGL(dgc_mask, dim3((uint32_t)blocks), dim3(kBlock), 0, s, d, T, idx, total);
     return hipGetLastError();
 }
 

@@ -269,15 +269,71 @@ __device__ __forceinline__ void half_loads(const TDesc& td, uint32_t lo, int lan
             for (int i = 0; i < 4; ++i) v[4 * r + i] = g_elem<DT>(gf[r], gh[r], i);
     }
 }
+
+// The DGC velocity step over the same 32 elements: td holds u (as the fp32
+// gradient) and e, tg the step's gradient; u receives fl32(fl32(m * u) +
+// fl32(c * g)) and v fl32(u + e).  `whole`: all 2048 elements inside the
+// tensor; else each element is checked, and those past the end read +0.0
+// and are left out of `valid`.
+template <int DT, bool kNT>
+__device__ __forceinline__ void half_loads_dgc(const TDesc& td, const TDesc& tg, uint32_t lo, int lane, bool whole,
+                                               const DgcFuse& f, float (&v)[32], float (&u)[32], uint32_t& valid) {
+    const uint32_t e0 = lo + 4u * (uint32_t)lane;
+    const bool clip = f.clip != nullptr;
+    const float cf = clip ? *f.clip : 1.f;
+    auto step = [&](float g, float uo, float e, float& un, float& vn) {
+        if (clip) g = cf * g;
+        const float mu = f.m * uo;
+        un = mu + g;
+        vn = un + e;
+    };
+    if (whole) {
+        f32x4 gf[8], uf[8], ef[8];
+        u32x2 gh[8];
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+            if constexpr (DT == 0) gf[r] = ldg4f_s<kNT>((const float*)tg.grad + e0 + 256u * r);
+            else gh[r] = ldg2u_s<kNT>((const uint16_t*)tg.grad + e0 + 256u * r);
+            uf[r] = ldg4f_s<kNT>((const float*)td.grad + e0 + 256u * r);
+            ef[r] = ldg4f_s<kNT>(td.resid + e0 + 256u * r);
+        }
+#pragma unroll
+        for (int r = 0; r < 8; ++r)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) step(g_elem<DT>(gf[r], gh[r], i), uf[r][i], ef[r][i], u[4 * r + i], v[4 * r + i]);
+        valid = 0xFFFFFFFFu;
+        return;
+    }
+    valid = 0;
+#pragma unroll
+    for (int r = 0; r < 8; ++r)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t x = e0 + 256u * r + i;
+            const bool ok = x < td.n;
+            float gx = 0.f, ux = 0.f, ex = 0.f;
+            if (ok) {
+                gx = DT == 0 ? gp((const float*)tg.grad)[x] : h2f(gp((const uint16_t*)tg.grad)[x]);
+                ux = gp((const float*)td.grad)[x];
+                ex = gp(td.resid)[x];
+            }
+            step(gx, ux, ex, u[4 * r + i], v[4 * r + i]);
+            valid |= (ok ? 1u : 0u) << (4 * r + i);
+        }
+}
 }  // namespace
 
-// kHalves (runs of at most 2 chunks): each wave takes half a chunk, so that
-// all four waves have work; else each wave takes whole chunks.
-template <bool kNT, bool kHalves>
+// kHalves (runs of at most 2 chunks, not with kDGC): each wave takes half a
+// chunk, so that all four waves have work; else each wave takes whole
+// chunks.  kDGC: a DGC
+// step (d holds u in the gradient's place, f.dg the gradients) whose
+// velocity update runs here and whose masking is the zeroing of the
+// selected entries of u, written back with e_new.
+template <bool kNT, bool kHalves, bool kDGC>
 __global__ __launch_bounds__(kBlock) void randk_stream(const TDesc* __restrict__ d, int T, uint32_t C,
                                                        uint32_t S, uint32_t SP, uint32_t NB,
                                                        uint32_t* __restrict__ idx, float* __restrict__ val,
-                                                       Ws ws) {
+                                                       Ws ws, DgcFuse f) {
     extern __shared__ uint32_t bm[];  // [2^SP * 128] bits of the run's chunks
     __shared__ uint32_t coff[(1u << kRandkMaxShift) + 1];
     __shared__ uint32_t below_sh;
@@ -347,7 +403,8 @@ __global__ __launch_bounds__(kBlock) void randk_stream(const TDesc* __restrict__
     const uint32_t units = kHalves ? 2 * nc : nc;
     for (uint32_t unit = (uint32_t)wave; unit < units; unit += kBlock / 64) {
         const uint32_t q = kHalves ? unit >> 1 : unit;
-        const TDesc td = d[tensor_of_chunk(d, T, c0 + q)];
+        const int tq = tensor_of_chunk(d, T, c0 + q);
+        const TDesc td = d[tq];
         const uint32_t j = c0 + q - td.chunk0;
         const bool use_e = td.resid != nullptr;
         uint64_t base = beg + below_sh + coff[q];
@@ -363,16 +420,21 @@ __global__ __launch_bounds__(kBlock) void randk_stream(const TDesc* __restrict__
             const uint32_t half = kHalves ? (unit & 1u) : h;
             const uint32_t lo = j * (uint32_t)kChunk + 2048u * half;
             float v[32];
+            float un[kDGC ? 32 : 1];  // kDGC: the velocity after the step
             uint32_t valid = 0;
             const bool whole = (uint64_t)lo + 2048u <= td.n;
-            if (whole) {
+            if constexpr (kDGC) {
+                const TDesc tg = f.dg[tq];
+                if (tg.dtype == 0) half_loads_dgc<0, kNT>(td, tg, lo, lane, whole, f, v, un, valid);
+                else half_loads_dgc<1, kNT>(td, tg, lo, lane, whole, f, v, un, valid);
+            } else if (whole) {
                 // straight-line: every load of the half is issued before any is used
                 if (td.dtype == 0) half_loads<0, kNT>(td, lo, lane, use_e, v);
                 else half_loads<1, kNT>(td, lo, lane, use_e, v);
                 valid = 0xFFFFFFFFu;
             }
 #pragma unroll
-            for (int r = 0; r < 8 && !whole; ++r) {
+            for (int r = 0; r < 8 && !(whole || kDGC); ++r) {
                 const uint32_t e0 = lo + 256u * r + 4u * (uint32_t)lane;
                 float g4[4] = {0.f, 0.f, 0.f, 0.f}, e4[4] = {0.f, 0.f, 0.f, 0.f};
                 if (e0 + 3 < td.n) {
@@ -425,6 +487,18 @@ __global__ __launch_bounds__(kBlock) void randk_stream(const TDesc* __restrict__
 #pragma unroll
                         for (int i = 0; i < 4; ++i)
                             if (e0 + i < td.n) gp(td.resid)[e0 + i] = o[i];
+                    }
+                    if constexpr (kDGC) {  // u with the selected entries masked
+                        float* vel = (float*)const_cast<void*>(td.grad);
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) o[i] = ((pm >> (4 * r + i)) & 1u) ? 0.f : un[4 * r + i];
+                        if (whole || e0 + 3 < td.n) {
+                            stg4f_s<kNT>(vel + e0, f32x4{o[0], o[1], o[2], o[3]});
+                        } else {
+#pragma unroll
+                            for (int i = 0; i < 4; ++i)
+                                if (e0 + i < td.n) gp(vel)[e0 + i] = o[i];
+                        }
                     }
                 }
             }
@@ -482,11 +556,16 @@ hipError_t need_lds(const void* f, size_t bytes, size_t& allowed) {
     return e;
 }
 std::mutex g_lds_mu;
-size_t g_lds_place = 0, g_lds_stream = 0, g_lds_stream_nt = 0;
+size_t g_lds_place = 0, g_lds_stream[2][2] = {{0, 0}, {0, 0}};  // [non-temporal][DGC]
+
+template <bool kNT, bool kDGC>
+hipError_t need_lds_stream(size_t bytes) {
+    return need_lds((const void*)randk_stream<kNT, false, kDGC>, bytes, g_lds_stream[kNT][kDGC]);
+}
 }  // namespace
 
 hipError_t launch_randk(uint64_t seed, const TDesc* d, int T, uint32_t C, uint64_t sum_k, bool,
-                        bool, uint32_t* idx, float* val, const Ws& ws, hipStream_t s) {
+                        bool, uint32_t* idx, float* val, const Ws& ws, hipStream_t s, const DgcFuse* dgc) {
     if (C == 0 || T == 0) return hipSuccess;
     uint32_t S, NB;
     if (!randk_buckets(C, &S, &NB) || sum_k >= (1ull << 32)) return hipErrorInvalidValue;
@@ -496,16 +575,20 @@ hipError_t launch_randk(uint64_t seed, const TDesc* d, int T, uint32_t C, uint64
     // workgroups reads the whole bucket list, so runs are split only while
     // those re-reads stay under a quarter of the 8 B-per-element input, at
     // most 32 runs per bucket, and never below 2 chunks (half a chunk per
-    // wave)
+    // wave).  A DGC step keeps whole chunks per wave (its half-chunk form
+    // holds too many registers) and so runs of at least 4 chunks.
     uint32_t SP = S;
-    while (SP > 1 && S - SP < 5 && ((sum_k << (S - SP + 1)) * 4 <= (uint64_t)C * kChunk * 2)) --SP;
+    const uint32_t sp_min = dgc ? 2u : 1u;
+    while (SP > sp_min && S - SP < 5 && ((sum_k << (S - SP + 1)) * 4 <= (uint64_t)C * kChunk * 2)) --SP;
     const size_t lds_place = (size_t)NB * 8, lds_stream = ((size_t)kChunkWords * 4) << SP;
     {
         std::lock_guard<std::mutex> lk(g_lds_mu);
         hipError_t e = need_lds((const void*)randk_place, lds_place, g_lds_place);
         // (runs of more than 2 chunks: 2^SP * 512 bytes, at most 128 KiB)
-        if (e == hipSuccess) e = need_lds((const void*)randk_stream<false, false>, lds_stream, g_lds_stream);
-        if (e == hipSuccess) e = need_lds((const void*)randk_stream<true, false>, lds_stream, g_lds_stream_nt);
+        if (e == hipSuccess) e = need_lds_stream<false, false>(lds_stream);
+        if (e == hipSuccess) e = need_lds_stream<true, false>(lds_stream);
+        if (e == hipSuccess) e = need_lds_stream<false, true>(lds_stream);
+        if (e == hipSuccess) e = need_lds_stream<true, true>(lds_stream);
         if (e != hipSuccess) return e;
     }
     const dim3 blk(kBlock);
@@ -527,9 +610,12 @@ hipError_t launch_randk(uint64_t seed, const TDesc* d, int T, uint32_t C, uint64
     // fewer buckets: its surplus workgroups return at once)
     const uint32_t F = 1u << (S - SP);
     const dim3 sgrid((NB + 7) / 8 * 8 * F);
-    const auto kern = C > kNtChunks ? (SP <= 1 ? randk_stream<true, true> : randk_stream<true, false>)
-                                     : (SP <= 1 ? randk_stream<false, true> : randk_stream<false, false>);
-    return launch_timed(kTimedRandkStream, kern, sgrid, blk, lds_stream, s, d, T, C, S, SP, NB, idx, val, ws);
+    const bool nt = C > kNtChunks, halves = SP <= 1;
+    const DgcFuse f = dgc ? *dgc : DgcFuse{nullptr, 0.f, nullptr};
+    const auto kern = dgc ? (nt ? randk_stream<true, false, true> : randk_stream<false, false, true>)
+                          : (nt ? (halves ? randk_stream<true, true, false> : randk_stream<true, false, false>)
+                                : (halves ? randk_stream<false, true, false> : randk_stream<false, false, false>));
+    return launch_timed(kTimedRandkStream, kern, sgrid, blk, lds_stream, s, d, T, C, S, SP, NB, idx, val, ws, f);
 }
 
 }  // namespace bc

@@ -153,8 +153,9 @@ constexpr uint32_t kNtChunks = 8192;
 hipError_t launch_sign_compress(const TDesc* d, int T, uint32_t C, uint32_t max_chunks, bool any_empty,
                                 bool any_f16, bool any_f32, uint32_t* bits, float* scale, const Ws& ws, int cus,
                                 hipStream_t s);
-// A DGC step folded into the top-k passes: the velocity step runs inside
-// the stream pass that forms v, the masking inside the emit pass.  The
+// A DGC step folded into the compress passes: the velocity step runs
+// inside the stream pass that forms v, the masking inside the pass that
+// knows the selection (the top-k emit pass, the random-k stream pass).  The
 // call's table d then holds u (as the fp32 gradient) and e; dg holds the
 // step's gradients (same tensors, chunks and k); clip is the device
 // clipping factor or NULL.
@@ -169,7 +170,7 @@ hipError_t launch_topk(int kind, double ratio, uint64_t seed, const TDesc* d, in
                        hipStream_t s, const DgcFuse* dgc = nullptr);
 hipError_t launch_randk(uint64_t seed, const TDesc* d, int T, uint32_t C, uint64_t sum_k,
                         bool any_f16, bool any_f32, uint32_t* idx, float* val, const Ws& ws,
-                        hipStream_t s);
+                        hipStream_t s, const DgcFuse* dgc = nullptr);
 hipError_t launch_residual_update(int kind, const TDesc* d, int T, uint32_t C, bool any_f16,
                                   bool any_f32, const uint32_t* idx, const float* val,
                                   const uint32_t* bits, const float* scale, hipStream_t s);
@@ -190,17 +191,10 @@ hipError_t launch_quant_compress(int bits, uint64_t seed, const TDesc* d, int T,
                                  const Ws& ws, int cus, hipStream_t s);
 hipError_t launch_quant_residual_update(int bits, const TDesc* d, int T, uint32_t C, const uint32_t* words,
                                         const float* scale, hipStream_t s);
-// DGC momentum correction (d: tensors with resid = the velocity u) and
-// momentum-factor masking (idx: the call's payload indices, total entries).
-// clipping: first the local clipping factor of the list (chunk sums of
-// squares in part[C], the factor in factor[0] and, when given,
-// factor_out[0]), then the step with the clipped gradient.
-hipError_t launch_dgc_momentum(const TDesc* d, int T, uint32_t C, float m, bool clipping, double clip,
-                               double* part, float* factor, float* factor_out, hipStream_t s);
-// The clipping factor alone (for a step folded into the top-k passes).
+// DGC local clipping: chunk sums of squares of the gradients of table d in
+// part[C], the factor in factor[0] and, when given, factor_out[0].
 hipError_t launch_dgc_clip(const TDesc* d, int T, uint32_t C, double clip, double* part, float* factor,
                            float* factor_out, hipStream_t s);
-hipError_t launch_dgc_mask(const TDesc* d, int T, const uint32_t* idx, uint64_t total, hipStream_t s);
 // units of kSignAggUnit elements; W <= 1024
 // info, tabs: the TernGrad exact form's per-tensor forms and tables (2-bit only).
 hipError_t launch_aggregate_quant(int bits, const ADesc* a, int T, uint32_t units, const uint64_t* wp, int W,

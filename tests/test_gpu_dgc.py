@@ -167,3 +167,36 @@ def test_dgc_sampled_fallback_mixed(ratio):
             for t in range(len(ns)):
                 assert np.array_equal(bits(de[t].cpu().numpy()), bits(e[t])), (step, t)
                 assert np.array_equal(bits(du[t].cpu().numpy()), bits(u[t])), (step, t)
+
+
+@pytest.mark.timeout(600)
+def test_dgc_randk_many_chunks():
+    """Random-k DGC on a call of more than 32768 chunks (40000 one-chunk
+    tensors): buckets of 8 chunks streamed in runs of 4 by two workgroups
+    each, the velocity step and the masking inside that pass.  Two steps,
+    payloads, residuals and velocities bit for bit."""
+    import torch
+    from paper_2205_14465_amd import binding as B
+    rng = np.random.default_rng(43)
+    ns = [int(x) for x in rng.integers(1, 4097, size=40000)]
+    ns[7] = 0
+    ratio, m = 0.01, 0.9
+    e = [(rng.standard_normal(n) * 1e-3).astype(np.float32) for n in ns]
+    u = [(rng.standard_normal(n) * 1e-2).astype(np.float32) for n in ns]
+    de = [torch_dev(x) for x in e]
+    du = [torch_dev(x) for x in u]
+    out = B.alloc_payload("randk", ratio, ns)
+    ws = B.alloc_workspace("randk", ratio, ns, 1)
+    for step, seed in enumerate((21, 22)):
+        grads = [(rng.standard_normal(n) * 0.01).astype(np.float32) for n in ns]
+        B.bytecomp_compress_dgc("randk", ratio, seed, m, [torch_dev(g) for g in grads], de, du, out, ws)
+        torch.cuda.synchronize()
+        assert B.bytecomp_device_status(ws) == 0
+        want, e, u = O.compress_dgc_set("randk", ratio, seed, m, grads, e, u)
+        total = int(want["off"][-1])
+        assert np.array_equal(out["idx"].cpu().numpy().view(np.uint32)[:total], want["idx"]), step
+        assert np.array_equal(bits(out["val"].cpu().numpy()[:total]), bits(want["val"])), step
+        got_e = torch.cat([x for x in de if x.numel()]).cpu().numpy()
+        got_u = torch.cat([x for x in du if x.numel()]).cpu().numpy()
+        assert np.array_equal(bits(got_e), bits(np.concatenate(e))), step
+        assert np.array_equal(bits(got_u), bits(np.concatenate(u))), step

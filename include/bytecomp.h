@@ -199,7 +199,8 @@ int bytecomp_compress_noalloc(int kind, double ratio, uint64_t seed, const bc_te
  *   kind      BC_TOPK, BC_TOPK_SAMPLED or BC_RANDK (BC_E_KIND otherwise)
  *   velocity  host array of T device pointers: n_t fp32 values each,
  *             16-byte aligned, updated in place (zero them before the
- *             first step)
+ *             first step); a tensor's velocity, gradient and residual
+ *             must not overlap (the step reads and writes them in one pass)
  *   t         the tensors; every residual must be non-NULL (it is DGC's
  *             accumulated gradient)
  * Every other argument, the workspace and the limits are bytecomp_compress's.

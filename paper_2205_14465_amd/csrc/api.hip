@@ -587,11 +587,11 @@ int compress_dgc_impl(int kind, double ratio, uint64_t seed, float momentum, boo
         tc.resize((size_t)T);
         for (int i = 0; i < T; ++i) {
             if (t[i].n > 0 && (!velocity[i] || !t[i].residual)) return BC_E_NULL;
-            tv[(size_t)i] = t[i];
-            tv[(size_t)i].residual = velocity[i];  // the velocity step updates u in place
+            tv[(size_t)i] = t[i];  // dm: the gradients (u in the residual's place, checked like one)
+            tv[(size_t)i].residual = velocity[i];
             tc[(size_t)i] = bc_tensor{velocity[i], t[i].residual, t[i].n, BC_F32, t[i].tensor_id};
         }
-        // every argument of the three steps is checked before anything is enqueued
+        // every argument is checked before anything is enqueued
         rc = build_tdesc(kind, ppm, tv.data(), T, true, dm, C, maxc, sum_k, a16, a32);
         if (rc == BC_OK) rc = build_tdesc(kind, ppm, tc.data(), T, true, dc, C2, maxc2, sum_k2, b16, b32);
     } catch (const std::bad_alloc&) {

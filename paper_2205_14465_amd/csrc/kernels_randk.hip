@@ -235,11 +235,12 @@ __global__ __launch_bounds__(kGenBlock) void randk_place(const TDesc* __restrict
 // SP = S).  The run's indices, read from the bucket's list, are marked in
 // an LDS bitmap, and the list's indices below the run are counted; these
 // and the per-chunk counts of the bitmap with their prefix give each
-// chunk's payload position.  Then every wave streams whole chunks on its own (no
-// workgroup barrier): lane l holds elements 256 r + 4 l + i (r < 16, i < 4)
-// of the chunk, writes e_new (selected entries zeroed) and emits its
-// selected (index, v) pairs at positions from a wave prefix over the
-// rounds, which is ascending index order.
+// chunk's payload position.  Then every wave streams whole chunks (or, in
+// runs of at most 2 chunks, half chunks) on its own (no workgroup
+// barrier): lane l holds elements 256 r + 4 l + i (r < 16, i < 4) of the
+// chunk, writes e_new (selected entries zeroed) and emits its selected
+// (index, v) pairs at positions from a wave prefix over the rounds, which
+// is ascending index order.
 namespace {
 // v = widen(g) + e (or widen(g)) for the 32 elements a lane owns of the
 // 2048 elements from `lo` (all inside the tensor): element 256 r + 4 lane + i
@@ -377,20 +378,20 @@ __global__ __launch_bounds__(kBlock) void randk_stream(const TDesc* __restrict__
     __syncthreads();
     if (wave == 0) {
         // exclusive prefix of nc <= 256 counts: four per lane
-        uint32_t x[4], run = 0;
+        uint32_t x[4], mine = 0;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const uint32_t q = 4u * lane + i;
             x[i] = q < nc ? coff[q] : 0u;
-            run += x[i];
+            mine += x[i];
         }
-        uint32_t inc = run;
+        uint32_t inc = mine;
 #pragma unroll
         for (int o = 1; o < 64; o <<= 1) {
             const uint32_t y = __shfl_up(inc, o, 64);
             if (lane >= o) inc += y;
         }
-        uint32_t at = inc - run;
+        uint32_t at = inc - mine;
         __builtin_amdgcn_wave_barrier();
 #pragma unroll
         for (int i = 0; i < 4; ++i) {

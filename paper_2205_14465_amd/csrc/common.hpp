@@ -449,8 +449,16 @@ struct U64x4 { uint64_t v[4]; };
 
 __host__ __device__ inline void mul_hilo64(uint64_t a, uint64_t b, uint64_t& hi, uint64_t& lo) {
 #if defined(__HIP_DEVICE_COMPILE__)
-    hi = __umul64hi(a, b);
-    lo = a * b;
+    // the 128-bit product from four 32x32+64-bit multiply-adds (v_mad_u64_u32),
+    // sharing the partial products between the two halves; no sum overflows:
+    // (2^32 - 1)^2 + (2^32 - 1) < 2^64
+    const uint32_t a0 = (uint32_t)a, a1 = (uint32_t)(a >> 32);
+    const uint32_t b0 = (uint32_t)b, b1 = (uint32_t)(b >> 32);
+    const uint64_t p00 = (uint64_t)a0 * b0;
+    const uint64_t p10 = (uint64_t)a1 * b0 + (p00 >> 32);
+    const uint64_t p01 = (uint64_t)a0 * b1 + (uint32_t)p10;
+    hi = (uint64_t)a1 * b1 + (p10 >> 32) + (p01 >> 32);
+    lo = (p01 << 32) | (uint32_t)p00;
 #else
     unsigned __int128 p = (unsigned __int128)a * b;
     hi = (uint64_t)(p >> 64);
